@@ -1,0 +1,190 @@
+"""fp64 CPU oracle for the PatchKV context-loading path.
+
+TEST INFRASTRUCTURE ONLY. This module is the correctness reference for the GPU
+library. Only the test suite, the smoke check and the benchmark's CPU-baseline
+leg may import it; the product path never calls it and never falls back to it.
+It shares no code with the GPU implementation: it reads the seeded inputs
+(raw bf16 bit patterns or float32 values) and decodes them itself.
+
+What it computes, per transformer block (paper, Sec. 2.2-2.3 and Alg. 1):
+
+  (a1) teacher attention: every reference query attends over the full cache;
+  (a2) student attention: the same queries over the compressed cache;
+  (a3) per-token targets t_i = W (h_i - h'_i) + (z_i - z'_i)            (Eq. 5);
+  (a4) sufficient statistics S_H = H'^T H', S_T = T^T H', summed over
+       reference chunks starting from zero                              (Eq. 9);
+  (a5) ridge patch  Delta W = S_T (S_H + lambda I)^{-1}                 (Eq. 8),
+       with lambda absolute or adaptive, lambda_0 ||S_H||_F^2 / tr S_H   (Eq. 7).
+
+Readings where the paper is silent (each is also listed in the design notes):
+
+* Row-vector orientation. Activations are rows (one token per row), so with
+  X = H' (tokens x d_in) and T (tokens x d_out) the statistics are
+  G = X^T X (= S_H) and C = X^T T (= S_T^T), and the returned patch is
+  Delta W = (G + lambda I)^{-1} C, the transpose of the paper's column-vector
+  Delta W. The patched layer computes X (W + Delta W) (+ rho X).
+* Synthetic block: the block has no MLP; the patched projection W is d x d and
+  both h and z are the concatenated attention heads O (z is the attention output
+  in Sec. 2.2). Eq. 5 then reads T = (O_f - O_c) W + rho (O_f - O_c) with
+  rho = 1; rho = 0 gives the pure projection form.
+* Attention: every query attends to every cache entry (no mask, RoPE already
+  applied), softmax scale 1/sqrt(dh) unless given, GQA query head h reads KV
+  head floor(h / (Hq / Hkv)).
+
+Parity pins for every function live in the CPU test suite (closed forms,
+invariants, brute force, library routines). Nothing here is "parity unpinned".
+"""
+from __future__ import annotations
+
+import numpy as np
+import scipy.linalg
+
+__all__ = [
+    "decode", "softmax_rows", "attention", "gather_cache", "targets",
+    "normal_equations", "normal_equations_chunked", "ridge_lambda", "solve_patch",
+    "layer_patch", "attention_rows",
+]
+
+
+def decode(x: np.ndarray, dtype: str) -> np.ndarray:
+    """Stored input -> float64, exactly.
+
+    ``dtype == "bf16"``: x holds bf16 bit patterns (uint16); the value is the
+    float32 whose upper 16 bits are those bits. ``"f32"``: x holds float32.
+    """
+    if dtype == "bf16":
+        a = np.ascontiguousarray(x, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
+        return a.view(np.float32).astype(np.float64)
+    if dtype == "f32":
+        return np.asarray(x, dtype=np.float32).astype(np.float64)
+    if dtype == "f64":
+        return np.asarray(x, dtype=np.float64)
+    raise ValueError(dtype)
+
+
+def softmax_rows(S: np.ndarray) -> np.ndarray:
+    """Row-wise softmax, two passes: subtract the row max, exponentiate, normalise."""
+    S = S - S.max(axis=1, keepdims=True)
+    P = np.exp(S)
+    P /= P.sum(axis=1, keepdims=True)
+    return P
+
+
+def attention(Q: np.ndarray, K: np.ndarray, V: np.ndarray, scale: float | None = None,
+              max_score_bytes: int = 1 << 28) -> np.ndarray:
+    """Reference-query attention over one cache (teacher Alg. 1 / student Alg. 1).
+
+    Q [M, Hq, dh], K and V [Hkv, Nk, dh], all float64. Returns O [M, Hq*dh]
+    with O[m, h*dh:(h+1)*dh] = softmax(scale * Q[m,h] K[g]^T) V[g],
+    g = floor(h / (Hq/Hkv)). Rows are processed in chunks only to bound memory.
+    """
+    M, Hq, dh = Q.shape
+    Hkv, Nk, dh2 = K.shape
+    if dh2 != dh or V.shape != K.shape or Hq % Hkv:
+        raise ValueError("shape mismatch")
+    if scale is None:
+        scale = 1.0 / np.sqrt(dh)
+    group = Hq // Hkv
+    O = np.empty((M, Hq * dh), dtype=np.float64)
+    rows = max(1, min(M, max_score_bytes // (8 * max(Nk, 1))))
+    for h in range(Hq):
+        g = h // group
+        for r0 in range(0, M, rows):
+            r1 = min(M, r0 + rows)
+            S = (Q[r0:r1, h, :] @ K[g].T) * scale
+            O[r0:r1, h * dh:(h + 1) * dh] = softmax_rows(S) @ V[g]
+    return O
+
+
+def attention_rows(Q: np.ndarray, K: np.ndarray, V: np.ndarray, rows: np.ndarray,
+                   scale: float | None = None) -> np.ndarray:
+    """Attention output of a subset of query rows (each row is independent)."""
+    return attention(Q[np.asarray(rows)], K, V, scale)
+
+
+def gather_cache(K: np.ndarray, V: np.ndarray, idx: np.ndarray):
+    """Eviction-style compressed cache: the kept entries K[:, idx], V[:, idx]."""
+    idx = np.asarray(idx)
+    return K[:, idx, :], V[:, idx, :]
+
+
+def targets(Of: np.ndarray, Oc: np.ndarray, W: np.ndarray, rho: int = 1) -> np.ndarray:
+    """Per-token targets of Eq. 5 in row form: T = (O_f - O_c) W + rho (O_f - O_c).
+
+    h - h' = O_f - O_c enters through the patched projection W; z - z' = O_f - O_c
+    is the residual attention-output term (present when rho = 1).
+    """
+    D = Of - Oc
+    T = D @ W
+    if rho:
+        if W.shape[0] != W.shape[1]:
+            raise ValueError("the residual term needs a square W")
+        T = T + rho * D
+    return T
+
+
+def normal_equations(Xc: np.ndarray, T: np.ndarray):
+    """Sufficient statistics of Eq. 9 in row form: G = Xc^T Xc, C = Xc^T T."""
+    return Xc.T @ Xc, Xc.T @ T
+
+
+def normal_equations_chunked(chunks):
+    """Eq. 9 accumulated over reference chunks, starting from zero (Alg. 1).
+
+    ``chunks`` yields (Xc_j, T_j) pairs; each chunk's outer-product sums are added
+    to running totals and the chunk is then dropped.
+    """
+    G = C = None
+    for Xj, Tj in chunks:
+        if G is None:
+            G = np.zeros((Xj.shape[1], Xj.shape[1]))
+            C = np.zeros((Xj.shape[1], Tj.shape[1]))
+        G += Xj.T @ Xj
+        C += Xj.T @ Tj
+    return G, C
+
+
+def ridge_lambda(G0: np.ndarray, lam: float, mode: str = "absolute") -> float:
+    """The ridge coefficient: absolute, or adaptive per Eq. 7 (lam is then lambda_0)."""
+    if mode == "absolute":
+        return float(lam)
+    if mode == "adaptive":
+        return float(lam) * float(np.sum(G0 * G0)) / float(np.trace(G0))
+    raise ValueError(mode)
+
+
+def solve_patch(G0: np.ndarray, C: np.ndarray, lam: float) -> np.ndarray:
+    """Eq. 8 in row form: Delta W = (G0 + lam I)^{-1} C, via LAPACK Cholesky."""
+    if not lam > 0:
+        raise ValueError("ridge coefficient must be positive")
+    A = G0 + lam * np.eye(G0.shape[0])
+    return scipy.linalg.cho_solve(scipy.linalg.cho_factor(A, lower=True), C)
+
+
+def layer_patch(inp, rho: int = 1, mode: str = "absolute", lam: float | None = None,
+                keep: bool = True) -> dict:
+    """One block's patch from a ``workloads`` LayerInputs (all steps in fp64).
+
+    Returns a dict with dW and, when ``keep``, the intermediates O_f, O_c, T,
+    G (without the ridge), C and the lambda used.
+    """
+    dt = inp.dtype
+    Q = decode(inp.Q, dt)
+    K = decode(inp.K, dt)
+    V = decode(inp.V, dt)
+    W = decode(inp.W, dt)
+    Of = attention(Q, K, V, inp.scale)
+    if inp.idx is not None:
+        Kc, Vc = gather_cache(K, V, inp.idx)
+    else:
+        Kc, Vc = decode(inp.Kc, dt), decode(inp.Vc, dt)
+    del K, V
+    Oc = attention(Q, Kc, Vc, inp.scale)
+    T = targets(Of, Oc, W, rho)
+    G0, C = normal_equations(Oc, T)
+    lam_used = ridge_lambda(G0, inp.lam if lam is None else lam, mode)
+    dW = solve_patch(G0, C, lam_used)
+    out = {"dW": dW, "lam": lam_used}
+    if keep:
+        out.update(Of=Of, Oc=Oc, T=T, G=G0, C=C)
+    return out

@@ -1,0 +1,423 @@
+"""Pins for the fp64 oracle: it is checked against things other than itself.
+
+Each pin is a closed form, an invariant the paper states, brute force on tiny
+inputs, exact rational arithmetic, or an independent library routine. The
+``check_*`` helpers take the function under test as an argument so that the
+mutation tests at the bottom can show that a planted mistake (in a copy of the
+oracle, on the CPU) fails at least one pin.
+"""
+import json
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import scipy.special
+import torch
+
+import oracle
+from workloads import CONFIGS, make_custom_inputs, make_layer_inputs
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden", "hand_worked.json")
+
+
+def rel(a, b):
+    a, b = np.asarray(a), np.asarray(b)
+    if a.shape != b.shape:
+        return float("inf")
+    return float(np.linalg.norm(np.asarray(a) - np.asarray(b)) / max(np.linalg.norm(np.asarray(b)), 1e-300))
+
+
+def rand_attn(rng, M, N, Hq, Hkv, dh, kscale=1.0):
+    Q = rng.standard_normal((M, Hq, dh))
+    K = rng.standard_normal((Hkv, N, dh)) * kscale
+    V = rng.standard_normal((Hkv, N, dh))
+    return Q, K, V
+
+
+# --------------------------------------------------------------------------- checks
+
+def brute_attention(Q, K, V, scale):
+    """Scalar loops: softmax attention written out term by term."""
+    M, Hq, dh = Q.shape
+    Hkv, N, _ = K.shape
+    grp = Hq // Hkv
+    O = [[0.0] * (Hq * dh) for _ in range(M)]
+    for m in range(M):
+        for h in range(Hq):
+            g = h // grp
+            s = [scale * sum(Q[m, h, c] * K[g, n, c] for c in range(dh)) for n in range(N)]
+            mx = max(s)
+            e = [math.exp(x - mx) for x in s]
+            z = sum(e)
+            for c in range(dh):
+                O[m][h * dh + c] = sum(e[n] * V[g, n, c] for n in range(N)) / z
+    return np.array(O)
+
+
+def check_attention_bruteforce(attn):
+    rng = np.random.default_rng(1)
+    worst = 0.0
+    for (M, N, Hq, Hkv, dh) in [(3, 5, 4, 2, 4), (2, 7, 6, 3, 3), (4, 1, 2, 1, 5)]:
+        Q, K, V = rand_attn(rng, M, N, Hq, Hkv, dh)
+        s = 0.37
+        worst = max(worst, rel(attn(Q, K, V, s), brute_attention(Q, K, V, s)))
+    return worst
+
+
+def check_attention_sdpa(attn):
+    """torch's scaled_dot_product_attention (float64, CPU) with KV heads repeated."""
+    rng = np.random.default_rng(2)
+    worst = 0.0
+    for (M, N, Hq, Hkv, dh) in [(17, 33, 4, 2, 8), (9, 64, 28, 4, 16), (5, 40, 8, 8, 8)]:
+        Q, K, V = rand_attn(rng, M, N, Hq, Hkv, dh, kscale=1.5)
+        s = 1.0 / math.sqrt(dh)
+        q = torch.from_numpy(Q).permute(1, 0, 2)                      # [Hq, M, dh]
+        k = torch.from_numpy(K).repeat_interleave(Hq // Hkv, dim=0)   # [Hq, N, dh]
+        v = torch.from_numpy(V).repeat_interleave(Hq // Hkv, dim=0)
+        o = torch.nn.functional.scaled_dot_product_attention(q, k, v, scale=s)
+        ref = o.permute(1, 0, 2).reshape(M, Hq * dh).numpy()
+        worst = max(worst, rel(attn(Q, K, V, s), ref))
+    return worst
+
+
+def brute_targets(Of, Oc, W, rho):
+    M, d = Of.shape
+    dout = W.shape[1]
+    T = np.zeros((M, dout))
+    for i in range(M):
+        for j in range(dout):
+            acc = 0.0
+            for k in range(d):
+                acc += W[k, j] * (Of[i, k] - Oc[i, k])
+            if rho:
+                acc += Of[i, j] - Oc[i, j]
+            T[i, j] = acc
+    return T
+
+
+def check_targets(tg):
+    rng = np.random.default_rng(3)
+    Of, Oc = rng.standard_normal((5, 4)), rng.standard_normal((5, 4))
+    W = rng.standard_normal((4, 4))
+    return max(rel(tg(Of, Oc, W, r), brute_targets(Of, Oc, W, r)) for r in (0, 1))
+
+
+def check_normal_equations(ne):
+    """Eq. 9: sums of per-token outer products."""
+    rng = np.random.default_rng(4)
+    X, T = rng.standard_normal((7, 3)), rng.standard_normal((7, 2))
+    G, C = ne(X, T)
+    Gb = sum(np.outer(X[i], X[i]) for i in range(7))
+    Cb = sum(np.outer(X[i], T[i]) for i in range(7))
+    return max(rel(G, Gb), rel(C, Cb))
+
+
+def frac_solve(A, B):
+    """Exact Gauss-Jordan elimination over the rationals."""
+    n = len(A)
+    m = len(B[0])
+    A = [row[:] + brow[:] for row, brow in zip(A, B)]
+    for c in range(n):
+        p = next(r for r in range(c, n) if A[r][c] != 0)
+        A[c], A[p] = A[p], A[c]
+        piv = A[c][c]
+        A[c] = [x / piv for x in A[c]]
+        for r in range(n):
+            if r != c and A[r][c] != 0:
+                f = A[r][c]
+                A[r] = [x - f * y for x, y in zip(A[r], A[c])]
+    return [row[n:n + m] for row in A]
+
+
+def check_solve_rational(solve):
+    """Eq. 8 on small integer data, solved exactly in rational arithmetic."""
+    rng = np.random.default_rng(5)
+    worst = 0.0
+    for (rows, din, dout, lam) in [(4, 3, 2, Fraction(1, 3)), (2, 4, 3, Fraction(1, 10)),
+                                   (6, 2, 5, Fraction(2))]:
+        X = rng.integers(-3, 4, size=(rows, din))
+        T = rng.integers(-3, 4, size=(rows, dout))
+        Xf = [[Fraction(int(v)) for v in r] for r in X]
+        Tf = [[Fraction(int(v)) for v in r] for r in T]
+        A = [[sum(Xf[k][i] * Xf[k][j] for k in range(rows)) + (lam if i == j else 0)
+              for j in range(din)] for i in range(din)]
+        Bm = [[sum(Xf[k][i] * Tf[k][j] for k in range(rows)) for j in range(dout)]
+              for i in range(din)]
+        exact = np.array([[float(v) for v in r] for r in frac_solve(A, Bm)])
+        G = X.T.astype(float) @ X
+        C = X.T.astype(float) @ T
+        worst = max(worst, rel(solve(G, C, float(lam)), exact))
+    return worst
+
+
+def check_solve_lstsq(solve):
+    """Ridge = least squares on the augmented system [X; sqrt(lam) I] dW ~ [T; 0]."""
+    rng = np.random.default_rng(6)
+    worst = 0.0
+    for (rows, din, dout, lam) in [(50, 20, 7, 0.3), (10, 30, 30, 1e-2)]:
+        X, T = rng.standard_normal((rows, din)), rng.standard_normal((rows, dout))
+        A = np.vstack([X, np.sqrt(lam) * np.eye(din)])
+        Bm = np.vstack([T, np.zeros((din, dout))])
+        ref = np.linalg.lstsq(A, Bm, rcond=None)[0]
+        worst = max(worst, rel(solve(X.T @ X, X.T @ T, lam), ref))
+    return worst
+
+
+# --------------------------------------------------------------------------- pins
+
+def test_golden_hand_worked():
+    gold = json.load(open(GOLD))
+    a = gold["attention_two_keys"]
+    O = oracle.attention(np.array(a["Q"]), np.array(a["K"]), np.array(a["V"]), a["scale"])
+    assert rel(O, a["O"]) < 1e-15
+    t = gold["targets_eq5"]
+    T = oracle.targets(np.array(t["Of"]), np.array(t["Oc"]), np.array(t["W"]), t["rho"])
+    assert np.array_equal(T, np.array(t["T"]))
+    r = gold["ridge_eq8"]
+    G, C = oracle.normal_equations(np.array(r["X"]), np.array(r["T"]))
+    assert np.array_equal(G, np.array(r["G"])) and np.array_equal(C, np.array(r["C"]))
+    assert rel(oracle.solve_patch(G, C, r["lam"]), r["dW"]) < 1e-15
+    ad = gold["adaptive_ridge_eq7"]
+    assert abs(oracle.ridge_lambda(np.array(ad["G"]), ad["lam0"], "adaptive") - ad["lam"]) < 1e-16
+
+
+def test_softmax_rows_library_and_sum():
+    rng = np.random.default_rng(0)
+    S = rng.standard_normal((64, 300)) * 20
+    P = oracle.softmax_rows(S)
+    assert rel(P, scipy.special.softmax(S, axis=1)) < 1e-14
+    assert np.max(np.abs(P.sum(axis=1) - 1.0)) < 1e-15
+
+
+def test_attention_bruteforce():
+    assert check_attention_bruteforce(oracle.attention) < 1e-13
+
+
+def test_attention_library_sdpa():
+    assert check_attention_sdpa(oracle.attention) < 1e-13
+
+
+def test_attention_closed_forms():
+    rng = np.random.default_rng(7)
+    M, Hq, Hkv, dh = 6, 4, 2, 8
+    # one key: O = its V
+    Q, K, V = rand_attn(rng, M, 1, Hq, Hkv, dh)
+    O = oracle.attention(Q, K, V).reshape(M, Hq, dh)
+    for h in range(Hq):
+        assert np.allclose(O[:, h], V[h // 2, 0][None, :], atol=1e-15)
+    # zero keys: uniform weights, O = mean of V
+    Q, K, V = rand_attn(rng, M, 9, Hq, Hkv, dh)
+    O = oracle.attention(Q, 0 * K, V).reshape(M, Hq, dh)
+    for h in range(Hq):
+        assert np.allclose(O[:, h], V[h // 2].mean(axis=0)[None, :], atol=1e-14)
+    # a dominant key: O -> its V
+    K = rng.standard_normal((Hkv, 9, dh)) * 1e-3
+    Q = np.abs(rng.standard_normal((M, Hq, dh)))
+    K[:, 4, :] = 1e3
+    O = oracle.attention(Q, K, V).reshape(M, Hq, dh)
+    for h in range(Hq):
+        assert np.allclose(O[:, h], V[h // 2, 4][None, :], atol=1e-12)
+
+
+def test_attention_invariances():
+    rng = np.random.default_rng(8)
+    Q, K, V = rand_attn(rng, 11, 50, 8, 2, 16)
+    O = oracle.attention(Q, K, V)
+    perm = rng.permutation(50)
+    assert rel(oracle.attention(Q, K[:, perm], V[:, perm]), O) < 1e-14
+    # GQA == MHA with each KV head repeated for its query heads
+    Kr = np.repeat(K, 4, axis=0)
+    Vr = np.repeat(V, 4, axis=0)
+    assert rel(oracle.attention(Q, Kr, Vr), O) < 1e-15
+    # row chunking changes nothing
+    assert rel(oracle.attention(Q, K, V, max_score_bytes=8 * 50 * 3), O) == 0.0
+    # attention_rows is the row subset
+    rows = np.array([0, 5, 10])
+    assert rel(oracle.attention_rows(Q, K, V, rows), O[rows]) == 0.0
+
+
+def test_gather_cache():
+    rng = np.random.default_rng(9)
+    Q, K, V = rand_attn(rng, 5, 20, 4, 2, 8)
+    Kg, Vg = oracle.gather_cache(K, V, np.arange(20))
+    assert np.array_equal(Kg, K) and np.array_equal(Vg, V)
+    idx = np.array([0, 3, 4, 19])
+    Kg, Vg = oracle.gather_cache(K, V, idx)
+    for j, n in enumerate(idx):
+        assert np.array_equal(Kg[:, j], K[:, n]) and np.array_equal(Vg[:, j], V[:, n])
+
+
+def test_targets_bruteforce_and_linearity():
+    assert check_targets(oracle.targets) < 1e-15
+    rng = np.random.default_rng(10)
+    Of, Oc = rng.standard_normal((6, 5)), rng.standard_normal((6, 5))
+    W1, W2 = rng.standard_normal((5, 5)), rng.standard_normal((5, 5))
+    lin = oracle.targets(Of, Oc, W1 + W2, 0) - oracle.targets(Of, Oc, W1, 0) - oracle.targets(Of, Oc, W2, 0)
+    assert np.max(np.abs(lin)) < 1e-13
+    assert np.array_equal(oracle.targets(Of, Of, W1, 1), np.zeros((6, 5)))
+
+
+def test_normal_equations_outer_products_and_chunks():
+    assert check_normal_equations(oracle.normal_equations) < 1e-15
+    rng = np.random.default_rng(11)
+    X, T = rng.standard_normal((100, 12)), rng.standard_normal((100, 9))
+    G, C = oracle.normal_equations(X, T)
+    cuts = [0, 7, 8, 40, 99, 100]
+    Gc, Cc = oracle.normal_equations_chunked((X[a:b], T[a:b]) for a, b in zip(cuts, cuts[1:]))
+    assert rel(Gc, G) < 1e-14 and rel(Cc, C) < 1e-14
+    assert np.array_equal(G, G.T)
+    assert np.min(np.linalg.eigvalsh(G)) > -1e-12
+
+
+def test_solve_rational_exact():
+    assert check_solve_rational(oracle.solve_patch) < 1e-14
+
+
+def test_solve_lstsq_library():
+    assert check_solve_lstsq(oracle.solve_patch) < 1e-12
+
+
+def test_solve_push_through_and_residual():
+    rng = np.random.default_rng(12)
+    X, T = rng.standard_normal((40, 60)), rng.standard_normal((40, 25))
+    lam = 0.05
+    G, C = oracle.normal_equations(X, T)
+    dW = oracle.solve_patch(G, C, lam)
+    push = X.T @ np.linalg.solve(X @ X.T + lam * np.eye(40), T)
+    assert rel(dW, push) < 1e-11
+    A = G + lam * np.eye(60)
+    res = np.linalg.norm(A @ dW - C) / (np.linalg.norm(A) * np.linalg.norm(dW) + np.linalg.norm(C))
+    assert res < 1e-15
+
+
+def test_solve_closed_forms_and_limits():
+    rng = np.random.default_rng(13)
+    # d_in = 1: dW = sum x t / (sum x^2 + lam)
+    x, t = rng.standard_normal((30, 1)), rng.standard_normal((30, 4))
+    G, C = oracle.normal_equations(x, t)
+    assert rel(oracle.solve_patch(G, C, 0.7), (x.T @ t) / (np.sum(x * x) + 0.7)) < 1e-15
+    # diagonal G: dW = C / (diag + lam)
+    Gd = np.diag(rng.uniform(0.5, 3.0, 6))
+    Cd = rng.standard_normal((6, 3))
+    assert rel(oracle.solve_patch(Gd, Cd, 0.2), Cd / (np.diag(Gd)[:, None] + 0.2)) < 1e-15
+    # lambda -> infinity: dW -> 0 and lam dW -> C, with O(1/lam) error
+    X, T = rng.standard_normal((20, 8)), rng.standard_normal((20, 5))
+    G, C = oracle.normal_equations(X, T)
+    errs = []
+    for lam in (1e4, 1e6, 1e8):
+        dW = oracle.solve_patch(G, C, lam)
+        errs.append(rel(lam * dW, C))
+        assert np.linalg.norm(dW) < 10 * np.linalg.norm(C) / lam
+    assert errs[1] < errs[0] / 50 and errs[2] < errs[1] / 50
+    # optimality: the ridge objective grows in every random direction
+    lam = 0.3
+    dW = oracle.solve_patch(G, C, lam)
+    J = lambda D: np.sum((X @ D - T) ** 2) + lam * np.sum(D * D)
+    for _ in range(5):
+        E = rng.standard_normal(dW.shape) * 1e-3
+        assert J(dW + E) > J(dW) and J(dW - E) > J(dW)
+    assert J(dW) < J(np.zeros_like(dW))
+
+
+def test_solve_scaling_laws():
+    rng = np.random.default_rng(14)
+    X, T = rng.standard_normal((30, 10)), rng.standard_normal((30, 4))
+    G, C = oracle.normal_equations(X, T)
+    dW = oracle.solve_patch(G, C, 0.5)
+    a = 3.0
+    G2, C2 = oracle.normal_equations(a * X, T)
+    assert rel(oracle.solve_patch(G2, C2, a * a * 0.5), dW / a) < 1e-13
+    G3, C3 = oracle.normal_equations(X, a * T)
+    assert rel(oracle.solve_patch(G3, C3, 0.5), a * dW) < 1e-14
+    # adaptive ridge (Eq. 7): dW(aX) = dW(X) / a with lambda_0 fixed
+    lam_a = oracle.ridge_lambda(G, 0.1, "adaptive")
+    lam_b = oracle.ridge_lambda(G2, 0.1, "adaptive")
+    assert abs(lam_b / lam_a - a * a) < 1e-12
+    assert rel(oracle.solve_patch(G2, C2, lam_b), oracle.solve_patch(G, C, lam_a) / a) < 1e-13
+    with pytest.raises(ValueError):
+        oracle.solve_patch(G, C, 0.0)
+
+
+def test_layer_patch_identity_cache_gives_zero_patch():
+    """Compressed cache == full cache => T = 0 => C = 0 => dW = 0 exactly."""
+    inp = make_custom_inputs(M=24, N=40, B=40, Hq=4, Hkv=2, dh=8, dtype="bf16",
+                             cache="identity", seed=3)
+    out = oracle.layer_patch(inp)
+    assert np.max(np.abs(out["dW"])) == 0.0
+    assert np.max(np.abs(out["T"])) == 0.0
+
+
+def test_layer_patch_config0_properties():
+    cfg = CONFIGS[0]
+    inp = make_layer_inputs(cfg)
+    out = oracle.layer_patch(inp)
+    dW, G, C, lam = out["dW"], out["G"], out["C"], out["lam"]
+    assert dW.shape == (cfg.d, cfg.d) and np.all(np.isfinite(dW))
+    A = G + lam * np.eye(cfg.d)
+    res = np.linalg.norm(A @ dW - C) / (np.linalg.norm(A) * np.linalg.norm(dW) + np.linalg.norm(C))
+    assert res < 1e-15
+    push = out["Oc"].T @ np.linalg.solve(out["Oc"] @ out["Oc"].T + lam * np.eye(cfg.M), out["T"])
+    assert rel(dW, push) < 1e-9
+    # chunked accumulation over the reference tokens gives the same patch
+    Gc, Cc = oracle.normal_equations_chunked(
+        (out["Oc"][a:a + 40], out["T"][a:a + 40]) for a in range(0, cfg.M, 40))
+    assert rel(oracle.solve_patch(Gc, Cc, lam), dW) < 1e-10
+    # the compressed cache is the sorted eviction subset of the recipe
+    idx = inp.idx
+    assert idx.shape == (cfg.B,) and np.all(np.diff(idx) > 0)
+    assert list(idx[:4]) == [0, 1, 2, 3] and list(idx[-cfg.n_recent:]) == list(range(cfg.N - cfg.n_recent, cfg.N))
+
+
+def test_synthesized_cache_is_convex_mix():
+    inp = make_custom_inputs(M=8, N=100, B=6, Hq=4, Hkv=2, dh=8, dtype="f32",
+                             cache="synthesize", n_mix=5, seed=1)
+    pos, w = inp.extra["syn_pos"], inp.extra["syn_w"]
+    assert np.allclose(w.sum(axis=1), 1.0) and np.all(w > 0)
+    assert all(len(set(p)) == 5 for p in pos)
+    K = inp.K.astype(np.float64)
+    for g in range(2):
+        for b in range(6):
+            assert np.allclose(inp.Kc[g, b], w[b] @ K[g, pos[b]], rtol=1e-6, atol=1e-6)
+
+
+# --------------------------------------------------------------------------- mutations
+
+def test_pins_catch_planted_mistakes():
+    """Copies of oracle functions with one planted mistake each fail a pin."""
+    def attn_wrong_group(Q, K, V, scale=None):
+        M, Hq, dh = Q.shape
+        Hkv = K.shape[0]
+        O = np.empty((M, Hq * dh))
+        for h in range(Hq):
+            g = h % Hkv                                # wrong GQA mapping
+            S = Q[:, h, :] @ K[g].T * scale
+            O[:, h * dh:(h + 1) * dh] = oracle.softmax_rows(S) @ V[g]
+        return O
+
+    def attn_no_scale(Q, K, V, scale=None):
+        return oracle.attention(Q, K, V, 1.0)         # scale dropped
+
+    def targets_no_residual(Of, Oc, W, rho=1):
+        return (Of - Oc) @ W                          # residual term dropped
+
+    def targets_transposed(Of, Oc, W, rho=1):
+        return (Of - Oc) @ W.T + rho * (Of - Oc)      # transposed operand
+
+    def ne_transposed(X, T):
+        return X.T @ X, T.T @ X                        # wrong orientation
+
+    def solve_no_ridge(G, C, lam):
+        return np.linalg.lstsq(G, C, rcond=None)[0]   # lambda dropped
+
+    def solve_sign(G, C, lam):
+        return np.linalg.solve(G - lam * np.eye(G.shape[0]), C)   # wrong sign
+
+    assert check_attention_bruteforce(attn_wrong_group) > 1e-2
+    assert check_attention_bruteforce(attn_no_scale) > 1e-2
+    assert check_targets(targets_no_residual) > 1e-2
+    assert check_targets(targets_transposed) > 1e-2
+    assert check_normal_equations(ne_transposed) > 1e-2
+    assert check_solve_rational(solve_no_ridge) > 1e-3
+    assert check_solve_rational(solve_sign) > 1e-3

@@ -1,0 +1,70 @@
+"""The five synthetic workload shapes.
+
+Each stands in for a setting the paper measures (Sec. 3 and App. B): contexts up to
+~170K tokens, aggressive cache budgets (down to ~1 % of the context), and one
+reference chunk of a few thousand query tokens per block. The model shapes are
+those of Llama-3-8B (d=4096, 32 query / 8 KV heads, head_dim 128) and Qwen-2.5-7B
+(d=3584, 28 / 4 heads), plus a tiny fp32 layer that a CPU finishes in seconds.
+
+Compressed-cache structure:
+  * "evict":      B = n_sink sink tokens + the last n_recent tokens + n_random
+                  seeded-random middle positions (sorted), i.e. an eviction subset
+                  of the full cache, standing in for KVzip's output.
+  * "synthesize": B synthetic entries, each a seeded-random convex combination of
+                  n_mix full-cache entries, standing in for an approximation method
+                  (Attention Matching) whose entries are not a subset.
+"""
+from dataclasses import dataclass
+
+
+@dataclass(frozen=True)
+class Config:
+    cid: int
+    name: str
+    d: int            # model width = Hq * dh
+    Hq: int
+    Hkv: int
+    dh: int
+    N: int            # full-cache tokens
+    B: int            # compressed-cache entries
+    M: int            # reference query tokens
+    lam: float        # absolute ridge coefficient
+    dtype: str        # "f32" or "bf16" (Q, K, V and W)
+    layers: int = 1
+    cache: str = "evict"     # "evict" | "synthesize"
+    n_sink: int = 0
+    n_recent: int = 0
+    n_random: int = 0
+    n_mix: int = 0           # synthesize: entries mixed per synthetic entry
+
+    @property
+    def group(self) -> int:
+        return self.Hq // self.Hkv
+
+    @property
+    def scale(self) -> float:
+        return 1.0 / float(self.dh) ** 0.5
+
+    @property
+    def acc(self) -> str:
+        """Accumulation type of the normal equations for this input dtype."""
+        return "f64" if self.dtype == "f32" else "f32"
+
+
+CONFIGS = (
+    Config(0, "tiny-fp32", d=256, Hq=4, Hkv=2, dh=64, N=2048, B=256, M=128,
+           lam=1e-2, dtype="f32", n_sink=4, n_recent=124, n_random=128),
+    Config(1, "llama3-8b-layer-32k", d=4096, Hq=32, Hkv=8, dh=128, N=32768, B=2048,
+           M=1024, lam=1e-1, dtype="bf16", n_sink=4, n_recent=1020, n_random=1024),
+    Config(2, "llama3-8b-layer-128k", d=4096, Hq=32, Hkv=8, dh=128, N=131072, B=4096,
+           M=2048, lam=1e-1, dtype="bf16", n_sink=4, n_recent=2044, n_random=2048),
+    Config(3, "llama3-8b-32layer-172k", d=4096, Hq=32, Hkv=8, dh=128, N=172032,
+           B=1720, M=4096, lam=1e-1, dtype="bf16", layers=32, n_sink=4, n_recent=860,
+           n_random=856),
+    Config(4, "qwen2.5-7b-layer-64k-synth", d=3584, Hq=28, Hkv=4, dh=128, N=65536,
+           B=1024, M=2048, lam=5e-2, dtype="bf16", cache="synthesize", n_mix=64),
+)
+
+
+def get_config(cid: int) -> Config:
+    return CONFIGS[cid]

@@ -1,0 +1,208 @@
+"""Seeded input generation.
+
+Recipe (the same bytes feed the oracle and the GPU path):
+
+* Every random tensor has a tensor id: 0 key scales, 1 K, 2 V, 3 Q, 4 W,
+  5 eviction middle positions, 6 synthesis positions, 7 synthesis weights.
+* Normal tensors are drawn in C order in blocks of ``BLOCK`` elements; block ``b``
+  of tensor ``tid`` uses ``Generator(PCG64(SeedSequence([seed, cid, layer, tid, b])))``
+  and ``standard_normal(n, dtype=float32)``. Blocks are independent streams, so
+  they are drawn on several threads and the result does not depend on the
+  thread count.
+* Q, V ~ N(0, 1). K = Z * s with a per-(kv head, channel) scale
+  s ~ LogNormal(0, 0.5) (float32 product). W = Z * float32(1/sqrt(d)).
+* bf16 tensors are rounded from those float32 values with round-to-nearest-even
+  and stored as their raw uint16 bit patterns; fp32 tensors are stored as is.
+* Eviction subset: ``n_sink`` sinks, the last ``n_recent`` tokens, and
+  ``n_random`` positions drawn uniformly without replacement from
+  [n_sink, N - n_recent), sorted ascending, int32, shared by all KV heads.
+* Synthesized compressed cache: entry b mixes ``n_mix`` distinct full-cache
+  positions (uniform without replacement over [0, N)) with weights u / sum(u),
+  u ~ U(0, 1). The mix is formed in float64 from the (already rounded) K and V,
+  shared by all KV heads, then rounded to float32 (RNE) and, for bf16, to bf16
+  (RNE).
+"""
+from __future__ import annotations
+
+import concurrent.futures as _cf
+import os
+from dataclasses import dataclass, field
+from typing import Callable, Optional
+
+import numpy as np
+from numpy.random import PCG64, Generator, SeedSequence
+
+from .configs import Config
+
+BLOCK = 1 << 22
+
+TID_SCALE, TID_K, TID_V, TID_Q, TID_W, TID_EVICT, TID_SYN_POS, TID_SYN_W = range(8)
+
+
+def _threads() -> int:
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+def _rng(seed: int, cid: int, layer: int, tid: int, block: int = 0) -> Generator:
+    return Generator(PCG64(SeedSequence([seed, cid, layer, tid, block])))
+
+
+def bf16_round_bits(x: np.ndarray) -> np.ndarray:
+    """float32 -> bf16 bit patterns (uint16), round to nearest even (finite inputs)."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    r = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
+    return r.astype(np.uint16)
+
+
+def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
+    """bf16 bit patterns (uint16) -> float32 (exact)."""
+    return (np.ascontiguousarray(b, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def _normal_tensor(seed: int, cid: int, layer: int, tid: int, shape: tuple,
+                   bf16: bool, post: Optional[Callable[[np.ndarray, int], np.ndarray]] = None
+                   ) -> np.ndarray:
+    n = int(np.prod(shape))
+    out = np.empty(n, dtype=np.uint16 if bf16 else np.float32)
+    nblk = (n + BLOCK - 1) // BLOCK
+
+    def work(b: int) -> None:
+        lo = b * BLOCK
+        hi = min(n, lo + BLOCK)
+        z = _rng(seed, cid, layer, tid, b).standard_normal(hi - lo, dtype=np.float32)
+        if post is not None:
+            z = post(z, lo)
+        out[lo:hi] = bf16_round_bits(z) if bf16 else z
+
+    if nblk == 1:
+        work(0)
+    else:
+        with _cf.ThreadPoolExecutor(_threads()) as ex:
+            list(ex.map(work, range(nblk)))
+    return out.reshape(shape)
+
+
+@dataclass
+class LayerInputs:
+    """One layer's inputs. bf16 tensors hold uint16 bit patterns."""
+    cid: int
+    layer: int
+    dtype: str                   # "bf16" or "f32"
+    M: int
+    N: int
+    B: int
+    Hq: int
+    Hkv: int
+    dh: int
+    lam: float
+    scale: float
+    Q: np.ndarray                # [M, Hq, dh]
+    K: np.ndarray                # [Hkv, N, dh]
+    V: np.ndarray                # [Hkv, N, dh]
+    W: np.ndarray                # [d, d]
+    idx: Optional[np.ndarray] = None   # [B] int32 (eviction) or None
+    Kc: Optional[np.ndarray] = None    # [Hkv, B, dh] (synthesized) or None
+    Vc: Optional[np.ndarray] = None
+    extra: dict = field(default_factory=dict)
+
+    @property
+    def d(self) -> int:
+        return self.Hq * self.dh
+
+
+def _eviction_idx(rng: Generator, N: int, n_sink: int, n_recent: int, n_random: int) -> np.ndarray:
+    if n_sink + n_recent + n_random > N:
+        raise ValueError("eviction subset larger than the cache")
+    mid = rng.choice(np.arange(n_sink, N - n_recent, dtype=np.int64), size=n_random, replace=False)
+    idx = np.concatenate([np.arange(n_sink, dtype=np.int64), mid,
+                          np.arange(N - n_recent, N, dtype=np.int64)])
+    idx.sort()
+    return idx.astype(np.int32)
+
+
+def make_custom_inputs(*, M: int, N: int, B: int, Hq: int, Hkv: int, dh: int,
+                       dtype: str = "bf16", cache: str = "evict", lam: float = 1e-1,
+                       seed: int = 0, cid: int = 100, layer: int = 0,
+                       n_sink: Optional[int] = None, n_recent: Optional[int] = None,
+                       n_mix: int = 64, key_sigma: float = 0.5,
+                       d_out: Optional[int] = None) -> LayerInputs:
+    """Draw one layer of inputs of any shape with the recipe above.
+
+    For ``cache == "evict"`` the B kept positions are ``n_sink`` sinks + ``n_recent``
+    recent + the rest random (defaults: 4 sinks, half of the remainder recent).
+    ``cache == "identity"`` keeps every position (B = N): the compressed cache equals
+    the full cache.
+    """
+    if dtype not in ("bf16", "f32"):
+        raise ValueError(dtype)
+    bf16 = dtype == "bf16"
+    d = Hq * dh
+    d_out = d if d_out is None else d_out
+
+    s = _rng(seed, cid, layer, TID_SCALE).lognormal(mean=0.0, sigma=key_sigma,
+                                                    size=(Hkv, dh)).astype(np.float32)
+
+    def scale_k(z: np.ndarray, lo: int) -> np.ndarray:
+        rows = np.arange(lo // dh, (lo + z.size) // dh)
+        return (z.reshape(-1, dh) * s[rows // N]).reshape(-1)
+
+    K = _normal_tensor(seed, cid, layer, TID_K, (Hkv, N, dh), bf16, scale_k)
+    V = _normal_tensor(seed, cid, layer, TID_V, (Hkv, N, dh), bf16)
+    Q = _normal_tensor(seed, cid, layer, TID_Q, (M, Hq, dh), bf16)
+    wscale = np.float32(1.0 / np.sqrt(d))
+    W = _normal_tensor(seed, cid, layer, TID_W, (d, d_out), bf16, lambda z, lo: z * wscale)
+
+    out = LayerInputs(cid=cid, layer=layer, dtype=dtype, M=M, N=N, B=B, Hq=Hq, Hkv=Hkv,
+                      dh=dh, lam=lam, scale=1.0 / float(dh) ** 0.5, Q=Q, K=K, V=V, W=W)
+    if cache == "evict":
+        ns = 4 if n_sink is None else n_sink
+        ns = min(ns, B)
+        nr = (B - ns) // 2 if n_recent is None else n_recent
+        out.idx = _eviction_idx(_rng(seed, cid, layer, TID_EVICT), N, ns, nr, B - ns - nr)
+    elif cache == "identity":
+        if B != N:
+            raise ValueError("identity cache needs B == N")
+        out.idx = np.arange(N, dtype=np.int32)
+    elif cache == "synthesize":
+        rp = _rng(seed, cid, layer, TID_SYN_POS)
+        if n_mix > N:
+            raise ValueError("n_mix larger than the cache")
+        pos = np.stack([rp.choice(N, size=n_mix, replace=False) for _ in range(B)])
+        u = _rng(seed, cid, layer, TID_SYN_W).random((B, n_mix))
+        w = u / u.sum(axis=1, keepdims=True)
+        out.Kc = _mix(K, pos, w, bf16)
+        out.Vc = _mix(V, pos, w, bf16)
+        out.extra["syn_pos"] = pos
+        out.extra["syn_w"] = w
+    else:
+        raise ValueError(cache)
+    return out
+
+
+def _mix(X: np.ndarray, pos: np.ndarray, w: np.ndarray, bf16: bool) -> np.ndarray:
+    Hkv, _, dh = X.shape
+    B = pos.shape[0]
+    res = np.empty((Hkv, B, dh), dtype=np.uint16 if bf16 else np.float32)
+    for g in range(Hkv):
+        xg = bf16_bits_to_f32(X[g]) if bf16 else X[g]
+        mixed = np.einsum("bi,bid->bd", w, xg[pos].astype(np.float64)).astype(np.float32)
+        res[g] = bf16_round_bits(mixed) if bf16 else mixed
+    return res
+
+
+def make_layer_inputs(cfg: Config, layer: int = 0, seed: int = 0) -> LayerInputs:
+    """Inputs of layer ``layer`` of one of the five workload configs."""
+    if not 0 <= layer < cfg.layers:
+        raise ValueError(f"config {cfg.cid} has {cfg.layers} layer(s)")
+    if cfg.cache == "evict":
+        return make_custom_inputs(M=cfg.M, N=cfg.N, B=cfg.B, Hq=cfg.Hq, Hkv=cfg.Hkv,
+                                  dh=cfg.dh, dtype=cfg.dtype, cache="evict", lam=cfg.lam,
+                                  seed=seed, cid=cfg.cid, layer=layer, n_sink=cfg.n_sink,
+                                  n_recent=cfg.n_recent)
+    return make_custom_inputs(M=cfg.M, N=cfg.N, B=cfg.B, Hq=cfg.Hq, Hkv=cfg.Hkv, dh=cfg.dh,
+                              dtype=cfg.dtype, cache="synthesize", lam=cfg.lam, seed=seed,
+                              cid=cfg.cid, layer=layer, n_mix=cfg.n_mix)
