@@ -1,0 +1,190 @@
+/*
+ * patchkv.h - C ABI of the PatchKV context-loading path on one MI355X (gfx950).
+ *
+ * PatchKV (weight-space compensation of a compressed KV cache) builds, for every
+ * transformer block, a closed-form weight patch that makes the block's output
+ * under a compressed cache match its output under the full cache on a set of
+ * context-derived reference queries (Sec. 2.2-2.3, Alg. 1 of the paper). Per
+ * block the path is:
+ *
+ *   attend_full        reference queries attend over the full cache     (Alg. 1, teacher forward)
+ *   attend_compressed  the same queries over the compressed cache       (Alg. 1, student forward)
+ *   compute_targets    T = (O_f - O_c) W + rho (O_f - O_c)              (Eq. 5)
+ *   accumulate_normal_eq  G (+)= Xc^T Xc, C (+)= Xc^T (Yf - Yc)          (Eq. 9)
+ *   solve_patch        (G + lambda I) dW = C by blocked Cholesky         (Eq. 6, 8; Eq. 7 adaptive lambda)
+ *   compute_layer_patch   all of the above for one block
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Orientation: activations are rows (one token per row). With X = the
+ *   compressed-cache features (the paper's H') and T the targets, G = X^T X is the
+ *   paper's S_H, C = X^T T is the transpose of its S_T, and the returned
+ *   dW [d_in][d_out] is the transpose of its column-vector Delta W; the patched
+ *   projection is X (W + dW).
+ * - All tensor pointers are DEVICE pointers to contiguous row-major arrays owned
+ *   by the caller. The library never allocates device memory and never frees
+ *   caller memory; scratch space is the caller's `workspace` (size from the
+ *   matching *_workspace_bytes query, 256-byte aligned start recommended; at least
+ *   `workspace_bytes` bytes must be valid).
+ * - Calls are asynchronous: kernels are enqueued on `stream` (a hipStream_t; NULL
+ *   means the default stream) and the call returns. Outputs are valid once the
+ *   stream has completed. Inputs must stay valid and unmodified until then.
+ * - bf16 data are raw bfloat16 values (uint16 bit patterns); f32 are IEEE floats;
+ *   f64 are IEEE doubles.
+ * - Every argument is validated on the host before anything is enqueued. On any
+ *   error nothing is enqueued and a non-zero patchkv_status is returned.
+ *   PATCHKV_E_HIP means a HIP launch reported an error (work enqueued earlier in
+ *   the same call may have run).
+ * - Calls that share a workspace, or write the same outputs, race unless they are
+ *   ordered on one stream.
+ */
+#ifndef PATCHKV_H
+#define PATCHKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  PATCHKV_OK = 0,
+  PATCHKV_E_NULL = 1,        /* a required pointer is NULL */
+  PATCHKV_E_SHAPE = 2,       /* a size is <= 0, too large, or inconsistent (e.g. Hq % Hkv != 0) */
+  PATCHKV_E_DTYPE = 3,       /* unknown or unsupported dtype code for this argument */
+  PATCHKV_E_VALUE = 4,       /* a scalar is out of range (lambda <= 0, scale <= 0, rho not 0/1, ...) */
+  PATCHKV_E_WORKSPACE = 5,   /* workspace NULL or smaller than the matching *_workspace_bytes */
+  PATCHKV_E_UNSUPPORTED = 6, /* head_dim other than 64 or 128 */
+  PATCHKV_E_HIP = 7          /* the HIP runtime reported an error */
+} patchkv_status;
+
+typedef enum {
+  PATCHKV_F32 = 0,
+  PATCHKV_BF16 = 1,
+  PATCHKV_F64 = 2
+} patchkv_dtype;
+
+typedef enum {
+  PATCHKV_RIDGE_ABSOLUTE = 0, /* lambda is the ridge coefficient itself (Eq. 6) */
+  PATCHKV_RIDGE_ADAPTIVE = 1  /* lambda is lambda_0; ridge = lambda_0 ||G||_F^2 / tr(G) (Eq. 7) */
+} patchkv_ridge_mode;
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char* patchkv_status_string(int status);
+
+/* Library version as 10000*major + 100*minor + patch. */
+int patchkv_version(void);
+
+/* ------------------------------------------------------------------------- */
+/* Attention of reference queries over a cache (Sec. 2.2 teacher/student       */
+/* forward passes; Alg. 1).                                                    */
+/*                                                                           */
+/* O[m, h*dh + j] = sum_n softmax_n(scale * <Q[m,h,:], K[g,n,:]>) V[g,n,j],    */
+/* g = floor(h / (Hq/Hkv)) (grouped-query attention), over all cache entries   */
+/* n, with no mask (rotary embeddings already applied to Q and K).             */
+/*                                                                           */
+/* dtype: PATCHKV_BF16 (bf16 MFMA products, fp32 softmax and accumulation) or  */
+/*        PATCHKV_F32 (fp32 throughout).                                       */
+/* Q  [M][Hq][dh]      queries (dtype)                                          */
+/* K, V [Hkv][N][dh]   full cache (dtype)                                       */
+/* O  [M][Hq*dh]       float output, written (not accumulated)                  */
+/* Limits: 1 <= Hkv <= Hq, Hq % Hkv == 0, dh in {64, 128}, M >= 1, N >= 1,      */
+/*         M*Hq and N below 2^31, scale > 0 and finite.                        */
+/* ------------------------------------------------------------------------- */
+size_t patchkv_attend_workspace_bytes(int dtype, int64_t M, int64_t N, int Hq, int Hkv, int dh);
+
+int patchkv_attend_full(int dtype, const void* Q, const void* K, const void* V,
+                        int64_t M, int64_t N, int Hq, int Hkv, int dh, float scale,
+                        float* O, void* workspace, size_t workspace_bytes, void* stream);
+
+/* The same attention over a compressed cache of B entries (Alg. 1, student     */
+/* forward; Sec. 2.1 compressed cache C_b).                                     */
+/*  - idx != NULL: eviction subset. K, V are the FULL cache [Hkv][N][dh] and the */
+/*    compressed cache is K[:, idx[b], :], V[:, idx[b], :] for b < B, gathered   */
+/*    on the fly. idx [B] int32, every entry in [0, N) (precondition; entries    */
+/*    outside it are clamped into range by the kernel, never dereferenced).     */
+/*  - idx == NULL: synthesized cache. K, V are [Hkv][B][dh]; N is ignored.       */
+/* The workspace size is patchkv_attend_workspace_bytes(dtype, M, B, ...).       */
+int patchkv_attend_compressed(int dtype, const void* Q, const void* K, const void* V,
+                              const int32_t* idx, int64_t M, int64_t N, int64_t B,
+                              int Hq, int Hkv, int dh, float scale,
+                              float* O, void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------- */
+/* Per-token targets, Eq. 5 in row form with h = z = the attention output:      */
+/*   T = (O_f - O_c) W + rho (O_f - O_c)                                        */
+/* Of, Oc [M][d_in] float; W [d_in][d_out] (w_dtype PATCHKV_BF16 or F32);        */
+/* rho in {0, 1}; rho = 1 requires d_in == d_out. T [M][d_out] float, written.   */
+/* The product is formed from a two-term bf16 split of (O_f - O_c) (and of W     */
+/* when W is f32) on bf16 MFMA with fp32 accumulation (relative error ~1e-5).   */
+/* ------------------------------------------------------------------------- */
+size_t patchkv_targets_workspace_bytes(int w_dtype, int64_t M, int64_t d_in, int64_t d_out);
+
+int patchkv_compute_targets(int w_dtype, const float* Of, const float* Oc, const void* W,
+                            int64_t M, int64_t d_in, int64_t d_out, int rho, float* T,
+                            void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------- */
+/* Sufficient statistics, Eq. 9 (row form; Alg. 1 accumulation over chunks):    */
+/*   G (+)= Xc^T Xc              [d_in][d_in]                                   */
+/*   C (+)= Xc^T (Yf - Yc)       [d_in][d_out]                                  */
+/* Xc [rows][d_in], Yf [rows][d_out] float; Yc NULL means zero (Yf is then the   */
+/* target T itself). accumulate = 0 overwrites G and C, 1 adds to them (running */
+/* sums over reference chunks start from zero: call with 0 first).              */
+/* acc_dtype: PATCHKV_F32 -> G, C are float*, products from a split-bf16 MFMA   */
+/*   scheme (error ~1e-5 relative) accumulated in fp32;                        */
+/*   PATCHKV_F64 -> G, C are double*, fp64 products and accumulation.           */
+/* G is written in full (both triangles).                                       */
+/* ------------------------------------------------------------------------- */
+size_t patchkv_normal_eq_workspace_bytes(int acc_dtype, int64_t rows, int64_t d_in, int64_t d_out);
+
+int patchkv_accumulate_normal_eq(int acc_dtype, const float* Xc, const float* Yf,
+                                 const float* Yc, int64_t rows, int64_t d_in, int64_t d_out,
+                                 int accumulate, void* G, void* C,
+                                 void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------- */
+/* Ridge patch, Eq. 8 (row form): dW = (G + lambda I)^{-1} C, by a blocked      */
+/* Cholesky factorisation (G + lambda I = L L^T) and two triangular solves.     */
+/* G [d_in][d_in] (only the lower triangle is read), C [d_in][d_out], both of   */
+/* acc_dtype (F32: float, F64: double); they are not modified.                  */
+/* ridge_mode ABSOLUTE: lambda is the ridge coefficient (> 0).                  */
+/* ridge_mode ADAPTIVE: lambda is lambda_0 (> 0) and the coefficient is         */
+/*   lambda_0 ||G||_F^2 / tr(G) (Eq. 7), computed on the device in fp64.        */
+/* dW [d_in][d_out] float, written.                                             */
+/* info: device int32, written: 0 on success, else the 1-based column of the    */
+/*   first non-positive (or NaN) pivot, LAPACK style (dW is then meaningless).  */
+/* ------------------------------------------------------------------------- */
+size_t patchkv_solve_workspace_bytes(int acc_dtype, int64_t d_in, int64_t d_out);
+
+int patchkv_solve_patch(int acc_dtype, const void* G, const void* C, int64_t d_in, int64_t d_out,
+                        double lambda, int ridge_mode, float* dW, int32_t* info,
+                        void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------- */
+/* One block's patch (Alg. 1, one block and one reference chunk):               */
+/*   O_f = attend_full(Q, K, V); O_c = attend over the compressed cache;        */
+/*   T = (O_f - O_c) W + rho (O_f - O_c); G = O_c^T O_c, C = O_c^T T;           */
+/*   dW = (G + lambda I)^{-1} C.                                                */
+/* dtype: input type of Q, K, V, Kc, Vc and W (PATCHKV_BF16 or PATCHKV_F32).     */
+/* acc_dtype: statistics and solve precision (PATCHKV_F32 or PATCHKV_F64).      */
+/* Compressed cache: idx != NULL -> eviction subset of (K, V) (Kc, Vc ignored); */
+/*   idx == NULL -> synthesized Kc, Vc [Hkv][B][dh].                            */
+/* W [d][d] with d = Hq*dh. dW [d][d] float. info as in solve_patch.            */
+/* ------------------------------------------------------------------------- */
+size_t patchkv_layer_workspace_bytes(int dtype, int acc_dtype, int64_t M, int64_t N, int64_t B,
+                                     int Hq, int Hkv, int dh);
+
+int patchkv_compute_layer_patch(int dtype, int acc_dtype, const void* Q, const void* K,
+                                const void* V, const int32_t* idx, const void* Kc,
+                                const void* Vc, const void* W, int64_t M, int64_t N, int64_t B,
+                                int Hq, int Hkv, int dh, float scale, int rho, double lambda,
+                                int ridge_mode, float* dW, int32_t* info,
+                                void* workspace, size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PATCHKV_H */

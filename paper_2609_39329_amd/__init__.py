@@ -1,0 +1,12 @@
+"""PatchKV context-loading path on MI355X (gfx950): HIP kernels behind a C ABI.
+
+The library (``lib/libpatchkv.so``) is loaded on first use by :mod:`.binding`;
+there is no CPU fallback.
+"""
+from .binding import (BF16, F32, F64, RIDGE_ABSOLUTE, RIDGE_ADAPTIVE, PatchKVError,
+                      accumulate_normal_eq, attend_compressed, attend_full, compute_layer_patch,
+                      compute_targets, layer_workspace_bytes, lib, solve_patch)
+
+__all__ = ["BF16", "F32", "F64", "RIDGE_ABSOLUTE", "RIDGE_ADAPTIVE", "PatchKVError",
+           "accumulate_normal_eq", "attend_compressed", "attend_full", "compute_layer_patch",
+           "compute_targets", "layer_workspace_bytes", "lib", "solve_patch"]

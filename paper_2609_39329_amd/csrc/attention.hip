@@ -1,0 +1,505 @@
+// Reference-query attention over a KV cache (the teacher and student forward
+// passes of Alg. 1): O[m, h*dh:(h+1)*dh] = softmax(scale q_{m,h} K_g^T) V_g,
+// g = floor(h / (Hq/Hkv)), every query against every cache entry.
+//
+// bf16 path (attn_bf16_kernel): one workgroup = 4 waves x 64 query rows of one KV
+// head. The query heads of a GQA group are packed into the row dimension (row
+// r <-> query r / G, head g*G + r % G), so one K/V tile in LDS serves all of them.
+// Each wave keeps its 64 rows of Q in registers and computes S^T = K Q^T on
+// bf16 MFMA 32x32x16 (keys along the MFMA rows, queries along its columns), so a
+// lane owns one query and softmax statistics need only one cross-lane exchange
+// (lane l with l^32). P stays in registers and feeds O^T += V^T P^T directly: the
+// MFMA k-slot order is permuted consistently between P (accumulator order) and V
+// (read with the LDS transpose instruction). The online softmax runs in fp32 in
+// the exp2 domain and only rescales O when a running max grows by more than
+// 2^kTau (the result is identical, P just carries a bounded extra factor).
+// K/V tiles are double-buffered in LDS and prefetched into registers one tile
+// ahead; the workgroup -> work-item map keeps all row tiles of one KV head (and
+// key range) on one XCD so its L2 serves the K/V re-reads.
+//
+// f32 path (attn_f32_kernel): one thread per query row, fp32 FMA dot products
+// against K/V tiles broadcast from LDS, exact online softmax with expf.
+//
+// Both paths can split the cache into key ranges (more workgroups for small M);
+// attn_combine_kernel then merges the partial (O, m, l) triples.
+#include <math.h>
+
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace pkv {
+
+namespace {
+
+constexpr float kTau = 8.0f;  // lazy-rescale threshold (log2 units)
+constexpr int kKeyTile = 64;  // keys per iteration, bf16 path
+constexpr int kRowsWG = 256;  // query rows per workgroup (both paths)
+constexpr int kKeyTileF32 = 32;
+
+struct AttnParams {
+  const void* Q;
+  const void* K;
+  const void* V;
+  const int32_t* idx;
+  float* O;
+  float* Opart;
+  float* ML;
+  int Hq, G;
+  int64_t src_rows;
+  int src_valid;
+  int Nk;
+  int n_split, keys_per_split;
+  int rows;
+  int row_tiles;
+  int total_items, per_xcd;
+  float c;  // bf16: scale * log2(e); f32: scale
+};
+
+template <int DH, bool GATHER, bool PSPLIT, bool PARTIAL>
+__global__ __launch_bounds__(256, 1) void attn_bf16_kernel(AttnParams p) {
+  constexpr int KT = kKeyTile;
+  constexpr int KP = DH + 8;   // K tile pitch (elements): conflict-free 16-byte row reads
+  constexpr int VP = DH + 16;  // V tile pitch: transposing reads hit distinct banks
+  constexpr int NS = DH / 16;  // MFMA k-steps over head_dim
+  constexpr int ND = DH / 32;  // 32-wide head_dim tiles of O
+  constexpr int CH = DH / 8;   // 16-byte chunks per K/V row
+  constexpr int LPT = KT * CH / 256;
+  __shared__ __attribute__((aligned(16))) __bf16 Ks[2][KT * KP];
+  __shared__ __attribute__((aligned(16))) __bf16 Vs[2][KT * VP];
+
+  const int w = xcd_item(p.per_xcd);
+  if (w >= p.total_items) return;
+  const int rt = w % p.row_tiles;
+  const int t2 = w / p.row_tiles;
+  const int split = t2 % p.n_split;
+  const int g = t2 / p.n_split;
+  const int k_begin = split * p.keys_per_split;
+  const int k_end = min(p.Nk, k_begin + p.keys_per_split);
+  const int ntiles = (k_end - k_begin + KT - 1) / KT;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wid = tid >> 6;
+  const int h32 = lane >> 5, l32 = lane & 31;
+  const __bf16* Qb = (const __bf16*)p.Q;
+  const __bf16* Kb = (const __bf16*)p.K + (int64_t)g * p.src_rows * DH;
+  const __bf16* Vb = (const __bf16*)p.V + (int64_t)g * p.src_rows * DH;
+  const int row_base = rt * kRowsWG + wid * 64;
+
+  bf16x8 qf[2][NS];
+#pragma unroll
+  for (int qt = 0; qt < 2; ++qt) {
+    const int r = min(row_base + qt * 32 + l32, p.rows - 1);
+    const int m = r / p.G, j = r - m * p.G;
+    const __bf16* qp = Qb + ((int64_t)m * p.Hq + g * p.G + j) * DH + h32 * 8;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) qf[qt][s] = load_bf16x8(qp + s * 16);
+  }
+
+  u32x4 kreg[LPT], vreg[LPT];
+  auto load_tile = [&](int tile) {
+    const int kb0 = k_begin + tile * KT;
+#pragma unroll
+    for (int i = 0; i < LPT; ++i) {
+      const int c = i * 256 + tid;
+      const int row = c / CH, col = c % CH;
+      int src = min(kb0 + row, k_end - 1);
+      if constexpr (GATHER) src = min(max(p.idx[src], 0), p.src_valid - 1);
+      kreg[i] = *(const u32x4*)(Kb + (int64_t)src * DH + col * 8);
+      vreg[i] = *(const u32x4*)(Vb + (int64_t)src * DH + col * 8);
+    }
+  };
+  auto store_tile = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < LPT; ++i) {
+      const int c = i * 256 + tid;
+      const int row = c / CH, col = c % CH;
+      *(u32x4*)(&Ks[buf][row * KP + col * 8]) = kreg[i];
+      *(u32x4*)(&Vs[buf][row * VP + col * 8]) = vreg[i];
+    }
+  };
+
+  f32x16 o[2][ND];
+#pragma unroll
+  for (int qt = 0; qt < 2; ++qt)
+#pragma unroll
+    for (int dt = 0; dt < ND; ++dt) o[qt][dt] = f32x16{};
+  float m_run[2] = {-INFINITY, -INFINITY};
+  float l_part[2] = {0.f, 0.f};
+  const float c = p.c;
+
+  // lane-dependent offsets of the transposing V reads (see lds_read_tr16)
+  const int tr_row = 4 * h32 + ((lane & 15) >> 2);
+  const int tr_col = ((lane >> 4) & 1) * 16 + 4 * (lane & 3);
+
+  load_tile(0);
+  store_tile(0);
+  __syncthreads();
+
+  for (int t = 0; t < ntiles; ++t) {
+    const int cur = t & 1;
+    if (t + 1 < ntiles) load_tile(t + 1);
+    const __bf16* ks = Ks[cur];
+    const __bf16* vs = Vs[cur];
+
+    f32x16 s[2][2];
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int qt = 0; qt < 2; ++qt) s[kt][qt] = f32x16{};
+#pragma unroll
+    for (int st = 0; st < NS; ++st) {
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt) {
+        const bf16x8 a = *(const bf16x8*)(ks + (kt * 32 + l32) * KP + st * 16 + h32 * 8);
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt) s[kt][qt] = mfma32(a, qf[qt][st], s[kt][qt]);
+      }
+    }
+
+    const int tb = k_begin + t * KT;
+    if (tb + KT > k_end) {
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int key = tb + kt * 32 + 8 * (e >> 2) + 4 * h32 + (e & 3);
+          if (key >= k_end) {
+            s[kt][0][e] = -INFINITY;
+            s[kt][1][e] = -INFINITY;
+          }
+        }
+    }
+
+    float mt[2];
+    bool need = false;
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt) {
+      float mx = s[0][qt][0];
+#pragma unroll
+      for (int e = 1; e < 16; ++e) mx = fmaxf(mx, s[0][qt][e]);
+#pragma unroll
+      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[1][qt][e]);
+      mt[qt] = pair_max(mx) * c;
+      need |= mt[qt] > m_run[qt] + kTau;
+    }
+    if (__ballot(need) != 0) {
+#pragma unroll
+      for (int qt = 0; qt < 2; ++qt) {
+        const float mn = fmaxf(m_run[qt], mt[qt]);
+        const float alpha = fast_exp2(m_run[qt] - mn);
+        m_run[qt] = mn;
+        l_part[qt] *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt) o[qt][dt] *= alpha;
+      }
+    }
+
+    bf16x8 pb[2][2][2];
+    bf16x8 pl[2][2][2];
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int qt = 0; qt < 2; ++qt) {
+        const float nm = -m_run[qt];
+        float sum = 0.f;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const float pv = fast_exp2(fmaf(s[kt][qt][e], c, nm));
+          s[kt][qt][e] = pv;
+          sum += pv;
+        }
+        l_part[qt] += sum;
+#pragma unroll
+        for (int p2 = 0; p2 < 2; ++p2)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float pv = s[kt][qt][8 * p2 + e];
+            const __bf16 hi = to_bf16(pv);
+            pb[kt][qt][p2][e] = hi;
+            if constexpr (PSPLIT) pl[kt][qt][p2][e] = to_bf16(pv - (float)hi);
+          }
+      }
+
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int p2 = 0; p2 < 2; ++p2) {
+        const __bf16* vrow = vs + (kt * 32 + 16 * p2 + tr_row) * VP + tr_col;
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt) {
+          const PKV_LDS __bf16* vp = (const PKV_LDS __bf16*)(vrow + dt * 32);
+          const bf16x8 a = cat8(lds_read_tr16(vp), lds_read_tr16(vp + 8 * VP));
+#pragma unroll
+          for (int qt = 0; qt < 2; ++qt) {
+            o[qt][dt] = mfma32(a, pb[kt][qt][p2], o[qt][dt]);
+            if constexpr (PSPLIT) o[qt][dt] = mfma32(a, pl[kt][qt][p2], o[qt][dt]);
+          }
+        }
+      }
+
+    if (t + 1 < ntiles) store_tile(cur ^ 1);
+    __syncthreads();
+  }
+
+#pragma unroll
+  for (int qt = 0; qt < 2; ++qt) {
+    const float l = pair_sum(l_part[qt]);
+    const int r = row_base + qt * 32 + l32;
+    if (r >= p.rows) continue;
+    if constexpr (!PARTIAL) {
+      const float inv = 1.0f / l;
+      const int m = r / p.G, j = r - m * p.G;
+      float* op = p.O + ((int64_t)m * p.Hq + g * p.G + j) * DH + 4 * h32;
+#pragma unroll
+      for (int dt = 0; dt < ND; ++dt)
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          f32x4 v = {o[qt][dt][4 * jj] * inv, o[qt][dt][4 * jj + 1] * inv,
+                     o[qt][dt][4 * jj + 2] * inv, o[qt][dt][4 * jj + 3] * inv};
+          *(f32x4*)(op + dt * 32 + 8 * jj) = v;
+        }
+    } else {
+      const int64_t rid = ((int64_t)(g * p.n_split + split)) * p.rows + r;
+      float* op = p.Opart + rid * DH + 4 * h32;
+#pragma unroll
+      for (int dt = 0; dt < ND; ++dt)
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          f32x4 v = {o[qt][dt][4 * jj], o[qt][dt][4 * jj + 1], o[qt][dt][4 * jj + 2],
+                     o[qt][dt][4 * jj + 3]};
+          *(f32x4*)(op + dt * 32 + 8 * jj) = v;
+        }
+      if (h32 == 0) {
+        p.ML[2 * rid] = m_run[qt];
+        p.ML[2 * rid + 1] = l;
+      }
+    }
+  }
+}
+
+template <int DH, bool GATHER, bool PARTIAL>
+__global__ __launch_bounds__(256) void attn_f32_kernel(AttnParams p) {
+  constexpr int KT = kKeyTileF32;
+  constexpr int C4 = DH / 4;
+  __shared__ f32x4 Ks[KT * C4];
+  __shared__ f32x4 Vs[KT * C4];
+
+  const int w = xcd_item(p.per_xcd);
+  if (w >= p.total_items) return;
+  const int rt = w % p.row_tiles;
+  const int t2 = w / p.row_tiles;
+  const int split = t2 % p.n_split;
+  const int g = t2 / p.n_split;
+  const int k_begin = split * p.keys_per_split;
+  const int k_end = min(p.Nk, k_begin + p.keys_per_split);
+
+  const int tid = threadIdx.x;
+  const int r = rt * kRowsWG + tid;
+  const int rr = min(r, p.rows - 1);
+  const int m = rr / p.G, j = rr - m * p.G;
+  const float* Kb = (const float*)p.K + (int64_t)g * p.src_rows * DH;
+  const float* Vb = (const float*)p.V + (int64_t)g * p.src_rows * DH;
+  const f32x4* qp = (const f32x4*)((const float*)p.Q + ((int64_t)m * p.Hq + g * p.G + j) * DH);
+
+  f32x4 q[C4], o[C4];
+#pragma unroll
+  for (int i = 0; i < C4; ++i) {
+    q[i] = qp[i];
+    o[i] = f32x4{};
+  }
+  float mrun = -INFINITY, l = 0.f;
+
+  for (int tb = k_begin; tb < k_end; tb += KT) {
+    const int nk = min(KT, k_end - tb);
+    for (int c = tid; c < KT * C4; c += 256) {
+      const int row = c / C4, col = c % C4;
+      int src = min(tb + row, k_end - 1);
+      if constexpr (GATHER) src = min(max(p.idx[src], 0), p.src_valid - 1);
+      Ks[c] = *((const f32x4*)(Kb + (int64_t)src * DH) + col);
+      Vs[c] = *((const f32x4*)(Vb + (int64_t)src * DH) + col);
+    }
+    __syncthreads();
+    for (int kk = 0; kk < nk; ++kk) {
+      f32x4 acc = {};
+#pragma unroll
+      for (int i = 0; i < C4; ++i) {
+        const f32x4 kv = Ks[kk * C4 + i];
+        acc[0] = fmaf(q[i][0], kv[0], acc[0]);
+        acc[1] = fmaf(q[i][1], kv[1], acc[1]);
+        acc[2] = fmaf(q[i][2], kv[2], acc[2]);
+        acc[3] = fmaf(q[i][3], kv[3], acc[3]);
+      }
+      const float sc = ((acc[0] + acc[1]) + (acc[2] + acc[3])) * p.c;
+      if (sc > mrun) {
+        const float a = expf(mrun - sc);
+        l *= a;
+#pragma unroll
+        for (int i = 0; i < C4; ++i) o[i] *= a;
+        mrun = sc;
+      }
+      const float pe = expf(sc - mrun);
+      l += pe;
+#pragma unroll
+      for (int i = 0; i < C4; ++i) {
+        const f32x4 vv = Vs[kk * C4 + i];
+        o[i][0] = fmaf(pe, vv[0], o[i][0]);
+        o[i][1] = fmaf(pe, vv[1], o[i][1]);
+        o[i][2] = fmaf(pe, vv[2], o[i][2]);
+        o[i][3] = fmaf(pe, vv[3], o[i][3]);
+      }
+    }
+    __syncthreads();
+  }
+
+  if (r >= p.rows) return;
+  if constexpr (!PARTIAL) {
+    const float inv = 1.0f / l;
+    f32x4* op = (f32x4*)(p.O + ((int64_t)m * p.Hq + g * p.G + j) * DH);
+#pragma unroll
+    for (int i = 0; i < C4; ++i) op[i] = o[i] * inv;
+  } else {
+    const int64_t rid = ((int64_t)(g * p.n_split + split)) * p.rows + r;
+    f32x4* op = (f32x4*)(p.Opart + rid * DH);
+#pragma unroll
+    for (int i = 0; i < C4; ++i) op[i] = o[i];
+    p.ML[2 * rid] = mrun;
+    p.ML[2 * rid + 1] = l;
+  }
+}
+
+// Merge split-key partials: O = sum_s e^(m_s - m*) O_s / sum_s e^(m_s - m*) l_s.
+template <int DH, bool LOG2>
+__global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restrict__ Opart,
+                                                           const float* __restrict__ ML,
+                                                           float* __restrict__ O, int rows,
+                                                           int n_split, int Hkv, int G, int Hq) {
+  constexpr int C4 = DH / 4;
+  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t total = (int64_t)Hkv * rows * C4;
+  if (gid >= total) return;
+  const int c4 = (int)(gid % C4);
+  const int64_t t = gid / C4;
+  const int r = (int)(t % rows);
+  const int g = (int)(t / rows);
+  float mx = -INFINITY;
+  for (int s = 0; s < n_split; ++s) mx = fmaxf(mx, ML[2 * (((int64_t)g * n_split + s) * rows + r)]);
+  f32x4 acc = {};
+  float l = 0.f;
+  for (int s = 0; s < n_split; ++s) {
+    const int64_t rid = ((int64_t)g * n_split + s) * rows + r;
+    const float ms = ML[2 * rid];
+    const float wgt = LOG2 ? exp2f(ms - mx) : expf(ms - mx);
+    l += wgt * ML[2 * rid + 1];
+    const f32x4 v = *((const f32x4*)(Opart + rid * DH) + c4);
+    acc += wgt * v;
+  }
+  const int m = r / G, j = r - m * G;
+  *((f32x4*)(O + ((int64_t)m * Hq + g * G + j) * DH) + c4) = acc * (1.0f / l);
+}
+
+template <int DH>
+hipError_t launch_dh(const AttnShape& s, const AttnPlan& pl, AttnParams& p, bool gather,
+                     bool psplit, hipStream_t st) {
+  const bool part = pl.n_split > 1;
+  dim3 grid(pl.grid), block(256);
+  if (s.bf16) {
+#define PKV_L(G_, P_, S_) \
+  hipLaunchKernelGGL((attn_bf16_kernel<DH, G_, P_, S_>), grid, block, 0, st, p)
+    if (gather) {
+      if (psplit) { if (part) PKV_L(true, true, true); else PKV_L(true, true, false); }
+      else { if (part) PKV_L(true, false, true); else PKV_L(true, false, false); }
+    } else {
+      if (psplit) { if (part) PKV_L(false, true, true); else PKV_L(false, true, false); }
+      else { if (part) PKV_L(false, false, true); else PKV_L(false, false, false); }
+    }
+#undef PKV_L
+  } else {
+#define PKV_L(G_, S_) hipLaunchKernelGGL((attn_f32_kernel<DH, G_, S_>), grid, block, 0, st, p)
+    if (gather) { if (part) PKV_L(true, true); else PKV_L(true, false); }
+    else { if (part) PKV_L(false, true); else PKV_L(false, false); }
+#undef PKV_L
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || !part) return e;
+  const int64_t total = (int64_t)s.Hkv * p.rows * (DH / 4);
+  dim3 cg((unsigned)((total + 255) / 256));
+  if (s.bf16)
+    hipLaunchKernelGGL((attn_combine_kernel<DH, true>), cg, block, 0, st, p.Opart, p.ML, p.O,
+                       p.rows, pl.n_split, s.Hkv, p.G, s.Hq);
+  else
+    hipLaunchKernelGGL((attn_combine_kernel<DH, false>), cg, block, 0, st, p.Opart, p.ML, p.O,
+                       p.rows, pl.n_split, s.Hkv, p.G, s.Hq);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+AttnPlan plan_attention(const AttnShape& s) {
+  AttnPlan pl{};
+  const int64_t rows = s.M * (s.Hq / s.Hkv);
+  pl.row_tiles = (int)((rows + kRowsWG - 1) / kRowsWG);
+  const int kt = s.bf16 ? kKeyTile : kKeyTileF32;
+  const int64_t ntiles = (s.Nk + kt - 1) / kt;
+  const int64_t items = (int64_t)s.Hkv * pl.row_tiles;
+  // Pick the number of key ranges that minimises (rounds of workgroups) x (tiles
+  // per workgroup) plus the merge traffic, on 256 CUs with one workgroup each.
+  const double slots = 256.0;
+  // one bf16 tile-iteration of a workgroup ~ 64 x 256 x dh x 4 flops at ~4 TFLOP/s per CU
+  const double tile_s = (double)kt * kRowsWG * s.dh * 4.0 / (s.bf16 ? 4e12 : 0.25e12);
+  double best = 1e300;
+  int best_s = 1;
+  for (int sp = 1; sp <= 64 && sp <= ntiles; ++sp) {
+    const int64_t tps = (ntiles + sp - 1) / sp;
+    const int64_t waves = (items * sp + (int64_t)slots - 1) / (int64_t)slots;
+    double cost = (double)waves * tps * tile_s;
+    if (sp > 1) cost += (double)s.Hkv * rows * (s.dh + 2) * 4.0 * sp * 2 / 4e12 + 4e-6;
+    if (cost < best * 0.98) {
+      best = cost;
+      best_s = sp;
+    }
+  }
+  const int64_t tps = (ntiles + best_s - 1) / best_s;
+  pl.keys_per_split = (int)(tps * kt);
+  pl.n_split = (int)((s.Nk + pl.keys_per_split - 1) / pl.keys_per_split);
+  pl.total_items = (int)(items * pl.n_split);
+  pl.per_xcd = (pl.total_items + kXcds - 1) / kXcds;
+  pl.grid = pl.per_xcd * kXcds;
+  pl.ws_bytes = pl.n_split > 1
+                    ? align_up((size_t)s.Hkv * pl.n_split * rows * s.dh * sizeof(float)) +
+                          align_up((size_t)s.Hkv * pl.n_split * rows * 2 * sizeof(float))
+                    : 0;
+  return pl;
+}
+
+hipError_t launch_attention(const AttnShape& s, const void* Q, const void* K, const void* V,
+                            const int32_t* idx, int64_t src_rows, int64_t src_valid,
+                            float scale, bool psplit, float* O, void* ws, hipStream_t st) {
+  const AttnPlan pl = plan_attention(s);
+  AttnParams p{};
+  p.Q = Q;
+  p.K = K;
+  p.V = V;
+  p.idx = idx;
+  p.O = O;
+  if (pl.n_split > 1) {
+    p.Opart = (float*)ws;
+    p.ML = (float*)((char*)ws +
+                    align_up((size_t)s.Hkv * pl.n_split * s.M * (s.Hq / s.Hkv) * s.dh * sizeof(float)));
+  }
+  p.Hq = s.Hq;
+  p.G = s.Hq / s.Hkv;
+  p.src_rows = src_rows;
+  p.src_valid = (int)src_valid;
+  p.Nk = (int)s.Nk;
+  p.n_split = pl.n_split;
+  p.keys_per_split = pl.keys_per_split;
+  p.rows = (int)(s.M * p.G);
+  p.row_tiles = pl.row_tiles;
+  p.total_items = pl.total_items;
+  p.per_xcd = pl.per_xcd;
+  p.c = s.bf16 ? scale * 1.4426950408889634f : scale;
+  if (s.dh == 128) return launch_dh<128>(s, pl, p, idx != nullptr, psplit, st);
+  return launch_dh<64>(s, pl, p, idx != nullptr, psplit, st);
+}
+
+}  // namespace pkv

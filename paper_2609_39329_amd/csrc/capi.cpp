@@ -1,0 +1,277 @@
+// C ABI of the PatchKV context-loading path: argument validation, workspace
+// carving and kernel dispatch. Every check runs on the host before anything is
+// enqueued; the kernels themselves assume validated arguments.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include <algorithm>
+
+#include "../../include/patchkv.h"
+#include "kernels.hpp"
+
+using namespace pkv;
+
+namespace {
+
+constexpr int64_t kMaxDim = 1 << 16;           // d_in, d_out
+constexpr int64_t kMaxRows = (int64_t)1 << 31;  // M*Hq, N, B, rows
+
+bool al16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
+int status_of(hipError_t e) { return e == hipSuccess ? PATCHKV_OK : PATCHKV_E_HIP; }
+
+int check_attn_shape(int dtype, int64_t M, int64_t Nk, int Hq, int Hkv, int dh) {
+  if (dtype != PATCHKV_F32 && dtype != PATCHKV_BF16) return PATCHKV_E_DTYPE;
+  if (M < 1 || Nk < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0) return PATCHKV_E_SHAPE;
+  if (M * Hq >= kMaxRows || Nk >= kMaxRows) return PATCHKV_E_SHAPE;
+  if (dh != 64 && dh != 128) return PATCHKV_E_UNSUPPORTED;
+  return PATCHKV_OK;
+}
+
+AttnShape attn_shape(int dtype, int64_t M, int64_t Nk, int Hq, int Hkv, int dh) {
+  AttnShape s{};
+  s.M = M;
+  s.Nk = Nk;
+  s.Hq = Hq;
+  s.Hkv = Hkv;
+  s.dh = dh;
+  s.bf16 = dtype == PATCHKV_BF16;
+  return s;
+}
+
+int check_ws(const void* ws, size_t have, size_t need) {
+  if (need == 0) return PATCHKV_OK;
+  if (!ws || have < need || !al16(ws)) return PATCHKV_E_WORKSPACE;
+  return PATCHKV_OK;
+}
+
+bool finite_pos(double x) { return isfinite(x) && x > 0.0; }
+
+int check_stats_dims(int64_t rows, int64_t din, int64_t dout) {
+  if (rows < 1 || din < 1 || dout < 1) return PATCHKV_E_SHAPE;
+  if (rows >= kMaxRows || din > kMaxDim || dout > kMaxDim) return PATCHKV_E_SHAPE;
+  return PATCHKV_OK;
+}
+
+// Layer-patch workspace layout.
+struct LayerWs {
+  size_t Of, Oc, T, G, C, attn, solve, total;
+};
+
+LayerWs layer_ws(int dtype, int acc, int64_t M, int64_t N, int64_t B, int Hq, int Hkv, int dh) {
+  LayerWs L{};
+  const int64_t d = (int64_t)Hq * dh;
+  const size_t accb = acc == PATCHKV_F64 ? sizeof(double) : sizeof(float);
+  size_t o = 0;
+  L.Of = o; o += align_up(sizeof(float) * M * d);
+  L.Oc = o; o += align_up(sizeof(float) * M * d);
+  L.T = o; o += align_up(accb * M * d);
+  L.G = o; o += align_up(accb * d * d);
+  L.C = o; o += align_up(accb * d * d);
+  L.attn = o;
+  o += align_up(std::max(plan_attention(attn_shape(dtype, M, N, Hq, Hkv, dh)).ws_bytes,
+                         plan_attention(attn_shape(dtype, M, B, Hq, Hkv, dh)).ws_bytes));
+  L.solve = o; o += align_up(solve_ws_bytes(acc == PATCHKV_F64, d, d));
+  L.total = o;
+  return L;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* patchkv_status_string(int status) {
+  switch (status) {
+    case PATCHKV_OK: return "ok";
+    case PATCHKV_E_NULL: return "null pointer argument";
+    case PATCHKV_E_SHAPE: return "invalid or inconsistent shape";
+    case PATCHKV_E_DTYPE: return "unsupported dtype";
+    case PATCHKV_E_VALUE: return "scalar argument out of range or misaligned pointer";
+    case PATCHKV_E_WORKSPACE: return "workspace missing, misaligned or too small";
+    case PATCHKV_E_UNSUPPORTED: return "unsupported head_dim (64 or 128 only)";
+    case PATCHKV_E_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+int patchkv_version(void) { return 10000; }
+
+size_t patchkv_attend_workspace_bytes(int dtype, int64_t M, int64_t N, int Hq, int Hkv, int dh) {
+  if (check_attn_shape(dtype, M, N, Hq, Hkv, dh) != PATCHKV_OK) return 0;
+  return plan_attention(attn_shape(dtype, M, N, Hq, Hkv, dh)).ws_bytes;
+}
+
+int patchkv_attend_full(int dtype, const void* Q, const void* K, const void* V, int64_t M,
+                        int64_t N, int Hq, int Hkv, int dh, float scale, float* O, void* workspace,
+                        size_t workspace_bytes, void* stream) {
+  if (!Q || !K || !V || !O) return PATCHKV_E_NULL;
+  int s = check_attn_shape(dtype, M, N, Hq, Hkv, dh);
+  if (s) return s;
+  if (!finite_pos(scale)) return PATCHKV_E_VALUE;
+  if (!al16(Q) || !al16(K) || !al16(V) || !al16(O)) return PATCHKV_E_VALUE;
+  const AttnShape sh = attn_shape(dtype, M, N, Hq, Hkv, dh);
+  s = check_ws(workspace, workspace_bytes, plan_attention(sh).ws_bytes);
+  if (s) return s;
+  return status_of(launch_attention(sh, Q, K, V, nullptr, N, N, scale, false, O, workspace,
+                                    (hipStream_t)stream));
+}
+
+int patchkv_attend_compressed(int dtype, const void* Q, const void* K, const void* V,
+                              const int32_t* idx, int64_t M, int64_t N, int64_t B, int Hq, int Hkv,
+                              int dh, float scale, float* O, void* workspace,
+                              size_t workspace_bytes, void* stream) {
+  if (!Q || !K || !V || !O) return PATCHKV_E_NULL;
+  int s = check_attn_shape(dtype, M, B, Hq, Hkv, dh);
+  if (s) return s;
+  if (idx && (N < 1 || N >= kMaxRows)) return PATCHKV_E_SHAPE;
+  if (!finite_pos(scale)) return PATCHKV_E_VALUE;
+  if (!al16(Q) || !al16(K) || !al16(V) || !al16(O)) return PATCHKV_E_VALUE;
+  const AttnShape sh = attn_shape(dtype, M, B, Hq, Hkv, dh);
+  s = check_ws(workspace, workspace_bytes, plan_attention(sh).ws_bytes);
+  if (s) return s;
+  const int64_t src = idx ? N : B;
+  return status_of(launch_attention(sh, Q, K, V, idx, src, src, scale, true, O, workspace,
+                                    (hipStream_t)stream));
+}
+
+size_t patchkv_targets_workspace_bytes(int w_dtype, int64_t M, int64_t d_in, int64_t d_out) {
+  (void)w_dtype;
+  return targets_ws_bytes(M, d_in, d_out);
+}
+
+int patchkv_compute_targets(int w_dtype, const float* Of, const float* Oc, const void* W,
+                            int64_t M, int64_t d_in, int64_t d_out, int rho, float* T,
+                            void* workspace, size_t workspace_bytes, void* stream) {
+  if (!Of || !Oc || !W || !T) return PATCHKV_E_NULL;
+  if (w_dtype != PATCHKV_BF16 && w_dtype != PATCHKV_F32) return PATCHKV_E_DTYPE;
+  int s = check_stats_dims(M, d_in, d_out);
+  if (s) return s;
+  if (rho != 0 && rho != 1) return PATCHKV_E_VALUE;
+  if (rho == 1 && d_in != d_out) return PATCHKV_E_SHAPE;
+  s = check_ws(workspace, workspace_bytes, targets_ws_bytes(M, d_in, d_out));
+  if (s) return s;
+  return status_of(launch_targets(Of, Oc, W, w_dtype == PATCHKV_BF16, M, d_in, d_out, rho, T,
+                                  workspace, (hipStream_t)stream));
+}
+
+size_t patchkv_normal_eq_workspace_bytes(int acc_dtype, int64_t rows, int64_t d_in,
+                                         int64_t d_out) {
+  (void)acc_dtype;
+  return normal_eq_ws_bytes(rows, d_in, d_out);
+}
+
+int patchkv_accumulate_normal_eq(int acc_dtype, const float* Xc, const float* Yf, const float* Yc,
+                                 int64_t rows, int64_t d_in, int64_t d_out, int accumulate,
+                                 void* G, void* C, void* workspace, size_t workspace_bytes,
+                                 void* stream) {
+  if (!Xc || !Yf || !G || !C) return PATCHKV_E_NULL;
+  if (acc_dtype != PATCHKV_F32 && acc_dtype != PATCHKV_F64) return PATCHKV_E_DTYPE;
+  int s = check_stats_dims(rows, d_in, d_out);
+  if (s) return s;
+  if (accumulate != 0 && accumulate != 1) return PATCHKV_E_VALUE;
+  s = check_ws(workspace, workspace_bytes, normal_eq_ws_bytes(rows, d_in, d_out));
+  if (s) return s;
+  hipStream_t st = (hipStream_t)stream;
+  if (acc_dtype == PATCHKV_F32)
+    return status_of(launch_normal_eq_f32(Xc, Yf, Yc, rows, d_in, d_out, accumulate != 0,
+                                          (float*)G, (float*)C, workspace, st));
+  return status_of(launch_normal_eq_f64(Xc, Yf, Yc, nullptr, rows, d_in, d_out, accumulate != 0,
+                                        (double*)G, (double*)C, st));
+}
+
+size_t patchkv_solve_workspace_bytes(int acc_dtype, int64_t d_in, int64_t d_out) {
+  if (acc_dtype != PATCHKV_F32 && acc_dtype != PATCHKV_F64) return 0;
+  if (d_in < 1 || d_out < 1 || d_in > kMaxDim || d_out > kMaxDim) return 0;
+  return solve_ws_bytes(acc_dtype == PATCHKV_F64, d_in, d_out);
+}
+
+int patchkv_solve_patch(int acc_dtype, const void* G, const void* C, int64_t d_in, int64_t d_out,
+                        double lambda, int ridge_mode, float* dW, int32_t* info, void* workspace,
+                        size_t workspace_bytes, void* stream) {
+  if (!G || !C || !dW || !info) return PATCHKV_E_NULL;
+  if (acc_dtype != PATCHKV_F32 && acc_dtype != PATCHKV_F64) return PATCHKV_E_DTYPE;
+  if (d_in < 1 || d_out < 1 || d_in > kMaxDim || d_out > kMaxDim) return PATCHKV_E_SHAPE;
+  if (!finite_pos(lambda)) return PATCHKV_E_VALUE;
+  if (ridge_mode != PATCHKV_RIDGE_ABSOLUTE && ridge_mode != PATCHKV_RIDGE_ADAPTIVE)
+    return PATCHKV_E_VALUE;
+  int s = check_ws(workspace, workspace_bytes, solve_ws_bytes(acc_dtype == PATCHKV_F64, d_in, d_out));
+  if (s) return s;
+  return status_of(launch_solve(acc_dtype == PATCHKV_F64, G, C, d_in, d_out, lambda,
+                                ridge_mode == PATCHKV_RIDGE_ADAPTIVE, dW, info, workspace,
+                                (hipStream_t)stream));
+}
+
+size_t patchkv_layer_workspace_bytes(int dtype, int acc_dtype, int64_t M, int64_t N, int64_t B,
+                                     int Hq, int Hkv, int dh) {
+  if (acc_dtype != PATCHKV_F32 && acc_dtype != PATCHKV_F64) return 0;
+  if (check_attn_shape(dtype, M, N, Hq, Hkv, dh) || check_attn_shape(dtype, M, B, Hq, Hkv, dh))
+    return 0;
+  if ((int64_t)Hq * dh > kMaxDim) return 0;
+  return layer_ws(dtype, acc_dtype, M, N, B, Hq, Hkv, dh).total;
+}
+
+int patchkv_compute_layer_patch(int dtype, int acc_dtype, const void* Q, const void* K,
+                                const void* V, const int32_t* idx, const void* Kc, const void* Vc,
+                                const void* W, int64_t M, int64_t N, int64_t B, int Hq, int Hkv,
+                                int dh, float scale, int rho, double lambda, int ridge_mode,
+                                float* dW, int32_t* info, void* workspace, size_t workspace_bytes,
+                                void* stream) {
+  if (!Q || !K || !V || !W || !dW || !info) return PATCHKV_E_NULL;
+  if (!idx && (!Kc || !Vc)) return PATCHKV_E_NULL;
+  if (acc_dtype != PATCHKV_F32 && acc_dtype != PATCHKV_F64) return PATCHKV_E_DTYPE;
+  int s = check_attn_shape(dtype, M, N, Hq, Hkv, dh);
+  if (s) return s;
+  s = check_attn_shape(dtype, M, B, Hq, Hkv, dh);
+  if (s) return s;
+  const int64_t d = (int64_t)Hq * dh;
+  if (d > kMaxDim) return PATCHKV_E_SHAPE;
+  if (!finite_pos(scale) || !finite_pos(lambda)) return PATCHKV_E_VALUE;
+  if (rho != 0 && rho != 1) return PATCHKV_E_VALUE;
+  if (ridge_mode != PATCHKV_RIDGE_ABSOLUTE && ridge_mode != PATCHKV_RIDGE_ADAPTIVE)
+    return PATCHKV_E_VALUE;
+  if (!al16(Q) || !al16(K) || !al16(V) || !al16(W) || (!idx && (!al16(Kc) || !al16(Vc))))
+    return PATCHKV_E_VALUE;
+  const LayerWs L = layer_ws(dtype, acc_dtype, M, N, B, Hq, Hkv, dh);
+  s = check_ws(workspace, workspace_bytes, L.total);
+  if (s) return s;
+
+  hipStream_t st = (hipStream_t)stream;
+  char* w = (char*)workspace;
+  float* Of = (float*)(w + L.Of);
+  float* Oc = (float*)(w + L.Oc);
+  void* T = w + L.T;
+  void* G = w + L.G;
+  void* C = w + L.C;
+  void* wa = w + L.attn;
+  void* wsv = w + L.solve;
+
+  hipError_t e = launch_attention(attn_shape(dtype, M, N, Hq, Hkv, dh), Q, K, V, nullptr, N, N,
+                                  scale, false, Of, wa, st);
+  if (e != hipSuccess) return PATCHKV_E_HIP;
+  if (idx)
+    e = launch_attention(attn_shape(dtype, M, B, Hq, Hkv, dh), Q, K, V, idx, N, N, scale, true, Oc,
+                         wa, st);
+  else
+    e = launch_attention(attn_shape(dtype, M, B, Hq, Hkv, dh), Q, Kc, Vc, nullptr, B, B, scale,
+                         true, Oc, wa, st);
+  if (e != hipSuccess) return PATCHKV_E_HIP;
+  const bool wbf = dtype == PATCHKV_BF16;
+  if (acc_dtype == PATCHKV_F32) {
+    e = launch_targets(Of, Oc, W, wbf, M, d, d, rho, (float*)T, nullptr, st);
+    if (e == hipSuccess)
+      e = launch_normal_eq_f32(Oc, (const float*)T, nullptr, M, d, d, false, (float*)G, (float*)C,
+                               nullptr, st);
+  } else {
+    e = launch_targets_f64(Of, Oc, W, wbf, M, d, d, rho, (double*)T, st);
+    if (e == hipSuccess)
+      e = launch_normal_eq_f64(Oc, nullptr, nullptr, (const double*)T, M, d, d, false, (double*)G,
+                               (double*)C, st);
+  }
+  if (e != hipSuccess) return PATCHKV_E_HIP;
+  e = launch_solve(acc_dtype == PATCHKV_F64, G, C, d, d, lambda,
+                   ridge_mode == PATCHKV_RIDGE_ADAPTIVE, dW, info, wsv, st);
+  return status_of(e);
+}
+
+}  // extern "C"

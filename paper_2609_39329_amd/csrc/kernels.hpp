@@ -1,0 +1,67 @@
+// Internal launcher interface between the C ABI (capi.cpp) and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace pkv {
+
+// ---------------------------------------------------------------- attention
+struct AttnShape {
+  int64_t M;         // reference queries
+  int64_t Nk;        // cache entries attended
+  int Hq, Hkv, dh;
+  bool bf16;         // input dtype: bf16 (MFMA path) or f32
+};
+
+struct AttnPlan {
+  int n_split;         // number of key ranges (1 = no partial outputs)
+  int keys_per_split;  // multiple of the key tile
+  int row_tiles;       // query-row tiles per KV head
+  int total_items;     // Hkv * n_split * row_tiles
+  int per_xcd;         // work items per XCD
+  int grid;            // launched workgroups (multiple of the XCD count)
+  size_t ws_bytes;     // workspace: partial outputs and (m, l) pairs
+};
+
+AttnPlan plan_attention(const AttnShape& s);
+
+// Q [M][Hq][dh]; K, V rows of KV head g start at (g * src_rows) * dh; when idx is
+// non-null, cache entry n is row idx[n] (clamped into [0, src_valid)).
+// psplit: form P V from a two-term bf16 split of P (bf16 path only).
+hipError_t launch_attention(const AttnShape& s, const void* Q, const void* K, const void* V,
+                            const int32_t* idx, int64_t src_rows, int64_t src_valid,
+                            float scale, bool psplit, float* O, void* ws, hipStream_t st);
+
+// ---------------------------------------------------------------- statistics (fp32 acc)
+size_t targets_ws_bytes(int64_t M, int64_t din, int64_t dout);
+// T = (Of - Oc) W + rho (Of - Oc); W bf16 (w_bf16) or f32.
+hipError_t launch_targets(const float* Of, const float* Oc, const void* W, bool w_bf16,
+                          int64_t M, int64_t din, int64_t dout, int rho, float* T, void* ws,
+                          hipStream_t st);
+size_t normal_eq_ws_bytes(int64_t rows, int64_t din, int64_t dout);
+// G (+)= X^T X, C (+)= X^T (Yf - Yc) with split-bf16 MFMA, fp32 accumulation.
+hipError_t launch_normal_eq_f32(const float* X, const float* Yf, const float* Yc, int64_t rows,
+                                int64_t din, int64_t dout, bool accumulate, float* G, float* C,
+                                void* ws, hipStream_t st);
+
+// ---------------------------------------------------------------- statistics (fp64 acc)
+hipError_t launch_targets_f64(const float* Of, const float* Oc, const void* W, bool w_bf16,
+                              int64_t M, int64_t din, int64_t dout, int rho, double* T,
+                              hipStream_t st);
+// G (+)= X^T X, C (+)= X^T Y with Y = Yf - Yc (floats) or Yd (doubles, when non-null).
+hipError_t launch_normal_eq_f64(const float* X, const float* Yf, const float* Yc, const double* Yd,
+                                int64_t rows, int64_t din, int64_t dout, bool accumulate,
+                                double* G, double* C, hipStream_t st);
+
+// ---------------------------------------------------------------- ridge solve
+size_t solve_ws_bytes(bool f64, int64_t din, int64_t dout);
+hipError_t launch_solve(bool f64, const void* G, const void* C, int64_t din, int64_t dout,
+                        double lambda, bool adaptive, float* dW, int32_t* info, void* ws,
+                        hipStream_t st);
+
+// Small helpers.
+inline size_t align_up(size_t x, size_t a = 256) { return (x + a - 1) / a * a; }
+
+}  // namespace pkv

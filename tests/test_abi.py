@@ -1,0 +1,128 @@
+"""CPU checks of the C ABI: the library loads, exports every declared symbol, and
+rejects invalid arguments on the host (no GPU work is ever enqueued here)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_39329_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "patchkv.h")
+FAKE = 1 << 12  # a non-null, 16-byte aligned fake address; never dereferenced
+
+
+def declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(patchkv_\w+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    return B.lib()
+
+
+def test_exports_every_declared_symbol(L):
+    names = declared()
+    assert len(names) >= 13
+    for n in names:
+        assert hasattr(L, n), n
+        assert n in B.SIGNATURES, f"binding lacks {n}"
+    assert set(B.SIGNATURES) == set(names)
+
+
+def test_status_strings(L):
+    for s in range(8):
+        assert L.patchkv_status_string(s)
+    assert L.patchkv_status_string(99) == b"unknown status"
+    assert L.patchkv_version() >= 10000
+
+
+def test_workspace_queries(L):
+    assert L.patchkv_attend_workspace_bytes(B.BF16, 4096, 172032, 32, 8, 128) == 0  # no split
+    assert L.patchkv_attend_workspace_bytes(B.BF16, 1024, 32768, 32, 8, 128) > 0    # split
+    assert L.patchkv_attend_workspace_bytes(B.BF16, 10, 10, 3, 2, 128) == 0          # invalid
+    assert L.patchkv_solve_workspace_bytes(B.F32, 4096, 4096) >= 5 * 4096 * 4096 * 4
+    assert L.patchkv_solve_workspace_bytes(B.F64, 256, 256) >= 5 * 256 * 256 * 8
+    lw = L.patchkv_layer_workspace_bytes(B.BF16, B.F32, 4096, 172032, 1720, 32, 8, 128)
+    assert lw > 3 * 4096 * 4096 * 4
+    assert L.patchkv_layer_workspace_bytes(B.BF16, 7, 4096, 1, 1, 32, 8, 128) == 0
+
+
+def attend(L, dt=B.BF16, Q=FAKE, K=FAKE, V=FAKE, M=8, N=64, Hq=4, Hkv=2, dh=128, scale=0.1, O=FAKE,
+           ws=None, wsb=0):
+    return L.patchkv_attend_full(dt, Q, K, V, M, N, Hq, Hkv, dh, scale, O, ws, wsb, None)
+
+
+def test_attend_validation(L):
+    assert attend(L, Q=None) == B.E_NULL
+    assert attend(L, O=None) == B.E_NULL
+    assert attend(L, dt=B.F64) == B.E_DTYPE
+    assert attend(L, dt=5) == B.E_DTYPE
+    assert attend(L, M=0) == B.E_SHAPE
+    assert attend(L, N=-1) == B.E_SHAPE
+    assert attend(L, Hq=3, Hkv=2) == B.E_SHAPE
+    assert attend(L, dh=96) == B.E_UNSUPPORTED
+    assert attend(L, scale=0.0) == B.E_VALUE
+    assert attend(L, scale=float("nan")) == B.E_VALUE
+    assert attend(L, Q=FAKE + 2) == B.E_VALUE           # misaligned
+    # a shape that needs split-key workspace, given none
+    assert attend(L, M=16, N=1 << 15, Hq=32, Hkv=8) == B.E_WORKSPACE
+    r = L.patchkv_attend_compressed(B.BF16, FAKE, FAKE, FAKE, FAKE, 8, 0, 16, 4, 2, 128, 0.1, FAKE,
+                                    None, 0, None)
+    assert r == B.E_SHAPE                                 # idx given but N = 0
+    r = L.patchkv_attend_compressed(B.BF16, FAKE, FAKE, FAKE, None, 8, 64, 0, 4, 2, 128, 0.1, FAKE,
+                                    None, 0, None)
+    assert r == B.E_SHAPE                                 # B = 0
+
+
+def test_targets_validation(L):
+    f = L.patchkv_compute_targets
+    assert f(B.BF16, None, FAKE, FAKE, 4, 8, 8, 1, FAKE, None, 0, None) == B.E_NULL
+    assert f(B.F64, FAKE, FAKE, FAKE, 4, 8, 8, 1, FAKE, None, 0, None) == B.E_DTYPE
+    assert f(B.BF16, FAKE, FAKE, FAKE, 4, 8, 6, 1, FAKE, None, 0, None) == B.E_SHAPE  # rho needs square
+    assert f(B.BF16, FAKE, FAKE, FAKE, 4, 8, 8, 2, FAKE, None, 0, None) == B.E_VALUE
+    assert f(B.BF16, FAKE, FAKE, FAKE, 0, 8, 8, 1, FAKE, None, 0, None) == B.E_SHAPE
+
+
+def test_normal_eq_validation(L):
+    f = L.patchkv_accumulate_normal_eq
+    assert f(B.F32, FAKE, None, None, 4, 8, 8, 0, FAKE, FAKE, None, 0, None) == B.E_NULL
+    assert f(B.BF16, FAKE, FAKE, None, 4, 8, 8, 0, FAKE, FAKE, None, 0, None) == B.E_DTYPE
+    assert f(B.F32, FAKE, FAKE, None, 4, 1 << 17, 8, 0, FAKE, FAKE, None, 0, None) == B.E_SHAPE
+    assert f(B.F32, FAKE, FAKE, None, 4, 8, 8, 3, FAKE, FAKE, None, 0, None) == B.E_VALUE
+
+
+def test_solve_validation(L):
+    f = L.patchkv_solve_patch
+    nb = L.patchkv_solve_workspace_bytes(B.F32, 16, 16)
+    assert f(B.F32, FAKE, FAKE, 16, 16, 0.1, 0, FAKE, None, FAKE, nb, None) == B.E_NULL
+    assert f(B.F32, FAKE, FAKE, 16, 16, 0.0, 0, FAKE, FAKE, FAKE, nb, None) == B.E_VALUE
+    assert f(B.F32, FAKE, FAKE, 16, 16, -1.0, 0, FAKE, FAKE, FAKE, nb, None) == B.E_VALUE
+    assert f(B.F32, FAKE, FAKE, 16, 16, 0.1, 2, FAKE, FAKE, FAKE, nb, None) == B.E_VALUE
+    assert f(B.F32, FAKE, FAKE, 16, 16, 0.1, 0, FAKE, FAKE, None, nb, None) == B.E_WORKSPACE
+    assert f(B.F32, FAKE, FAKE, 16, 16, 0.1, 0, FAKE, FAKE, FAKE, nb - 1, None) == B.E_WORKSPACE
+    assert f(B.F32, FAKE, FAKE, 0, 16, 0.1, 0, FAKE, FAKE, FAKE, nb, None) == B.E_SHAPE
+
+
+def test_layer_validation(L):
+    f = L.patchkv_compute_layer_patch
+    args = dict(dt=B.BF16, acc=B.F32, Q=FAKE, K=FAKE, V=FAKE, idx=FAKE, Kc=None, Vc=None, W=FAKE,
+                M=8, N=64, Bn=16, Hq=4, Hkv=2, dh=128, scale=0.1, rho=1, lam=0.1, mode=0, dW=FAKE,
+                info=FAKE, ws=None, wsb=0)
+
+    def call(**kw):
+        a = dict(args, **kw)
+        return f(a["dt"], a["acc"], a["Q"], a["K"], a["V"], a["idx"], a["Kc"], a["Vc"], a["W"],
+                 a["M"], a["N"], a["Bn"], a["Hq"], a["Hkv"], a["dh"], a["scale"], a["rho"],
+                 a["lam"], a["mode"], a["dW"], a["info"], a["ws"], a["wsb"], None)
+
+    assert call(idx=None) == B.E_NULL            # neither idx nor Kc/Vc
+    assert call(acc=B.BF16) == B.E_DTYPE
+    assert call(Hq=4, Hkv=3) == B.E_SHAPE
+    assert call(lam=0.0) == B.E_VALUE
+    assert call(rho=3) == B.E_VALUE
+    assert call(mode=7) == B.E_VALUE
+    assert call() == B.E_WORKSPACE               # needs a workspace

@@ -1,0 +1,108 @@
+"""GPU parity of the attention entry points against the fp64 oracle.
+
+Tolerances (relative Frobenius error of O):
+* bf16 full-cache pass: P enters the P V product rounded to bf16 (relative
+  rounding error <= 2^-9 per weight, RMS ~1.1e-3), Q K^T and the accumulation are
+  exact / fp32, so the error of O stays near 1e-3; bound 4e-3.
+* bf16 compressed pass: P enters as a two-term bf16 split (error ~2^-17), so only
+  fp32 accumulation remains; bound 5e-5.
+* fp32 inputs: fp32 dot products, softmax and accumulation; bound 2e-5.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_39329_amd as pkv
+from gpu_util import DEV, host, idx_dev, rel, to_dev
+from workloads import make_custom_inputs
+
+pytestmark = pytest.mark.gpu
+
+TOL_FULL = {"bf16": 4e-3, "f32": 2e-5}
+TOL_COMP = {"bf16": 5e-5, "f32": 2e-5}
+
+SHAPES = [
+    # M, N, B, Hq, Hkv, dh, dtype
+    (64, 700, 150, 8, 2, 128, "bf16"),      # ragged N (not a multiple of the 64-key tile)
+    (100, 1000, 333, 28, 4, 128, "bf16"),   # GQA group of 7, ragged row tiles
+    (33, 129, 17, 4, 4, 64, "bf16"),        # head_dim 64, group 1
+    (300, 2049, 260, 32, 8, 128, "bf16"),   # several row tiles, ragged tail
+    (16, 40000, 4000, 8, 8, 128, "bf16"),   # few rows, long cache: split-key path + merge
+    (128, 2048, 256, 4, 2, 64, "f32"),      # tiny fp32 layer shape
+    (50, 333, 100, 8, 2, 128, "f32"),
+    (8, 20000, 3000, 4, 2, 64, "f32"),      # fp32 split-key path
+]
+
+
+def _decode(inp):
+    return (oracle.decode(inp.Q, inp.dtype), oracle.decode(inp.K, inp.dtype),
+            oracle.decode(inp.V, inp.dtype))
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_attend_full_and_compressed(shape):
+    M, N, B, Hq, Hkv, dh, dt = shape
+    print(f"attention parity M={M} N={N} B={B} Hq={Hq} Hkv={Hkv} dh={dh} {dt}", flush=True)
+    inp = make_custom_inputs(M=M, N=N, B=B, Hq=Hq, Hkv=Hkv, dh=dh, dtype=dt, seed=M + N)
+    Q, K, V = _decode(inp)
+    q, k, v = to_dev(inp.Q, dt), to_dev(inp.K, dt), to_dev(inp.V, dt)
+    Of = host(pkv.attend_full(q, k, v))
+    ref = oracle.attention(Q, K, V, inp.scale)
+    assert rel(Of, ref) <= TOL_FULL[dt]
+    Oc = host(pkv.attend_compressed(q, k, v, idx=idx_dev(inp.idx)))
+    Kc, Vc = oracle.gather_cache(K, V, inp.idx)
+    assert rel(Oc, oracle.attention(Q, Kc, Vc, inp.scale)) <= TOL_COMP[dt]
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+def test_attend_synthesized_cache(dt):
+    inp = make_custom_inputs(M=70, N=900, B=120, Hq=8, Hkv=2, dh=128, dtype=dt, cache="synthesize",
+                             n_mix=16, seed=5)
+    Q = oracle.decode(inp.Q, dt)
+    Kc, Vc = oracle.decode(inp.Kc, dt), oracle.decode(inp.Vc, dt)
+    Oc = host(pkv.attend_compressed(to_dev(inp.Q, dt), to_dev(inp.Kc, dt), to_dev(inp.Vc, dt)))
+    assert rel(Oc, oracle.attention(Q, Kc, Vc, inp.scale)) <= TOL_COMP[dt]
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+def test_identity_gather_matches_full(dt):
+    """idx = 0..N-1 reproduces the full-cache attention."""
+    inp = make_custom_inputs(M=40, N=500, B=500, Hq=4, Hkv=2, dh=128, dtype=dt, cache="identity",
+                             seed=2)
+    q, k, v = to_dev(inp.Q, dt), to_dev(inp.K, dt), to_dev(inp.V, dt)
+    Of = host(pkv.attend_full(q, k, v))
+    Oc = host(pkv.attend_compressed(q, k, v, idx=idx_dev(inp.idx)))
+    assert rel(Oc, Of) <= TOL_FULL[dt]
+
+
+def test_gather_permutation_and_duplicates():
+    """A permuted index set gives the same output; a duplicated entry counts twice."""
+    inp = make_custom_inputs(M=30, N=300, B=64, Hq=8, Hkv=4, dh=128, dtype="bf16", seed=4)
+    q, k, v = to_dev(inp.Q, "bf16"), to_dev(inp.K, "bf16"), to_dev(inp.V, "bf16")
+    base = host(pkv.attend_compressed(q, k, v, idx=idx_dev(inp.idx)))
+    perm = np.random.default_rng(0).permutation(inp.idx)
+    assert rel(host(pkv.attend_compressed(q, k, v, idx=idx_dev(perm))), base) <= 1e-5
+    dup = np.concatenate([inp.idx, inp.idx[:5]])
+    Q, K, V = _decode(inp)
+    Kc, Vc = oracle.gather_cache(K, V, dup)
+    got = host(pkv.attend_compressed(q, k, v, idx=idx_dev(dup)))
+    assert rel(got, oracle.attention(Q, Kc, Vc, inp.scale)) <= TOL_COMP["bf16"]
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+def test_single_entry_cache_returns_its_value(dt):
+    inp = make_custom_inputs(M=20, N=1, B=1, Hq=4, Hkv=2, dh=64, dtype=dt, cache="identity", seed=9)
+    O = host(pkv.attend_full(to_dev(inp.Q, dt), to_dev(inp.K, dt), to_dev(inp.V, dt)))
+    V = oracle.decode(inp.V, dt)
+    ref = np.concatenate([V[h // 2, 0] for h in range(4)])[None, :].repeat(20, axis=0)
+    assert np.array_equal(O, ref)
+
+
+def test_attention_deterministic():
+    inp = make_custom_inputs(M=64, N=3000, B=100, Hq=8, Hkv=2, dh=128, dtype="bf16", seed=8)
+    q, k, v = to_dev(inp.Q, "bf16"), to_dev(inp.K, "bf16"), to_dev(inp.V, "bf16")
+    a = pkv.attend_full(q, k, v)
+    b = pkv.attend_full(q, k, v)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)

@@ -1,0 +1,150 @@
+"""GPU parity of targets, sufficient statistics and the ridge solve.
+
+Tolerances (relative Frobenius error):
+* fp32 accumulation path: operands split into two bf16 terms (representation
+  error ~2^-17 relative) with fp32 accumulation: targets and statistics within
+  5e-5.
+* fp64 accumulation path: fp64 products of fp32 inputs: 1e-12.
+* solve, fp32: Cholesky + triangular solves in fp32 on a system with condition
+  number ~1e2-1e3: error ~ kappa * 1e-7, bound 1e-4. fp64: 1e-10.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_39329_amd as pkv
+from gpu_util import DEV, host, rel
+
+pytestmark = pytest.mark.gpu
+
+
+def randn(shape, seed, scale=1.0):
+    return np.random.default_rng(seed).standard_normal(shape).astype(np.float32) * np.float32(scale)
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+@pytest.mark.parametrize("M,din,dout,wdt,rho", [
+    (200, 256, 256, "bf16", 1),
+    (77, 300, 300, "f32", 1),
+    (130, 200, 96, "bf16", 0),       # rectangular, ragged tiles
+    (1024, 1024, 1024, "bf16", 1),
+])
+def test_targets(M, din, dout, wdt, rho):
+    Of, Oc = randn((M, din), 1, 0.3), randn((M, din), 2, 0.3)
+    W = randn((din, dout), 3, 1 / np.sqrt(din))
+    if wdt == "bf16":
+        Wt = dev(W).to(torch.bfloat16)
+        Wref = Wt.float().cpu().numpy().astype(np.float64)
+    else:
+        Wt = dev(W)
+        Wref = W.astype(np.float64)
+    T = host(pkv.compute_targets(dev(Of), dev(Oc), Wt, rho=rho))
+    ref = oracle.targets(Of.astype(np.float64), Oc.astype(np.float64), Wref, rho)
+    assert rel(T, ref) <= 5e-5
+
+
+@pytest.mark.parametrize("rows,din,dout", [(128, 256, 256), (300, 200, 130), (2048, 1024, 1024),
+                                           (5, 64, 33)])
+def test_normal_equations_f32(rows, din, dout):
+    X, Yf, Yc = randn((rows, din), 4, 0.2), randn((rows, dout), 5), randn((rows, dout), 6)
+    G, C = pkv.accumulate_normal_eq(dev(X), dev(Yf), dev(Yc), acc=pkv.F32)
+    Gr, Cr = oracle.normal_equations(X.astype(np.float64), Yf.astype(np.float64) - Yc.astype(np.float64))
+    assert rel(host(G), Gr) <= 5e-5
+    assert rel(host(C), Cr) <= 5e-5
+    g = host(G)
+    assert np.array_equal(g, g.T)
+
+
+@pytest.mark.parametrize("acc", ["f32", "f64"])
+def test_normal_equations_accumulate_chunks(acc):
+    """Eq. 9: running sums over reference chunks equal the one-shot statistics."""
+    code = pkv.F32 if acc == "f32" else pkv.F64
+    rows, din, dout = 700, 192, 160
+    X, Y = randn((rows, din), 7, 0.5), randn((rows, dout), 8)
+    Gr, Cr = oracle.normal_equations(X.astype(np.float64), Y.astype(np.float64))
+    G = C = None
+    for a, b in [(0, 100), (100, 101), (101, 450), (450, 700)]:
+        G, C = pkv.accumulate_normal_eq(dev(X[a:b]), dev(Y[a:b]), G=G, C=C, acc=code,
+                                        accumulate=a > 0)
+    tol = 5e-5 if acc == "f32" else 1e-12
+    assert rel(host(G), Gr) <= tol and rel(host(C), Cr) <= tol
+
+
+def test_normal_equations_f64():
+    rows, din, dout = 150, 256, 256
+    X, Yf, Yc = randn((rows, din), 9, 0.2), randn((rows, dout), 10), randn((rows, dout), 11)
+    G, C = pkv.accumulate_normal_eq(dev(X), dev(Yf), dev(Yc), acc=pkv.F64)
+    Gr, Cr = oracle.normal_equations(X.astype(np.float64), Yf.astype(np.float64) - Yc.astype(np.float64))
+    assert rel(host(G), Gr) <= 1e-12 and rel(host(C), Cr) <= 1e-12
+
+
+def _spd_system(d, dout, rows, seed, scale=0.3):
+    X = randn((rows, d), seed, scale).astype(np.float64)
+    T = randn((rows, dout), seed + 1).astype(np.float64)
+    return oracle.normal_equations(X, T)
+
+
+@pytest.mark.parametrize("d,dout,rows,acc,lam", [
+    (256, 256, 400, "f64", 1e-2),
+    (300, 130, 500, "f64", 0.3),     # ragged last block, rectangular right-hand side
+    (512, 512, 1000, "f32", 0.1),
+    (1000, 700, 1500, "f32", 0.5),
+    (64, 64, 30, "f32", 1.0),        # single block, rank-deficient X
+])
+def test_solve(d, dout, rows, acc, lam):
+    G, C = _spd_system(d, dout, rows, d + dout)
+    tdt = torch.float64 if acc == "f64" else torch.float32
+    dW, info = pkv.solve_patch(dev(G).to(tdt), dev(C).to(tdt), lam)
+    assert int(info.item()) == 0
+    Gin = G if acc == "f64" else G.astype(np.float32).astype(np.float64)
+    Cin = C if acc == "f64" else C.astype(np.float32).astype(np.float64)
+    ref = oracle.solve_patch(Gin, Cin, lam)
+    assert rel(host(dW), ref) <= (1e-10 if acc == "f64" else 1e-4)
+
+
+@pytest.mark.parametrize("acc", ["f32", "f64"])
+def test_solve_adaptive_ridge(acc):
+    G, C = _spd_system(200, 150, 300, 3)
+    tdt = torch.float64 if acc == "f64" else torch.float32
+    dW, info = pkv.solve_patch(dev(G).to(tdt), dev(C).to(tdt), 0.01, mode=pkv.RIDGE_ADAPTIVE)
+    assert int(info.item()) == 0
+    Gin = G if acc == "f64" else G.astype(np.float32).astype(np.float64)
+    Cin = C if acc == "f64" else C.astype(np.float32).astype(np.float64)
+    lam = oracle.ridge_lambda(Gin, 0.01, "adaptive")
+    assert rel(host(dW), oracle.solve_patch(Gin, Cin, lam)) <= (1e-10 if acc == "f64" else 1e-4)
+
+
+@pytest.mark.parametrize("acc", ["f32", "f64"])
+def test_solve_reports_non_positive_pivot(acc):
+    """A G that is not positive semidefinite gives info = first failing column."""
+    d = 300
+    G = np.eye(d)
+    G[150, 150] = -5.0
+    C = np.ones((d, 8))
+    tdt = torch.float64 if acc == "f64" else torch.float32
+    _, info = pkv.solve_patch(dev(G).to(tdt), dev(C).to(tdt), 1.0)
+    assert int(info.item()) == 151
+
+
+def test_zero_patch_for_identical_caches():
+    """O_c == O_f bitwise => T = 0 => C = 0 => dW = 0 exactly."""
+    from workloads import make_custom_inputs
+    from gpu_util import idx_dev, to_dev
+    inp = make_custom_inputs(M=64, N=256, B=256, Hq=4, Hkv=2, dh=64, dtype="bf16",
+                             cache="identity", seed=1)
+    q, k, v = to_dev(inp.Q, "bf16"), to_dev(inp.K, "bf16"), to_dev(inp.V, "bf16")
+    idx = idx_dev(inp.idx)
+    O1 = pkv.attend_compressed(q, k, v, idx=idx)
+    O2 = pkv.attend_compressed(q, k, v, idx=idx)
+    T = pkv.compute_targets(O1, O2, to_dev(inp.W, "bf16"), rho=1)
+    G, C = pkv.accumulate_normal_eq(O2, T, acc=pkv.F32)
+    dW, info = pkv.solve_patch(G, C, 0.1)
+    torch.cuda.synchronize()
+    assert int(info.item()) == 0
+    assert torch.count_nonzero(T).item() == 0
+    assert torch.count_nonzero(C).item() == 0
+    assert torch.count_nonzero(dW).item() == 0
