@@ -1,0 +1,243 @@
+"""Benchmark of the PatchKV context-loading path on one MI355X.
+
+A step is one pass of the whole hot path over one batch of synthetic input: for
+every layer of the workload, attention of the M reference queries over the full
+cache and over the compressed cache, targets, normal equations and the ridge
+solve (the same five library calls, in the same order, that
+patchkv_compute_layer_patch makes). The default workload is the 32-layer
+Llama-3-8B-shaped patch build over a 172,032-token context (1 % cache budget,
+4,096 reference queries per layer). All layer inputs are resident in HBM before
+the timed region starts.
+
+Prints one JSON line: seconds per layer patch (value), attention TFLOP/s and its
+fraction of the bf16 MFMA peak, context tokens/s, the roofline of the dominant
+kernel (the full-cache attention, timed with HIP events on its stream inside the
+timed region) and the fp64 CPU oracle timed on a bounded sample of the same
+workload.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 3] [--layers L]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "sec per layer patch + ref-query attention TFLOP/s (% of MFMA peak), 1 MI355X"
+PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3     # MI355X fp32 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--config", type=int, default=3)
+    ap.add_argument("--layers", type=int, default=None, help="layers per step (default: all)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-rows", type=int, default=32,
+                    help="query rows of the oracle sample for the CPU baseline")
+    return ap.parse_args()
+
+
+class LayerDev:
+    """One layer's inputs on the device."""
+
+    def __init__(self, inp, torch, dev):
+        def t(a):
+            x = torch.from_numpy(np.ascontiguousarray(a))
+            if inp.dtype == "bf16":
+                x = x.view(torch.bfloat16)
+            return x.to(dev, non_blocking=False)
+        self.Q, self.K, self.V, self.W = t(inp.Q), t(inp.K), t(inp.V), t(inp.W)
+        self.idx = (torch.from_numpy(inp.idx).to(dev) if inp.idx is not None else None)
+        self.Kc = t(inp.Kc) if inp.Kc is not None else None
+        self.Vc = t(inp.Vc) if inp.Vc is not None else None
+
+
+def cpu_baseline(cfg, rows: int) -> dict:
+    """The fp64 oracle on a bounded sample of one layer, scaled to s / layer patch.
+
+    Sample: layer 0's attention (full and compressed cache) and statistics for
+    ``rows`` of the M reference queries (their cost is linear in M, so it is scaled
+    by M / rows), plus the complete d x d ridge solve (independent of M).
+    """
+    import oracle
+    from workloads import make_layer_inputs
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        blas_threads = None
+    cores = len(os.sched_getaffinity(0))
+    inp = make_layer_inputs(cfg, 0)
+    dt = inp.dtype
+    sel = np.linspace(0, cfg.M - 1, rows).astype(np.int64)
+    t0 = time.perf_counter()
+    Q = oracle.decode(inp.Q[sel], dt)
+    K, V = oracle.decode(inp.K, dt), oracle.decode(inp.V, dt)
+    W = oracle.decode(inp.W, dt)
+    Of = oracle.attention(Q, K, V, inp.scale)
+    if inp.idx is not None:
+        Kc, Vc = oracle.gather_cache(K, V, inp.idx)
+    else:
+        Kc, Vc = oracle.decode(inp.Kc, dt), oracle.decode(inp.Vc, dt)
+    Oc = oracle.attention(Q, Kc, Vc, inp.scale)
+    T = oracle.targets(Of, Oc, W, 1)
+    G, C = oracle.normal_equations(Oc, T)
+    t_rows = time.perf_counter() - t0
+    # the solve at full size needs a well-posed full-size G: scale the sampled
+    # statistics up to M rows' worth of mass (its cost does not depend on G's values)
+    t1 = time.perf_counter()
+    oracle.solve_patch(G * (cfg.M / rows), C * (cfg.M / rows), cfg.lam)
+    t_solve = time.perf_counter() - t1
+    est = t_rows * (cfg.M / rows) + t_solve
+    return {"value": est, "unit": "s/layer-patch", "cores": cores, "blas_threads": blas_threads,
+            "kind": "oracle",
+            "sample": f"config {cfg.cid} layer 0: fp64 attention (full + compressed), targets and "
+                      f"statistics for {rows} of {cfg.M} reference queries "
+                      f"({t_rows:.2f} s, scaled x{cfg.M / rows:.0f}) + full {cfg.d}x{cfg.d} "
+                      f"Cholesky solve ({t_solve:.2f} s); input decoding included"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on exactly one GPU: this build has no multi-GPU path "
+              f"(asked for --gpus {args.gpus}).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2609_39329_amd as pkv
+    from workloads import get_config, make_layer_inputs
+
+    cfg = get_config(args.config)
+    nl = cfg.layers if args.layers is None else min(args.layers, cfg.layers)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    dt_code = pkv.BF16 if cfg.dtype == "bf16" else pkv.F32
+    acc = pkv.F64 if cfg.dtype == "f32" else pkv.F32
+    adt = torch.float64 if acc == pkv.F64 else torch.float32
+
+    t0 = time.perf_counter()
+    layers = []
+    for layer in range(nl):
+        layers.append(LayerDev(make_layer_inputs(cfg, layer), torch, dev))
+        if layer % 8 == 7 or layer == nl - 1:
+            log(f"[bench] inputs of {layer + 1}/{nl} layers resident ({time.perf_counter() - t0:.1f} s)")
+    torch.cuda.synchronize()
+
+    M, d = cfg.M, cfg.d
+    Of = torch.empty((M, d), dtype=torch.float32, device=dev)
+    Oc = torch.empty((M, d), dtype=torch.float32, device=dev)
+    T = torch.empty((M, d), dtype=torch.float32, device=dev)
+    G = torch.empty((d, d), dtype=adt, device=dev)
+    C = torch.empty((d, d), dtype=adt, device=dev)
+    dW = [torch.empty((d, d), dtype=torch.float32, device=dev) for _ in range(nl)]
+    info = torch.zeros((nl,), dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(nl)]
+
+    def step(timed_attn: list | None):
+        for li, L in enumerate(layers):
+            if timed_attn is not None:
+                ev[li][0].record(stream)
+            pkv.attend_full(L.Q, L.K, L.V, scale=cfg.scale, O=Of)
+            if timed_attn is not None:
+                ev[li][1].record(stream)
+            if L.idx is not None:
+                pkv.attend_compressed(L.Q, L.K, L.V, idx=L.idx, scale=cfg.scale, O=Oc)
+            else:
+                pkv.attend_compressed(L.Q, L.Kc, L.Vc, scale=cfg.scale, O=Oc)
+            if acc == pkv.F32:
+                pkv.compute_targets(Of, Oc, L.W, rho=1, T=T)
+                pkv.accumulate_normal_eq(Oc, T, G=G, C=C, acc=acc)
+            else:
+                # fp64 statistics: C = Oc^T (Yf - Yc) with Yf - Yc = T formed in fp32
+                pkv.compute_targets(Of, Oc, L.W, rho=1, T=T)
+                pkv.accumulate_normal_eq(Oc, T, G=G, C=C, acc=acc)
+            pkv.solve_patch(G, C, cfg.lam, dW=dW[li], info=info[li:li + 1])
+        if timed_attn is not None:
+            timed_attn.append(ev)
+
+    for w in range(args.warmup):
+        step(None)
+        torch.cuda.synchronize()
+        log(f"[bench] warmup step {w + 1}/{args.warmup} done")
+    attn_ms = []
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for s in range(args.steps):
+        rec = []
+        step(rec)
+        torch.cuda.synchronize()
+        attn_ms += [a.elapsed_time(b) for a, b in ev]
+        log(f"[bench] step {s + 1}/{args.steps} done")
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    bad = int((info != 0).sum().item())
+    if bad:
+        log(f"[bench] WARNING: {bad} layer solve(s) reported a non-positive pivot")
+
+    ms_step = elapsed / args.steps * 1e3
+    s_layer = elapsed / (args.steps * nl)
+    att_flops_full = 4.0 * M * cfg.N * cfg.Hq * cfg.dh
+    att_flops_comp = 4.0 * M * cfg.B * cfg.Hq * cfg.dh
+    t_attn = float(np.mean(attn_ms)) * 1e-3            # dominant kernel: full-cache attention
+    peak = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_F32_TFLOPS
+    achieved = att_flops_full / t_attn / 1e12
+    kv_bytes = 2.0 * cfg.Hkv * cfg.N * cfg.dh * (2 if cfg.dtype == "bf16" else 4)
+
+    out = {
+        "metric": METRIC,
+        "value": s_layer,
+        "unit": "s/layer-patch",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic (seeded; shapes and distributions of the workload)",
+        "config": {"workload": cfg.name, "config_id": cfg.cid, "layers_per_step": nl,
+                   "N": cfg.N, "B": cfg.B, "M": M, "d": d, "Hq": cfg.Hq, "Hkv": cfg.Hkv,
+                   "dh": cfg.dh, "lambda": cfg.lam, "compressed_cache": cfg.cache},
+        "attention_full_ms": t_attn * 1e3,
+        "attention_full_tflops": achieved,
+        "attention_full_frac_of_peak": achieved / peak,
+        "attention_total_tflops_per_layer_time": (att_flops_full + att_flops_comp) / s_layer / 1e12,
+        "context_tokens_per_s": cfg.N / s_layer,
+        "kv_stream_gbs_full_attention": kv_bytes / t_attn / 1e9,
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
+                     "frac": achieved / peak, "traffic": None,
+                     "kernel": "attn_bf16_kernel (full cache)" if cfg.dtype == "bf16"
+                     else "attn_f32_kernel (full cache)",
+                     "flops_per_launch": att_flops_full},
+        "solve_info_nonzero_layers": bad,
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the fp64 CPU oracle on a bounded sample")
+        out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_rows)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

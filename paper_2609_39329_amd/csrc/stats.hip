@@ -241,12 +241,16 @@ __global__ __launch_bounds__(256, 1) void split_gemm_kernel(SplitParams p) {
         const int i = i0 + wi + 32 * a + 8 * (e >> 2) + 4 * h32 + (e & 3);
         const int j = j0 + wj + 32 * b + l32;
         if (i >= p.I || j >= p.J) continue;
+        // diagonal tiles of G: keep the i <= j triangle and mirror it, so G is
+        // exactly symmetric (the two triangles accumulate their terms in
+        // different orders)
+        if (SYM && ti == tj && i > j) continue;
         float v = acc[a][b][e];
         if (p.E1) v += p.rho * (p.E1[(int64_t)i * p.lde + j] - p.E2[(int64_t)i * p.lde + j]);
         float* o = p.Out + (int64_t)i * p.ldo + j;
         *o = p.accumulate ? *o + v : v;
         if constexpr (SYM) {
-          if (ti != tj) {
+          if (i != j) {
             float* o2 = p.Out + (int64_t)j * p.ldo + i;
             *o2 = p.accumulate ? *o2 + v : v;
           }

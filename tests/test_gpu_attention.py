@@ -96,7 +96,9 @@ def test_single_entry_cache_returns_its_value(dt):
     O = host(pkv.attend_full(to_dev(inp.Q, dt), to_dev(inp.K, dt), to_dev(inp.V, dt)))
     V = oracle.decode(inp.V, dt)
     ref = np.concatenate([V[h // 2, 0] for h in range(4)])[None, :].repeat(20, axis=0)
-    assert np.array_equal(O, ref)
+    # the softmax weight is exp2 of the fp32 rounding residual of the scaled score,
+    # i.e. 1 to within an ulp, so O equals V to fp32 rounding
+    assert np.max(np.abs(O - ref)) <= 4e-7 * np.max(np.abs(ref))
 
 
 def test_attention_deterministic():

@@ -6,7 +6,8 @@ Tolerances (relative Frobenius error):
   5e-5.
 * fp64 accumulation path: fp64 products of fp32 inputs: 1e-12.
 * solve, fp32: Cholesky + triangular solves in fp32 on a system with condition
-  number ~1e2-1e3: error ~ kappa * 1e-7, bound 1e-4. fp64: 1e-10.
+  number ~1e2-1e3: error ~ kappa * 1e-7, bound 1e-4. fp64: the solve is fp64 but
+  dW is returned in fp32, whose rounding alone is ~3e-8 RMS; bound 1e-7.
 """
 import numpy as np
 import pytest
@@ -103,7 +104,7 @@ def test_solve(d, dout, rows, acc, lam):
     Gin = G if acc == "f64" else G.astype(np.float32).astype(np.float64)
     Cin = C if acc == "f64" else C.astype(np.float32).astype(np.float64)
     ref = oracle.solve_patch(Gin, Cin, lam)
-    assert rel(host(dW), ref) <= (1e-10 if acc == "f64" else 1e-4)
+    assert rel(host(dW), ref) <= (1e-7 if acc == "f64" else 1e-4)
 
 
 @pytest.mark.parametrize("acc", ["f32", "f64"])
@@ -115,7 +116,7 @@ def test_solve_adaptive_ridge(acc):
     Gin = G if acc == "f64" else G.astype(np.float32).astype(np.float64)
     Cin = C if acc == "f64" else C.astype(np.float32).astype(np.float64)
     lam = oracle.ridge_lambda(Gin, 0.01, "adaptive")
-    assert rel(host(dW), oracle.solve_patch(Gin, Cin, lam)) <= (1e-10 if acc == "f64" else 1e-4)
+    assert rel(host(dW), oracle.solve_patch(Gin, Cin, lam)) <= (1e-7 if acc == "f64" else 1e-4)
 
 
 @pytest.mark.parametrize("acc", ["f32", "f64"])
