@@ -69,6 +69,41 @@ class LayerDev:
         self.Vc = t(inp.Vc) if inp.Vc is not None else None
 
 
+class Buffers:
+    """Per-step device buffers shared by all layers (the stream orders their reuse)."""
+
+    def __init__(self, cfg, torch, dev, nl: int):
+        self.acc = 1 if cfg.dtype == "bf16" else 2  # F32 statistics for bf16 inputs, F64 for fp32
+        adt = torch.float64 if self.acc == 2 else torch.float32
+        M, d = cfg.M, cfg.d
+        self.Of = torch.empty((M, d), dtype=torch.float32, device=dev)
+        self.Oc = torch.empty((M, d), dtype=torch.float32, device=dev)
+        self.T = torch.empty((M, d), dtype=torch.float32, device=dev)
+        self.G = torch.empty((d, d), dtype=adt, device=dev)
+        self.C = torch.empty((d, d), dtype=adt, device=dev)
+        self.dW = [torch.empty((d, d), dtype=torch.float32, device=dev) for _ in range(nl)]
+        self.info = torch.zeros((nl,), dtype=torch.int32, device=dev)
+
+
+def layer_steps(pkv, cfg, L, bufs, li: int, events=None):
+    """One layer patch through the five library calls, in the order
+    patchkv_compute_layer_patch makes them; ``events`` = (start, end) CUDA events
+    recorded around the full-cache attention on the current stream."""
+    acc = pkv.F32 if bufs.acc == 1 else pkv.F64
+    if events is not None:
+        events[0].record()
+    pkv.attend_full(L.Q, L.K, L.V, scale=cfg.scale, O=bufs.Of)
+    if events is not None:
+        events[1].record()
+    if L.idx is not None:
+        pkv.attend_compressed(L.Q, L.K, L.V, idx=L.idx, scale=cfg.scale, O=bufs.Oc)
+    else:
+        pkv.attend_compressed(L.Q, L.Kc, L.Vc, scale=cfg.scale, O=bufs.Oc)
+    pkv.compute_targets(bufs.Of, bufs.Oc, L.W, rho=1, T=bufs.T)
+    pkv.accumulate_normal_eq(bufs.Oc, bufs.T, G=bufs.G, C=bufs.C, acc=acc)
+    pkv.solve_patch(bufs.G, bufs.C, cfg.lam, dW=bufs.dW[li], info=bufs.info[li:li + 1])
+
+
 def cpu_baseline(cfg, rows: int) -> dict:
     """The fp64 oracle on a bounded sample of one layer, scaled to s / layer patch.
 
@@ -130,9 +165,6 @@ def main():
     nl = cfg.layers if args.layers is None else min(args.layers, cfg.layers)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    dt_code = pkv.BF16 if cfg.dtype == "bf16" else pkv.F32
-    acc = pkv.F64 if cfg.dtype == "f32" else pkv.F32
-    adt = torch.float64 if acc == pkv.F64 else torch.float32
 
     t0 = time.perf_counter()
     layers = []
@@ -143,55 +175,30 @@ def main():
     torch.cuda.synchronize()
 
     M, d = cfg.M, cfg.d
-    Of = torch.empty((M, d), dtype=torch.float32, device=dev)
-    Oc = torch.empty((M, d), dtype=torch.float32, device=dev)
-    T = torch.empty((M, d), dtype=torch.float32, device=dev)
-    G = torch.empty((d, d), dtype=adt, device=dev)
-    C = torch.empty((d, d), dtype=adt, device=dev)
-    dW = [torch.empty((d, d), dtype=torch.float32, device=dev) for _ in range(nl)]
-    info = torch.zeros((nl,), dtype=torch.int32, device=dev)
-    stream = torch.cuda.current_stream()
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(nl)]
 
-    def step(timed_attn: list | None):
+    bufs = Buffers(cfg, torch, dev, nl)
+
+    def step(timed: bool):
         for li, L in enumerate(layers):
-            if timed_attn is not None:
-                ev[li][0].record(stream)
-            pkv.attend_full(L.Q, L.K, L.V, scale=cfg.scale, O=Of)
-            if timed_attn is not None:
-                ev[li][1].record(stream)
-            if L.idx is not None:
-                pkv.attend_compressed(L.Q, L.K, L.V, idx=L.idx, scale=cfg.scale, O=Oc)
-            else:
-                pkv.attend_compressed(L.Q, L.Kc, L.Vc, scale=cfg.scale, O=Oc)
-            if acc == pkv.F32:
-                pkv.compute_targets(Of, Oc, L.W, rho=1, T=T)
-                pkv.accumulate_normal_eq(Oc, T, G=G, C=C, acc=acc)
-            else:
-                # fp64 statistics: C = Oc^T (Yf - Yc) with Yf - Yc = T formed in fp32
-                pkv.compute_targets(Of, Oc, L.W, rho=1, T=T)
-                pkv.accumulate_normal_eq(Oc, T, G=G, C=C, acc=acc)
-            pkv.solve_patch(G, C, cfg.lam, dW=dW[li], info=info[li:li + 1])
-        if timed_attn is not None:
-            timed_attn.append(ev)
+            layer_steps(pkv, cfg, L, bufs, li, ev[li] if timed else None)
 
     for w in range(args.warmup):
-        step(None)
+        step(False)
         torch.cuda.synchronize()
         log(f"[bench] warmup step {w + 1}/{args.warmup} done")
     attn_ms = []
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for s in range(args.steps):
-        rec = []
-        step(rec)
+        step(True)
         torch.cuda.synchronize()
         attn_ms += [a.elapsed_time(b) for a, b in ev]
         log(f"[bench] step {s + 1}/{args.steps} done")
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
-    bad = int((info != 0).sum().item())
+    bad = int((bufs.info != 0).sum().item())
     if bad:
         log(f"[bench] WARNING: {bad} layer solve(s) reported a non-positive pivot")
 

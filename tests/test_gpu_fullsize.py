@@ -1,0 +1,83 @@
+"""Parity at the workloads' full sizes, in the launch sequence bench.py times.
+
+For every stored oracle fixture (written by tests/golden/make_oracle_fixtures.py
+from the fp64 oracle alone) the patch dW of the GPU path is compared on
+  * 8 sampled rows, element by element (relative Frobenius error of those rows),
+  * a seeded random sketch dW @ R (tracks the relative error of the whole matrix),
+  * ||dW||_F,
+each against the 2e-2 bar for bf16 inputs. Attention outputs are compared on
+sampled query rows that the oracle computes one by one. The single-call entry
+point patchkv_compute_layer_patch must reproduce the step-by-step result bitwise.
+"""
+import glob
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_39329_amd as pkv
+from gpu_util import DEV, host, rel
+from workloads import CONFIGS, make_layer_inputs
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+from bench import Buffers, LayerDev, layer_steps  # noqa: E402
+
+sys.path.insert(0, os.path.join(ROOT, "tests", "golden"))
+from make_oracle_fixtures import fixture_path, sample_rows, sketch_matrix  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+CASES = [(1, 0), (2, 0), (4, 0), (3, 0), (3, 8), (3, 16), (3, 24), (3, 31)]
+TOL = 2e-2
+
+
+@pytest.mark.parametrize("cid,layer", CASES, ids=[f"c{c}-l{l}" for c, l in CASES])
+def test_full_size_layer_patch(cid, layer):
+    path = fixture_path(cid, layer)
+    if not os.path.exists(path):
+        pytest.skip(f"oracle fixture {os.path.basename(path)} not generated")
+    cfg = CONFIGS[cid]
+    print(f"full-size parity: config {cid} ({cfg.name}) layer {layer}", flush=True)
+    fx = np.load(path)
+    inp = make_layer_inputs(cfg, layer)
+    L = LayerDev(inp, torch, DEV)
+    bufs = Buffers(cfg, torch, DEV, 1)
+    layer_steps(pkv, cfg, L, bufs, 0)
+    torch.cuda.synchronize()
+    assert int(bufs.info[0].item()) == 0
+    dW = host(bufs.dW[0])
+
+    rows = sample_rows(cid, layer, cfg.d)
+    assert np.array_equal(rows, fx["rows"])
+    e_rows = rel(dW[rows], fx["dW_rows"])
+    e_sk = rel(dW @ sketch_matrix(cid, layer, cfg.d), fx["sketch"])
+    e_norm = abs(np.linalg.norm(dW) - float(fx["norm"])) / float(fx["norm"])
+    print(f"  rows {e_rows:.3e}  sketch {e_sk:.3e}  norm {e_norm:.3e}", flush=True)
+    assert e_rows <= TOL and e_sk <= TOL and e_norm <= TOL
+
+    # attention outputs on sampled query rows, computed by the oracle row by row
+    q_rows = np.random.default_rng([cid, layer, 7]).choice(cfg.M, 3, replace=False)
+    dt = inp.dtype
+    Q = oracle.decode(inp.Q[q_rows], dt)
+    K, V = oracle.decode(inp.K, dt), oracle.decode(inp.V, dt)
+    ref_f = oracle.attention(Q, K, V, inp.scale)
+    if inp.idx is not None:
+        Kc, Vc = oracle.gather_cache(K, V, inp.idx)
+    else:
+        Kc, Vc = oracle.decode(inp.Kc, dt), oracle.decode(inp.Vc, dt)
+    ref_c = oracle.attention(Q, Kc, Vc, inp.scale)
+    e_of = rel(host(bufs.Of)[q_rows], ref_f)
+    e_oc = rel(host(bufs.Oc)[q_rows], ref_c)
+    print(f"  O_f rows {e_of:.3e}  O_c rows {e_oc:.3e}", flush=True)
+    assert e_of <= 4e-3 and e_oc <= 5e-5
+
+    # the single-call entry point runs the same kernels in the same order
+    dW2, info2 = pkv.compute_layer_patch(L.Q, L.K, L.V, L.W, idx=L.idx, Kc=L.Kc, Vc=L.Vc,
+                                         lam=cfg.lam, scale=cfg.scale)
+    torch.cuda.synchronize()
+    assert int(info2.item()) == 0
+    assert torch.equal(dW2, bufs.dW[0])
