@@ -23,6 +23,9 @@ SOURCES = ["attention.hip", "stats.hip", "solve.hip", "capi.cpp"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function"]
 DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# Per-source extras. The attention kernels never see NaNs (masked scores are -inf),
+# so they run with the IEEE mode bit off, which lets max() skip NaN quieting.
+EXTRA = {"attention.hip": ["-mno-amdgpu-ieee", "-fno-honor-nans"]}
 
 
 def hipcc() -> str:
@@ -37,6 +40,7 @@ def _compile(src: str) -> str:
     cmd = [hipcc(), *COMMON]
     if src.endswith(".hip"):
         cmd += DEVICE
+    cmd += EXTRA.get(src, [])
     cmd += ["-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:

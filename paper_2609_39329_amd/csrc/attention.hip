@@ -24,6 +24,8 @@
 // attn_combine_kernel then merges the partial (O, m, l) triples.
 #include <math.h>
 
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -31,8 +33,9 @@ namespace pkv {
 
 namespace {
 
-constexpr float kTau = 8.0f;  // lazy-rescale threshold (log2 units)
-constexpr int kKeyTile = 64;  // keys per iteration, bf16 path
+constexpr float kTau = 8.0f;   // lazy-rescale threshold of the fixup path (log2 units)
+constexpr float kBig = 64.0f;  // headroom of the fixed offset in the fast path (log2 units)
+constexpr int kKeyTile = 32;  // keys per iteration, bf16 path
 constexpr int kRowsWG = 256;  // query rows per workgroup (both paths)
 constexpr int kKeyTileF32 = 32;
 
@@ -44,6 +47,7 @@ struct AttnParams {
   float* O;
   float* Opart;
   float* ML;
+  int* flags;  // bf16 path: per work item, 1 = the fast path left it to the fixup
   int Hq, G;
   int64_t src_rows;
   int src_valid;
@@ -55,24 +59,38 @@ struct AttnParams {
   float c;  // bf16: scale * log2(e); f32: scale
 };
 
-template <int DH, bool GATHER, bool PSPLIT, bool PARTIAL>
+// SAFE = false (fast path): each row's exponent offset is fixed to the exact max of
+// its first key tile, so O is never rescaled and only MFMA touches it. A later tile
+// may exceed that offset by up to 2^kBig (P, l and O stay far from fp32 overflow);
+// if any row of the workgroup exceeds it, the work item is marked in p.flags (its
+// outputs are then not trusted). SAFE = true (fixup, launched right after on the
+// same stream): the lazy-rescale online softmax, run only for marked work items,
+// overwriting their outputs.
+template <int DH, bool GATHER, bool PSPLIT, bool PARTIAL, bool SAFE>
 __global__ __launch_bounds__(256, 1) void attn_bf16_kernel(AttnParams p) {
   constexpr int KT = kKeyTile;
+  constexpr int NKT = KT / 32;  // 32-key MFMA tiles per iteration
   constexpr int KP = DH + 8;   // K tile pitch (elements): conflict-free 16-byte row reads
   constexpr int VP = DH + 16;  // V tile pitch: transposing reads hit distinct banks
   constexpr int NS = DH / 16;  // MFMA k-steps over head_dim
   constexpr int ND = DH / 32;  // 32-wide head_dim tiles of O
   constexpr int CH = DH / 8;   // 16-byte chunks per K/V row
   constexpr int LPT = KT * CH / 256;
-  __shared__ __attribute__((aligned(16))) __bf16 Ks[2][KT * KP];
-  __shared__ __attribute__((aligned(16))) __bf16 Vs[2][KT * VP];
+  __shared__ __attribute__((aligned(16))) __bf16 Ks[4][KT * KP];
+  __shared__ __attribute__((aligned(16))) __bf16 Vs[4][KT * VP];
+  __shared__ int overflow;
 
-  const int w = xcd_item(p.per_xcd);
+  // work-item coordinates are workgroup-uniform; readfirstlane keeps them (and the
+  // buffer descriptors and offsets built from them) in scalar registers
+  const int w = __builtin_amdgcn_readfirstlane(xcd_item(p.per_xcd));
   if (w >= p.total_items) return;
-  const int rt = w % p.row_tiles;
-  const int t2 = w / p.row_tiles;
-  const int split = t2 % p.n_split;
-  const int g = t2 / p.n_split;
+  if constexpr (SAFE) {
+    if (p.flags[w] == 0) return;
+  }
+  const int rt = __builtin_amdgcn_readfirstlane(w % p.row_tiles);
+  const int t2 = __builtin_amdgcn_readfirstlane(w / p.row_tiles);
+  const int split = __builtin_amdgcn_readfirstlane(t2 % p.n_split);
+  const int g = __builtin_amdgcn_readfirstlane(t2 / p.n_split);
   const int k_begin = split * p.keys_per_split;
   const int k_end = min(p.Nk, k_begin + p.keys_per_split);
   const int ntiles = (k_end - k_begin + KT - 1) / KT;
@@ -95,28 +113,47 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_kernel(AttnParams p) {
     for (int s = 0; s < NS; ++s) qf[qt][s] = load_bf16x8(qp + s * 16);
   }
 
-  u32x4 kreg[LPT], vreg[LPT];
-  auto load_tile = [&](int tile) {
+  // K/V are read with buffer loads: the per-tile offset is a scalar, and rows past
+  // the end of this KV head's buffer read as zeros (such keys are masked anyway).
+  // Two register staging sets: a tile's loads are issued one step before its LDS
+  // store, so their latency hides behind a whole step of MFMA work.
+  const uint32_t head_bytes = (uint32_t)(p.src_rows * DH * 2);
+  const __amdgpu_buffer_rsrc_t krs =
+      __builtin_amdgcn_make_buffer_rsrc((void*)Kb, 0, head_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t vrs =
+      __builtin_amdgcn_make_buffer_rsrc((void*)Vb, 0, head_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t irs =
+      __builtin_amdgcn_make_buffer_rsrc((void*)p.idx, 0, (uint32_t)(p.Nk * 4), 0x00020000);
+  u32x4 kreg[2][LPT], vreg[2][LPT];
+  auto load_tile_to = [&](int tile, int set) {
     const int kb0 = k_begin + tile * KT;
 #pragma unroll
     for (int i = 0; i < LPT; ++i) {
-      const int c = i * 256 + tid;
-      const int row = c / CH, col = c % CH;
-      int src = min(kb0 + row, k_end - 1);
-      if constexpr (GATHER) src = min(max(p.idx[src], 0), p.src_valid - 1);
-      kreg[i] = *(const u32x4*)(Kb + (int64_t)src * DH + col * 8);
-      vreg[i] = *(const u32x4*)(Vb + (int64_t)src * DH + col * 8);
+      const int c = i * 256 + tid;  // 16-byte chunk: row c / CH, column c % CH
+      if constexpr (GATHER) {
+        // entries past the index array read as 0; rows outside the cache read as 0
+        const int src = (int)__builtin_amdgcn_raw_buffer_load_b32(irs, (kb0 + c / CH) * 4, 0, 0);
+        const uint32_t off = (uint32_t)src * (DH * 2) + (c % CH) * 16;
+        kreg[set][i] = __builtin_amdgcn_raw_buffer_load_b128(krs, off, 0, 0);
+        vreg[set][i] = __builtin_amdgcn_raw_buffer_load_b128(vrs, off, 0, 0);
+      } else {
+        const uint32_t soff = (uint32_t)kb0 * (DH * 2);
+        kreg[set][i] = __builtin_amdgcn_raw_buffer_load_b128(krs, c * 16, soff, 0);
+        vreg[set][i] = __builtin_amdgcn_raw_buffer_load_b128(vrs, c * 16, soff, 0);
+      }
     }
   };
-  auto store_tile = [&](int buf) {
+  auto store_tile_from = [&](int buf, int set) {
 #pragma unroll
     for (int i = 0; i < LPT; ++i) {
       const int c = i * 256 + tid;
       const int row = c / CH, col = c % CH;
-      *(u32x4*)(&Ks[buf][row * KP + col * 8]) = kreg[i];
-      *(u32x4*)(&Vs[buf][row * VP + col * 8]) = vreg[i];
+      *(u32x4*)(&Ks[buf][row * KP + col * 8]) = kreg[set][i];
+      *(u32x4*)(&Vs[buf][row * VP + col * 8]) = vreg[set][i];
     }
   };
+  auto load_tile = [&](int tile) { load_tile_to(tile, 0); };
+  auto store_tile = [&](int buf) { store_tile_from(buf, 0); };
 
   f32x16 o[2][ND];
 #pragma unroll
@@ -131,35 +168,29 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_kernel(AttnParams p) {
   const int tr_row = 4 * h32 + ((lane & 15) >> 2);
   const int tr_col = ((lane >> 4) & 1) * 16 + 4 * (lane & 3);
 
-  load_tile(0);
-  store_tile(0);
-  __syncthreads();
-
-  for (int t = 0; t < ntiles; ++t) {
-    const int cur = t & 1;
-    if (t + 1 < ntiles) load_tile(t + 1);
-    const __bf16* ks = Ks[cur];
-    const __bf16* vs = Vs[cur];
-
-    f32x16 s[2][2];
+  // S^T = K Q^T (+ init) for the tile in LDS slot `buf`
+  auto scores_init = [&](f32x16 (&s)[NKT][2], int buf, const f32x16 (&init)[NKT]) {
+    const __bf16* ks = Ks[buf];
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
+    for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
-      for (int qt = 0; qt < 2; ++qt) s[kt][qt] = f32x16{};
+      for (int qt = 0; qt < 2; ++qt) s[kt][qt] = init[kt];
 #pragma unroll
     for (int st = 0; st < NS; ++st) {
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
+      for (int kt = 0; kt < NKT; ++kt) {
         const bf16x8 a = *(const bf16x8*)(ks + (kt * 32 + l32) * KP + st * 16 + h32 * 8);
 #pragma unroll
         for (int qt = 0; qt < 2; ++qt) s[kt][qt] = mfma32(a, qf[qt][st], s[kt][qt]);
       }
     }
-
+  };
+  // keys >= k_end of tile t set to -inf
+  auto mask = [&](f32x16 (&s)[NKT][2], int t) {
     const int tb = k_begin + t * KT;
     if (tb + KT > k_end) {
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
+      for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int key = tb + kt * 32 + 8 * (e >> 2) + 4 * h32 + (e & 3);
@@ -169,59 +200,64 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_kernel(AttnParams p) {
           }
         }
     }
-
-    float mt[2];
-    bool need = false;
+  };
+  auto scores = [&](f32x16 (&s)[NKT][2], int buf, int t) {
+    f32x16 zero[NKT];
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt) zero[kt] = f32x16{};
+    scores_init(s, buf, zero);
+    mask(s, t);
+  };
+  // scaled row max of the tile (both halves of the 64-lane wave)
+  auto row_max = [&](f32x16 (&s)[NKT][2], float (&mt)[2]) {
 #pragma unroll
     for (int qt = 0; qt < 2; ++qt) {
       float mx = s[0][qt][0];
 #pragma unroll
       for (int e = 1; e < 16; ++e) mx = fmaxf(mx, s[0][qt][e]);
 #pragma unroll
-      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[1][qt][e]);
+      for (int kt = 1; kt < NKT; ++kt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[kt][qt][e]);
       mt[qt] = pair_max(mx) * c;
-      need |= mt[qt] > m_run[qt] + kTau;
     }
-    if (__ballot(need) != 0) {
+  };
+  // P = exp2(S c - m_run) as bf16 MFMA operands (two-term split when PSPLIT). The row
+  // sums add up the bf16 values the MFMA actually uses (v_dot2 with (1, 1)).
+  auto softmax = [&](f32x16 (&s)[NKT][2], bf16x8 (&pb)[NKT][2][2], bf16x8 (&pl)[NKT][2][2]) {
+    const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 #pragma unroll
-      for (int qt = 0; qt < 2; ++qt) {
-        const float mn = fmaxf(m_run[qt], mt[qt]);
-        const float alpha = fast_exp2(m_run[qt] - mn);
-        m_run[qt] = mn;
-        l_part[qt] *= alpha;
-#pragma unroll
-        for (int dt = 0; dt < ND; ++dt) o[qt][dt] *= alpha;
-      }
-    }
-
-    bf16x8 pb[2][2][2];
-    bf16x8 pl[2][2][2];
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
+    for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
       for (int qt = 0; qt < 2; ++qt) {
         const float nm = -m_run[qt];
-        float sum = 0.f;
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const float pv = fast_exp2(fmaf(s[kt][qt][e], c, nm));
-          s[kt][qt][e] = pv;
-          sum += pv;
-        }
-        l_part[qt] += sum;
+        for (int e = 0; e < 16; ++e) s[kt][qt][e] = fast_exp2(fmaf(s[kt][qt][e], c, nm));
+        float sum0 = 0.f, sum1 = 0.f;
 #pragma unroll
         for (int p2 = 0; p2 < 2; ++p2)
 #pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const float pv = s[kt][qt][8 * p2 + e];
-            const __bf16 hi = to_bf16(pv);
-            pb[kt][qt][p2][e] = hi;
-            if constexpr (PSPLIT) pl[kt][qt][p2][e] = to_bf16(pv - (float)hi);
+          for (int e = 0; e < 8; e += 2) {
+            const float v0 = s[kt][qt][8 * p2 + e], v1 = s[kt][qt][8 * p2 + e + 1];
+            const bf16x2 h = {to_bf16(v0), to_bf16(v1)};
+            pb[kt][qt][p2][e] = h[0];
+            pb[kt][qt][p2][e + 1] = h[1];
+            sum0 = __builtin_amdgcn_fdot2_f32_bf16(h, ones, sum0, false);
+            if constexpr (PSPLIT) {
+              const bf16x2 lo = {to_bf16(v0 - (float)h[0]), to_bf16(v1 - (float)h[1])};
+              pl[kt][qt][p2][e] = lo[0];
+              pl[kt][qt][p2][e + 1] = lo[1];
+              sum1 = __builtin_amdgcn_fdot2_f32_bf16(lo, ones, sum1, false);
+            }
           }
+        l_part[qt] += sum0 + sum1;
       }
-
+  };
+  // O^T += V^T P^T with V of LDS slot `buf`
+  auto pv = [&](bf16x8 (&pb)[NKT][2][2], bf16x8 (&pl)[NKT][2][2], int buf) {
+    const __bf16* vs = Vs[buf];
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
+    for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
       for (int p2 = 0; p2 < 2; ++p2) {
         const __bf16* vrow = vs + (kt * 32 + 16 * p2 + tr_row) * VP + tr_col;
@@ -236,9 +272,89 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_kernel(AttnParams p) {
           }
         }
       }
+  };
+  auto accumulate = [&](f32x16 (&s)[NKT][2], int buf) {
+    bf16x8 pb[NKT][2][2];
+    bf16x8 pl[NKT][2][2];
+    softmax(s, pb, pl);
+    pv(pb, pl, buf);
+  };
 
-    if (t + 1 < ntiles) store_tile(cur ^ 1);
+  if (tid == 0) overflow = 0;
+  load_tile_to(0, 0);
+  store_tile_from(0, 0);
+
+  if constexpr (!SAFE) {
+    // Software pipeline over four LDS slots (tile t in slot t % 4). Step t:
+    //   issue the loads of tile t+3 (register set (t+1) % 2);
+    //   MFMA S_{t+1} = K_{t+1} Q^T  while the VALU forms P_t from S_t;
+    //   MFMA O += V_t P_t           while the VALU takes S_{t+1}'s row max;
+    //   store tile t+2 (loaded in step t-1) into its slot, last read in step t-2;
+    //   one barrier.
+    // The loop runs an even number of steps; tiles past the key range are fully
+    // masked (they contribute nothing), so every step has the same shape.
+    load_tile_to(1, 0);
+    store_tile_from(1, 0);
+    load_tile_to(2, 0);
     __syncthreads();
+    f32x16 sa[NKT][2], sb[NKT][2];
+    scores(sa, 0, 0);
+    {
+      float mt[2];
+      row_max(sa, mt);
+      m_run[0] = mt[0];
+      m_run[1] = mt[1];
+    }
+    bool over = false;
+    auto step = [&](auto set_t, f32x16 (&sc)[NKT][2], f32x16 (&sn)[NKT][2], int t) {
+      constexpr int set_ld = decltype(set_t)::value;
+      load_tile_to(t + 3, set_ld);
+      scores(sn, (t + 1) & 3, t + 1);
+      bf16x8 pb[NKT][2][2];
+      bf16x8 pl[NKT][2][2];
+      softmax(sc, pb, pl);
+      pv(pb, pl, t & 3);
+      float mt[2];
+      row_max(sn, mt);
+      over |= mt[0] > m_run[0] + kBig || mt[1] > m_run[1] + kBig;
+      store_tile_from((t + 2) & 3, set_ld ^ 1);
+      __syncthreads();
+    };
+    using S0 = std::integral_constant<int, 0>;
+    using S1 = std::integral_constant<int, 1>;
+    for (int t = 0; t < ntiles; t += 2) {
+      step(S1{}, sa, sb, t);
+      step(S0{}, sb, sa, t + 1);
+    }
+    if (__ballot(over) != 0) overflow = 1;
+    __syncthreads();
+  } else {
+    // lazy rescale: when a row's running max would grow by more than 2^kTau the
+    // wave rescales O first (m_run = -inf on the first tile: alpha = 0)
+    __syncthreads();
+    for (int t = 0; t < ntiles; ++t) {
+      const int cur = t & 1;
+      if (t + 1 < ntiles) load_tile(t + 1);
+      f32x16 s[NKT][2];
+      scores(s, cur, t);
+      float mt[2];
+      row_max(s, mt);
+      const bool need = mt[0] > m_run[0] + kTau || mt[1] > m_run[1] + kTau;
+      if (__ballot(need) != 0) {
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt) {
+          const float mn = fmaxf(m_run[qt], mt[qt]);
+          const float alpha = fast_exp2(m_run[qt] - mn);
+          m_run[qt] = mn;
+          l_part[qt] *= alpha;
+#pragma unroll
+          for (int dt = 0; dt < ND; ++dt) o[qt][dt] *= alpha;
+        }
+      }
+      accumulate(s, cur);
+      if (t + 1 < ntiles) store_tile(cur ^ 1);
+      __syncthreads();
+    }
   }
 
 #pragma unroll
@@ -274,6 +390,9 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_kernel(AttnParams p) {
         p.ML[2 * rid + 1] = l;
       }
     }
+  }
+  if constexpr (!SAFE) {
+    if (tid == 0) p.flags[w] = overflow;
   }
 }
 
@@ -403,8 +522,12 @@ hipError_t launch_dh(const AttnShape& s, const AttnPlan& pl, AttnParams& p, bool
   const bool part = pl.n_split > 1;
   dim3 grid(pl.grid), block(256);
   if (s.bf16) {
-#define PKV_L(G_, P_, S_) \
-  hipLaunchKernelGGL((attn_bf16_kernel<DH, G_, P_, S_>), grid, block, 0, st, p)
+    // fast path, then the lazy-rescale fixup for any work item it handed back
+#define PKV_L(G_, P_, S_)                                                               \
+  do {                                                                                  \
+    hipLaunchKernelGGL((attn_bf16_kernel<DH, G_, P_, S_, false>), grid, block, 0, st, p); \
+    hipLaunchKernelGGL((attn_bf16_kernel<DH, G_, P_, S_, true>), grid, block, 0, st, p);  \
+  } while (0)
     if (gather) {
       if (psplit) { if (part) PKV_L(true, true, true); else PKV_L(true, true, false); }
       else { if (part) PKV_L(true, false, true); else PKV_L(true, false, false); }
@@ -468,6 +591,7 @@ AttnPlan plan_attention(const AttnShape& s) {
                     ? align_up((size_t)s.Hkv * pl.n_split * rows * s.dh * sizeof(float)) +
                           align_up((size_t)s.Hkv * pl.n_split * rows * 2 * sizeof(float))
                     : 0;
+  if (s.bf16) pl.ws_bytes += align_up((size_t)pl.total_items * sizeof(int));
   return pl;
 }
 
@@ -481,11 +605,15 @@ hipError_t launch_attention(const AttnShape& s, const void* Q, const void* K, co
   p.V = V;
   p.idx = idx;
   p.O = O;
+  size_t off = 0;
   if (pl.n_split > 1) {
+    const size_t n = (size_t)s.Hkv * pl.n_split * s.M * (s.Hq / s.Hkv);
     p.Opart = (float*)ws;
-    p.ML = (float*)((char*)ws +
-                    align_up((size_t)s.Hkv * pl.n_split * s.M * (s.Hq / s.Hkv) * s.dh * sizeof(float)));
+    off += align_up(n * s.dh * sizeof(float));
+    p.ML = (float*)((char*)ws + off);
+    off += align_up(n * 2 * sizeof(float));
   }
+  if (s.bf16) p.flags = (int*)((char*)ws + off);
   p.Hq = s.Hq;
   p.G = s.Hq / s.Hkv;
   p.src_rows = src_rows;

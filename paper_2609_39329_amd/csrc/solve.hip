@@ -1,18 +1,18 @@
 // Ridge patch, Eq. 8 in row form: dW = (G + lambda I)^{-1} C.
 //
-// Right-looking blocked Cholesky with block size NB, fused with the forward
-// substitution of the right-hand side:
+// Right-looking blocked Cholesky with block size NB (128 for fp32, 64 for fp64),
+// fused with the forward substitution of the right-hand side:
 //   for each block column k:
-//     potrf_inv_kernel   A_kk = L_kk L_kk^T in LDS, then L_kk^{-1} in place (1 WG)
+//     potrf_inv_kernel   A_kk = L_kk L_kk^T and L_kk^{-1}, in registers (1 WG)
 //     grouped GEMM       L_ik = A_ik L_kk^{-T} (i > k);  Z_k = L_kk^{-1} R_k
 //     grouped GEMM       A_ij -= L_ik L_jk^T (lower blocks);  R_i -= L_ik Z_k (i > k)
 //   then backward:  X_k = L_kk^{-T} Z_k;  Z_i -= L_ki^T X_k (i < k), k descending.
 // Triangular solves against a diagonal block use that block's explicit inverse (a
 // GEMM instead of a substitution); its condition number is at most the square root
 // of that of G + lambda I.
-// fp32 (acc F32) GEMM tiles run on MFMA 32x32x2 f32; fp64 (acc F64) on fp64 FMA.
-// The adaptive ridge of Eq. 7, lambda_0 ||G||_F^2 / tr G, is reduced on the device
-// in fp64 in a fixed order (deterministic).
+// fp32 GEMM tiles run on MFMA 32x32x2 f32 (128 x 128 tiles, double-buffered LDS);
+// fp64 tiles on fp64 FMA. The adaptive ridge of Eq. 7, lambda_0 ||G||_F^2 / tr G,
+// is reduced on the device in fp64 in a fixed order (deterministic).
 #include <math.h>
 
 #include <algorithm>
@@ -24,9 +24,23 @@ namespace pkv {
 
 namespace {
 
-constexpr int NB = 128;      // Cholesky block size
-constexpr int GT = 64;       // GEMM tile
-constexpr int GK = 32;       // GEMM k chunk
+template <class T>
+struct Blk;
+template <>
+struct Blk<float> {
+  static constexpr int NB = 128, TS = 4;  // block size, register tile of the diagonal kernel
+};
+template <>
+struct Blk<double> {
+  static constexpr int NB = 64, TS = 4;
+};
+// threads of the diagonal kernel: one per TS x TS tile of the lower triangle
+template <class T>
+constexpr int diag_threads() {
+  constexpr int NT = Blk<T>::NB / Blk<T>::TS;
+  return (NT * (NT + 1) / 2 + 63) / 64 * 64;
+}
+
 constexpr int kRedBlocks = 256;
 
 template <class T>
@@ -42,153 +56,389 @@ struct GemmDesc {
   int lower;       // only tiles with tile_row >= tile_col
   int tiles_n;
   int ntiles;
+  int vecA, vecB;  // 16-byte loads along the contiguous dimension are allowed
 };
 
-template <class T>
-struct GemmGroup {
-  GemmDesc<T> d[2];
-  int n;
-};
+// ---- fp32: BM x BM output tile (128 or 64), 4 waves, MFMA 32x32x2 f32 ---------------
+constexpr int F_KC = 32;
 
-template <class T>
-__global__ __launch_bounds__(256) void solve_gemm_kernel(GemmGroup<T> grp) {
-  __shared__ T As[GK][GT + 4];
-  __shared__ T Bs[GK][GT + 4];
-  int t = blockIdx.x;
-  int which = 0;
-  if (t >= grp.d[0].ntiles) {
-    t -= grp.d[0].ntiles;
-    which = 1;
-    if (which >= grp.n || t >= grp.d[1].ntiles) return;
-  }
-  const GemmDesc<T>& g = grp.d[which];
+template <int BM>
+__device__ __forceinline__ void gemm_f32_body(const GemmDesc<float>& g, int t) {
+  constexpr int P = BM + 4;
+  constexpr int WT = BM / 64;                 // MFMA tiles per wave and dimension
+  constexpr int NU = BM * F_KC / 4 / 256;     // float4 per thread per operand and chunk
+  __shared__ float As[2][F_KC][P];
+  __shared__ float Bs[2][F_KC][P];
   const int ti = t / g.tiles_n, tj = t % g.tiles_n;
   if (g.lower && tj > ti) return;
-  const int i0 = ti * GT, j0 = tj * GT;
-  const int tid = threadIdx.x;
+  const int i0 = ti * BM, j0 = tj * BM;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int wi = (wid >> 1) * (BM / 2), wj = (wid & 1) * (BM / 2);
 
-  f32x16 acc32 = {};
-  double acc64[4][4] = {};
-  const int lane = tid & 63, wid = tid >> 6;
-  const int wi = (wid >> 1) * 32, wj = (wid & 1) * 32;
-  const int ty = tid / 16, tx = tid % 16;
+  f32x16 acc[WT][WT];
+#pragma unroll
+  for (int a = 0; a < WT; ++a)
+#pragma unroll
+    for (int b = 0; b < WT; ++b) acc[a][b] = f32x16{};
 
-  for (int k0 = 0; k0 < g.K; k0 += GK) {
-    for (int e = tid; e < GT * GK; e += 256) {
+  f32x4 ra[NU], rb[NU];
+  const bool a_k = g.sak == 1;  // A contiguous along k (else along i)
+  const bool b_j = g.sbj == 1;  // B contiguous along j (else along k)
+  auto fetch = [&](int k0) {
+#pragma unroll
+    for (int u = 0; u < NU; ++u) {
+      const int c = u * 256 + tid;
       int i, k;
-      if (g.sak == 1) { i = e / GK; k = e % GK; } else { k = e / GT; i = e % GT; }
+      if (a_k) { i = c / (F_KC / 4); k = (c % (F_KC / 4)) * 4; }
+      else { k = c / (BM / 4); i = (c % (BM / 4)) * 4; }
       const int gi = i0 + i, gk = k0 + k;
-      As[k][i] = (gi < g.M && gk < g.K) ? g.A[(int64_t)gi * g.sai + (int64_t)gk * g.sak] : T(0);
-      int j, kb;
-      if (g.sbj == 1) { kb = e / GT; j = e % GT; } else { j = e / GK; kb = e % GK; }
-      const int gj = j0 + j, gkb = k0 + kb;
-      Bs[kb][j] = (gj < g.N && gkb < g.K) ? g.B[(int64_t)gkb * g.sbk + (int64_t)gj * g.sbj] : T(0);
-    }
-    __syncthreads();
-    if constexpr (sizeof(T) == 4) {
-#pragma unroll
-      for (int kk = 0; kk < GK; kk += 2) {
-        const float a = As[kk + (lane >> 5)][wi + (lane & 31)];
-        const float b = Bs[kk + (lane >> 5)][wj + (lane & 31)];
-        acc32 = mfma32_f32(a, b, acc32);
-      }
-    } else {
-#pragma unroll 4
-      for (int kk = 0; kk < GK; ++kk) {
-        double a[4], b[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          a[u] = As[kk][ty * 4 + u];
-          b[u] = Bs[kk][tx * 4 + u];
+      f32x4 v = {};
+      if (a_k) {
+        if (gi < g.M) {
+          const float* s = g.A + (int64_t)gi * g.sai + gk;
+          if (g.vecA && gk + 3 < g.K) v = *(const f32x4*)s;
+          else
+            for (int e = 0; e < 4; ++e) v[e] = gk + e < g.K ? s[e] : 0.f;
         }
+      } else {
+        if (gk < g.K) {
+          const float* s = g.A + (int64_t)gk * g.sak + gi;
+          if (g.vecA && gi + 3 < g.M) v = *(const f32x4*)s;
+          else
+            for (int e = 0; e < 4; ++e) v[e] = gi + e < g.M ? s[(int64_t)e * g.sai] : 0.f;
+        }
+      }
+      ra[u] = v;
+      int j, kb;
+      if (b_j) { kb = c / (BM / 4); j = (c % (BM / 4)) * 4; }
+      else { j = c / (F_KC / 4); kb = (c % (F_KC / 4)) * 4; }
+      const int gj = j0 + j, gkb = k0 + kb;
+      f32x4 w = {};
+      if (b_j) {
+        if (gkb < g.K) {
+          const float* s = g.B + (int64_t)gkb * g.sbk + gj;
+          if (g.vecB && gj + 3 < g.N) w = *(const f32x4*)s;
+          else
+            for (int e = 0; e < 4; ++e) w[e] = gj + e < g.N ? s[(int64_t)e * g.sbj] : 0.f;
+        }
+      } else {
+        if (gj < g.N) {
+          const float* s = g.B + (int64_t)gj * g.sbj + gkb;
+          if (g.vecB && gkb + 3 < g.K) w = *(const f32x4*)s;
+          else
+            for (int e = 0; e < 4; ++e) w[e] = gkb + e < g.K ? s[(int64_t)e * g.sbk] : 0.f;
+        }
+      }
+      rb[u] = w;
+    }
+  };
+  auto stash = [&](int buf) {
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
+    for (int u = 0; u < NU; ++u) {
+      const int c = u * 256 + tid;
+      if (a_k) {
+        const int i = c / (F_KC / 4), k = (c % (F_KC / 4)) * 4;
 #pragma unroll
-          for (int v = 0; v < 4; ++v) acc64[u][v] = fma(a[u], b[v], acc64[u][v]);
+        for (int e = 0; e < 4; ++e) As[buf][k + e][i] = ra[u][e];
+      } else {
+        *(f32x4*)&As[buf][c / (BM / 4)][(c % (BM / 4)) * 4] = ra[u];
+      }
+      if (b_j) {
+        *(f32x4*)&Bs[buf][c / (BM / 4)][(c % (BM / 4)) * 4] = rb[u];
+      } else {
+        const int j = c / (F_KC / 4), k = (c % (F_KC / 4)) * 4;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) Bs[buf][k + e][j] = rb[u][e];
       }
     }
+  };
+
+  const int nk = (g.K + F_KC - 1) / F_KC;
+  fetch(0);
+  stash(0);
+  __syncthreads();
+  for (int kc = 0; kc < nk; ++kc) {
+    const int buf = kc & 1;
+    if (kc + 1 < nk) fetch((kc + 1) * F_KC);
+#pragma unroll
+    for (int ks = 0; ks < F_KC; ks += 2) {
+      float av[WT], bv[WT];
+#pragma unroll
+      for (int a = 0; a < WT; ++a) av[a] = As[buf][ks + (lane >> 5)][wi + 32 * a + (lane & 31)];
+#pragma unroll
+      for (int b = 0; b < WT; ++b) bv[b] = Bs[buf][ks + (lane >> 5)][wj + 32 * b + (lane & 31)];
+#pragma unroll
+      for (int a = 0; a < WT; ++a)
+#pragma unroll
+        for (int b = 0; b < WT; ++b) acc[a][b] = mfma32_f32(av[a], bv[b], acc[a][b]);
+    }
+    if (kc + 1 < nk) stash(buf ^ 1);
     __syncthreads();
   }
 
-  if constexpr (sizeof(T) == 4) {
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int i = i0 + wi + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-      const int j = j0 + wj + (lane & 31);
-      if (i < g.M && j < g.N) {
-        T* c = g.C + (int64_t)i * g.ldc + j;
-        const T v = g.alpha * (T)acc32[e];
-        *c = g.beta != T(0) ? g.beta * *c + v : v;
-      }
-    }
-  } else {
+  for (int a = 0; a < WT; ++a)
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
+    for (int b = 0; b < WT; ++b)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int i = i0 + ty * 4 + u, j = j0 + tx * 4 + v;
+      for (int e = 0; e < 16; ++e) {
+        const int i = i0 + wi + 32 * a + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+        const int j = j0 + wj + 32 * b + (lane & 31);
         if (i < g.M && j < g.N) {
-          T* c = g.C + (int64_t)i * g.ldc + j;
-          const T r = g.alpha * (T)acc64[u][v];
-          *c = g.beta != T(0) ? g.beta * *c + r : r;
+          float* c = g.C + (int64_t)i * g.ldc + j;
+          const float v = g.alpha * acc[a][b][e];
+          *c = g.beta != 0.f ? g.beta * *c + v : v;
         }
       }
-  }
 }
 
-// Factor the bs x bs diagonal block at (kb, kb) of A (lower) and replace it by the
-// inverse of its Cholesky factor (upper part of the block zeroed).
-template <class T>
-__global__ __launch_bounds__(512) void potrf_inv_kernel(T* A, int64_t lda, int kb, int bs,
-                                                        int32_t* info) {
-  constexpr int P = NB + 1;
-  __shared__ T L[NB * P];
-  __shared__ T colbuf[NB];
-  const int tid = threadIdx.x, nt = blockDim.x;
-  for (int e = tid; e < bs * bs; e += nt) {
-    const int i = e / bs, j = e % bs;
-    L[i * P + j] = j <= i ? A[(int64_t)(kb + i) * lda + kb + j] : T(0);
-  }
-  __syncthreads();
-  // right-looking unblocked Cholesky
-  for (int j = 0; j < bs; ++j) {
-    const T ajj = L[j * P + j];
-    const bool bad = !(ajj > T(0));
-    const T d = sqrt(ajj);
-    __syncthreads();
-    if (tid == 0) {
-      L[j * P + j] = d;
-      if (bad && *info == 0) *info = kb + j + 1;
+// ---- fp64: 64 x 64 output tile, fp64 FMA, 4 x 4 outputs per thread ----------------
+constexpr int D_T = 64, D_KC = 32;
+
+__device__ __forceinline__ void gemm_f64_body(const GemmDesc<double>& g, int t) {
+  __shared__ double As[D_KC][D_T + 1];
+  __shared__ double Bs[D_KC][D_T + 1];
+  const int ti = t / g.tiles_n, tj = t % g.tiles_n;
+  if (g.lower && tj > ti) return;
+  const int i0 = ti * D_T, j0 = tj * D_T;
+  const int tid = threadIdx.x, ty = tid / 16, tx = tid % 16;
+  double acc[4][4] = {};
+  for (int k0 = 0; k0 < g.K; k0 += D_KC) {
+    for (int e = tid; e < D_T * D_KC; e += 256) {
+      int i, k;
+      if (g.sak == 1) { i = e / D_KC; k = e % D_KC; } else { k = e / D_T; i = e % D_T; }
+      const int gi = i0 + i, gk = k0 + k;
+      As[k][i] = (gi < g.M && gk < g.K) ? g.A[(int64_t)gi * g.sai + (int64_t)gk * g.sak] : 0.0;
+      int j, kb;
+      if (g.sbj == 1) { kb = e / D_T; j = e % D_T; } else { j = e / D_KC; kb = e % D_KC; }
+      const int gj = j0 + j, gkb = k0 + kb;
+      Bs[kb][j] = (gj < g.N && gkb < g.K) ? g.B[(int64_t)gkb * g.sbk + (int64_t)gj * g.sbj] : 0.0;
     }
-    for (int i = j + 1 + tid; i < bs; i += nt) L[i * P + j] /= d;
     __syncthreads();
-    const int n = bs - j - 1;  // trailing block; only its lower triangle is updated
-    for (int e = tid; e < n * n; e += nt) {
-      const int r = e / n, c = e % n;
-      if (c <= r) {
-        const int gi = j + 1 + r, gc = j + 1 + c;
-        L[gi * P + gc] -= L[gi * P + j] * L[gc * P + j];
+#pragma unroll 4
+    for (int kk = 0; kk < D_KC; ++kk) {
+      double a[4], b[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        a[u] = As[kk][ty * 4 + u];
+        b[u] = Bs[kk][tx * 4 + u];
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) acc[u][v] = fma(a[u], b[v], acc[u][v]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int u = 0; u < 4; ++u)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int i = i0 + ty * 4 + u, j = j0 + tx * 4 + v;
+      if (i < g.M && j < g.N) {
+        double* c = g.C + (int64_t)i * g.ldc + j;
+        const double r = g.alpha * acc[u][v];
+        *c = g.beta != 0.0 ? g.beta * *c + r : r;
       }
     }
-    __syncthreads();
-  }
-  // in-place inverse of the lower-triangular factor, last column first:
-  // column j below the diagonal becomes -(Linv_trailing * L[j+1:, j]) / L[j][j].
-  for (int j = bs - 1; j >= 0; --j) {
-    const T inv = T(1) / L[j * P + j];
-    for (int i = j + 1 + tid; i < bs; i += nt) {
-      T s = T(0);
-      for (int t = j + 1; t <= i; ++t) s += L[i * P + t] * L[t * P + j];
-      colbuf[i] = -s * inv;
+}
+
+// Up to two independent GEMM problems per launch: blocks [0, d0.ntiles) work on d0,
+// the rest on d1. Each problem is its own by-value argument so no descriptor is
+// ever indexed dynamically.
+template <int BM>
+__global__ __launch_bounds__(256) void gemm_f32_kernel(GemmDesc<float> d0, GemmDesc<float> d1) {
+  const int t = blockIdx.x;
+  if (t < d0.ntiles) gemm_f32_body<BM>(d0, t);
+  else if (t - d0.ntiles < d1.ntiles) gemm_f32_body<BM>(d1, t - d0.ntiles);
+}
+
+__global__ __launch_bounds__(256) void gemm_f64_kernel(GemmDesc<double> d0, GemmDesc<double> d1) {
+  const int t = blockIdx.x;
+  if (t < d0.ntiles) gemm_f64_body(d0, t);
+  else if (t - d0.ntiles < d1.ntiles) gemm_f64_body(d1, t - d0.ntiles);
+}
+
+// ---- diagonal block: Cholesky factor and its inverse, in registers ---------------
+//
+// The NB x NB lower triangle is split into TS x TS tiles, one per thread (thread
+// (ti, tj), tj <= ti). Step j of the right-looking factorisation publishes the
+// unscaled column u = A[j:, j] (pivot p = u_j) through LDS; after one barrier every
+// thread updates its tile with A_rc -= u_r u_c / p (= L_rj L_cj) and the owners of
+// column j keep L_rj = u_r / sqrt(p). The inverse X = L^{-1} is formed in the same
+// sweep, one step behind, by right-looking forward substitution on X = I: row j-1
+// of X (final) updates rows >= j with L's column j-1, and row j becomes final and
+// is scaled by 1/L_jj. One barrier per step; three column buffers and two row
+// buffers make every LDS slot's readers finish before it is rewritten.
+template <class T>
+__global__ __launch_bounds__(diag_threads<T>()) void potrf_inv_kernel(T* A, int64_t lda, int kb, int bs,
+                                                        int32_t* info) {
+  constexpr int NB = Blk<T>::NB, TS = Blk<T>::TS, NT = NB / TS;
+  constexpr int NTILES = NT * (NT + 1) / 2;
+  __shared__ T cb[3][NB];
+  __shared__ T rb[2][NB];
+  const int tid = threadIdx.x;
+  const bool own = tid < NTILES;
+  int ti = 0, tj = 0;
+  {
+    int rem = own ? tid : 0;
+    while (rem >= ti + 1) {
+      rem -= ti + 1;
+      ++ti;
     }
-    __syncthreads();
-    for (int i = j + 1 + tid; i < bs; i += nt) L[i * P + j] = colbuf[i];
-    if (tid == 0) L[j * P + j] = inv;
-    __syncthreads();
+    tj = rem;
   }
-  for (int e = tid; e < bs * bs; e += nt) {
-    const int i = e / bs, j = e % bs;
-    A[(int64_t)(kb + i) * lda + kb + j] = j <= i ? L[i * P + j] : T(0);
+  const int r0 = ti * TS, c0 = tj * TS;
+
+  T a[TS][TS], x[TS][TS];
+#pragma unroll
+  for (int r = 0; r < TS; ++r)
+#pragma unroll
+    for (int c = 0; c < TS; ++c) {
+      const int gi = r0 + r, gj = c0 + c;
+      T v = gi == gj ? T(1) : T(0);
+      if (own && gi < bs && gj < bs) v = gj <= gi ? A[(int64_t)(kb + gi) * lda + kb + gj] : T(0);
+      a[r][c] = v;
+      x[r][c] = gi == gj ? T(1) : T(0);
+    }
+
+  // publish column 0
+  if (own && tj == 0) {
+#pragma unroll
+    for (int r = 0; r < TS; ++r) cb[0][r0 + r] = a[r][0];
+  }
+  __syncthreads();
+
+  bool failed = false;
+  T inv_d_prev = T(0);
+  int s = 0;  // j % 3
+  for (int jb = 0; jb < NT; ++jb) {
+#pragma unroll
+    for (int jj = 0; jj < TS; ++jj) {
+      const int j = jb * TS + jj;
+      const T* u = cb[s];
+      const T* up = cb[s == 0 ? 2 : s - 1];
+      const T p = u[j];
+      if (tid == 0 && !failed && j < bs && !(p > T(0))) {
+        failed = true;
+        if (*info == 0) *info = kb + j + 1;
+      }
+      const T inv_d = T(1) / sqrt(p);
+      const T inv_p = inv_d * inv_d;
+      if (own) {
+        // (a) factorisation: finish column j, update the trailing lower triangle.
+        // jj is a compile-time constant here, so every mask below is too; only the
+        // tile position (ti, tj) relative to jb is tested at run time.
+        if (tj == jb) {
+#pragma unroll
+          for (int r = 0; r < TS; ++r)
+            if (ti > jb || r >= jj) a[r][jj] = a[r][jj] * inv_d;
+        }
+        if (tj >= jb) {
+          T ur[TS], uc[TS];
+#pragma unroll
+          for (int r = 0; r < TS; ++r) ur[r] = u[r0 + r];
+#pragma unroll
+          for (int c = 0; c < TS; ++c) uc[c] = u[c0 + c] * inv_p;
+          if (tj > jb) {
+            if (ti > tj) {
+#pragma unroll
+              for (int r = 0; r < TS; ++r)
+#pragma unroll
+                for (int c = 0; c < TS; ++c) a[r][c] -= ur[r] * uc[c];
+            } else {
+#pragma unroll
+              for (int r = 0; r < TS; ++r)
+#pragma unroll
+                for (int c = 0; c <= r; ++c) a[r][c] -= ur[r] * uc[c];
+            }
+          } else if (ti > tj) {
+#pragma unroll
+            for (int r = 0; r < TS; ++r)
+#pragma unroll
+              for (int c = jj + 1; c < TS; ++c) a[r][c] -= ur[r] * uc[c];
+          } else {
+#pragma unroll
+            for (int r = jj + 1; r < TS; ++r)
+#pragma unroll
+              for (int c = jj + 1; c <= r; ++c) a[r][c] -= ur[r] * uc[c];
+          }
+        }
+        // (b) inverse: row j-1 of X updates rows >= j through L's column j-1:
+        // x[r][c] -= L[r][j-1] X[j-1][c] for global rows >= j, columns <= j-1
+        if (j > 0 && ti >= jb && tj <= (j - 1) / TS) {
+          const T* xr = rb[(j - 1) & 1];
+          T lr[TS], xc[TS];
+#pragma unroll
+          for (int r = 0; r < TS; ++r) lr[r] = up[r0 + r] * inv_d_prev;
+#pragma unroll
+          for (int c = 0; c < TS; ++c) xc[c] = xr[c0 + c];
+          // rows: all when ti > jb, else r >= jj; columns: all when tj*TS + TS-1 <= j-1,
+          // else (tj == jb, jj >= 1) c <= jj-1
+          const bool all_rows = ti > jb;
+          const bool all_cols = tj < jb;
+          if (all_rows && all_cols) {
+#pragma unroll
+            for (int r = 0; r < TS; ++r)
+#pragma unroll
+              for (int c = 0; c < TS; ++c) x[r][c] -= lr[r] * xc[c];
+          } else if (all_rows) {
+#pragma unroll
+            for (int r = 0; r < TS; ++r)
+#pragma unroll
+              for (int c = 0; c < jj; ++c) x[r][c] -= lr[r] * xc[c];
+          } else if (all_cols) {
+#pragma unroll
+            for (int r = jj; r < TS; ++r)
+#pragma unroll
+              for (int c = 0; c < TS; ++c) x[r][c] -= lr[r] * xc[c];
+          } else {
+#pragma unroll
+            for (int r = jj; r < TS; ++r)
+#pragma unroll
+              for (int c = 0; c < jj; ++c) x[r][c] -= lr[r] * xc[c];
+          }
+        }
+        // (c) row j of X is final: scale by 1/L_jj and publish (columns <= j)
+        if (ti == jb) {
+#pragma unroll
+          for (int c = 0; c < TS; ++c)
+            if (tj < jb || c <= jj) {
+              x[jj][c] *= inv_d;
+              rb[j & 1][c0 + c] = x[jj][c];
+            }
+        }
+        // publish the (updated, unscaled) column j+1
+        if (j + 1 < NB) {
+          const int jn = (jj + 1) % TS;
+          const int jbn = jj + 1 == TS ? jb + 1 : jb;
+          if (tj == jbn) {
+            T* un = cb[s == 2 ? 0 : s + 1];
+#pragma unroll
+            for (int r = 0; r < TS; ++r)
+              if (ti > jbn || r >= jn) un[r0 + r] = a[r][jn];
+          }
+        }
+      }
+      inv_d_prev = inv_d;
+      s = s == 2 ? 0 : s + 1;
+      __syncthreads();
+    }
+  }
+
+  // write L^{-1} (lower triangle, zeros above) over the diagonal block
+  if (own) {
+#pragma unroll
+    for (int r = 0; r < TS; ++r)
+#pragma unroll
+      for (int c = 0; c < TS; ++c) {
+        const int gi = r0 + r, gj = c0 + c;
+        if (gi < bs && gj < bs) A[(int64_t)(kb + gi) * lda + kb + gj] = gj <= gi ? x[r][c] : T(0);
+      }
+  }
+  for (int e = tid; e < NB * NB; e += blockDim.x) {
+    const int gi = e / NB, gj = e % NB;
+    if (gj / TS > gi / TS && gi < bs && gj < bs) A[(int64_t)(kb + gi) * lda + kb + gj] = T(0);
   }
 }
 
@@ -218,7 +468,8 @@ __global__ __launch_bounds__(256) void ridge_partial_kernel(const T* __restrict_
                                                             double* part) {
   __shared__ double s2[256], st[256];
   double a = 0.0, b = 0.0;
-  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < d * d; e += (int64_t)kRedBlocks * 256) {
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < d * d;
+       e += (int64_t)kRedBlocks * 256) {
     const double v = (double)G[e];
     a += v * v;
     if (e / d == e % d) b += v;
@@ -264,6 +515,8 @@ __global__ __launch_bounds__(256) void to_float_kernel(const T* __restrict__ X, 
     Y[e] = (float)X[e];
 }
 
+bool al16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
 template <class T>
 GemmDesc<T> desc(const T* A, int64_t sai, int64_t sak, const T* B, int64_t sbk, int64_t sbj, T* C,
                  int64_t ldc, int M, int N, int K, T alpha, T beta, int lower = 0) {
@@ -274,24 +527,43 @@ GemmDesc<T> desc(const T* A, int64_t sai, int64_t sak, const T* B, int64_t sbk, 
   g.M = M; g.N = N; g.K = K;
   g.alpha = alpha; g.beta = beta;
   g.lower = lower;
-  g.tiles_n = (N + GT - 1) / GT;
-  g.ntiles = (M > 0 && N > 0 && K > 0) ? ((M + GT - 1) / GT) * g.tiles_n : 0;
+  // vector loads along the contiguous dimension: the other stride and the base must
+  // keep every 4-element group 16-byte aligned
+  g.vecA = al16(A) && ((sak == 1 && sai % 4 == 0) || (sai == 1 && sak % 4 == 0));
+  g.vecB = al16(B) && ((sbj == 1 && sbk % 4 == 0) || (sbk == 1 && sbj % 4 == 0));
   return g;
 }
 
 template <class T>
+void set_tiles(GemmDesc<T>& g, int tile) {
+  g.tiles_n = (g.N + tile - 1) / tile;
+  g.ntiles = (g.M > 0 && g.N > 0 && g.K > 0) ? ((g.M + tile - 1) / tile) * g.tiles_n : 0;
+}
+
+// One launch for up to two problems. fp32 uses 128 x 128 tiles unless that would
+// leave most of the 256 CUs idle, then 64 x 64.
+template <class T>
 hipError_t run_group(const GemmDesc<T>* ds, int n, hipStream_t st) {
-  GemmGroup<T> grp{};
-  int total = 0;
+  GemmDesc<T> d[2] = {};
   int m = 0;
   for (int i = 0; i < n; ++i)
-    if (ds[i].ntiles > 0) {
-      grp.d[m++] = ds[i];
-      total += ds[i].ntiles;
-    }
+    if (ds[i].M > 0 && ds[i].N > 0 && ds[i].K > 0) d[m++] = ds[i];
   if (m == 0) return hipSuccess;
-  grp.n = m;
-  hipLaunchKernelGGL((solve_gemm_kernel<T>), dim3(total), dim3(256), 0, st, grp);
+  if constexpr (sizeof(T) == 4) {
+    for (int i = 0; i < m; ++i) set_tiles(d[i], 128);
+    const bool small = d[0].ntiles + d[1].ntiles < 256;
+    if (small)
+      for (int i = 0; i < m; ++i) set_tiles(d[i], 64);
+    const int total = d[0].ntiles + d[1].ntiles;
+    if (small)
+      hipLaunchKernelGGL(gemm_f32_kernel<64>, dim3(total), dim3(256), 0, st, d[0], d[1]);
+    else
+      hipLaunchKernelGGL(gemm_f32_kernel<128>, dim3(total), dim3(256), 0, st, d[0], d[1]);
+  } else {
+    for (int i = 0; i < m; ++i) set_tiles(d[i], D_T);
+    const int total = d[0].ntiles + d[1].ntiles;
+    hipLaunchKernelGGL(gemm_f64_kernel, dim3(total), dim3(256), 0, st, d[0], d[1]);
+  }
   return hipGetLastError();
 }
 
@@ -323,6 +595,7 @@ SolveLayout layout(int64_t d, int64_t dout) {
 template <class T>
 hipError_t solve_t(const T* G, const T* C, int64_t d64, int64_t dout64, double lambda,
                    bool adaptive, float* dW, int32_t* info, void* ws, hipStream_t st) {
+  constexpr int NB = Blk<T>::NB;
   const SolveLayout L = layout<T>(d64, dout64);
   char* w = (char*)ws;
   T* A = (T*)(w + L.A);
@@ -352,7 +625,8 @@ hipError_t solve_t(const T* G, const T* C, int64_t d64, int64_t dout64, double l
   for (int k = 0; k < nblk; ++k) {
     const int kb = k * NB, bs = std::min(NB, d - kb);
     const int rest = d - kb - bs;
-    hipLaunchKernelGGL((potrf_inv_kernel<T>), dim3(1), dim3(512), 0, st, A, d64, kb, bs, info);
+    hipLaunchKernelGGL((potrf_inv_kernel<T>), dim3(1), dim3(diag_threads<T>()), 0, st, A, d64, kb,
+                       bs, info);
     PKV_TRY(hipGetLastError());
     const T* Linv = A + (int64_t)kb * d + kb;  // Linv(i,t) = Linv[i*d + t]
     {

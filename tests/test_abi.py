@@ -41,8 +41,10 @@ def test_status_strings(L):
 
 
 def test_workspace_queries(L):
-    assert L.patchkv_attend_workspace_bytes(B.BF16, 4096, 172032, 32, 8, 128) == 0  # no split
-    assert L.patchkv_attend_workspace_bytes(B.BF16, 1024, 32768, 32, 8, 128) > 0    # split
+    # bf16: one flag per work item (no split-key partials at this shape)
+    assert 0 < L.patchkv_attend_workspace_bytes(B.BF16, 4096, 172032, 32, 8, 128) <= 4096
+    assert L.patchkv_attend_workspace_bytes(B.F32, 4096, 172032, 32, 8, 128) == 0
+    assert L.patchkv_attend_workspace_bytes(B.BF16, 1024, 32768, 32, 8, 128) > 1 << 20  # split
     assert L.patchkv_attend_workspace_bytes(B.BF16, 10, 10, 3, 2, 128) == 0          # invalid
     assert L.patchkv_solve_workspace_bytes(B.F32, 4096, 4096) >= 5 * 4096 * 4096 * 4
     assert L.patchkv_solve_workspace_bytes(B.F64, 256, 256) >= 5 * 256 * 256 * 8
@@ -68,8 +70,9 @@ def test_attend_validation(L):
     assert attend(L, scale=0.0) == B.E_VALUE
     assert attend(L, scale=float("nan")) == B.E_VALUE
     assert attend(L, Q=FAKE + 2) == B.E_VALUE           # misaligned
-    # a shape that needs split-key workspace, given none
+    # bf16 needs a workspace (flags, split-key partials), given none
     assert attend(L, M=16, N=1 << 15, Hq=32, Hkv=8) == B.E_WORKSPACE
+    assert attend(L) == B.E_WORKSPACE
     r = L.patchkv_attend_compressed(B.BF16, FAKE, FAKE, FAKE, FAKE, 8, 0, 16, 4, 2, 128, 0.1, FAKE,
                                     None, 0, None)
     assert r == B.E_SHAPE                                 # idx given but N = 0
