@@ -67,7 +67,13 @@ typedef enum {
 
 typedef enum {
   PATCHKV_RIDGE_ABSOLUTE = 0, /* lambda is the ridge coefficient itself (Eq. 6) */
-  PATCHKV_RIDGE_ADAPTIVE = 1  /* lambda is lambda_0; ridge = lambda_0 ||G||_F^2 / tr(G) (Eq. 7) */
+  PATCHKV_RIDGE_ADAPTIVE = 1, /* lambda is lambda_0; ridge = lambda_0 ||G||_F^2 / tr(G) (Eq. 7) */
+  /* Flag OR-ed into either mode; used by the F32 solve only (F64 ignores it).
+   * Without it the F32 solve forms its block products on bf16 MFMA with every fp32
+   * operand split into two bf16 terms (hi + lo) and three cross products kept,
+   * i.e. about 2^-16 relative error per product instead of fp32's 2^-24, at
+   * 2.5x-5x the speed. With it the products are exact fp32 multiplies (fp32 MFMA). */
+  PATCHKV_SOLVE_EXACT_F32 = 16
 } patchkv_ridge_mode;
 
 /* Human-readable name of a status code (static string, never NULL). */
@@ -152,6 +158,8 @@ int patchkv_accumulate_normal_eq(int acc_dtype, const float* Xc, const float* Yf
 /* ridge_mode ABSOLUTE: lambda is the ridge coefficient (> 0).                  */
 /* ridge_mode ADAPTIVE: lambda is lambda_0 (> 0) and the coefficient is         */
 /*   lambda_0 ||G||_F^2 / tr(G) (Eq. 7), computed on the device in fp64.        */
+/* ridge_mode | PATCHKV_SOLVE_EXACT_F32: exact fp32 products in the F32 solve.   */
+/*   Any other bit set in ridge_mode: PATCHKV_E_VALUE.                          */
 /* dW [d_in][d_out] float, written.                                             */
 /* info: device int32, written: 0 on success, else the 1-based column of the    */
 /*   first non-positive (or NaN) pivot, LAPACK style (dW is then meaningless).  */

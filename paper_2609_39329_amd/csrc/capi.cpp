@@ -47,6 +47,12 @@ int check_ws(const void* ws, size_t have, size_t need) {
 }
 
 bool finite_pos(double x) { return isfinite(x) && x > 0.0; }
+bool valid_ridge_mode(int m) {
+  const int base = m & ~PATCHKV_SOLVE_EXACT_F32;
+  return base == PATCHKV_RIDGE_ABSOLUTE || base == PATCHKV_RIDGE_ADAPTIVE;
+}
+bool adaptive(int m) { return (m & ~PATCHKV_SOLVE_EXACT_F32) == PATCHKV_RIDGE_ADAPTIVE; }
+bool exact(int m) { return (m & PATCHKV_SOLVE_EXACT_F32) != 0; }
 
 int check_stats_dims(int64_t rows, int64_t din, int64_t dout) {
   if (rows < 1 || din < 1 || dout < 1) return PATCHKV_E_SHAPE;
@@ -193,12 +199,11 @@ int patchkv_solve_patch(int acc_dtype, const void* G, const void* C, int64_t d_i
   if (acc_dtype != PATCHKV_F32 && acc_dtype != PATCHKV_F64) return PATCHKV_E_DTYPE;
   if (d_in < 1 || d_out < 1 || d_in > kMaxDim || d_out > kMaxDim) return PATCHKV_E_SHAPE;
   if (!finite_pos(lambda)) return PATCHKV_E_VALUE;
-  if (ridge_mode != PATCHKV_RIDGE_ABSOLUTE && ridge_mode != PATCHKV_RIDGE_ADAPTIVE)
-    return PATCHKV_E_VALUE;
+  if (!valid_ridge_mode(ridge_mode)) return PATCHKV_E_VALUE;
   int s = check_ws(workspace, workspace_bytes, solve_ws_bytes(acc_dtype == PATCHKV_F64, d_in, d_out));
   if (s) return s;
   return status_of(launch_solve(acc_dtype == PATCHKV_F64, G, C, d_in, d_out, lambda,
-                                ridge_mode == PATCHKV_RIDGE_ADAPTIVE, dW, info, workspace,
+                                adaptive(ridge_mode), exact(ridge_mode), dW, info, workspace,
                                 (hipStream_t)stream));
 }
 
@@ -228,8 +233,7 @@ int patchkv_compute_layer_patch(int dtype, int acc_dtype, const void* Q, const v
   if (d > kMaxDim) return PATCHKV_E_SHAPE;
   if (!finite_pos(scale) || !finite_pos(lambda)) return PATCHKV_E_VALUE;
   if (rho != 0 && rho != 1) return PATCHKV_E_VALUE;
-  if (ridge_mode != PATCHKV_RIDGE_ABSOLUTE && ridge_mode != PATCHKV_RIDGE_ADAPTIVE)
-    return PATCHKV_E_VALUE;
+  if (!valid_ridge_mode(ridge_mode)) return PATCHKV_E_VALUE;
   if (!al16(Q) || !al16(K) || !al16(V) || !al16(W) || (!idx && (!al16(Kc) || !al16(Vc))))
     return PATCHKV_E_VALUE;
   const LayerWs L = layer_ws(dtype, acc_dtype, M, N, B, Hq, Hkv, dh);
@@ -269,8 +273,8 @@ int patchkv_compute_layer_patch(int dtype, int acc_dtype, const void* Q, const v
                                (double*)C, st);
   }
   if (e != hipSuccess) return PATCHKV_E_HIP;
-  e = launch_solve(acc_dtype == PATCHKV_F64, G, C, d, d, lambda,
-                   ridge_mode == PATCHKV_RIDGE_ADAPTIVE, dW, info, wsv, st);
+  e = launch_solve(acc_dtype == PATCHKV_F64, G, C, d, d, lambda, adaptive(ridge_mode),
+                   exact(ridge_mode), dW, info, wsv, st);
   return status_of(e);
 }
 

@@ -57,9 +57,11 @@ hipError_t launch_normal_eq_f64(const float* X, const float* Yf, const float* Yc
 
 // ---------------------------------------------------------------- ridge solve
 size_t solve_ws_bytes(bool f64, int64_t din, int64_t dout);
+// exact_f32: fp32 block products on fp32 MFMA (else three bf16 MFMA terms); the
+// fp64 solve always uses fp64 arithmetic.
 hipError_t launch_solve(bool f64, const void* G, const void* C, int64_t din, int64_t dout,
-                        double lambda, bool adaptive, float* dW, int32_t* info, void* ws,
-                        hipStream_t st);
+                        double lambda, bool adaptive, bool exact_f32, float* dW, int32_t* info,
+                        void* ws, hipStream_t st);
 
 // Small helpers.
 inline size_t align_up(size_t x, size_t a = 256) { return (x + a - 1) / a * a; }

@@ -192,6 +192,216 @@ __device__ __forceinline__ void gemm_f32_body(const GemmDesc<float>& g, int t) {
       }
 }
 
+// ---- fp32 via three bf16 MFMA terms: 128 x 128 output tile, 4 waves ------------------
+//
+// Each fp32 operand x is split as x_hi = bf16(x), x_lo = bf16(x - x_hi) while it is
+// staged into LDS, and a b ~ a_hi b_hi + a_hi b_lo + a_lo b_hi on MFMA 32x32x16 bf16
+// with fp32 accumulation (representation error of the split about 2^-18 relative,
+// the dropped a_lo b_lo term about the same). The MFMA computes the transposed tile
+// (rows = output columns), so every lane owns 4 consecutive output columns of one
+// output row and the read-modify-write of C uses 16-byte accesses. The C tile is
+// fetched before the K loop so its latency hides behind the products.
+struct SGemm {
+  const float* A;  // A(i,k) = AK ? A[i*sa + k] : A[k*sa + i]
+  int64_t sa;
+  const float* B;  // B(k,j) = BJ ? B[k*sb + j] : B[j*sb + k]
+  int64_t sb;
+  float* C;        // C[i*ldc + j] = beta C + alpha sum_k A(i,k) B(k,j)
+  int64_t ldc;
+  int M, N, K;
+  float alpha, beta;
+  int lower;       // only tiles with tile_row >= tile_col (enumerated triangularly)
+  int tiles_n, ntiles;
+  int vecA, vecB, vecC;
+};
+
+constexpr int S_BM = 128, S_KC = 32;
+constexpr int S_PK = S_KC + 8;    // pitch of a [row][k] LDS tile (bf16)
+constexpr int S_PR = S_BM + 16;   // pitch of a [k][row] LDS tile (bf16)
+constexpr int S_TILE = S_BM * S_PK > S_KC * S_PR ? S_BM * S_PK : S_KC * S_PR;  // bf16 per plane
+constexpr int S_LDS = 2 * 4 * S_TILE;  // 2 buffers x {A hi, A lo, B hi, B lo}
+
+template <bool AK, bool BJ>
+__device__ __forceinline__ void sgemm3_body(const SGemm& g, int t, __bf16* lds) {
+  int ti, tj;
+  if (g.lower) {
+    ti = (int)((sqrtf(8.f * (float)t + 1.f) - 1.f) * 0.5f);
+    while ((ti + 1) * (ti + 2) / 2 <= t) ++ti;
+    while (ti * (ti + 1) / 2 > t) --ti;
+    tj = t - ti * (ti + 1) / 2;
+  } else {
+    ti = t / g.tiles_n;
+    tj = t % g.tiles_n;
+  }
+  const int i0 = ti * S_BM, j0 = tj * S_BM;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int h32 = lane >> 5, l32 = lane & 31;
+  const int wi = (wid >> 1) * 64, wj = (wid & 1) * 64;
+  // [row][k] when the contraction index is contiguous in memory, else [k][row]
+  constexpr bool a_rk = AK, b_rk = !BJ;
+  constexpr int PA = a_rk ? S_PK : S_PR, PB = b_rk ? S_PK : S_PR;
+
+  // C tile prefetch: lane owns C[i0+wi+32a+l32][j0+wj+32b+8q+4h32 .. +3]
+  f32x4 cpre[2][2][4];
+  const bool use_c = g.beta != 0.f;
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        f32x4 v = {};
+        const int i = i0 + wi + 32 * a + l32, j = j0 + wj + 32 * b + 8 * q + 4 * h32;
+        if (use_c && i < g.M && j < g.N) {
+          const float* s = g.C + (int64_t)i * g.ldc + j;
+          if (g.vecC && j + 3 < g.N) v = *(const f32x4*)s;
+          else
+            for (int e = 0; e < 4; ++e) v[e] = j + e < g.N ? s[e] : 0.f;
+        }
+        cpre[a][b][q] = v;
+      }
+
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
+
+  // staging: 128 x 32 floats per operand and chunk = 4 float4 per thread, each a
+  // run of 4 elements contiguous in memory
+  f32x4 ra[4], rb[4];
+  auto fetch = [&](int k0) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int c = u * 256 + tid;
+      {
+        int i, k;
+        if constexpr (AK) { i = c / (S_KC / 4); k = (c % (S_KC / 4)) * 4; }
+        else { k = c / (S_BM / 4); i = (c % (S_BM / 4)) * 4; }
+        const int gi = i0 + i, gk = k0 + k;
+        const int nvalid = AK ? (gi < g.M ? g.K - gk : 0) : (gk < g.K ? g.M - gi : 0);
+        const float* s = g.A + (AK ? (int64_t)gi * g.sa + gk : (int64_t)gk * g.sa + gi);
+        f32x4 v = {};
+        if (nvalid >= 4 && g.vecA) v = *(const f32x4*)s;
+        else
+          for (int e = 0; e < 4; ++e)
+            if (e < nvalid) v[e] = s[e];
+        ra[u] = v;
+      }
+      {
+        int j, k;
+        if constexpr (BJ) { k = c / (S_BM / 4); j = (c % (S_BM / 4)) * 4; }
+        else { j = c / (S_KC / 4); k = (c % (S_KC / 4)) * 4; }
+        const int gj = j0 + j, gk = k0 + k;
+        const int nvalid = BJ ? (gk < g.K ? g.N - gj : 0) : (gj < g.N ? g.K - gk : 0);
+        const float* s = g.B + (BJ ? (int64_t)gk * g.sb + gj : (int64_t)gj * g.sb + gk);
+        f32x4 v = {};
+        if (nvalid >= 4 && g.vecB) v = *(const f32x4*)s;
+        else
+          for (int e = 0; e < 4; ++e)
+            if (e < nvalid) v[e] = s[e];
+        rb[u] = v;
+      }
+    }
+  };
+  auto split_store = [](__bf16* hi, __bf16* lo, int off, f32x4 v) {
+    bf16x4 h, l;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      h[e] = to_bf16(v[e]);
+      l[e] = to_bf16(v[e] - (float)h[e]);
+    }
+    *(bf16x4*)(hi + off) = h;
+    *(bf16x4*)(lo + off) = l;
+  };
+  auto plane = [&](int buf, int p) { return lds + (buf * 4 + p) * S_TILE; };
+  auto stash = [&](int buf) {
+    __bf16 *ah = plane(buf, 0), *al = plane(buf, 1), *bh = plane(buf, 2), *bl = plane(buf, 3);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int c = u * 256 + tid;
+      split_store(ah, al, a_rk ? (c / (S_KC / 4)) * PA + (c % (S_KC / 4)) * 4
+                               : (c / (S_BM / 4)) * PA + (c % (S_BM / 4)) * 4, ra[u]);
+      split_store(bh, bl, b_rk ? (c / (S_KC / 4)) * PB + (c % (S_KC / 4)) * 4
+                               : (c / (S_BM / 4)) * PB + (c % (S_BM / 4)) * 4, rb[u]);
+    }
+  };
+  // 32 rows x 8 k fragment (row r0 + l32, k k0 + 8 h32 ..) of an LDS tile
+  const int tr_k = 8 * h32 + ((lane & 15) >> 2);
+  const int tr_r = ((lane >> 4) & 1) * 16 + 4 * (lane & 3);
+  auto frag = [&](const __bf16* base, int pitch, bool rk, int r0, int k0) -> bf16x8 {
+    if (rk) return *(const bf16x8*)(base + (r0 + l32) * pitch + k0 + h32 * 8);
+    const PKV_LDS __bf16* q = (const PKV_LDS __bf16*)(base + (k0 + tr_k) * pitch + r0 + tr_r);
+    return cat8(lds_read_tr16(q), lds_read_tr16(q + 4 * pitch));
+  };
+
+  const int nk = (g.K + S_KC - 1) / S_KC;
+  fetch(0);
+  stash(0);
+  __syncthreads();
+  for (int kc = 0; kc < nk; ++kc) {
+    const int buf = kc & 1;
+    if (kc + 1 < nk) fetch((kc + 1) * S_KC);
+    const __bf16 *ah = plane(buf, 0), *al = plane(buf, 1), *bh = plane(buf, 2), *bl = plane(buf, 3);
+#pragma unroll
+    for (int ks = 0; ks < S_KC; ks += 16) {
+      bf16x8 fah[2], fal[2], fbh[2], fbl[2];
+#pragma unroll
+      for (int a = 0; a < 2; ++a) {
+        fah[a] = frag(ah, PA, a_rk, wi + 32 * a, ks);
+        fal[a] = frag(al, PA, a_rk, wi + 32 * a, ks);
+      }
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        fbh[b] = frag(bh, PB, b_rk, wj + 32 * b, ks);
+        fbl[b] = frag(bl, PB, b_rk, wj + 32 * b, ks);
+      }
+      // transposed tile: MFMA rows are output columns (B), MFMA columns output rows (A)
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+          acc[a][b] = mfma32(fbh[b], fah[a], acc[a][b]);
+          acc[a][b] = mfma32(fbh[b], fal[a], acc[a][b]);
+          acc[a][b] = mfma32(fbl[b], fah[a], acc[a][b]);
+        }
+    }
+    if (kc + 1 < nk) stash(buf ^ 1);
+    __syncthreads();
+  }
+
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int i = i0 + wi + 32 * a + l32, j = j0 + wj + 32 * b + 8 * q + 4 * h32;
+        if (i >= g.M || j >= g.N) continue;
+        f32x4 v;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = g.alpha * acc[a][b][4 * q + e];
+        if (use_c) v += g.beta * cpre[a][b][q];
+        float* d = g.C + (int64_t)i * g.ldc + j;
+        if (g.vecC && j + 3 < g.N) *(f32x4*)d = v;
+        else
+          for (int e = 0; e < 4; ++e)
+            if (j + e < g.N) d[e] = v[e];
+      }
+}
+
+// Up to two problems per launch, each with its own operand layout; work items are
+// spread so that consecutive tiles of one problem share an XCD (and its L2).
+template <bool AK0, bool BJ0, bool AK1, bool BJ1>
+__global__ __launch_bounds__(256, 2) void sgemm3_kernel(SGemm d0, SGemm d1) {
+  __shared__ __attribute__((aligned(16))) __bf16 lds[S_LDS];
+  const int total = d0.ntiles + d1.ntiles;
+  const int t = xcd_item((total + kXcds - 1) / kXcds);
+  if (t >= total) return;
+  if (t < d0.ntiles) sgemm3_body<AK0, BJ0>(d0, t, lds);
+  else sgemm3_body<AK1, BJ1>(d1, t - d0.ntiles, lds);
+}
+
 // ---- fp64: 64 x 64 output tile, fp64 FMA, 4 x 4 outputs per thread ----------------
 constexpr int D_T = 64, D_KC = 32;
 
@@ -323,7 +533,9 @@ __global__ __launch_bounds__(diag_threads<T>()) void potrf_inv_kernel(T* A, int6
         failed = true;
         if (*info == 0) *info = kb + j + 1;
       }
-      const T inv_d = T(1) / sqrt(p);
+      T inv_d;
+      if constexpr (sizeof(T) == 4) inv_d = __builtin_amdgcn_rsqf(p);  // v_rsq_f32, about 1 ulp
+      else inv_d = T(1) / sqrt(p);
       const T inv_p = inv_d * inv_d;
       if (own) {
         // (a) factorisation: finish column j, update the trailing lower triangle.
@@ -567,6 +779,54 @@ hipError_t run_group(const GemmDesc<T>* ds, int n, hipStream_t st) {
   return hipGetLastError();
 }
 
+SGemm to_sgemm(const GemmDesc<float>& g, bool& ak, bool& bj) {
+  SGemm s{};
+  ak = g.sak == 1;
+  bj = g.sbj == 1;
+  s.A = g.A; s.sa = ak ? g.sai : g.sak;
+  s.B = g.B; s.sb = bj ? g.sbk : g.sbj;
+  s.C = g.C; s.ldc = g.ldc;
+  s.M = g.M; s.N = g.N; s.K = g.K;
+  s.alpha = g.alpha; s.beta = g.beta;
+  s.lower = g.lower;
+  const int tm = (g.M + S_BM - 1) / S_BM, tn = (g.N + S_BM - 1) / S_BM;
+  s.tiles_n = tn;
+  s.ntiles = g.lower ? tm * (tm + 1) / 2 : tm * tn;  // a lower-triangle update is square
+  s.vecA = g.vecA; s.vecB = g.vecB;
+  s.vecC = al16(g.C) && g.ldc % 4 == 0;
+  return s;
+}
+
+// fp32 products on three bf16 MFMA terms, up to two problems per launch. The
+// operand layouts the solve uses: A contiguous along k with B along k or j, or A
+// contiguous along i with B along j.
+hipError_t run_group_split(const GemmDesc<float>* ds, int n, hipStream_t st) {
+  SGemm s[2] = {};
+  bool ak[2] = {true, true}, bj[2] = {true, true};
+  int m = 0;
+  for (int i = 0; i < n; ++i)
+    if (ds[i].M > 0 && ds[i].N > 0 && ds[i].K > 0) {
+      s[m] = to_sgemm(ds[i], ak[m], bj[m]);
+      ++m;
+    }
+  if (m == 0) return hipSuccess;
+  if (m == 1) {
+    ak[1] = ak[0];
+    bj[1] = bj[0];
+  }
+  const int total = s[0].ntiles + s[1].ntiles;
+  const dim3 grid((total + kXcds - 1) / kXcds * kXcds), block(256);
+  const int key = (ak[0] << 3) | (bj[0] << 2) | (ak[1] << 1) | (int)bj[1];
+  switch (key) {
+    case 0b1011: hipLaunchKernelGGL((sgemm3_kernel<true, false, true, true>), grid, block, 0, st, s[0], s[1]); break;
+    case 0b1010: hipLaunchKernelGGL((sgemm3_kernel<true, false, true, false>), grid, block, 0, st, s[0], s[1]); break;
+    case 0b1111: hipLaunchKernelGGL((sgemm3_kernel<true, true, true, true>), grid, block, 0, st, s[0], s[1]); break;
+    case 0b0101: hipLaunchKernelGGL((sgemm3_kernel<false, true, false, true>), grid, block, 0, st, s[0], s[1]); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 struct SolveLayout {
   size_t A, Lm, R, Z, X, part, lam, total;
 };
@@ -594,7 +854,7 @@ SolveLayout layout(int64_t d, int64_t dout) {
 
 template <class T>
 hipError_t solve_t(const T* G, const T* C, int64_t d64, int64_t dout64, double lambda,
-                   bool adaptive, float* dW, int32_t* info, void* ws, hipStream_t st) {
+                   bool adaptive, bool exact, float* dW, int32_t* info, void* ws, hipStream_t st) {
   constexpr int NB = Blk<T>::NB;
   const SolveLayout L = layout<T>(d64, dout64);
   char* w = (char*)ws;
@@ -621,6 +881,11 @@ hipError_t solve_t(const T* G, const T* C, int64_t d64, int64_t dout64, double l
     PKV_TRY(hipGetLastError());
   }
   const T one = T(1), zero = T(0), mone = T(-1);
+  auto run = [&](const GemmDesc<T>* g, int n) -> hipError_t {
+    if constexpr (sizeof(T) == 4)
+      if (!exact) return run_group_split(g, n, st);
+    return run_group(g, n, st);
+  };
   const int nblk = (d + NB - 1) / NB;
   for (int k = 0; k < nblk; ++k) {
     const int kb = k * NB, bs = std::min(NB, d - kb);
@@ -637,7 +902,7 @@ hipError_t solve_t(const T* G, const T* C, int64_t d64, int64_t dout64, double l
       // Z_k = Linv R_k : (bs x dout)
       g[1] = desc<T>(Linv, d, 1, R + (int64_t)kb * dout, dout, 1, Z + (int64_t)kb * dout, dout, bs,
                      dout, bs, one, zero);
-      PKV_TRY(run_group(g, 2, st));
+      PKV_TRY(run(g, 2));
     }
     if (rest > 0) {
       GemmDesc<T> g[2];
@@ -648,7 +913,7 @@ hipError_t solve_t(const T* G, const T* C, int64_t d64, int64_t dout64, double l
       // R_i -= L_ik Z_k
       g[1] = desc<T>(Lp, d, 1, Z + (int64_t)kb * dout, dout, 1, R + (int64_t)(kb + bs) * dout, dout,
                      rest, dout, bs, mone, one);
-      PKV_TRY(run_group(g, 2, st));
+      PKV_TRY(run(g, 2));
     }
   }
   for (int k = nblk - 1; k >= 0; --k) {
@@ -658,13 +923,13 @@ hipError_t solve_t(const T* G, const T* C, int64_t d64, int64_t dout64, double l
       // X_k = Linv^T Z_k : X(i,n) = sum_t Linv[t][i] Z[kb+t][n]
       GemmDesc<T> g = desc<T>(Linv, 1, d, Z + (int64_t)kb * dout, dout, 1, X + (int64_t)kb * dout,
                               dout, bs, dout, bs, one, zero);
-      PKV_TRY(run_group(&g, 1, st));
+      PKV_TRY(run(&g, 1));
     }
     if (kb > 0) {
       // Z_i -= L_ki^T X_k for i < kb : Z(i,n) -= sum_t Lm[kb+t][i] X[kb+t][n]
       GemmDesc<T> g = desc<T>(Lm + (int64_t)kb * d, 1, d, X + (int64_t)kb * dout, dout, 1, Z, dout, kb,
                               dout, bs, mone, one);
-      PKV_TRY(run_group(&g, 1, st));
+      PKV_TRY(run(&g, 1));
     }
   }
   {
@@ -683,13 +948,13 @@ size_t solve_ws_bytes(bool f64, int64_t din, int64_t dout) {
 }
 
 hipError_t launch_solve(bool f64, const void* G, const void* C, int64_t din, int64_t dout,
-                        double lambda, bool adaptive, float* dW, int32_t* info, void* ws,
-                        hipStream_t st) {
+                        double lambda, bool adaptive, bool exact_f32, float* dW, int32_t* info,
+                        void* ws, hipStream_t st) {
   if (f64)
-    return solve_t<double>((const double*)G, (const double*)C, din, dout, lambda, adaptive, dW, info,
-                           ws, st);
-  return solve_t<float>((const float*)G, (const float*)C, din, dout, lambda, adaptive, dW, info, ws,
-                        st);
+    return solve_t<double>((const double*)G, (const double*)C, din, dout, lambda, adaptive, true, dW,
+                           info, ws, st);
+  return solve_t<float>((const float*)G, (const float*)C, din, dout, lambda, adaptive, exact_f32, dW,
+                        info, ws, st);
 }
 
 }  // namespace pkv

@@ -105,6 +105,8 @@ def test_solve_validation(L):
     assert f(B.F32, FAKE, FAKE, 16, 16, 0.0, 0, FAKE, FAKE, FAKE, nb, None) == B.E_VALUE
     assert f(B.F32, FAKE, FAKE, 16, 16, -1.0, 0, FAKE, FAKE, FAKE, nb, None) == B.E_VALUE
     assert f(B.F32, FAKE, FAKE, 16, 16, 0.1, 2, FAKE, FAKE, FAKE, nb, None) == B.E_VALUE
+    assert f(B.F32, FAKE, FAKE, 16, 16, 0.1, 2 | B.SOLVE_EXACT_F32, FAKE, FAKE, FAKE, nb, None) == B.E_VALUE
+    assert f(B.F32, FAKE, FAKE, 16, 16, 0.1, 32, FAKE, FAKE, FAKE, nb, None) == B.E_VALUE
     assert f(B.F32, FAKE, FAKE, 16, 16, 0.1, 0, FAKE, FAKE, None, nb, None) == B.E_WORKSPACE
     assert f(B.F32, FAKE, FAKE, 16, 16, 0.1, 0, FAKE, FAKE, FAKE, nb - 1, None) == B.E_WORKSPACE
     assert f(B.F32, FAKE, FAKE, 0, 16, 0.1, 0, FAKE, FAKE, FAKE, nb, None) == B.E_SHAPE
