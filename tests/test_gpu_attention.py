@@ -24,7 +24,7 @@ TOL_COMP = {"bf16": 5e-5, "f32": 2e-5}
 
 SHAPES = [
     # M, N, B, Hq, Hkv, dh, dtype
-    (64, 700, 150, 8, 2, 128, "bf16"),      # ragged N (not a multiple of the 64-key tile)
+    (64, 700, 150, 8, 2, 128, "bf16"),      # ragged N (not a multiple of the 32-key tile)
     (100, 1000, 333, 28, 4, 128, "bf16"),   # GQA group of 7, ragged row tiles
     (33, 129, 17, 4, 4, 64, "bf16"),        # head_dim 64, group 1
     (300, 2049, 260, 32, 8, 128, "bf16"),   # several row tiles, ragged tail
