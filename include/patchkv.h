@@ -96,7 +96,11 @@ int patchkv_version(void);
 /* K, V [Hkv][N][dh]   full cache (dtype)                                       */
 /* O  [M][Hq*dh]       float output, written (not accumulated)                  */
 /* Limits: 1 <= Hkv <= Hq, Hq % Hkv == 0, dh in {64, 128}, M >= 1, N >= 1,      */
-/*         M*Hq and N below 2^31, scale > 0 and finite.                        */
+/*         M*Hq and N below 2^31, and for bf16 N*dh*2 below 2^32 (N < 2^24 at   */
+/*         dh = 128); scale > 0 and finite.                                    */
+/* Workspace: bf16 needs a transposed copy of V (Hkv*N*dh bf16, laid out in     */
+/*   32-key tiles) plus a few bytes per work item; both dtypes need partial     */
+/*   results when the key range is split (small M).                             */
 /* ------------------------------------------------------------------------- */
 size_t patchkv_attend_workspace_bytes(int dtype, int64_t M, int64_t N, int Hq, int Hkv, int dh);
 
@@ -108,8 +112,9 @@ int patchkv_attend_full(int dtype, const void* Q, const void* K, const void* V,
 /* forward; Sec. 2.1 compressed cache C_b).                                     */
 /*  - idx != NULL: eviction subset. K, V are the FULL cache [Hkv][N][dh] and the */
 /*    compressed cache is K[:, idx[b], :], V[:, idx[b], :] for b < B, gathered   */
-/*    on the fly. idx [B] int32, every entry in [0, N) (precondition; entries    */
-/*    outside it are clamped into range by the kernel, never dereferenced).     */
+/*    on the fly. idx [B] int32, every entry in [0, N) (precondition; no memory  */
+/*    outside the cache is read for entries outside it: the bf16 path reads     */
+/*    them as zero rows, the f32 path clamps them into range).                  */
 /*  - idx == NULL: synthesized cache. K, V are [Hkv][B][dh]; N is ignored.       */
 /* The workspace size is patchkv_attend_workspace_bytes(dtype, M, B, ...).       */
 int patchkv_attend_compressed(int dtype, const void* Q, const void* K, const void* V,

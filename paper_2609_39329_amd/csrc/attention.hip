@@ -2,20 +2,22 @@
 // passes of Alg. 1): O[m, h*dh:(h+1)*dh] = softmax(scale q_{m,h} K_g^T) V_g,
 // g = floor(h / (Hq/Hkv)), every query against every cache entry.
 //
-// bf16 path (attn_bf16_kernel): one workgroup = 4 waves x 64 query rows of one KV
-// head. The query heads of a GQA group are packed into the row dimension (row
-// r <-> query r / G, head g*G + r % G), so one K/V tile in LDS serves all of them.
-// Each wave keeps its 64 rows of Q in registers and computes S^T = K Q^T on
-// bf16 MFMA 32x32x16 (keys along the MFMA rows, queries along its columns), so a
-// lane owns one query and softmax statistics need only one cross-lane exchange
-// (lane l with l^32). P stays in registers and feeds O^T += V^T P^T directly: the
-// MFMA k-slot order is permuted consistently between P (accumulator order) and V
-// (read with the LDS transpose instruction). The online softmax runs in fp32 in
-// the exp2 domain and only rescales O when a running max grows by more than
-// 2^kTau (the result is identical, P just carries a bounded extra factor).
-// K/V tiles are double-buffered in LDS and prefetched into registers one tile
-// ahead; the workgroup -> work-item map keeps all row tiles of one KV head (and
-// key range) on one XCD so its L2 serves the K/V re-reads.
+// bf16 path (attn_bf16_kernel): one workgroup = 8 waves x 32 query rows of one KV
+// head (two waves per SIMD, so one wave's softmax runs under the other's MFMAs).
+// The query heads of a GQA group are packed into the row dimension (row r <->
+// query r / G, head g*G + r % G), so one K/V tile in LDS serves all of them.
+// Each wave keeps its rows of Q in registers and computes S^T = K Q^T on bf16 MFMA
+// 32x32x16 (keys along the MFMA rows, queries along its columns), so a lane owns
+// one query and softmax statistics need only one cross-lane exchange (lane l with
+// l^32). P stays in registers and feeds O^T += V^T P^T directly. V is first
+// rewritten by vt_kernel into 32-key tiles of V^T whose key order matches the
+// P fragments' k-slots, so the V operand is one 16-byte LDS read (the transposing
+// LDS read delivers about a third of the bandwidth). The online softmax runs in
+// fp32 in the exp2 domain with a fixed per-row offset (fast path) and falls back
+// to a lazily rescaled pass for work items whose scores outgrow it. K/V tiles
+// stream through four LDS slots with register prefetch; the workgroup -> work-item
+// map keeps all row tiles of one KV head (and key range) on one XCD so its L2
+// serves the K/V re-reads.
 //
 // f32 path (attn_f32_kernel): one thread per query row, fp32 FMA dot products
 // against K/V tiles broadcast from LDS, exact online softmax with expf.
@@ -37,12 +39,21 @@ constexpr float kTau = 8.0f;   // lazy-rescale threshold of the fixup path (log2
 constexpr float kBig = 64.0f;  // headroom of the fixed offset in the fast path (log2 units)
 constexpr int kKeyTile = 32;  // keys per iteration, bf16 path
 constexpr int kRowsWG = 256;  // query rows per workgroup (both paths)
+// bf16 path: 32-row query tiles per wave (1: eight waves of 32 rows per workgroup,
+// two waves per SIMD, everything in VGPRs; 2: four waves of 64 rows, one per SIMD,
+// accumulators in AGPRs) and register staging sets of the K/V tile loads
+// (prefetch depth kLoadSets - 1 steps; 2 or 4).
+constexpr int kQT = 1;
+constexpr int kThreadsBf16 = kRowsWG / (32 * kQT) * 64;
+constexpr int kLoadSets = 2;
 constexpr int kKeyTileF32 = 32;
 
 struct AttnParams {
   const void* Q;
   const void* K;
   const void* V;
+  const __bf16* Vt;  // bf16 path: V transposed into 32-key tiles (see vt_kernel)
+  int vt_tiles;      // tiles per KV head in Vt
   const int32_t* idx;
   float* O;
   float* Opart;
@@ -59,6 +70,47 @@ struct AttnParams {
   float c;  // bf16: scale * log2(e); f32: scale
 };
 
+// V -> V^T in 32-key tiles, so that the P V product reads V with plain 16-byte LDS
+// reads: Vt[g][tile][d][pos] (bf16). Within a tile the keys are stored in the
+// k-slot order of the P fragments: key 16b + r (r < 16) sits at position
+// 16b + 8((r % 8) / 4) + 4(r / 8) + r % 4, so the 8 keys one lane feeds into an MFMA
+// (keys 16b + 4h + {0..3} and 16b + 8 + 4h + {0..3}) are 8 consecutive positions.
+// Keys at or past Nk (and gathered rows outside the cache) are zero. GATHER: key n
+// is row idx[n] of V.
+template <int DH, bool GATHER>
+__global__ __launch_bounds__(256) void vt_kernel(const __bf16* __restrict__ V,
+                                                 const int32_t* __restrict__ idx, int64_t src_rows,
+                                                 int Nk, int ntiles, __bf16* __restrict__ Vt) {
+  constexpr int CH = DH / 8;     // 16-byte chunks per V row
+  constexpr int SP = DH + 2;     // LDS pitch (elements) of the [key][d] staging tile
+  __shared__ __bf16 sm[32 * SP];
+  const int tile = blockIdx.x, g = blockIdx.y, tid = threadIdx.x;
+  const __bf16* Vg = V + (int64_t)g * src_rows * DH;
+  for (int c = tid; c < 32 * CH; c += 256) {
+    const int key = c / CH, col = (c % CH) * 8;
+    const int n = tile * 32 + key;
+    bf16x8 v = {};
+    if (n < Nk) {
+      const int64_t src = GATHER ? (int64_t)idx[n] : (int64_t)n;
+      if (src >= 0 && src < src_rows) v = load_bf16x8(Vg + src * DH + col);
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) sm[key * SP + col + e] = v[e];
+  }
+  __syncthreads();
+  __bf16* out = Vt + ((int64_t)g * ntiles + tile) * DH * 32;
+  for (int c = tid; c < DH * 4; c += 256) {
+    const int d = c / 4, q = c % 4;  // positions 8q .. 8q+7 of row d
+    bf16x8 v;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int key = 16 * (q / 2) + 8 * (e / 4) + 4 * (q % 2) + (e % 4);
+      v[e] = sm[key * SP + d];
+    }
+    *(u32x4*)(out + d * 32 + 8 * q) = __builtin_bit_cast(u32x4, v);
+  }
+}
+
 // SAFE = false (fast path): each row's exponent offset is fixed to the exact max of
 // its first key tile, so O is never rescaled and only MFMA touches it. A later tile
 // may exceed that offset by up to 2^kBig (P, l and O stay far from fp32 overflow);
@@ -67,17 +119,20 @@ struct AttnParams {
 // same stream): the lazy-rescale online softmax, run only for marked work items,
 // overwriting their outputs.
 template <int DH, bool GATHER, bool PSPLIT, bool PARTIAL, bool SAFE>
-__global__ __launch_bounds__(256, 1) void attn_bf16_kernel(AttnParams p) {
+__global__ __launch_bounds__(kThreadsBf16, 1) void attn_bf16_kernel(AttnParams p) {
   constexpr int KT = kKeyTile;
   constexpr int NKT = KT / 32;  // 32-key MFMA tiles per iteration
   constexpr int KP = DH + 8;   // K tile pitch (elements): conflict-free 16-byte row reads
-  constexpr int VP = DH + 16;  // V tile pitch: transposing reads hit distinct banks
+  constexpr int VTP = 40;      // V^T tile pitch (elements): 32 keys + 8, conflict-free 16-byte reads
   constexpr int NS = DH / 16;  // MFMA k-steps over head_dim
   constexpr int ND = DH / 32;  // 32-wide head_dim tiles of O
   constexpr int CH = DH / 8;   // 16-byte chunks per K/V row
-  constexpr int LPT = KT * CH / 256;
+  constexpr int QT = kQT;        // 32-row query tiles per wave
+  constexpr int NT = kThreadsBf16;
+  constexpr int NCH = KT * CH;             // 16-byte chunks per K tile (= per V^T tile)
+  constexpr int LPT = (NCH + NT - 1) / NT;  // chunks per thread
   __shared__ __attribute__((aligned(16))) __bf16 Ks[4][KT * KP];
-  __shared__ __attribute__((aligned(16))) __bf16 Vs[4][KT * VP];
+  __shared__ __attribute__((aligned(16))) __bf16 Vs[4][DH * VTP];
   __shared__ int overflow;
 
   // work-item coordinates are workgroup-uniform; readfirstlane keeps them (and the
@@ -100,12 +155,11 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_kernel(AttnParams p) {
   const int h32 = lane >> 5, l32 = lane & 31;
   const __bf16* Qb = (const __bf16*)p.Q;
   const __bf16* Kb = (const __bf16*)p.K + (int64_t)g * p.src_rows * DH;
-  const __bf16* Vb = (const __bf16*)p.V + (int64_t)g * p.src_rows * DH;
-  const int row_base = rt * kRowsWG + wid * 64;
+  const int row_base = rt * kRowsWG + wid * (32 * QT);
 
-  bf16x8 qf[2][NS];
+  bf16x8 qf[QT][NS];
 #pragma unroll
-  for (int qt = 0; qt < 2; ++qt) {
+  for (int qt = 0; qt < QT; ++qt) {
     const int r = min(row_base + qt * 32 + l32, p.rows - 1);
     const int m = r / p.G, j = r - m * p.G;
     const __bf16* qp = Qb + ((int64_t)m * p.Hq + g * p.G + j) * DH + h32 * 8;
@@ -120,73 +174,78 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_kernel(AttnParams p) {
   const uint32_t head_bytes = (uint32_t)(p.src_rows * DH * 2);
   const __amdgpu_buffer_rsrc_t krs =
       __builtin_amdgcn_make_buffer_rsrc((void*)Kb, 0, head_bytes, 0x00020000);
-  const __amdgpu_buffer_rsrc_t vrs =
-      __builtin_amdgcn_make_buffer_rsrc((void*)Vb, 0, head_bytes, 0x00020000);
+  const __bf16* Vtg = p.Vt + (int64_t)g * p.vt_tiles * DH * 32;
+  const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)Vtg, 0, (uint32_t)p.vt_tiles * (DH * 32 * 2), 0x00020000);
   const __amdgpu_buffer_rsrc_t irs =
       __builtin_amdgcn_make_buffer_rsrc((void*)p.idx, 0, (uint32_t)(p.Nk * 4), 0x00020000);
-  u32x4 kreg[2][LPT], vreg[2][LPT];
+  constexpr int NSET = kLoadSets;
+  u32x4 kreg[NSET][LPT], vreg[NSET][LPT];
   auto load_tile_to = [&](int tile, int set) {
     const int kb0 = k_begin + tile * KT;
 #pragma unroll
     for (int i = 0; i < LPT; ++i) {
-      const int c = i * 256 + tid;  // 16-byte chunk: row c / CH, column c % CH
+      const int c = i * NT + tid;  // 16-byte chunk: row c / CH, column c % CH
+      if (NCH % NT != 0 && c >= NCH) break;
       if constexpr (GATHER) {
         // entries past the index array read as 0; rows outside the cache read as 0
         const int src = (int)__builtin_amdgcn_raw_buffer_load_b32(irs, (kb0 + c / CH) * 4, 0, 0);
         const uint32_t off = (uint32_t)src * (DH * 2) + (c % CH) * 16;
         kreg[set][i] = __builtin_amdgcn_raw_buffer_load_b128(krs, off, 0, 0);
-        vreg[set][i] = __builtin_amdgcn_raw_buffer_load_b128(vrs, off, 0, 0);
       } else {
         const uint32_t soff = (uint32_t)kb0 * (DH * 2);
         kreg[set][i] = __builtin_amdgcn_raw_buffer_load_b128(krs, c * 16, soff, 0);
-        vreg[set][i] = __builtin_amdgcn_raw_buffer_load_b128(vrs, c * 16, soff, 0);
       }
+      // V^T tile kb0 / 32 (already gathered); tiles past the end read as 0
+      vreg[set][i] = __builtin_amdgcn_raw_buffer_load_b128(vrs, c * 16, (uint32_t)(kb0 / 32) * (DH * 64), 0);
     }
   };
   auto store_tile_from = [&](int buf, int set) {
 #pragma unroll
     for (int i = 0; i < LPT; ++i) {
-      const int c = i * 256 + tid;
+      const int c = i * NT + tid;
+      if (NCH % NT != 0 && c >= NCH) break;
       const int row = c / CH, col = c % CH;
       *(u32x4*)(&Ks[buf][row * KP + col * 8]) = kreg[set][i];
-      *(u32x4*)(&Vs[buf][row * VP + col * 8]) = vreg[set][i];
+      *(u32x4*)(&Vs[buf][(c / 4) * VTP + (c % 4) * 8]) = vreg[set][i];
     }
   };
   auto load_tile = [&](int tile) { load_tile_to(tile, 0); };
   auto store_tile = [&](int buf) { store_tile_from(buf, 0); };
 
-  f32x16 o[2][ND];
+  f32x16 o[QT][ND];
 #pragma unroll
-  for (int qt = 0; qt < 2; ++qt)
+  for (int qt = 0; qt < QT; ++qt)
 #pragma unroll
     for (int dt = 0; dt < ND; ++dt) o[qt][dt] = f32x16{};
-  float m_run[2] = {-INFINITY, -INFINITY};
-  float l_part[2] = {0.f, 0.f};
+  float m_run[QT], l_part[QT];
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt) {
+    m_run[qt] = -INFINITY;
+    l_part[qt] = 0.f;
+  }
   const float c = p.c;
 
-  // lane-dependent offsets of the transposing V reads (see lds_read_tr16)
-  const int tr_row = 4 * h32 + ((lane & 15) >> 2);
-  const int tr_col = ((lane >> 4) & 1) * 16 + 4 * (lane & 3);
 
   // S^T = K Q^T (+ init) for the tile in LDS slot `buf`
-  auto scores_init = [&](f32x16 (&s)[NKT][2], int buf, const f32x16 (&init)[NKT]) {
+  auto scores_init = [&](f32x16 (&s)[NKT][QT], int buf, const f32x16 (&init)[NKT]) {
     const __bf16* ks = Ks[buf];
 #pragma unroll
     for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
-      for (int qt = 0; qt < 2; ++qt) s[kt][qt] = init[kt];
+      for (int qt = 0; qt < QT; ++qt) s[kt][qt] = init[kt];
 #pragma unroll
     for (int st = 0; st < NS; ++st) {
 #pragma unroll
       for (int kt = 0; kt < NKT; ++kt) {
         const bf16x8 a = *(const bf16x8*)(ks + (kt * 32 + l32) * KP + st * 16 + h32 * 8);
 #pragma unroll
-        for (int qt = 0; qt < 2; ++qt) s[kt][qt] = mfma32(a, qf[qt][st], s[kt][qt]);
+        for (int qt = 0; qt < QT; ++qt) s[kt][qt] = mfma32(a, qf[qt][st], s[kt][qt]);
       }
     }
   };
   // keys >= k_end of tile t set to -inf
-  auto mask = [&](f32x16 (&s)[NKT][2], int t) {
+  auto mask = [&](f32x16 (&s)[NKT][QT], int t) {
     const int tb = k_begin + t * KT;
     if (tb + KT > k_end) {
 #pragma unroll
@@ -195,13 +254,13 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_kernel(AttnParams p) {
         for (int e = 0; e < 16; ++e) {
           const int key = tb + kt * 32 + 8 * (e >> 2) + 4 * h32 + (e & 3);
           if (key >= k_end) {
-            s[kt][0][e] = -INFINITY;
-            s[kt][1][e] = -INFINITY;
+#pragma unroll
+            for (int qt = 0; qt < QT; ++qt) s[kt][qt][e] = -INFINITY;
           }
         }
     }
   };
-  auto scores = [&](f32x16 (&s)[NKT][2], int buf, int t) {
+  auto scores = [&](f32x16 (&s)[NKT][QT], int buf, int t) {
     f32x16 zero[NKT];
 #pragma unroll
     for (int kt = 0; kt < NKT; ++kt) zero[kt] = f32x16{};
@@ -209,9 +268,9 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_kernel(AttnParams p) {
     mask(s, t);
   };
   // scaled row max of the tile (both halves of the 64-lane wave)
-  auto row_max = [&](f32x16 (&s)[NKT][2], float (&mt)[2]) {
+  auto row_max = [&](f32x16 (&s)[NKT][QT], float (&mt)[QT]) {
 #pragma unroll
-    for (int qt = 0; qt < 2; ++qt) {
+    for (int qt = 0; qt < QT; ++qt) {
       float mx = s[0][qt][0];
 #pragma unroll
       for (int e = 1; e < 16; ++e) mx = fmaxf(mx, s[0][qt][e]);
@@ -224,12 +283,12 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_kernel(AttnParams p) {
   };
   // P = exp2(S c - m_run) as bf16 MFMA operands (two-term split when PSPLIT). The row
   // sums add up the bf16 values the MFMA actually uses (v_dot2 with (1, 1)).
-  auto softmax = [&](f32x16 (&s)[NKT][2], bf16x8 (&pb)[NKT][2][2], bf16x8 (&pl)[NKT][2][2]) {
+  auto softmax = [&](f32x16 (&s)[NKT][QT], bf16x8 (&pb)[NKT][QT][2], bf16x8 (&pl)[NKT][QT][2]) {
     const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 #pragma unroll
     for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
-      for (int qt = 0; qt < 2; ++qt) {
+      for (int qt = 0; qt < QT; ++qt) {
         const float nm = -m_run[qt];
 #pragma unroll
         for (int e = 0; e < 16; ++e) s[kt][qt][e] = fast_exp2(fmaf(s[kt][qt][e], c, nm));
@@ -253,29 +312,28 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_kernel(AttnParams p) {
         l_part[qt] += sum0 + sum1;
       }
   };
-  // O^T += V^T P^T with V of LDS slot `buf`
-  auto pv = [&](bf16x8 (&pb)[NKT][2][2], bf16x8 (&pl)[NKT][2][2], int buf) {
+  // O^T += V^T P^T with the V^T tile of LDS slot `buf`: the A operand (32 rows of d,
+  // 8 keys) is one 16-byte read, in the P fragments' key order
+  auto pv = [&](bf16x8 (&pb)[NKT][QT][2], bf16x8 (&pl)[NKT][QT][2], int buf) {
     const __bf16* vs = Vs[buf];
 #pragma unroll
     for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
       for (int p2 = 0; p2 < 2; ++p2) {
-        const __bf16* vrow = vs + (kt * 32 + 16 * p2 + tr_row) * VP + tr_col;
 #pragma unroll
         for (int dt = 0; dt < ND; ++dt) {
-          const PKV_LDS __bf16* vp = (const PKV_LDS __bf16*)(vrow + dt * 32);
-          const bf16x8 a = cat8(lds_read_tr16(vp), lds_read_tr16(vp + 8 * VP));
+          const bf16x8 a = *(const bf16x8*)(vs + (dt * 32 + l32) * VTP + kt * 32 + 16 * p2 + 8 * h32);
 #pragma unroll
-          for (int qt = 0; qt < 2; ++qt) {
+          for (int qt = 0; qt < QT; ++qt) {
             o[qt][dt] = mfma32(a, pb[kt][qt][p2], o[qt][dt]);
             if constexpr (PSPLIT) o[qt][dt] = mfma32(a, pl[kt][qt][p2], o[qt][dt]);
           }
         }
       }
   };
-  auto accumulate = [&](f32x16 (&s)[NKT][2], int buf) {
-    bf16x8 pb[NKT][2][2];
-    bf16x8 pl[NKT][2][2];
+  auto accumulate = [&](f32x16 (&s)[NKT][QT], int buf) {
+    bf16x8 pb[NKT][QT][2];
+    bf16x8 pl[NKT][QT][2];
     softmax(s, pb, pl);
     pv(pb, pl, buf);
   };
@@ -285,47 +343,72 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_kernel(AttnParams p) {
   store_tile_from(0, 0);
 
   if constexpr (!SAFE) {
-    // Software pipeline over four LDS slots (tile t in slot t % 4). Step t:
-    //   issue the loads of tile t+3 (register set (t+1) % 2);
+    // Software pipeline over four LDS slots (tile t in slot t % 4) and NSET register
+    // staging sets (tile j is loaded into set j % NSET). Step t:
+    //   issue the loads of tile t + NSET + 1;
     //   MFMA S_{t+1} = K_{t+1} Q^T  while the VALU forms P_t from S_t;
     //   MFMA O += V_t P_t           while the VALU takes S_{t+1}'s row max;
-    //   store tile t+2 (loaded in step t-1) into its slot, last read in step t-2;
-    //   one barrier.
-    // The loop runs an even number of steps; tiles past the key range are fully
+    //   store tile t+2 (loaded in step t - NSET + 1) into its slot, last read in
+    //   step t-2; one barrier.
+    // A tile's loads thus have NSET - 1 whole steps to arrive: the workgroups of an
+    // XCD stream the same K/V rows at about the same time, so most loads wait for
+    // one shared miss and see close to the full memory latency.
+    // The loop runs a multiple of UNR steps; tiles past the key range are fully
     // masked (they contribute nothing), so every step has the same shape.
+    constexpr int UNR = NSET > 2 ? NSET : 2;
     load_tile_to(1, 0);
     store_tile_from(1, 0);
-    load_tile_to(2, 0);
+#pragma unroll
+    for (int j = 2; j <= NSET; ++j) load_tile_to(j, j % NSET);
     __syncthreads();
-    f32x16 sa[NKT][2], sb[NKT][2];
+    f32x16 sa[NKT][QT], sb[NKT][QT];
     scores(sa, 0, 0);
     {
-      float mt[2];
+      float mt[QT];
       row_max(sa, mt);
-      m_run[0] = mt[0];
-      m_run[1] = mt[1];
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt) m_run[qt] = mt[qt];
     }
     bool over = false;
-    auto step = [&](auto set_t, f32x16 (&sc)[NKT][2], f32x16 (&sn)[NKT][2], int t) {
-      constexpr int set_ld = decltype(set_t)::value;
-      load_tile_to(t + 3, set_ld);
-      scores(sn, (t + 1) & 3, t + 1);
-      bf16x8 pb[NKT][2][2];
-      bf16x8 pl[NKT][2][2];
+    // I: step index modulo UNR (compile time); MASKED: the tile scored in this step
+    // may reach past k_end
+    auto step = [&](auto i_t, auto masked_t, f32x16 (&sc)[NKT][QT], f32x16 (&sn)[NKT][QT], int t) {
+      constexpr int I = decltype(i_t)::value;
+      constexpr bool MASKED = decltype(masked_t)::value;
+      load_tile_to(t + NSET + 1, (I + NSET + 1) % NSET);
+      if constexpr (MASKED) {
+        scores(sn, (t + 1) & 3, t + 1);
+      } else {
+        f32x16 zero[NKT];
+#pragma unroll
+        for (int kt = 0; kt < NKT; ++kt) zero[kt] = f32x16{};
+        scores_init(sn, (t + 1) & 3, zero);
+      }
+      bf16x8 pb[NKT][QT][2];
+      bf16x8 pl[NKT][QT][2];
       softmax(sc, pb, pl);
       pv(pb, pl, t & 3);
-      float mt[2];
+      float mt[QT];
       row_max(sn, mt);
-      over |= mt[0] > m_run[0] + kBig || mt[1] > m_run[1] + kBig;
-      store_tile_from((t + 2) & 3, set_ld ^ 1);
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt) over |= mt[qt] > m_run[qt] + kBig;
+      store_tile_from((t + 2) & 3, (I + 2) % NSET);
       __syncthreads();
     };
-    using S0 = std::integral_constant<int, 0>;
-    using S1 = std::integral_constant<int, 1>;
-    for (int t = 0; t < ntiles; t += 2) {
-      step(S1{}, sa, sb, t);
-      step(S0{}, sb, sa, t + 1);
-    }
+    auto steps = [&](auto masked_t, int t) {
+      step(std::integral_constant<int, 0>{}, masked_t, sa, sb, t);
+      step(std::integral_constant<int, 1>{}, masked_t, sb, sa, t + 1);
+      if constexpr (UNR == 4) {
+        step(std::integral_constant<int, 2>{}, masked_t, sa, sb, t + 2);
+        step(std::integral_constant<int, 3>{}, masked_t, sb, sa, t + 3);
+      }
+    };
+    static_assert(UNR == 2 || UNR == 4, "pipeline unroll");
+    // tiles [0, t_full) lie entirely inside the key range; step t scores tile t+1
+    const int t_full = (k_end - k_begin) / KT;
+    int t = 0;
+    for (; t + UNR < t_full; t += UNR) steps(std::false_type{}, t);
+    for (; t < ntiles; t += UNR) steps(std::true_type{}, t);
     if (__ballot(over) != 0) overflow = 1;
     __syncthreads();
   } else {
@@ -335,14 +418,16 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_kernel(AttnParams p) {
     for (int t = 0; t < ntiles; ++t) {
       const int cur = t & 1;
       if (t + 1 < ntiles) load_tile(t + 1);
-      f32x16 s[NKT][2];
+      f32x16 s[NKT][QT];
       scores(s, cur, t);
-      float mt[2];
+      float mt[QT];
       row_max(s, mt);
-      const bool need = mt[0] > m_run[0] + kTau || mt[1] > m_run[1] + kTau;
+      bool need = false;
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt) need |= mt[qt] > m_run[qt] + kTau;
       if (__ballot(need) != 0) {
 #pragma unroll
-        for (int qt = 0; qt < 2; ++qt) {
+        for (int qt = 0; qt < QT; ++qt) {
           const float mn = fmaxf(m_run[qt], mt[qt]);
           const float alpha = fast_exp2(m_run[qt] - mn);
           m_run[qt] = mn;
@@ -358,7 +443,7 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_kernel(AttnParams p) {
   }
 
 #pragma unroll
-  for (int qt = 0; qt < 2; ++qt) {
+  for (int qt = 0; qt < QT; ++qt) {
     const float l = pair_sum(l_part[qt]);
     const int r = row_base + qt * 32 + l32;
     if (r >= p.rows) continue;
@@ -522,11 +607,12 @@ hipError_t launch_dh(const AttnShape& s, const AttnPlan& pl, AttnParams& p, bool
   const bool part = pl.n_split > 1;
   dim3 grid(pl.grid), block(256);
   if (s.bf16) {
+    const dim3 bblock(kThreadsBf16);
     // fast path, then the lazy-rescale fixup for any work item it handed back
 #define PKV_L(G_, P_, S_)                                                               \
   do {                                                                                  \
-    hipLaunchKernelGGL((attn_bf16_kernel<DH, G_, P_, S_, false>), grid, block, 0, st, p); \
-    hipLaunchKernelGGL((attn_bf16_kernel<DH, G_, P_, S_, true>), grid, block, 0, st, p);  \
+    hipLaunchKernelGGL((attn_bf16_kernel<DH, G_, P_, S_, false>), grid, bblock, 0, st, p); \
+    hipLaunchKernelGGL((attn_bf16_kernel<DH, G_, P_, S_, true>), grid, bblock, 0, st, p);  \
   } while (0)
     if (gather) {
       if (psplit) { if (part) PKV_L(true, true, true); else PKV_L(true, true, false); }
@@ -591,7 +677,10 @@ AttnPlan plan_attention(const AttnShape& s) {
                     ? align_up((size_t)s.Hkv * pl.n_split * rows * s.dh * sizeof(float)) +
                           align_up((size_t)s.Hkv * pl.n_split * rows * 2 * sizeof(float))
                     : 0;
-  if (s.bf16) pl.ws_bytes += align_up((size_t)pl.total_items * sizeof(int));
+  if (s.bf16) {
+    pl.ws_bytes += align_up((size_t)pl.total_items * sizeof(int));
+    pl.ws_bytes += align_up((size_t)s.Hkv * ntiles * 32 * s.dh * 2);  // V^T tiles
+  }
   return pl;
 }
 
@@ -613,7 +702,23 @@ hipError_t launch_attention(const AttnShape& s, const void* Q, const void* K, co
     p.ML = (float*)((char*)ws + off);
     off += align_up(n * 2 * sizeof(float));
   }
-  if (s.bf16) p.flags = (int*)((char*)ws + off);
+  const int64_t vt_tiles = (s.Nk + kKeyTile - 1) / kKeyTile;
+  if (s.bf16) {
+    p.flags = (int*)((char*)ws + off);
+    off += align_up((size_t)pl.total_items * sizeof(int));
+    __bf16* vt = (__bf16*)((char*)ws + off);
+    p.Vt = vt;
+    p.vt_tiles = (int)vt_tiles;
+    const dim3 vg((unsigned)vt_tiles, (unsigned)s.Hkv), vb(256);
+    const __bf16* Vb = (const __bf16*)V;
+#define PKV_VT(D_, G_) \
+  hipLaunchKernelGGL((vt_kernel<D_, G_>), vg, vb, 0, st, Vb, idx, src_rows, (int)s.Nk, (int)vt_tiles, vt)
+    if (s.dh == 128) { if (idx) PKV_VT(128, true); else PKV_VT(128, false); }
+    else { if (idx) PKV_VT(64, true); else PKV_VT(64, false); }
+#undef PKV_VT
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   p.Hq = s.Hq;
   p.G = s.Hq / s.Hkv;
   p.src_rows = src_rows;

@@ -21,11 +21,17 @@ bool al16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 
 int status_of(hipError_t e) { return e == hipSuccess ? PATCHKV_OK : PATCHKV_E_HIP; }
 
+// The bf16 kernels address one KV head's rows (and its V^T tiles) with 32-bit
+// buffer offsets: rows * dh * 2 bytes must stay below 2^32.
+bool src_rows_ok(int dtype, int64_t rows, int dh) {
+  return rows >= 1 && rows < kMaxRows && (dtype != PATCHKV_BF16 || rows * dh * 2 < ((int64_t)1 << 32));
+}
+
 int check_attn_shape(int dtype, int64_t M, int64_t Nk, int Hq, int Hkv, int dh) {
   if (dtype != PATCHKV_F32 && dtype != PATCHKV_BF16) return PATCHKV_E_DTYPE;
   if (M < 1 || Nk < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0) return PATCHKV_E_SHAPE;
-  if (M * Hq >= kMaxRows || Nk >= kMaxRows) return PATCHKV_E_SHAPE;
   if (dh != 64 && dh != 128) return PATCHKV_E_UNSUPPORTED;
+  if (M * Hq >= kMaxRows || !src_rows_ok(dtype, Nk, dh)) return PATCHKV_E_SHAPE;
   return PATCHKV_OK;
 }
 
@@ -130,7 +136,7 @@ int patchkv_attend_compressed(int dtype, const void* Q, const void* K, const voi
   if (!Q || !K || !V || !O) return PATCHKV_E_NULL;
   int s = check_attn_shape(dtype, M, B, Hq, Hkv, dh);
   if (s) return s;
-  if (idx && (N < 1 || N >= kMaxRows)) return PATCHKV_E_SHAPE;
+  if (idx && !src_rows_ok(dtype, N, dh)) return PATCHKV_E_SHAPE;
   if (!finite_pos(scale)) return PATCHKV_E_VALUE;
   if (!al16(Q) || !al16(K) || !al16(V) || !al16(O)) return PATCHKV_E_VALUE;
   const AttnShape sh = attn_shape(dtype, M, B, Hq, Hkv, dh);

@@ -41,8 +41,10 @@ def test_status_strings(L):
 
 
 def test_workspace_queries(L):
-    # bf16: one flag per work item (no split-key partials at this shape)
-    assert 0 < L.patchkv_attend_workspace_bytes(B.BF16, 4096, 172032, 32, 8, 128) <= 4096
+    # bf16: V^T tiles (Hkv x N x dh bf16) plus one flag per work item (no split-key
+    # partials at this shape)
+    vt = 8 * 172032 * 128 * 2
+    assert vt < L.patchkv_attend_workspace_bytes(B.BF16, 4096, 172032, 32, 8, 128) <= vt + 4096
     assert L.patchkv_attend_workspace_bytes(B.F32, 4096, 172032, 32, 8, 128) == 0
     assert L.patchkv_attend_workspace_bytes(B.BF16, 1024, 32768, 32, 8, 128) > 1 << 20  # split
     assert L.patchkv_attend_workspace_bytes(B.BF16, 10, 10, 3, 2, 128) == 0          # invalid
@@ -67,10 +69,13 @@ def test_attend_validation(L):
     assert attend(L, N=-1) == B.E_SHAPE
     assert attend(L, Hq=3, Hkv=2) == B.E_SHAPE
     assert attend(L, dh=96) == B.E_UNSUPPORTED
+    # bf16 rows of one KV head are addressed with 32-bit byte offsets
+    assert attend(L, N=1 << 24) == B.E_SHAPE                   # 2^24 * 128 * 2 = 2^32 bytes
+    assert attend(L, N=1 << 24, dh=64) == B.E_WORKSPACE        # 2^31 bytes: shape accepted
     assert attend(L, scale=0.0) == B.E_VALUE
     assert attend(L, scale=float("nan")) == B.E_VALUE
     assert attend(L, Q=FAKE + 2) == B.E_VALUE           # misaligned
-    # bf16 needs a workspace (flags, split-key partials), given none
+    # bf16 needs a workspace (V^T tiles, flags, split-key partials), given none
     assert attend(L, M=16, N=1 << 15, Hq=32, Hkv=8) == B.E_WORKSPACE
     assert attend(L) == B.E_WORKSPACE
     r = L.patchkv_attend_compressed(B.BF16, FAKE, FAKE, FAKE, FAKE, 8, 0, 16, 4, 2, 128, 0.1, FAKE,
