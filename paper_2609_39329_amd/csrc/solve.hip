@@ -654,6 +654,195 @@ __global__ __launch_bounds__(diag_threads<T>()) void potrf_inv_kernel(T* A, int6
   }
 }
 
+// ---- fp32 diagonal block, blocked: 4 x 4 sub-blocks of 32 ----------------------------
+//
+// The 128 x 128 block A (lower triangle read; zero-padded with an identity past bs)
+// and E = L^{-1} live in LDS. For each sub-block column k = 0..3:
+//   leaf (one wave):  A_kk = L_kk L_kk^T and X_kk = L_kk^{-1}, in registers;
+//   phase B:          L_ik = A_ik X_kk^T (i > k);  E_km = X_kk E_km (m < k);  E_kk = X_kk
+//   phase C:          A_ij -= L_ik L_jk^T (k < j <= i);  E_im -= L_ik E_km (i > k, m <= k)
+// i.e. right-looking blocked Cholesky with the forward substitution of the identity
+// carried along; phases B and C are independent 32 x 32 x 32 products on fp32 MFMA
+// (exact fp32 products), spread over the four waves, one barrier between phases.
+constexpr int PB = 130;  // LDS pitch (floats): lane-per-row reads hit 64 distinct banks
+
+// D = sgn * P Q' (+ C), 32 x 32 blocks in LDS (pitch PB); Q' = Q^T if QT else Q.
+// One wave; D may alias P, Q or C (every operand is read before D is written).
+template <bool QT>
+__device__ __forceinline__ void mm32(float* D, const float* P, const float* Q, const float* C, float sgn,
+                                     int lane) {
+  const int h = lane >> 5, l32 = lane & 31;
+  f32x16 acc;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) acc[e] = C ? C[(8 * (e >> 2) + 4 * h + (e & 3)) * PB + l32] : 0.f;
+#pragma unroll
+  for (int ks = 0; ks < 16; ++ks) {
+    const int k = 2 * ks + h;
+    const float a = sgn * P[l32 * PB + k];
+    const float b = QT ? Q[l32 * PB + k] : Q[k * PB + l32];
+    acc = mfma32_f32(a, b, acc);
+  }
+#pragma unroll
+  for (int e = 0; e < 16; ++e) D[(8 * (e >> 2) + 4 * h + (e & 3)) * PB + l32] = acc[e];
+}
+
+__device__ __forceinline__ float bcast(float x, int src_lane) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), src_lane));
+}
+
+// One wave: factor the SPD 32 x 32 block S (lower triangle read) and write
+// X = L^{-1} (lower, zeros above) to Xo.
+//  1. Right-looking factorisation: lane r (and its twin r + 32, which repeats the
+//     same work so the wave never diverges) holds row r of the trailing matrix;
+//     step j reads the pivot and column j through scalar registers (readlane).
+//     L overwrites S. A pivot that is not positive (or NaN) makes its L_jj, and
+//     every later one, NaN: the first NaN on the diagonal is the failing column.
+//  2. Column-parallel inverse: lane c solves L x = e_c by forward substitution,
+//     x_r = (delta_rc - sum_{m<r} L_rm x_m) / L_rr, reading L with broadcast LDS
+//     reads (the same address in every lane), no cross-lane traffic.
+__device__ __forceinline__ void leaf32(float* S, float* Xo, int lane, int col0, int bs, int32_t* info,
+                                       bool& failed) {
+  int r = lane & 31;
+  // opaque per call: keeps the per-step lane comparisons inside the call instead of
+  // hoisting them into scalar registers for the whole kernel
+  asm volatile("" : "+v"(r));
+  float v[32];
+#pragma unroll
+  for (int c = 0; c < 32; ++c) v[c] = S[r * PB + c];
+#pragma unroll
+  for (int j = 0; j < 32; ++j) {
+    const float rs = __builtin_amdgcn_rsqf(bcast(v[j], j));
+    const float u = v[j] * (rs * rs);  // A[r][j] / p
+    // in chunks of 8 broadcasts: the scheduler would otherwise hoist all of them and
+    // run out of scalar registers
+#pragma unroll
+    for (int c0 = j + 1; c0 < 32; c0 += 8) {
+#pragma unroll
+      for (int c = c0; c < c0 + 8 && c < 32; ++c) v[c] = fmaf(-u, bcast(v[j], c), v[c]);  // A[c][j]
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    v[j] *= rs;
+  }
+  // first failing pivot of this block (padding pivots past bs are 1)
+  float diag = 0.f;
+#pragma unroll
+  for (int c = 0; c < 32; ++c)
+    if (c == r) diag = v[c];
+  const uint64_t bad = __ballot(lane < 32 && col0 + r < bs && !(diag > 0.f));
+  if (bad != 0 && !failed) {
+    failed = true;
+    if (lane == 0 && *info == 0) *info = col0 + __builtin_ctzll(bad) + 1;
+  }
+  if (lane < 32) {
+#pragma unroll
+    for (int c = 0; c < 32; ++c) S[r * PB + c] = v[c];  // row r of L (upper part unused)
+  }
+  // (single wave: its LDS operations complete in program order)
+  float x[32];
+#pragma unroll
+  for (int i = 0; i < 32; ++i) {
+    float acc = i == r ? 1.f : 0.f;
+    const float* Li = S + i * PB;
+#pragma unroll
+    for (int m = 0; m < i; m += 4) {
+      const f32x4 l4 = *(const f32x4*)(Li + m);
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+        if (m + t < i) acc = fmaf(-l4[t], x[m + t], acc);
+    }
+    x[i] = acc * __builtin_amdgcn_rcpf(Li[i]);
+  }
+  if (lane < 32) {
+#pragma unroll
+    for (int i = 0; i < 32; ++i) Xo[i * PB + r] = x[i];  // column r of X (zeros above)
+  }
+}
+
+__global__ __launch_bounds__(256) void potrf128_kernel(float* A, int64_t lda, int kb, int bs,
+                                                       int32_t* info) {
+  __shared__ float As[128 * PB];
+  __shared__ float Es[128 * PB];
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  // 16-byte accesses when every row start is 16-byte aligned (kb is a multiple of 128)
+  const bool vec = (lda & 3) == 0 && (((uintptr_t)A) & 15) == 0;
+  const float* Ab = A + (int64_t)kb * lda + kb;
+#pragma unroll
+  for (int u = 0; u < 16; ++u) {
+    const int e = (u * 256 + tid) * 4;  // 4 consecutive columns of one row
+    const int i = e >> 7, j0 = e & 127;
+    f32x4 v = {};
+    const float* src = Ab + (int64_t)i * lda + j0;
+    if (i < bs && vec && j0 + 3 < bs) {
+      v = *(const f32x4*)src;
+    } else if (i < bs) {
+      for (int t = 0; t < 4; ++t) v[t] = j0 + t < bs ? src[t] : 0.f;
+    }
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int j = j0 + t;
+      float x = j <= i ? v[t] : 0.f;  // lower triangle only
+      if (i >= bs || j >= bs) x = i == j ? 1.f : 0.f;
+      As[i * PB + j] = x;
+      Es[i * PB + j] = 0.f;
+    }
+  }
+  __syncthreads();
+  auto blk = [](float* base, int i, int j) { return base + (32 * i) * PB + 32 * j; };
+  bool failed = false;
+  for (int k = 0; k < 4; ++k) {
+    if (wid == 0) leaf32(blk(As, k, k), blk(Es, k, k), lane, kb + 32 * k, kb + bs, info, failed);
+    __syncthreads();
+    // phase B: (3 - k) panel products, k products of the identity's row block k
+    for (int q = wid; q < 3; q += 4) {
+      if (q < 3 - k) {
+        const int i = k + 1 + q;
+        mm32<true>(blk(As, i, k), blk(As, i, k), blk(Es, k, k), nullptr, 1.f, lane);
+      } else {
+        const int m = q - (3 - k);
+        mm32<false>(blk(Es, k, m), blk(Es, k, k), blk(Es, k, m), nullptr, 1.f, lane);
+      }
+    }
+    __syncthreads();
+    // phase C: trailing lower blocks (k < j <= i), then E_im for i > k, m <= k
+    const int ntr = (3 - k) * (4 - k) / 2;
+    const int njobs = ntr + (3 - k) * (k + 1);
+    for (int q = wid; q < njobs; q += 4) {
+      if (q < ntr) {
+        int i = k + 1, t = q;
+        while (t > i - k - 1) {  // row i holds i - k blocks (j = k+1..i)
+          t -= i - k;
+          ++i;
+        }
+        const int j = k + 1 + t;
+        mm32<true>(blk(As, i, j), blk(As, i, k), blk(As, j, k), blk(As, i, j), -1.f, lane);
+      } else {
+        const int t = q - ntr;
+        const int i = k + 1 + t / (k + 1), m = t % (k + 1);
+        mm32<false>(blk(Es, i, m), blk(As, i, k), blk(Es, k, m), blk(Es, i, m), -1.f, lane);
+      }
+    }
+    __syncthreads();
+  }
+  float* Ad = A + (int64_t)kb * lda + kb;
+  // recompute the store's bounds masks here rather than keep the load's alive
+  int tid2 = tid;
+  asm volatile("" : "+v"(tid2));
+#pragma unroll
+  for (int u = 0; u < 16; ++u) {
+    const int e = (u * 256 + tid2) * 4;
+    const int i = e >> 7, j0 = e & 127;
+    if (i >= bs) continue;
+    f32x4 v;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) v[t] = j0 + t <= i ? Es[i * PB + j0 + t] : 0.f;
+    float* dst = Ad + (int64_t)i * lda + j0;
+    if (vec && j0 + 3 < bs) *(f32x4*)dst = v;
+    else
+      for (int t = 0; t < 4; ++t)
+        if (j0 + t < bs) dst[t] = v[t];
+  }
+}
+
 // A = G + lambda I (full copy), R = C, info = 0.
 template <class T>
 __global__ __launch_bounds__(256) void init_kernel(const T* __restrict__ G, const T* __restrict__ C,
@@ -890,8 +1079,11 @@ hipError_t solve_t(const T* G, const T* C, int64_t d64, int64_t dout64, double l
   for (int k = 0; k < nblk; ++k) {
     const int kb = k * NB, bs = std::min(NB, d - kb);
     const int rest = d - kb - bs;
-    hipLaunchKernelGGL((potrf_inv_kernel<T>), dim3(1), dim3(diag_threads<T>()), 0, st, A, d64, kb,
-                       bs, info);
+    if constexpr (sizeof(T) == 4)
+      hipLaunchKernelGGL(potrf128_kernel, dim3(1), dim3(256), 0, st, A, d64, kb, bs, info);
+    else
+      hipLaunchKernelGGL((potrf_inv_kernel<T>), dim3(1), dim3(diag_threads<T>()), 0, st, A, d64, kb,
+                         bs, info);
     PKV_TRY(hipGetLastError());
     const T* Linv = A + (int64_t)kb * d + kb;  // Linv(i,t) = Linv[i*d + t]
     {
