@@ -81,9 +81,14 @@ LayerWs layer_ws(int dtype, int acc, int64_t M, int64_t N, int64_t B, int Hq, in
   L.T = o; o += align_up(accb * M * d);
   L.G = o; o += align_up(accb * d * d);
   L.C = o; o += align_up(accb * d * d);
+  // scratch shared by the two attention passes, then by the targets and statistics
+  // pre-passes (all ordered on one stream)
   L.attn = o;
-  o += align_up(std::max(plan_attention(attn_shape(dtype, M, N, Hq, Hkv, dh)).ws_bytes,
-                         plan_attention(attn_shape(dtype, M, B, Hq, Hkv, dh)).ws_bytes));
+  size_t scratch = std::max(plan_attention(attn_shape(dtype, M, N, Hq, Hkv, dh)).ws_bytes,
+                            plan_attention(attn_shape(dtype, M, B, Hq, Hkv, dh)).ws_bytes);
+  if (acc == PATCHKV_F32)
+    scratch = std::max({scratch, targets_ws_bytes(M, d, d), normal_eq_ws_bytes(M, d, d)});
+  o += align_up(scratch);
   L.solve = o; o += align_up(solve_ws_bytes(acc == PATCHKV_F64, d, d));
   L.total = o;
   return L;
@@ -148,7 +153,8 @@ int patchkv_attend_compressed(int dtype, const void* Q, const void* K, const voi
 }
 
 size_t patchkv_targets_workspace_bytes(int w_dtype, int64_t M, int64_t d_in, int64_t d_out) {
-  (void)w_dtype;
+  if (w_dtype != PATCHKV_BF16 && w_dtype != PATCHKV_F32) return 0;
+  if (check_stats_dims(M, d_in, d_out)) return 0;
   return targets_ws_bytes(M, d_in, d_out);
 }
 
@@ -169,8 +175,9 @@ int patchkv_compute_targets(int w_dtype, const float* Of, const float* Oc, const
 
 size_t patchkv_normal_eq_workspace_bytes(int acc_dtype, int64_t rows, int64_t d_in,
                                          int64_t d_out) {
-  (void)acc_dtype;
-  return normal_eq_ws_bytes(rows, d_in, d_out);
+  if (acc_dtype != PATCHKV_F32 && acc_dtype != PATCHKV_F64) return 0;
+  if (check_stats_dims(rows, d_in, d_out)) return 0;
+  return acc_dtype == PATCHKV_F32 ? normal_eq_ws_bytes(rows, d_in, d_out) : 0;
 }
 
 int patchkv_accumulate_normal_eq(int acc_dtype, const float* Xc, const float* Yf, const float* Yc,
@@ -182,7 +189,8 @@ int patchkv_accumulate_normal_eq(int acc_dtype, const float* Xc, const float* Yf
   int s = check_stats_dims(rows, d_in, d_out);
   if (s) return s;
   if (accumulate != 0 && accumulate != 1) return PATCHKV_E_VALUE;
-  s = check_ws(workspace, workspace_bytes, normal_eq_ws_bytes(rows, d_in, d_out));
+  s = check_ws(workspace, workspace_bytes,
+               acc_dtype == PATCHKV_F32 ? normal_eq_ws_bytes(rows, d_in, d_out) : 0);
   if (s) return s;
   hipStream_t st = (hipStream_t)stream;
   if (acc_dtype == PATCHKV_F32)
@@ -268,10 +276,10 @@ int patchkv_compute_layer_patch(int dtype, int acc_dtype, const void* Q, const v
   if (e != hipSuccess) return PATCHKV_E_HIP;
   const bool wbf = dtype == PATCHKV_BF16;
   if (acc_dtype == PATCHKV_F32) {
-    e = launch_targets(Of, Oc, W, wbf, M, d, d, rho, (float*)T, nullptr, st);
+    e = launch_targets(Of, Oc, W, wbf, M, d, d, rho, (float*)T, wa, st);
     if (e == hipSuccess)
       e = launch_normal_eq_f32(Oc, (const float*)T, nullptr, M, d, d, false, (float*)G, (float*)C,
-                               nullptr, st);
+                               wa, st);
   } else {
     e = launch_targets_f64(Of, Oc, W, wbf, M, d, d, rho, (double*)T, st);
     if (e == hipSuccess)

@@ -2,20 +2,7 @@
 //   T = (O_f - O_c) W + rho (O_f - O_c)
 //   G (+)= X^T X,   C (+)= X^T (Yf - Yc)
 //
-// fp32-accumulate path (split_gemm_kernel): gfx950 has no fp32-input MFMA faster
-// than 157 TFLOP/s and no xf32 mode, so every fp32 operand x is split into
-// x_hi = bf16(x) and x_lo = bf16(x - x_hi) while it is staged from HBM into LDS,
-// and the product is formed on bf16 MFMA 32x32x16 with fp32 accumulation:
-//   x y ~ x_hi y_hi + x_hi y_lo + x_lo y_hi (+ x_lo y_lo for the Gram matrix).
-// Dropping x_lo y_lo in G would subtract a PSD matrix L^T L whose diagonal grows
-// with the number of rows (a systematic shift of the ridge), so G keeps all four
-// products; C keeps three (its lo x lo cross term has no such bias). A bf16
-// operand (W) has no low part. Operands whose contraction index is contiguous
-// in memory are stored [i][k] in LDS and read with 16-byte reads; operands whose
-// output index is contiguous (X^T for the Gram, W for the targets) are stored
-// [k][i] and read with the LDS transpose instruction. G is computed on the upper
-// block triangle only and mirrored.
-//
+// fp32-accumulate path: split pre-passes + bgemm_kernel (bf16 MFMA, fp32 accumulation).
 // fp64-accumulate path (f64_gemm_kernel): plain fp64 FMA tiles through LDS.
 #include "common.hpp"
 #include "kernels.hpp"
@@ -24,47 +11,156 @@ namespace pkv {
 
 namespace {
 
-constexpr int BM = 128, BN = 128, KC = 32;
+// ---------------------------------------------------------------- fp32 path
+//
+// Every fp32 operand x is first split, once, into x_hi = bf16(x) and
+// x_lo = bf16(x - x_hi) by a memory-bound pre-pass that also lays it out with the
+// contraction index contiguous and zero-pads both dimensions (rows to 128, the
+// contraction to 64). The products then run on one bf16 MFMA GEMM kernel that sums
+// several (A_t, B_t) term pairs with fp32 accumulation:
+//   x y ~ x_hi y_hi + x_hi y_lo + x_lo y_hi (+ x_lo y_lo for the Gram matrix).
+// Dropping x_lo y_lo in G would subtract a PSD matrix L^T L whose diagonal grows
+// with the number of rows (a systematic shift of the ridge), so G keeps all four
+// products; C keeps three (its lo x lo cross term has no such bias). A bf16 operand
+// (W) has no low part.
 
-struct SplitParams {
-  const float* A1;   // A(i,k) = A1 - A2 (A2 may be null)
-  const float* A2;
-  int64_t lda;
-  const void* B1;    // B(j,k) = B1 - B2 (B2 may be null; B1 float or bf16)
-  const float* B2;
-  int64_t ldb;
+constexpr int G_BM = 256, G_KC = 64;  // row and contraction padding of the split planes
+
+inline int64_t pad_to(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+// dst[r][c] (r < rows_p, c < cols_p), hi and lo planes, = split(S1 - S2)[r][c] inside
+// rows x cols, zero outside. One thread per 8 consecutive columns.
+__global__ __launch_bounds__(256) void split_rows_kernel(const float* __restrict__ S1,
+                                                         const float* __restrict__ S2, int rows,
+                                                         int cols, int64_t ld, __bf16* __restrict__ hi,
+                                                         __bf16* __restrict__ lo, int rows_p,
+                                                         int cols_p) {
+  const int64_t g = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int per_row = cols_p / 8;
+  if (g >= (int64_t)rows_p * per_row) return;
+  const int r = (int)(g / per_row), c0 = (int)(g % per_row) * 8;
+  float v[8];
+  const bool vec = (ld & 3) == 0 && (((uintptr_t)S1 | (uintptr_t)S2) & 15) == 0;
+  if (r < rows && c0 + 7 < cols && vec) {
+    const f32x4* p1 = (const f32x4*)(S1 + (int64_t)r * ld + c0);
+    f32x4 a = p1[0], b = p1[1];
+    if (S2) {
+      const f32x4* p2 = (const f32x4*)(S2 + (int64_t)r * ld + c0);
+      a -= p2[0];
+      b -= p2[1];
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      v[e] = a[e];
+      v[4 + e] = b[e];
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int c = c0 + e;
+      v[e] = (r < rows && c < cols)
+                 ? S1[(int64_t)r * ld + c] - (S2 ? S2[(int64_t)r * ld + c] : 0.f)
+                 : 0.f;
+    }
+  }
+  bf16x8 h, l;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    h[e] = to_bf16(v[e]);
+    l[e] = to_bf16(v[e] - (float)h[e]);
+  }
+  const int64_t o = (int64_t)r * cols_p + c0;
+  *(bf16x8*)(hi + o) = h;
+  *(bf16x8*)(lo + o) = l;
+}
+
+// dst[c][r] (c < cols_p, r < rows_p) = split(S1 - S2)[r][c] inside rows x cols, zero
+// outside: the transpose, through a 64 x 64 LDS tile. SRC float (hi and lo planes,
+// lo may be null for a bf16 source) or bf16 (hi plane only).
+template <class SRC>
+__global__ __launch_bounds__(256) void split_transpose_kernel(const SRC* __restrict__ S1,
+                                                              const float* __restrict__ S2, int rows,
+                                                              int cols, int64_t ld,
+                                                              __bf16* __restrict__ hi,
+                                                              __bf16* __restrict__ lo, int rows_p,
+                                                              int cols_p) {
+  __shared__ float tile[64][65];
+  const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int u = 0; u < 16; ++u) {
+    const int e = u * 256 + tid;
+    const int rr = e / 64, cc = e % 64;
+    const int r = r0 + rr, c = c0 + cc;
+    float v = 0.f;
+    if (r < rows && c < cols) {
+      v = (float)S1[(int64_t)r * ld + c];
+      if (S2) v -= S2[(int64_t)r * ld + c];
+    }
+    tile[rr][cc] = v;
+  }
+  __syncthreads();
+  // write rows c of dst: 64 consecutive r as 8 chunks of 8 bf16
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int e = u * 256 + tid;
+    const int cc = e / 8, rr0 = (e % 8) * 8;
+    const int c = c0 + cc;
+    if (c >= cols_p || r0 + rr0 >= rows_p) continue;
+    bf16x8 h, l;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      const float v = tile[rr0 + t][cc];
+      h[t] = to_bf16(v);
+      l[t] = to_bf16(v - (float)h[t]);
+    }
+    const int64_t o = (int64_t)c * rows_p + r0 + rr0;
+    *(bf16x8*)(hi + o) = h;
+    if (lo) *(bf16x8*)(lo + o) = l;
+  }
+}
+
+// Out[i][j] (+)= sum_t sum_k A_{a(t)}[i][k] B_{b(t)}[j][k] (+ rho (E1 - E2)[i][j]).
+// The operands are up to two bf16 planes per side (hi, lo), each [rows_p][Kp] with
+// the contraction index contiguous and zero padding (rows_p multiple of the tile,
+// Kp of 64), so the main loop has no bounds checks. Each K chunk loads every plane
+// once and applies all term products to it: term t multiplies plane a(t) = bit t of
+// TA with plane b(t) = bit t of TB. 256 x 256 tiles, 8 waves of 128 x 64, two LDS
+// stages with the next chunk prefetched into registers. The MFMA computes the
+// transposed tile (rows = output columns), so a lane owns 4 consecutive output
+// columns and the epilogue uses 16-byte accesses. SYM: only tiles with
+// tile_i <= tile_j; the diagonal tiles keep their i <= j half and every tile is
+// mirrored, so the result is exactly symmetric.
+struct BGemm {
+  const __bf16* A[2];  // planes of A [Ip][Kp]
+  const __bf16* B[2];  // planes of B [Jp][Kp]
+  int64_t ld;          // Kp
   float* Out;
   int64_t ldo;
-  const float* E1;   // epilogue: + rho (E1 - E2)[i][j]
+  const float* E1;
   const float* E2;
   int64_t lde;
   float rho;
-  int I, J, K;
+  int I, J, Kp;
   int accumulate;
-  int tiles_j;
-  int ntiles;
-  bool vecA, vecB;   // 16-byte loads allowed (strides and bases aligned)
+  int tiles_j, ntiles;
+  int vec_out;
 };
 
-// AK: A(i,k) at A[i*lda + k] (else A[k*lda + i]); BK likewise for B(j,k).
-template <bool AK, bool BK, bool B_BF16, bool SYM, int NTERMS>
-__global__ __launch_bounds__(256, 1) void split_gemm_kernel(SplitParams p) {
-  // LDS tiles, hi and lo parts. [i][k] layout pitch KC+8, [k][i] layout pitch BM+16.
-  constexpr int PA = AK ? (KC + 8) : (BM + 16);
-  constexpr int PB = BK ? (KC + 8) : (BN + 16);
-  constexpr int SA = AK ? BM * PA : KC * PA;
-  constexpr int SB = BK ? BN * PB : KC * PB;
-  __shared__ __attribute__((aligned(16))) __bf16 Ah[SA];
-  __shared__ __attribute__((aligned(16))) __bf16 Al[SA];
-  __shared__ __attribute__((aligned(16))) __bf16 Bh[SB];
-  __shared__ __attribute__((aligned(16))) __bf16 Bl[B_BF16 ? 8 : SB];
+constexpr int BG_T = 256, BG_WM = 128, BG_WN = 64, BG_KC = 32, BG_PK = BG_KC + 8;
+constexpr int BG_THREADS = (BG_T / BG_WM) * (BG_T / BG_WN) * 64;  // 512
 
+template <int NA, int NB, int NT, int TA, int TB, bool SYM>
+__global__ __launch_bounds__(BG_THREADS, 1) void bgemm_kernel(BGemm p) {
+  constexpr int ROWS = (NA + NB) * BG_T;            // stacked plane rows per stage
+  constexpr int LPT = ROWS * (BG_KC / 8) / BG_THREADS;  // 16-byte loads per thread
+  constexpr int MA = BG_WM / 32, MB = BG_WN / 32;
+  __shared__ __attribute__((aligned(16))) __bf16 lds[2][ROWS * BG_PK];
   int ti, tj;
   {
     const int t = xcd_item((p.ntiles + kXcds - 1) / kXcds);
     if (t >= p.ntiles) return;
     if constexpr (SYM) {
-      // upper block triangle, row-major enumeration
       int r = 0, rem = t;
       while (rem >= p.tiles_j - r) {
         rem -= p.tiles_j - r;
@@ -77,185 +173,169 @@ __global__ __launch_bounds__(256, 1) void split_gemm_kernel(SplitParams p) {
       tj = t % p.tiles_j;
     }
   }
-  const int i0 = ti * BM, j0 = tj * BN;
+  const int i0 = ti * BG_T, j0 = tj * BG_T;
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int h32 = lane >> 5, l32 = lane & 31;
-  const int wi = (wid >> 1) * 64, wj = (wid & 1) * 64;
+  const int wi = (wid / (BG_T / BG_WN)) * BG_WM, wj = (wid % (BG_T / BG_WN)) * BG_WN;
+  const int nq = p.Kp / BG_KC;
 
-  f32x16 acc[2][2];
+  f32x16 acc[MA][MB];
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < MA; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
+    for (int b = 0; b < MB; ++b) acc[a][b] = f32x16{};
 
-  // staging registers: A and B tiles of 128 x 32 floats (4 float4 per thread).
-  // The 4 (or 8) elements one thread loads are contiguous in memory.
-  f32x4 ra[4], rb[4];
-  u32x4 rbw[2];
-  auto ld4 = [](const float* s1, const float* s2, int nvalid, bool vec) -> f32x4 {
-    f32x4 v = {};
-    if (nvalid >= 4 && vec) {
-      v = *(const f32x4*)s1;
-      if (s2) v -= *(const f32x4*)s2;
-    } else {
+  // piece c: stacked row c / 4 (plane (row / 256), row % 256 within it), k (c % 4) * 8
+  u32x4 rg[LPT];
+  auto fetch = [&](int q) {
+    const int k0 = q * BG_KC;
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
-        if (e < nvalid) v[e] = s1[e] - (s2 ? s2[e] : 0.f);
-    }
-    return v;
-  };
-  auto fetch = [&](int k0) {
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int c = u * 256 + tid;
-      int i, k;
-      if constexpr (AK) { i = c / (KC / 4); k = (c % (KC / 4)) * 4; }
-      else { k = c / (BM / 4); i = (c % (BM / 4)) * 4; }
-      const int gi = i0 + i, gk = k0 + k;
-      const int64_t off = AK ? (int64_t)gi * p.lda + gk : (int64_t)gk * p.lda + gi;
-      const int nvalid = AK ? (gi < p.I ? p.K - gk : 0) : (gk < p.K ? p.I - gi : 0);
-      ra[u] = nvalid > 0 ? ld4(p.A1 + off, p.A2 ? p.A2 + off : nullptr, nvalid, p.vecA)
-                         : f32x4{};
-    }
-    if constexpr (B_BF16) {
-      // B(j,k) = W[k][j], bf16, [k][j] layout: 32 x 128 bf16 = 512 chunks of 16 B
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const int c = u * 256 + tid;
-        const int k = c / (BN / 8), j = (c % (BN / 8)) * 8;
-        const int gk = k0 + k, gj = j0 + j;
-        const int nvalid = gk < p.K ? p.J - gj : 0;
-        u32x4 v = {};
-        if (nvalid > 0) {
-          const __bf16* s = (const __bf16*)p.B1 + (int64_t)gk * p.ldb + gj;
-          if (nvalid >= 8 && p.vecB) {
-            v = *(const u32x4*)s;
-          } else {
-            bf16x8 t8 = __builtin_bit_cast(bf16x8, v);
-#pragma unroll
-            for (int e = 0; e < 8; ++e)
-              if (e < nvalid) t8[e] = s[e];
-            v = __builtin_bit_cast(u32x4, t8);
-          }
-        }
-        rbw[u] = v;
-      }
-    } else {
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int c = u * 256 + tid;
-        int j, k;
-        if constexpr (BK) { j = c / (KC / 4); k = (c % (KC / 4)) * 4; }
-        else { k = c / (BN / 4); j = (c % (BN / 4)) * 4; }
-        const int gj = j0 + j, gk = k0 + k;
-        const int64_t off = BK ? (int64_t)gj * p.ldb + gk : (int64_t)gk * p.ldb + gj;
-        const int nvalid = BK ? (gj < p.J ? p.K - gk : 0) : (gk < p.K ? p.J - gj : 0);
-        rb[u] = nvalid > 0 ? ld4((const float*)p.B1 + off, p.B2 ? p.B2 + off : nullptr, nvalid,
-                                 p.vecB)
-                           : f32x4{};
-      }
+    for (int u = 0; u < LPT; ++u) {
+      const int c = u * BG_THREADS + tid;
+      const int row = c >> 2, kk = (c & 3) * 8;
+      const int pl = row / BG_T, rr = row % BG_T;  // pl is uniform per u
+      const __bf16* src = pl < NA ? p.A[pl] + (int64_t)(i0 + rr) * p.ld
+                                  : p.B[pl - NA] + (int64_t)(j0 + rr) * p.ld;
+      rg[u] = *(const u32x4*)(src + k0 + kk);
     }
   };
-  auto split_store = [&](__bf16* hi, __bf16* lo, int off, f32x4 v) {
-    bf16x4 h, l;
+  auto stash = [&](int buf) {
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      h[e] = to_bf16(v[e]);
-      l[e] = to_bf16(v[e] - (float)h[e]);
+    for (int u = 0; u < LPT; ++u) {
+      const int c = u * BG_THREADS + tid;
+      const int row = c >> 2, kk = (c & 3) * 8;
+      *(u32x4*)(&lds[buf][row * BG_PK + kk]) = rg[u];
     }
-    *(bf16x4*)(hi + off) = h;
-    *(bf16x4*)(lo + off) = l;
-  };
-  auto stash = [&]() {
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int c = u * 256 + tid;
-      if constexpr (AK) split_store(Ah, Al, (c / (KC / 4)) * PA + (c % (KC / 4)) * 4, ra[u]);
-      else split_store(Ah, Al, (c / (BM / 4)) * PA + (c % (BM / 4)) * 4, ra[u]);
-    }
-    if constexpr (B_BF16) {
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const int c = u * 256 + tid;
-        *(u32x4*)(Bh + (c / (BN / 8)) * PB + (c % (BN / 8)) * 8) = rbw[u];
-      }
-    } else {
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int c = u * 256 + tid;
-        if constexpr (BK) split_store(Bh, Bl, (c / (KC / 4)) * PB + (c % (KC / 4)) * 4, rb[u]);
-        else split_store(Bh, Bl, (c / (BN / 4)) * PB + (c % (BN / 4)) * 4, rb[u]);
-      }
-    }
-  };
-
-  // operand fragment (32 rows x 16 k) at row offset r0 and k offset k0 of an LDS tile
-  const int tr_k = 8 * h32 + ((lane & 15) >> 2);
-  const int tr_i = ((lane >> 4) & 1) * 16 + 4 * (lane & 3);
-  auto frag = [&](const __bf16* base, int pitch, bool kcontig, int r0, int k0) -> bf16x8 {
-    if (kcontig) return *(const bf16x8*)(base + (r0 + l32) * pitch + k0 + h32 * 8);
-    const PKV_LDS __bf16* q = (const PKV_LDS __bf16*)(base + (k0 + tr_k) * pitch + r0 + tr_i);
-    return cat8(lds_read_tr16(q), lds_read_tr16(q + 4 * pitch));
   };
 
   fetch(0);
-  for (int k0 = 0; k0 < p.K; k0 += KC) {
-    __syncthreads();
-    stash();
-    __syncthreads();
-    if (k0 + KC < p.K) fetch(k0 + KC);
+  stash(0);
+  __syncthreads();
+  for (int q = 0; q < nq; ++q) {
+    const int buf = q & 1;
+    if (q + 1 < nq) fetch(q + 1);
+    const __bf16* L0 = lds[buf];
 #pragma unroll
-    for (int ks = 0; ks < KC; ks += 16) {
-      bf16x8 ah[2], al[2], bh[2], bl[2];
+    for (int ks = 0; ks < BG_KC; ks += 16) {
+      bf16x8 fa[NA][MA], fb[NB][MB];
 #pragma unroll
-      for (int a = 0; a < 2; ++a) {
-        ah[a] = frag(Ah, PA, AK, wi + 32 * a, ks);
-        al[a] = frag(Al, PA, AK, wi + 32 * a, ks);
-      }
+      for (int pa = 0; pa < NA; ++pa)
 #pragma unroll
-      for (int b = 0; b < 2; ++b) {
-        bh[b] = frag(Bh, PB, BK, wj + 32 * b, ks);
-        if constexpr (!B_BF16) bl[b] = frag(Bl, PB, BK, wj + 32 * b, ks);
-      }
+        for (int a = 0; a < MA; ++a)
+          fa[pa][a] = *(const bf16x8*)(L0 + (pa * BG_T + wi + 32 * a + l32) * BG_PK + ks + 8 * h32);
 #pragma unroll
-      for (int a = 0; a < 2; ++a)
+      for (int pb = 0; pb < NB; ++pb)
 #pragma unroll
-        for (int b = 0; b < 2; ++b) {
-          acc[a][b] = mfma32(ah[a], bh[b], acc[a][b]);
-          acc[a][b] = mfma32(al[a], bh[b], acc[a][b]);
-          if constexpr (!B_BF16) {
-            acc[a][b] = mfma32(ah[a], bl[b], acc[a][b]);
-            if constexpr (NTERMS == 4) acc[a][b] = mfma32(al[a], bl[b], acc[a][b]);
-          }
-        }
+        for (int b = 0; b < MB; ++b)
+          fb[pb][b] = *(const bf16x8*)(L0 + ((NA + pb) * BG_T + wj + 32 * b + l32) * BG_PK + ks + 8 * h32);
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int a = 0; a < MA; ++a)
+#pragma unroll
+          for (int b = 0; b < MB; ++b)
+            acc[a][b] = mfma32(fb[(TB >> t) & 1][b], fa[(TA >> t) & 1][a], acc[a][b]);
     }
+    if (q + 1 < nq) stash(buf ^ 1);
+    __syncthreads();
   }
 
-  // epilogue
+  // lane owns Out[i0+wi+32a+l32][j0+wj+32b+8g+4h32 .. +3]
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < MA; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+    for (int b = 0; b < MB; ++b)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int i = i0 + wi + 32 * a + 8 * (e >> 2) + 4 * h32 + (e & 3);
-        const int j = j0 + wj + 32 * b + l32;
+      for (int g = 0; g < 4; ++g) {
+        const int i = i0 + wi + 32 * a + l32, j = j0 + wj + 32 * b + 8 * g + 4 * h32;
         if (i >= p.I || j >= p.J) continue;
-        // diagonal tiles of G: keep the i <= j triangle and mirror it, so G is
-        // exactly symmetric (the two triangles accumulate their terms in
-        // different orders)
-        if (SYM && ti == tj && i > j) continue;
-        float v = acc[a][b][e];
-        if (p.E1) v += p.rho * (p.E1[(int64_t)i * p.lde + j] - p.E2[(int64_t)i * p.lde + j]);
+        f32x4 v;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = acc[a][b][4 * g + e];
+        if (p.E1) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (j + e < p.J)
+              v[e] += p.rho * (p.E1[(int64_t)i * p.lde + j + e] - p.E2[(int64_t)i * p.lde + j + e]);
+        }
         float* o = p.Out + (int64_t)i * p.ldo + j;
-        *o = p.accumulate ? *o + v : v;
+        const bool diag = SYM && ti == tj;
+        if (p.vec_out && j + 3 < p.J && !diag) {
+          if (p.accumulate) v += *(const f32x4*)o;
+          *(f32x4*)o = v;
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (j + e < p.J && !(diag && i > j + e)) o[e] = p.accumulate ? o[e] + v[e] : v[e];
+        }
         if constexpr (SYM) {
-          if (i != j) {
-            float* o2 = p.Out + (int64_t)j * p.ldo + i;
-            *o2 = p.accumulate ? *o2 + v : v;
+          // mirror to (j + e, i): the 32 lanes of a half write 32 consecutive floats
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int jj = j + e;
+            if (jj >= p.J || i >= jj) continue;
+            float* o2 = p.Out + (int64_t)jj * p.ldo + i;
+            *o2 = p.accumulate ? *o2 + v[e] : v[e];
           }
         }
       }
+}
+
+template <int NA, int NB, int NT, int TA, int TB, bool SYM>
+hipError_t run_bgemm(BGemm p, hipStream_t st) {
+  p.tiles_j = (int)((p.J + BG_T - 1) / BG_T);
+  p.ntiles = SYM ? p.tiles_j * (p.tiles_j + 1) / 2 : (int)((p.I + BG_T - 1) / BG_T) * p.tiles_j;
+  p.vec_out = (p.ldo & 3) == 0 && ((uintptr_t)p.Out & 15) == 0;
+  const dim3 grid((p.ntiles + kXcds - 1) / kXcds * kXcds), block(BG_THREADS);
+  hipLaunchKernelGGL((bgemm_kernel<NA, NB, NT, TA, TB, SYM>), grid, block, 0, st, p);
+  return hipGetLastError();
+}
+
+hipError_t run_split_rows(const float* S1, const float* S2, int64_t rows, int64_t cols, int64_t ld,
+                          __bf16* hi, __bf16* lo, int64_t rows_p, int64_t cols_p, hipStream_t st) {
+  const int64_t n = rows_p * (cols_p / 8);
+  hipLaunchKernelGGL(split_rows_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, S1, S2,
+                     (int)rows, (int)cols, ld, hi, lo, (int)rows_p, (int)cols_p);
+  return hipGetLastError();
+}
+
+template <class SRC>
+hipError_t run_split_transpose(const SRC* S1, const float* S2, int64_t rows, int64_t cols,
+                               int64_t ld, __bf16* hi, __bf16* lo, int64_t rows_p, int64_t cols_p,
+                               hipStream_t st) {
+  const dim3 grid((unsigned)((cols_p + 63) / 64), (unsigned)((rows_p + 63) / 64));
+  hipLaunchKernelGGL((split_transpose_kernel<SRC>), grid, dim3(256), 0, st, S1, S2, (int)rows,
+                     (int)cols, ld, hi, lo, (int)rows_p, (int)cols_p);
+  return hipGetLastError();
+}
+
+struct TargetsWs {
+  size_t Dh, Dl, Wh, Wl, total;
+};
+TargetsWs targets_layout(int64_t M, int64_t din, int64_t dout) {
+  const int64_t Mp = pad_to(M, G_BM), Kp = pad_to(din, G_KC), Jp = pad_to(dout, G_BM);
+  TargetsWs L{};
+  size_t o = 0;
+  L.Dh = o; o += align_up((size_t)Mp * Kp * 2);
+  L.Dl = o; o += align_up((size_t)Mp * Kp * 2);
+  L.Wh = o; o += align_up((size_t)Jp * Kp * 2);
+  L.Wl = o; o += align_up((size_t)Jp * Kp * 2);
+  L.total = o;
+  return L;
+}
+struct NormalEqWs {
+  size_t Xh, Xl, Yh, Yl, total;
+};
+NormalEqWs normal_eq_layout(int64_t rows, int64_t din, int64_t dout) {
+  const int64_t Kp = pad_to(rows, G_KC), Ip = pad_to(din, G_BM), Jp = pad_to(dout, G_BM);
+  NormalEqWs L{};
+  size_t o = 0;
+  L.Xh = o; o += align_up((size_t)Ip * Kp * 2);
+  L.Xl = o; o += align_up((size_t)Ip * Kp * 2);
+  L.Yh = o; o += align_up((size_t)Jp * Kp * 2);
+  L.Yl = o; o += align_up((size_t)Jp * Kp * 2);
+  L.total = o;
+  return L;
 }
 
 // ---------------------------------------------------------------- fp64 path
@@ -356,34 +436,32 @@ hipError_t run_f64(F64Params<TA, TB> p, hipStream_t st) {
   return hipGetLastError();
 }
 
-SplitParams base_params(int I, int J, int K) {
-  SplitParams p{};
-  p.I = I;
-  p.J = J;
-  p.K = K;
-  return p;
-}
-
-bool al16(const void* q) { return ((uintptr_t)q & 15) == 0; }
-
-void set_vec(SplitParams& p, bool b_bf16) {
-  p.vecA = p.lda % 4 == 0 && al16(p.A1) && al16(p.A2);
-  p.vecB = p.ldb % (b_bf16 ? 8 : 4) == 0 && al16(p.B1) && al16(p.B2);
-}
-
 }  // namespace
 
-size_t targets_ws_bytes(int64_t, int64_t, int64_t) { return 0; }
-size_t normal_eq_ws_bytes(int64_t, int64_t, int64_t) { return 0; }
+size_t targets_ws_bytes(int64_t M, int64_t din, int64_t dout) {
+  return targets_layout(M, din, dout).total;
+}
+size_t normal_eq_ws_bytes(int64_t rows, int64_t din, int64_t dout) {
+  return normal_eq_layout(rows, din, dout).total;
+}
 
 hipError_t launch_targets(const float* Of, const float* Oc, const void* W, bool w_bf16, int64_t M,
-                          int64_t din, int64_t dout, int rho, float* T, void*, hipStream_t st) {
-  SplitParams p = base_params((int)M, (int)dout, (int)din);
-  p.A1 = Of;
-  p.A2 = Oc;
-  p.lda = din;
-  p.B1 = W;
-  p.ldb = dout;
+                          int64_t din, int64_t dout, int rho, float* T, void* ws, hipStream_t st) {
+  const TargetsWs L = targets_layout(M, din, dout);
+  const int64_t Mp = pad_to(M, G_BM), Kp = pad_to(din, G_KC), Jp = pad_to(dout, G_BM);
+  char* w = (char*)ws;
+  __bf16 *Dh = (__bf16*)(w + L.Dh), *Dl = (__bf16*)(w + L.Dl);
+  __bf16 *Wh = (__bf16*)(w + L.Wh), *Wl = (__bf16*)(w + L.Wl);
+  hipError_t e = run_split_rows(Of, Oc, M, din, din, Dh, Dl, Mp, Kp, st);
+  if (e != hipSuccess) return e;
+  // W [din][dout] -> W^T [dout][din] (rows j, contraction k contiguous)
+  if (w_bf16)
+    e = run_split_transpose((const __bf16*)W, nullptr, din, dout, dout, Wh, nullptr, Kp, Jp, st);
+  else
+    e = run_split_transpose((const float*)W, nullptr, din, dout, dout, Wh, Wl, Kp, Jp, st);
+  if (e != hipSuccess) return e;
+  BGemm p{};
+  p.ld = Kp;
   p.Out = T;
   p.ldo = dout;
   if (rho) {
@@ -392,52 +470,54 @@ hipError_t launch_targets(const float* Of, const float* Oc, const void* W, bool 
     p.lde = din;
     p.rho = (float)rho;
   }
-  p.tiles_j = (int)((dout + BN - 1) / BN);
-  p.ntiles = (int)((M + BM - 1) / BM) * p.tiles_j;
-  set_vec(p, w_bf16);
-  dim3 grid((p.ntiles + kXcds - 1) / kXcds * kXcds), block(256);
-  if (w_bf16)
-    hipLaunchKernelGGL((split_gemm_kernel<true, false, true, false, 2>), grid, block, 0, st, p);
-  else
-    hipLaunchKernelGGL((split_gemm_kernel<true, false, false, false, 3>), grid, block, 0, st, p);
-  return hipGetLastError();
+  p.I = (int)M;
+  p.J = (int)dout;
+  p.Kp = (int)Kp;
+  p.A[0] = Dh; p.A[1] = Dl;
+  p.B[0] = Wh; p.B[1] = Wl;
+  // terms (a, b): bf16 W (0,0) (1,0); fp32 W (0,0) (1,0) (0,1)
+  if (w_bf16) return run_bgemm<2, 1, 2, 0b10, 0b00, false>(p, st);
+  return run_bgemm<2, 2, 3, 0b010, 0b100, false>(p, st);
 }
 
 hipError_t launch_normal_eq_f32(const float* X, const float* Yf, const float* Yc, int64_t rows,
                                 int64_t din, int64_t dout, bool accumulate, float* G, float* C,
-                                void*, hipStream_t st) {
-  {  // G = X^T X on the upper block triangle, mirrored
-    SplitParams p = base_params((int)din, (int)din, (int)rows);
-    p.A1 = X;
-    p.lda = din;
-    p.B1 = X;
-    p.ldb = din;
-    p.Out = G;
-    p.ldo = din;
-    p.accumulate = accumulate;
-    p.tiles_j = (int)((din + BN - 1) / BN);
-    p.ntiles = p.tiles_j * (p.tiles_j + 1) / 2;
-    set_vec(p, false);
-    dim3 grid((p.ntiles + kXcds - 1) / kXcds * kXcds), block(256);
-    hipLaunchKernelGGL((split_gemm_kernel<false, false, false, true, 4>), grid, block, 0, st, p);
-    hipError_t e = hipGetLastError();
+                                void* ws, hipStream_t st) {
+  const NormalEqWs L = normal_eq_layout(rows, din, dout);
+  const int64_t Kp = pad_to(rows, G_KC), Ip = pad_to(din, G_BM), Jp = pad_to(dout, G_BM);
+  char* w = (char*)ws;
+  __bf16 *Xh = (__bf16*)(w + L.Xh), *Xl = (__bf16*)(w + L.Xl);
+  __bf16 *Yh = (__bf16*)(w + L.Yh), *Yl = (__bf16*)(w + L.Yl);
+  // X [rows][din] -> X^T [din][rows]; (Yf - Yc) [rows][dout] -> [dout][rows]
+  hipError_t e = run_split_transpose(X, (const float*)nullptr, rows, din, din, Xh, Xl, Kp, Ip, st);
+  if (e != hipSuccess) return e;
+  e = run_split_transpose(Yf, Yc, rows, dout, dout, Yh, Yl, Kp, Jp, st);
+  if (e != hipSuccess) return e;
+  {  // G = X^T X: terms (0,0) (0,1) (1,0) (1,1), upper block triangle, mirrored
+    BGemm g{};
+    g.ld = Kp;
+    g.Out = G;
+    g.ldo = din;
+    g.I = (int)din;
+    g.J = (int)din;
+    g.Kp = (int)Kp;
+    g.accumulate = accumulate;
+    g.A[0] = Xh; g.A[1] = Xl;
+    g.B[0] = Xh; g.B[1] = Xl;
+    e = run_bgemm<2, 2, 4, 0b1100, 0b1010, true>(g, st);
     if (e != hipSuccess) return e;
   }
-  SplitParams p = base_params((int)din, (int)dout, (int)rows);
-  p.A1 = X;
-  p.lda = din;
-  p.B1 = Yf;
-  p.B2 = Yc;
-  p.ldb = dout;
+  BGemm p{};  // C = X^T (Yf - Yc): terms (0,0) (0,1) (1,0)
+  p.ld = Kp;
   p.Out = C;
   p.ldo = dout;
+  p.I = (int)din;
+  p.J = (int)dout;
+  p.Kp = (int)Kp;
   p.accumulate = accumulate;
-  p.tiles_j = (int)((dout + BN - 1) / BN);
-  p.ntiles = (int)((din + BM - 1) / BM) * p.tiles_j;
-  set_vec(p, false);
-  dim3 grid((p.ntiles + kXcds - 1) / kXcds * kXcds), block(256);
-  hipLaunchKernelGGL((split_gemm_kernel<false, false, false, false, 3>), grid, block, 0, st, p);
-  return hipGetLastError();
+  p.A[0] = Xh; p.A[1] = Xl;
+  p.B[0] = Yh; p.B[1] = Yl;
+  return run_bgemm<2, 2, 3, 0b100, 0b010, false>(p, st);
 }
 
 hipError_t launch_targets_f64(const float* Of, const float* Oc, const void* W, bool w_bf16,
