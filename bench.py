@@ -35,6 +35,29 @@ METRIC = "sec per layer patch + ref-query attention TFLOP/s (% of MFMA peak), 1 
 PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 MFMA
 PEAK_F32_TFLOPS = 157.3     # MI355X fp32 MFMA
 PEAK_HBM_GBS = 8000.0
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "attn_bf16_kernel_hbm_traffic__llama3-8b-32layer-172k.md")
+
+
+def measured_traffic(cfg):
+    """HBM bytes per full-cache attention launch from the committed counter summary
+    (FETCH_SIZE and WRITE_SIZE, calibrated on a plain copy), or None when the
+    workload differs or the kernel source changed since the counters were taken."""
+    import hashlib
+    if cfg.cid != 3 or not os.path.exists(TRAFFIC_PROFILE):
+        return None
+    want, nbytes = None, None
+    for line in open(TRAFFIC_PROFILE):
+        t = line.split()
+        if len(t) == 3 and t[0] == "source_sha256":
+            want = (t[1], t[2])
+        elif len(t) == 2 and t[0] == "traffic_bytes_per_launch":
+            nbytes = float(t[1])
+    if want is None or nbytes is None:
+        return None
+    with open(os.path.join(ROOT, want[0]), "rb") as f:
+        if hashlib.sha256(f.read()).hexdigest() != want[1]:
+            return None
+    return nbytes
 
 
 def log(*a):
@@ -210,6 +233,7 @@ def main():
     peak = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_F32_TFLOPS
     achieved = att_flops_full / t_attn / 1e12
     kv_bytes = 2.0 * cfg.Hkv * cfg.N * cfg.dh * (2 if cfg.dtype == "bf16" else 4)
+    traffic = measured_traffic(cfg)
 
     out = {
         "metric": METRIC,
@@ -234,10 +258,12 @@ def main():
         "context_tokens_per_s": cfg.N / s_layer,
         "kv_stream_gbs_full_attention": kv_bytes / t_attn / 1e9,
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
-                     "frac": achieved / peak, "traffic": None,
-                     "kernel": "attn_bf16_kernel (full cache)" if cfg.dtype == "bf16"
-                     else "attn_f32_kernel (full cache)",
-                     "flops_per_launch": att_flops_full},
+                     "frac": achieved / peak, "traffic": traffic,
+                     "kernel": ("patchkv_attend_full: vt_kernel + attn_bf16_kernel fast path + fixup"
+                                if cfg.dtype == "bf16" else "patchkv_attend_full: attn_f32_kernel"),
+                     "flops_per_launch": att_flops_full,
+                     "traffic_unit": "HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
+                     "traffic_source": os.path.relpath(TRAFFIC_PROFILE, ROOT) if traffic else None},
         "solve_info_nonzero_layers": bad,
     }
     if not args.no_cpu_baseline:
