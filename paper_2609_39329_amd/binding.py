@@ -119,11 +119,16 @@ def _require_gpu(*ts) -> None:
             raise ValueError("tensors must be contiguous and on the GPU")
 
 
-def _workspace(nbytes: int, device):
+def _workspace(nbytes: int, device, stream=None):
+    """Scratch for one call, allocated on the stream the call runs on (torch's caching
+    allocator may hand the block to later work on that stream once it is freed)."""
     torch = _torch()
     if nbytes == 0:
         return None
-    return torch.empty(nbytes, dtype=torch.uint8, device=device)
+    if stream is None:
+        return torch.empty(nbytes, dtype=torch.uint8, device=device)
+    with torch.cuda.stream(stream):
+        return torch.empty(nbytes, dtype=torch.uint8, device=device)
 
 
 def attend_full(Q, K, V, scale: Optional[float] = None, O=None, stream=None):
@@ -138,7 +143,7 @@ def attend_full(Q, K, V, scale: Optional[float] = None, O=None, stream=None):
         O = torch.empty((M, Hq * dh), dtype=torch.float32, device=Q.device)
     L = lib()
     nb = L.patchkv_attend_workspace_bytes(dt, M, N, Hq, Hkv, dh)
-    ws = _workspace(nb, Q.device)
+    ws = _workspace(nb, Q.device, stream)
     _check("patchkv_attend_full",
            L.patchkv_attend_full(dt, _ptr(Q), _ptr(K), _ptr(V), M, N, Hq, Hkv, dh, scale,
                                  _ptr(O), _ptr(ws), nb, _stream(stream)))
@@ -161,7 +166,7 @@ def attend_compressed(Q, K, V, idx=None, scale: Optional[float] = None, O=None, 
         O = torch.empty((M, Hq * dh), dtype=torch.float32, device=Q.device)
     L = lib()
     nb = L.patchkv_attend_workspace_bytes(dt, M, B, Hq, Hkv, dh)
-    ws = _workspace(nb, Q.device)
+    ws = _workspace(nb, Q.device, stream)
     _check("patchkv_attend_compressed",
            L.patchkv_attend_compressed(dt, _ptr(Q), _ptr(K), _ptr(V), _ptr(idx), M, N, B, Hq, Hkv,
                                        dh, scale, _ptr(O), _ptr(ws), nb, _stream(stream)))
@@ -179,7 +184,7 @@ def compute_targets(Of, Oc, W, rho: int = 1, T=None, stream=None):
         T = torch.empty((M, dout), dtype=torch.float32, device=Of.device)
     L = lib()
     nb = L.patchkv_targets_workspace_bytes(wdt, M, din, dout)
-    ws = _workspace(nb, Of.device)
+    ws = _workspace(nb, Of.device, stream)
     _check("patchkv_compute_targets",
            L.patchkv_compute_targets(wdt, _ptr(Of), _ptr(Oc), _ptr(W), M, din, dout, rho, _ptr(T),
                                      _ptr(ws), nb, _stream(stream)))
@@ -200,7 +205,7 @@ def accumulate_normal_eq(Xc, Yf, Yc=None, G=None, C=None, acc: int = F32, accumu
         C = torch.zeros((din, dout), dtype=tdt, device=Xc.device)
     L = lib()
     nb = L.patchkv_normal_eq_workspace_bytes(acc, rows, din, dout)
-    ws = _workspace(nb, Xc.device)
+    ws = _workspace(nb, Xc.device, stream)
     _check("patchkv_accumulate_normal_eq",
            L.patchkv_accumulate_normal_eq(acc, _ptr(Xc), _ptr(Yf), _ptr(Yc), rows, din, dout,
                                           int(accumulate), _ptr(G), _ptr(C), _ptr(ws), nb,
@@ -220,7 +225,7 @@ def solve_patch(G, C, lam: float, mode: int = RIDGE_ABSOLUTE, dW=None, info=None
         info = torch.empty((1,), dtype=torch.int32, device=G.device)
     L = lib()
     nb = L.patchkv_solve_workspace_bytes(acc, din, dout)
-    ws = _workspace(nb, G.device)
+    ws = _workspace(nb, G.device, stream)
     _check("patchkv_solve_patch",
            L.patchkv_solve_patch(acc, _ptr(G), _ptr(C), din, dout, lam, mode, _ptr(dW), _ptr(info),
                                  _ptr(ws), nb, _stream(stream)))
@@ -253,7 +258,7 @@ def compute_layer_patch(Q, K, V, W, idx=None, Kc=None, Vc=None, lam: float = 0.1
         info = torch.empty((1,), dtype=torch.int32, device=Q.device)
     L = lib()
     nb = L.patchkv_layer_workspace_bytes(dt, acc, M, N, B, Hq, Hkv, dh)
-    ws = workspace if workspace is not None else _workspace(nb, Q.device)
+    ws = workspace if workspace is not None else _workspace(nb, Q.device, stream)
     wsz = ws.numel() * ws.element_size() if ws is not None else 0
     _check("patchkv_compute_layer_patch",
            L.patchkv_compute_layer_patch(dt, acc, _ptr(Q), _ptr(K), _ptr(V), _ptr(idx), _ptr(Kc),

@@ -36,7 +36,7 @@ namespace pkv {
 namespace {
 
 constexpr float kTau = 8.0f;   // lazy-rescale threshold of the fixup path (log2 units)
-constexpr float kBig = 64.0f;  // headroom of the fixed offset in the fast path (log2 units)
+constexpr float kBigSum = 0x1p64f;  // fast path: largest trusted partial row sum (2^kBig, kBig = 64)
 constexpr int kKeyTile = 32;  // keys per iteration, bf16 path
 constexpr int kRowsWG = 256;  // query rows per workgroup (both paths)
 // bf16 path: 32-row query tiles per wave (1: eight waves of 32 rows per workgroup,
@@ -112,12 +112,14 @@ __global__ __launch_bounds__(256) void vt_kernel(const __bf16* __restrict__ V,
 }
 
 // SAFE = false (fast path): each row's exponent offset is fixed to the exact max of
-// its first key tile, so O is never rescaled and only MFMA touches it. A later tile
-// may exceed that offset by up to 2^kBig (P, l and O stay far from fp32 overflow);
-// if any row of the workgroup exceeds it, the work item is marked in p.flags (its
-// outputs are then not trusted). SAFE = true (fixup, launched right after on the
-// same stream): the lazy-rescale online softmax, run only for marked work items,
-// overwriting their outputs.
+// its first key tile, so O is never rescaled and only MFMA touches it, and the
+// steady-state loop takes no row maxima at all. Every weight P a lane adds is at most
+// that lane's partial row sum, so a row whose partial sums all stay at or below
+// 2^kBig never met a score more than about kBig (log2 units) above its offset: P, l and O stay far from fp32
+// overflow. A work item with a larger (or non-finite) partial sum in any row is
+// marked in p.flags at the end and its outputs are not trusted. SAFE = true (fixup,
+// launched right after on the same stream): the lazy-rescale online softmax, run
+// only for marked work items, overwriting their outputs.
 template <int DH, bool GATHER, bool PSPLIT, bool PARTIAL, bool SAFE>
 __global__ __launch_bounds__(kThreadsBf16, 1) void attn_bf16_kernel(AttnParams p) {
   constexpr int KT = kKeyTile;
@@ -388,10 +390,6 @@ __global__ __launch_bounds__(kThreadsBf16, 1) void attn_bf16_kernel(AttnParams p
       bf16x8 pl[NKT][QT][2];
       softmax(sc, pb, pl);
       pv(pb, pl, t & 3);
-      float mt[QT];
-      row_max(sn, mt);
-#pragma unroll
-      for (int qt = 0; qt < QT; ++qt) over |= mt[qt] > m_run[qt] + kBig;
       store_tile_from((t + 2) & 3, (I + 2) % NSET);
       __syncthreads();
     };
@@ -409,6 +407,9 @@ __global__ __launch_bounds__(kThreadsBf16, 1) void attn_bf16_kernel(AttnParams p
     int t = 0;
     for (; t + UNR < t_full; t += UNR) steps(std::false_type{}, t);
     for (; t < ntiles; t += UNR) steps(std::true_type{}, t);
+    // a lane's partial sum bounds every weight it added (NaN fails the test too)
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) over |= !(l_part[qt] <= kBigSum);
     if (__ballot(over) != 0) overflow = 1;
     __syncthreads();
   } else {

@@ -29,7 +29,7 @@ template <class T>
 struct Blk;
 template <>
 struct Blk<float> {
-  static constexpr int NB = 128, TS = 4;  // block size, register tile of the diagonal kernel
+  static constexpr int NB = 128;  // block size
 };
 template <>
 struct Blk<double> {

@@ -108,3 +108,31 @@ def test_attention_deterministic():
     b = pkv.attend_full(q, k, v)
     torch.cuda.synchronize()
     assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("a", [1.0, 3.0, 4.0, 5.0, 8.0, 10.0])
+def test_scores_outgrowing_the_first_tile(a):
+    """One late key (position 1500 of 2000) scores about 16a - 4 log2 units above the
+    first key tile's maximum for every query row. Small excesses stay on the fast
+    path's fixed offset; large ones (row sums above 2^64, fp32 overflow of P or O,
+    exp2 overflow to inf) send the work item to the lazily rescaled fixup. Every
+    case must match the fp64 oracle."""
+    M, N, Hq, Hkv, dh, late = 64, 2000, 8, 2, 128, 1500
+    print(f"late-key excess a={a}", flush=True)
+    rng = np.random.default_rng(int(a * 10))
+    Qf = (rng.standard_normal((M, Hq, dh)) * 0.5 + 1.0).astype(np.float32)
+    Kf = rng.standard_normal((Hkv, N, dh)).astype(np.float32)
+    Vf = rng.standard_normal((Hkv, N, dh)).astype(np.float32)
+    Kf[:, late, :] = a
+    q, k, v = (torch.from_numpy(x).bfloat16().to(DEV) for x in (Qf, Kf, Vf))
+    Q, K, V = (x.double().cpu().numpy() for x in (q, k, v))
+    scale = dh ** -0.5
+    Of = host(pkv.attend_full(q, k, v, scale=scale))
+    e_f = rel(Of, oracle.attention(Q, K, V, scale))
+    idx = np.sort(np.concatenate([np.arange(0, 200), np.arange(1400, 1600)])).astype(np.int32)
+    Oc = host(pkv.attend_compressed(q, k, v, idx=idx_dev(idx), scale=scale))
+    Kc, Vc = oracle.gather_cache(K, V, idx)
+    e_c = rel(Oc, oracle.attention(Q, Kc, Vc, scale))
+    print(f"  O_f {e_f:.3e}  O_c {e_c:.3e}", flush=True)
+    assert np.isfinite(Of).all() and np.isfinite(Oc).all()
+    assert e_f <= TOL_FULL["bf16"] and e_c <= TOL_COMP["bf16"]
