@@ -16,6 +16,13 @@ What it computes, per transformer block (paper, Sec. 2.2-2.3 and Alg. 1):
   (a5) ridge patch  Delta W = S_T (S_H + lambda I)^{-1}                 (Eq. 8),
        with lambda absolute or adaptive, lambda_0 ||S_H||_F^2 / tr S_H   (Eq. 7).
 
+and, for a reference set split into chunks (Sec. 2.4, chunked query encoding;
+Alg. 1, the loop over reference chunks):
+
+  (f2) each chunk's tokens attend over the cache and over the chunk's own
+       causal prefix (cross-chunk attention dropped); the statistics of all
+       chunks are summed before the single solve.
+
 Readings where the paper is silent (each is also listed in the design notes):
 
 * Row-vector orientation. Activations are rows (one token per row), so with
@@ -30,6 +37,11 @@ Readings where the paper is silent (each is also listed in the design notes):
 * Attention: every query attends to every cache entry (no mask, RoPE already
   applied), softmax scale 1/sqrt(dh) unless given, GQA query head h reads KV
   head floor(h / (Hq / Hkv)).
+* Chunked reference set: token m of a chunk also attends to the chunk's own
+  tokens 0..m (its causal prefix, itself included), whose keys and values the
+  caller supplies. At the first block the teacher's and the student's chunk
+  states coincide (both are the token embeddings), so the same own keys and
+  values serve both passes there; in general each pass takes its own.
 
 Parity pins for every function live in the CPU test suite (closed forms,
 invariants, brute force, library routines). Nothing here is "parity unpinned".
@@ -42,7 +54,7 @@ import scipy.linalg
 __all__ = [
     "decode", "softmax_rows", "attention", "gather_cache", "targets",
     "normal_equations", "normal_equations_chunked", "ridge_lambda", "solve_patch",
-    "layer_patch", "attention_rows",
+    "layer_patch", "attention_rows", "attention_chunk", "layer_patch_chunked",
 ]
 
 
@@ -100,6 +112,41 @@ def attention_rows(Q: np.ndarray, K: np.ndarray, V: np.ndarray, rows: np.ndarray
                    scale: float | None = None) -> np.ndarray:
     """Attention output of a subset of query rows (each row is independent)."""
     return attention(Q[np.asarray(rows)], K, V, scale)
+
+
+def attention_chunk(Q: np.ndarray, K: np.ndarray, V: np.ndarray, Ks: np.ndarray,
+                    Vs: np.ndarray, scale: float | None = None,
+                    max_score_bytes: int = 1 << 28) -> np.ndarray:
+    """One reference chunk's attention (Sec. 2.4, chunked query encoding; Alg. 1).
+
+    Q [Mc, Hq, dh] are the chunk's queries, K and V [Hkv, Nk, dh] the cache (full
+    or compressed), Ks and Vs [Hkv, Mc, dh] the chunk's own keys and values. Query
+    m attends over all Nk cache entries and over its own entries 0..m: the own
+    entries m+1.. get a score of -inf before the softmax. Returns O [Mc, Hq*dh].
+    """
+    M, Hq, dh = Q.shape
+    Hkv, Nk, dh2 = K.shape
+    if dh2 != dh or V.shape != K.shape or Ks.shape != (Hkv, M, dh) or Vs.shape != Ks.shape:
+        raise ValueError("shape mismatch")
+    if Hq % Hkv:
+        raise ValueError("Hq must be a multiple of Hkv")
+    if scale is None:
+        scale = 1.0 / np.sqrt(dh)
+    group = Hq // Hkv
+    O = np.empty((M, Hq * dh), dtype=np.float64)
+    rows = max(1, min(M, max_score_bytes // (8 * (Nk + M))))
+    for h in range(Hq):
+        g = h // group
+        Kall = np.concatenate([K[g], Ks[g]], axis=0)     # [Nk + M, dh]
+        Vall = np.concatenate([V[g], Vs[g]], axis=0)
+        for r0 in range(0, M, rows):
+            r1 = min(M, r0 + rows)
+            S = (Q[r0:r1, h, :] @ Kall.T) * scale
+            own = np.arange(M)[None, :]                  # own entry index j
+            query = np.arange(r0, r1)[:, None]           # query position m
+            S[:, Nk:][own > query] = -np.inf
+            O[r0:r1, h * dh:(h + 1) * dh] = softmax_rows(S) @ Vall
+    return O
 
 
 def gather_cache(K: np.ndarray, V: np.ndarray, idx: np.ndarray):
@@ -188,3 +235,36 @@ def layer_patch(inp, rho: int = 1, mode: str = "absolute", lam: float | None = N
     if keep:
         out.update(Of=Of, Oc=Oc, T=T, G=G0, C=C)
     return out
+
+
+def layer_patch_chunked(inp, chunks, rho: int = 1, mode: str = "absolute",
+                        lam: float | None = None) -> dict:
+    """One block's patch from a reference set split into chunks (Sec. 2.4; Alg. 1).
+
+    ``inp`` is a ``workloads`` LayerInputs (the cache, the compressed cache and W);
+    ``chunks`` yields per-chunk (Q, Ks, Vs) in the same stored form. For every chunk
+    the teacher pass attends over the full cache and the student pass over the
+    compressed cache, both plus the chunk's causal prefix; the chunk's targets and
+    statistics are formed and added to running sums that start from zero; one
+    ridge solve follows. Returns dW, lambda, G (without the ridge) and C.
+    """
+    dt = inp.dtype
+    K = decode(inp.K, dt)
+    V = decode(inp.V, dt)
+    W = decode(inp.W, dt)
+    if inp.idx is not None:
+        Kc, Vc = gather_cache(K, V, inp.idx)
+    else:
+        Kc, Vc = decode(inp.Kc, dt), decode(inp.Vc, dt)
+    G0 = np.zeros((W.shape[0], W.shape[0]))
+    C = np.zeros((W.shape[0], W.shape[1]))
+    for Qj, Ksj, Vsj in chunks:
+        Qj, Ksj, Vsj = decode(Qj, dt), decode(Ksj, dt), decode(Vsj, dt)
+        Of = attention_chunk(Qj, K, V, Ksj, Vsj, inp.scale)
+        Oc = attention_chunk(Qj, Kc, Vc, Ksj, Vsj, inp.scale)
+        T = targets(Of, Oc, W, rho)
+        Gj, Cj = normal_equations(Oc, T)
+        G0 += Gj
+        C += Cj
+    lam_used = ridge_lambda(G0, inp.lam if lam is None else lam, mode)
+    return {"dW": solve_patch(G0, C, lam_used), "lam": lam_used, "G": G0, "C": C}

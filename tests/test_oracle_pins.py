@@ -421,3 +421,147 @@ def test_pins_catch_planted_mistakes():
     assert check_normal_equations(ne_transposed) > 1e-2
     assert check_solve_rational(solve_no_ridge) > 1e-3
     assert check_solve_rational(solve_sign) > 1e-3
+
+
+# ------------------------------------------------------- chunked reference set (f2)
+
+def brute_attention_chunk(Q, K, V, Ks, Vs, scale):
+    """Scalar loops: query m of the chunk sees every cache entry and its own
+    entries 0..m, written out term by term."""
+    M, Hq, dh = Q.shape
+    Hkv, N, _ = K.shape
+    grp = Hq // Hkv
+    O = np.zeros((M, Hq * dh))
+    for m in range(M):
+        for h in range(Hq):
+            g = h // grp
+            keys = [K[g, n] for n in range(N)] + [Ks[g, j] for j in range(m + 1)]
+            vals = [V[g, n] for n in range(N)] + [Vs[g, j] for j in range(m + 1)]
+            s = [scale * sum(Q[m, h, c] * k[c] for c in range(dh)) for k in keys]
+            mx = max(s)
+            e = [math.exp(x - mx) for x in s]
+            z = sum(e)
+            for c in range(dh):
+                O[m, h * dh + c] = sum(e[i] * vals[i][c] for i in range(len(e))) / z
+    return O
+
+
+def rand_chunk(rng, M, N, Hq, Hkv, dh):
+    Q, K, V = rand_attn(rng, M, N, Hq, Hkv, dh)
+    Ks = rng.standard_normal((Hkv, M, dh))
+    Vs = rng.standard_normal((Hkv, M, dh))
+    return Q, K, V, Ks, Vs
+
+
+def check_attention_chunk_bruteforce(fn):
+    rng = np.random.default_rng(11)
+    worst = 0.0
+    for (M, N, Hq, Hkv, dh) in [(4, 5, 4, 2, 3), (3, 0, 2, 1, 4), (5, 2, 6, 3, 2), (1, 3, 2, 2, 3)]:
+        Q, K, V, Ks, Vs = rand_chunk(rng, M, N, Hq, Hkv, dh)
+        worst = max(worst, rel(fn(Q, K, V, Ks, Vs, 0.41), brute_attention_chunk(Q, K, V, Ks, Vs, 0.41)))
+    return worst
+
+
+def test_attention_chunk_bruteforce():
+    assert check_attention_chunk_bruteforce(oracle.attention_chunk) < 1e-13
+
+
+def test_attention_chunk_empty_cache_is_causal_sdpa():
+    """With no cache entries a chunk is plain causal self-attention: torch's
+    scaled_dot_product_attention(is_causal=True), float64 on the CPU."""
+    rng = np.random.default_rng(12)
+    for (M, Hq, Hkv, dh) in [(23, 4, 2, 8), (40, 8, 8, 16)]:
+        Q, K, V, Ks, Vs = rand_chunk(rng, M, 0, Hq, Hkv, dh)
+        s = 1.0 / math.sqrt(dh)
+        q = torch.from_numpy(Q).permute(1, 0, 2)
+        k = torch.from_numpy(Ks).repeat_interleave(Hq // Hkv, dim=0)
+        v = torch.from_numpy(Vs).repeat_interleave(Hq // Hkv, dim=0)
+        o = torch.nn.functional.scaled_dot_product_attention(q, k, v, is_causal=True, scale=s)
+        ref = o.permute(1, 0, 2).reshape(M, Hq * dh).numpy()
+        assert rel(oracle.attention_chunk(Q, K, V, Ks, Vs, s), ref) < 1e-13
+
+
+def test_attention_chunk_rows_reduce_to_plain_attention():
+    """Row m equals the (pinned) unmasked attention of that one query over the
+    cache followed by the chunk's entries 0..m."""
+    rng = np.random.default_rng(13)
+    Q, K, V, Ks, Vs = rand_chunk(rng, 9, 30, 8, 2, 16)
+    O = oracle.attention_chunk(Q, K, V, Ks, Vs)
+    for m in range(9):
+        Kc = np.concatenate([K, Ks[:, :m + 1]], axis=1)
+        Vc = np.concatenate([V, Vs[:, :m + 1]], axis=1)
+        assert rel(O[m:m + 1], oracle.attention(Q[m:m + 1], Kc, Vc)) < 1e-14
+
+
+def test_attention_chunk_causality_and_prefix():
+    rng = np.random.default_rng(14)
+    Q, K, V, Ks, Vs = rand_chunk(rng, 12, 20, 4, 2, 8)
+    O = oracle.attention_chunk(Q, K, V, Ks, Vs)
+    # own entries after position 5 cannot reach queries 0..5, and do reach the rest
+    Ks2, Vs2 = Ks.copy(), Vs.copy()
+    Ks2[:, 6:] += 3.0
+    Vs2[:, 6:] -= 2.0
+    O2 = oracle.attention_chunk(Q, K, V, Ks2, Vs2)
+    assert np.array_equal(O2[:6], O[:6])
+    assert np.all(np.abs(O2[6:] - O[6:]).max(axis=1) > 1e-6)
+    # a chunk's prefix is itself a chunk
+    assert rel(oracle.attention_chunk(Q[:7], K, V, Ks[:, :7], Vs[:, :7]), O[:7]) < 1e-15
+    # rows sum to one: all-ones values give all-ones outputs
+    O1 = oracle.attention_chunk(Q, K, np.ones_like(V), Ks, np.ones_like(Vs))
+    assert np.max(np.abs(O1 - 1.0)) < 1e-14
+
+
+def test_layer_patch_chunked_properties():
+    from workloads import make_chunk_inputs
+    inp = make_custom_inputs(M=16, N=96, B=96, Hq=4, Hkv=2, dh=16, dtype="f32",
+                             cache="identity", lam=1e-2, seed=5)
+    chunks = [make_chunk_inputs(inp, j, 16) for j in range(3)]
+    triples = [(c.Q, c.Ks, c.Vs) for c in chunks]
+    # compressed cache == full cache: teacher and student agree, Delta W = 0 exactly
+    out = oracle.layer_patch_chunked(inp, triples)
+    assert np.array_equal(out["dW"], np.zeros_like(out["dW"]))
+    # eviction cache: the statistics are the sums over chunks of each chunk's own
+    # outer products (Eq. 9), and the patch solves the stacked regression
+    inp = make_custom_inputs(M=16, N=96, B=40, Hq=4, Hkv=2, dh=16, dtype="f32", lam=1e-2, seed=6)
+    chunks = [make_chunk_inputs(inp, j, 16) for j in range(3)]
+    out = oracle.layer_patch_chunked(inp, [(c.Q, c.Ks, c.Vs) for c in chunks])
+    K, V = oracle.decode(inp.K, "f32"), oracle.decode(inp.V, "f32")
+    Kc, Vc = oracle.gather_cache(K, V, inp.idx)
+    W = oracle.decode(inp.W, "f32")
+    X, T = [], []
+    for c in chunks:
+        Q, Ks, Vs = (oracle.decode(a, "f32") for a in (c.Q, c.Ks, c.Vs))
+        Of = brute_attention_chunk(Q, K, V, Ks, Vs, inp.scale)
+        Oc = brute_attention_chunk(Q, Kc, Vc, Ks, Vs, inp.scale)
+        X.append(Oc)
+        T.append((Of - Oc) @ W + (Of - Oc))
+    X, T = np.vstack(X), np.vstack(T)
+    Gs = sum(np.outer(X[i], X[i]) for i in range(X.shape[0]))
+    Cs = sum(np.outer(X[i], T[i]) for i in range(X.shape[0]))
+    assert rel(out["G"], Gs) < 1e-12 and rel(out["C"], Cs) < 1e-12
+    A = np.vstack([X, np.sqrt(1e-2) * np.eye(X.shape[1])])
+    Bm = np.vstack([T, np.zeros((X.shape[1], T.shape[1]))])
+    assert rel(out["dW"], np.linalg.lstsq(A, Bm, rcond=None)[0]) < 1e-9
+
+
+def test_chunk_pins_catch_planted_mistakes():
+    def no_self(Q, K, V, Ks, Vs, scale=None):           # own prefix excludes the token itself
+        M = Q.shape[0]
+        O = np.empty((M, Q.shape[1] * Q.shape[2]))
+        for m in range(M):
+            Kc = np.concatenate([K, Ks[:, :m]], axis=1)
+            Vc = np.concatenate([V, Vs[:, :m]], axis=1)
+            if Kc.shape[1] == 0:
+                Kc, Vc = Ks[:, :1], Vs[:, :1]
+            O[m] = oracle.attention(Q[m:m + 1], Kc, Vc, scale)[0]
+        return O
+
+    def no_mask(Q, K, V, Ks, Vs, scale=None):           # the whole chunk is visible
+        return oracle.attention(Q, np.concatenate([K, Ks], 1), np.concatenate([V, Vs], 1), scale)
+
+    def own_from_cache_values(Q, K, V, Ks, Vs, scale=None):   # own keys paired with wrong values
+        return oracle.attention_chunk(Q, K, V, Ks, Vs[:, ::-1], scale)
+
+    assert check_attention_chunk_bruteforce(no_self) > 1e-2
+    assert check_attention_chunk_bruteforce(no_mask) > 1e-2
+    assert check_attention_chunk_bruteforce(own_from_cache_values) > 1e-2

@@ -1,4 +1,4 @@
-"""The five synthetic workload shapes.
+"""The synthetic workload shapes.
 
 Each stands in for a setting the paper measures (Sec. 3 and App. B): contexts up to
 ~170K tokens, aggressive cache budgets (down to ~1 % of the context), and one
@@ -36,6 +36,7 @@ class Config:
     n_recent: int = 0
     n_random: int = 0
     n_mix: int = 0           # synthesize: entries mixed per synthetic entry
+    chunks: int = 1          # reference chunks per layer (M tokens each, own causal prefix)
 
     @property
     def group(self) -> int:
@@ -63,6 +64,11 @@ CONFIGS = (
            n_random=856),
     Config(4, "qwen2.5-7b-layer-64k-synth", d=3584, Hq=28, Hkv=4, dh=128, N=65536,
            B=1024, M=2048, lam=5e-2, dtype="bf16", cache="synthesize", n_mix=64),
+    # chunked reference set: 4 chunks of 5,120 tokens (the paper's default chunk
+    # size), each attending over the cache plus its own causal prefix
+    Config(5, "llama3-8b-layer-172k-4x5k-chunks", d=4096, Hq=32, Hkv=8, dh=128, N=172032,
+           B=1720, M=5120, lam=1e-1, dtype="bf16", chunks=4, n_sink=4, n_recent=860,
+           n_random=856),
 )
 
 

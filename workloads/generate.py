@@ -3,7 +3,9 @@
 Recipe (the same bytes feed the oracle and the GPU path):
 
 * Every random tensor has a tensor id: 0 key scales, 1 K, 2 V, 3 Q, 4 W,
-  5 eviction middle positions, 6 synthesis positions, 7 synthesis weights.
+  5 eviction middle positions, 6 synthesis positions, 7 synthesis weights;
+  reference chunk j of a chunked reference set: 16 + 4j its queries, 17 + 4j its
+  own keys, 18 + 4j its own values.
 * Normal tensors are drawn in C order in blocks of ``BLOCK`` elements; block ``b``
   of tensor ``tid`` uses ``Generator(PCG64(SeedSequence([seed, cid, layer, tid, b])))``
   and ``standard_normal(n, dtype=float32)``. Blocks are independent streams, so
@@ -11,6 +13,8 @@ Recipe (the same bytes feed the oracle and the GPU path):
   thread count.
 * Q, V ~ N(0, 1). K = Z * s with a per-(kv head, channel) scale
   s ~ LogNormal(0, 0.5) (float32 product). W = Z * float32(1/sqrt(d)).
+  A chunk's queries and own values are N(0, 1); its own keys carry the layer's
+  key scales s like the cache keys.
 * bf16 tensors are rounded from those float32 values with round-to-nearest-even
   and stored as their raw uint16 bit patterns; fp32 tensors are stored as is.
 * Eviction subset: ``n_sink`` sinks, the last ``n_recent`` tokens, and
@@ -37,6 +41,7 @@ from .configs import Config
 BLOCK = 1 << 22
 
 TID_SCALE, TID_K, TID_V, TID_Q, TID_W, TID_EVICT, TID_SYN_POS, TID_SYN_W = range(8)
+TID_CHUNK = 16  # chunk j: 16 + 4j queries, 17 + 4j own keys, 18 + 4j own values
 
 
 def _threads() -> int:
@@ -158,6 +163,8 @@ def make_custom_inputs(*, M: int, N: int, B: int, Hq: int, Hkv: int, dh: int,
 
     out = LayerInputs(cid=cid, layer=layer, dtype=dtype, M=M, N=N, B=B, Hq=Hq, Hkv=Hkv,
                       dh=dh, lam=lam, scale=1.0 / float(dh) ** 0.5, Q=Q, K=K, V=V, W=W)
+    out.extra["seed"] = seed
+    out.extra["key_scale"] = s
     if cache == "evict":
         ns = 4 if n_sink is None else n_sink
         ns = min(ns, B)
@@ -181,6 +188,33 @@ def make_custom_inputs(*, M: int, N: int, B: int, Hq: int, Hkv: int, dh: int,
     else:
         raise ValueError(cache)
     return out
+
+
+@dataclass
+class ChunkInputs:
+    """One reference chunk: its queries and its own keys and values."""
+    chunk: int
+    Q: np.ndarray                # [Mc, Hq, dh]
+    Ks: np.ndarray               # [Hkv, Mc, dh]
+    Vs: np.ndarray               # [Hkv, Mc, dh]
+
+
+def make_chunk_inputs(inp: LayerInputs, chunk: int, M: int) -> ChunkInputs:
+    """Reference chunk ``chunk`` (M tokens) of the layer ``inp``: queries, own keys
+    (scaled by the layer's key scales) and own values, drawn with the recipe above."""
+    bf16 = inp.dtype == "bf16"
+    seed, s = inp.extra["seed"], inp.extra["key_scale"]
+    Hq, Hkv, dh = inp.Hq, inp.Hkv, inp.dh
+    base = TID_CHUNK + 4 * chunk
+
+    def scale_k(z: np.ndarray, lo: int) -> np.ndarray:
+        rows = np.arange(lo // dh, (lo + z.size) // dh)
+        return (z.reshape(-1, dh) * s[rows // M]).reshape(-1)
+
+    Q = _normal_tensor(seed, inp.cid, inp.layer, base, (M, Hq, dh), bf16)
+    Ks = _normal_tensor(seed, inp.cid, inp.layer, base + 1, (Hkv, M, dh), bf16, scale_k)
+    Vs = _normal_tensor(seed, inp.cid, inp.layer, base + 2, (Hkv, M, dh), bf16)
+    return ChunkInputs(chunk=chunk, Q=Q, Ks=Ks, Vs=Vs)
 
 
 def _mix(X: np.ndarray, pos: np.ndarray, w: np.ndarray, bf16: bool) -> np.ndarray:
