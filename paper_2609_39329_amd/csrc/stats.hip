@@ -261,8 +261,8 @@ __global__ __launch_bounds__(BG_THREADS, 1) void bgemm_kernel(BGemm p) {
         float* o = p.Out + (int64_t)i * p.ldo + j;
         const bool diag = SYM && ti == tj;
         if (p.vec_out && j + 3 < p.J && !diag) {
-          if (p.accumulate) v += *(const f32x4*)o;
-          *(f32x4*)o = v;
+          // v stays this call's contribution: the mirror below adds it again
+          *(f32x4*)o = p.accumulate ? v + *(const f32x4*)o : v;
         } else {
 #pragma unroll
           for (int e = 0; e < 4; ++e)

@@ -67,11 +67,13 @@ def test_normal_equations_f32(rows, din, dout):
     assert np.array_equal(g, g.T)
 
 
-@pytest.mark.parametrize("acc", ["f32", "f64"])
-def test_normal_equations_accumulate_chunks(acc):
-    """Eq. 9: running sums over reference chunks equal the one-shot statistics."""
+@pytest.mark.parametrize("acc,din,dout", [("f32", 192, 160), ("f64", 192, 160), ("f32", 600, 300),
+                                          ("f64", 600, 300)])
+def test_normal_equations_accumulate_chunks(acc, din, dout):
+    """Eq. 9: running sums over reference chunks equal the one-shot statistics. With
+    d_in = 600 G spans 3x3 tiles, so the mirrored lower triangle is accumulated too."""
     code = pkv.F32 if acc == "f32" else pkv.F64
-    rows, din, dout = 700, 192, 160
+    rows = 700
     X, Y = randn((rows, din), 7, 0.5), randn((rows, dout), 8)
     Gr, Cr = oracle.normal_equations(X.astype(np.float64), Y.astype(np.float64))
     G = C = None
@@ -79,7 +81,9 @@ def test_normal_equations_accumulate_chunks(acc):
         G, C = pkv.accumulate_normal_eq(dev(X[a:b]), dev(Y[a:b]), G=G, C=C, acc=code,
                                         accumulate=a > 0)
     tol = 5e-5 if acc == "f32" else 1e-12
-    assert rel(host(G), Gr) <= tol and rel(host(C), Cr) <= tol
+    g = host(G)
+    assert np.array_equal(g, g.T)
+    assert rel(g, Gr) <= tol and rel(host(C), Cr) <= tol
 
 
 def test_normal_equations_f64():
