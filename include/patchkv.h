@@ -123,6 +123,38 @@ int patchkv_attend_compressed(int dtype, const void* Q, const void* K, const voi
                               float* O, void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------- */
+/* Attention of one reference chunk over a cache plus the chunk's own causal    */
+/* prefix (Sec. 2.4, chunked query encoding; Alg. 1, loop over reference       */
+/* chunks). The chunk's M tokens are the queries; token m attends over every    */
+/* cache entry and over the chunk's own entries 0..m (itself included), never   */
+/* over other chunks:                                                          */
+/*   O[m, h*dh + j] = sum_e softmax_e(scale * <Q[m,h,:], key_e>) value_e[j],    */
+/*   e over the n_cache cache entries of KV head g = floor(h / (Hq/Hkv)) and    */
+/*   the own entries Ks[g, 0..m, :] / Vs[g, 0..m, :].                           */
+/* The cache:                                                                  */
+/*  - idx != NULL: K, V [Hkv][n_src][dh] and the cache is rows idx[0..n_cache)  */
+/*    (eviction subset, gathered on the fly; every idx entry in [0, n_src)).   */
+/*  - idx == NULL: rows 0..n_cache of K, V [Hkv][n_src][dh] (n_cache <= n_src); */
+/*    n_cache = n_src is the full cache, a synthesized cache is passed as is.   */
+/* Ks, Vs [Hkv][M][dh] (dtype): the chunk's own keys and values.                */
+/* p_terms: 1 = P enters the P V product rounded to bf16 (as attend_full),      */
+/*          2 = as a two-term bf16 split (as attend_compressed); f32 ignores it.*/
+/* Limits as patchkv_attend_full with N = n_cache, plus n_src and M within the  */
+/* same row limits. Own entries are attended without a key split.              */
+/* Workspace: patchkv_attend_chunk_workspace_bytes(dtype, M, n_cache, ...):     */
+/*   for bf16, transposed copies of the cache's and the own values plus a few   */
+/*   bytes per work item; 0 for f32.                                           */
+/* ------------------------------------------------------------------------- */
+size_t patchkv_attend_chunk_workspace_bytes(int dtype, int64_t M, int64_t n_cache, int Hq, int Hkv,
+                                            int dh);
+
+int patchkv_attend_chunk(int dtype, const void* Q, const void* K, const void* V,
+                         const int32_t* idx, int64_t n_src, int64_t n_cache, const void* Ks,
+                         const void* Vs, int64_t M, int Hq, int Hkv, int dh, float scale,
+                         int p_terms, float* O, void* workspace, size_t workspace_bytes,
+                         void* stream);
+
+/* ------------------------------------------------------------------------- */
 /* Per-token targets, Eq. 5 in row form with h = z = the attention output:      */
 /*   T = (O_f - O_c) W + rho (O_f - O_c)                                        */
 /* Of, Oc [M][d_in] float; W [d_in][d_out] (w_dtype PATCHKV_BF16 or F32);        */

@@ -4,11 +4,11 @@ The library (``lib/libpatchkv.so``) is loaded on first use by :mod:`.binding`;
 there is no CPU fallback.
 """
 from .binding import (BF16, F32, F64, RIDGE_ABSOLUTE, RIDGE_ADAPTIVE, SOLVE_EXACT_F32,
-                      PatchKVError,
-                      accumulate_normal_eq, attend_compressed, attend_full, compute_layer_patch,
-                      compute_targets, layer_workspace_bytes, lib, solve_patch)
+                      PatchKVError, accumulate_normal_eq, attend_chunk, attend_compressed,
+                      attend_full, compute_layer_patch, compute_targets, layer_workspace_bytes,
+                      lib, solve_patch)
 
 __all__ = ["BF16", "F32", "F64", "RIDGE_ABSOLUTE", "RIDGE_ADAPTIVE", "SOLVE_EXACT_F32",
-           "PatchKVError",
-           "accumulate_normal_eq", "attend_compressed", "attend_full", "compute_layer_patch",
-           "compute_targets", "layer_workspace_bytes", "lib", "solve_patch"]
+           "PatchKVError", "accumulate_normal_eq", "attend_chunk", "attend_compressed",
+           "attend_full", "compute_layer_patch", "compute_targets", "layer_workspace_bytes", "lib",
+           "solve_patch"]

@@ -37,6 +37,11 @@ SIGNATURES = {
     "patchkv_attend_compressed": (_c_int, [_c_int, _c_vp, _c_vp, _c_vp, _c_vp, _c_i64, _c_i64,
                                            _c_i64, _c_int, _c_int, _c_int, ctypes.c_float, _c_vp,
                                            _c_vp, _c_sz, _c_vp]),
+    "patchkv_attend_chunk_workspace_bytes": (_c_sz, [_c_int, _c_i64, _c_i64, _c_int, _c_int,
+                                                     _c_int]),
+    "patchkv_attend_chunk": (_c_int, [_c_int, _c_vp, _c_vp, _c_vp, _c_vp, _c_i64, _c_i64, _c_vp,
+                                      _c_vp, _c_i64, _c_int, _c_int, _c_int, ctypes.c_float,
+                                      _c_int, _c_vp, _c_vp, _c_sz, _c_vp]),
     "patchkv_targets_workspace_bytes": (_c_sz, [_c_int, _c_i64, _c_i64, _c_i64]),
     "patchkv_compute_targets": (_c_int, [_c_int, _c_vp, _c_vp, _c_vp, _c_i64, _c_i64, _c_i64,
                                          _c_int, _c_vp, _c_vp, _c_sz, _c_vp]),
@@ -170,6 +175,38 @@ def attend_compressed(Q, K, V, idx=None, scale: Optional[float] = None, O=None, 
     _check("patchkv_attend_compressed",
            L.patchkv_attend_compressed(dt, _ptr(Q), _ptr(K), _ptr(V), _ptr(idx), M, N, B, Hq, Hkv,
                                        dh, scale, _ptr(O), _ptr(ws), nb, _stream(stream)))
+    return O
+
+
+
+def attend_chunk(Q, K, V, Ks, Vs, idx=None, n_cache: Optional[int] = None,
+                 scale: Optional[float] = None, p_terms: int = 1, O=None, stream=None):
+    """Attention of one reference chunk (queries Q [M,Hq,dh]) over a cache plus the
+    chunk's own causal prefix Ks, Vs [Hkv,M,dh]: token m sees the cache and own
+    entries 0..m. The cache is K[:, idx], V[:, idx] (idx int32 [n_cache]) or, with
+    idx None, the first n_cache rows of K, V (default: all of them). p_terms = 2
+    forms P V from a two-term bf16 split of P (as attend_compressed)."""
+    torch = _torch()
+    _require_gpu(Q, K, V, Ks, Vs, idx, O)
+    M, Hq, dh = Q.shape
+    Hkv, n_src, _ = K.shape
+    if idx is not None:
+        if idx.dtype != torch.int32:
+            raise TypeError("idx must be int32")
+        n_cache = idx.shape[0]
+    elif n_cache is None:
+        n_cache = n_src
+    dt = _dtype_code(Q)
+    scale = 1.0 / dh ** 0.5 if scale is None else scale
+    if O is None:
+        O = torch.empty((M, Hq * dh), dtype=torch.float32, device=Q.device)
+    L = lib()
+    nb = L.patchkv_attend_chunk_workspace_bytes(dt, M, n_cache, Hq, Hkv, dh)
+    ws = _workspace(nb, Q.device, stream)
+    _check("patchkv_attend_chunk",
+           L.patchkv_attend_chunk(dt, _ptr(Q), _ptr(K), _ptr(V), _ptr(idx), n_src, n_cache,
+                                  _ptr(Ks), _ptr(Vs), M, Hq, Hkv, dh, scale, p_terms, _ptr(O),
+                                  _ptr(ws), nb, _stream(stream)))
     return O
 
 

@@ -24,6 +24,11 @@
 //
 // Both paths can split the cache into key ranges (more workgroups for small M);
 // attn_combine_kernel then merges the partial (O, m, l) triples.
+//
+// Chunked reference sets (OWN = true): the queries are one chunk's tokens, and
+// token m also attends to the chunk's own entries 0..m (its causal prefix), which
+// follow the cache in the key order: key tiles [0, ct) are the cache's, tiles
+// ct.. the own entries', masked per query. Such calls use no key split.
 #include <math.h>
 
 #include <type_traits>
@@ -68,6 +73,12 @@ struct AttnParams {
   int row_tiles;
   int total_items, per_xcd;
   float c;  // bf16: scale * log2(e); f32: scale
+  // own entries of a reference chunk (OWN kernels): Ks, Vs [Hkv][Ms][dh]; Vts their
+  // V^T tiles (bf16); ct = number of cache key tiles before them
+  const void* Ks;
+  const void* Vs;
+  const __bf16* Vts;
+  int Ms, own_tiles, ct;
 };
 
 // V -> V^T in 32-key tiles, so that the P V product reads V with plain 16-byte LDS
@@ -120,8 +131,9 @@ __global__ __launch_bounds__(256) void vt_kernel(const __bf16* __restrict__ V,
 // marked in p.flags at the end and its outputs are not trusted. SAFE = true (fixup,
 // launched right after on the same stream): the lazy-rescale online softmax, run
 // only for marked work items, overwriting their outputs.
-template <int DH, bool GATHER, bool PSPLIT, bool PARTIAL, bool SAFE>
+template <int DH, bool GATHER, bool PSPLIT, bool PARTIAL, bool SAFE, bool OWN>
 __global__ __launch_bounds__(kThreadsBf16, 1) void attn_bf16_kernel(AttnParams p) {
+  static_assert(!(OWN && PARTIAL), "own entries are attended without a key split");
   constexpr int KT = kKeyTile;
   constexpr int NKT = KT / 32;  // 32-key MFMA tiles per iteration
   constexpr int KP = DH + 8;   // K tile pitch (elements): conflict-free 16-byte row reads
@@ -150,7 +162,12 @@ __global__ __launch_bounds__(kThreadsBf16, 1) void attn_bf16_kernel(AttnParams p
   const int g = __builtin_amdgcn_readfirstlane(t2 / p.n_split);
   const int k_begin = split * p.keys_per_split;
   const int k_end = min(p.Nk, k_begin + p.keys_per_split);
-  const int ntiles = (k_end - k_begin + KT - 1) / KT;
+  // cache tiles, then (OWN) the own tiles up to this workgroup's last query
+  int ntiles = (k_end - k_begin + KT - 1) / KT;
+  if constexpr (OWN) {
+    const int last_q = min(p.rows - 1, rt * kRowsWG + kRowsWG - 1) / p.G;
+    ntiles = p.ct + last_q / KT + 1;
+  }
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wid = tid >> 6;
@@ -181,9 +198,28 @@ __global__ __launch_bounds__(kThreadsBf16, 1) void attn_bf16_kernel(AttnParams p
       (void*)Vtg, 0, (uint32_t)p.vt_tiles * (DH * 32 * 2), 0x00020000);
   const __amdgpu_buffer_rsrc_t irs =
       __builtin_amdgcn_make_buffer_rsrc((void*)p.idx, 0, (uint32_t)(p.Nk * 4), 0x00020000);
+  // own entries (OWN): rows past Ms and tiles past the last read as zeros
+  const __amdgpu_buffer_rsrc_t ksrs = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)((const __bf16*)p.Ks + (int64_t)g * p.Ms * DH), 0, (uint32_t)(p.Ms * DH * 2), 0x00020000);
+  const __amdgpu_buffer_rsrc_t vtsrs = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(p.Vts + (int64_t)g * p.own_tiles * DH * 32), 0, (uint32_t)p.own_tiles * (DH * 64),
+      0x00020000);
   constexpr int NSET = kLoadSets;
   u32x4 kreg[NSET][LPT], vreg[NSET][LPT];
   auto load_tile_to = [&](int tile, int set) {
+    if constexpr (OWN) {
+      if (tile >= p.ct) {
+        const int j0 = (tile - p.ct) * KT;  // first own entry of the tile
+#pragma unroll
+        for (int i = 0; i < LPT; ++i) {
+          const int c = i * NT + tid;
+          if (NCH % NT != 0 && c >= NCH) break;
+          kreg[set][i] = __builtin_amdgcn_raw_buffer_load_b128(ksrs, c * 16, (uint32_t)j0 * (DH * 2), 0);
+          vreg[set][i] = __builtin_amdgcn_raw_buffer_load_b128(vtsrs, c * 16, (uint32_t)(j0 / 32) * (DH * 64), 0);
+        }
+        return;
+      }
+    }
     const int kb0 = k_begin + tile * KT;
 #pragma unroll
     for (int i = 0; i < LPT; ++i) {
@@ -246,8 +282,25 @@ __global__ __launch_bounds__(kThreadsBf16, 1) void attn_bf16_kernel(AttnParams p
       }
     }
   };
-  // keys >= k_end of tile t set to -inf
+  // keys >= k_end of tile t set to -inf; own entries j > m of query m set to -inf
   auto mask = [&](f32x16 (&s)[NKT][QT], int t) {
+    if constexpr (OWN) {
+      if (t >= p.ct) {
+        const int j0 = (t - p.ct) * KT;
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) {
+          const int mq = min(row_base + qt * 32 + l32, p.rows - 1) / p.G;
+#pragma unroll
+          for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+              const int j = j0 + kt * 32 + 8 * (e >> 2) + 4 * h32 + (e & 3);
+              if (j > mq) s[kt][qt][e] = -INFINITY;
+            }
+        }
+        return;
+      }
+    }
     const int tb = k_begin + t * KT;
     if (tb + KT > k_end) {
 #pragma unroll
@@ -482,8 +535,9 @@ __global__ __launch_bounds__(kThreadsBf16, 1) void attn_bf16_kernel(AttnParams p
   }
 }
 
-template <int DH, bool GATHER, bool PARTIAL>
+template <int DH, bool GATHER, bool PARTIAL, bool OWN>
 __global__ __launch_bounds__(256) void attn_f32_kernel(AttnParams p) {
+  static_assert(!(OWN && PARTIAL), "own entries are attended without a key split");
   constexpr int KT = kKeyTileF32;
   constexpr int C4 = DH / 4;
   __shared__ f32x4 Ks[KT * C4];
@@ -514,6 +568,37 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnParams p) {
   }
   float mrun = -INFINITY, l = 0.f;
 
+  // one key: online-softmax update of (mrun, l, o) with row kk of the LDS tiles
+  auto attend_key = [&](int kk) {
+    f32x4 acc = {};
+#pragma unroll
+    for (int i = 0; i < C4; ++i) {
+      const f32x4 kv = Ks[kk * C4 + i];
+      acc[0] = fmaf(q[i][0], kv[0], acc[0]);
+      acc[1] = fmaf(q[i][1], kv[1], acc[1]);
+      acc[2] = fmaf(q[i][2], kv[2], acc[2]);
+      acc[3] = fmaf(q[i][3], kv[3], acc[3]);
+    }
+    const float sc = ((acc[0] + acc[1]) + (acc[2] + acc[3])) * p.c;
+    if (sc > mrun) {
+      const float a = expf(mrun - sc);
+      l *= a;
+#pragma unroll
+      for (int i = 0; i < C4; ++i) o[i] *= a;
+      mrun = sc;
+    }
+    const float pe = expf(sc - mrun);
+    l += pe;
+#pragma unroll
+    for (int i = 0; i < C4; ++i) {
+      const f32x4 vv = Vs[kk * C4 + i];
+      o[i][0] = fmaf(pe, vv[0], o[i][0]);
+      o[i][1] = fmaf(pe, vv[1], o[i][1]);
+      o[i][2] = fmaf(pe, vv[2], o[i][2]);
+      o[i][3] = fmaf(pe, vv[3], o[i][3]);
+    }
+  };
+
   for (int tb = k_begin; tb < k_end; tb += KT) {
     const int nk = min(KT, k_end - tb);
     for (int c = tid; c < KT * C4; c += 256) {
@@ -524,36 +609,26 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnParams p) {
       Vs[c] = *((const f32x4*)(Vb + (int64_t)src * DH) + col);
     }
     __syncthreads();
-    for (int kk = 0; kk < nk; ++kk) {
-      f32x4 acc = {};
-#pragma unroll
-      for (int i = 0; i < C4; ++i) {
-        const f32x4 kv = Ks[kk * C4 + i];
-        acc[0] = fmaf(q[i][0], kv[0], acc[0]);
-        acc[1] = fmaf(q[i][1], kv[1], acc[1]);
-        acc[2] = fmaf(q[i][2], kv[2], acc[2]);
-        acc[3] = fmaf(q[i][3], kv[3], acc[3]);
-      }
-      const float sc = ((acc[0] + acc[1]) + (acc[2] + acc[3])) * p.c;
-      if (sc > mrun) {
-        const float a = expf(mrun - sc);
-        l *= a;
-#pragma unroll
-        for (int i = 0; i < C4; ++i) o[i] *= a;
-        mrun = sc;
-      }
-      const float pe = expf(sc - mrun);
-      l += pe;
-#pragma unroll
-      for (int i = 0; i < C4; ++i) {
-        const f32x4 vv = Vs[kk * C4 + i];
-        o[i][0] = fmaf(pe, vv[0], o[i][0]);
-        o[i][1] = fmaf(pe, vv[1], o[i][1]);
-        o[i][2] = fmaf(pe, vv[2], o[i][2]);
-        o[i][3] = fmaf(pe, vv[3], o[i][3]);
-      }
-    }
+    for (int kk = 0; kk < nk; ++kk) attend_key(kk);
     __syncthreads();
+  }
+  if constexpr (OWN) {
+    // own entries 0..m of this thread's query m, up to the workgroup's last query
+    const float* Ksb = (const float*)p.Ks + (int64_t)g * p.Ms * DH;
+    const float* Vsb = (const float*)p.Vs + (int64_t)g * p.Ms * DH;
+    const int last_q = min(p.rows - 1, rt * kRowsWG + kRowsWG - 1) / p.G;
+    for (int tb = 0; tb <= last_q; tb += KT) {
+      for (int c = tid; c < KT * C4; c += 256) {
+        const int row = c / C4, col = c % C4;
+        const int src = min(tb + row, p.Ms - 1);
+        Ks[c] = *((const f32x4*)(Ksb + (int64_t)src * DH) + col);
+        Vs[c] = *((const f32x4*)(Vsb + (int64_t)src * DH) + col);
+      }
+      __syncthreads();
+      const int nk = min(KT, m - tb + 1);  // own entries tb .. m of this query
+      for (int kk = 0; kk < nk; ++kk) attend_key(kk);
+      __syncthreads();
+    }
   }
 
   if (r >= p.rows) return;
@@ -606,27 +681,32 @@ template <int DH>
 hipError_t launch_dh(const AttnShape& s, const AttnPlan& pl, AttnParams& p, bool gather,
                      bool psplit, hipStream_t st) {
   const bool part = pl.n_split > 1;
+  const bool own = s.Ms > 0;
   dim3 grid(pl.grid), block(256);
   if (s.bf16) {
     const dim3 bblock(kThreadsBf16);
     // fast path, then the lazy-rescale fixup for any work item it handed back
-#define PKV_L(G_, P_, S_)                                                               \
-  do {                                                                                  \
-    hipLaunchKernelGGL((attn_bf16_kernel<DH, G_, P_, S_, false>), grid, bblock, 0, st, p); \
-    hipLaunchKernelGGL((attn_bf16_kernel<DH, G_, P_, S_, true>), grid, bblock, 0, st, p);  \
+#define PKV_L(G_, P_, S_, O_)                                                                 \
+  do {                                                                                        \
+    hipLaunchKernelGGL((attn_bf16_kernel<DH, G_, P_, S_, false, O_>), grid, bblock, 0, st, p); \
+    hipLaunchKernelGGL((attn_bf16_kernel<DH, G_, P_, S_, true, O_>), grid, bblock, 0, st, p);  \
   } while (0)
-    if (gather) {
-      if (psplit) { if (part) PKV_L(true, true, true); else PKV_L(true, true, false); }
-      else { if (part) PKV_L(true, false, true); else PKV_L(true, false, false); }
+    if (own) {
+      if (gather) { if (psplit) PKV_L(true, true, false, true); else PKV_L(true, false, false, true); }
+      else { if (psplit) PKV_L(false, true, false, true); else PKV_L(false, false, false, true); }
+    } else if (gather) {
+      if (psplit) { if (part) PKV_L(true, true, true, false); else PKV_L(true, true, false, false); }
+      else { if (part) PKV_L(true, false, true, false); else PKV_L(true, false, false, false); }
     } else {
-      if (psplit) { if (part) PKV_L(false, true, true); else PKV_L(false, true, false); }
-      else { if (part) PKV_L(false, false, true); else PKV_L(false, false, false); }
+      if (psplit) { if (part) PKV_L(false, true, true, false); else PKV_L(false, true, false, false); }
+      else { if (part) PKV_L(false, false, true, false); else PKV_L(false, false, false, false); }
     }
 #undef PKV_L
   } else {
-#define PKV_L(G_, S_) hipLaunchKernelGGL((attn_f32_kernel<DH, G_, S_>), grid, block, 0, st, p)
-    if (gather) { if (part) PKV_L(true, true); else PKV_L(true, false); }
-    else { if (part) PKV_L(false, true); else PKV_L(false, false); }
+#define PKV_L(G_, S_, O_) hipLaunchKernelGGL((attn_f32_kernel<DH, G_, S_, O_>), grid, block, 0, st, p)
+    if (own) { if (gather) PKV_L(true, false, true); else PKV_L(false, false, true); }
+    else if (gather) { if (part) PKV_L(true, true, false); else PKV_L(true, false, false); }
+    else { if (part) PKV_L(false, true, false); else PKV_L(false, false, false); }
 #undef PKV_L
   }
   hipError_t e = hipGetLastError();
@@ -658,7 +738,7 @@ AttnPlan plan_attention(const AttnShape& s) {
   const double tile_s = (double)kt * kRowsWG * s.dh * 4.0 / (s.bf16 ? 4e12 : 0.25e12);
   double best = 1e300;
   int best_s = 1;
-  for (int sp = 1; sp <= 64 && sp <= ntiles; ++sp) {
+  for (int sp = 1; sp <= (s.Ms > 0 ? 1 : 64) && sp <= ntiles; ++sp) {
     const int64_t tps = (ntiles + sp - 1) / sp;
     const int64_t waves = (items * sp + (int64_t)slots - 1) / (int64_t)slots;
     double cost = (double)waves * tps * tile_s;
@@ -681,13 +761,16 @@ AttnPlan plan_attention(const AttnShape& s) {
   if (s.bf16) {
     pl.ws_bytes += align_up((size_t)pl.total_items * sizeof(int));
     pl.ws_bytes += align_up((size_t)s.Hkv * ntiles * 32 * s.dh * 2);  // V^T tiles
+    if (s.Ms > 0)  // V^T tiles of the own entries
+      pl.ws_bytes += align_up((size_t)s.Hkv * ((s.Ms + kKeyTile - 1) / kKeyTile) * 32 * s.dh * 2);
   }
   return pl;
 }
 
 hipError_t launch_attention(const AttnShape& s, const void* Q, const void* K, const void* V,
                             const int32_t* idx, int64_t src_rows, int64_t src_valid,
-                            float scale, bool psplit, float* O, void* ws, hipStream_t st) {
+                            float scale, bool psplit, float* O, void* ws, hipStream_t st,
+                            const void* Ks, const void* Vs) {
   const AttnPlan pl = plan_attention(s);
   AttnParams p{};
   p.Q = Q;
@@ -695,6 +778,10 @@ hipError_t launch_attention(const AttnShape& s, const void* Q, const void* K, co
   p.V = V;
   p.idx = idx;
   p.O = O;
+  p.Ks = Ks;
+  p.Vs = Vs;
+  p.Ms = (int)s.Ms;
+  p.ct = (int)((s.Nk + (s.bf16 ? kKeyTile : kKeyTileF32) - 1) / (s.bf16 ? kKeyTile : kKeyTileF32));
   size_t off = 0;
   if (pl.n_split > 1) {
     const size_t n = (size_t)s.Hkv * pl.n_split * s.M * (s.Hq / s.Hkv);
@@ -716,6 +803,22 @@ hipError_t launch_attention(const AttnShape& s, const void* Q, const void* K, co
   hipLaunchKernelGGL((vt_kernel<D_, G_>), vg, vb, 0, st, Vb, idx, src_rows, (int)s.Nk, (int)vt_tiles, vt)
     if (s.dh == 128) { if (idx) PKV_VT(128, true); else PKV_VT(128, false); }
     else { if (idx) PKV_VT(64, true); else PKV_VT(64, false); }
+    if (s.Ms > 0) {
+      // V^T tiles of the chunk's own entries, after the cache's
+      off += align_up((size_t)s.Hkv * vt_tiles * 32 * s.dh * 2);
+      const int own_tiles = (int)((s.Ms + kKeyTile - 1) / kKeyTile);
+      __bf16* vts = (__bf16*)((char*)ws + off);
+      p.Vts = vts;
+      p.own_tiles = own_tiles;
+      const dim3 og((unsigned)own_tiles, (unsigned)s.Hkv);
+      const __bf16* Vsb = (const __bf16*)Vs;
+      if (s.dh == 128)
+        hipLaunchKernelGGL((vt_kernel<128, false>), og, vb, 0, st, Vsb, nullptr, s.Ms, (int)s.Ms,
+                           own_tiles, vts);
+      else
+        hipLaunchKernelGGL((vt_kernel<64, false>), og, vb, 0, st, Vsb, nullptr, s.Ms, (int)s.Ms,
+                           own_tiles, vts);
+    }
 #undef PKV_VT
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

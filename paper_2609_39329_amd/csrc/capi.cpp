@@ -152,6 +152,37 @@ int patchkv_attend_compressed(int dtype, const void* Q, const void* K, const voi
                                     (hipStream_t)stream));
 }
 
+size_t patchkv_attend_chunk_workspace_bytes(int dtype, int64_t M, int64_t n_cache, int Hq, int Hkv,
+                                            int dh) {
+  if (check_attn_shape(dtype, M, n_cache, Hq, Hkv, dh) != PATCHKV_OK) return 0;
+  if (!src_rows_ok(dtype, M, dh)) return 0;
+  AttnShape sh = attn_shape(dtype, M, n_cache, Hq, Hkv, dh);
+  sh.Ms = M;
+  return plan_attention(sh).ws_bytes;
+}
+
+int patchkv_attend_chunk(int dtype, const void* Q, const void* K, const void* V,
+                         const int32_t* idx, int64_t n_src, int64_t n_cache, const void* Ks,
+                         const void* Vs, int64_t M, int Hq, int Hkv, int dh, float scale,
+                         int p_terms, float* O, void* workspace, size_t workspace_bytes,
+                         void* stream) {
+  if (!Q || !K || !V || !Ks || !Vs || !O) return PATCHKV_E_NULL;
+  int s = check_attn_shape(dtype, M, n_cache, Hq, Hkv, dh);
+  if (s) return s;
+  if (!src_rows_ok(dtype, n_src, dh) || !src_rows_ok(dtype, M, dh)) return PATCHKV_E_SHAPE;
+  if (!idx && n_cache > n_src) return PATCHKV_E_SHAPE;
+  if (p_terms != 1 && p_terms != 2) return PATCHKV_E_VALUE;
+  if (!finite_pos(scale)) return PATCHKV_E_VALUE;
+  if (!al16(Q) || !al16(K) || !al16(V) || !al16(Ks) || !al16(Vs) || !al16(O))
+    return PATCHKV_E_VALUE;
+  AttnShape sh = attn_shape(dtype, M, n_cache, Hq, Hkv, dh);
+  sh.Ms = M;
+  s = check_ws(workspace, workspace_bytes, plan_attention(sh).ws_bytes);
+  if (s) return s;
+  return status_of(launch_attention(sh, Q, K, V, idx, n_src, n_src, scale, p_terms == 2, O,
+                                    workspace, (hipStream_t)stream, Ks, Vs));
+}
+
 size_t patchkv_targets_workspace_bytes(int w_dtype, int64_t M, int64_t d_in, int64_t d_out) {
   if (w_dtype != PATCHKV_BF16 && w_dtype != PATCHKV_F32) return 0;
   if (check_stats_dims(M, d_in, d_out)) return 0;

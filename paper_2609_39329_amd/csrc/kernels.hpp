@@ -13,6 +13,7 @@ struct AttnShape {
   int64_t Nk;        // cache entries attended
   int Hq, Hkv, dh;
   bool bf16;         // input dtype: bf16 (MFMA path) or f32
+  int64_t Ms = 0;    // own entries of a reference chunk (0, or M: query m sees own 0..m)
 };
 
 struct AttnPlan {
@@ -30,9 +31,11 @@ AttnPlan plan_attention(const AttnShape& s);
 // Q [M][Hq][dh]; K, V rows of KV head g start at (g * src_rows) * dh; when idx is
 // non-null, cache entry n is row idx[n] (clamped into [0, src_valid)).
 // psplit: form P V from a two-term bf16 split of P (bf16 path only).
+// s.Ms > 0: Ks, Vs [Hkv][Ms][dh] are the chunk's own entries (causal, after the cache).
 hipError_t launch_attention(const AttnShape& s, const void* Q, const void* K, const void* V,
                             const int32_t* idx, int64_t src_rows, int64_t src_valid,
-                            float scale, bool psplit, float* O, void* ws, hipStream_t st);
+                            float scale, bool psplit, float* O, void* ws, hipStream_t st,
+                            const void* Ks = nullptr, const void* Vs = nullptr);
 
 // ---------------------------------------------------------------- statistics (fp32 acc)
 size_t targets_ws_bytes(int64_t M, int64_t din, int64_t dout);

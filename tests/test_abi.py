@@ -86,6 +86,29 @@ def test_attend_validation(L):
     assert r == B.E_SHAPE                                 # B = 0
 
 
+def test_attend_chunk_validation(L):
+    def chunk(dt=B.BF16, Q=FAKE, K=FAKE, V=FAKE, idx=None, n_src=64, n_cache=64, Ks=FAKE, Vs=FAKE,
+              M=8, Hq=4, Hkv=2, dh=128, scale=0.1, p_terms=1, O=FAKE, ws=None, wsb=0):
+        return L.patchkv_attend_chunk(dt, Q, K, V, idx, n_src, n_cache, Ks, Vs, M, Hq, Hkv, dh,
+                                      scale, p_terms, O, ws, wsb, None)
+    assert chunk(Ks=None) == B.E_NULL
+    assert chunk(Vs=None) == B.E_NULL
+    assert chunk(dt=B.F64) == B.E_DTYPE
+    assert chunk(n_cache=0) == B.E_SHAPE
+    assert chunk(n_cache=65) == B.E_SHAPE                 # more cache rows than K holds
+    assert chunk(idx=FAKE, n_cache=65) == B.E_WORKSPACE   # a gather may pick any n_cache rows
+    assert chunk(M=1 << 24) == B.E_SHAPE                  # own rows: 2^24 * 128 * 2 = 2^32 bytes
+    assert chunk(p_terms=3) == B.E_VALUE
+    assert chunk(scale=-1.0) == B.E_VALUE
+    assert chunk(Ks=FAKE + 8) == B.E_VALUE                # misaligned
+    assert chunk() == B.E_WORKSPACE
+    # bf16 workspace: V^T tiles of the cache and of the own entries, one flag per item
+    vt = 2 * (32 * 128 * 2) + 4 * (32 * 128 * 2)          # Hkv=2: 64 cache keys, 8 own keys
+    w = L.patchkv_attend_chunk_workspace_bytes(B.BF16, 8, 64, 4, 2, 128)
+    assert vt <= w <= vt + 4096
+    assert L.patchkv_attend_chunk_workspace_bytes(B.F32, 8, 64, 4, 2, 128) == 0
+
+
 def test_targets_validation(L):
     f = L.patchkv_compute_targets
     assert f(B.BF16, None, FAKE, FAKE, 4, 8, 8, 1, FAKE, None, 0, None) == B.E_NULL
