@@ -4,7 +4,9 @@ A step is one pass of the whole hot path over one batch of synthetic input: for
 every layer of the workload, attention of the M reference queries over the full
 cache and over the compressed cache, targets, normal equations and the ridge
 solve (the same five library calls, in the same order, that
-patchkv_compute_layer_patch makes). The default workload is the 32-layer
+patchkv_compute_layer_patch makes; for a chunked reference set, the two
+attention passes, targets and statistics of every chunk, then one solve). The
+default workload is the 32-layer
 Llama-3-8B-shaped patch build over a 172,032-token context (1 % cache budget,
 4,096 reference queries per layer). All layer inputs are resident in HBM before
 the timed region starts.
@@ -78,15 +80,17 @@ def parse():
 
 
 class LayerDev:
-    """One layer's inputs on the device."""
+    """One layer's inputs on the device (and, for a chunked reference set, every
+    chunk's queries and own keys and values)."""
 
-    def __init__(self, inp, torch, dev):
+    def __init__(self, inp, torch, dev, chunks=()):
         def t(a):
             x = torch.from_numpy(np.ascontiguousarray(a))
             if inp.dtype == "bf16":
                 x = x.view(torch.bfloat16)
             return x.to(dev, non_blocking=False)
         self.Q, self.K, self.V, self.W = t(inp.Q), t(inp.K), t(inp.V), t(inp.W)
+        self.chunks = [(t(c.Q), t(c.Ks), t(c.Vs)) for c in chunks]
         self.idx = (torch.from_numpy(inp.idx).to(dev) if inp.idx is not None else None)
         self.Kc = t(inp.Kc) if inp.Kc is not None else None
         self.Vc = t(inp.Vc) if inp.Vc is not None else None
@@ -127,6 +131,27 @@ def layer_steps(pkv, cfg, L, bufs, li: int, events=None):
     pkv.solve_patch(bufs.G, bufs.C, cfg.lam, dW=bufs.dW[li], info=bufs.info[li:li + 1])
 
 
+def chunked_layer_steps(pkv, cfg, L, bufs, li: int, events=None):
+    """One layer patch from a chunked reference set: for each chunk, attention over
+    the full cache and over the compressed cache, each plus the chunk's own causal
+    prefix, targets and statistics (summed over chunks); then one solve. ``events``
+    holds a (start, end) pair per chunk around its full-cache attention."""
+    acc = pkv.F32 if bufs.acc == 1 else pkv.F64
+    for j, (Q, Ks, Vs) in enumerate(L.chunks):
+        if events is not None:
+            events[j][0].record()
+        pkv.attend_chunk(Q, L.K, L.V, Ks, Vs, scale=cfg.scale, p_terms=1, O=bufs.Of)
+        if events is not None:
+            events[j][1].record()
+        if L.idx is not None:
+            pkv.attend_chunk(Q, L.K, L.V, Ks, Vs, idx=L.idx, scale=cfg.scale, p_terms=2, O=bufs.Oc)
+        else:
+            pkv.attend_chunk(Q, L.Kc, L.Vc, Ks, Vs, scale=cfg.scale, p_terms=2, O=bufs.Oc)
+        pkv.compute_targets(bufs.Of, bufs.Oc, L.W, rho=1, T=bufs.T)
+        pkv.accumulate_normal_eq(bufs.Oc, bufs.T, G=bufs.G, C=bufs.C, acc=acc, accumulate=j > 0)
+    pkv.solve_patch(bufs.G, bufs.C, cfg.lam, dW=bufs.dW[li], info=bufs.info[li:li + 1])
+
+
 def cpu_baseline(cfg, rows: int) -> dict:
     """The fp64 oracle on a bounded sample of one layer, scaled to s / layer patch.
 
@@ -135,7 +160,7 @@ def cpu_baseline(cfg, rows: int) -> dict:
     by M / rows), plus the complete d x d ridge solve (independent of M).
     """
     import oracle
-    from workloads import make_layer_inputs
+    from workloads import make_chunk_inputs, make_layer_inputs
     try:
         from threadpoolctl import threadpool_info
         blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
@@ -144,32 +169,44 @@ def cpu_baseline(cfg, rows: int) -> dict:
     cores = len(os.sched_getaffinity(0))
     inp = make_layer_inputs(cfg, 0)
     dt = inp.dtype
+    ch = make_chunk_inputs(inp, 0, cfg.M) if cfg.chunks > 1 else None
     sel = np.linspace(0, cfg.M - 1, rows).astype(np.int64)
     t0 = time.perf_counter()
-    Q = oracle.decode(inp.Q[sel], dt)
     K, V = oracle.decode(inp.K, dt), oracle.decode(inp.V, dt)
     W = oracle.decode(inp.W, dt)
-    Of = oracle.attention(Q, K, V, inp.scale)
     if inp.idx is not None:
         Kc, Vc = oracle.gather_cache(K, V, inp.idx)
     else:
         Kc, Vc = oracle.decode(inp.Kc, dt), oracle.decode(inp.Vc, dt)
-    Oc = oracle.attention(Q, Kc, Vc, inp.scale)
+    if ch is None:
+        Q = oracle.decode(inp.Q[sel], dt)
+        Of = oracle.attention(Q, K, V, inp.scale)
+        Oc = oracle.attention(Q, Kc, Vc, inp.scale)
+    else:
+        # the first ``rows`` tokens of chunk 0 (a chunk's prefix is itself a chunk)
+        Q = oracle.decode(ch.Q[:rows], dt)
+        Ks, Vs = oracle.decode(ch.Ks[:, :rows], dt), oracle.decode(ch.Vs[:, :rows], dt)
+        Of = oracle.attention_chunk(Q, K, V, Ks, Vs, inp.scale)
+        Oc = oracle.attention_chunk(Q, Kc, Vc, Ks, Vs, inp.scale)
     T = oracle.targets(Of, Oc, W, 1)
     G, C = oracle.normal_equations(Oc, T)
     t_rows = time.perf_counter() - t0
+    tokens = cfg.M * cfg.chunks
     # the solve at full size needs a well-posed full-size G: scale the sampled
-    # statistics up to M rows' worth of mass (its cost does not depend on G's values)
+    # statistics up to all reference tokens' worth of mass (its cost does not
+    # depend on G's values)
     t1 = time.perf_counter()
-    oracle.solve_patch(G * (cfg.M / rows), C * (cfg.M / rows), cfg.lam)
+    oracle.solve_patch(G * (tokens / rows), C * (tokens / rows), cfg.lam)
     t_solve = time.perf_counter() - t1
-    est = t_rows * (cfg.M / rows) + t_solve
+    est = t_rows * (tokens / rows) + t_solve
+    what = (f"the first {rows} tokens of reference chunk 0 (of {cfg.chunks} chunks x {cfg.M})"
+            if ch is not None else f"{rows} of {cfg.M} reference queries")
     return {"value": est, "unit": "s/layer-patch", "cores": cores, "blas_threads": blas_threads,
             "kind": "oracle",
             "sample": f"config {cfg.cid} layer 0: fp64 attention (full + compressed), targets and "
-                      f"statistics for {rows} of {cfg.M} reference queries "
-                      f"({t_rows:.2f} s, scaled x{cfg.M / rows:.0f}) + full {cfg.d}x{cfg.d} "
-                      f"Cholesky solve ({t_solve:.2f} s); input decoding included"}
+                      f"statistics for {what} ({t_rows:.2f} s, scaled x{tokens / rows:.0f}) + "
+                      f"full {cfg.d}x{cfg.d} Cholesky solve ({t_solve:.2f} s); input decoding "
+                      f"included"}
 
 
 def main():
@@ -182,7 +219,7 @@ def main():
     import torch
 
     import paper_2609_39329_amd as pkv
-    from workloads import get_config, make_layer_inputs
+    from workloads import get_config, make_chunk_inputs, make_layer_inputs
 
     cfg = get_config(args.config)
     nl = cfg.layers if args.layers is None else min(args.layers, cfg.layers)
@@ -192,20 +229,26 @@ def main():
     t0 = time.perf_counter()
     layers = []
     for layer in range(nl):
-        layers.append(LayerDev(make_layer_inputs(cfg, layer), torch, dev))
+        inp = make_layer_inputs(cfg, layer)
+        chunks = [make_chunk_inputs(inp, j, cfg.M) for j in range(cfg.chunks)] if cfg.chunks > 1 else ()
+        layers.append(LayerDev(inp, torch, dev, chunks))
         if layer % 8 == 7 or layer == nl - 1:
             log(f"[bench] inputs of {layer + 1}/{nl} layers resident ({time.perf_counter() - t0:.1f} s)")
     torch.cuda.synchronize()
 
     M, d = cfg.M, cfg.d
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(nl)]
+    chunked = cfg.chunks > 1
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(cfg.chunks)] for _ in range(nl)]
 
     bufs = Buffers(cfg, torch, dev, nl)
 
     def step(timed: bool):
         for li, L in enumerate(layers):
-            layer_steps(pkv, cfg, L, bufs, li, ev[li] if timed else None)
+            if chunked:
+                chunked_layer_steps(pkv, cfg, L, bufs, li, ev[li] if timed else None)
+            else:
+                layer_steps(pkv, cfg, L, bufs, li, ev[li][0] if timed else None)
 
     for w in range(args.warmup):
         step(False)
@@ -217,7 +260,7 @@ def main():
     for s in range(args.steps):
         step(True)
         torch.cuda.synchronize()
-        attn_ms += [a.elapsed_time(b) for a, b in ev]
+        attn_ms += [a.elapsed_time(b) for pairs in ev for a, b in pairs]
         log(f"[bench] step {s + 1}/{args.steps} done")
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
@@ -227,8 +270,11 @@ def main():
 
     ms_step = elapsed / args.steps * 1e3
     s_layer = elapsed / (args.steps * nl)
-    att_flops_full = 4.0 * M * cfg.N * cfg.Hq * cfg.dh
-    att_flops_comp = 4.0 * M * cfg.B * cfg.Hq * cfg.dh
+    # per launch; a chunk's own causal prefix adds sum_m (m + 1) = M (M + 1) / 2 keys
+    own = M * (M + 1) / 2.0 if chunked else 0.0
+    att_flops_full = 4.0 * cfg.Hq * cfg.dh * (M * cfg.N + own)
+    att_flops_comp = 4.0 * cfg.Hq * cfg.dh * (M * cfg.B + own)
+    launches = cfg.chunks                               # full-cache attention launches per layer
     t_attn = float(np.mean(attn_ms)) * 1e-3            # dominant kernel: full-cache attention
     peak = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_F32_TFLOPS
     achieved = att_flops_full / t_attn / 1e12
@@ -250,17 +296,21 @@ def main():
         "data": "synthetic (seeded; shapes and distributions of the workload)",
         "config": {"workload": cfg.name, "config_id": cfg.cid, "layers_per_step": nl,
                    "N": cfg.N, "B": cfg.B, "M": M, "d": d, "Hq": cfg.Hq, "Hkv": cfg.Hkv,
-                   "dh": cfg.dh, "lambda": cfg.lam, "compressed_cache": cfg.cache},
+                   "dh": cfg.dh, "lambda": cfg.lam, "compressed_cache": cfg.cache,
+                   "reference_chunks": cfg.chunks,
+                   "own_causal_prefix": chunked},
         "attention_full_ms": t_attn * 1e3,
         "attention_full_tflops": achieved,
         "attention_full_frac_of_peak": achieved / peak,
-        "attention_total_tflops_per_layer_time": (att_flops_full + att_flops_comp) / s_layer / 1e12,
+        "attention_total_tflops_per_layer_time":
+            launches * (att_flops_full + att_flops_comp) / s_layer / 1e12,
         "context_tokens_per_s": cfg.N / s_layer,
         "kv_stream_gbs_full_attention": kv_bytes / t_attn / 1e9,
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                      "frac": achieved / peak, "traffic": traffic,
-                     "kernel": ("patchkv_attend_full: vt_kernel + attn_bf16_kernel fast path + fixup"
-                                if cfg.dtype == "bf16" else "patchkv_attend_full: attn_f32_kernel"),
+                     "kernel": (("patchkv_attend_chunk" if chunked else "patchkv_attend_full")
+                                + (": vt_kernel + attn_bf16_kernel fast path + fixup"
+                                   if cfg.dtype == "bf16" else ": attn_f32_kernel")),
                      "flops_per_launch": att_flops_full,
                      "traffic_unit": "HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
                      "traffic_source": os.path.relpath(TRAFFIC_PROFILE, ROOT) if traffic else None},

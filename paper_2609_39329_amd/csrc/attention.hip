@@ -27,8 +27,10 @@
 //
 // Chunked reference sets (OWN = true): the queries are one chunk's tokens, and
 // token m also attends to the chunk's own entries 0..m (its causal prefix), which
-// follow the cache in the key order: key tiles [0, ct) are the cache's, tiles
-// ct.. the own entries', masked per query. Such calls use no key split.
+// follow the cache in the key order: a work item's first key tiles are its range
+// of the cache, and the work item of the last key range then takes the own
+// entries' tiles, masked per query. Every range keeps at least one cache key, so
+// every row of every partial result has a finite maximum.
 #include <math.h>
 
 #include <type_traits>
@@ -74,11 +76,11 @@ struct AttnParams {
   int total_items, per_xcd;
   float c;  // bf16: scale * log2(e); f32: scale
   // own entries of a reference chunk (OWN kernels): Ks, Vs [Hkv][Ms][dh]; Vts their
-  // V^T tiles (bf16); ct = number of cache key tiles before them
+  // V^T tiles (bf16)
   const void* Ks;
   const void* Vs;
   const __bf16* Vts;
-  int Ms, own_tiles, ct;
+  int Ms, own_tiles;
 };
 
 // V -> V^T in 32-key tiles, so that the P V product reads V with plain 16-byte LDS
@@ -133,7 +135,6 @@ __global__ __launch_bounds__(256) void vt_kernel(const __bf16* __restrict__ V,
 // only for marked work items, overwriting their outputs.
 template <int DH, bool GATHER, bool PSPLIT, bool PARTIAL, bool SAFE, bool OWN>
 __global__ __launch_bounds__(kThreadsBf16, 1) void attn_bf16_kernel(AttnParams p) {
-  static_assert(!(OWN && PARTIAL), "own entries are attended without a key split");
   constexpr int KT = kKeyTile;
   constexpr int NKT = KT / 32;  // 32-key MFMA tiles per iteration
   constexpr int KP = DH + 8;   // K tile pitch (elements): conflict-free 16-byte row reads
@@ -162,11 +163,15 @@ __global__ __launch_bounds__(kThreadsBf16, 1) void attn_bf16_kernel(AttnParams p
   const int g = __builtin_amdgcn_readfirstlane(t2 / p.n_split);
   const int k_begin = split * p.keys_per_split;
   const int k_end = min(p.Nk, k_begin + p.keys_per_split);
-  // cache tiles, then (OWN) the own tiles up to this workgroup's last query
-  int ntiles = (k_end - k_begin + KT - 1) / KT;
-  if constexpr (OWN) {
+  // cache tiles [0, ct) of this key range, then (OWN, last range) the own tiles up
+  // to this workgroup's last query
+  // (tiles past ntiles are masked like keys past k_end, also in the other ranges)
+  const int ct = (k_end - k_begin + KT - 1) / KT;
+  const bool own_range = OWN && split == p.n_split - 1;
+  int ntiles = ct;
+  if (own_range) {
     const int last_q = min(p.rows - 1, rt * kRowsWG + kRowsWG - 1) / p.G;
-    ntiles = p.ct + last_q / KT + 1;
+    ntiles = ct + last_q / KT + 1;
   }
 
   const int tid = threadIdx.x;
@@ -208,8 +213,8 @@ __global__ __launch_bounds__(kThreadsBf16, 1) void attn_bf16_kernel(AttnParams p
   u32x4 kreg[NSET][LPT], vreg[NSET][LPT];
   auto load_tile_to = [&](int tile, int set) {
     if constexpr (OWN) {
-      if (tile >= p.ct) {
-        const int j0 = (tile - p.ct) * KT;  // first own entry of the tile
+      if (own_range && tile >= ct) {
+        const int j0 = (tile - ct) * KT;  // first own entry of the tile
 #pragma unroll
         for (int i = 0; i < LPT; ++i) {
           const int c = i * NT + tid;
@@ -285,8 +290,8 @@ __global__ __launch_bounds__(kThreadsBf16, 1) void attn_bf16_kernel(AttnParams p
   // keys >= k_end of tile t set to -inf; own entries j > m of query m set to -inf
   auto mask = [&](f32x16 (&s)[NKT][QT], int t) {
     if constexpr (OWN) {
-      if (t >= p.ct) {
-        const int j0 = (t - p.ct) * KT;
+      if (own_range && t >= ct) {
+        const int j0 = (t - ct) * KT;
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt) {
           const int mq = min(row_base + qt * 32 + l32, p.rows - 1) / p.G;
@@ -537,7 +542,6 @@ __global__ __launch_bounds__(kThreadsBf16, 1) void attn_bf16_kernel(AttnParams p
 
 template <int DH, bool GATHER, bool PARTIAL, bool OWN>
 __global__ __launch_bounds__(256) void attn_f32_kernel(AttnParams p) {
-  static_assert(!(OWN && PARTIAL), "own entries are attended without a key split");
   constexpr int KT = kKeyTileF32;
   constexpr int C4 = DH / 4;
   __shared__ f32x4 Ks[KT * C4];
@@ -612,7 +616,7 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnParams p) {
     for (int kk = 0; kk < nk; ++kk) attend_key(kk);
     __syncthreads();
   }
-  if constexpr (OWN) {
+  if (OWN && split == p.n_split - 1) {
     // own entries 0..m of this thread's query m, up to the workgroup's last query
     const float* Ksb = (const float*)p.Ks + (int64_t)g * p.Ms * DH;
     const float* Vsb = (const float*)p.Vs + (int64_t)g * p.Ms * DH;
@@ -692,8 +696,13 @@ hipError_t launch_dh(const AttnShape& s, const AttnPlan& pl, AttnParams& p, bool
     hipLaunchKernelGGL((attn_bf16_kernel<DH, G_, P_, S_, true, O_>), grid, bblock, 0, st, p);  \
   } while (0)
     if (own) {
-      if (gather) { if (psplit) PKV_L(true, true, false, true); else PKV_L(true, false, false, true); }
-      else { if (psplit) PKV_L(false, true, false, true); else PKV_L(false, false, false, true); }
+      if (gather) {
+        if (psplit) { if (part) PKV_L(true, true, true, true); else PKV_L(true, true, false, true); }
+        else { if (part) PKV_L(true, false, true, true); else PKV_L(true, false, false, true); }
+      } else {
+        if (psplit) { if (part) PKV_L(false, true, true, true); else PKV_L(false, true, false, true); }
+        else { if (part) PKV_L(false, false, true, true); else PKV_L(false, false, false, true); }
+      }
     } else if (gather) {
       if (psplit) { if (part) PKV_L(true, true, true, false); else PKV_L(true, true, false, false); }
       else { if (part) PKV_L(true, false, true, false); else PKV_L(true, false, false, false); }
@@ -704,7 +713,10 @@ hipError_t launch_dh(const AttnShape& s, const AttnPlan& pl, AttnParams& p, bool
 #undef PKV_L
   } else {
 #define PKV_L(G_, S_, O_) hipLaunchKernelGGL((attn_f32_kernel<DH, G_, S_, O_>), grid, block, 0, st, p)
-    if (own) { if (gather) PKV_L(true, false, true); else PKV_L(false, false, true); }
+    if (own) {
+      if (gather) { if (part) PKV_L(true, true, true); else PKV_L(true, false, true); }
+      else { if (part) PKV_L(false, true, true); else PKV_L(false, false, true); }
+    }
     else if (gather) { if (part) PKV_L(true, true, false); else PKV_L(true, false, false); }
     else { if (part) PKV_L(false, true, false); else PKV_L(false, false, false); }
 #undef PKV_L
@@ -738,7 +750,7 @@ AttnPlan plan_attention(const AttnShape& s) {
   const double tile_s = (double)kt * kRowsWG * s.dh * 4.0 / (s.bf16 ? 4e12 : 0.25e12);
   double best = 1e300;
   int best_s = 1;
-  for (int sp = 1; sp <= (s.Ms > 0 ? 1 : 64) && sp <= ntiles; ++sp) {
+  for (int sp = 1; sp <= 64 && sp <= ntiles; ++sp) {
     const int64_t tps = (ntiles + sp - 1) / sp;
     const int64_t waves = (items * sp + (int64_t)slots - 1) / (int64_t)slots;
     double cost = (double)waves * tps * tile_s;
@@ -781,7 +793,6 @@ hipError_t launch_attention(const AttnShape& s, const void* Q, const void* K, co
   p.Ks = Ks;
   p.Vs = Vs;
   p.Ms = (int)s.Ms;
-  p.ct = (int)((s.Nk + (s.bf16 ? kKeyTile : kKeyTileF32) - 1) / (s.bf16 ? kKeyTile : kKeyTileF32));
   size_t off = 0;
   if (pl.n_split > 1) {
     const size_t n = (size_t)s.Hkv * pl.n_split * s.M * (s.Hq / s.Hkv);

@@ -8,6 +8,9 @@ from the fp64 oracle alone) the patch dW of the GPU path is compared on
 each against the 2e-2 bar for bf16 inputs. Attention outputs are compared on
 sampled query rows that the oracle computes one by one. The single-call entry
 point patchkv_compute_layer_patch must reproduce the step-by-step result bitwise.
+For the chunked workload (4 reference chunks of 5,120 tokens) the sampled attention
+rows are those of the last chunk, each computed by the oracle as plain attention of
+that token over the cache followed by the chunk's own entries up to it.
 """
 import glob
 import os
@@ -20,18 +23,18 @@ import torch
 import oracle
 import paper_2609_39329_amd as pkv
 from gpu_util import DEV, host, rel
-from workloads import CONFIGS, make_layer_inputs
+from workloads import CONFIGS, make_chunk_inputs, make_layer_inputs
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 sys.path.insert(0, ROOT)
-from bench import Buffers, LayerDev, layer_steps  # noqa: E402
+from bench import Buffers, LayerDev, chunked_layer_steps, layer_steps  # noqa: E402
 
 sys.path.insert(0, os.path.join(ROOT, "tests", "golden"))
 from make_oracle_fixtures import fixture_path, sample_rows, sketch_matrix  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
-CASES = [(1, 0), (2, 0), (4, 0), (3, 0), (3, 8), (3, 16), (3, 24), (3, 31)]
+CASES = [(1, 0), (2, 0), (4, 0), (3, 0), (3, 8), (3, 16), (3, 24), (3, 31), (5, 0)]
 TOL = 2e-2
 
 
@@ -44,9 +47,13 @@ def test_full_size_layer_patch(cid, layer):
     print(f"full-size parity: config {cid} ({cfg.name}) layer {layer}", flush=True)
     fx = np.load(path)
     inp = make_layer_inputs(cfg, layer)
-    L = LayerDev(inp, torch, DEV)
+    chunks = [make_chunk_inputs(inp, j, cfg.M) for j in range(cfg.chunks)] if cfg.chunks > 1 else ()
+    L = LayerDev(inp, torch, DEV, chunks)
     bufs = Buffers(cfg, torch, DEV, 1)
-    layer_steps(pkv, cfg, L, bufs, 0)
+    if chunks:
+        chunked_layer_steps(pkv, cfg, L, bufs, 0)
+    else:
+        layer_steps(pkv, cfg, L, bufs, 0)
     torch.cuda.synchronize()
     assert int(bufs.info[0].item()) == 0
     dW = host(bufs.dW[0])
@@ -62,19 +69,33 @@ def test_full_size_layer_patch(cid, layer):
     # attention outputs on sampled query rows, computed by the oracle row by row
     q_rows = np.random.default_rng([cid, layer, 7]).choice(cfg.M, 3, replace=False)
     dt = inp.dtype
-    Q = oracle.decode(inp.Q[q_rows], dt)
     K, V = oracle.decode(inp.K, dt), oracle.decode(inp.V, dt)
-    ref_f = oracle.attention(Q, K, V, inp.scale)
     if inp.idx is not None:
         Kc, Vc = oracle.gather_cache(K, V, inp.idx)
     else:
         Kc, Vc = oracle.decode(inp.Kc, dt), oracle.decode(inp.Vc, dt)
-    ref_c = oracle.attention(Q, Kc, Vc, inp.scale)
+    if chunks:
+        last = chunks[-1]
+        ref_f, ref_c = [], []
+        for m in q_rows:
+            q = oracle.decode(last.Q[m:m + 1], dt)
+            ks, vs = oracle.decode(last.Ks[:, :m + 1], dt), oracle.decode(last.Vs[:, :m + 1], dt)
+            ref_f.append(oracle.attention(q, np.concatenate([K, ks], 1), np.concatenate([V, vs], 1),
+                                          inp.scale)[0])
+            ref_c.append(oracle.attention(q, np.concatenate([Kc, ks], 1),
+                                          np.concatenate([Vc, vs], 1), inp.scale)[0])
+        ref_f, ref_c = np.array(ref_f), np.array(ref_c)
+    else:
+        Q = oracle.decode(inp.Q[q_rows], dt)
+        ref_f = oracle.attention(Q, K, V, inp.scale)
+        ref_c = oracle.attention(Q, Kc, Vc, inp.scale)
     e_of = rel(host(bufs.Of)[q_rows], ref_f)
     e_oc = rel(host(bufs.Oc)[q_rows], ref_c)
     print(f"  O_f rows {e_of:.3e}  O_c rows {e_oc:.3e}", flush=True)
     assert e_of <= 4e-3 and e_oc <= 5e-5
 
+    if chunks:
+        return
     # the single-call entry point runs the same kernels in the same order
     dW2, info2 = pkv.compute_layer_patch(L.Q, L.K, L.V, L.W, idx=L.idx, Kc=L.Kc, Vc=L.Vc,
                                          lam=cfg.lam, scale=cfg.scale)
