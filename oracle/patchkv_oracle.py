@@ -23,6 +23,13 @@ Alg. 1, the loop over reference chunks):
        causal prefix (cross-chunk attention dropped); the statistics of all
        chunks are summed before the single solve.
 
+and, for the MLP-shaped patch of the paper's own block (Sec. 2.3; Alg. 1):
+
+  (f3) h = SwiGLU features of the normalised attention output, W the
+       d_ff x d down-projection, z the attention output; targets
+       t = W (h - h') + (z - z'), a d_ff x d patch, and the student state the
+       patched block passes on, h' (W + Delta W) + z'.
+
 Readings where the paper is silent (each is also listed in the design notes):
 
 * Row-vector orientation. Activations are rows (one token per row), so with
@@ -37,6 +44,11 @@ Readings where the paper is silent (each is also listed in the design notes):
 * Attention: every query attends to every cache entry (no mask, RoPE already
   applied), softmax scale 1/sqrt(dh) unless given, GQA query head h reads KV
   head floor(h / (Hq / Hkv)).
+* MLP block (f3): the MLP reads the attention output through an RMS norm with
+  unit gain and eps = 1e-5, u = z / sqrt(mean(z^2) + eps), then
+  h = silu(u W_gate) * (u W_up), silu(x) = x / (1 + e^-x), and the block output
+  is y = h W + z (Llama- and Qwen-style SwiGLU; the block's own input and the
+  output projection of attention are folded into z).
 * Chunked reference set: token m of a chunk also attends to the chunk's own
   tokens 0..m (its causal prefix, itself included), whose keys and values the
   caller supplies. At the first block the teacher's and the student's chunk
@@ -54,7 +66,8 @@ import scipy.linalg
 __all__ = [
     "decode", "softmax_rows", "attention", "gather_cache", "targets",
     "normal_equations", "normal_equations_chunked", "ridge_lambda", "solve_patch",
-    "layer_patch", "attention_rows", "attention_chunk", "layer_patch_chunked",
+    "layer_patch", "attention_rows", "attention_chunk", "layer_patch_chunked", "rms_norm",
+    "silu", "mlp_features", "block_targets", "propagate_student", "mlp_layer_patch",
 ]
 
 
@@ -268,3 +281,63 @@ def layer_patch_chunked(inp, chunks, rho: int = 1, mode: str = "absolute",
         C += Cj
     lam_used = ridge_lambda(G0, inp.lam if lam is None else lam, mode)
     return {"dW": solve_patch(G0, C, lam_used), "lam": lam_used, "G": G0, "C": C}
+
+
+def rms_norm(X: np.ndarray, eps: float = 1e-5) -> np.ndarray:
+    """Row-wise RMS normalisation with unit gain: x / sqrt(mean(x^2) + eps)."""
+    return X / np.sqrt(np.mean(X * X, axis=1, keepdims=True) + eps)
+
+
+def silu(X: np.ndarray) -> np.ndarray:
+    """x * sigmoid(x) = x / (1 + e^-x)."""
+    return X / (1.0 + np.exp(-X))
+
+
+def mlp_features(Z: np.ndarray, Wg: np.ndarray, Wu: np.ndarray, eps: float = 1e-5) -> np.ndarray:
+    """The post-activation MLP intermediate h of Sec. 2.3 for a SwiGLU block whose
+    MLP reads the attention output z: u = rms_norm(z), h = silu(u Wg) * (u Wu).
+    Z [M, d], Wg and Wu [d, d_ff]; returns H [M, d_ff]."""
+    U = rms_norm(Z, eps)
+    return silu(U @ Wg) * (U @ Wu)
+
+
+def block_targets(Hf: np.ndarray, Hc: np.ndarray, W: np.ndarray, Zf: np.ndarray,
+                  Zc: np.ndarray) -> np.ndarray:
+    """Eq. 5 for the MLP-shaped block, row form: T = (Hf - Hc) W + (Zf - Zc), with
+    W [d_ff, d] the down-projection and Z the attention outputs."""
+    return (Hf - Hc) @ W + (Zf - Zc)
+
+
+def propagate_student(Hc: np.ndarray, W: np.ndarray, dW: np.ndarray, Zc: np.ndarray) -> np.ndarray:
+    """Student-state propagation (Alg. 1): the patched block's output on the
+    student's activations, Hc (W + dW) + Zc, the next block's student input."""
+    return Hc @ (W + dW) + Zc
+
+
+def mlp_layer_patch(inp, mlp, mode: str = "absolute", lam: float | None = None) -> dict:
+    """The MLP-shaped patch of one block (Sec. 2.3; Alg. 1), all in fp64.
+
+    ``inp``: a ``workloads`` LayerInputs (queries, caches); ``mlp``: MlpWeights
+    with Wg, Wu [d, d_ff] and Wd [d_ff, d] (stored form) and eps. Teacher and
+    student attention give z = O_f, O_c; h = mlp_features(z); the patch solves
+    Eq. 8 with G = Hc^T Hc, C = Hc^T T; the student state is propagated through
+    the patched block. Returns dW [d_ff, d], Y_student, Y_teacher, lambda, G, C.
+    """
+    dt = inp.dtype
+    Q, K, V = decode(inp.Q, dt), decode(inp.K, dt), decode(inp.V, dt)
+    Wg, Wu, Wd = decode(mlp.Wg, dt), decode(mlp.Wu, dt), decode(mlp.Wd, dt)
+    Of = attention(Q, K, V, inp.scale)
+    if inp.idx is not None:
+        Kc, Vc = gather_cache(K, V, inp.idx)
+    else:
+        Kc, Vc = decode(inp.Kc, dt), decode(inp.Vc, dt)
+    del K, V
+    Oc = attention(Q, Kc, Vc, inp.scale)
+    Hf = mlp_features(Of, Wg, Wu, mlp.eps)
+    Hc = mlp_features(Oc, Wg, Wu, mlp.eps)
+    T = block_targets(Hf, Hc, Wd, Of, Oc)
+    G0, C = normal_equations(Hc, T)
+    lam_used = ridge_lambda(G0, inp.lam if lam is None else lam, mode)
+    dW = solve_patch(G0, C, lam_used)
+    return {"dW": dW, "lam": lam_used, "G": G0, "C": C,
+            "Y_student": propagate_student(Hc, Wd, dW, Oc), "Y_teacher": Hf @ Wd + Of}

@@ -565,3 +565,128 @@ def test_chunk_pins_catch_planted_mistakes():
     assert check_attention_chunk_bruteforce(no_self) > 1e-2
     assert check_attention_chunk_bruteforce(no_mask) > 1e-2
     assert check_attention_chunk_bruteforce(own_from_cache_values) > 1e-2
+
+
+# ------------------------------------------------------------ MLP-shaped patch (f3)
+
+def brute_mlp_features(Z, Wg, Wu, eps):
+    M, d = Z.shape
+    d_ff = Wg.shape[1]
+    H = np.zeros((M, d_ff))
+    for i in range(M):
+        r = math.sqrt(sum(Z[i, k] ** 2 for k in range(d)) / d + eps)
+        u = [Z[i, k] / r for k in range(d)]
+        for j in range(d_ff):
+            g = sum(u[k] * Wg[k, j] for k in range(d))
+            up = sum(u[k] * Wu[k, j] for k in range(d))
+            H[i, j] = g / (1.0 + math.exp(-g)) * up
+    return H
+
+
+def check_mlp_features(fn):
+    rng = np.random.default_rng(31)
+    Z = rng.standard_normal((5, 6)) * 0.3
+    Wg, Wu = rng.standard_normal((6, 7)), rng.standard_normal((6, 7))
+    return rel(fn(Z, Wg, Wu, 1e-5), brute_mlp_features(Z, Wg, Wu, 1e-5))
+
+
+def check_block_targets(fn):
+    rng = np.random.default_rng(32)
+    Hf, Hc = rng.standard_normal((4, 6)), rng.standard_normal((4, 6))
+    Zf, Zc = rng.standard_normal((4, 3)), rng.standard_normal((4, 3))
+    W = rng.standard_normal((6, 3))
+    ref = np.array([[sum(W[k, j] * (Hf[i, k] - Hc[i, k]) for k in range(6)) + Zf[i, j] - Zc[i, j]
+                     for j in range(3)] for i in range(4)])
+    return rel(fn(Hf, Hc, W, Zf, Zc), ref)
+
+
+def test_silu_and_rms_norm_library_and_closed_forms():
+    x = np.linspace(-30, 30, 601)
+    assert rel(oracle.silu(x), x * scipy.special.expit(x)) < 1e-15
+    assert oracle.silu(np.zeros(1))[0] == 0.0
+    assert rel(oracle.silu(-x), oracle.silu(x) - x) < 1e-13          # silu(-x) = silu(x) - x
+    rng = np.random.default_rng(33)
+    Z = rng.standard_normal((9, 40)) * 3
+    ref = torch.nn.functional.rms_norm(torch.from_numpy(Z), (40,), eps=1e-5).numpy()
+    assert rel(oracle.rms_norm(Z, 1e-5), ref) < 1e-15
+    # unit gain: the output's mean square is ms / (ms + eps)
+    U = oracle.rms_norm(Z, 1e-5)
+    ms = np.mean(Z * Z, axis=1)
+    assert np.max(np.abs(np.mean(U * U, axis=1) - ms / (ms + 1e-5))) < 1e-14
+
+
+def test_mlp_features_bruteforce_and_library():
+    assert check_mlp_features(oracle.mlp_features) < 1e-13
+    rng = np.random.default_rng(34)
+    Z = rng.standard_normal((20, 32))
+    Wg, Wu = rng.standard_normal((32, 48)) / 6, rng.standard_normal((32, 48)) / 6
+    F = torch.nn.functional
+    z = torch.from_numpy(Z)
+    u = F.rms_norm(z, (32,), eps=1e-5)
+    ref = (F.silu(u @ torch.from_numpy(Wg)) * (u @ torch.from_numpy(Wu))).numpy()
+    assert rel(oracle.mlp_features(Z, Wg, Wu), ref) < 1e-14
+
+
+def test_block_targets_bruteforce():
+    assert check_block_targets(oracle.block_targets) < 1e-14
+
+
+def test_mlp_layer_patch_properties():
+    from workloads import make_mlp_weights
+    # compressed cache == full cache: no correction, the student already matches
+    inp = make_custom_inputs(M=12, N=80, B=80, Hq=4, Hkv=2, dh=8, dtype="f32", cache="identity",
+                             lam=1e-2, seed=3)
+    mlp = make_mlp_weights(inp, 48)
+    out = oracle.mlp_layer_patch(inp, mlp)
+    assert np.array_equal(out["dW"], np.zeros((48, 32)))
+    assert np.array_equal(out["Y_student"], out["Y_teacher"])
+    # fewer tokens than features: the per-token condition (Eq. 4) can be met exactly,
+    # so as lambda -> 0 the patched student's output reaches the teacher's, O(lambda)
+    inp = make_custom_inputs(M=12, N=80, B=20, Hq=4, Hkv=2, dh=8, dtype="f32", lam=1e-2, seed=4)
+    mlp = make_mlp_weights(inp, 48)
+    gaps = []
+    for lam in (1e-2, 1e-4, 1e-6):
+        out = oracle.mlp_layer_patch(inp, mlp, lam=lam)
+        gaps.append(rel(out["Y_student"], out["Y_teacher"]))
+    assert gaps[0] > gaps[1] > gaps[2] and gaps[2] < 1e-6 and gaps[1] < 2e-2 * gaps[0]
+    # the patch solves its normal equations and agrees with the push-through form
+    # Hc^T (Hc Hc^T + lambda I)^{-1} T, a different route through the same algebra
+    out = oracle.mlp_layer_patch(inp, mlp, lam=1e-2)
+    Q, K, V = (oracle.decode(a, "f32") for a in (inp.Q, inp.K, inp.V))
+    Kc, Vc = oracle.gather_cache(K, V, inp.idx)
+    Wg, Wu, Wd = (oracle.decode(a, "f32") for a in (mlp.Wg, mlp.Wu, mlp.Wd))
+    Of = oracle.attention(Q, K, V, inp.scale)
+    Oc = oracle.attention(Q, Kc, Vc, inp.scale)
+    Hf, Hc = oracle.mlp_features(Of, Wg, Wu), oracle.mlp_features(Oc, Wg, Wu)
+    T = (Hf - Hc) @ Wd + (Of - Oc)
+    assert rel(out["G"], Hc.T @ Hc) < 1e-14 and rel(out["C"], Hc.T @ T) < 1e-14
+    resid = (out["G"] + 1e-2 * np.eye(48)) @ out["dW"] - out["C"]
+    assert np.linalg.norm(resid) / np.linalg.norm(out["C"]) < 1e-12
+    push = Hc.T @ np.linalg.solve(Hc @ Hc.T + 1e-2 * np.eye(12), T)
+    assert rel(out["dW"], push) < 1e-10
+    assert rel(out["Y_student"], Hc @ (Wd + out["dW"]) + Oc) < 1e-15
+
+
+def test_mlp_pins_catch_planted_mistakes():
+    def feats_wrong_sign(Z, Wg, Wu, eps=1e-5):        # silu with e^{+x}
+        U = oracle.rms_norm(Z, eps)
+        G = U @ Wg
+        return G / (1.0 + np.exp(G)) * (U @ Wu)
+
+    def feats_no_norm(Z, Wg, Wu, eps=1e-5):           # RMS norm dropped
+        return oracle.silu(Z @ Wg) * (Z @ Wu)
+
+    def feats_swapped(Z, Wg, Wu, eps=1e-5):           # gate and up swapped
+        return oracle.mlp_features(Z, Wu, Wg, eps)
+
+    def targets_no_residual(Hf, Hc, W, Zf, Zc):
+        return (Hf - Hc) @ W
+
+    def targets_student_weights(Hf, Hc, W, Zf, Zc):   # residual sign flipped
+        return (Hf - Hc) @ W - (Zf - Zc)
+
+    assert check_mlp_features(feats_wrong_sign) > 1e-2
+    assert check_mlp_features(feats_no_norm) > 1e-2
+    assert check_mlp_features(feats_swapped) > 1e-2
+    assert check_block_targets(targets_no_residual) > 1e-2
+    assert check_block_targets(targets_student_weights) > 1e-2

@@ -37,6 +37,7 @@ class Config:
     n_random: int = 0
     n_mix: int = 0           # synthesize: entries mixed per synthetic entry
     chunks: int = 1          # reference chunks per layer (M tokens each, own causal prefix)
+    d_ff: int = 0            # > 0: patch the d_ff x d down-projection of a SwiGLU MLP
 
     @property
     def group(self) -> int:
@@ -69,6 +70,10 @@ CONFIGS = (
     Config(5, "llama3-8b-layer-172k-4x5k-chunks", d=4096, Hq=32, Hkv=8, dh=128, N=172032,
            B=1720, M=5120, lam=1e-1, dtype="bf16", chunks=4, n_sink=4, n_recent=860,
            n_random=856),
+    # the paper's own block: the patch is the 14336 x 4096 down-projection of
+    # Llama-3-8B's SwiGLU MLP, fed by the attention output of config 3's layer
+    Config(6, "llama3-8b-mlp-layer-172k", d=4096, Hq=32, Hkv=8, dh=128, N=172032, B=1720,
+           M=4096, lam=1e-1, dtype="bf16", d_ff=14336, n_sink=4, n_recent=860, n_random=856),
 )
 
 

@@ -4,6 +4,7 @@ Recipe (the same bytes feed the oracle and the GPU path):
 
 * Every random tensor has a tensor id: 0 key scales, 1 K, 2 V, 3 Q, 4 W,
   5 eviction middle positions, 6 synthesis positions, 7 synthesis weights;
+  8 MLP gate projection, 9 MLP up projection, 10 MLP down projection;
   reference chunk j of a chunked reference set: 16 + 4j its queries, 17 + 4j its
   own keys, 18 + 4j its own values.
 * Normal tensors are drawn in C order in blocks of ``BLOCK`` elements; block ``b``
@@ -14,7 +15,8 @@ Recipe (the same bytes feed the oracle and the GPU path):
 * Q, V ~ N(0, 1). K = Z * s with a per-(kv head, channel) scale
   s ~ LogNormal(0, 0.5) (float32 product). W = Z * float32(1/sqrt(d)).
   A chunk's queries and own values are N(0, 1); its own keys carry the layer's
-  key scales s like the cache keys.
+  key scales s like the cache keys. MLP weights: gate and up [d, d_ff] are
+  Z * float32(1/sqrt(d)), down [d_ff, d] is Z * float32(1/sqrt(d_ff)).
 * bf16 tensors are rounded from those float32 values with round-to-nearest-even
   and stored as their raw uint16 bit patterns; fp32 tensors are stored as is.
 * Eviction subset: ``n_sink`` sinks, the last ``n_recent`` tokens, and
@@ -41,6 +43,7 @@ from .configs import Config
 BLOCK = 1 << 22
 
 TID_SCALE, TID_K, TID_V, TID_Q, TID_W, TID_EVICT, TID_SYN_POS, TID_SYN_W = range(8)
+TID_GATE, TID_UP, TID_DOWN = 8, 9, 10
 TID_CHUNK = 16  # chunk j: 16 + 4j queries, 17 + 4j own keys, 18 + 4j own values
 
 
@@ -215,6 +218,28 @@ def make_chunk_inputs(inp: LayerInputs, chunk: int, M: int) -> ChunkInputs:
     Ks = _normal_tensor(seed, inp.cid, inp.layer, base + 1, (Hkv, M, dh), bf16, scale_k)
     Vs = _normal_tensor(seed, inp.cid, inp.layer, base + 2, (Hkv, M, dh), bf16)
     return ChunkInputs(chunk=chunk, Q=Q, Ks=Ks, Vs=Vs)
+
+
+@dataclass
+class MlpWeights:
+    """A SwiGLU MLP of one block: gate and up [d, d_ff], down [d_ff, d] (stored form)."""
+    Wg: np.ndarray
+    Wu: np.ndarray
+    Wd: np.ndarray
+    d_ff: int
+    eps: float = 1e-5
+
+
+def make_mlp_weights(inp: LayerInputs, d_ff: int) -> MlpWeights:
+    """The MLP weights of the layer ``inp`` with intermediate width d_ff."""
+    bf16 = inp.dtype == "bf16"
+    seed, d = inp.extra["seed"], inp.d
+    sg = np.float32(1.0 / np.sqrt(d))
+    sd = np.float32(1.0 / np.sqrt(d_ff))
+    Wg = _normal_tensor(seed, inp.cid, inp.layer, TID_GATE, (d, d_ff), bf16, lambda z, lo: z * sg)
+    Wu = _normal_tensor(seed, inp.cid, inp.layer, TID_UP, (d, d_ff), bf16, lambda z, lo: z * sg)
+    Wd = _normal_tensor(seed, inp.cid, inp.layer, TID_DOWN, (d_ff, d), bf16, lambda z, lo: z * sd)
+    return MlpWeights(Wg=Wg, Wu=Wu, Wd=Wd, d_ff=d_ff)
 
 
 def _mix(X: np.ndarray, pos: np.ndarray, w: np.ndarray, bf16: bool) -> np.ndarray:
