@@ -4,12 +4,13 @@ A step is one pass of the whole hot path over one batch of synthetic input: for
 every layer of the workload, attention of the M reference queries over the full
 cache and over the compressed cache, targets, normal equations and the ridge
 solve (the same five library calls, in the same order, that
-patchkv_compute_layer_patch makes; for a chunked reference set, the two
-attention passes, targets and statistics of every chunk, then one solve). The
-default workload is the 32-layer
-Llama-3-8B-shaped patch build over a 172,032-token context (1 % cache budget,
-4,096 reference queries per layer). All layer inputs are resident in HBM before
-the timed region starts.
+patchkv_compute_layer_patch makes). For a chunked reference set: the two
+attention passes, targets and statistics of every chunk, then one solve. For the
+MLP-shaped patch: both attention passes, the SwiGLU features of both, the block
+targets, the d_ff x d statistics and solve, and the student-state propagation.
+The default workload is the 32-layer Llama-3-8B-shaped patch build over a
+172,032-token context (1 % cache budget, 4,096 reference queries per layer). All
+layer inputs are resident in HBM before the timed region starts.
 
 Prints one JSON line: seconds per layer patch (value), attention TFLOP/s and its
 fraction of the bf16 MFMA peak, context tokens/s, the roofline of the dominant
@@ -83,7 +84,7 @@ class LayerDev:
     """One layer's inputs on the device (and, for a chunked reference set, every
     chunk's queries and own keys and values)."""
 
-    def __init__(self, inp, torch, dev, chunks=()):
+    def __init__(self, inp, torch, dev, chunks=(), mlp=None):
         def t(a):
             x = torch.from_numpy(np.ascontiguousarray(a))
             if inp.dtype == "bf16":
@@ -91,6 +92,9 @@ class LayerDev:
             return x.to(dev, non_blocking=False)
         self.Q, self.K, self.V, self.W = t(inp.Q), t(inp.K), t(inp.V), t(inp.W)
         self.chunks = [(t(c.Q), t(c.Ks), t(c.Vs)) for c in chunks]
+        self.Wg = self.Wu = self.Wd = None
+        if mlp is not None:
+            self.Wg, self.Wu, self.Wd, self.eps = t(mlp.Wg), t(mlp.Wu), t(mlp.Wd), mlp.eps
         self.idx = (torch.from_numpy(inp.idx).to(dev) if inp.idx is not None else None)
         self.Kc = t(inp.Kc) if inp.Kc is not None else None
         self.Vc = t(inp.Vc) if inp.Vc is not None else None
@@ -103,19 +107,27 @@ class Buffers:
         self.acc = 1 if cfg.dtype == "bf16" else 2  # F32 statistics for bf16 inputs, F64 for fp32
         adt = torch.float64 if self.acc == 2 else torch.float32
         M, d = cfg.M, cfg.d
+        din = cfg.d_ff or d  # the patched projection's input width
+        self.mode = 1 if cfg.ridge == "adaptive" else 0  # RIDGE_ADAPTIVE / RIDGE_ABSOLUTE
         self.Of = torch.empty((M, d), dtype=torch.float32, device=dev)
         self.Oc = torch.empty((M, d), dtype=torch.float32, device=dev)
         self.T = torch.empty((M, d), dtype=torch.float32, device=dev)
-        self.G = torch.empty((d, d), dtype=adt, device=dev)
-        self.C = torch.empty((d, d), dtype=adt, device=dev)
-        self.dW = [torch.empty((d, d), dtype=torch.float32, device=dev) for _ in range(nl)]
+        self.G = torch.empty((din, din), dtype=adt, device=dev)
+        self.C = torch.empty((din, d), dtype=adt, device=dev)
+        self.dW = [torch.empty((din, d), dtype=torch.float32, device=dev) for _ in range(nl)]
         self.info = torch.zeros((nl,), dtype=torch.int32, device=dev)
+        if cfg.d_ff:
+            self.Hf = torch.empty((M, din), dtype=torch.float32, device=dev)
+            self.Hc = torch.empty((M, din), dtype=torch.float32, device=dev)
+            self.Y = torch.empty((M, d), dtype=torch.float32, device=dev)
 
 
 def layer_steps(pkv, cfg, L, bufs, li: int, events=None):
     """One layer patch through the five library calls, in the order
-    patchkv_compute_layer_patch makes them; ``events`` = (start, end) CUDA events
-    recorded around the full-cache attention on the current stream."""
+    patchkv_compute_layer_patch makes them (for the MLP-shaped patch: with the
+    SwiGLU features of both passes, the block targets and, after the solve, the
+    student-state propagation); ``events`` = (start, end) CUDA events recorded
+    around the full-cache attention on the current stream."""
     acc = pkv.F32 if bufs.acc == 1 else pkv.F64
     if events is not None:
         events[0].record()
@@ -126,9 +138,18 @@ def layer_steps(pkv, cfg, L, bufs, li: int, events=None):
         pkv.attend_compressed(L.Q, L.K, L.V, idx=L.idx, scale=cfg.scale, O=bufs.Oc)
     else:
         pkv.attend_compressed(L.Q, L.Kc, L.Vc, scale=cfg.scale, O=bufs.Oc)
-    pkv.compute_targets(bufs.Of, bufs.Oc, L.W, rho=1, T=bufs.T)
-    pkv.accumulate_normal_eq(bufs.Oc, bufs.T, G=bufs.G, C=bufs.C, acc=acc)
-    pkv.solve_patch(bufs.G, bufs.C, cfg.lam, dW=bufs.dW[li], info=bufs.info[li:li + 1])
+    if cfg.d_ff:  # MLP-shaped patch
+        pkv.mlp_features(bufs.Of, L.Wg, L.Wu, eps=L.eps, H=bufs.Hf)
+        pkv.mlp_features(bufs.Oc, L.Wg, L.Wu, eps=L.eps, H=bufs.Hc)
+        pkv.compute_block_targets(bufs.Hf, bufs.Hc, L.Wd, bufs.Of, bufs.Oc, T=bufs.T)
+        pkv.accumulate_normal_eq(bufs.Hc, bufs.T, G=bufs.G, C=bufs.C, acc=acc)
+    else:
+        pkv.compute_targets(bufs.Of, bufs.Oc, L.W, rho=1, T=bufs.T)
+        pkv.accumulate_normal_eq(bufs.Oc, bufs.T, G=bufs.G, C=bufs.C, acc=acc)
+    pkv.solve_patch(bufs.G, bufs.C, cfg.lam, mode=bufs.mode, dW=bufs.dW[li],
+                    info=bufs.info[li:li + 1])
+    if cfg.d_ff:  # the student state through the patched block
+        pkv.propagate_student(bufs.Hc, L.Wd, bufs.dW[li], bufs.Oc, Y=bufs.Y)
 
 
 def chunked_layer_steps(pkv, cfg, L, bufs, li: int, events=None):
@@ -149,7 +170,8 @@ def chunked_layer_steps(pkv, cfg, L, bufs, li: int, events=None):
             pkv.attend_chunk(Q, L.Kc, L.Vc, Ks, Vs, scale=cfg.scale, p_terms=2, O=bufs.Oc)
         pkv.compute_targets(bufs.Of, bufs.Oc, L.W, rho=1, T=bufs.T)
         pkv.accumulate_normal_eq(bufs.Oc, bufs.T, G=bufs.G, C=bufs.C, acc=acc, accumulate=j > 0)
-    pkv.solve_patch(bufs.G, bufs.C, cfg.lam, dW=bufs.dW[li], info=bufs.info[li:li + 1])
+    pkv.solve_patch(bufs.G, bufs.C, cfg.lam, mode=bufs.mode, dW=bufs.dW[li],
+                    info=bufs.info[li:li + 1])
 
 
 def cpu_baseline(cfg, rows: int) -> dict:
@@ -160,7 +182,7 @@ def cpu_baseline(cfg, rows: int) -> dict:
     by M / rows), plus the complete d x d ridge solve (independent of M).
     """
     import oracle
-    from workloads import make_chunk_inputs, make_layer_inputs
+    from workloads import make_chunk_inputs, make_layer_inputs, make_mlp_weights
     try:
         from threadpoolctl import threadpool_info
         blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
@@ -188,16 +210,28 @@ def cpu_baseline(cfg, rows: int) -> dict:
         Ks, Vs = oracle.decode(ch.Ks[:, :rows], dt), oracle.decode(ch.Vs[:, :rows], dt)
         Of = oracle.attention_chunk(Q, K, V, Ks, Vs, inp.scale)
         Oc = oracle.attention_chunk(Q, Kc, Vc, Ks, Vs, inp.scale)
-    T = oracle.targets(Of, Oc, W, 1)
-    G, C = oracle.normal_equations(Oc, T)
+    if cfg.d_ff:
+        mlp = make_mlp_weights(inp, cfg.d_ff)
+        Wg, Wu, Wd = (oracle.decode(a, dt) for a in (mlp.Wg, mlp.Wu, mlp.Wd))
+        Hf, Hc = oracle.mlp_features(Of, Wg, Wu, mlp.eps), oracle.mlp_features(Oc, Wg, Wu, mlp.eps)
+        T = oracle.block_targets(Hf, Hc, Wd, Of, Oc)
+        G, C = oracle.normal_equations(Hc, T)
+    else:
+        T = oracle.targets(Of, Oc, W, 1)
+        G, C = oracle.normal_equations(Oc, T)
     t_rows = time.perf_counter() - t0
     tokens = cfg.M * cfg.chunks
     # the solve at full size needs a well-posed full-size G: scale the sampled
     # statistics up to all reference tokens' worth of mass (its cost does not
     # depend on G's values)
     t1 = time.perf_counter()
-    oracle.solve_patch(G * (tokens / rows), C * (tokens / rows), cfg.lam)
+    Gs, Cs = G * (tokens / rows), C * (tokens / rows)
+    dW = oracle.solve_patch(Gs, Cs, oracle.ridge_lambda(Gs, cfg.lam, cfg.ridge))
     t_solve = time.perf_counter() - t1
+    if cfg.d_ff:  # the propagation is linear in the rows, like the rest of the sample
+        t2 = time.perf_counter()
+        oracle.propagate_student(Hc, Wd, dW, Oc)
+        t_rows += time.perf_counter() - t2
     est = t_rows * (tokens / rows) + t_solve
     what = (f"the first {rows} tokens of reference chunk 0 (of {cfg.chunks} chunks x {cfg.M})"
             if ch is not None else f"{rows} of {cfg.M} reference queries")
@@ -205,8 +239,8 @@ def cpu_baseline(cfg, rows: int) -> dict:
             "kind": "oracle",
             "sample": f"config {cfg.cid} layer 0: fp64 attention (full + compressed), targets and "
                       f"statistics for {what} ({t_rows:.2f} s, scaled x{tokens / rows:.0f}) + "
-                      f"full {cfg.d}x{cfg.d} Cholesky solve ({t_solve:.2f} s); input decoding "
-                      f"included"}
+                      f"full {G.shape[0]}x{cfg.d} Cholesky solve ({t_solve:.2f} s); input "
+                      f"decoding included"}
 
 
 def main():
@@ -219,7 +253,7 @@ def main():
     import torch
 
     import paper_2609_39329_amd as pkv
-    from workloads import get_config, make_chunk_inputs, make_layer_inputs
+    from workloads import get_config, make_chunk_inputs, make_layer_inputs, make_mlp_weights
 
     cfg = get_config(args.config)
     nl = cfg.layers if args.layers is None else min(args.layers, cfg.layers)
@@ -231,7 +265,8 @@ def main():
     for layer in range(nl):
         inp = make_layer_inputs(cfg, layer)
         chunks = [make_chunk_inputs(inp, j, cfg.M) for j in range(cfg.chunks)] if cfg.chunks > 1 else ()
-        layers.append(LayerDev(inp, torch, dev, chunks))
+        mlp = make_mlp_weights(inp, cfg.d_ff) if cfg.d_ff else None
+        layers.append(LayerDev(inp, torch, dev, chunks, mlp))
         if layer % 8 == 7 or layer == nl - 1:
             log(f"[bench] inputs of {layer + 1}/{nl} layers resident ({time.perf_counter() - t0:.1f} s)")
     torch.cuda.synchronize()
@@ -298,7 +333,9 @@ def main():
                    "N": cfg.N, "B": cfg.B, "M": M, "d": d, "Hq": cfg.Hq, "Hkv": cfg.Hkv,
                    "dh": cfg.dh, "lambda": cfg.lam, "compressed_cache": cfg.cache,
                    "reference_chunks": cfg.chunks,
-                   "own_causal_prefix": chunked},
+                   "own_causal_prefix": chunked, "ridge": cfg.ridge,
+                   "patch": (f"MLP down-projection {cfg.d_ff}x{d} (SwiGLU features, student "
+                             f"propagation)" if cfg.d_ff else f"{d}x{d} projection")},
         "attention_full_ms": t_attn * 1e3,
         "attention_full_tflops": achieved,
         "attention_full_frac_of_peak": achieved / peak,

@@ -140,10 +140,11 @@ int patchkv_attend_compressed(int dtype, const void* Q, const void* K, const voi
 /* p_terms: 1 = P enters the P V product rounded to bf16 (as attend_full),      */
 /*          2 = as a two-term bf16 split (as attend_compressed); f32 ignores it.*/
 /* Limits as patchkv_attend_full with N = n_cache, plus n_src and M within the  */
-/* same row limits. Own entries are attended without a key split.              */
+/* same row limits. When the cache is split into key ranges (small M), the own  */
+/* entries go with the last range.                                             */
 /* Workspace: patchkv_attend_chunk_workspace_bytes(dtype, M, n_cache, ...):     */
-/*   for bf16, transposed copies of the cache's and the own values plus a few   */
-/*   bytes per work item; 0 for f32.                                           */
+/*   that of patchkv_attend_full for (M, n_cache) plus, for bf16, a transposed  */
+/*   copy of the own values (Hkv*ceil(M/32)*32*dh bf16).                        */
 /* ------------------------------------------------------------------------- */
 size_t patchkv_attend_chunk_workspace_bytes(int dtype, int64_t M, int64_t n_cache, int Hq, int Hkv,
                                             int dh);
@@ -167,6 +168,46 @@ size_t patchkv_targets_workspace_bytes(int w_dtype, int64_t M, int64_t d_in, int
 int patchkv_compute_targets(int w_dtype, const float* Of, const float* Oc, const void* W,
                             int64_t M, int64_t d_in, int64_t d_out, int rho, float* T,
                             void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------- */
+/* The MLP-shaped block (Sec. 2.3, "MLP activation matching"; Alg. 1). The      */
+/* block output is y = h W + z: z [M][d] is the attention output, h [M][d_ff]   */
+/* the post-activation SwiGLU intermediate, W [d_ff][d] the down-projection     */
+/* that the patch corrects. The MLP reads z through an RMS norm with unit gain.  */
+/*                                                                           */
+/* patchkv_mlp_features:  H = silu(u Wg) * (u Wu), u = z / sqrt(mean(z^2)+eps)  */
+/*   per row, silu(x) = x / (1 + e^-x). Z [M][d] float; Wg, Wu [d][d_ff]        */
+/*   (w_dtype); H [M][d_ff] float, written. u enters the MFMA products as a      */
+/*   two-term bf16 split (and W too when f32): relative error ~1e-5.            */
+/* patchkv_compute_block_targets:  Eq. 5, T = (Hf - Hc) W + (Zf - Zc).          */
+/*   Hf, Hc [M][d_ff] float; W [d_ff][d] (w_dtype); Zf, Zc [M][d] float;        */
+/*   T [M][d] float, written.                                                  */
+/* patchkv_propagate_student:  student-state propagation of Alg. 1, the patched */
+/*   block's output Y = Hc (W + dW) + Zc. Hc [M][d_ff], dW [d_ff][d], Zc [M][d] */
+/*   float; W [d_ff][d] (w_dtype); Y [M][d] float, written.                     */
+/* The patch itself is patchkv_accumulate_normal_eq on (Hc, T) with d_in = d_ff */
+/* and patchkv_solve_patch (d_in = d_ff, d_out = d).                           */
+/* Limits: M >= 1 (M below 2^31), 1 <= d, d_ff <= 65536, d_ff a multiple of 4; */
+/*   eps >= 0 and finite; every pointer 16-byte aligned.                       */
+/* ------------------------------------------------------------------------- */
+size_t patchkv_mlp_features_workspace_bytes(int w_dtype, int64_t M, int64_t d, int64_t d_ff);
+
+int patchkv_mlp_features(int w_dtype, const float* Z, const void* Wg, const void* Wu, int64_t M,
+                         int64_t d, int64_t d_ff, float eps, float* H, void* workspace,
+                         size_t workspace_bytes, void* stream);
+
+size_t patchkv_block_targets_workspace_bytes(int w_dtype, int64_t M, int64_t d_ff, int64_t d);
+
+int patchkv_compute_block_targets(int w_dtype, const float* Hf, const float* Hc, const void* W,
+                                  const float* Zf, const float* Zc, int64_t M, int64_t d_ff,
+                                  int64_t d, float* T, void* workspace, size_t workspace_bytes,
+                                  void* stream);
+
+size_t patchkv_propagate_workspace_bytes(int w_dtype, int64_t M, int64_t d_ff, int64_t d);
+
+int patchkv_propagate_student(int w_dtype, const float* Hc, const void* W, const float* dW,
+                              const float* Zc, int64_t M, int64_t d_ff, int64_t d, float* Y,
+                              void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------- */
 /* Sufficient statistics, Eq. 9 (row form; Alg. 1 accumulation over chunks):    */

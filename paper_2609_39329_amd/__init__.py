@@ -5,10 +5,10 @@ there is no CPU fallback.
 """
 from .binding import (BF16, F32, F64, RIDGE_ABSOLUTE, RIDGE_ADAPTIVE, SOLVE_EXACT_F32,
                       PatchKVError, accumulate_normal_eq, attend_chunk, attend_compressed,
-                      attend_full, compute_layer_patch, compute_targets, layer_workspace_bytes,
-                      lib, solve_patch)
+                      attend_full, compute_block_targets, compute_layer_patch, compute_targets,
+                      layer_workspace_bytes, lib, mlp_features, propagate_student, solve_patch)
 
 __all__ = ["BF16", "F32", "F64", "RIDGE_ABSOLUTE", "RIDGE_ADAPTIVE", "SOLVE_EXACT_F32",
            "PatchKVError", "accumulate_normal_eq", "attend_chunk", "attend_compressed",
-           "attend_full", "compute_layer_patch", "compute_targets", "layer_workspace_bytes", "lib",
-           "solve_patch"]
+           "attend_full", "compute_block_targets", "compute_layer_patch", "compute_targets",
+           "layer_workspace_bytes", "lib", "mlp_features", "propagate_student", "solve_patch"]

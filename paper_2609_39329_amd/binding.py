@@ -45,6 +45,15 @@ SIGNATURES = {
     "patchkv_targets_workspace_bytes": (_c_sz, [_c_int, _c_i64, _c_i64, _c_i64]),
     "patchkv_compute_targets": (_c_int, [_c_int, _c_vp, _c_vp, _c_vp, _c_i64, _c_i64, _c_i64,
                                          _c_int, _c_vp, _c_vp, _c_sz, _c_vp]),
+    "patchkv_mlp_features_workspace_bytes": (_c_sz, [_c_int, _c_i64, _c_i64, _c_i64]),
+    "patchkv_mlp_features": (_c_int, [_c_int, _c_vp, _c_vp, _c_vp, _c_i64, _c_i64, _c_i64,
+                                      ctypes.c_float, _c_vp, _c_vp, _c_sz, _c_vp]),
+    "patchkv_block_targets_workspace_bytes": (_c_sz, [_c_int, _c_i64, _c_i64, _c_i64]),
+    "patchkv_compute_block_targets": (_c_int, [_c_int, _c_vp, _c_vp, _c_vp, _c_vp, _c_vp, _c_i64,
+                                               _c_i64, _c_i64, _c_vp, _c_vp, _c_sz, _c_vp]),
+    "patchkv_propagate_workspace_bytes": (_c_sz, [_c_int, _c_i64, _c_i64, _c_i64]),
+    "patchkv_propagate_student": (_c_int, [_c_int, _c_vp, _c_vp, _c_vp, _c_vp, _c_i64, _c_i64,
+                                           _c_i64, _c_vp, _c_vp, _c_sz, _c_vp]),
     "patchkv_normal_eq_workspace_bytes": (_c_sz, [_c_int, _c_i64, _c_i64, _c_i64]),
     "patchkv_accumulate_normal_eq": (_c_int, [_c_int, _c_vp, _c_vp, _c_vp, _c_i64, _c_i64, _c_i64,
                                               _c_int, _c_vp, _c_vp, _c_vp, _c_sz, _c_vp]),
@@ -226,6 +235,60 @@ def compute_targets(Of, Oc, W, rho: int = 1, T=None, stream=None):
            L.patchkv_compute_targets(wdt, _ptr(Of), _ptr(Oc), _ptr(W), M, din, dout, rho, _ptr(T),
                                      _ptr(ws), nb, _stream(stream)))
     return T
+
+
+def mlp_features(Z, Wg, Wu, eps: float = 1e-5, H=None, stream=None):
+    """H [M, d_ff] = silu(u Wg) * (u Wu), u = RMS-normed Z [M, d] (unit gain)."""
+    torch = _torch()
+    _require_gpu(Z, Wg, Wu, H)
+    M, d = Z.shape
+    d_ff = Wg.shape[1]
+    wt = _dtype_code(Wg)
+    if H is None:
+        H = torch.empty((M, d_ff), dtype=torch.float32, device=Z.device)
+    L = lib()
+    nb = L.patchkv_mlp_features_workspace_bytes(wt, M, d, d_ff)
+    ws = _workspace(nb, Z.device, stream)
+    _check("patchkv_mlp_features",
+           L.patchkv_mlp_features(wt, _ptr(Z), _ptr(Wg), _ptr(Wu), M, d, d_ff, eps, _ptr(H),
+                                  _ptr(ws), nb, _stream(stream)))
+    return H
+
+
+def compute_block_targets(Hf, Hc, W, Zf, Zc, T=None, stream=None):
+    """T [M, d] = (Hf - Hc) W + (Zf - Zc) for the MLP-shaped block (W [d_ff, d])."""
+    torch = _torch()
+    _require_gpu(Hf, Hc, W, Zf, Zc, T)
+    M, d_ff = Hf.shape
+    d = W.shape[1]
+    wt = _dtype_code(W)
+    if T is None:
+        T = torch.empty((M, d), dtype=torch.float32, device=Hf.device)
+    L = lib()
+    nb = L.patchkv_block_targets_workspace_bytes(wt, M, d_ff, d)
+    ws = _workspace(nb, Hf.device, stream)
+    _check("patchkv_compute_block_targets",
+           L.patchkv_compute_block_targets(wt, _ptr(Hf), _ptr(Hc), _ptr(W), _ptr(Zf), _ptr(Zc), M,
+                                           d_ff, d, _ptr(T), _ptr(ws), nb, _stream(stream)))
+    return T
+
+
+def propagate_student(Hc, W, dW, Zc, Y=None, stream=None):
+    """Y [M, d] = Hc (W + dW) + Zc: the patched block's output on the student side."""
+    torch = _torch()
+    _require_gpu(Hc, W, dW, Zc, Y)
+    M, d_ff = Hc.shape
+    d = W.shape[1]
+    wt = _dtype_code(W)
+    if Y is None:
+        Y = torch.empty((M, d), dtype=torch.float32, device=Hc.device)
+    L = lib()
+    nb = L.patchkv_propagate_workspace_bytes(wt, M, d_ff, d)
+    ws = _workspace(nb, Hc.device, stream)
+    _check("patchkv_propagate_student",
+           L.patchkv_propagate_student(wt, _ptr(Hc), _ptr(W), _ptr(dW), _ptr(Zc), M, d_ff, d,
+                                       _ptr(Y), _ptr(ws), nb, _stream(stream)))
+    return Y
 
 
 def accumulate_normal_eq(Xc, Yf, Yc=None, G=None, C=None, acc: int = F32, accumulate: bool = False,

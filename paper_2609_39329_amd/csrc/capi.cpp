@@ -204,6 +204,73 @@ int patchkv_compute_targets(int w_dtype, const float* Of, const float* Oc, const
                                   workspace, (hipStream_t)stream));
 }
 
+namespace {
+int check_mlp(int w_dtype, int64_t M, int64_t d, int64_t d_ff) {
+  if (w_dtype != PATCHKV_BF16 && w_dtype != PATCHKV_F32) return PATCHKV_E_DTYPE;
+  int s = check_stats_dims(M, d, d_ff);
+  if (s) return s;
+  if (d_ff % 4 != 0) return PATCHKV_E_SHAPE;
+  return PATCHKV_OK;
+}
+}  // namespace
+
+size_t patchkv_mlp_features_workspace_bytes(int w_dtype, int64_t M, int64_t d, int64_t d_ff) {
+  if (check_mlp(w_dtype, M, d, d_ff)) return 0;
+  return mlp_features_ws_bytes(M, d, d_ff);
+}
+
+int patchkv_mlp_features(int w_dtype, const float* Z, const void* Wg, const void* Wu, int64_t M,
+                         int64_t d, int64_t d_ff, float eps, float* H, void* workspace,
+                         size_t workspace_bytes, void* stream) {
+  if (!Z || !Wg || !Wu || !H) return PATCHKV_E_NULL;
+  int s = check_mlp(w_dtype, M, d, d_ff);
+  if (s) return s;
+  if (!(isfinite(eps) && eps >= 0.f)) return PATCHKV_E_VALUE;
+  if (!al16(Z) || !al16(Wg) || !al16(Wu) || !al16(H)) return PATCHKV_E_VALUE;
+  s = check_ws(workspace, workspace_bytes, mlp_features_ws_bytes(M, d, d_ff));
+  if (s) return s;
+  return status_of(launch_mlp_features(Z, Wg, Wu, w_dtype == PATCHKV_BF16, M, d, d_ff, eps, H,
+                                       workspace, (hipStream_t)stream));
+}
+
+size_t patchkv_block_targets_workspace_bytes(int w_dtype, int64_t M, int64_t d_ff, int64_t d) {
+  if (check_mlp(w_dtype, M, d, d_ff)) return 0;
+  return targets_ws_bytes(M, d_ff, d);
+}
+
+int patchkv_compute_block_targets(int w_dtype, const float* Hf, const float* Hc, const void* W,
+                                  const float* Zf, const float* Zc, int64_t M, int64_t d_ff,
+                                  int64_t d, float* T, void* workspace, size_t workspace_bytes,
+                                  void* stream) {
+  if (!Hf || !Hc || !W || !Zf || !Zc || !T) return PATCHKV_E_NULL;
+  int s = check_mlp(w_dtype, M, d, d_ff);
+  if (s) return s;
+  if (!al16(Hf) || !al16(Hc) || !al16(W) || !al16(Zf) || !al16(Zc) || !al16(T))
+    return PATCHKV_E_VALUE;
+  s = check_ws(workspace, workspace_bytes, targets_ws_bytes(M, d_ff, d));
+  if (s) return s;
+  return status_of(launch_targets(Hf, Hc, W, w_dtype == PATCHKV_BF16, M, d_ff, d, 0, T, workspace,
+                                  (hipStream_t)stream, Zf, Zc));
+}
+
+size_t patchkv_propagate_workspace_bytes(int w_dtype, int64_t M, int64_t d_ff, int64_t d) {
+  if (check_mlp(w_dtype, M, d, d_ff)) return 0;
+  return propagate_ws_bytes(M, d_ff, d);
+}
+
+int patchkv_propagate_student(int w_dtype, const float* Hc, const void* W, const float* dW,
+                              const float* Zc, int64_t M, int64_t d_ff, int64_t d, float* Y,
+                              void* workspace, size_t workspace_bytes, void* stream) {
+  if (!Hc || !W || !dW || !Zc || !Y) return PATCHKV_E_NULL;
+  int s = check_mlp(w_dtype, M, d, d_ff);
+  if (s) return s;
+  if (!al16(Hc) || !al16(W) || !al16(dW) || !al16(Zc) || !al16(Y)) return PATCHKV_E_VALUE;
+  s = check_ws(workspace, workspace_bytes, propagate_ws_bytes(M, d_ff, d));
+  if (s) return s;
+  return status_of(launch_propagate(Hc, W, w_dtype == PATCHKV_BF16, dW, Zc, M, d_ff, d, Y,
+                                    workspace, (hipStream_t)stream));
+}
+
 size_t patchkv_normal_eq_workspace_bytes(int acc_dtype, int64_t rows, int64_t d_in,
                                          int64_t d_out) {
   if (acc_dtype != PATCHKV_F32 && acc_dtype != PATCHKV_F64) return 0;

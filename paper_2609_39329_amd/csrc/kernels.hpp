@@ -39,10 +39,21 @@ hipError_t launch_attention(const AttnShape& s, const void* Q, const void* K, co
 
 // ---------------------------------------------------------------- statistics (fp32 acc)
 size_t targets_ws_bytes(int64_t M, int64_t din, int64_t dout);
-// T = (Of - Oc) W + rho (Of - Oc); W bf16 (w_bf16) or f32.
+// T = (Of - Oc) W + rho (Of - Oc); W bf16 (w_bf16) or f32. With Zf non-null the
+// residual is (Zf - Zc) [M][dout] instead (the MLP-shaped block).
 hipError_t launch_targets(const float* Of, const float* Oc, const void* W, bool w_bf16,
                           int64_t M, int64_t din, int64_t dout, int rho, float* T, void* ws,
-                          hipStream_t st);
+                          hipStream_t st, const float* Zf = nullptr, const float* Zc = nullptr);
+// H [M][d_ff] = silu(u Wg) * (u Wu), u = rms_norm(Z) (unit gain), Wg, Wu [d][d_ff].
+size_t mlp_features_ws_bytes(int64_t M, int64_t d, int64_t d_ff);
+hipError_t launch_mlp_features(const float* Z, const void* Wg, const void* Wu, bool w_bf16,
+                               int64_t M, int64_t d, int64_t d_ff, float eps, float* H, void* ws,
+                               hipStream_t st);
+// Y [M][d] = Hc (W + dW) + Zc, W [d_ff][d] (bf16 or f32), dW fp32.
+size_t propagate_ws_bytes(int64_t M, int64_t d_ff, int64_t d);
+hipError_t launch_propagate(const float* Hc, const void* W, bool w_bf16, const float* dW,
+                            const float* Zc, int64_t M, int64_t d_ff, int64_t d, float* Y, void* ws,
+                            hipStream_t st);
 size_t normal_eq_ws_bytes(int64_t rows, int64_t din, int64_t dout);
 // G (+)= X^T X, C (+)= X^T (Yf - Yc) with split-bf16 MFMA, fp32 accumulation.
 hipError_t launch_normal_eq_f32(const float* X, const float* Yf, const float* Yc, int64_t rows,

@@ -1,6 +1,9 @@
 // Targets and sufficient statistics (Eq. 5 and Eq. 9, row form):
 //   T = (O_f - O_c) W + rho (O_f - O_c)
 //   G (+)= X^T X,   C (+)= X^T (Yf - Yc)
+// and the MLP-shaped block (Sec. 2.3; Alg. 1): SwiGLU features of the RMS-normed
+// attention output, targets through the down-projection plus the attention
+// residual, and the student state through the patched block.
 //
 // fp32-accumulate path: split pre-passes + bgemm_kernel (bf16 MFMA, fp32 accumulation).
 // fp64-accumulate path (f64_gemm_kernel): plain fp64 FMA tiles through LDS.
@@ -74,13 +77,14 @@ __global__ __launch_bounds__(256) void split_rows_kernel(const float* __restrict
   *(bf16x8*)(lo + o) = l;
 }
 
-// dst[c][r] (c < cols_p, r < rows_p) = split(S1 - S2)[r][c] inside rows x cols, zero
-// outside: the transpose, through a 64 x 64 LDS tile. SRC float (hi and lo planes,
+// dst[c][r] (c < cols_p, r < rows_p) = split(S1 + s2 S2)[r][c] inside rows x cols,
+// zero outside: the transpose, through a 64 x 64 LDS tile (s2 = -1: a difference,
+// +1: a bf16 weight plus an fp32 patch). SRC float (hi and lo planes,
 // lo may be null for a bf16 source) or bf16 (hi plane only).
 template <class SRC>
 __global__ __launch_bounds__(256) void split_transpose_kernel(const SRC* __restrict__ S1,
-                                                              const float* __restrict__ S2, int rows,
-                                                              int cols, int64_t ld,
+                                                              const float* __restrict__ S2, float s2,
+                                                              int rows, int cols, int64_t ld,
                                                               __bf16* __restrict__ hi,
                                                               __bf16* __restrict__ lo, int rows_p,
                                                               int cols_p) {
@@ -95,7 +99,7 @@ __global__ __launch_bounds__(256) void split_transpose_kernel(const SRC* __restr
     float v = 0.f;
     if (r < rows && c < cols) {
       v = (float)S1[(int64_t)r * ld + c];
-      if (S2) v -= S2[(int64_t)r * ld + c];
+      if (S2) v = fmaf(s2, S2[(int64_t)r * ld + c], v);
     }
     tile[rr][cc] = v;
   }
@@ -256,7 +260,8 @@ __global__ __launch_bounds__(BG_THREADS, 1) void bgemm_kernel(BGemm p) {
 #pragma unroll
           for (int e = 0; e < 4; ++e)
             if (j + e < p.J)
-              v[e] += p.rho * (p.E1[(int64_t)i * p.lde + j + e] - p.E2[(int64_t)i * p.lde + j + e]);
+              v[e] += p.rho * (p.E1[(int64_t)i * p.lde + j + e] -
+                               (p.E2 ? p.E2[(int64_t)i * p.lde + j + e] : 0.f));
         }
         float* o = p.Out + (int64_t)i * p.ldo + j;
         const bool diag = SYM && ti == tj;
@@ -302,11 +307,62 @@ hipError_t run_split_rows(const float* S1, const float* S2, int64_t rows, int64_
 template <class SRC>
 hipError_t run_split_transpose(const SRC* S1, const float* S2, int64_t rows, int64_t cols,
                                int64_t ld, __bf16* hi, __bf16* lo, int64_t rows_p, int64_t cols_p,
-                               hipStream_t st) {
+                               hipStream_t st, float s2 = -1.f) {
   const dim3 grid((unsigned)((cols_p + 63) / 64), (unsigned)((rows_p + 63) / 64));
-  hipLaunchKernelGGL((split_transpose_kernel<SRC>), grid, dim3(256), 0, st, S1, S2, (int)rows,
+  hipLaunchKernelGGL((split_transpose_kernel<SRC>), grid, dim3(256), 0, st, S1, S2, s2, (int)rows,
                      (int)cols, ld, hi, lo, (int)rows_p, (int)cols_p);
   return hipGetLastError();
+}
+
+// u = z / sqrt(mean(z^2) + eps) per row, split into hi and lo planes [rows_p][cols_p]
+// (zero outside rows x cols). One workgroup per row; the mean square in fp32.
+__global__ __launch_bounds__(256) void rmsnorm_split_kernel(const float* __restrict__ Z, int rows,
+                                                            int cols, float eps,
+                                                            __bf16* __restrict__ hi,
+                                                            __bf16* __restrict__ lo, int cols_p) {
+  __shared__ float part[8];
+  const int r = blockIdx.x, tid = threadIdx.x;
+  float inv = 0.f;
+  if (r < rows) {
+    const float* z = Z + (int64_t)r * cols;
+    float ss = 0.f;
+    for (int c = tid; c < cols; c += 256) ss = fmaf(z[c], z[c], ss);
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) ss += __shfl_xor(ss, o);
+    if ((tid & 63) == 0) part[tid >> 6] = ss;
+    __syncthreads();
+    if (tid == 0) part[4] = 1.0f / sqrtf((part[0] + part[1] + part[2] + part[3]) / (float)cols + eps);
+    __syncthreads();
+    inv = part[4];
+  }
+  for (int c0 = tid * 8; c0 < cols_p; c0 += 256 * 8) {
+    bf16x8 h, l;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int c = c0 + e;
+      const float v = (r < rows && c < cols) ? Z[(int64_t)r * cols + c] * inv : 0.f;
+      h[e] = to_bf16(v);
+      l[e] = to_bf16(v - (float)h[e]);
+    }
+    *(bf16x8*)(hi + (int64_t)r * cols_p + c0) = h;
+    *(bf16x8*)(lo + (int64_t)r * cols_p + c0) = l;
+  }
+}
+
+// H[m][j] = silu(GU[m][j]) * GU[m][up + j], silu(g) = g / (1 + e^-g), for j < d_ff.
+__global__ __launch_bounds__(256) void swiglu_kernel(const float* __restrict__ GU, int64_t ldgu,
+                                                     int64_t up, int rows, int d_ff,
+                                                     float* __restrict__ H) {
+  const int64_t g = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int per_row = d_ff / 4;
+  if (g >= (int64_t)rows * per_row) return;
+  const int r = (int)(g / per_row), j = (int)(g % per_row) * 4;
+  const f32x4 a = *(const f32x4*)(GU + (int64_t)r * ldgu + j);
+  const f32x4 b = *(const f32x4*)(GU + (int64_t)r * ldgu + up + j);
+  f32x4 h;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) h[e] = a[e] / (1.0f + expf(-a[e])) * b[e];
+  *(f32x4*)(H + (int64_t)r * d_ff + j) = h;
 }
 
 struct TargetsWs {
@@ -334,6 +390,25 @@ NormalEqWs normal_eq_layout(int64_t rows, int64_t din, int64_t dout) {
   L.Xl = o; o += align_up((size_t)Ip * Kp * 2);
   L.Yh = o; o += align_up((size_t)Jp * Kp * 2);
   L.Yl = o; o += align_up((size_t)Jp * Kp * 2);
+  L.total = o;
+  return L;
+}
+
+struct MlpWs {
+  size_t Uh, Ul, Wh, Wl, GU, total;
+  int64_t Mp, Kp, Jh;  // padded rows, padded d, padded d_ff (one half of the gate|up planes)
+};
+MlpWs mlp_layout(int64_t M, int64_t d, int64_t d_ff) {
+  MlpWs L{};
+  L.Mp = pad_to(M, G_BM);
+  L.Kp = pad_to(d, G_KC);
+  L.Jh = pad_to(d_ff, G_BM);
+  size_t o = 0;
+  L.Uh = o; o += align_up((size_t)L.Mp * L.Kp * 2);
+  L.Ul = o; o += align_up((size_t)L.Mp * L.Kp * 2);
+  L.Wh = o; o += align_up((size_t)2 * L.Jh * L.Kp * 2);
+  L.Wl = o; o += align_up((size_t)2 * L.Jh * L.Kp * 2);
+  L.GU = o; o += align_up((size_t)M * 2 * L.Jh * 4);
   L.total = o;
   return L;
 }
@@ -441,12 +516,93 @@ hipError_t run_f64(F64Params<TA, TB> p, hipStream_t st) {
 size_t targets_ws_bytes(int64_t M, int64_t din, int64_t dout) {
   return targets_layout(M, din, dout).total;
 }
+size_t mlp_features_ws_bytes(int64_t M, int64_t d, int64_t d_ff) {
+  return mlp_layout(M, d, d_ff).total;
+}
+
+hipError_t launch_mlp_features(const float* Z, const void* Wg, const void* Wu, bool w_bf16,
+                               int64_t M, int64_t d, int64_t d_ff, float eps, float* H, void* ws,
+                               hipStream_t st) {
+  const MlpWs L = mlp_layout(M, d, d_ff);
+  char* w = (char*)ws;
+  __bf16 *Uh = (__bf16*)(w + L.Uh), *Ul = (__bf16*)(w + L.Ul);
+  __bf16 *Wh = (__bf16*)(w + L.Wh), *Wl = (__bf16*)(w + L.Wl);
+  float* GU = (float*)(w + L.GU);
+  hipLaunchKernelGGL(rmsnorm_split_kernel, dim3((unsigned)L.Mp), dim3(256), 0, st, Z, (int)M, (int)d,
+                     eps, Uh, Ul, (int)L.Kp);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // [Wg | Wu] transposed: rows [0, d_ff) gate, rows [Jh, Jh + d_ff) up
+  const int64_t off = L.Jh * L.Kp;
+  for (int h = 0; h < 2; ++h) {
+    const void* Wx = h ? Wu : Wg;
+    if (w_bf16)
+      e = run_split_transpose((const __bf16*)Wx, nullptr, d, d_ff, d_ff, Wh + h * off, nullptr, L.Kp,
+                              L.Jh, st);
+    else
+      e = run_split_transpose((const float*)Wx, nullptr, d, d_ff, d_ff, Wh + h * off,
+                              Wl + h * off, L.Kp, L.Jh, st);
+    if (e != hipSuccess) return e;
+  }
+  BGemm p{};
+  p.ld = L.Kp;
+  p.Out = GU;
+  p.ldo = 2 * L.Jh;
+  p.I = (int)M;
+  p.J = (int)(2 * L.Jh);
+  p.Kp = (int)L.Kp;
+  p.A[0] = Uh; p.A[1] = Ul;
+  p.B[0] = Wh; p.B[1] = Wl;
+  e = w_bf16 ? run_bgemm<2, 1, 2, 0b10, 0b00, false>(p, st)
+             : run_bgemm<2, 2, 3, 0b010, 0b100, false>(p, st);
+  if (e != hipSuccess) return e;
+  const int64_t n = M * (d_ff / 4);
+  hipLaunchKernelGGL(swiglu_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, GU, 2 * L.Jh,
+                     L.Jh, (int)M, (int)d_ff, H);
+  return hipGetLastError();
+}
+
+size_t propagate_ws_bytes(int64_t M, int64_t d_ff, int64_t d) {
+  return targets_layout(M, d_ff, d).total;
+}
+
+hipError_t launch_propagate(const float* Hc, const void* W, bool w_bf16, const float* dW,
+                            const float* Zc, int64_t M, int64_t d_ff, int64_t d, float* Y, void* ws,
+                            hipStream_t st) {
+  const TargetsWs L = targets_layout(M, d_ff, d);
+  const int64_t Mp = pad_to(M, G_BM), Kp = pad_to(d_ff, G_KC), Jp = pad_to(d, G_BM);
+  char* w = (char*)ws;
+  __bf16 *Hh = (__bf16*)(w + L.Dh), *Hl = (__bf16*)(w + L.Dl);
+  __bf16 *Wh = (__bf16*)(w + L.Wh), *Wl = (__bf16*)(w + L.Wl);
+  hipError_t e = run_split_rows(Hc, nullptr, M, d_ff, d_ff, Hh, Hl, Mp, Kp, st);
+  if (e != hipSuccess) return e;
+  // (W + dW) [d_ff][d] -> transposed [d][d_ff], split
+  if (w_bf16)
+    e = run_split_transpose((const __bf16*)W, dW, d_ff, d, d, Wh, Wl, Kp, Jp, st, 1.f);
+  else
+    e = run_split_transpose((const float*)W, dW, d_ff, d, d, Wh, Wl, Kp, Jp, st, 1.f);
+  if (e != hipSuccess) return e;
+  BGemm p{};  // Y = Hc (W + dW) + Zc: terms (0,0) (0,1) (1,0)
+  p.ld = Kp;
+  p.Out = Y;
+  p.ldo = d;
+  p.E1 = Zc;
+  p.lde = d;
+  p.rho = 1.f;
+  p.I = (int)M;
+  p.J = (int)d;
+  p.Kp = (int)Kp;
+  p.A[0] = Hh; p.A[1] = Hl;
+  p.B[0] = Wh; p.B[1] = Wl;
+  return run_bgemm<2, 2, 3, 0b100, 0b010, false>(p, st);
+}
 size_t normal_eq_ws_bytes(int64_t rows, int64_t din, int64_t dout) {
   return normal_eq_layout(rows, din, dout).total;
 }
 
 hipError_t launch_targets(const float* Of, const float* Oc, const void* W, bool w_bf16, int64_t M,
-                          int64_t din, int64_t dout, int rho, float* T, void* ws, hipStream_t st) {
+                          int64_t din, int64_t dout, int rho, float* T, void* ws, hipStream_t st,
+                          const float* Zf, const float* Zc) {
   const TargetsWs L = targets_layout(M, din, dout);
   const int64_t Mp = pad_to(M, G_BM), Kp = pad_to(din, G_KC), Jp = pad_to(dout, G_BM);
   char* w = (char*)ws;
@@ -464,7 +620,12 @@ hipError_t launch_targets(const float* Of, const float* Oc, const void* W, bool 
   p.ld = Kp;
   p.Out = T;
   p.ldo = dout;
-  if (rho) {
+  if (Zf) {  // residual pair of its own (width dout)
+    p.E1 = Zf;
+    p.E2 = Zc;
+    p.lde = dout;
+    p.rho = 1.f;
+  } else if (rho) {
     p.E1 = Of;
     p.E2 = Oc;
     p.lde = din;

@@ -103,10 +103,13 @@ def test_attend_chunk_validation(L):
     assert chunk(Ks=FAKE + 8) == B.E_VALUE                # misaligned
     assert chunk() == B.E_WORKSPACE
     # bf16 workspace: V^T tiles of the cache and of the own entries, one flag per item
-    vt = 2 * (32 * 128 * 2) + 4 * (32 * 128 * 2)          # Hkv=2: 64 cache keys, 8 own keys
+    # (plus split-key partials, as for attend_full at the same shape)
+    vt = 2 * (32 * 128 * 2)                               # Hkv=2: 8 own keys in one tile
     w = L.patchkv_attend_chunk_workspace_bytes(B.BF16, 8, 64, 4, 2, 128)
-    assert vt <= w <= vt + 4096
-    assert L.patchkv_attend_chunk_workspace_bytes(B.F32, 8, 64, 4, 2, 128) == 0
+    assert w - L.patchkv_attend_workspace_bytes(B.BF16, 8, 64, 4, 2, 128) == vt
+    # f32: only the partial results of a key split, as for the other attention calls
+    assert (L.patchkv_attend_chunk_workspace_bytes(B.F32, 8, 64, 4, 2, 128)
+            == L.patchkv_attend_workspace_bytes(B.F32, 8, 64, 4, 2, 128))
 
 
 def test_targets_validation(L):
@@ -159,3 +162,23 @@ def test_layer_validation(L):
     assert call(rho=3) == B.E_VALUE
     assert call(mode=7) == B.E_VALUE
     assert call() == B.E_WORKSPACE               # needs a workspace
+
+
+def test_mlp_validation(L):
+    f = L.patchkv_mlp_features
+    assert f(B.BF16, None, FAKE, FAKE, 4, 64, 128, 1e-5, FAKE, None, 0, None) == B.E_NULL
+    assert f(B.F64, FAKE, FAKE, FAKE, 4, 64, 128, 1e-5, FAKE, None, 0, None) == B.E_DTYPE
+    assert f(B.BF16, FAKE, FAKE, FAKE, 4, 64, 130, 1e-5, FAKE, None, 0, None) == B.E_SHAPE  # d_ff % 4
+    assert f(B.BF16, FAKE, FAKE, FAKE, 4, 64, 1 << 17, 1e-5, FAKE, None, 0, None) == B.E_SHAPE
+    assert f(B.BF16, FAKE, FAKE, FAKE, 4, 64, 128, -1.0, FAKE, None, 0, None) == B.E_VALUE
+    assert f(B.BF16, FAKE, FAKE, FAKE, 4, 64, 128, 1e-5, FAKE + 4, None, 0, None) == B.E_VALUE
+    assert f(B.BF16, FAKE, FAKE, FAKE, 4, 64, 128, 1e-5, FAKE, None, 0, None) == B.E_WORKSPACE
+    assert L.patchkv_mlp_features_workspace_bytes(B.BF16, 4096, 4096, 14336) > 2 * 4096 * 28672 * 2
+    t = L.patchkv_compute_block_targets
+    assert t(B.BF16, FAKE, FAKE, FAKE, None, FAKE, 4, 128, 64, FAKE, None, 0, None) == B.E_NULL
+    assert t(B.BF16, FAKE, FAKE, FAKE, FAKE, FAKE, 0, 128, 64, FAKE, None, 0, None) == B.E_SHAPE
+    assert t(B.BF16, FAKE, FAKE, FAKE, FAKE, FAKE, 4, 128, 64, FAKE, None, 0, None) == B.E_WORKSPACE
+    p = L.patchkv_propagate_student
+    assert p(B.BF16, FAKE, FAKE, None, FAKE, 4, 128, 64, FAKE, None, 0, None) == B.E_NULL
+    assert p(B.F64, FAKE, FAKE, FAKE, FAKE, 4, 128, 64, FAKE, None, 0, None) == B.E_DTYPE
+    assert p(B.BF16, FAKE, FAKE, FAKE, FAKE, 4, 128, 64, FAKE, None, 0, None) == B.E_WORKSPACE

@@ -23,18 +23,18 @@ import torch
 import oracle
 import paper_2609_39329_amd as pkv
 from gpu_util import DEV, host, rel
-from workloads import CONFIGS, make_chunk_inputs, make_layer_inputs
+from workloads import CONFIGS, make_chunk_inputs, make_layer_inputs, make_mlp_weights
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 sys.path.insert(0, ROOT)
 from bench import Buffers, LayerDev, chunked_layer_steps, layer_steps  # noqa: E402
 
 sys.path.insert(0, os.path.join(ROOT, "tests", "golden"))
-from make_oracle_fixtures import fixture_path, sample_rows, sketch_matrix  # noqa: E402
+from make_oracle_fixtures import fixture_path, sample_rows, sample_tokens, sketch_matrix  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
-CASES = [(1, 0), (2, 0), (4, 0), (3, 0), (3, 8), (3, 16), (3, 24), (3, 31), (5, 0)]
+CASES = [(1, 0), (2, 0), (4, 0), (3, 0), (3, 8), (3, 16), (3, 24), (3, 31), (5, 0), (6, 0)]
 TOL = 2e-2
 
 
@@ -48,7 +48,8 @@ def test_full_size_layer_patch(cid, layer):
     fx = np.load(path)
     inp = make_layer_inputs(cfg, layer)
     chunks = [make_chunk_inputs(inp, j, cfg.M) for j in range(cfg.chunks)] if cfg.chunks > 1 else ()
-    L = LayerDev(inp, torch, DEV, chunks)
+    mlp = make_mlp_weights(inp, cfg.d_ff) if cfg.d_ff else None
+    L = LayerDev(inp, torch, DEV, chunks, mlp)
     bufs = Buffers(cfg, torch, DEV, 1)
     if chunks:
         chunked_layer_steps(pkv, cfg, L, bufs, 0)
@@ -58,13 +59,19 @@ def test_full_size_layer_patch(cid, layer):
     assert int(bufs.info[0].item()) == 0
     dW = host(bufs.dW[0])
 
-    rows = sample_rows(cid, layer, cfg.d)
+    rows = sample_rows(cid, layer, dW.shape[0])
     assert np.array_equal(rows, fx["rows"])
     e_rows = rel(dW[rows], fx["dW_rows"])
     e_sk = rel(dW @ sketch_matrix(cid, layer, cfg.d), fx["sketch"])
     e_norm = abs(np.linalg.norm(dW) - float(fx["norm"])) / float(fx["norm"])
     print(f"  rows {e_rows:.3e}  sketch {e_sk:.3e}  norm {e_norm:.3e}", flush=True)
     assert e_rows <= TOL and e_sk <= TOL and e_norm <= TOL
+    if cfg.d_ff:  # the propagated student state on sampled tokens
+        y_rows = sample_tokens(cid, layer, cfg.M)
+        assert np.array_equal(y_rows, fx["y_rows"])
+        e_y = rel(host(bufs.Y)[y_rows], fx["Y_rows"])
+        print(f"  Y rows {e_y:.3e}", flush=True)
+        assert e_y <= TOL
 
     # attention outputs on sampled query rows, computed by the oracle row by row
     q_rows = np.random.default_rng([cid, layer, 7]).choice(cfg.M, 3, replace=False)
@@ -94,7 +101,7 @@ def test_full_size_layer_patch(cid, layer):
     print(f"  O_f rows {e_of:.3e}  O_c rows {e_oc:.3e}", flush=True)
     assert e_of <= 4e-3 and e_oc <= 5e-5
 
-    if chunks:
+    if chunks or cfg.d_ff:
         return
     # the single-call entry point runs the same kernels in the same order
     dW2, info2 = pkv.compute_layer_patch(L.Q, L.K, L.V, L.W, idx=L.idx, Kc=L.Kc, Vc=L.Vc,

@@ -38,6 +38,7 @@ class Config:
     n_mix: int = 0           # synthesize: entries mixed per synthetic entry
     chunks: int = 1          # reference chunks per layer (M tokens each, own causal prefix)
     d_ff: int = 0            # > 0: patch the d_ff x d down-projection of a SwiGLU MLP
+    ridge: str = "absolute"  # "absolute": lam is lambda; "adaptive": lam is lambda_0 of Eq. 7
 
     @property
     def group(self) -> int:
@@ -71,9 +72,11 @@ CONFIGS = (
            B=1720, M=5120, lam=1e-1, dtype="bf16", chunks=4, n_sink=4, n_recent=860,
            n_random=856),
     # the paper's own block: the patch is the 14336 x 4096 down-projection of
-    # Llama-3-8B's SwiGLU MLP, fed by the attention output of config 3's layer
+    # Llama-3-8B's SwiGLU MLP, fed by the attention output of config 3's layer, with
+    # the paper's adaptive ridge (Eq. 7), lambda_0 = 1e-3
     Config(6, "llama3-8b-mlp-layer-172k", d=4096, Hq=32, Hkv=8, dh=128, N=172032, B=1720,
-           M=4096, lam=1e-1, dtype="bf16", d_ff=14336, n_sink=4, n_recent=860, n_random=856),
+           M=4096, lam=1e-3, dtype="bf16", d_ff=14336, ridge="adaptive", n_sink=4, n_recent=860,
+           n_random=856),
 )
 
 
