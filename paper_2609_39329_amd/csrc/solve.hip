@@ -42,7 +42,7 @@ constexpr int diag_threads() {
   return (NT * (NT + 1) / 2 + 63) / 64 * 64;
 }
 
-constexpr int kRedBlocks = 256;
+constexpr int kRedBlocks = 1024;  // workgroups of the adaptive-ridge reduction
 
 template <class T>
 struct GemmDesc {
@@ -864,18 +864,19 @@ __global__ __launch_bounds__(256) void init_kernel(const T* __restrict__ G, cons
   if (blockIdx.x == 0 && threadIdx.x == 0) *info = 0;
 }
 
-// Stage 1 of the adaptive ridge: per-block partial sums of G_ij^2 and G_ii.
+// Stage 1 of the adaptive ridge: per-block partial sums of G_ij^2 and G_ii, in fp64
+// and in a fixed order (each thread strides over the matrix, then the diagonal).
 template <class T>
 __global__ __launch_bounds__(256) void ridge_partial_kernel(const T* __restrict__ G, int64_t d,
                                                             double* part) {
   __shared__ double s2[256], st[256];
   double a = 0.0, b = 0.0;
-  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < d * d;
-       e += (int64_t)kRedBlocks * 256) {
+  const int64_t first = (int64_t)blockIdx.x * 256 + threadIdx.x, stride = (int64_t)kRedBlocks * 256;
+  for (int64_t e = first; e < d * d; e += stride) {
     const double v = (double)G[e];
-    a += v * v;
-    if (e / d == e % d) b += v;
+    a = fma(v, v, a);
   }
+  for (int64_t i = first; i < d; i += stride) b += (double)G[i * d + i];
   s2[threadIdx.x] = a;
   st[threadIdx.x] = b;
   __syncthreads();
@@ -896,8 +897,13 @@ __global__ __launch_bounds__(256) void ridge_partial_kernel(const T* __restrict_
 __global__ __launch_bounds__(256) void ridge_final_kernel(const double* part, double lam0,
                                                           double* lam_out) {
   __shared__ double s2[256], st[256];
-  s2[threadIdx.x] = part[2 * threadIdx.x];
-  st[threadIdx.x] = part[2 * threadIdx.x + 1];
+  double a = 0.0, b = 0.0;
+  for (int i = threadIdx.x; i < kRedBlocks; i += 256) {
+    a += part[2 * i];
+    b += part[2 * i + 1];
+  }
+  s2[threadIdx.x] = a;
+  st[threadIdx.x] = b;
   __syncthreads();
   for (int s = 128; s > 0; s >>= 1) {
     if ((int)threadIdx.x < s) {
