@@ -68,6 +68,7 @@ __all__ = [
     "normal_equations", "normal_equations_chunked", "ridge_lambda", "solve_patch",
     "layer_patch", "attention_rows", "attention_chunk", "layer_patch_chunked", "rms_norm",
     "silu", "mlp_features", "block_targets", "propagate_student", "mlp_layer_patch",
+    "dequantize_mx",
 ]
 
 
@@ -96,12 +97,14 @@ def softmax_rows(S: np.ndarray) -> np.ndarray:
 
 
 def attention(Q: np.ndarray, K: np.ndarray, V: np.ndarray, scale: float | None = None,
-              max_score_bytes: int = 1 << 28) -> np.ndarray:
+              max_score_bytes: int = 1 << 28, bias: np.ndarray | None = None) -> np.ndarray:
     """Reference-query attention over one cache (teacher Alg. 1 / student Alg. 1).
 
     Q [M, Hq, dh], K and V [Hkv, Nk, dh], all float64. Returns O [M, Hq*dh]
-    with O[m, h*dh:(h+1)*dh] = softmax(scale * Q[m,h] K[g]^T) V[g],
-    g = floor(h / (Hq/Hkv)). Rows are processed in chunks only to bound memory.
+    with O[m, h*dh:(h+1)*dh] = softmax(scale * Q[m,h] K[g]^T + bias[g]) V[g],
+    g = floor(h / (Hq/Hkv)); ``bias`` [Hkv, Nk] (natural-log units, default none)
+    is a per-entry logit bias, as an attention-matching compressed cache carries
+    with its entries (Sec. 3.1). Rows are processed in chunks only to bound memory.
     """
     M, Hq, dh = Q.shape
     Hkv, Nk, dh2 = K.shape
@@ -117,8 +120,19 @@ def attention(Q: np.ndarray, K: np.ndarray, V: np.ndarray, scale: float | None =
         for r0 in range(0, M, rows):
             r1 = min(M, r0 + rows)
             S = (Q[r0:r1, h, :] @ K[g].T) * scale
+            if bias is not None:
+                S = S + bias[g][None, :]
             O[r0:r1, h * dh:(h + 1) * dh] = softmax_rows(S) @ V[g]
     return O
+
+
+def dequantize_mx(q: np.ndarray, e: np.ndarray, block: int = 32) -> np.ndarray:
+    """A block-scaled integer cache entry (Sec. 4, quantized KV caches) as float64:
+    value = q * 2^e, q [..., dh] integers, e [..., dh / block] one power-of-two
+    exponent per block of ``block`` consecutive channels."""
+    q = np.asarray(q, dtype=np.float64)
+    scale = np.exp2(np.repeat(np.asarray(e, dtype=np.float64), block, axis=-1))
+    return q * scale
 
 
 def attention_rows(Q: np.ndarray, K: np.ndarray, V: np.ndarray, rows: np.ndarray,

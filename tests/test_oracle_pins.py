@@ -690,3 +690,64 @@ def test_mlp_pins_catch_planted_mistakes():
     assert check_mlp_features(feats_swapped) > 1e-2
     assert check_block_targets(targets_no_residual) > 1e-2
     assert check_block_targets(targets_student_weights) > 1e-2
+
+
+# ------------------------------------------- compressed-cache formats (f4): bias, MX int
+
+def brute_attention_bias(Q, K, V, scale, bias):
+    M, Hq, dh = Q.shape
+    Hkv, N, _ = K.shape
+    grp = Hq // Hkv
+    O = np.zeros((M, Hq * dh))
+    for m in range(M):
+        for h in range(Hq):
+            g = h // grp
+            s = [scale * sum(Q[m, h, c] * K[g, n, c] for c in range(dh)) + bias[g, n] for n in range(N)]
+            mx = max(s)
+            e = [math.exp(x - mx) for x in s]
+            for c in range(dh):
+                O[m, h * dh + c] = sum(e[n] * V[g, n, c] for n in range(N)) / sum(e)
+    return O
+
+
+def test_attention_bias_bruteforce_and_closed_forms():
+    rng = np.random.default_rng(51)
+    Q, K, V = rand_attn(rng, 3, 6, 4, 2, 3)
+    bias = rng.standard_normal((2, 6))
+    assert rel(oracle.attention(Q, K, V, 0.3, bias=bias), brute_attention_bias(Q, K, V, 0.3, bias)) < 1e-13
+    # a bias constant per KV head changes nothing (softmax shift invariance)
+    Q, K, V = rand_attn(rng, 7, 20, 8, 2, 8)
+    O = oracle.attention(Q, K, V)
+    const = np.repeat(np.array([[3.0], [-2.0]]), 20, axis=1)
+    assert rel(oracle.attention(Q, K, V, bias=const), O) < 1e-14
+    # zero keys: the weights are exactly e^bias, O = the bias-weighted mean of V
+    w = rng.random((2, 20)) + 0.1
+    Ob = oracle.attention(Q, 0 * K, V, bias=np.log(w)).reshape(7, 8, 8)
+    for h in range(8):
+        g = h // 4
+        ref = (w[g][:, None] * V[g]).sum(0) / w[g].sum()
+        assert np.allclose(Ob[:, h], ref[None, :], atol=1e-14)
+    # a bias of log(k) on an entry equals k copies of that entry
+    b = np.zeros((2, 20))
+    b[:, 5] = np.log(3.0)
+    K3 = np.concatenate([K, K[:, 5:6], K[:, 5:6]], axis=1)
+    V3 = np.concatenate([V, V[:, 5:6], V[:, 5:6]], axis=1)
+    assert rel(oracle.attention(Q, K, V, bias=b), oracle.attention(Q, K3, V3)) < 1e-14
+
+
+def test_dequantize_mx_library_and_exactness():
+    from workloads import bf16_bits_to_f32, bf16_round_bits, quantize_mx
+    rng = np.random.default_rng(52)
+    q = rng.integers(-127, 128, size=(3, 4, 64)).astype(np.int8)
+    e = rng.integers(-20, 5, size=(3, 4, 2)).astype(np.int8)
+    d = oracle.dequantize_mx(q, e)
+    assert np.array_equal(d, np.ldexp(q.astype(np.float64), np.repeat(e, 32, axis=-1).astype(np.int64)))
+    # int8 magnitudes times powers of two are bf16 numbers: the round trip is exact
+    f = d.astype(np.float32)
+    assert np.array_equal(bf16_bits_to_f32(bf16_round_bits(f)), f)
+    # the quantizer of the inputs stays within half a step of the value
+    x = rng.standard_normal((2, 9, 128)).astype(np.float32) * 3
+    for bits in (8, 4):
+        qq, ee = quantize_mx(x, bits)
+        step = np.exp2(np.repeat(ee.astype(np.float64), 32, axis=-1))
+        assert np.all(np.abs(oracle.dequantize_mx(qq, ee) - x) <= 0.5 * step + 1e-12)

@@ -4,7 +4,8 @@ Recipe (the same bytes feed the oracle and the GPU path):
 
 * Every random tensor has a tensor id: 0 key scales, 1 K, 2 V, 3 Q, 4 W,
   5 eviction middle positions, 6 synthesis positions, 7 synthesis weights;
-  8 MLP gate projection, 9 MLP up projection, 10 MLP down projection;
+  8 MLP gate projection, 9 MLP up projection, 10 MLP down projection,
+  11 the compressed cache's per-entry logit bias;
   reference chunk j of a chunked reference set: 16 + 4j its queries, 17 + 4j its
   own keys, 18 + 4j its own values.
 * Normal tensors are drawn in C order in blocks of ``BLOCK`` elements; block ``b``
@@ -17,6 +18,13 @@ Recipe (the same bytes feed the oracle and the GPU path):
   A chunk's queries and own values are N(0, 1); its own keys carry the layer's
   key scales s like the cache keys. MLP weights: gate and up [d, d_ff] are
   Z * float32(1/sqrt(d)), down [d_ff, d] is Z * float32(1/sqrt(d_ff)).
+* Attention-matching logit bias of a compressed cache: per (KV head, entry)
+  beta = log(n_mix) + 0.25 Z (an entry standing for n_mix originals), float32.
+* Block-scaled integer cache (MX-style): per (KV head, entry) and block of 32
+  channels, e = ceil(log2(max|x| / q_max)) (q_max 127 for int8, 7 for int4;
+  e = 0 for an all-zero block) and q = round-half-even(x / 2^e) clipped to
+  [-q_max, q_max]; int8 q as int8, int4 q packed two per byte (even channel in
+  the low nibble), e as int8. q * 2^e is exact in bf16.
 * bf16 tensors are rounded from those float32 values with round-to-nearest-even
   and stored as their raw uint16 bit patterns; fp32 tensors are stored as is.
 * Eviction subset: ``n_sink`` sinks, the last ``n_recent`` tokens, and
@@ -43,7 +51,7 @@ from .configs import Config
 BLOCK = 1 << 22
 
 TID_SCALE, TID_K, TID_V, TID_Q, TID_W, TID_EVICT, TID_SYN_POS, TID_SYN_W = range(8)
-TID_GATE, TID_UP, TID_DOWN = 8, 9, 10
+TID_GATE, TID_UP, TID_DOWN, TID_BIAS = 8, 9, 10, 11
 TID_CHUNK = 16  # chunk j: 16 + 4j queries, 17 + 4j own keys, 18 + 4j own values
 
 
@@ -240,6 +248,53 @@ def make_mlp_weights(inp: LayerInputs, d_ff: int) -> MlpWeights:
     Wu = _normal_tensor(seed, inp.cid, inp.layer, TID_UP, (d, d_ff), bf16, lambda z, lo: z * sg)
     Wd = _normal_tensor(seed, inp.cid, inp.layer, TID_DOWN, (d_ff, d), bf16, lambda z, lo: z * sd)
     return MlpWeights(Wg=Wg, Wu=Wu, Wd=Wd, d_ff=d_ff)
+
+
+def make_cache_bias(inp: LayerInputs, n_mix: int = 64, sigma: float = 0.25) -> np.ndarray:
+    """Per-entry logit bias [Hkv, B] of the layer's compressed cache (float32)."""
+    z = _rng(inp.extra["seed"], inp.cid, inp.layer, TID_BIAS).standard_normal(
+        (inp.Hkv, inp.B), dtype=np.float32)
+    return (np.float32(np.log(n_mix)) + np.float32(sigma) * z).astype(np.float32)
+
+
+@dataclass
+class QuantCache:
+    """A block-scaled integer cache: q (int8 [Hkv, n, dh], or uint8 [Hkv, n, dh/2]
+    holding two int4 per byte) and e (int8 [Hkv, n, dh/32]) for K and for V."""
+    bits: int
+    Kq: np.ndarray
+    Ke: np.ndarray
+    Vq: np.ndarray
+    Ve: np.ndarray
+
+
+def quantize_mx(X: np.ndarray, bits: int, block: int = 32):
+    """float array [..., dh] -> (q, e) per the recipe above (q unpacked, int8)."""
+    qmax = {8: 127, 4: 7}[bits]
+    shp = X.shape
+    xb = np.asarray(X, dtype=np.float64).reshape(shp[:-1] + (shp[-1] // block, block))
+    amax = np.abs(xb).max(axis=-1)
+    with np.errstate(divide="ignore"):
+        e = np.where(amax > 0, np.ceil(np.log2(np.where(amax > 0, amax, 1.0) / qmax)), 0.0)
+    q = np.clip(np.rint(xb / np.exp2(e)[..., None]), -qmax, qmax)
+    return q.reshape(shp).astype(np.int8), e.astype(np.int8)
+
+
+def pack_int4(q: np.ndarray) -> np.ndarray:
+    """int8 values in [-8, 7] [..., dh] -> uint8 [..., dh/2], even channel in the low nibble."""
+    u = (q.astype(np.int16) & 0xF).astype(np.uint8)
+    return (u[..., 0::2] | (u[..., 1::2] << 4)).astype(np.uint8)
+
+
+def make_quant_cache(K: np.ndarray, V: np.ndarray, bits: int, dtype: str) -> QuantCache:
+    """Block-scaled integer version of a cache K, V [Hkv, n, dh] (stored form)."""
+    kf = bf16_bits_to_f32(K) if dtype == "bf16" else K
+    vf = bf16_bits_to_f32(V) if dtype == "bf16" else V
+    Kq, Ke = quantize_mx(kf, bits)
+    Vq, Ve = quantize_mx(vf, bits)
+    if bits == 4:
+        Kq, Vq = pack_int4(Kq), pack_int4(Vq)
+    return QuantCache(bits=bits, Kq=Kq, Ke=Ke, Vq=Vq, Ve=Ve)
 
 
 def _mix(X: np.ndarray, pos: np.ndarray, w: np.ndarray, bf16: bool) -> np.ndarray:
