@@ -76,6 +76,13 @@ typedef enum {
   PATCHKV_SOLVE_EXACT_F32 = 16
 } patchkv_ridge_mode;
 
+/* Storage of a cache's keys and values (patchkv_attend_cache). */
+typedef enum {
+  PATCHKV_KV_PLAIN = 0,  /* K, V in the call's dtype */
+  PATCHKV_KV_MXINT8 = 1, /* int8 q and one int8 power-of-two exponent e per 32 channels: q * 2^e */
+  PATCHKV_KV_MXINT4 = 2  /* the same with int4 q in [-8, 7], two per byte, even channel low */
+} patchkv_kv_format;
+
 /* Human-readable name of a status code (static string, never NULL). */
 const char* patchkv_status_string(int status);
 
@@ -154,6 +161,35 @@ int patchkv_attend_chunk(int dtype, const void* Q, const void* K, const void* V,
                          const void* Vs, int64_t M, int Hq, int Hkv, int dh, float scale,
                          int p_terms, float* O, void* workspace, size_t workspace_bytes,
                          void* stream);
+
+/* ------------------------------------------------------------------------- */
+/* Attention over a compressed cache in the storage formats of Sec. 3.1 and     */
+/* Sec. 4 (attention-matching logit bias; quantized KV caches):                */
+/*   O[m, h*dh + j] = sum_n softmax_n(scale <Q[m,h,:], K_n> + bias[g, n]) V_n[j] */
+/* over the n_cache entries of KV head g = floor(h / (Hq/Hkv)).                 */
+/*  - kv_format PATCHKV_KV_PLAIN: K, V [Hkv][n_src][dh] in dtype; Ke, Ve NULL.   */
+/*  - PATCHKV_KV_MXINT8: K, V int8 [Hkv][n_src][dh]; Ke, Ve int8                */
+/*    [Hkv][n_src][dh/32]; entry value q * 2^e (exact in bf16).                 */
+/*  - PATCHKV_KV_MXINT4: K, V uint8 [Hkv][n_src][dh/2], two int4 per byte, the  */
+/*    even channel in the low nibble; Ke, Ve as for MXINT8.                     */
+/*  - idx != NULL: the cache is rows idx[0..n_cache) (eviction subset; entries  */
+/*    outside [0, n_src) read as zero rows); idx == NULL: rows 0..n_cache.       */
+/*  - bias [Hkv][n_cache] float (natural-log units, indexed by cache entry) or  */
+/*    NULL for none.                                                           */
+/*  - p_terms as for patchkv_attend_chunk (1: P rounded to bf16; 2: two terms). */
+/* Quantized entries are first expanded to dtype rows in the workspace (the      */
+/* compressed cache is small), then attended like a plain cache.               */
+/* Limits as patchkv_attend_compressed with B = n_cache; dh a multiple of 32.  */
+/* Workspace: patchkv_attend_cache_workspace_bytes(...).                       */
+/* ------------------------------------------------------------------------- */
+size_t patchkv_attend_cache_workspace_bytes(int dtype, int kv_format, int64_t M, int64_t n_cache,
+                                            int Hq, int Hkv, int dh);
+
+int patchkv_attend_cache(int dtype, const void* Q, const void* K, const void* V, int kv_format,
+                         const int8_t* Ke, const int8_t* Ve, const int32_t* idx, int64_t n_src,
+                         int64_t n_cache, const float* bias, int64_t M, int Hq, int Hkv, int dh,
+                         float scale, int p_terms, float* O, void* workspace,
+                         size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------- */
 /* Per-token targets, Eq. 5 in row form with h = z = the attention output:      */

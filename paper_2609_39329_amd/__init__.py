@@ -3,12 +3,14 @@
 The library (``lib/libpatchkv.so``) is loaded on first use by :mod:`.binding`;
 there is no CPU fallback.
 """
-from .binding import (BF16, F32, F64, RIDGE_ABSOLUTE, RIDGE_ADAPTIVE, SOLVE_EXACT_F32,
-                      PatchKVError, accumulate_normal_eq, attend_chunk, attend_compressed,
+from .binding import (BF16, F32, F64, KV_MXINT4, KV_MXINT8, KV_PLAIN, RIDGE_ABSOLUTE,
+                      RIDGE_ADAPTIVE, SOLVE_EXACT_F32, PatchKVError, accumulate_normal_eq,
+                      attend_cache, attend_chunk, attend_compressed,
                       attend_full, compute_block_targets, compute_layer_patch, compute_targets,
                       layer_workspace_bytes, lib, mlp_features, propagate_student, solve_patch)
 
-__all__ = ["BF16", "F32", "F64", "RIDGE_ABSOLUTE", "RIDGE_ADAPTIVE", "SOLVE_EXACT_F32",
-           "PatchKVError", "accumulate_normal_eq", "attend_chunk", "attend_compressed",
+__all__ = ["BF16", "F32", "F64", "KV_MXINT4", "KV_MXINT8", "KV_PLAIN", "RIDGE_ABSOLUTE",
+           "RIDGE_ADAPTIVE", "SOLVE_EXACT_F32", "PatchKVError", "accumulate_normal_eq",
+           "attend_cache", "attend_chunk", "attend_compressed",
            "attend_full", "compute_block_targets", "compute_layer_patch", "compute_targets",
            "layer_workspace_bytes", "lib", "mlp_features", "propagate_student", "solve_patch"]

@@ -42,6 +42,11 @@ SIGNATURES = {
     "patchkv_attend_chunk": (_c_int, [_c_int, _c_vp, _c_vp, _c_vp, _c_vp, _c_i64, _c_i64, _c_vp,
                                       _c_vp, _c_i64, _c_int, _c_int, _c_int, ctypes.c_float,
                                       _c_int, _c_vp, _c_vp, _c_sz, _c_vp]),
+    "patchkv_attend_cache_workspace_bytes": (_c_sz, [_c_int, _c_int, _c_i64, _c_i64, _c_int,
+                                                     _c_int, _c_int]),
+    "patchkv_attend_cache": (_c_int, [_c_int, _c_vp, _c_vp, _c_vp, _c_int, _c_vp, _c_vp, _c_vp,
+                                      _c_i64, _c_i64, _c_vp, _c_i64, _c_int, _c_int, _c_int,
+                                      ctypes.c_float, _c_int, _c_vp, _c_vp, _c_sz, _c_vp]),
     "patchkv_targets_workspace_bytes": (_c_sz, [_c_int, _c_i64, _c_i64, _c_i64]),
     "patchkv_compute_targets": (_c_int, [_c_int, _c_vp, _c_vp, _c_vp, _c_i64, _c_i64, _c_i64,
                                          _c_int, _c_vp, _c_vp, _c_sz, _c_vp]),
@@ -235,6 +240,41 @@ def compute_targets(Of, Oc, W, rho: int = 1, T=None, stream=None):
            L.patchkv_compute_targets(wdt, _ptr(Of), _ptr(Oc), _ptr(W), M, din, dout, rho, _ptr(T),
                                      _ptr(ws), nb, _stream(stream)))
     return T
+
+
+KV_PLAIN, KV_MXINT8, KV_MXINT4 = 0, 1, 2
+
+
+def attend_cache(Q, K, V, kv_format: int = KV_PLAIN, Ke=None, Ve=None, idx=None,
+                 n_cache: Optional[int] = None, bias=None, scale: Optional[float] = None,
+                 p_terms: int = 2, O=None, stream=None):
+    """Attention over a compressed cache with an optional per-entry logit bias
+    bias [Hkv, n_cache] (float32) and K, V stored plain (Q's dtype) or block-scaled:
+    KV_MXINT8 (int8 [Hkv, n, dh]) / KV_MXINT4 (uint8 [Hkv, n, dh/2]) with int8
+    exponents Ke, Ve [Hkv, n, dh/32]. The cache is rows idx (int32 [n_cache]) or the
+    first n_cache rows (default all)."""
+    torch = _torch()
+    _require_gpu(Q, K, V, Ke, Ve, idx, bias, O)
+    M, Hq, dh = Q.shape
+    Hkv, n_src = K.shape[0], K.shape[1]
+    if idx is not None:
+        if idx.dtype != torch.int32:
+            raise TypeError("idx must be int32")
+        n_cache = idx.shape[0]
+    elif n_cache is None:
+        n_cache = n_src
+    dt = _dtype_code(Q)
+    scale = 1.0 / dh ** 0.5 if scale is None else scale
+    if O is None:
+        O = torch.empty((M, Hq * dh), dtype=torch.float32, device=Q.device)
+    L = lib()
+    nb = L.patchkv_attend_cache_workspace_bytes(dt, kv_format, M, n_cache, Hq, Hkv, dh)
+    ws = _workspace(nb, Q.device, stream)
+    _check("patchkv_attend_cache",
+           L.patchkv_attend_cache(dt, _ptr(Q), _ptr(K), _ptr(V), kv_format, _ptr(Ke), _ptr(Ve),
+                                  _ptr(idx), n_src, n_cache, _ptr(bias), M, Hq, Hkv, dh, scale,
+                                  p_terms, _ptr(O), _ptr(ws), nb, _stream(stream)))
+    return O
 
 
 def mlp_features(Z, Wg, Wu, eps: float = 1e-5, H=None, stream=None):

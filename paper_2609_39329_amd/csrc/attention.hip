@@ -25,6 +25,12 @@
 // Both paths can split the cache into key ranges (more workgroups for small M);
 // attn_combine_kernel then merges the partial (O, m, l) triples.
 //
+// Per-entry logit bias (BIAS = true; an attention-matching compressed cache carries
+// one per entry): bias[g][n] is added to the logit of cache entry n. The bf16 path
+// stores each tile's 32 biases (divided by the softmax scale) in LDS with the K
+// tile and starts the score MFMA accumulator from them, so the steady-state loop
+// gains four 16-byte LDS reads per tile and no VALU work.
+//
 // Chunked reference sets (OWN = true): the queries are one chunk's tokens, and
 // token m also attends to the chunk's own entries 0..m (its causal prefix), which
 // follow the cache in the key order: a work item's first key tiles are its range
@@ -81,6 +87,10 @@ struct AttnParams {
   const void* Vs;
   const __bf16* Vts;
   int Ms, own_tiles;
+  // per-entry logit bias [Hkv][Nk] (BIAS kernels; natural-log units) and the factor
+  // that puts it in the units of the raw score q.k (bf16: 1 / scale; f32: 1)
+  const float* bias;
+  float bias_mul;
 };
 
 // V -> V^T in 32-key tiles, so that the P V product reads V with plain 16-byte LDS
@@ -133,8 +143,9 @@ __global__ __launch_bounds__(256) void vt_kernel(const __bf16* __restrict__ V,
 // marked in p.flags at the end and its outputs are not trusted. SAFE = true (fixup,
 // launched right after on the same stream): the lazy-rescale online softmax, run
 // only for marked work items, overwriting their outputs.
-template <int DH, bool GATHER, bool PSPLIT, bool PARTIAL, bool SAFE, bool OWN>
+template <int DH, bool GATHER, bool PSPLIT, bool PARTIAL, bool SAFE, bool OWN, bool BIAS>
 __global__ __launch_bounds__(kThreadsBf16, 1) void attn_bf16_kernel(AttnParams p) {
+  static_assert(!(OWN && BIAS), "own entries carry no bias");
   constexpr int KT = kKeyTile;
   constexpr int NKT = KT / 32;  // 32-key MFMA tiles per iteration
   constexpr int KP = DH + 8;   // K tile pitch (elements): conflict-free 16-byte row reads
@@ -148,6 +159,7 @@ __global__ __launch_bounds__(kThreadsBf16, 1) void attn_bf16_kernel(AttnParams p
   constexpr int LPT = (NCH + NT - 1) / NT;  // chunks per thread
   __shared__ __attribute__((aligned(16))) __bf16 Ks[4][KT * KP];
   __shared__ __attribute__((aligned(16))) __bf16 Vs[4][DH * VTP];
+  __shared__ __attribute__((aligned(16))) float Bs[BIAS ? 4 : 1][BIAS ? KT : 4];
   __shared__ int overflow;
 
   // work-item coordinates are workgroup-uniform; readfirstlane keeps them (and the
@@ -209,9 +221,17 @@ __global__ __launch_bounds__(kThreadsBf16, 1) void attn_bf16_kernel(AttnParams p
   const __amdgpu_buffer_rsrc_t vtsrs = __builtin_amdgcn_make_buffer_rsrc(
       (void*)(p.Vts + (int64_t)g * p.own_tiles * DH * 32), 0, (uint32_t)p.own_tiles * (DH * 64),
       0x00020000);
+  // logit bias of this KV head's entries (BIAS): entries past Nk read as 0
+  const __amdgpu_buffer_rsrc_t brs = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(p.bias + (int64_t)g * p.Nk), 0, (uint32_t)(p.Nk * 4), 0x00020000);
   constexpr int NSET = kLoadSets;
   u32x4 kreg[NSET][LPT], vreg[NSET][LPT];
+  float breg[NSET];
   auto load_tile_to = [&](int tile, int set) {
+    if constexpr (BIAS) {
+      if (tid < KT) breg[set] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                   brs, (k_begin + tile * KT + tid) * 4, 0, 0));
+    }
     if constexpr (OWN) {
       if (own_range && tile >= ct) {
         const int j0 = (tile - ct) * KT;  // first own entry of the tile
@@ -251,6 +271,9 @@ __global__ __launch_bounds__(kThreadsBf16, 1) void attn_bf16_kernel(AttnParams p
       const int row = c / CH, col = c % CH;
       *(u32x4*)(&Ks[buf][row * KP + col * 8]) = kreg[set][i];
       *(u32x4*)(&Vs[buf][(c / 4) * VTP + (c % 4) * 8]) = vreg[set][i];
+    }
+    if constexpr (BIAS) {
+      if (tid < KT) Bs[buf][tid] = breg[set] * p.bias_mul;
     }
   };
   auto load_tile = [&](int tile) { load_tile_to(tile, 0); };
@@ -320,11 +343,27 @@ __global__ __launch_bounds__(kThreadsBf16, 1) void attn_bf16_kernel(AttnParams p
         }
     }
   };
-  auto scores = [&](f32x16 (&s)[NKT][QT], int buf, int t) {
-    f32x16 zero[NKT];
+  // the accumulator's starting value: zero, or (BIAS) the tile's biases; element
+  // 4j + i of a lane's fragment is key 8j + 4 h32 + i of the 32-key tile
+  auto start = [&](int buf, f32x16 (&init)[NKT]) {
 #pragma unroll
-    for (int kt = 0; kt < NKT; ++kt) zero[kt] = f32x16{};
-    scores_init(s, buf, zero);
+    for (int kt = 0; kt < NKT; ++kt) {
+      if constexpr (BIAS) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const f32x4 b = *(const f32x4*)(&Bs[buf][kt * 32 + 8 * j + 4 * h32]);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) init[kt][4 * j + i] = b[i];
+        }
+      } else {
+        init[kt] = f32x16{};
+      }
+    }
+  };
+  auto scores = [&](f32x16 (&s)[NKT][QT], int buf, int t) {
+    f32x16 init[NKT];
+    start(buf, init);
+    scores_init(s, buf, init);
     mask(s, t);
   };
   // scaled row max of the tile (both halves of the 64-lane wave)
@@ -439,10 +478,9 @@ __global__ __launch_bounds__(kThreadsBf16, 1) void attn_bf16_kernel(AttnParams p
       if constexpr (MASKED) {
         scores(sn, (t + 1) & 3, t + 1);
       } else {
-        f32x16 zero[NKT];
-#pragma unroll
-        for (int kt = 0; kt < NKT; ++kt) zero[kt] = f32x16{};
-        scores_init(sn, (t + 1) & 3, zero);
+        f32x16 init[NKT];
+        start((t + 1) & 3, init);
+        scores_init(sn, (t + 1) & 3, init);
       }
       bf16x8 pb[NKT][QT][2];
       bf16x8 pl[NKT][QT][2];
@@ -540,8 +578,9 @@ __global__ __launch_bounds__(kThreadsBf16, 1) void attn_bf16_kernel(AttnParams p
   }
 }
 
-template <int DH, bool GATHER, bool PARTIAL, bool OWN>
+template <int DH, bool GATHER, bool PARTIAL, bool OWN, bool BIAS>
 __global__ __launch_bounds__(256) void attn_f32_kernel(AttnParams p) {
+  static_assert(!(OWN && BIAS), "own entries carry no bias");
   constexpr int KT = kKeyTileF32;
   constexpr int C4 = DH / 4;
   __shared__ f32x4 Ks[KT * C4];
@@ -572,8 +611,9 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnParams p) {
   }
   float mrun = -INFINITY, l = 0.f;
 
-  // one key: online-softmax update of (mrun, l, o) with row kk of the LDS tiles
-  auto attend_key = [&](int kk) {
+  // one key: online-softmax update of (mrun, l, o) with row kk of the LDS tiles and
+  // logit bias b
+  auto attend_key = [&](int kk, float b) {
     f32x4 acc = {};
 #pragma unroll
     for (int i = 0; i < C4; ++i) {
@@ -583,7 +623,7 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnParams p) {
       acc[2] = fmaf(q[i][2], kv[2], acc[2]);
       acc[3] = fmaf(q[i][3], kv[3], acc[3]);
     }
-    const float sc = ((acc[0] + acc[1]) + (acc[2] + acc[3])) * p.c;
+    const float sc = fmaf((acc[0] + acc[1]) + (acc[2] + acc[3]), p.c, b);
     if (sc > mrun) {
       const float a = expf(mrun - sc);
       l *= a;
@@ -613,7 +653,7 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnParams p) {
       Vs[c] = *((const f32x4*)(Vb + (int64_t)src * DH) + col);
     }
     __syncthreads();
-    for (int kk = 0; kk < nk; ++kk) attend_key(kk);
+    for (int kk = 0; kk < nk; ++kk) attend_key(kk, BIAS ? p.bias[(int64_t)g * p.Nk + tb + kk] : 0.f);
     __syncthreads();
   }
   if (OWN && split == p.n_split - 1) {
@@ -630,7 +670,7 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnParams p) {
       }
       __syncthreads();
       const int nk = min(KT, m - tb + 1);  // own entries tb .. m of this query
-      for (int kk = 0; kk < nk; ++kk) attend_key(kk);
+      for (int kk = 0; kk < nk; ++kk) attend_key(kk, 0.f);
       __syncthreads();
     }
   }
@@ -681,19 +721,65 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restri
   *((f32x4*)(O + ((int64_t)m * Hq + g * G + j) * DH) + c4) = acc * (1.0f / l);
 }
 
+// Block-scaled integer cache -> rows [Hkv][n_cache][dh] of OUT (bf16 or f32). Entry n
+// is source row idx[n] (or n); rows outside [0, n_src) read as zeros. Exact: an int8
+// or int4 value times a power of two is a bf16 number. One thread per 8 channels.
+template <class OUT, int BITS>
+__global__ __launch_bounds__(256) void mx_dequant_kernel(const uint8_t* __restrict__ q,
+                                                         const int8_t* __restrict__ e,
+                                                         const int32_t* __restrict__ idx,
+                                                         int64_t n_src, int n_cache, int dh,
+                                                         OUT* __restrict__ out) {
+  const int g = blockIdx.y;
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int per_row = dh / 8;
+  if (t >= (int64_t)n_cache * per_row) return;
+  const int n = (int)(t / per_row), c0 = (int)(t % per_row) * 8;
+  const int64_t src = idx ? (int64_t)idx[n] : (int64_t)n;
+  float v[8] = {};
+  if (src >= 0 && src < n_src) {
+    const int64_t row = (int64_t)g * n_src + src;
+    const int ex = e[row * (dh / 32) + c0 / 32];
+    if constexpr (BITS == 8) {
+      const uint2 w = *(const uint2*)(q + row * dh + c0);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const uint32_t word = i < 4 ? w.x : w.y;
+        v[i] = ldexpf((float)(int8_t)(word >> (8 * (i & 3))), ex);
+      }
+    } else {
+      const uint32_t w = *(const uint32_t*)(q + row * (dh / 2) + c0 / 2);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int nib = (int)((w >> (4 * i)) & 0xF);
+        v[i] = ldexpf((float)(nib >= 8 ? nib - 16 : nib), ex);
+      }
+    }
+  }
+  OUT* o = out + ((int64_t)g * n_cache + n) * dh + c0;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) o[i] = (OUT)v[i];
+}
+
 template <int DH>
 hipError_t launch_dh(const AttnShape& s, const AttnPlan& pl, AttnParams& p, bool gather,
                      bool psplit, hipStream_t st) {
   const bool part = pl.n_split > 1;
   const bool own = s.Ms > 0;
+  const bool bias = p.bias != nullptr;
   dim3 grid(pl.grid), block(256);
   if (s.bf16) {
     const dim3 bblock(kThreadsBf16);
     // fast path, then the lazy-rescale fixup for any work item it handed back
-#define PKV_L(G_, P_, S_, O_)                                                                 \
-  do {                                                                                        \
-    hipLaunchKernelGGL((attn_bf16_kernel<DH, G_, P_, S_, false, O_>), grid, bblock, 0, st, p); \
-    hipLaunchKernelGGL((attn_bf16_kernel<DH, G_, P_, S_, true, O_>), grid, bblock, 0, st, p);  \
+#define PKV_LB(G_, P_, S_, O_, B_)                                                                \
+  do {                                                                                            \
+    hipLaunchKernelGGL((attn_bf16_kernel<DH, G_, P_, S_, false, O_, B_>), grid, bblock, 0, st, p); \
+    hipLaunchKernelGGL((attn_bf16_kernel<DH, G_, P_, S_, true, O_, B_>), grid, bblock, 0, st, p);  \
+  } while (0)
+#define PKV_L(G_, P_, S_, O_)                      \
+  do {                                             \
+    if (bias) PKV_LB(G_, P_, S_, false, true);     \
+    else PKV_LB(G_, P_, S_, O_, false);            \
   } while (0)
     if (own) {
       if (gather) {
@@ -711,8 +797,13 @@ hipError_t launch_dh(const AttnShape& s, const AttnPlan& pl, AttnParams& p, bool
       else { if (part) PKV_L(false, false, true, false); else PKV_L(false, false, false, false); }
     }
 #undef PKV_L
+#undef PKV_LB
   } else {
-#define PKV_L(G_, S_, O_) hipLaunchKernelGGL((attn_f32_kernel<DH, G_, S_, O_>), grid, block, 0, st, p)
+#define PKV_L(G_, S_, O_)                                                                         \
+  do {                                                                                            \
+    if (bias) hipLaunchKernelGGL((attn_f32_kernel<DH, G_, S_, false, true>), grid, block, 0, st, p); \
+    else hipLaunchKernelGGL((attn_f32_kernel<DH, G_, S_, O_, false>), grid, block, 0, st, p);       \
+  } while (0)
     if (own) {
       if (gather) { if (part) PKV_L(true, true, true); else PKV_L(true, false, true); }
       else { if (part) PKV_L(false, true, true); else PKV_L(false, false, true); }
@@ -782,9 +873,11 @@ AttnPlan plan_attention(const AttnShape& s) {
 hipError_t launch_attention(const AttnShape& s, const void* Q, const void* K, const void* V,
                             const int32_t* idx, int64_t src_rows, int64_t src_valid,
                             float scale, bool psplit, float* O, void* ws, hipStream_t st,
-                            const void* Ks, const void* Vs) {
+                            const void* Ks, const void* Vs, const float* bias) {
   const AttnPlan pl = plan_attention(s);
   AttnParams p{};
+  p.bias = bias;
+  p.bias_mul = s.bf16 ? 1.0f / scale : 1.0f;
   p.Q = Q;
   p.K = K;
   p.V = V;
@@ -848,6 +941,34 @@ hipError_t launch_attention(const AttnShape& s, const void* Q, const void* K, co
   p.c = s.bf16 ? scale * 1.4426950408889634f : scale;
   if (s.dh == 128) return launch_dh<128>(s, pl, p, idx != nullptr, psplit, st);
   return launch_dh<64>(s, pl, p, idx != nullptr, psplit, st);
+}
+
+}  // namespace pkv
+
+namespace pkv {
+
+hipError_t launch_mx_dequant(bool bf16, int bits, const void* q, const int8_t* e,
+                             const int32_t* idx, int64_t n_src, int64_t n_cache, int Hkv, int dh,
+                             void* out, hipStream_t st) {
+  const int64_t n = n_cache * (dh / 8);
+  const dim3 grid((unsigned)((n + 255) / 256), (unsigned)Hkv), block(256);
+  const uint8_t* qb = (const uint8_t*)q;
+  if (bf16) {
+    if (bits == 8)
+      hipLaunchKernelGGL((mx_dequant_kernel<__bf16, 8>), grid, block, 0, st, qb, e, idx, n_src,
+                         (int)n_cache, dh, (__bf16*)out);
+    else
+      hipLaunchKernelGGL((mx_dequant_kernel<__bf16, 4>), grid, block, 0, st, qb, e, idx, n_src,
+                         (int)n_cache, dh, (__bf16*)out);
+  } else {
+    if (bits == 8)
+      hipLaunchKernelGGL((mx_dequant_kernel<float, 8>), grid, block, 0, st, qb, e, idx, n_src,
+                         (int)n_cache, dh, (float*)out);
+    else
+      hipLaunchKernelGGL((mx_dequant_kernel<float, 4>), grid, block, 0, st, qb, e, idx, n_src,
+                         (int)n_cache, dh, (float*)out);
+  }
+  return hipGetLastError();
 }
 
 }  // namespace pkv

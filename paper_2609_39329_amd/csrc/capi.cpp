@@ -183,6 +183,65 @@ int patchkv_attend_chunk(int dtype, const void* Q, const void* K, const void* V,
                                     workspace, (hipStream_t)stream, Ks, Vs));
 }
 
+namespace {
+bool valid_kv_format(int f) {
+  return f == PATCHKV_KV_PLAIN || f == PATCHKV_KV_MXINT8 || f == PATCHKV_KV_MXINT4;
+}
+// dequantized cache rows (quantized formats), carved after the attention workspace
+size_t dequant_bytes(int dtype, int kv_format, int64_t n_cache, int Hkv, int dh) {
+  if (kv_format == PATCHKV_KV_PLAIN) return 0;
+  const size_t e = dtype == PATCHKV_BF16 ? 2 : 4;
+  return 2 * ((size_t)Hkv * n_cache * dh * e + 255) / 256 * 256;
+}
+}  // namespace
+
+size_t patchkv_attend_cache_workspace_bytes(int dtype, int kv_format, int64_t M, int64_t n_cache,
+                                            int Hq, int Hkv, int dh) {
+  if (!valid_kv_format(kv_format)) return 0;
+  if (check_attn_shape(dtype, M, n_cache, Hq, Hkv, dh) != PATCHKV_OK) return 0;
+  const size_t a = (plan_attention(attn_shape(dtype, M, n_cache, Hq, Hkv, dh)).ws_bytes + 255) / 256 * 256;
+  return a + dequant_bytes(dtype, kv_format, n_cache, Hkv, dh);
+}
+
+int patchkv_attend_cache(int dtype, const void* Q, const void* K, const void* V, int kv_format,
+                         const int8_t* Ke, const int8_t* Ve, const int32_t* idx, int64_t n_src,
+                         int64_t n_cache, const float* bias, int64_t M, int Hq, int Hkv, int dh,
+                         float scale, int p_terms, float* O, void* workspace,
+                         size_t workspace_bytes, void* stream) {
+  if (!Q || !K || !V || !O) return PATCHKV_E_NULL;
+  if (!valid_kv_format(kv_format)) return PATCHKV_E_VALUE;
+  const bool quant = kv_format != PATCHKV_KV_PLAIN;
+  if (quant && (!Ke || !Ve)) return PATCHKV_E_NULL;
+  int s = check_attn_shape(dtype, M, n_cache, Hq, Hkv, dh);
+  if (s) return s;
+  if (!src_rows_ok(dtype, n_src, dh)) return PATCHKV_E_SHAPE;
+  if (!idx && n_cache > n_src) return PATCHKV_E_SHAPE;
+  if (p_terms != 1 && p_terms != 2) return PATCHKV_E_VALUE;
+  if (!finite_pos(scale)) return PATCHKV_E_VALUE;
+  if (!al16(Q) || !al16(K) || !al16(V) || !al16(O) || (bias && !al16(bias)))
+    return PATCHKV_E_VALUE;
+  const AttnShape sh = attn_shape(dtype, M, n_cache, Hq, Hkv, dh);
+  const size_t a = (plan_attention(sh).ws_bytes + 255) / 256 * 256;
+  s = check_ws(workspace, workspace_bytes, a + dequant_bytes(dtype, kv_format, n_cache, Hkv, dh));
+  if (s) return s;
+  if (!quant)
+    return status_of(launch_attention(sh, Q, K, V, idx, n_src, n_src, scale, p_terms == 2, O,
+                                      workspace, (hipStream_t)stream, nullptr, nullptr, bias));
+  // expand the quantized entries (gathered through idx) into dtype rows, then attend
+  const int bits = kv_format == PATCHKV_KV_MXINT8 ? 8 : 4;
+  const size_t half = dequant_bytes(dtype, kv_format, n_cache, Hkv, dh) / 2;
+  char* kx = (char*)workspace + a;
+  char* vx = kx + half;
+  const hipStream_t st = (hipStream_t)stream;
+  hipError_t e = launch_mx_dequant(dtype == PATCHKV_BF16, bits, K, Ke, idx, n_src, n_cache, Hkv,
+                                   dh, kx, st);
+  if (e == hipSuccess)
+    e = launch_mx_dequant(dtype == PATCHKV_BF16, bits, V, Ve, idx, n_src, n_cache, Hkv, dh, vx, st);
+  if (e != hipSuccess) return PATCHKV_E_HIP;
+  return status_of(launch_attention(sh, Q, kx, vx, nullptr, n_cache, n_cache, scale, p_terms == 2,
+                                    O, workspace, st, nullptr, nullptr, bias));
+}
+
 size_t patchkv_targets_workspace_bytes(int w_dtype, int64_t M, int64_t d_in, int64_t d_out) {
   if (w_dtype != PATCHKV_BF16 && w_dtype != PATCHKV_F32) return 0;
   if (check_stats_dims(M, d_in, d_out)) return 0;

@@ -35,7 +35,15 @@ AttnPlan plan_attention(const AttnShape& s);
 hipError_t launch_attention(const AttnShape& s, const void* Q, const void* K, const void* V,
                             const int32_t* idx, int64_t src_rows, int64_t src_valid,
                             float scale, bool psplit, float* O, void* ws, hipStream_t st,
-                            const void* Ks = nullptr, const void* Vs = nullptr);
+                            const void* Ks = nullptr, const void* Vs = nullptr,
+                            const float* bias = nullptr);
+// bias [Hkv][Nk]: per-entry logit bias (natural-log units), added to entry n's logit.
+// Block-scaled integer cache rows -> [Hkv][n_cache][dh] bf16 (bf16) or f32: value
+// q * 2^e, q int8 (bits 8) or int4 packed two per byte (bits 4, even channel in the
+// low nibble), e int8 per 32 channels; entry n is row idx[n] (or n) of n_src rows.
+hipError_t launch_mx_dequant(bool bf16, int bits, const void* q, const int8_t* e,
+                             const int32_t* idx, int64_t n_src, int64_t n_cache, int Hkv, int dh,
+                             void* out, hipStream_t st);
 
 // ---------------------------------------------------------------- statistics (fp32 acc)
 size_t targets_ws_bytes(int64_t M, int64_t din, int64_t dout);

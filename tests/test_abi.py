@@ -182,3 +182,23 @@ def test_mlp_validation(L):
     assert p(B.BF16, FAKE, FAKE, None, FAKE, 4, 128, 64, FAKE, None, 0, None) == B.E_NULL
     assert p(B.F64, FAKE, FAKE, FAKE, FAKE, 4, 128, 64, FAKE, None, 0, None) == B.E_DTYPE
     assert p(B.BF16, FAKE, FAKE, FAKE, FAKE, 4, 128, 64, FAKE, None, 0, None) == B.E_WORKSPACE
+
+
+def test_attend_cache_validation(L):
+    def cache(dt=B.BF16, Q=FAKE, K=FAKE, V=FAKE, fmt=0, Ke=None, Ve=None, idx=None, n_src=64,
+              n_cache=64, bias=None, M=8, Hq=4, Hkv=2, dh=128, scale=0.1, p_terms=2, O=FAKE,
+              ws=None, wsb=0):
+        return L.patchkv_attend_cache(dt, Q, K, V, fmt, Ke, Ve, idx, n_src, n_cache, bias, M, Hq,
+                                      Hkv, dh, scale, p_terms, O, ws, wsb, None)
+    assert cache(K=None) == B.E_NULL
+    assert cache(fmt=3) == B.E_VALUE
+    assert cache(fmt=B.KV_MXINT8) == B.E_NULL              # exponents missing
+    assert cache(fmt=B.KV_MXINT4, Ke=FAKE) == B.E_NULL
+    assert cache(n_cache=65) == B.E_SHAPE
+    assert cache(bias=FAKE + 4) == B.E_VALUE              # misaligned
+    assert cache(p_terms=0) == B.E_VALUE
+    assert cache() == B.E_WORKSPACE
+    plain = L.patchkv_attend_cache_workspace_bytes(B.BF16, B.KV_PLAIN, 8, 64, 4, 2, 128)
+    q8 = L.patchkv_attend_cache_workspace_bytes(B.BF16, B.KV_MXINT8, 8, 64, 4, 2, 128)
+    assert q8 - plain >= 2 * 2 * 64 * 128 * 2             # expanded K and V rows
+    assert L.patchkv_attend_cache_workspace_bytes(B.BF16, 7, 8, 64, 4, 2, 128) == 0
