@@ -68,7 +68,7 @@ __all__ = [
     "normal_equations", "normal_equations_chunked", "ridge_lambda", "solve_patch",
     "layer_patch", "attention_rows", "attention_chunk", "layer_patch_chunked", "rms_norm",
     "silu", "mlp_features", "block_targets", "propagate_student", "mlp_layer_patch",
-    "dequantize_mx",
+    "dequantize_mx", "low_rank_patch",
 ]
 
 
@@ -355,3 +355,19 @@ def mlp_layer_patch(inp, mlp, mode: str = "absolute", lam: float | None = None) 
     dW = solve_patch(G0, C, lam_used)
     return {"dW": dW, "lam": lam_used, "G": G0, "C": C,
             "Y_student": propagate_student(Hc, Wd, dW, Oc), "Y_teacher": Hf @ Wd + Of}
+
+
+def low_rank_patch(G0: np.ndarray, dW: np.ndarray, r: int) -> dict:
+    """The reduced-rank patch (App., low-rank weight patches; reduced-rank regression).
+
+    In the paper's column form the ridge patch is projected onto its top-r output
+    subspace, U_r U_r^T dW, with U_r the top-r eigenvectors of dW S_H dW^T. In row
+    form (dW [d_in, d_out], G0 = S_H) that is dW_r = dW U_r U_r^T with U_r [d_out, r]
+    the top-r eigenvectors of dW^T G0 dW, the covariance of the fitted targets.
+    Returns dW_r, the factors A = dW U_r [d_in, r] and U_r, and all eigenvalues in
+    descending order (LAPACK eigh).
+    """
+    S = dW.T @ G0 @ dW
+    w, V = np.linalg.eigh(S)
+    U = V[:, ::-1][:, :r]
+    return {"dW": dW @ U @ U.T, "A": dW @ U, "U": U, "eig": w[::-1].copy()}

@@ -751,3 +751,75 @@ def test_dequantize_mx_library_and_exactness():
         qq, ee = quantize_mx(x, bits)
         step = np.exp2(np.repeat(ee.astype(np.float64), 32, axis=-1))
         assert np.all(np.abs(oracle.dequantize_mx(qq, ee) - x) <= 0.5 * step + 1e-12)
+
+
+# ----------------------------------------------------------- low-rank patch (f4)
+
+def _rrr_case(rng, rows=60, din=24, dout=16, planted=None):
+    X = rng.standard_normal((rows, din))
+    if planted is None:
+        dW = rng.standard_normal((din, dout))
+    else:  # a strong rank-`planted` part plus noise: a clear gap after eigenvalue `planted`
+        dW = rng.standard_normal((din, planted)) @ rng.standard_normal((planted, dout)) * 3
+        dW += 0.01 * rng.standard_normal((din, dout))
+    return X, X.T @ X, dW
+
+
+def check_low_rank(fn):
+    """The reduced-rank fit loses exactly the discarded eigenvalues: with Yhat = X dW,
+    ||X (dW - dW_r)||_F^2 = sum of the eigenvalues of Yhat^T Yhat past r, the optimum
+    over all rank-r output projections (Eckart-Young on the fitted targets)."""
+    rng = np.random.default_rng(61)
+    X, G, dW = _rrr_case(rng)
+    r = 5
+    out = fn(G, dW, r)
+    s = np.linalg.svd(X @ dW, compute_uv=False)
+    lost = np.linalg.norm(X @ (dW - out["dW"])) ** 2
+    return abs(lost - np.sum(s[r:] ** 2)) / np.sum(s ** 2)
+
+
+def test_low_rank_patch_optimal_loss_and_rank():
+    assert check_low_rank(oracle.low_rank_patch) < 1e-12
+    rng = np.random.default_rng(62)
+    X, G, dW = _rrr_case(rng)
+    out = oracle.low_rank_patch(G, dW, 5)
+    assert np.linalg.matrix_rank(out["dW"], tol=1e-9 * np.linalg.norm(dW)) == 5
+    assert rel(out["A"] @ out["U"].T, out["dW"]) < 1e-14
+    assert np.max(np.abs(out["U"].T @ out["U"] - np.eye(5))) < 1e-13
+    # full rank keeps the patch
+    assert rel(oracle.low_rank_patch(G, dW, 16)["dW"], dW) < 1e-13
+    # no other rank-5 output projection fits better
+    best = np.linalg.norm(X @ (dW - out["dW"])) ** 2
+    for _ in range(20):
+        P, _ = np.linalg.qr(rng.standard_normal((16, 5)))
+        assert np.linalg.norm(X @ (dW - dW @ P @ P.T)) ** 2 >= best * (1 - 1e-12)
+
+
+def test_low_rank_patch_matches_svd_of_fitted_targets():
+    """With a clear gap, the projector is the one of the top right singular vectors
+    of the fitted targets X dW (numpy SVD, a different route)."""
+    rng = np.random.default_rng(63)
+    X, G, dW = _rrr_case(rng, planted=4)
+    out = oracle.low_rank_patch(G, dW, 4)
+    _, _, Vt = np.linalg.svd(X @ dW)
+    P = Vt[:4].T @ Vt[:4]
+    assert rel(out["dW"], dW @ P) < 1e-10
+
+
+def test_low_rank_pins_catch_planted_mistakes():
+    def bottom(G, dW, r):                       # smallest eigenvalues kept
+        w, V = np.linalg.eigh(dW.T @ G @ dW)
+        U = V[:, :r]
+        return {"dW": dW @ U @ U.T}
+
+    def no_gram(G, dW, r):                      # S_H dropped: eigenvectors of dW^T dW
+        w, V = np.linalg.eigh(dW.T @ dW)
+        U = V[:, ::-1][:, :r]
+        return {"dW": dW @ U @ U.T}
+
+    def truncated_svd(G, dW, r):                # best rank-r approximation of dW itself
+        U, s, Vt = np.linalg.svd(dW, full_matrices=False)
+        return {"dW": (U[:, :r] * s[:r]) @ Vt[:r]}
+
+    for f in (bottom, no_gram, truncated_svd):
+        assert check_low_rank(f) > 1e-4
