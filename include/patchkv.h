@@ -285,6 +285,25 @@ int patchkv_solve_patch(int acc_dtype, const void* G, const void* C, int64_t d_i
                         void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------- */
+/* Reduced-rank patch (App., low-rank weight patches; reduced-rank regression): */
+/* the ridge patch projected onto its top-r output subspace. In row form,       */
+/*   dW_r = dW U_r U_r^T,  U_r [d_out][r] = top-r eigenvectors of dW^T G dW,    */
+/* stored as the factors A = dW U_r [d_in][r] and U_r, (d_in + d_out) r floats. */
+/* G [d_in][d_in] float (the statistic without the ridge), dW [d_in][d_out]      */
+/* float. Outputs: A, U written; dW_r [d_in][d_out] written when non-NULL.       */
+/* Method: subspace iteration with a block of b = min(64, d_out) (rounded down  */
+/* to even) columns for `iters` steps, then Rayleigh-Ritz (fp64 Jacobi on the   */
+/* b x b projection). Where eigenvalue r and r+1 of dW^T G dW nearly coincide,  */
+/* the subspace is ill-determined and only its captured energy is.             */
+/* Limits: 1 <= r <= b, 1 <= iters <= 1000, d_in, d_out <= 65536, d_out >= 2.   */
+/* ------------------------------------------------------------------------- */
+size_t patchkv_low_rank_workspace_bytes(int64_t d_in, int64_t d_out, int r);
+
+int patchkv_low_rank_patch(const float* G, const float* dW, int64_t d_in, int64_t d_out, int r,
+                           int iters, float* A, float* U, float* dW_r, void* workspace,
+                           size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------- */
 /* One block's patch (Alg. 1, one block and one reference chunk):               */
 /*   O_f = attend_full(Q, K, V); O_c = attend over the compressed cache;        */
 /*   T = (O_f - O_c) W + rho (O_f - O_c); G = O_c^T O_c, C = O_c^T T;           */

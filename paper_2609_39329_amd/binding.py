@@ -65,6 +65,9 @@ SIGNATURES = {
     "patchkv_solve_workspace_bytes": (_c_sz, [_c_int, _c_i64, _c_i64]),
     "patchkv_solve_patch": (_c_int, [_c_int, _c_vp, _c_vp, _c_i64, _c_i64, ctypes.c_double, _c_int,
                                      _c_vp, _c_vp, _c_vp, _c_sz, _c_vp]),
+    "patchkv_low_rank_workspace_bytes": (_c_sz, [_c_i64, _c_i64, _c_int]),
+    "patchkv_low_rank_patch": (_c_int, [_c_vp, _c_vp, _c_i64, _c_i64, _c_int, _c_int, _c_vp, _c_vp,
+                                        _c_vp, _c_vp, _c_sz, _c_vp]),
     "patchkv_layer_workspace_bytes": (_c_sz, [_c_int, _c_int, _c_i64, _c_i64, _c_i64, _c_int,
                                               _c_int, _c_int]),
     "patchkv_compute_layer_patch": (_c_int, [_c_int, _c_int, _c_vp, _c_vp, _c_vp, _c_vp, _c_vp,
@@ -375,6 +378,29 @@ def solve_patch(G, C, lam: float, mode: int = RIDGE_ABSOLUTE, dW=None, info=None
 def layer_workspace_bytes(dtype: int, acc: int, M: int, N: int, B: int, Hq: int, Hkv: int,
                           dh: int) -> int:
     return lib().patchkv_layer_workspace_bytes(dtype, acc, M, N, B, Hq, Hkv, dh)
+
+
+def low_rank_patch(G, dW, r: int = 32, iters: int = 40, A=None, U=None, dWr=None,
+                   want_full: bool = True, stream=None):
+    """Reduced-rank patch: (A [d_in, r], U [d_out, r], dW_r = A U^T or None) for the
+    projection of dW onto the top-r eigenvectors of dW^T G dW (G, dW float32)."""
+    torch = _torch()
+    _require_gpu(G, dW, A, U, dWr)
+    din, dout = dW.shape
+    dev = dW.device
+    if A is None:
+        A = torch.empty((din, r), dtype=torch.float32, device=dev)
+    if U is None:
+        U = torch.empty((dout, r), dtype=torch.float32, device=dev)
+    if dWr is None and want_full:
+        dWr = torch.empty((din, dout), dtype=torch.float32, device=dev)
+    L = lib()
+    nb = L.patchkv_low_rank_workspace_bytes(din, dout, r)
+    ws = _workspace(nb, dev, stream)
+    _check("patchkv_low_rank_patch",
+           L.patchkv_low_rank_patch(_ptr(G), _ptr(dW), din, dout, r, iters, _ptr(A), _ptr(U),
+                                    _ptr(dWr), _ptr(ws), nb, _stream(stream)))
+    return A, U, dWr
 
 
 def compute_layer_patch(Q, K, V, W, idx=None, Kc=None, Vc=None, lam: float = 0.1,

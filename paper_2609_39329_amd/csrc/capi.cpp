@@ -378,6 +378,34 @@ int patchkv_solve_patch(int acc_dtype, const void* G, const void* C, int64_t d_i
                                 (hipStream_t)stream));
 }
 
+namespace {
+int check_low_rank(int64_t din, int64_t dout, int r, int iters) {
+  if (din < 1 || dout < 2 || din > kMaxDim || dout > kMaxDim) return PATCHKV_E_SHAPE;
+  const int b = (int)std::min<int64_t>(64, dout) & ~1;
+  if (r < 1 || r > b || iters < 1 || iters > 1000) return PATCHKV_E_VALUE;
+  return PATCHKV_OK;
+}
+}  // namespace
+
+size_t patchkv_low_rank_workspace_bytes(int64_t d_in, int64_t d_out, int r) {
+  if (check_low_rank(d_in, d_out, r, 1)) return 0;
+  return low_rank_ws_bytes(d_in, d_out);
+}
+
+int patchkv_low_rank_patch(const float* G, const float* dW, int64_t d_in, int64_t d_out, int r,
+                           int iters, float* A, float* U, float* dW_r, void* workspace,
+                           size_t workspace_bytes, void* stream) {
+  if (!G || !dW || !A || !U) return PATCHKV_E_NULL;
+  int s = check_low_rank(d_in, d_out, r, iters);
+  if (s) return s;
+  if (!al16(G) || !al16(dW) || !al16(A) || !al16(U) || (dW_r && !al16(dW_r)))
+    return PATCHKV_E_VALUE;
+  s = check_ws(workspace, workspace_bytes, low_rank_ws_bytes(d_in, d_out));
+  if (s) return s;
+  return status_of(launch_low_rank(G, dW, d_in, d_out, r, iters, A, U, dW_r, workspace,
+                                   (hipStream_t)stream));
+}
+
 size_t patchkv_layer_workspace_bytes(int dtype, int acc_dtype, int64_t M, int64_t N, int64_t B,
                                      int Hq, int Hkv, int dh) {
   if (acc_dtype != PATCHKV_F32 && acc_dtype != PATCHKV_F64) return 0;

@@ -78,6 +78,12 @@ hipError_t launch_normal_eq_f64(const float* X, const float* Yf, const float* Yc
                                 double* G, double* C, hipStream_t st);
 
 // ---------------------------------------------------------------- ridge solve
+// Reduced-rank patch: A [din][r], U [dout][r] with dW_r = A U^T the projection of dW
+// onto the top-r eigenvectors of dW^T G dW; dWr [din][dout] written when non-null.
+// r <= min(dout, 64) rounded down to even; iters subspace iterations.
+size_t low_rank_ws_bytes(int64_t din, int64_t dout);
+hipError_t launch_low_rank(const float* G, const float* dW, int64_t din, int64_t dout, int r,
+                           int iters, float* A, float* U, float* dWr, void* ws, hipStream_t st);
 size_t solve_ws_bytes(bool f64, int64_t din, int64_t dout);
 // exact_f32: fp32 block products on fp32 MFMA (else three bf16 MFMA terms); the
 // fp64 solve always uses fp64 arithmetic.

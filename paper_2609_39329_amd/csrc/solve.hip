@@ -1173,7 +1173,250 @@ hipError_t solve_t(const T* G, const T* C, int64_t d64, int64_t dout64, double l
   return hipSuccess;
 }
 
+// ---------------------------------------------------------------- reduced-rank patch
+//
+// dW_r = dW U_r U_r^T with U_r the top-r eigenvectors of S = dW^T G dW (d_out x d_out),
+// found by subspace iteration on MFMA GEMMs: Q <- orth(S' Q) with a block of
+// kRrrBlock >= r columns, S' = S + mu I with mu = 1e-5 trace(S) >= 1e-5 lambda_max
+// (the same eigenvectors; S' Q keeps full column rank, to fp32 accuracy, when S has
+// a low numerical rank). orth is Cholesky QR with the Gram matrix Z^T Z formed and
+// factored in fp64 (its condition number is that of Z squared, up to 1e10), then
+// Q = Z L^-T on fp32 MFMA; two more passes at the end make Q orthonormal to
+// rounding. Rayleigh-Ritz: the kRrrBlock x kRrrBlock matrix Q^T S' Q is
+// diagonalised by parallel Jacobi in fp64 in one workgroup and its top-r
+// eigenvectors map back through Q.
+
+constexpr int kRrrBlock = 64;   // subspace width (r <= it)
+constexpr int kJacobiSweeps = 14;
+
+// M[i][i] += rel * trace(M) / n (one workgroup; the trace in fp64, fixed order)
+__global__ __launch_bounds__(256) void diag_shift_kernel(float* M, int64_t n, int64_t ld, float rel) {
+  __shared__ double part[256];
+  double t = 0.0;
+  for (int64_t i = threadIdx.x; i < n; i += 256) t += (double)M[i * ld + i];
+  part[threadIdx.x] = t;
+  __syncthreads();
+  for (int s2 = 128; s2 > 0; s2 >>= 1) {
+    if ((int)threadIdx.x < s2) part[threadIdx.x] += part[threadIdx.x + s2];
+    __syncthreads();
+  }
+  const float mu = (float)(rel * part[0] / (double)n);
+  for (int64_t i = threadIdx.x; i < n; i += 256) M[i * ld + i] += mu;
+}
+
+// W[i][j] = sum_k Z[k][i] Z[k][j] in fp64 (Z [rows][b] fp32, b <= kRrrBlock): one
+// workgroup per 16 x 16 tile of W, rows streamed through LDS in chunks of 64.
+__global__ __launch_bounds__(256) void gram64_kernel(const float* __restrict__ Z, int64_t rows, int b,
+                                                     double* __restrict__ W) {
+  __shared__ float zi[64][17], zj[64][17];
+  const int i0 = blockIdx.y * 16, j0 = blockIdx.x * 16, tid = threadIdx.x;
+  const int ti = tid / 16, tj = tid % 16;
+  double acc = 0.0;
+  for (int64_t k0 = 0; k0 < rows; k0 += 64) {
+    for (int e = tid; e < 64 * 16; e += 256) {
+      const int kk = e / 16, c = e % 16;
+      const int64_t k = k0 + kk;
+      zi[kk][c] = (k < rows && i0 + c < b) ? Z[k * b + i0 + c] : 0.f;
+      zj[kk][c] = (k < rows && j0 + c < b) ? Z[k * b + j0 + c] : 0.f;
+    }
+    __syncthreads();
+#pragma unroll 8
+    for (int kk = 0; kk < 64; ++kk) acc = fma((double)zi[kk][ti], (double)zj[kk][tj], acc);
+    __syncthreads();
+  }
+  if (i0 + ti < b && j0 + tj < b) W[(int64_t)(i0 + ti) * b + j0 + tj] = acc;
+}
+
+// Q[i][j] = a counter-based pseudo-random value in [-1, 1) of (i, j)
+__global__ __launch_bounds__(256) void rrr_init_kernel(float* Q, int64_t rows, int b, int* info) {
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (e == 0) *info = 0;
+  if (e >= rows * b) return;
+  uint32_t h = (uint32_t)e * 0x9E3779B9u + 0x7F4A7C15u;
+  h ^= h >> 16;
+  h *= 0x85EBCA6Bu;
+  h ^= h >> 13;
+  h *= 0xC2B2AE35u;
+  h ^= h >> 16;
+  Q[e] = (float)(h >> 8) * (2.0f / 16777216.0f) - 1.0f;
+}
+
+// Eigenvectors of the symmetric b x b matrix (T + T^T) / 2 (b even, <= kRrrBlock) by
+// parallel cyclic Jacobi in fp64: each step rotates b/2 disjoint index pairs of a
+// round-robin schedule, columns then rows. Vr [b][r] receives the eigenvectors of the
+// r largest eigenvalues, in descending order (ties: lower index first); w [b] all
+// eigenvalues by index.
+__global__ __launch_bounds__(256) void jacobi_top_kernel(const float* __restrict__ T, int b, int r,
+                                                         float* __restrict__ Vr,
+                                                         double* __restrict__ w) {
+  constexpr int NB = kRrrBlock, P = NB + 1;
+  __shared__ double A[NB * P], V[NB * P];
+  __shared__ double cs[NB / 2][2];
+  __shared__ int pq[NB / 2][2];
+  const int tid = threadIdx.x;
+  for (int e = tid; e < b * b; e += 256) {
+    const int i = e / b, j = e % b;
+    A[i * P + j] = 0.5 * ((double)T[i * b + j] + (double)T[j * b + i]);
+    V[i * P + j] = i == j ? 1.0 : 0.0;
+  }
+  __syncthreads();
+  const int half = b / 2;
+  for (int sweep = 0; sweep < kJacobiSweeps; ++sweep) {
+    for (int step = 0; step < b - 1; ++step) {
+      if (tid < half) {
+        // round robin: position 0 fixed, the others rotate by `step`
+        auto at = [&](int k) { return k == 0 ? 0 : (k - 1 + step) % (b - 1) + 1; };
+        int p = at(tid), q = at(b - 1 - tid);
+        if (p > q) { const int t = p; p = q; q = t; }
+        const double apq = A[p * P + q];
+        double c = 1.0, s = 0.0;
+        if (fabs(apq) > 1e-300) {
+          const double th = (A[q * P + q] - A[p * P + p]) / (2.0 * apq);
+          const double t = (th >= 0.0 ? 1.0 : -1.0) / (fabs(th) + sqrt(th * th + 1.0));
+          c = 1.0 / sqrt(t * t + 1.0);
+          s = t * c;
+        }
+        pq[tid][0] = p;
+        pq[tid][1] = q;
+        cs[tid][0] = c;
+        cs[tid][1] = s;
+      }
+      __syncthreads();
+      // columns: A <- A J, V <- V J
+      for (int e = tid; e < b * half; e += 256) {
+        const int k = e / half, t = e % half;
+        const int p = pq[t][0], q = pq[t][1];
+        const double c = cs[t][0], s = cs[t][1];
+        const double akp = A[k * P + p], akq = A[k * P + q];
+        A[k * P + p] = c * akp - s * akq;
+        A[k * P + q] = s * akp + c * akq;
+        const double vkp = V[k * P + p], vkq = V[k * P + q];
+        V[k * P + p] = c * vkp - s * vkq;
+        V[k * P + q] = s * vkp + c * vkq;
+      }
+      __syncthreads();
+      // rows: A <- J^T A
+      for (int e = tid; e < b * half; e += 256) {
+        const int k = e / half, t = e % half;
+        const int p = pq[t][0], q = pq[t][1];
+        const double c = cs[t][0], s = cs[t][1];
+        const double apk = A[p * P + k], aqk = A[q * P + k];
+        A[p * P + k] = c * apk - s * aqk;
+        A[q * P + k] = s * apk + c * aqk;
+      }
+      __syncthreads();
+    }
+  }
+  if (tid < b) {
+    const double wi = A[tid * P + tid];
+    w[tid] = wi;
+    int rank = 0;
+    for (int j = 0; j < b; ++j) {
+      const double wj = A[j * P + j];
+      rank += (wj > wi || (wj == wi && j < tid)) ? 1 : 0;
+    }
+    if (rank < r)
+      for (int k = 0; k < b; ++k) Vr[k * r + rank] = (float)V[k * P + tid];
+  }
+}
+
+struct RrrWs {
+  size_t X, S, Q, Z, Y, W, W64, T, Vr, w, info, total;
+};
+RrrWs rrr_layout(int64_t din, int64_t dout, int b) {
+  RrrWs L{};
+  size_t o = 0;
+  auto take = [&](size_t n) { const size_t at = o; o += align_up(n); return at; };
+  L.X = take((size_t)din * dout * 4);
+  L.S = take((size_t)dout * dout * 4);
+  L.Q = take((size_t)dout * b * 4);
+  L.Z = take((size_t)dout * b * 4);
+  L.Y = take((size_t)dout * b * 4);
+  L.W = take((size_t)b * b * 4);
+  L.W64 = take((size_t)b * b * 8);
+  L.T = take((size_t)b * b * 4);
+  L.Vr = take((size_t)b * b * 4);
+  L.w = take((size_t)b * 8);
+  L.info = take(16);
+  L.total = o;
+  return L;
+}
+int rrr_block(int64_t dout) { return (int)std::min<int64_t>(kRrrBlock, dout) & ~1; }
+
 }  // namespace
+
+size_t low_rank_ws_bytes(int64_t din, int64_t dout) {
+  return rrr_layout(din, dout, rrr_block(dout)).total;
+}
+
+hipError_t launch_low_rank(const float* G, const float* dW, int64_t din, int64_t dout, int r,
+                           int iters, float* A, float* U, float* dWr, void* ws, hipStream_t st) {
+  const int b = rrr_block(dout);
+  const RrrWs L = rrr_layout(din, dout, b);
+  char* w = (char*)ws;
+  float *X = (float*)(w + L.X), *S = (float*)(w + L.S), *Q = (float*)(w + L.Q);
+  float *Z = (float*)(w + L.Z), *Y = (float*)(w + L.Y), *W = (float*)(w + L.W);
+  float *T = (float*)(w + L.T), *Vr = (float*)(w + L.Vr);
+  double* W64 = (double*)(w + L.W64);
+  double* ev = (double*)(w + L.w);
+  int32_t* info = (int32_t*)(w + L.info);
+  const int din_i = (int)din, dout_i = (int)dout;
+  // S = dW^T (G dW): the two large products on the split-bf16 path
+  {
+    GemmDesc<float> g = desc<float>(G, din, 1, dW, dout, 1, X, dout, din_i, dout_i, din_i, 1.f, 0.f);
+    PKV_TRY(run_group_split(&g, 1, st));
+    g = desc<float>(dW, 1, dout, X, dout, 1, S, dout, dout_i, dout_i, din_i, 1.f, 0.f);
+    PKV_TRY(run_group_split(&g, 1, st));
+  }
+  hipLaunchKernelGGL(diag_shift_kernel, dim3(1), dim3(256), 0, st, S, dout, dout,
+                     (float)(1e-5 * (double)dout));
+  PKV_TRY(hipGetLastError());
+  {
+    const int64_t n = dout * b;
+    hipLaunchKernelGGL(rrr_init_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, Q, dout,
+                       b, info);
+    PKV_TRY(hipGetLastError());
+  }
+  // src (dout x b) -> dst = src L^-T with src^T src = L L^T (Gram and factor in fp64)
+  auto orth = [&](const float* src, float* dst) -> hipError_t {
+    const dim3 gg((unsigned)((b + 15) / 16), (unsigned)((b + 15) / 16));
+    hipLaunchKernelGGL(gram64_kernel, gg, dim3(256), 0, st, src, dout, b, W64);
+    PKV_TRY(hipGetLastError());
+    hipLaunchKernelGGL((potrf_inv_kernel<double>), dim3(1), dim3(diag_threads<double>()), 0, st, W64,
+                       (int64_t)b, 0, b, info);
+    PKV_TRY(hipGetLastError());
+    hipLaunchKernelGGL((to_float_kernel<double>), dim3((b * b + 255) / 256), dim3(256), 0, st, W64, W,
+                       (int64_t)b * b);
+    PKV_TRY(hipGetLastError());
+    GemmDesc<float> g = desc<float>(src, b, 1, W, 1, b, dst, b, dout_i, b, b, 1.f, 0.f);
+    return run_group(&g, 1, st);
+  };
+  for (int it = 0; it < iters; ++it) {
+    GemmDesc<float> g = desc<float>(S, dout, 1, Q, b, 1, Z, b, dout_i, b, dout_i, 1.f, 0.f);
+    PKV_TRY(run_group(&g, 1, st));
+    PKV_TRY(orth(Z, Q));
+  }
+  PKV_TRY(orth(Q, Y));  // two more passes: orthonormal to rounding
+  PKV_TRY(orth(Y, Z));
+  {
+    // Rayleigh-Ritz: T = Z^T S Z, its top-r eigenvectors, U = Z Vr
+    GemmDesc<float> g = desc<float>(S, dout, 1, Z, b, 1, Y, b, dout_i, b, dout_i, 1.f, 0.f);
+    PKV_TRY(run_group(&g, 1, st));
+    g = desc<float>(Z, 1, b, Y, b, 1, T, b, b, b, dout_i, 1.f, 0.f);
+    PKV_TRY(run_group(&g, 1, st));
+    hipLaunchKernelGGL(jacobi_top_kernel, dim3(1), dim3(256), 0, st, T, b, r, Vr, ev);
+    PKV_TRY(hipGetLastError());
+    g = desc<float>(Z, b, 1, Vr, r, 1, U, r, dout_i, r, b, 1.f, 0.f);
+    PKV_TRY(run_group(&g, 1, st));
+    g = desc<float>(dW, dout, 1, U, r, 1, A, r, din_i, r, dout_i, 1.f, 0.f);
+    PKV_TRY(run_group(&g, 1, st));
+    if (dWr) {
+      g = desc<float>(A, r, 1, U, 1, r, dWr, dout, din_i, dout_i, r, 1.f, 0.f);
+      PKV_TRY(run_group(&g, 1, st));
+    }
+  }
+  return hipSuccess;
+}
 
 size_t solve_ws_bytes(bool f64, int64_t din, int64_t dout) {
   return f64 ? layout<double>(din, dout).total : layout<float>(din, dout).total;

@@ -202,3 +202,16 @@ def test_attend_cache_validation(L):
     q8 = L.patchkv_attend_cache_workspace_bytes(B.BF16, B.KV_MXINT8, 8, 64, 4, 2, 128)
     assert q8 - plain >= 2 * 2 * 64 * 128 * 2             # expanded K and V rows
     assert L.patchkv_attend_cache_workspace_bytes(B.BF16, 7, 8, 64, 4, 2, 128) == 0
+
+
+def test_low_rank_validation(L):
+    f = L.patchkv_low_rank_patch
+    nb = L.patchkv_low_rank_workspace_bytes(256, 128, 32)
+    assert nb > 256 * 128 * 4 + 128 * 128 * 4
+    assert f(None, FAKE, 256, 128, 32, 40, FAKE, FAKE, None, FAKE, nb, None) == B.E_NULL
+    assert f(FAKE, FAKE, 256, 128, 0, 40, FAKE, FAKE, None, FAKE, nb, None) == B.E_VALUE
+    assert f(FAKE, FAKE, 256, 128, 65, 40, FAKE, FAKE, None, FAKE, nb, None) == B.E_VALUE
+    assert f(FAKE, FAKE, 256, 40, 41, 40, FAKE, FAKE, None, FAKE, nb, None) == B.E_VALUE  # r > d_out
+    assert f(FAKE, FAKE, 256, 128, 32, 0, FAKE, FAKE, None, FAKE, nb, None) == B.E_VALUE
+    assert f(FAKE, FAKE, 256, 1, 1, 40, FAKE, FAKE, None, FAKE, nb, None) == B.E_SHAPE
+    assert f(FAKE, FAKE, 256, 128, 32, 40, FAKE, FAKE, None, FAKE, nb - 1, None) == B.E_WORKSPACE
