@@ -84,7 +84,7 @@ class LayerDev:
     """One layer's inputs on the device (and, for a chunked reference set, every
     chunk's queries and own keys and values)."""
 
-    def __init__(self, inp, torch, dev, chunks=(), mlp=None):
+    def __init__(self, inp, torch, dev, chunks=(), mlp=None, extras=(None, None)):
         def t(a):
             x = torch.from_numpy(np.ascontiguousarray(a))
             if inp.dtype == "bf16":
@@ -92,6 +92,13 @@ class LayerDev:
             return x.to(dev, non_blocking=False)
         self.Q, self.K, self.V, self.W = t(inp.Q), t(inp.K), t(inp.V), t(inp.W)
         self.chunks = [(t(c.Q), t(c.Ks), t(c.Vs)) for c in chunks]
+        qc, bias = extras
+        self.kv_format, self.Kq = 0, None
+        if qc is not None:  # block-scaled compressed cache (MXINT8 = 1, MXINT4 = 2)
+            self.kv_format = 1 if qc.bits == 8 else 2
+            self.Kq, self.Vq, self.Ke, self.Ve = (torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+                                                  for a in (qc.Kq, qc.Vq, qc.Ke, qc.Ve))
+        self.bias = torch.from_numpy(bias).to(dev) if bias is not None else None
         self.Wg = self.Wu = self.Wd = None
         if mlp is not None:
             self.Wg, self.Wu, self.Wd, self.eps = t(mlp.Wg), t(mlp.Wu), t(mlp.Wd), mlp.eps
@@ -116,6 +123,9 @@ class Buffers:
         self.C = torch.empty((din, d), dtype=adt, device=dev)
         self.dW = [torch.empty((din, d), dtype=torch.float32, device=dev) for _ in range(nl)]
         self.info = torch.zeros((nl,), dtype=torch.int32, device=dev)
+        if cfg.rank:  # reduced-rank factors of every layer's patch
+            self.A = [torch.empty((din, cfg.rank), dtype=torch.float32, device=dev) for _ in range(nl)]
+            self.U = [torch.empty((d, cfg.rank), dtype=torch.float32, device=dev) for _ in range(nl)]
         if cfg.d_ff:
             self.Hf = torch.empty((M, din), dtype=torch.float32, device=dev)
             self.Hc = torch.empty((M, din), dtype=torch.float32, device=dev)
@@ -134,7 +144,13 @@ def layer_steps(pkv, cfg, L, bufs, li: int, events=None):
     pkv.attend_full(L.Q, L.K, L.V, scale=cfg.scale, O=bufs.Of)
     if events is not None:
         events[1].record()
-    if L.idx is not None:
+    if L.Kq is not None:  # block-scaled compressed cache (the compressed entries themselves)
+        pkv.attend_cache(L.Q, L.Kq, L.Vq, kv_format=L.kv_format, Ke=L.Ke, Ve=L.Ve, bias=L.bias,
+                         scale=cfg.scale, p_terms=2, O=bufs.Oc)
+    elif L.bias is not None:
+        pkv.attend_cache(L.Q, *((L.K, L.V) if L.idx is not None else (L.Kc, L.Vc)), idx=L.idx,
+                         bias=L.bias, scale=cfg.scale, p_terms=2, O=bufs.Oc)
+    elif L.idx is not None:
         pkv.attend_compressed(L.Q, L.K, L.V, idx=L.idx, scale=cfg.scale, O=bufs.Oc)
     else:
         pkv.attend_compressed(L.Q, L.Kc, L.Vc, scale=cfg.scale, O=bufs.Oc)
@@ -150,6 +166,9 @@ def layer_steps(pkv, cfg, L, bufs, li: int, events=None):
                     info=bufs.info[li:li + 1])
     if cfg.d_ff:  # the student state through the patched block
         pkv.propagate_student(bufs.Hc, L.Wd, bufs.dW[li], bufs.Oc, Y=bufs.Y)
+    if cfg.rank:  # the reduced-rank factors (A, U): dW_r = A U^T
+        pkv.low_rank_patch(bufs.G, bufs.dW[li], r=cfg.rank, A=bufs.A[li], U=bufs.U[li],
+                           want_full=False)
 
 
 def chunked_layer_steps(pkv, cfg, L, bufs, li: int, events=None):
@@ -182,7 +201,8 @@ def cpu_baseline(cfg, rows: int) -> dict:
     by M / rows), plus the complete d x d ridge solve (independent of M).
     """
     import oracle
-    from workloads import make_chunk_inputs, make_layer_inputs, make_mlp_weights
+    from workloads import (make_cache_extras, make_chunk_inputs, make_layer_inputs,
+                           make_mlp_weights, unpack_int4)
     try:
         from threadpoolctl import threadpool_info
         blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
@@ -196,14 +216,19 @@ def cpu_baseline(cfg, rows: int) -> dict:
     t0 = time.perf_counter()
     K, V = oracle.decode(inp.K, dt), oracle.decode(inp.V, dt)
     W = oracle.decode(inp.W, dt)
-    if inp.idx is not None:
+    qc, cbias = make_cache_extras(cfg, inp)
+    cb = None if cbias is None else cbias.astype(np.float64)
+    if qc is not None:
+        unq = (lambda a: a) if qc.bits == 8 else unpack_int4
+        Kc, Vc = oracle.dequantize_mx(unq(qc.Kq), qc.Ke), oracle.dequantize_mx(unq(qc.Vq), qc.Ve)
+    elif inp.idx is not None:
         Kc, Vc = oracle.gather_cache(K, V, inp.idx)
     else:
         Kc, Vc = oracle.decode(inp.Kc, dt), oracle.decode(inp.Vc, dt)
     if ch is None:
         Q = oracle.decode(inp.Q[sel], dt)
         Of = oracle.attention(Q, K, V, inp.scale)
-        Oc = oracle.attention(Q, Kc, Vc, inp.scale)
+        Oc = oracle.attention(Q, Kc, Vc, inp.scale, bias=cb)
     else:
         # the first ``rows`` tokens of chunk 0 (a chunk's prefix is itself a chunk)
         Q = oracle.decode(ch.Q[:rows], dt)
@@ -227,6 +252,8 @@ def cpu_baseline(cfg, rows: int) -> dict:
     t1 = time.perf_counter()
     Gs, Cs = G * (tokens / rows), C * (tokens / rows)
     dW = oracle.solve_patch(Gs, Cs, oracle.ridge_lambda(Gs, cfg.lam, cfg.ridge))
+    if cfg.rank:
+        oracle.low_rank_patch(Gs, dW, cfg.rank)
     t_solve = time.perf_counter() - t1
     if cfg.d_ff:  # the propagation is linear in the rows, like the rest of the sample
         t2 = time.perf_counter()
@@ -239,8 +266,9 @@ def cpu_baseline(cfg, rows: int) -> dict:
             "kind": "oracle",
             "sample": f"config {cfg.cid} layer 0: fp64 attention (full + compressed), targets and "
                       f"statistics for {what} ({t_rows:.2f} s, scaled x{tokens / rows:.0f}) + "
-                      f"full {G.shape[0]}x{cfg.d} Cholesky solve ({t_solve:.2f} s); input "
-                      f"decoding included"}
+                      f"full {G.shape[0]}x{cfg.d} Cholesky solve"
+                      f"{' and rank-%d reduction' % cfg.rank if cfg.rank else ''} "
+                      f"({t_solve:.2f} s); input decoding included"}
 
 
 def main():
@@ -253,7 +281,8 @@ def main():
     import torch
 
     import paper_2609_39329_amd as pkv
-    from workloads import get_config, make_chunk_inputs, make_layer_inputs, make_mlp_weights
+    from workloads import (get_config, make_cache_extras, make_chunk_inputs, make_layer_inputs,
+                           make_mlp_weights)
 
     cfg = get_config(args.config)
     nl = cfg.layers if args.layers is None else min(args.layers, cfg.layers)
@@ -266,7 +295,7 @@ def main():
         inp = make_layer_inputs(cfg, layer)
         chunks = [make_chunk_inputs(inp, j, cfg.M) for j in range(cfg.chunks)] if cfg.chunks > 1 else ()
         mlp = make_mlp_weights(inp, cfg.d_ff) if cfg.d_ff else None
-        layers.append(LayerDev(inp, torch, dev, chunks, mlp))
+        layers.append(LayerDev(inp, torch, dev, chunks, mlp, make_cache_extras(cfg, inp)))
         if layer % 8 == 7 or layer == nl - 1:
             log(f"[bench] inputs of {layer + 1}/{nl} layers resident ({time.perf_counter() - t0:.1f} s)")
     torch.cuda.synchronize()
@@ -333,7 +362,8 @@ def main():
                    "N": cfg.N, "B": cfg.B, "M": M, "d": d, "Hq": cfg.Hq, "Hkv": cfg.Hkv,
                    "dh": cfg.dh, "lambda": cfg.lam, "compressed_cache": cfg.cache,
                    "reference_chunks": cfg.chunks,
-                   "own_causal_prefix": chunked, "ridge": cfg.ridge,
+                   "own_causal_prefix": chunked, "ridge": cfg.ridge, "rank": cfg.rank,
+                   "kv_format": cfg.kv_format, "cache_bias": cfg.cache_bias,
                    "patch": (f"MLP down-projection {cfg.d_ff}x{d} (SwiGLU features, student "
                              f"propagation)" if cfg.d_ff else f"{d}x{d} projection")},
         "attention_full_ms": t_attn * 1e3,

@@ -236,11 +236,13 @@ def solve_patch(G0: np.ndarray, C: np.ndarray, lam: float) -> np.ndarray:
 
 
 def layer_patch(inp, rho: int = 1, mode: str = "absolute", lam: float | None = None,
-                keep: bool = True) -> dict:
+                keep: bool = True, cache=None, bias: np.ndarray | None = None) -> dict:
     """One block's patch from a ``workloads`` LayerInputs (all steps in fp64).
 
-    Returns a dict with dW and, when ``keep``, the intermediates O_f, O_c, T,
-    G (without the ridge), C and the lambda used.
+    ``cache`` = (Kc, Vc) float64 replaces the layer's own compressed cache (e.g. a
+    dequantized one); ``bias`` [Hkv, B] is its per-entry logit bias. Returns a dict
+    with dW and, when ``keep``, the intermediates O_f, O_c, T, G (without the
+    ridge), C and the lambda used.
     """
     dt = inp.dtype
     Q = decode(inp.Q, dt)
@@ -248,12 +250,14 @@ def layer_patch(inp, rho: int = 1, mode: str = "absolute", lam: float | None = N
     V = decode(inp.V, dt)
     W = decode(inp.W, dt)
     Of = attention(Q, K, V, inp.scale)
-    if inp.idx is not None:
+    if cache is not None:
+        Kc, Vc = cache
+    elif inp.idx is not None:
         Kc, Vc = gather_cache(K, V, inp.idx)
     else:
         Kc, Vc = decode(inp.Kc, dt), decode(inp.Vc, dt)
     del K, V
-    Oc = attention(Q, Kc, Vc, inp.scale)
+    Oc = attention(Q, Kc, Vc, inp.scale, bias=bias)
     T = targets(Of, Oc, W, rho)
     G0, C = normal_equations(Oc, T)
     lam_used = ridge_lambda(G0, inp.lam if lam is None else lam, mode)

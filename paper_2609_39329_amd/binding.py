@@ -380,7 +380,7 @@ def layer_workspace_bytes(dtype: int, acc: int, M: int, N: int, B: int, Hq: int,
     return lib().patchkv_layer_workspace_bytes(dtype, acc, M, N, B, Hq, Hkv, dh)
 
 
-def low_rank_patch(G, dW, r: int = 32, iters: int = 40, A=None, U=None, dWr=None,
+def low_rank_patch(G, dW, r: int = 32, iters: int = 24, A=None, U=None, dWr=None,
                    want_full: bool = True, stream=None):
     """Reduced-rank patch: (A [d_in, r], U [d_out, r], dW_r = A U^T or None) for the
     projection of dW onto the top-r eigenvectors of dW^T G dW (G, dW float32)."""

@@ -1204,27 +1204,110 @@ __global__ __launch_bounds__(256) void diag_shift_kernel(float* M, int64_t n, in
   for (int64_t i = threadIdx.x; i < n; i += 256) M[i * ld + i] += mu;
 }
 
-// W[i][j] = sum_k Z[k][i] Z[k][j] in fp64 (Z [rows][b] fp32, b <= kRrrBlock): one
-// workgroup per 16 x 16 tile of W, rows streamed through LDS in chunks of 64.
-__global__ __launch_bounds__(256) void gram64_kernel(const float* __restrict__ Z, int64_t rows, int b,
-                                                     double* __restrict__ W) {
-  __shared__ float zi[64][17], zj[64][17];
-  const int i0 = blockIdx.y * 16, j0 = blockIdx.x * 16, tid = threadIdx.x;
+// Tall-skinny products of the subspace iteration (nc <= kRrrBlock columns): one
+// workgroup per 16 rows of C, K streamed through LDS in chunks of 64 with the next
+// chunk loaded into registers while the current one is multiplied, fp32 FMA in a
+// fixed order. C[i][j] = sum_k A[i][k] B[k][j], A [rows][K] (lda), B [K][nc] (ldb).
+__global__ __launch_bounds__(256) void tsgemm_kernel(const float* __restrict__ A, int64_t lda,
+                                                     const float* __restrict__ B, int64_t ldb,
+                                                     int64_t rows, int K, int nc,
+                                                     float* __restrict__ C, int64_t ldc) {
+  __shared__ __attribute__((aligned(16))) float As[16][68];
+  __shared__ __attribute__((aligned(16))) float Bs[64][kRrrBlock];
+  const int tid = threadIdx.x, i = tid / 16, j4 = (tid % 16) * 4;
+  const int64_t r0 = (int64_t)blockIdx.x * 16;
+  // this thread's share of a chunk: A row ra, columns ca..ca+3; B rows kb + 16u, cols cb..cb+3
+  const int ra = tid / 16, ca = (tid % 16) * 4, kb = tid / 16, cb = (tid % 16) * 4;
+  const bool va = (lda & 3) == 0 && (((uintptr_t)A) & 15) == 0;
+  const bool vb = (ldb & 3) == 0 && (((uintptr_t)B) & 15) == 0;
+  f32x4 ra4, rb4[4];
+  auto load = [&](int k0) {
+    const int64_t row = r0 + ra;
+    const int k = k0 + ca;
+    if (row < rows && va && k + 3 < K) {
+      ra4 = *(const f32x4*)(A + row * lda + k);
+    } else {
+      for (int t = 0; t < 4; ++t) ra4[t] = (row < rows && k + t < K) ? A[row * lda + k + t] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int kk = k0 + kb + 16 * u;
+      if (kk < K && vb && cb + 3 < nc) {
+        rb4[u] = *(const f32x4*)(B + (int64_t)kk * ldb + cb);
+      } else {
+        for (int t = 0; t < 4; ++t)
+          rb4[u][t] = (kk < K && cb + t < nc) ? B[(int64_t)kk * ldb + cb + t] : 0.f;
+      }
+    }
+  };
+  f32x4 acc = {};
+  load(0);
+  for (int k0 = 0; k0 < K; k0 += 64) {
+    *(f32x4*)(&As[ra][ca]) = ra4;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) *(f32x4*)(&Bs[kb + 16 * u][cb]) = rb4[u];
+    __syncthreads();
+    if (k0 + 64 < K) load(k0 + 64);
+#pragma unroll 8
+    for (int kk = 0; kk < 64; ++kk) {
+      const float a = As[i][kk];
+      const f32x4 bv = *(const f32x4*)(&Bs[kk][j4]);
+      acc[0] = fmaf(a, bv[0], acc[0]);
+      acc[1] = fmaf(a, bv[1], acc[1]);
+      acc[2] = fmaf(a, bv[2], acc[2]);
+      acc[3] = fmaf(a, bv[3], acc[3]);
+    }
+    __syncthreads();
+  }
+  if (r0 + i < rows)
+    for (int t = 0; t < 4; ++t)
+      if (j4 + t < nc) C[(r0 + i) * ldc + j4 + t] = acc[t];
+}
+
+// Partial sums of X^T Y in fp64 (X, Y [rows][b] fp32, b <= kRrrBlock) over slice z of
+// the rows: part[z][i][j]; one workgroup per 16 x 16 tile and slice.
+constexpr int kGramSlices = 16;
+__global__ __launch_bounds__(256) void gram_partial_kernel(const float* __restrict__ X,
+                                                           const float* __restrict__ Y, int64_t rows,
+                                                           int b, double* __restrict__ part) {
+  __shared__ float xs[64][17], ys[64][17];
+  const int i0 = blockIdx.y * 16, j0 = blockIdx.x * 16, z = blockIdx.z, tid = threadIdx.x;
   const int ti = tid / 16, tj = tid % 16;
+  const int64_t per = (rows + kGramSlices - 1) / kGramSlices;
+  const int64_t lo = z * per, hi = std::min<int64_t>(rows, lo + per);
   double acc = 0.0;
-  for (int64_t k0 = 0; k0 < rows; k0 += 64) {
+  for (int64_t k0 = lo; k0 < hi; k0 += 64) {
     for (int e = tid; e < 64 * 16; e += 256) {
       const int kk = e / 16, c = e % 16;
       const int64_t k = k0 + kk;
-      zi[kk][c] = (k < rows && i0 + c < b) ? Z[k * b + i0 + c] : 0.f;
-      zj[kk][c] = (k < rows && j0 + c < b) ? Z[k * b + j0 + c] : 0.f;
+      xs[kk][c] = (k < hi && i0 + c < b) ? X[k * b + i0 + c] : 0.f;
+      ys[kk][c] = (k < hi && j0 + c < b) ? Y[k * b + j0 + c] : 0.f;
     }
     __syncthreads();
 #pragma unroll 8
-    for (int kk = 0; kk < 64; ++kk) acc = fma((double)zi[kk][ti], (double)zj[kk][tj], acc);
+    for (int kk = 0; kk < 64; ++kk) acc = fma((double)xs[kk][ti], (double)ys[kk][tj], acc);
     __syncthreads();
   }
-  if (i0 + ti < b && j0 + tj < b) W[(int64_t)(i0 + ti) * b + j0 + tj] = acc;
+  if (i0 + ti < b && j0 + tj < b) part[((int64_t)z * b + i0 + ti) * b + j0 + tj] = acc;
+}
+
+// W = sum over the slices, in slice order (fp64)
+__global__ __launch_bounds__(256) void gram_reduce_kernel(const double* __restrict__ part, int b,
+                                                          double* __restrict__ W) {
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= b * b) return;
+  double s = 0.0;
+  for (int z = 0; z < kGramSlices; ++z) s += part[(int64_t)z * b * b + e];
+  W[e] = s;
+}
+
+// Wt[k][j] = (float) L^-1[j][k]: the transposed inverse factor, row-major, for tsgemm
+__global__ __launch_bounds__(256) void linv_t_kernel(const double* __restrict__ Linv, int b,
+                                                     float* __restrict__ Wt) {
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= b * b) return;
+  const int k = e / b, j = e % b;
+  Wt[e] = (float)Linv[j * b + k];
 }
 
 // Q[i][j] = a counter-based pseudo-random value in [-1, 1) of (i, j)
@@ -1246,7 +1329,7 @@ __global__ __launch_bounds__(256) void rrr_init_kernel(float* Q, int64_t rows, i
 // round-robin schedule, columns then rows. Vr [b][r] receives the eigenvectors of the
 // r largest eigenvalues, in descending order (ties: lower index first); w [b] all
 // eigenvalues by index.
-__global__ __launch_bounds__(256) void jacobi_top_kernel(const float* __restrict__ T, int b, int r,
+__global__ __launch_bounds__(256) void jacobi_top_kernel(const double* __restrict__ T, int b, int r,
                                                          float* __restrict__ Vr,
                                                          double* __restrict__ w) {
   constexpr int NB = kRrrBlock, P = NB + 1;
@@ -1256,12 +1339,38 @@ __global__ __launch_bounds__(256) void jacobi_top_kernel(const float* __restrict
   const int tid = threadIdx.x;
   for (int e = tid; e < b * b; e += 256) {
     const int i = e / b, j = e % b;
-    A[i * P + j] = 0.5 * ((double)T[i * b + j] + (double)T[j * b + i]);
+    A[i * P + j] = 0.5 * (T[i * b + j] + T[j * b + i]);
     V[i * P + j] = i == j ? 1.0 : 0.0;
   }
   __syncthreads();
   const int half = b / 2;
+  __shared__ double red[256];
+  __shared__ int done;
   for (int sweep = 0; sweep < kJacobiSweeps; ++sweep) {
+    // stop once the off-diagonal mass is below 1e-30 of the diagonal's (fp64 rounding)
+    double off = 0.0, dia = 0.0;
+    for (int e = tid; e < b * b; e += 256) {
+      const int i = e / b, j = e % b;
+      const double v = A[i * P + j] * A[i * P + j];
+      if (i == j) dia += v; else off += v;
+    }
+    red[tid] = off;
+    __syncthreads();
+    for (int s2 = 128; s2 > 0; s2 >>= 1) {
+      if (tid < s2) red[tid] += red[tid + s2];
+      __syncthreads();
+    }
+    const double off_all = red[0];
+    __syncthreads();
+    red[tid] = dia;
+    __syncthreads();
+    for (int s2 = 128; s2 > 0; s2 >>= 1) {
+      if (tid < s2) red[tid] += red[tid + s2];
+      __syncthreads();
+    }
+    if (tid == 0) done = off_all <= 1e-30 * red[0];
+    __syncthreads();
+    if (done) break;
     for (int step = 0; step < b - 1; ++step) {
       if (tid < half) {
         // round robin: position 0 fixed, the others rotate by `step`
@@ -1321,7 +1430,7 @@ __global__ __launch_bounds__(256) void jacobi_top_kernel(const float* __restrict
 }
 
 struct RrrWs {
-  size_t X, S, Q, Z, Y, W, W64, T, Vr, w, info, total;
+  size_t X, S, Q, Z, Y, W, W64, part, T, Vr, w, info, total;
 };
 RrrWs rrr_layout(int64_t din, int64_t dout, int b) {
   RrrWs L{};
@@ -1334,7 +1443,8 @@ RrrWs rrr_layout(int64_t din, int64_t dout, int b) {
   L.Y = take((size_t)dout * b * 4);
   L.W = take((size_t)b * b * 4);
   L.W64 = take((size_t)b * b * 8);
-  L.T = take((size_t)b * b * 4);
+  L.part = take((size_t)kGramSlices * b * b * 8);
+  L.T = take((size_t)b * b * 8);
   L.Vr = take((size_t)b * b * 4);
   L.w = take((size_t)b * 8);
   L.info = take(16);
@@ -1356,8 +1466,8 @@ hipError_t launch_low_rank(const float* G, const float* dW, int64_t din, int64_t
   char* w = (char*)ws;
   float *X = (float*)(w + L.X), *S = (float*)(w + L.S), *Q = (float*)(w + L.Q);
   float *Z = (float*)(w + L.Z), *Y = (float*)(w + L.Y), *W = (float*)(w + L.W);
-  float *T = (float*)(w + L.T), *Vr = (float*)(w + L.Vr);
-  double* W64 = (double*)(w + L.W64);
+  float* Vr = (float*)(w + L.Vr);
+  double *W64 = (double*)(w + L.W64), *part = (double*)(w + L.part), *T = (double*)(w + L.T);
   double* ev = (double*)(w + L.w);
   int32_t* info = (int32_t*)(w + L.info);
   const int din_i = (int)din, dout_i = (int)dout;
@@ -1377,43 +1487,49 @@ hipError_t launch_low_rank(const float* G, const float* dW, int64_t din, int64_t
                        b, info);
     PKV_TRY(hipGetLastError());
   }
+  // C [rows][nc] = A [rows][K] B [K][nc] (tall-skinny, fp32)
+  auto ts = [&](const float* Am, int64_t lda, const float* Bm, int64_t ldb, int64_t rows, int K,
+                int nc, float* Cm, int64_t ldc) -> hipError_t {
+    hipLaunchKernelGGL(tsgemm_kernel, dim3((unsigned)((rows + 15) / 16)), dim3(256), 0, st, Am, lda,
+                       Bm, ldb, rows, K, nc, Cm, ldc);
+    return hipGetLastError();
+  };
+  // fp64 X^T Y [b][b]
+  auto gram = [&](const float* Xm, const float* Ym, double* out) -> hipError_t {
+    const dim3 gg((unsigned)((b + 15) / 16), (unsigned)((b + 15) / 16), kGramSlices);
+    hipLaunchKernelGGL(gram_partial_kernel, gg, dim3(256), 0, st, Xm, Ym, dout, b, part);
+    PKV_TRY(hipGetLastError());
+    hipLaunchKernelGGL(gram_reduce_kernel, dim3((b * b + 255) / 256), dim3(256), 0, st, part, b, out);
+    return hipGetLastError();
+  };
   // src (dout x b) -> dst = src L^-T with src^T src = L L^T (Gram and factor in fp64)
   auto orth = [&](const float* src, float* dst) -> hipError_t {
-    const dim3 gg((unsigned)((b + 15) / 16), (unsigned)((b + 15) / 16));
-    hipLaunchKernelGGL(gram64_kernel, gg, dim3(256), 0, st, src, dout, b, W64);
-    PKV_TRY(hipGetLastError());
+    PKV_TRY(gram(src, src, W64));
     hipLaunchKernelGGL((potrf_inv_kernel<double>), dim3(1), dim3(diag_threads<double>()), 0, st, W64,
                        (int64_t)b, 0, b, info);
     PKV_TRY(hipGetLastError());
-    hipLaunchKernelGGL((to_float_kernel<double>), dim3((b * b + 255) / 256), dim3(256), 0, st, W64, W,
-                       (int64_t)b * b);
+    hipLaunchKernelGGL(linv_t_kernel, dim3((b * b + 255) / 256), dim3(256), 0, st, W64, b, W);
     PKV_TRY(hipGetLastError());
-    GemmDesc<float> g = desc<float>(src, b, 1, W, 1, b, dst, b, dout_i, b, b, 1.f, 0.f);
-    return run_group(&g, 1, st);
+    return ts(src, b, W, b, dout, b, b, dst, b);
   };
+  // one power step per orthonormalisation: cond(Z) <= lambda_max / mu <= 1e5, so the
+  // fp64 Gram matrix (its square) stays factorable
   for (int it = 0; it < iters; ++it) {
-    GemmDesc<float> g = desc<float>(S, dout, 1, Q, b, 1, Z, b, dout_i, b, dout_i, 1.f, 0.f);
-    PKV_TRY(run_group(&g, 1, st));
+    PKV_TRY(ts(S, dout, Q, b, dout, dout_i, b, Z, b));
     PKV_TRY(orth(Z, Q));
   }
   PKV_TRY(orth(Q, Y));  // two more passes: orthonormal to rounding
   PKV_TRY(orth(Y, Z));
-  {
-    // Rayleigh-Ritz: T = Z^T S Z, its top-r eigenvectors, U = Z Vr
-    GemmDesc<float> g = desc<float>(S, dout, 1, Z, b, 1, Y, b, dout_i, b, dout_i, 1.f, 0.f);
+  // Rayleigh-Ritz: T = Z^T S Z (fp64), its top-r eigenvectors, U = Z Vr
+  PKV_TRY(ts(S, dout, Z, b, dout, dout_i, b, Y, b));
+  PKV_TRY(gram(Z, Y, T));
+  hipLaunchKernelGGL(jacobi_top_kernel, dim3(1), dim3(256), 0, st, T, b, r, Vr, ev);
+  PKV_TRY(hipGetLastError());
+  PKV_TRY(ts(Z, b, Vr, r, dout, b, r, U, r));
+  PKV_TRY(ts(dW, dout, U, r, din, dout_i, r, A, r));
+  if (dWr) {
+    GemmDesc<float> g = desc<float>(A, r, 1, U, 1, r, dWr, dout, din_i, dout_i, r, 1.f, 0.f);
     PKV_TRY(run_group(&g, 1, st));
-    g = desc<float>(Z, 1, b, Y, b, 1, T, b, b, b, dout_i, 1.f, 0.f);
-    PKV_TRY(run_group(&g, 1, st));
-    hipLaunchKernelGGL(jacobi_top_kernel, dim3(1), dim3(256), 0, st, T, b, r, Vr, ev);
-    PKV_TRY(hipGetLastError());
-    g = desc<float>(Z, b, 1, Vr, r, 1, U, r, dout_i, r, b, 1.f, 0.f);
-    PKV_TRY(run_group(&g, 1, st));
-    g = desc<float>(dW, dout, 1, U, r, 1, A, r, din_i, r, dout_i, 1.f, 0.f);
-    PKV_TRY(run_group(&g, 1, st));
-    if (dWr) {
-      g = desc<float>(A, r, 1, U, 1, r, dWr, dout, din_i, dout_i, r, 1.f, 0.f);
-      PKV_TRY(run_group(&g, 1, st));
-    }
   }
   return hipSuccess;
 }

@@ -23,7 +23,8 @@ import torch
 import oracle
 import paper_2609_39329_amd as pkv
 from gpu_util import DEV, host, rel
-from workloads import CONFIGS, make_chunk_inputs, make_layer_inputs, make_mlp_weights
+from workloads import (CONFIGS, make_cache_extras, make_chunk_inputs, make_layer_inputs,
+                       make_mlp_weights, unpack_int4)
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 sys.path.insert(0, ROOT)
@@ -34,7 +35,8 @@ from make_oracle_fixtures import fixture_path, sample_rows, sample_tokens, sketc
 
 pytestmark = pytest.mark.gpu
 
-CASES = [(1, 0), (2, 0), (4, 0), (3, 0), (3, 8), (3, 16), (3, 24), (3, 31), (5, 0), (6, 0)]
+CASES = [(1, 0), (2, 0), (4, 0), (3, 0), (3, 8), (3, 16), (3, 24), (3, 31), (5, 0), (6, 0), (7, 0),
+         (8, 0)]
 TOL = 2e-2
 
 
@@ -49,7 +51,8 @@ def test_full_size_layer_patch(cid, layer):
     inp = make_layer_inputs(cfg, layer)
     chunks = [make_chunk_inputs(inp, j, cfg.M) for j in range(cfg.chunks)] if cfg.chunks > 1 else ()
     mlp = make_mlp_weights(inp, cfg.d_ff) if cfg.d_ff else None
-    L = LayerDev(inp, torch, DEV, chunks, mlp)
+    qc, cbias = make_cache_extras(cfg, inp)
+    L = LayerDev(inp, torch, DEV, chunks, mlp, (qc, cbias))
     bufs = Buffers(cfg, torch, DEV, 1)
     if chunks:
         chunked_layer_steps(pkv, cfg, L, bufs, 0)
@@ -66,6 +69,12 @@ def test_full_size_layer_patch(cid, layer):
     e_norm = abs(np.linalg.norm(dW) - float(fx["norm"])) / float(fx["norm"])
     print(f"  rows {e_rows:.3e}  sketch {e_sk:.3e}  norm {e_norm:.3e}", flush=True)
     assert e_rows <= TOL and e_sk <= TOL and e_norm <= TOL
+    if cfg.rank:  # the reduced-rank factors capture the oracle's top-r energy
+        X = bufs.dW[0] @ bufs.U[0]
+        energy = float((X * (bufs.G @ X)).sum().item())
+        e_en = abs(energy - float(fx["rank_energy"])) / float(fx["rank_energy"])
+        print(f"  rank-{cfg.rank} energy {e_en:.3e}", flush=True)
+        assert e_en <= TOL
     if cfg.d_ff:  # the propagated student state on sampled tokens
         y_rows = sample_tokens(cid, layer, cfg.M)
         assert np.array_equal(y_rows, fx["y_rows"])
@@ -77,10 +86,14 @@ def test_full_size_layer_patch(cid, layer):
     q_rows = np.random.default_rng([cid, layer, 7]).choice(cfg.M, 3, replace=False)
     dt = inp.dtype
     K, V = oracle.decode(inp.K, dt), oracle.decode(inp.V, dt)
-    if inp.idx is not None:
+    if qc is not None:
+        q = (lambda a: a) if qc.bits == 8 else unpack_int4
+        Kc, Vc = oracle.dequantize_mx(q(qc.Kq), qc.Ke), oracle.dequantize_mx(q(qc.Vq), qc.Ve)
+    elif inp.idx is not None:
         Kc, Vc = oracle.gather_cache(K, V, inp.idx)
     else:
         Kc, Vc = oracle.decode(inp.Kc, dt), oracle.decode(inp.Vc, dt)
+    cb = None if cbias is None else cbias.astype(np.float64)
     if chunks:
         last = chunks[-1]
         ref_f, ref_c = [], []
@@ -95,13 +108,13 @@ def test_full_size_layer_patch(cid, layer):
     else:
         Q = oracle.decode(inp.Q[q_rows], dt)
         ref_f = oracle.attention(Q, K, V, inp.scale)
-        ref_c = oracle.attention(Q, Kc, Vc, inp.scale)
+        ref_c = oracle.attention(Q, Kc, Vc, inp.scale, bias=cb)
     e_of = rel(host(bufs.Of)[q_rows], ref_f)
     e_oc = rel(host(bufs.Oc)[q_rows], ref_c)
     print(f"  O_f rows {e_of:.3e}  O_c rows {e_oc:.3e}", flush=True)
     assert e_of <= 4e-3 and e_oc <= 5e-5
 
-    if chunks or cfg.d_ff:
+    if chunks or cfg.d_ff or cfg.rank or qc is not None or cbias is not None:
         return
     # the single-call entry point runs the same kernels in the same order
     dW2, info2 = pkv.compute_layer_patch(L.Q, L.K, L.V, L.W, idx=L.idx, Kc=L.Kc, Vc=L.Vc,

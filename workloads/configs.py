@@ -39,6 +39,9 @@ class Config:
     chunks: int = 1          # reference chunks per layer (M tokens each, own causal prefix)
     d_ff: int = 0            # > 0: patch the d_ff x d down-projection of a SwiGLU MLP
     ridge: str = "absolute"  # "absolute": lam is lambda; "adaptive": lam is lambda_0 of Eq. 7
+    rank: int = 0            # > 0: also the reduced-rank patch of this rank
+    kv_format: str = "plain" # compressed cache storage: "plain", "mxint8" or "mxint4"
+    cache_bias: bool = False # compressed cache entries carry a logit bias
 
     @property
     def group(self) -> int:
@@ -77,6 +80,16 @@ CONFIGS = (
     Config(6, "llama3-8b-mlp-layer-172k", d=4096, Hq=32, Hkv=8, dh=128, N=172032, B=1720,
            M=4096, lam=1e-3, dtype="bf16", d_ff=14336, ridge="adaptive", n_sink=4, n_recent=860,
            n_random=856),
+    # config 3's build with every patch also reduced to rank 32 (the paper's low-rank
+    # variant: (d + d) * 32 numbers per patch instead of d * d)
+    Config(7, "llama3-8b-32layer-172k-rank32", d=4096, Hq=32, Hkv=8, dh=128, N=172032, B=1720,
+           M=4096, lam=1e-1, dtype="bf16", layers=32, rank=32, n_sink=4, n_recent=860,
+           n_random=856),
+    # config 4 with an attention-matching style compressed cache: synthesized entries
+    # with a per-entry logit bias, stored as block-scaled int8 (MX-style)
+    Config(8, "qwen2.5-7b-layer-64k-synth-bias-mxint8", d=3584, Hq=28, Hkv=4, dh=128, N=65536,
+           B=1024, M=2048, lam=5e-2, dtype="bf16", cache="synthesize", n_mix=64,
+           kv_format="mxint8", cache_bias=True),
 )
 
 

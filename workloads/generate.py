@@ -286,6 +286,33 @@ def pack_int4(q: np.ndarray) -> np.ndarray:
     return (u[..., 0::2] | (u[..., 1::2] << 4)).astype(np.uint8)
 
 
+def unpack_int4(p: np.ndarray) -> np.ndarray:
+    """uint8 [..., dh/2] (two int4, even channel low) -> int8 [..., dh]."""
+    lo = (p & 0xF).astype(np.int16)
+    hi = (p >> 4).astype(np.int16)
+    out = np.empty(p.shape[:-1] + (p.shape[-1] * 2,), dtype=np.int8)
+    out[..., 0::2] = np.where(lo >= 8, lo - 16, lo)
+    out[..., 1::2] = np.where(hi >= 8, hi - 16, hi)
+    return out
+
+
+def make_cache_extras(cfg, inp: LayerInputs):
+    """The compressed cache's storage and bias of a workload config: (QuantCache of
+    the compressed entries or None, logit bias [Hkv, B] or None). Quantized caches
+    hold the compressed entries themselves (the synthesized K_c, V_c, or the gathered
+    rows of an eviction subset)."""
+    qc = None
+    if cfg.kv_format != "plain":
+        bits = {"mxint8": 8, "mxint4": 4}[cfg.kv_format]
+        if inp.idx is not None:
+            Kc, Vc = inp.K[:, inp.idx], inp.V[:, inp.idx]
+        else:
+            Kc, Vc = inp.Kc, inp.Vc
+        qc = make_quant_cache(np.ascontiguousarray(Kc), np.ascontiguousarray(Vc), bits, inp.dtype)
+    bias = make_cache_bias(inp, n_mix=cfg.n_mix or 64) if cfg.cache_bias else None
+    return qc, bias
+
+
 def make_quant_cache(K: np.ndarray, V: np.ndarray, bits: int, dtype: str) -> QuantCache:
     """Block-scaled integer version of a cache K, V [Hkv, n, dh] (stored form)."""
     kf = bf16_bits_to_f32(K) if dtype == "bf16" else K
