@@ -75,7 +75,7 @@ def parse():
     ap.add_argument("--config", type=int, default=3)
     ap.add_argument("--layers", type=int, default=None, help="layers per step (default: all)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=32,
+    ap.add_argument("--cpu-rows", type=int, default=256,
                     help="query rows of the oracle sample for the CPU baseline")
     return ap.parse_args()
 
@@ -212,6 +212,7 @@ def cpu_baseline(cfg, rows: int) -> dict:
     inp = make_layer_inputs(cfg, 0)
     dt = inp.dtype
     ch = make_chunk_inputs(inp, 0, cfg.M) if cfg.chunks > 1 else None
+    rows = min(rows, cfg.M)
     sel = np.linspace(0, cfg.M - 1, rows).astype(np.int64)
     t0 = time.perf_counter()
     K, V = oracle.decode(inp.K, dt), oracle.decode(inp.V, dt)
