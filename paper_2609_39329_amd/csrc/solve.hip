@@ -17,6 +17,7 @@
 #include <math.h>
 
 #include <algorithm>
+#include <utility>
 
 #include "common.hpp"
 #include "kernels.hpp"
@@ -664,7 +665,11 @@ __global__ __launch_bounds__(diag_threads<T>()) void potrf_inv_kernel(T* A, int6
 //   phase C:          A_ij -= L_ik L_jk^T (k < j <= i);  E_im -= L_ik E_km (i > k, m <= k)
 // i.e. right-looking blocked Cholesky with the forward substitution of the identity
 // carried along; phases B and C are independent 32 x 32 x 32 products on fp32 MFMA
-// (exact fp32 products), spread over the four waves, one barrier between phases.
+// (exact fp32 products), spread over eight waves, one barrier between phases. The
+// leaf of step k + 1 needs only the first product of phase C of step k (its own
+// diagonal block), so wave 0 does that product and then the leaf while the other
+// seven waves do the rest of phase C: the single-wave leaf, the longest serial part,
+// overlaps the trailing products.
 constexpr int PB = 130;  // LDS pitch (floats): lane-per-row reads hit 64 distinct banks
 
 // D = sgn * P Q' (+ C), 32 x 32 blocks in LDS (pitch PB); Q' = Q^T if QT else Q.
@@ -691,39 +696,79 @@ __device__ __forceinline__ float bcast(float x, int src_lane) {
   return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), src_lane));
 }
 
+// f(integral_constant<int, I>) for I = 0..N-1, unrolled at compile time
+template <class F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
 // One wave: factor the SPD 32 x 32 block S (lower triangle read) and write
-// X = L^{-1} (lower, zeros above) to Xo.
-//  1. Right-looking factorisation: lane r (and its twin r + 32, which repeats the
-//     same work so the wave never diverges) holds row r of the trailing matrix;
-//     step j reads the pivot and column j through scalar registers (readlane).
-//     L overwrites S. A pivot that is not positive (or NaN) makes its L_jj, and
-//     every later one, NaN: the first NaN on the diagonal is the failing column.
-//  2. Column-parallel inverse: lane c solves L x = e_c by forward substitution,
-//     x_r = (delta_rc - sum_{m<r} L_rm x_m) / L_rr, reading L with broadcast LDS
-//     reads (the same address in every lane), no cross-lane traffic.
+// X = L^{-1} (lower, zeros above) to Xo, in one right-looking sweep.
+// Lane r (and its twin r + 32, which repeats the same work so the wave never
+// diverges) holds row r of the trailing matrix (v) and row r of Y, the identity
+// under forward substitution (x). Step j, with pivot p = A_jj and u_r = A_rj / p for
+// rows r > j (0 otherwise):
+//   A_rc -= u_r A_cj     (c > j: column j of every lane, read through readlane)
+//   Y_rm -= u_r Y_jm     (m <= j: row j of Y, read from lane j)
+// and column j of L is A_rj / sqrt(p). Row r of X is row r of Y over L_rr, applied at
+// the end (Y's row r is final after step r - 1). Each step reads 32 values across
+// lanes, in groups of up to 8 held in distinct scalar registers, so that a readlane
+// is not directly followed by its consumer. A pivot that is not positive (or NaN)
+// makes its L_jj, and every later one, NaN: the first NaN on the diagonal is the
+// failing column.
 __device__ __forceinline__ void leaf32(float* S, float* Xo, int lane, int col0, int bs, int32_t* info,
                                        bool& failed) {
   int r = lane & 31;
   // opaque per call: keeps the per-step lane comparisons inside the call instead of
   // hoisting them into scalar registers for the whole kernel
   asm volatile("" : "+v"(r));
-  float v[32];
+  float v[32], x[32];
 #pragma unroll
-  for (int c = 0; c < 32; ++c) v[c] = S[r * PB + c];
-#pragma unroll
-  for (int j = 0; j < 32; ++j) {
-    const float rs = __builtin_amdgcn_rsqf(bcast(v[j], j));
-    const float u = v[j] * (rs * rs);  // A[r][j] / p
-    // in chunks of 8 broadcasts: the scheduler would otherwise hoist all of them and
-    // run out of scalar registers
-#pragma unroll
-    for (int c0 = j + 1; c0 < 32; c0 += 8) {
-#pragma unroll
-      for (int c = c0; c < c0 + 8 && c < 32; ++c) v[c] = fmaf(-u, bcast(v[j], c), v[c]);  // A[c][j]
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    v[j] *= rs;
+  for (int c = 0; c < 32; ++c) {
+    v[c] = S[r * PB + c];
+    x[c] = c == r ? 1.f : 0.f;
   }
+  float rs_own = 0.f;
+  // w[c0 .. c0+n) -= u * src(c), the n <= 8 values read first (the empty asm makes
+  // them live at once, in distinct registers)
+  auto group = [&](float (&w)[32], auto c0_t, auto n_t, auto src, float u) {
+    constexpr int c0 = decltype(c0_t)::value, n = decltype(n_t)::value;
+    float t[8];
+#pragma unroll
+    for (int q = 0; q < n; ++q) t[q] = src(c0 + q);
+#pragma unroll
+    for (int q = n; q < 8; ++q) t[q] = t[0];
+    asm volatile("" ::"s"(t[0]), "s"(t[1]), "s"(t[2]), "s"(t[3]), "s"(t[4]), "s"(t[5]), "s"(t[6]),
+                 "s"(t[7]));
+#pragma unroll
+    for (int q = 0; q < n; ++q) w[c0 + q] = fmaf(-u, t[q], w[c0 + q]);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  static_for<32>([&](auto j_t) {
+    constexpr int j = decltype(j_t)::value;
+    const float rs = __builtin_amdgcn_rsqf(bcast(v[j], j));
+    const float u = r > j ? v[j] * (rs * rs) : 0.f;  // A[r][j] / p
+    if (r == j) rs_own = rs;
+    // A_rc -= u_r A_cj, c = j+1..31 (A_cj is lane c's v[j])
+    static_for<(31 - j + 7) / 8>([&](auto g_t) {
+      constexpr int c0 = j + 1 + 8 * decltype(g_t)::value;
+      constexpr int n = 32 - c0 < 8 ? 32 - c0 : 8;
+      group(v, std::integral_constant<int, c0>{}, std::integral_constant<int, n>{},
+            [&](int c) { return bcast(v[j], c); }, u);
+    });
+    // Y_rm -= u_r Y_jm, m = 0..j (lane j's x[m])
+    static_for<(j + 1 + 7) / 8>([&](auto g_t) {
+      constexpr int m0 = 8 * decltype(g_t)::value;
+      constexpr int n = j + 1 - m0 < 8 ? j + 1 - m0 : 8;
+      group(x, std::integral_constant<int, m0>{}, std::integral_constant<int, n>{},
+            [&](int m) { return bcast(x[m], j); }, u);
+    });
+    v[j] *= rs;
+  });
   // first failing pivot of this block (padding pivots past bs are 1)
   float diag = 0.f;
 #pragma unroll
@@ -736,65 +781,63 @@ __device__ __forceinline__ void leaf32(float* S, float* Xo, int lane, int col0, 
   }
   if (lane < 32) {
 #pragma unroll
-    for (int c = 0; c < 32; ++c) S[r * PB + c] = v[c];  // row r of L (upper part unused)
-  }
-  // (single wave: its LDS operations complete in program order)
-  float x[32];
-#pragma unroll
-  for (int i = 0; i < 32; ++i) {
-    float acc = i == r ? 1.f : 0.f;
-    const float* Li = S + i * PB;
-#pragma unroll
-    for (int m = 0; m < i; m += 4) {
-      const f32x4 l4 = *(const f32x4*)(Li + m);
-#pragma unroll
-      for (int t = 0; t < 4; ++t)
-        if (m + t < i) acc = fmaf(-l4[t], x[m + t], acc);
+    for (int c = 0; c < 32; ++c) {
+      S[r * PB + c] = v[c];            // row r of L (upper part unused)
+      Xo[r * PB + c] = x[c] * rs_own;  // row r of X (zeros above the diagonal)
     }
-    x[i] = acc * __builtin_amdgcn_rcpf(Li[i]);
-  }
-  if (lane < 32) {
-#pragma unroll
-    for (int i = 0; i < 32; ++i) Xo[i * PB + r] = x[i];  // column r of X (zeros above)
   }
 }
 
-__global__ __launch_bounds__(256) void potrf128_kernel(float* A, int64_t lda, int kb, int bs,
-                                                       int32_t* info) {
+constexpr int kPotrfWaves = 8;  // 8 waves: the next leaf overlaps the trailing products
+__global__ __launch_bounds__(64 * kPotrfWaves) void potrf128_kernel(float* A, int64_t lda, int kb, int bs,
+                                                                   int32_t* info) {
+  constexpr int NT = 64 * kPotrfWaves, NL = 128 * 128 / 4 / NT;  // 16-byte chunks per thread
   __shared__ float As[128 * PB];
   __shared__ float Es[128 * PB];
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   // 16-byte accesses when every row start is 16-byte aligned (kb is a multiple of 128)
   const bool vec = (lda & 3) == 0 && (((uintptr_t)A) & 15) == 0;
-  const float* Ab = A + (int64_t)kb * lda + kb;
+  float* Ab = A + (int64_t)kb * lda + kb;
+  {
+    // every load in flight before the first LDS write; both triangles are copied
+    // (the leaf reads whole rows of its diagonal block), identity past bs
+    f32x4 buf[NL];
 #pragma unroll
-  for (int u = 0; u < 16; ++u) {
-    const int e = (u * 256 + tid) * 4;  // 4 consecutive columns of one row
-    const int i = e >> 7, j0 = e & 127;
-    f32x4 v = {};
-    const float* src = Ab + (int64_t)i * lda + j0;
-    if (i < bs && vec && j0 + 3 < bs) {
-      v = *(const f32x4*)src;
-    } else if (i < bs) {
-      for (int t = 0; t < 4; ++t) v[t] = j0 + t < bs ? src[t] : 0.f;
+    for (int u = 0; u < NL; ++u) {
+      const int e = (u * NT + tid) * 4;  // 4 consecutive columns of one row
+      const int i = e >> 7, j0 = e & 127;
+      const float* src = Ab + (int64_t)i * lda + j0;
+      if (i < bs && vec && j0 + 3 < bs) {
+        buf[u] = *(const f32x4*)src;
+      } else {
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+          buf[u][t] = (i < bs && j0 + t < bs) ? src[t] : (i == j0 + t ? 1.f : 0.f);
+      }
     }
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const int j = j0 + t;
-      float x = j <= i ? v[t] : 0.f;  // lower triangle only
-      if (i >= bs || j >= bs) x = i == j ? 1.f : 0.f;
-      As[i * PB + j] = x;
-      Es[i * PB + j] = 0.f;
+    for (int u = 0; u < NL; ++u) {
+      const int e = (u * NT + tid) * 4;
+      const int i = e >> 7, j0 = e & 127;
+      *(f32x2*)&As[i * PB + j0] = f32x2{buf[u][0], buf[u][1]};
+      *(f32x2*)&As[i * PB + j0 + 2] = f32x2{buf[u][2], buf[u][3]};
+      // E = L^{-1} starts at zero in its strictly lower 32 x 32 blocks (the diagonal
+      // blocks are written whole by the leaf; the upper ones are never read)
+      if ((i >> 5) > (j0 >> 5)) {
+        *(f32x2*)&Es[i * PB + j0] = f32x2{0.f, 0.f};
+        *(f32x2*)&Es[i * PB + j0 + 2] = f32x2{0.f, 0.f};
+      }
     }
   }
   __syncthreads();
   auto blk = [](float* base, int i, int j) { return base + (32 * i) * PB + 32 * j; };
   bool failed = false;
+  if (wid == 0) leaf32(blk(As, 0, 0), blk(Es, 0, 0), lane, kb, kb + bs, info, failed);
+  __syncthreads();
   for (int k = 0; k < 4; ++k) {
-    if (wid == 0) leaf32(blk(As, k, k), blk(Es, k, k), lane, kb + 32 * k, kb + bs, info, failed);
-    __syncthreads();
     // phase B: (3 - k) panel products, k products of the identity's row block k
-    for (int q = wid; q < 3; q += 4) {
+    if (wid < 3) {
+      const int q = wid;
       if (q < 3 - k) {
         const int i = k + 1 + q;
         mm32<true>(blk(As, i, k), blk(As, i, k), blk(Es, k, k), nullptr, 1.f, lane);
@@ -804,10 +847,13 @@ __global__ __launch_bounds__(256) void potrf128_kernel(float* A, int64_t lda, in
       }
     }
     __syncthreads();
-    // phase C: trailing lower blocks (k < j <= i), then E_im for i > k, m <= k
+    if (k == 3) break;
+    // phase C: trailing lower blocks (k < j <= i), then E_im for i > k, m <= k. Job 0
+    // is the next diagonal block: wave 0 updates it and factors it (the next leaf)
+    // while the other waves share the remaining jobs.
     const int ntr = (3 - k) * (4 - k) / 2;
     const int njobs = ntr + (3 - k) * (k + 1);
-    for (int q = wid; q < njobs; q += 4) {
+    auto job = [&](int q) {
       if (q < ntr) {
         int i = k + 1, t = q;
         while (t > i - k - 1) {  // row i holds i - k blocks (j = k+1..i)
@@ -821,22 +867,28 @@ __global__ __launch_bounds__(256) void potrf128_kernel(float* A, int64_t lda, in
         const int i = k + 1 + t / (k + 1), m = t % (k + 1);
         mm32<false>(blk(Es, i, m), blk(As, i, k), blk(Es, k, m), blk(Es, i, m), -1.f, lane);
       }
+    };
+    if (wid == 0) {
+      job(0);
+      leaf32(blk(As, k + 1, k + 1), blk(Es, k + 1, k + 1), lane, kb + 32 * (k + 1), kb + bs, info,
+             failed);
+    } else {
+      for (int q = wid; q < njobs; q += kPotrfWaves - 1) job(q);
     }
     __syncthreads();
   }
-  float* Ad = A + (int64_t)kb * lda + kb;
   // recompute the store's bounds masks here rather than keep the load's alive
   int tid2 = tid;
   asm volatile("" : "+v"(tid2));
 #pragma unroll
-  for (int u = 0; u < 16; ++u) {
-    const int e = (u * 256 + tid2) * 4;
+  for (int u = 0; u < NL; ++u) {
+    const int e = (u * NT + tid2) * 4;
     const int i = e >> 7, j0 = e & 127;
     if (i >= bs) continue;
     f32x4 v;
 #pragma unroll
     for (int t = 0; t < 4; ++t) v[t] = j0 + t <= i ? Es[i * PB + j0 + t] : 0.f;
-    float* dst = Ad + (int64_t)i * lda + j0;
+    float* dst = Ab + (int64_t)i * lda + j0;
     if (vec && j0 + 3 < bs) *(f32x4*)dst = v;
     else
       for (int t = 0; t < 4; ++t)
@@ -1095,7 +1147,8 @@ hipError_t solve_t(const T* G, const T* C, int64_t d64, int64_t dout64, double l
       const int bs = std::min(NB, d - kb);
       const int rest = d - kb - bs;
       if constexpr (sizeof(T) == 4)
-        hipLaunchKernelGGL(potrf128_kernel, dim3(1), dim3(256), 0, st, A, d64, kb, bs, info);
+        hipLaunchKernelGGL(potrf128_kernel, dim3(1), dim3(64 * kPotrfWaves), 0, st, A, d64, kb, bs,
+                           info);
       else
         hipLaunchKernelGGL((potrf_inv_kernel<T>), dim3(1), dim3(diag_threads<T>()), 0, st, A, d64, kb,
                            bs, info);
@@ -1187,6 +1240,7 @@ hipError_t solve_t(const T* G, const T* C, int64_t d64, int64_t dout64, double l
 // eigenvectors map back through Q.
 
 constexpr int kRrrBlock = 64;   // subspace width (r <= it)
+static_assert(kRrrBlock <= 64, "the tall-skinny products take at most 64 columns");
 constexpr int kJacobiSweeps = 14;
 
 // M[i][i] += rel * trace(M) / n (one workgroup; the trace in fp64, fixed order)
@@ -1204,64 +1258,79 @@ __global__ __launch_bounds__(256) void diag_shift_kernel(float* M, int64_t n, in
   for (int64_t i = threadIdx.x; i < n; i += 256) M[i * ld + i] += mu;
 }
 
-// Tall-skinny products of the subspace iteration (nc <= kRrrBlock columns): one
-// workgroup per 16 rows of C, K streamed through LDS in chunks of 64 with the next
-// chunk loaded into registers while the current one is multiplied, fp32 FMA in a
-// fixed order. C[i][j] = sum_k A[i][k] B[k][j], A [rows][K] (lda), B [K][nc] (ldb).
-__global__ __launch_bounds__(256) void tsgemm_kernel(const float* __restrict__ A, int64_t lda,
-                                                     const float* __restrict__ B, int64_t ldb,
-                                                     int64_t rows, int K, int nc,
-                                                     float* __restrict__ C, int64_t ldc) {
-  __shared__ __attribute__((aligned(16))) float As[16][68];
-  __shared__ __attribute__((aligned(16))) float Bs[64][kRrrBlock];
-  const int tid = threadIdx.x, i = tid / 16, j4 = (tid % 16) * 4;
+// Tall-skinny products of the subspace iteration: C [rows][nc] = A [rows][K] B [K][nc]
+// (nc <= kRrrBlock), row-major with leading dimensions lda, ldb, ldc. One workgroup
+// per 16 rows of C; its eight waves take interleaved 16-wide chunks of K (wave w:
+// chunks w, w + 8, ...), so the waves of a workgroup read adjacent 64-byte segments of
+// the same rows of A. Each wave keeps a 16 x 16 tile per 16 columns of C on fp32 MFMA
+// 16x16x4 (exact fp32 products, fp32 accumulation) with the next chunk's operands
+// loaded while the current one is multiplied; the eight partial tiles are summed in
+// LDS in wave order (deterministic). Lane l holds row l % 16 of the A chunk, columns
+// 4 (l / 16) .. +3, and the matching rows of B for column l % 16 of each tile.
+constexpr int kTsWaves = 8;
+__device__ __forceinline__ f32x4 mfma16_f32(float a, float b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+template <int NCT>
+__global__ __launch_bounds__(64 * kTsWaves) void tsgemm_kernel(const float* __restrict__ A, int64_t lda,
+                                                               const float* __restrict__ B, int64_t ldb,
+                                                               int64_t rows, int K, int nc,
+                                                               float* __restrict__ C, int64_t ldc) {
+  __shared__ float red[kTsWaves][NCT][4][64];
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6, l16 = lane & 15, g = lane >> 4;
   const int64_t r0 = (int64_t)blockIdx.x * 16;
-  // this thread's share of a chunk: A row ra, columns ca..ca+3; B rows kb + 16u, cols cb..cb+3
-  const int ra = tid / 16, ca = (tid % 16) * 4, kb = tid / 16, cb = (tid % 16) * 4;
+  const int64_t row = r0 + l16;
   const bool va = (lda & 3) == 0 && (((uintptr_t)A) & 15) == 0;
-  const bool vb = (ldb & 3) == 0 && (((uintptr_t)B) & 15) == 0;
-  f32x4 ra4, rb4[4];
-  auto load = [&](int k0) {
-    const int64_t row = r0 + ra;
-    const int k = k0 + ca;
+  f32x4 a_cur, a_nxt;
+  float b_cur[NCT][4], b_nxt[NCT][4];
+  auto load = [&](int k0, f32x4& a, float (&b)[NCT][4]) {
+    const int k = k0 + 4 * g;
     if (row < rows && va && k + 3 < K) {
-      ra4 = *(const f32x4*)(A + row * lda + k);
+      a = *(const f32x4*)(A + row * lda + k);
     } else {
-      for (int t = 0; t < 4; ++t) ra4[t] = (row < rows && k + t < K) ? A[row * lda + k + t] : 0.f;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) a[t] = (row < rows && k + t < K) ? A[row * lda + k + t] : 0.f;
     }
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int kk = k0 + kb + 16 * u;
-      if (kk < K && vb && cb + 3 < nc) {
-        rb4[u] = *(const f32x4*)(B + (int64_t)kk * ldb + cb);
-      } else {
-        for (int t = 0; t < 4; ++t)
-          rb4[u][t] = (kk < K && cb + t < nc) ? B[(int64_t)kk * ldb + cb + t] : 0.f;
-      }
+    for (int ct = 0; ct < NCT; ++ct) {
+      const int c = 16 * ct + l16;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) b[ct][t] = (k + t < K && c < nc) ? B[(int64_t)(k + t) * ldb + c] : 0.f;
     }
   };
-  f32x4 acc = {};
-  load(0);
-  for (int k0 = 0; k0 < K; k0 += 64) {
-    *(f32x4*)(&As[ra][ca]) = ra4;
+  f32x4 acc[NCT];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) *(f32x4*)(&Bs[kb + 16 * u][cb]) = rb4[u];
-    __syncthreads();
-    if (k0 + 64 < K) load(k0 + 64);
-#pragma unroll 8
-    for (int kk = 0; kk < 64; ++kk) {
-      const float a = As[i][kk];
-      const f32x4 bv = *(const f32x4*)(&Bs[kk][j4]);
-      acc[0] = fmaf(a, bv[0], acc[0]);
-      acc[1] = fmaf(a, bv[1], acc[1]);
-      acc[2] = fmaf(a, bv[2], acc[2]);
-      acc[3] = fmaf(a, bv[3], acc[3]);
-    }
-    __syncthreads();
-  }
-  if (r0 + i < rows)
+  for (int ct = 0; ct < NCT; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+  constexpr int step = 16 * kTsWaves;
+  int k0 = 16 * wid;
+  if (k0 < K) load(k0, a_cur, b_cur);
+  for (; k0 < K; k0 += step) {
+    if (k0 + step < K) load(k0 + step, a_nxt, b_nxt);
+#pragma unroll
     for (int t = 0; t < 4; ++t)
-      if (j4 + t < nc) C[(r0 + i) * ldc + j4 + t] = acc[t];
+#pragma unroll
+      for (int ct = 0; ct < NCT; ++ct) acc[ct] = mfma16_f32(a_cur[t], b_cur[ct][t], acc[ct]);
+    a_cur = a_nxt;
+#pragma unroll
+    for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+      for (int t = 0; t < 4; ++t) b_cur[ct][t] = b_nxt[ct][t];
+  }
+#pragma unroll
+  for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) red[wid][ct][e][lane] = acc[ct][e];
+  __syncthreads();
+  // element (ct, e, lane) of the tile is C[r0 + 4 (lane / 16) + e][16 ct + lane % 16]
+  for (int q = tid; q < NCT * 4 * 64; q += 64 * kTsWaves) {
+    const int ct = q / 256, e = (q / 64) % 4, ln = q % 64;
+    float v = 0.f;
+#pragma unroll
+    for (int w = 0; w < kTsWaves; ++w) v += red[w][ct][e][ln];
+    const int64_t rr = r0 + 4 * (ln >> 4) + e;
+    const int c = 16 * ct + (ln & 15);
+    if (rr < rows && c < nc) C[rr * ldc + c] = v;
+  }
 }
 
 // Partial sums of X^T Y in fp64 (X, Y [rows][b] fp32, b <= kRrrBlock) over slice z of
@@ -1490,8 +1559,14 @@ hipError_t launch_low_rank(const float* G, const float* dW, int64_t din, int64_t
   // C [rows][nc] = A [rows][K] B [K][nc] (tall-skinny, fp32)
   auto ts = [&](const float* Am, int64_t lda, const float* Bm, int64_t ldb, int64_t rows, int K,
                 int nc, float* Cm, int64_t ldc) -> hipError_t {
-    hipLaunchKernelGGL(tsgemm_kernel, dim3((unsigned)((rows + 15) / 16)), dim3(256), 0, st, Am, lda,
-                       Bm, ldb, rows, K, nc, Cm, ldc);
+    const dim3 grid((unsigned)((rows + 15) / 16)), block(64 * kTsWaves);
+    switch ((nc + 15) / 16) {
+      case 1: hipLaunchKernelGGL(tsgemm_kernel<1>, grid, block, 0, st, Am, lda, Bm, ldb, rows, K, nc, Cm, ldc); break;
+      case 2: hipLaunchKernelGGL(tsgemm_kernel<2>, grid, block, 0, st, Am, lda, Bm, ldb, rows, K, nc, Cm, ldc); break;
+      case 3: hipLaunchKernelGGL(tsgemm_kernel<3>, grid, block, 0, st, Am, lda, Bm, ldb, rows, K, nc, Cm, ldc); break;
+      case 4: hipLaunchKernelGGL(tsgemm_kernel<4>, grid, block, 0, st, Am, lda, Bm, ldb, rows, K, nc, Cm, ldc); break;
+      default: return hipErrorInvalidValue;
+    }
     return hipGetLastError();
   };
   // fp64 X^T Y [b][b]
