@@ -6,11 +6,13 @@
 //     diagonal kernel    L_kk^{-1} (1 WG)
 //     grouped GEMM       L_ik = A_ik L_kk^{-T} (i > k);  Z_k = L_kk^{-1} R_k
 //     grouped GEMM       A_ij -= L_ik L_jk^T (lower blocks);  R_i -= L_ik Z_k (i > k)
-//   then backward:  X_k = L_kk^{-T} Z_k;  Z_i -= L_ki^T X_k (i < k), k descending.
-// The trailing updates are deferred to pairs of block columns (K = 2 NB), see solve_t.
+// The updates outside a group of four block columns (an outer block, OB = 4 NB) are
+// deferred to the end of the group (K = OB), see solve_t. Backward substitution runs
+// per outer block: X_O = L_OO^{-T} Z_O;  Z_i -= L_Oi^T X_O (i before O).
 // Triangular solves against a diagonal block use that block's explicit inverse (a
 // GEMM instead of a substitution); its condition number is at most the square root
-// of that of G + lambda I.
+// of that of G + lambda I. The OB-wide inverses are assembled from the NB-wide ones
+// by batched GEMMs.
 // fp32 GEMM tiles run on MFMA 32x32x2 f32 (128 x 128 tiles, double-buffered LDS);
 // fp64 tiles on fp64 FMA. The adaptive ridge of Eq. 7, lambda_0 ||G||_F^2 / tr G,
 // is reduced on the device in fp64 in a fixed order (deterministic).
@@ -59,7 +61,24 @@ struct GemmDesc {
   int tiles_n;
   int ntiles;
   int vecA, vecB;  // 16-byte loads along the contiguous dimension are allowed
+  // batch of equal-shaped problems: item b uses A + b bA, B + b bB, C + b bC
+  int batch, tiles_b;  // items, tiles per item (ntiles = batch * tiles_b)
+  int64_t bA, bB, bC;
 };
+
+// the problem of tile t of a batched descriptor (t becomes the tile within it)
+template <class D>
+__device__ __forceinline__ D batch_item(const D& g, int& t) {
+  D h = g;
+  if (g.batch > 1) {
+    const int b = t / g.tiles_b;
+    t -= b * g.tiles_b;
+    h.A += b * g.bA;
+    h.B += b * g.bB;
+    h.C += b * g.bC;
+  }
+  return h;
+}
 
 // ---- fp32: BM x BM output tile (128 or 64), 4 waves, MFMA 32x32x2 f32 ---------------
 constexpr int F_KC = 32;
@@ -215,6 +234,8 @@ struct SGemm {
   int lower;       // only tiles with tile_row >= tile_col (enumerated triangularly)
   int tiles_n, ntiles;
   int vecA, vecB, vecC;
+  int batch, tiles_b;  // as in GemmDesc
+  int64_t bA, bB, bC;
 };
 
 constexpr int S_BM = 128, S_KC = 32;
@@ -400,8 +421,15 @@ __global__ __launch_bounds__(256, 2) void sgemm3_kernel(SGemm d0, SGemm d1) {
   const int total = d0.ntiles + d1.ntiles;
   const int t = xcd_item((total + kXcds - 1) / kXcds);
   if (t >= total) return;
-  if (t < d0.ntiles) sgemm3_body<AK0, BJ0>(d0, t, lds);
-  else sgemm3_body<AK1, BJ1>(d1, t - d0.ntiles, lds);
+  if (t < d0.ntiles) {
+    int u = t;
+    const SGemm g = batch_item(d0, u);
+    sgemm3_body<AK0, BJ0>(g, u, lds);
+  } else {
+    int u = t - d0.ntiles;
+    const SGemm g = batch_item(d1, u);
+    sgemm3_body<AK1, BJ1>(g, u, lds);
+  }
 }
 
 // ---- fp64: 64 x 64 output tile, fp64 FMA, 4 x 4 outputs per thread ----------------
@@ -461,14 +489,28 @@ __device__ __forceinline__ void gemm_f64_body(const GemmDesc<double>& g, int t) 
 template <int BM>
 __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmDesc<float> d0, GemmDesc<float> d1) {
   const int t = blockIdx.x;
-  if (t < d0.ntiles) gemm_f32_body<BM>(d0, t);
-  else if (t - d0.ntiles < d1.ntiles) gemm_f32_body<BM>(d1, t - d0.ntiles);
+  if (t < d0.ntiles) {
+    int u = t;
+    const GemmDesc<float> g = batch_item(d0, u);
+    gemm_f32_body<BM>(g, u);
+  } else if (t - d0.ntiles < d1.ntiles) {
+    int u = t - d0.ntiles;
+    const GemmDesc<float> g = batch_item(d1, u);
+    gemm_f32_body<BM>(g, u);
+  }
 }
 
 __global__ __launch_bounds__(256) void gemm_f64_kernel(GemmDesc<double> d0, GemmDesc<double> d1) {
   const int t = blockIdx.x;
-  if (t < d0.ntiles) gemm_f64_body(d0, t);
-  else if (t - d0.ntiles < d1.ntiles) gemm_f64_body(d1, t - d0.ntiles);
+  if (t < d0.ntiles) {
+    int u = t;
+    const GemmDesc<double> g = batch_item(d0, u);
+    gemm_f64_body(g, u);
+  } else if (t - d0.ntiles < d1.ntiles) {
+    int u = t - d0.ntiles;
+    const GemmDesc<double> g = batch_item(d1, u);
+    gemm_f64_body(g, u);
+  }
 }
 
 // ---- diagonal block: Cholesky factor and its inverse, in registers ---------------
@@ -896,6 +938,17 @@ __global__ __launch_bounds__(64 * kPotrfWaves) void potrf128_kernel(float* A, in
   }
 }
 
+// Zeros above the nb x nb diagonal blocks inside each ob x ob diagonal block of A:
+// A[i][j] = 0 for (i / nb + 1) nb <= j < min((i / ob + 1) ob, d).
+template <class T>
+__global__ __launch_bounds__(256) void zero_upper_kernel(T* A, int64_t d, int nb, int ob) {
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < d * ob;
+       e += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t i = e / ob, j = (i / ob) * ob + e % ob;
+    if (j < d && j >= (i / nb + 1) * nb) A[i * d + j] = T(0);
+  }
+}
+
 // A = G + lambda I (full copy), R = C, info = 0.
 template <class T>
 __global__ __launch_bounds__(256) void init_kernel(const T* __restrict__ G, const T* __restrict__ C,
@@ -987,6 +1040,7 @@ GemmDesc<T> desc(const T* A, int64_t sai, int64_t sak, const T* B, int64_t sbk, 
   g.M = M; g.N = N; g.K = K;
   g.alpha = alpha; g.beta = beta;
   g.lower = lower;
+  g.batch = 1;
   // vector loads along the contiguous dimension: the other stride and the base must
   // keep every 4-element group 16-byte aligned
   g.vecA = al16(A) && ((sak == 1 && sai % 4 == 0) || (sai == 1 && sak % 4 == 0));
@@ -994,10 +1048,23 @@ GemmDesc<T> desc(const T* A, int64_t sai, int64_t sak, const T* B, int64_t sbk, 
   return g;
 }
 
+// g repeated over `count` problems, item b offset by (b bA, b bB, b bC) elements
+template <class T>
+GemmDesc<T> batched(GemmDesc<T> g, int count, int64_t bA, int64_t bB, int64_t bC) {
+  g.batch = count;
+  g.bA = bA;
+  g.bB = bB;
+  g.bC = bC;
+  if (bA % 4 != 0) g.vecA = 0;
+  if (bB % 4 != 0) g.vecB = 0;
+  return g;
+}
+
 template <class T>
 void set_tiles(GemmDesc<T>& g, int tile) {
   g.tiles_n = (g.N + tile - 1) / tile;
-  g.ntiles = (g.M > 0 && g.N > 0 && g.K > 0) ? ((g.M + tile - 1) / tile) * g.tiles_n : 0;
+  g.tiles_b = (g.M > 0 && g.N > 0 && g.K > 0) ? ((g.M + tile - 1) / tile) * g.tiles_n : 0;
+  g.ntiles = g.batch * g.tiles_b;
 }
 
 // One launch for up to two problems. fp32 uses 128 x 128 tiles unless that would
@@ -1039,9 +1106,12 @@ SGemm to_sgemm(const GemmDesc<float>& g, bool& ak, bool& bj) {
   s.lower = g.lower;
   const int tm = (g.M + S_BM - 1) / S_BM, tn = (g.N + S_BM - 1) / S_BM;
   s.tiles_n = tn;
-  s.ntiles = g.lower ? tm * (tm + 1) / 2 : tm * tn;  // a lower-triangle update is square
+  s.tiles_b = g.lower ? tm * (tm + 1) / 2 : tm * tn;  // a lower-triangle update is square
+  s.batch = g.batch;
+  s.ntiles = s.batch * s.tiles_b;
+  s.bA = g.bA; s.bB = g.bB; s.bC = g.bC;
   s.vecA = g.vecA; s.vecB = g.vecB;
-  s.vecC = al16(g.C) && g.ldc % 4 == 0;
+  s.vecC = al16(g.C) && g.ldc % 4 == 0 && g.bC % 4 == 0;
   return s;
 }
 
@@ -1075,8 +1145,11 @@ hipError_t run_group_split(const GemmDesc<float>* ds, int n, hipStream_t st) {
   return hipGetLastError();
 }
 
+// Column blocks of NB are grouped into outer blocks of kSolveNBO * NB (512 wide in fp32)
+constexpr int kSolveNBO = 4;
+
 struct SolveLayout {
-  size_t A, Lm, R, Z, X, part, lam, total;
+  size_t A, Lm, R, Z, X, Tw, part, lam, total;
 };
 
 template <class T>
@@ -1088,6 +1161,11 @@ SolveLayout layout(int64_t d, int64_t dout) {
   L.R = o; o += align_up(sizeof(T) * d * dout);
   L.Z = o; o += align_up(sizeof(T) * d * dout);
   L.X = o; o += align_up(sizeof(T) * d * dout);
+  // products of the backward's block inversion: at most (d / 2s + 1) s^2 for s <= OB / 2
+  {
+    const int64_t ob = (int64_t)kSolveNBO * Blk<T>::NB;
+    L.Tw = o; o += align_up(sizeof(T) * (d + ob) * ob / 2);
+  }
   L.part = o; o += align_up(sizeof(double) * 2 * kRedBlocks);
   L.lam = o; o += align_up(sizeof(double));
   L.total = o;
@@ -1139,7 +1217,7 @@ hipError_t solve_t(const T* G, const T* C, int64_t d64, int64_t dout64, double l
   // updated after each panel; the rest of the trailing matrix and of R is updated
   // once per outer block with K = OB, which divides the read-modify-write traffic
   // of the large updates by NBO. The backward substitution is grouped the same way.
-  constexpr int NBO = 4;  // 512-wide outer blocks in fp32 (3.60 ms at d = 4096; 2: 3.69, 3: 3.64)
+  constexpr int NBO = kSolveNBO;
   const int OB = NBO * NB;
   for (int K0 = 0; K0 < d; K0 += OB) {
     const int W = std::min(OB, d - K0);  // width of this outer block
@@ -1190,25 +1268,53 @@ hipError_t solve_t(const T* G, const T* C, int64_t d64, int64_t dout64, double l
       PKV_TRY(run(g, 2));
     }
   }
+  // Backward substitution, X = L^{-T} Z, one outer block at a time on the inverse
+  // M = L_OO^{-1} of its OB x OB diagonal block of L. M is assembled in place of that
+  // block of A from the NB x NB inverses the factorisation left there, by doubling:
+  // for s = NB, 2 NB, .., OB / 2, every pair of adjacent s-wide blocks (aligned to 2s)
+  // gets [[M_1, 0], [L_21, M_2]]^{-1} = [[M_1, 0], [-M_2 L_21 M_1, M_2]], all pairs
+  // of a level in one batched launch per product (the last pair, which may be short,
+  // as a second problem). Each outer block then takes two launches instead of two
+  // per column block.
+  T* Tw = (T*)(w + L.Tw);
+  {
+    const int blocks = (int)std::min<int64_t>((d64 * OB + 255) / 256, 4096);
+    hipLaunchKernelGGL((zero_upper_kernel<T>), dim3(blocks), dim3(256), 0, st, A, d64, NB, OB);
+    PKV_TRY(hipGetLastError());
+  }
+  for (int s = NB; s < OB && s < d; s *= 2) {
+    const int full = d / (2 * s);                // pairs with both halves s wide
+    const int q_r = full * 2 * s, s2_r = d - q_r - s;  // the short last pair, if s2_r > 0
+    const int64_t step = (int64_t)2 * s * (d + 1);    // diagonal offset between pairs
+    GemmDesc<T> g[2];
+    int n = 0;
+    // Tw_p = L_21 M_1
+    if (full > 0)
+      g[n++] = batched(desc<T>(Lm + (int64_t)s * d, d, 1, A, d, 1, Tw, s, s, s, s, one, zero), full, step,
+                       step, (int64_t)s * s);
+    if (s2_r > 0)
+      g[n++] = desc<T>(Lm + (int64_t)(q_r + s) * d + q_r, d, 1, A + (int64_t)q_r * d + q_r, d, 1,
+                       Tw + (int64_t)full * s * s, s, s2_r, s, s, one, zero);
+    PKV_TRY(run(g, n));
+    n = 0;
+    // M_21 = -M_2 Tw_p, into the lower-left block of the pair
+    if (full > 0)
+      g[n++] = batched(desc<T>(A + (int64_t)s * d + s, d, 1, Tw, s, 1, A + (int64_t)s * d, d, s, s, s, mone,
+                               zero),
+                       full, step, (int64_t)s * s, step);
+    if (s2_r > 0)
+      g[n++] = desc<T>(A + (int64_t)(q_r + s) * d + q_r + s, d, 1, Tw + (int64_t)full * s * s, s, 1,
+                       A + (int64_t)(q_r + s) * d + q_r, d, s2_r, s, s2_r, mone, zero);
+    PKV_TRY(run(g, n));
+  }
   const int nout = (d + OB - 1) / OB;
   for (int ko = nout - 1; ko >= 0; --ko) {
     const int K0 = ko * OB, W = std::min(OB, d - K0);
-    const int nin = (W + NB - 1) / NB;
-    for (int j = nin - 1; j >= 0; --j) {
-      const int kb = K0 + j * NB, bs = std::min(NB, d - kb);
-      const T* Linv = A + (int64_t)kb * d + kb;
-      {
-        // X_k = Linv^T Z_k : X(i,n) = sum_t Linv[t][i] Z[kb+t][n]
-        GemmDesc<T> g = desc<T>(Linv, 1, d, Z + (int64_t)kb * dout, dout, 1, X + (int64_t)kb * dout,
-                                dout, bs, dout, bs, one, zero);
-        PKV_TRY(run(&g, 1));
-      }
-      if (j > 0) {
-        // the earlier column blocks of this outer block: Z[K0..kb) -= L[k, K0..kb)^T X_k
-        GemmDesc<T> g = desc<T>(Lm + (int64_t)kb * d + K0, 1, d, X + (int64_t)kb * dout, dout, 1,
-                                Z + (int64_t)K0 * dout, dout, kb - K0, dout, bs, mone, one);
-        PKV_TRY(run(&g, 1));
-      }
+    {
+      // X_O = M^T Z_O : X(i,n) = sum_t M[t][i] Z[K0+t][n]
+      GemmDesc<T> g = desc<T>(A + (int64_t)K0 * d + K0, 1, d, Z + (int64_t)K0 * dout, dout, 1,
+                              X + (int64_t)K0 * dout, dout, W, dout, W, one, zero);
+      PKV_TRY(run(&g, 1));
     }
     if (K0 > 0) {
       // Z_i -= L_Ki^T X_K for i < K0 : Z(i,n) -= sum_t Lm[K0+t][i] X[K0+t][n] (K = W)

@@ -112,6 +112,7 @@ def _solve_tol(acc, exact, G, lam):
 SOLVE_CASES = [
     (256, 256, 400, "f64", 1e-2),
     (300, 130, 500, "f64", 0.3),     # ragged last block, rectangular right-hand side
+    (400, 130, 500, "f64", 0.3),     # short last pair in the backward's block inversion
     (512, 512, 1000, "f32", 0.1),
     (1000, 700, 1500, "f32", 0.5),
     (64, 64, 30, "f32", 1.0),        # single block, rank-deficient X
