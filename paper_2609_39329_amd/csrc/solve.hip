@@ -698,40 +698,44 @@ __global__ __launch_bounds__(diag_threads<T>()) void potrf_inv_kernel(T* A, int6
   }
 }
 
-// ---- fp32 diagonal block, blocked: 4 x 4 sub-blocks of 32 ----------------------------
+// ---- fp32 diagonal block, blocked: 8 x 8 sub-blocks of 16 ----------------------------
 //
 // The 128 x 128 block A (lower triangle read; zero-padded with an identity past bs)
-// and E = L^{-1} live in LDS. For each sub-block column k = 0..3:
+// and E = L^{-1} live in LDS. For each sub-block column k = 0..7:
 //   leaf (one wave):  A_kk = L_kk L_kk^T and X_kk = L_kk^{-1}, in registers;
 //   phase B:          L_ik = A_ik X_kk^T (i > k);  E_km = X_kk E_km (m < k);  E_kk = X_kk
 //   phase C:          A_ij -= L_ik L_jk^T (k < j <= i);  E_im -= L_ik E_km (i > k, m <= k)
 // i.e. right-looking blocked Cholesky with the forward substitution of the identity
-// carried along; phases B and C are independent 32 x 32 x 32 products on fp32 MFMA
-// (exact fp32 products), spread over eight waves, one barrier between phases. The
-// leaf of step k + 1 needs only the first product of phase C of step k (its own
-// diagonal block), so wave 0 does that product and then the leaf while the other
-// seven waves do the rest of phase C: the single-wave leaf, the longest serial part,
-// overlaps the trailing products.
+// carried along; phases B and C are independent 16 x 16 x 16 products on fp32 MFMA
+// 16x16x4 (exact fp32 products), spread over eight waves, one barrier between
+// phases. The leaf of step k + 1 needs only the first product of phase C of step k
+// (its own diagonal block), so wave 0 does that product and then the leaf while the
+// other seven waves do the rest of phase C: the single-wave leaf, the longest serial
+// part (its cost grows with the square of its width), overlaps the trailing products.
 constexpr int PB = 130;  // LDS pitch (floats): lane-per-row reads hit 64 distinct banks
 
-// D = sgn * P Q' (+ C), 32 x 32 blocks in LDS (pitch PB); Q' = Q^T if QT else Q.
-// One wave; D may alias P, Q or C (every operand is read before D is written).
+// D = sgn * P Q' (+ C), 16 x 16 blocks in LDS (pitch PB); Q' = Q^T if QT else Q.
+// One wave, MFMA 16x16x4 f32: lane l supplies row l % 16 of P and column l % 16 of
+// Q' at k = 4 ks + l / 16, and holds D[4 (l / 16) + e][l % 16]. D may alias P, Q or
+// C (every operand is read before D is written).
 template <bool QT>
-__device__ __forceinline__ void mm32(float* D, const float* P, const float* Q, const float* C, float sgn,
+__device__ __forceinline__ void mm16(float* D, const float* P, const float* Q, const float* C, float sgn,
                                      int lane) {
-  const int h = lane >> 5, l32 = lane & 31;
-  f32x16 acc;
+  const int g = lane >> 4, l16 = lane & 15;
+  f32x4 acc;
 #pragma unroll
-  for (int e = 0; e < 16; ++e) acc[e] = C ? C[(8 * (e >> 2) + 4 * h + (e & 3)) * PB + l32] : 0.f;
+  for (int e = 0; e < 4; ++e) acc[e] = C ? C[(4 * g + e) * PB + l16] : 0.f;
+  float a[4], b[4];
 #pragma unroll
-  for (int ks = 0; ks < 16; ++ks) {
-    const int k = 2 * ks + h;
-    const float a = sgn * P[l32 * PB + k];
-    const float b = QT ? Q[l32 * PB + k] : Q[k * PB + l32];
-    acc = mfma32_f32(a, b, acc);
+  for (int ks = 0; ks < 4; ++ks) {
+    const int k = 4 * ks + g;
+    a[ks] = sgn * P[l16 * PB + k];
+    b[ks] = QT ? Q[l16 * PB + k] : Q[k * PB + l16];
   }
 #pragma unroll
-  for (int e = 0; e < 16; ++e) D[(8 * (e >> 2) + 4 * h + (e & 3)) * PB + l32] = acc[e];
+  for (int ks = 0; ks < 4; ++ks) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[ks], b[ks], acc, 0, 0, 0);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) D[(4 * g + e) * PB + l16] = acc[e];
 }
 
 __device__ __forceinline__ float bcast(float x, int src_lane) {
@@ -748,36 +752,38 @@ __device__ __forceinline__ void static_for(F&& f) {
   static_for_impl(f, std::make_integer_sequence<int, N>{});
 }
 
-// One wave: factor the SPD 32 x 32 block S (lower triangle read) and write
+// One wave: factor the SPD N x N block S (lower triangle read) and write
 // X = L^{-1} (lower, zeros above) to Xo, in one right-looking sweep.
-// Lane r (and its twin r + 32, which repeats the same work so the wave never
-// diverges) holds row r of the trailing matrix (v) and row r of Y, the identity
+// Lane r (and its copies r + N, r + 2N, .., which repeat the same work so the wave
+// never diverges) holds row r of the trailing matrix (v) and row r of Y, the identity
 // under forward substitution (x). Step j, with pivot p = A_jj and u_r = A_rj / p for
 // rows r > j (0 otherwise):
 //   A_rc -= u_r A_cj     (c > j: column j of every lane, read through readlane)
 //   Y_rm -= u_r Y_jm     (m <= j: row j of Y, read from lane j)
 // and column j of L is A_rj / sqrt(p). Row r of X is row r of Y over L_rr, applied at
-// the end (Y's row r is final after step r - 1). Each step reads 32 values across
+// the end (Y's row r is final after step r - 1). Each step reads N values across
 // lanes, in groups of up to 8 held in distinct scalar registers, so that a readlane
 // is not directly followed by its consumer. A pivot that is not positive (or NaN)
 // makes its L_jj, and every later one, NaN: the first NaN on the diagonal is the
 // failing column.
-__device__ __forceinline__ void leaf32(float* S, float* Xo, int lane, int col0, int bs, int32_t* info,
-                                       bool& failed) {
-  int r = lane & 31;
+template <int N>
+__device__ __forceinline__ void leaf(float* S, float* Xo, int lane, int col0, int bs, int32_t* info,
+                                     bool& failed) {
+  static_assert(N == 16 || N == 32, "leaf width");
+  int r = lane & (N - 1);
   // opaque per call: keeps the per-step lane comparisons inside the call instead of
   // hoisting them into scalar registers for the whole kernel
   asm volatile("" : "+v"(r));
-  float v[32], x[32];
+  float v[N], x[N];
 #pragma unroll
-  for (int c = 0; c < 32; ++c) {
+  for (int c = 0; c < N; ++c) {
     v[c] = S[r * PB + c];
     x[c] = c == r ? 1.f : 0.f;
   }
   float rs_own = 0.f;
   // w[c0 .. c0+n) -= u * src(c), the n <= 8 values read first (the empty asm makes
   // them live at once, in distinct registers)
-  auto group = [&](float (&w)[32], auto c0_t, auto n_t, auto src, float u) {
+  auto group = [&](float (&w)[N], auto c0_t, auto n_t, auto src, float u) {
     constexpr int c0 = decltype(c0_t)::value, n = decltype(n_t)::value;
     float t[8];
 #pragma unroll
@@ -790,15 +796,15 @@ __device__ __forceinline__ void leaf32(float* S, float* Xo, int lane, int col0, 
     for (int q = 0; q < n; ++q) w[c0 + q] = fmaf(-u, t[q], w[c0 + q]);
     __builtin_amdgcn_sched_barrier(0);
   };
-  static_for<32>([&](auto j_t) {
+  static_for<N>([&](auto j_t) {
     constexpr int j = decltype(j_t)::value;
     const float rs = __builtin_amdgcn_rsqf(bcast(v[j], j));
     const float u = r > j ? v[j] * (rs * rs) : 0.f;  // A[r][j] / p
     if (r == j) rs_own = rs;
-    // A_rc -= u_r A_cj, c = j+1..31 (A_cj is lane c's v[j])
-    static_for<(31 - j + 7) / 8>([&](auto g_t) {
+    // A_rc -= u_r A_cj, c = j+1..N-1 (A_cj is lane c's v[j])
+    static_for<(N - 1 - j + 7) / 8>([&](auto g_t) {
       constexpr int c0 = j + 1 + 8 * decltype(g_t)::value;
-      constexpr int n = 32 - c0 < 8 ? 32 - c0 : 8;
+      constexpr int n = N - c0 < 8 ? N - c0 : 8;
       group(v, std::integral_constant<int, c0>{}, std::integral_constant<int, n>{},
             [&](int c) { return bcast(v[j], c); }, u);
     });
@@ -814,16 +820,16 @@ __device__ __forceinline__ void leaf32(float* S, float* Xo, int lane, int col0, 
   // first failing pivot of this block (padding pivots past bs are 1)
   float diag = 0.f;
 #pragma unroll
-  for (int c = 0; c < 32; ++c)
+  for (int c = 0; c < N; ++c)
     if (c == r) diag = v[c];
-  const uint64_t bad = __ballot(lane < 32 && col0 + r < bs && !(diag > 0.f));
+  const uint64_t bad = __ballot(lane < N && col0 + r < bs && !(diag > 0.f));
   if (bad != 0 && !failed) {
     failed = true;
     if (lane == 0 && *info == 0) *info = col0 + __builtin_ctzll(bad) + 1;
   }
-  if (lane < 32) {
+  if (lane < N) {
 #pragma unroll
-    for (int c = 0; c < 32; ++c) {
+    for (int c = 0; c < N; ++c) {
       S[r * PB + c] = v[c];            // row r of L (upper part unused)
       Xo[r * PB + c] = x[c] * rs_own;  // row r of X (zeros above the diagonal)
     }
@@ -831,6 +837,7 @@ __device__ __forceinline__ void leaf32(float* S, float* Xo, int lane, int col0, 
 }
 
 constexpr int kPotrfWaves = 8;  // 8 waves: the next leaf overlaps the trailing products
+constexpr int kLeaf = 16, kLeaves = 128 / kLeaf;  // leaf width, block steps
 __global__ __launch_bounds__(64 * kPotrfWaves) void potrf128_kernel(float* A, int64_t lda, int kb, int bs,
                                                                    int32_t* info) {
   constexpr int NT = 64 * kPotrfWaves, NL = 128 * 128 / 4 / NT;  // 16-byte chunks per thread
@@ -863,38 +870,38 @@ __global__ __launch_bounds__(64 * kPotrfWaves) void potrf128_kernel(float* A, in
       const int i = e >> 7, j0 = e & 127;
       *(f32x2*)&As[i * PB + j0] = f32x2{buf[u][0], buf[u][1]};
       *(f32x2*)&As[i * PB + j0 + 2] = f32x2{buf[u][2], buf[u][3]};
-      // E = L^{-1} starts at zero in its strictly lower 32 x 32 blocks (the diagonal
+      // E = L^{-1} starts at zero in its strictly lower kLeaf-blocks (the diagonal
       // blocks are written whole by the leaf; the upper ones are never read)
-      if ((i >> 5) > (j0 >> 5)) {
+      if (i / kLeaf > j0 / kLeaf) {
         *(f32x2*)&Es[i * PB + j0] = f32x2{0.f, 0.f};
         *(f32x2*)&Es[i * PB + j0 + 2] = f32x2{0.f, 0.f};
       }
     }
   }
   __syncthreads();
-  auto blk = [](float* base, int i, int j) { return base + (32 * i) * PB + 32 * j; };
+  auto blk = [](float* base, int i, int j) { return base + (kLeaf * i) * PB + kLeaf * j; };
   bool failed = false;
-  if (wid == 0) leaf32(blk(As, 0, 0), blk(Es, 0, 0), lane, kb, kb + bs, info, failed);
+  if (wid == 0) leaf<kLeaf>(blk(As, 0, 0), blk(Es, 0, 0), lane, kb, kb + bs, info, failed);
   __syncthreads();
-  for (int k = 0; k < 4; ++k) {
-    // phase B: (3 - k) panel products, k products of the identity's row block k
-    if (wid < 3) {
-      const int q = wid;
-      if (q < 3 - k) {
+  constexpr int NL1 = kLeaves - 1;
+  for (int k = 0; k < kLeaves; ++k) {
+    // phase B: (NL1 - k) panel products, k products of the identity's row block k
+    for (int q = wid; q < NL1; q += kPotrfWaves) {
+      if (q < NL1 - k) {
         const int i = k + 1 + q;
-        mm32<true>(blk(As, i, k), blk(As, i, k), blk(Es, k, k), nullptr, 1.f, lane);
+        mm16<true>(blk(As, i, k), blk(As, i, k), blk(Es, k, k), nullptr, 1.f, lane);
       } else {
-        const int m = q - (3 - k);
-        mm32<false>(blk(Es, k, m), blk(Es, k, k), blk(Es, k, m), nullptr, 1.f, lane);
+        const int m = q - (NL1 - k);
+        mm16<false>(blk(Es, k, m), blk(Es, k, k), blk(Es, k, m), nullptr, 1.f, lane);
       }
     }
     __syncthreads();
-    if (k == 3) break;
+    if (k == NL1) break;
     // phase C: trailing lower blocks (k < j <= i), then E_im for i > k, m <= k. Job 0
     // is the next diagonal block: wave 0 updates it and factors it (the next leaf)
     // while the other waves share the remaining jobs.
-    const int ntr = (3 - k) * (4 - k) / 2;
-    const int njobs = ntr + (3 - k) * (k + 1);
+    const int ntr = (NL1 - k) * (NL1 - k + 1) / 2;
+    const int njobs = ntr + (NL1 - k) * (k + 1);
     auto job = [&](int q) {
       if (q < ntr) {
         int i = k + 1, t = q;
@@ -903,17 +910,17 @@ __global__ __launch_bounds__(64 * kPotrfWaves) void potrf128_kernel(float* A, in
           ++i;
         }
         const int j = k + 1 + t;
-        mm32<true>(blk(As, i, j), blk(As, i, k), blk(As, j, k), blk(As, i, j), -1.f, lane);
+        mm16<true>(blk(As, i, j), blk(As, i, k), blk(As, j, k), blk(As, i, j), -1.f, lane);
       } else {
         const int t = q - ntr;
         const int i = k + 1 + t / (k + 1), m = t % (k + 1);
-        mm32<false>(blk(Es, i, m), blk(As, i, k), blk(Es, k, m), blk(Es, i, m), -1.f, lane);
+        mm16<false>(blk(Es, i, m), blk(As, i, k), blk(Es, k, m), blk(Es, i, m), -1.f, lane);
       }
     };
     if (wid == 0) {
       job(0);
-      leaf32(blk(As, k + 1, k + 1), blk(Es, k + 1, k + 1), lane, kb + 32 * (k + 1), kb + bs, info,
-             failed);
+      leaf<kLeaf>(blk(As, k + 1, k + 1), blk(Es, k + 1, k + 1), lane, kb + kLeaf * (k + 1), kb + bs,
+                  info, failed);
     } else {
       for (int q = wid; q < njobs; q += kPotrfWaves - 1) job(q);
     }
