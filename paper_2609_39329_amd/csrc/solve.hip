@@ -6,7 +6,7 @@
 //     diagonal kernel    L_kk^{-1} (1 WG)
 //     grouped GEMM       L_ik = A_ik L_kk^{-T} (i > k);  Z_k = L_kk^{-1} R_k
 //     grouped GEMM       A_ij -= L_ik L_jk^T (lower blocks);  R_i -= L_ik Z_k (i > k)
-// The updates outside a group of four block columns (an outer block, OB = 4 NB) are
+// The updates outside a group of eight block columns (an outer block, OB = 8 NB) are
 // deferred to the end of the group (K = OB), see solve_t. Backward substitution runs
 // per outer block: X_O = L_OO^{-T} Z_O;  Z_i -= L_Oi^T X_O (i before O).
 // Triangular solves against a diagonal block use that block's explicit inverse (a
@@ -1152,8 +1152,9 @@ hipError_t run_group_split(const GemmDesc<float>* ds, int n, hipStream_t st) {
   return hipGetLastError();
 }
 
-// Column blocks of NB are grouped into outer blocks of kSolveNBO * NB (512 wide in fp32)
-constexpr int kSolveNBO = 4;
+// Column blocks of NB are grouped into outer blocks of kSolveNBO * NB (1024 wide in fp32;
+// solve at d = 4096: 2.46 ms, 4 column blocks: 2.53, 16: 2.59)
+constexpr int kSolveNBO = 8;
 
 struct SolveLayout {
   size_t A, Lm, R, Z, X, Tw, part, lam, total;
