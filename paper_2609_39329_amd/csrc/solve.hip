@@ -1507,65 +1507,93 @@ __global__ __launch_bounds__(256) void rrr_init_kernel(float* Q, int64_t rows, i
   Q[e] = (float)(h >> 8) * (2.0f / 16777216.0f) - 1.0f;
 }
 
+// 1 / x and 1 / sqrt(x) in fp64: the native approximations and one Newton step each
+__device__ __forceinline__ double rcp64(double x) {
+  const double r = __builtin_amdgcn_rcp(x);
+  return fma(r, fma(-x, r, 1.0), r);
+}
+__device__ __forceinline__ double rsq64(double x) {
+  const double r = __builtin_amdgcn_rsq(x);
+  return fma(0.5 * r, fma(-x * r, r, 1.0), r);
+}
+
 // Eigenvectors of the symmetric b x b matrix (T + T^T) / 2 (b even, <= kRrrBlock) by
-// parallel cyclic Jacobi in fp64: each step rotates b/2 disjoint index pairs of a
-// round-robin schedule, columns then rows. Vr [b][r] receives the eigenvectors of the
-// r largest eigenvalues, in descending order (ties: lower index first); w [b] all
-// eigenvalues by index.
+// parallel cyclic Jacobi in fp64: each step rotates NB/2 disjoint index pairs of a
+// round-robin schedule, columns then rows. The matrix is padded with zeros to
+// NB = kRrrBlock (a padded index never couples, so its rotations are the identity,
+// and it never enters the ranking), so all index arithmetic is compile-time. Thread
+// tid takes row (column update) or column (row update) tid % 64 of pairs tid / 64 + 4u:
+// the lanes of a wave read one pair's entries down a column or along a row, which
+// spreads them over the LDS banks. Vr [b][r] receives the
+// eigenvectors of the r largest eigenvalues, in descending order (ties: lower index
+// first); w [b] all eigenvalues by index.
 __global__ __launch_bounds__(256) void jacobi_top_kernel(const double* __restrict__ T, int b, int r,
                                                          float* __restrict__ Vr,
                                                          double* __restrict__ w) {
-  constexpr int NB = kRrrBlock, P = NB + 1;
+  constexpr int NB = kRrrBlock, P = NB + 1, HALF = NB / 2;
+  static_assert(NB == 64, "thread mapping assumes a 64-wide block and 256 threads");
   __shared__ double A[NB * P], V[NB * P];
-  __shared__ double cs[NB / 2][2];
-  __shared__ int pq[NB / 2][2];
+  __shared__ double cs[HALF][2];
+  __shared__ int pq[HALF][2];
+  __shared__ double red[2][256];
+  __shared__ int done;
   const int tid = threadIdx.x;
-  for (int e = tid; e < b * b; e += 256) {
-    const int i = e / b, j = e % b;
-    A[i * P + j] = 0.5 * (T[i * b + j] + T[j * b + i]);
+  for (int e = tid; e < NB * NB; e += 256) {
+    const int i = e / NB, j = e % NB;
+    double a = 0.0;
+    if (i < b && j < b) a = 0.5 * (T[i * b + j] + T[j * b + i]);
+    A[i * P + j] = a;
     V[i * P + j] = i == j ? 1.0 : 0.0;
   }
   __syncthreads();
-  const int half = b / 2;
-  __shared__ double red[256];
-  __shared__ int done;
+  const int kk = tid % NB, t0 = tid / NB;  // this thread's row / column and first pair
   for (int sweep = 0; sweep < kJacobiSweeps; ++sweep) {
-    // stop once the off-diagonal mass is below 1e-30 of the diagonal's (fp64 rounding)
+    // stop once the off-diagonal mass is below 1e-24 of the diagonal's: an eigenvector
+    // is then off by about 1e-12 ||A|| / gap, far below the fp32 output's precision
     double off = 0.0, dia = 0.0;
-    for (int e = tid; e < b * b; e += 256) {
-      const int i = e / b, j = e % b;
+    for (int e = tid; e < NB * NB; e += 256) {
+      const int i = e / NB, j = e % NB;
+      if (i >= b || j >= b) continue;
       const double v = A[i * P + j] * A[i * P + j];
       if (i == j) dia += v; else off += v;
     }
-    red[tid] = off;
+    red[0][tid] = off;
+    red[1][tid] = dia;
     __syncthreads();
     for (int s2 = 128; s2 > 0; s2 >>= 1) {
-      if (tid < s2) red[tid] += red[tid + s2];
+      if (tid < s2) {
+        red[0][tid] += red[0][tid + s2];
+        red[1][tid] += red[1][tid + s2];
+      }
       __syncthreads();
     }
-    const double off_all = red[0];
-    __syncthreads();
-    red[tid] = dia;
-    __syncthreads();
-    for (int s2 = 128; s2 > 0; s2 >>= 1) {
-      if (tid < s2) red[tid] += red[tid + s2];
-      __syncthreads();
-    }
-    if (tid == 0) done = off_all <= 1e-30 * red[0];
+    if (tid == 0) done = red[0][0] <= 1e-24 * red[1][0];
     __syncthreads();
     if (done) break;
-    for (int step = 0; step < b - 1; ++step) {
-      if (tid < half) {
+#pragma unroll 1
+    for (int step = 0; step < NB - 1; ++step) {
+      if (tid < HALF) {
         // round robin: position 0 fixed, the others rotate by `step`
-        auto at = [&](int k) { return k == 0 ? 0 : (k - 1 + step) % (b - 1) + 1; };
-        int p = at(tid), q = at(b - 1 - tid);
+        auto at = [&](int k) { return k == 0 ? 0 : (k - 1 + step) % (NB - 1) + 1; };
+        int p = at(tid), q = at(NB - 1 - tid);
         if (p > q) { const int t = p; p = q; q = t; }
         const double apq = A[p * P + q];
         double c = 1.0, s = 0.0;
         if (fabs(apq) > 1e-300) {
-          const double th = (A[q * P + q] - A[p * P + p]) / (2.0 * apq);
-          const double t = (th >= 0.0 ? 1.0 : -1.0) / (fabs(th) + sqrt(th * th + 1.0));
-          c = 1.0 / sqrt(t * t + 1.0);
+          // t = tan of the rotation angle, the root of t^2 + 2 th t - 1 of smaller
+          // magnitude; native fp64 reciprocal and reciprocal square root, each with one
+          // Newton step, so that c^2 + s^2 = 1 to fp64 rounding
+          const double th = (A[q * P + q] - A[p * P + p]) * rcp64(2.0 * apq);
+          const double ath = fabs(th);
+          double t;
+          if (ath < 1e150) {
+            const double y = fma(th, th, 1.0);
+            t = rcp64(ath + y * rsq64(y));
+          } else {
+            t = 0.5 * rcp64(ath);
+          }
+          if (th < 0.0) t = -t;
+          c = rsq64(fma(t, t, 1.0));
           s = t * c;
         }
         pq[tid][0] = p;
@@ -1574,27 +1602,38 @@ __global__ __launch_bounds__(256) void jacobi_top_kernel(const double* __restric
         cs[tid][1] = s;
       }
       __syncthreads();
+      // this thread's 8 pairs, read once for both halves of the step
+      int pp[HALF / 4], qq[HALF / 4];
+      double cc[HALF / 4], ss[HALF / 4];
+#pragma unroll
+      for (int u = 0; u < HALF / 4; ++u) {
+        const int t = t0 + 4 * u;
+        pp[u] = pq[t][0];
+        qq[u] = pq[t][1];
+        cc[u] = cs[t][0];
+        ss[u] = cs[t][1];
+      }
       // columns: A <- A J, V <- V J
-      for (int e = tid; e < b * half; e += 256) {
-        const int k = e / half, t = e % half;
-        const int p = pq[t][0], q = pq[t][1];
-        const double c = cs[t][0], s = cs[t][1];
-        const double akp = A[k * P + p], akq = A[k * P + q];
-        A[k * P + p] = c * akp - s * akq;
-        A[k * P + q] = s * akp + c * akq;
-        const double vkp = V[k * P + p], vkq = V[k * P + q];
-        V[k * P + p] = c * vkp - s * vkq;
-        V[k * P + q] = s * vkp + c * vkq;
+#pragma unroll
+      for (int u = 0; u < HALF / 4; ++u) {
+        const int p = pp[u], q = qq[u];
+        const double c = cc[u], s = ss[u];
+        const double akp = A[kk * P + p], akq = A[kk * P + q];
+        A[kk * P + p] = c * akp - s * akq;
+        A[kk * P + q] = s * akp + c * akq;
+        const double vkp = V[kk * P + p], vkq = V[kk * P + q];
+        V[kk * P + p] = c * vkp - s * vkq;
+        V[kk * P + q] = s * vkp + c * vkq;
       }
       __syncthreads();
       // rows: A <- J^T A
-      for (int e = tid; e < b * half; e += 256) {
-        const int k = e / half, t = e % half;
-        const int p = pq[t][0], q = pq[t][1];
-        const double c = cs[t][0], s = cs[t][1];
-        const double apk = A[p * P + k], aqk = A[q * P + k];
-        A[p * P + k] = c * apk - s * aqk;
-        A[q * P + k] = s * apk + c * aqk;
+#pragma unroll
+      for (int u = 0; u < HALF / 4; ++u) {
+        const int p = pp[u], q = qq[u];
+        const double c = cc[u], s = ss[u];
+        const double apk = A[p * P + kk], aqk = A[q * P + kk];
+        A[p * P + kk] = c * apk - s * aqk;
+        A[q * P + kk] = s * apk + c * aqk;
       }
       __syncthreads();
     }
