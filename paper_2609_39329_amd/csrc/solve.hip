@@ -36,14 +36,8 @@ struct Blk<float> {
 };
 template <>
 struct Blk<double> {
-  static constexpr int NB = 64, TS = 4;
+  static constexpr int NB = 64;
 };
-// threads of the diagonal kernel: one per TS x TS tile of the lower triangle
-template <class T>
-constexpr int diag_threads() {
-  constexpr int NT = Blk<T>::NB / Blk<T>::TS;
-  return (NT * (NT + 1) / 2 + 63) / 64 * 64;
-}
 
 constexpr int kRedBlocks = 1024;  // workgroups of the adaptive-ridge reduction
 
@@ -513,234 +507,87 @@ __global__ __launch_bounds__(256) void gemm_f64_kernel(GemmDesc<double> d0, Gemm
   }
 }
 
-// ---- diagonal block: Cholesky factor and its inverse, in registers ---------------
+// ---- diagonal block, blocked: sub-blocks of 16 ----------------------------------------
 //
-// The NB x NB lower triangle is split into TS x TS tiles, one per thread (thread
-// (ti, tj), tj <= ti). Step j of the right-looking factorisation publishes the
-// unscaled column u = A[j:, j] (pivot p = u_j) through LDS; after one barrier every
-// thread updates its tile with A_rc -= u_r u_c / p (= L_rj L_cj) and the owners of
-// column j keep L_rj = u_r / sqrt(p). The inverse X = L^{-1} is formed in the same
-// sweep, one step behind, by right-looking forward substitution on X = I: row j-1
-// of X (final) updates rows >= j with L's column j-1, and row j becomes final and
-// is scaled by 1/L_jj. One barrier per step; three column buffers and two row
-// buffers make every LDS slot's readers finish before it is rewritten.
-template <class T>
-__global__ __launch_bounds__(diag_threads<T>()) void potrf_inv_kernel(T* A, int64_t lda, int kb, int bs,
-                                                        int32_t* info) {
-  constexpr int NB = Blk<T>::NB, TS = Blk<T>::TS, NT = NB / TS;
-  constexpr int NTILES = NT * (NT + 1) / 2;
-  __shared__ T cb[3][NB];
-  __shared__ T rb[2][NB];
-  const int tid = threadIdx.x;
-  const bool own = tid < NTILES;
-  int ti = 0, tj = 0;
-  {
-    int rem = own ? tid : 0;
-    while (rem >= ti + 1) {
-      rem -= ti + 1;
-      ++ti;
-    }
-    tj = rem;
-  }
-  const int r0 = ti * TS, c0 = tj * TS;
-
-  T a[TS][TS], x[TS][TS];
-#pragma unroll
-  for (int r = 0; r < TS; ++r)
-#pragma unroll
-    for (int c = 0; c < TS; ++c) {
-      const int gi = r0 + r, gj = c0 + c;
-      T v = gi == gj ? T(1) : T(0);
-      if (own && gi < bs && gj < bs) v = gj <= gi ? A[(int64_t)(kb + gi) * lda + kb + gj] : T(0);
-      a[r][c] = v;
-      x[r][c] = gi == gj ? T(1) : T(0);
-    }
-
-  // publish column 0
-  if (own && tj == 0) {
-#pragma unroll
-    for (int r = 0; r < TS; ++r) cb[0][r0 + r] = a[r][0];
-  }
-  __syncthreads();
-
-  bool failed = false;
-  T inv_d_prev = T(0);
-  int s = 0;  // j % 3
-  for (int jb = 0; jb < NT; ++jb) {
-#pragma unroll
-    for (int jj = 0; jj < TS; ++jj) {
-      const int j = jb * TS + jj;
-      const T* u = cb[s];
-      const T* up = cb[s == 0 ? 2 : s - 1];
-      const T p = u[j];
-      if (tid == 0 && !failed && j < bs && !(p > T(0))) {
-        failed = true;
-        if (*info == 0) *info = kb + j + 1;
-      }
-      T inv_d;
-      if constexpr (sizeof(T) == 4) inv_d = __builtin_amdgcn_rsqf(p);  // v_rsq_f32, about 1 ulp
-      else inv_d = T(1) / sqrt(p);
-      const T inv_p = inv_d * inv_d;
-      if (own) {
-        // (a) factorisation: finish column j, update the trailing lower triangle.
-        // jj is a compile-time constant here, so every mask below is too; only the
-        // tile position (ti, tj) relative to jb is tested at run time.
-        if (tj == jb) {
-#pragma unroll
-          for (int r = 0; r < TS; ++r)
-            if (ti > jb || r >= jj) a[r][jj] = a[r][jj] * inv_d;
-        }
-        if (tj >= jb) {
-          T ur[TS], uc[TS];
-#pragma unroll
-          for (int r = 0; r < TS; ++r) ur[r] = u[r0 + r];
-#pragma unroll
-          for (int c = 0; c < TS; ++c) uc[c] = u[c0 + c] * inv_p;
-          if (tj > jb) {
-            if (ti > tj) {
-#pragma unroll
-              for (int r = 0; r < TS; ++r)
-#pragma unroll
-                for (int c = 0; c < TS; ++c) a[r][c] -= ur[r] * uc[c];
-            } else {
-#pragma unroll
-              for (int r = 0; r < TS; ++r)
-#pragma unroll
-                for (int c = 0; c <= r; ++c) a[r][c] -= ur[r] * uc[c];
-            }
-          } else if (ti > tj) {
-#pragma unroll
-            for (int r = 0; r < TS; ++r)
-#pragma unroll
-              for (int c = jj + 1; c < TS; ++c) a[r][c] -= ur[r] * uc[c];
-          } else {
-#pragma unroll
-            for (int r = jj + 1; r < TS; ++r)
-#pragma unroll
-              for (int c = jj + 1; c <= r; ++c) a[r][c] -= ur[r] * uc[c];
-          }
-        }
-        // (b) inverse: row j-1 of X updates rows >= j through L's column j-1:
-        // x[r][c] -= L[r][j-1] X[j-1][c] for global rows >= j, columns <= j-1
-        if (j > 0 && ti >= jb && tj <= (j - 1) / TS) {
-          const T* xr = rb[(j - 1) & 1];
-          T lr[TS], xc[TS];
-#pragma unroll
-          for (int r = 0; r < TS; ++r) lr[r] = up[r0 + r] * inv_d_prev;
-#pragma unroll
-          for (int c = 0; c < TS; ++c) xc[c] = xr[c0 + c];
-          // rows: all when ti > jb, else r >= jj; columns: all when tj*TS + TS-1 <= j-1,
-          // else (tj == jb, jj >= 1) c <= jj-1
-          const bool all_rows = ti > jb;
-          const bool all_cols = tj < jb;
-          if (all_rows && all_cols) {
-#pragma unroll
-            for (int r = 0; r < TS; ++r)
-#pragma unroll
-              for (int c = 0; c < TS; ++c) x[r][c] -= lr[r] * xc[c];
-          } else if (all_rows) {
-#pragma unroll
-            for (int r = 0; r < TS; ++r)
-#pragma unroll
-              for (int c = 0; c < jj; ++c) x[r][c] -= lr[r] * xc[c];
-          } else if (all_cols) {
-#pragma unroll
-            for (int r = jj; r < TS; ++r)
-#pragma unroll
-              for (int c = 0; c < TS; ++c) x[r][c] -= lr[r] * xc[c];
-          } else {
-#pragma unroll
-            for (int r = jj; r < TS; ++r)
-#pragma unroll
-              for (int c = 0; c < jj; ++c) x[r][c] -= lr[r] * xc[c];
-          }
-        }
-        // (c) row j of X is final: scale by 1/L_jj and publish (columns <= j)
-        if (ti == jb) {
-#pragma unroll
-          for (int c = 0; c < TS; ++c)
-            if (tj < jb || c <= jj) {
-              x[jj][c] *= inv_d;
-              rb[j & 1][c0 + c] = x[jj][c];
-            }
-        }
-        // publish the (updated, unscaled) column j+1
-        if (j + 1 < NB) {
-          const int jn = (jj + 1) % TS;
-          const int jbn = jj + 1 == TS ? jb + 1 : jb;
-          if (tj == jbn) {
-            T* un = cb[s == 2 ? 0 : s + 1];
-#pragma unroll
-            for (int r = 0; r < TS; ++r)
-              if (ti > jbn || r >= jn) un[r0 + r] = a[r][jn];
-          }
-        }
-      }
-      inv_d_prev = inv_d;
-      s = s == 2 ? 0 : s + 1;
-      __syncthreads();
-    }
-  }
-
-  // write L^{-1} (lower triangle, zeros above) over the diagonal block
-  if (own) {
-#pragma unroll
-    for (int r = 0; r < TS; ++r)
-#pragma unroll
-      for (int c = 0; c < TS; ++c) {
-        const int gi = r0 + r, gj = c0 + c;
-        if (gi < bs && gj < bs) A[(int64_t)(kb + gi) * lda + kb + gj] = gj <= gi ? x[r][c] : T(0);
-      }
-  }
-  for (int e = tid; e < NB * NB; e += blockDim.x) {
-    const int gi = e / NB, gj = e % NB;
-    if (gj / TS > gi / TS && gi < bs && gj < bs) A[(int64_t)(kb + gi) * lda + kb + gj] = T(0);
-  }
-}
-
-// ---- fp32 diagonal block, blocked: 8 x 8 sub-blocks of 16 ----------------------------
-//
-// The 128 x 128 block A (lower triangle read; zero-padded with an identity past bs)
-// and E = L^{-1} live in LDS. For each sub-block column k = 0..7:
+// The NB x NB block A (128 fp32 or 64 fp64; lower triangle read; zero-padded with an
+// identity past bs) and E = L^{-1} live in LDS. For each sub-block column k:
 //   leaf (one wave):  A_kk = L_kk L_kk^T and X_kk = L_kk^{-1}, in registers;
 //   phase B:          L_ik = A_ik X_kk^T (i > k);  E_km = X_kk E_km (m < k);  E_kk = X_kk
 //   phase C:          A_ij -= L_ik L_jk^T (k < j <= i);  E_im -= L_ik E_km (i > k, m <= k)
 // i.e. right-looking blocked Cholesky with the forward substitution of the identity
-// carried along; phases B and C are independent 16 x 16 x 16 products on fp32 MFMA
-// 16x16x4 (exact fp32 products), spread over eight waves, one barrier between
-// phases. The leaf of step k + 1 needs only the first product of phase C of step k
-// (its own diagonal block), so wave 0 does that product and then the leaf while the
-// other seven waves do the rest of phase C: the single-wave leaf, the longest serial
-// part (its cost grows with the square of its width), overlaps the trailing products.
-constexpr int PB = 130;  // LDS pitch (floats): lane-per-row reads hit 64 distinct banks
+// carried along; phases B and C are independent 16 x 16 x 16 products (fp32: MFMA
+// 16x16x4 with exact fp32 products; fp64: fp64 FMA), spread over eight waves, one
+// barrier between phases. The leaf of step k + 1 needs only the first product of
+// phase C of step k (its own diagonal block), so wave 0 does that product and then
+// the leaf while the other seven waves do the rest of phase C: the single-wave leaf,
+// the longest serial part (its cost grows with the square of its width), overlaps
+// the trailing products.
 
-// D = sgn * P Q' (+ C), 16 x 16 blocks in LDS (pitch PB); Q' = Q^T if QT else Q.
-// One wave, MFMA 16x16x4 f32: lane l supplies row l % 16 of P and column l % 16 of
-// Q' at k = 4 ks + l / 16, and holds D[4 (l / 16) + e][l % 16]. D may alias P, Q or
-// C (every operand is read before D is written).
-template <bool QT>
-__device__ __forceinline__ void mm16(float* D, const float* P, const float* Q, const float* C, float sgn,
-                                     int lane) {
+// LDS pitch (elements): lane-per-row reads of one column hit distinct banks
+template <class T>
+constexpr int diag_pitch() { return Blk<T>::NB + 2; }
+
+// 1 / x and 1 / sqrt(x) in fp64: the native approximations and one Newton step each
+__device__ __forceinline__ double rcp64(double x) {
+  const double r = __builtin_amdgcn_rcp(x);
+  return fma(r, fma(-x, r, 1.0), r);
+}
+__device__ __forceinline__ double rsq64(double x) {
+  const double r = __builtin_amdgcn_rsq(x);
+  return fma(0.5 * r, fma(-x * r, r, 1.0), r);
+}
+
+// D = sgn * P Q' (+ C), 16 x 16 blocks in LDS (pitch PT); Q' = Q^T if QT else Q. One
+// wave; lane l holds D[4 (l / 16) + e][l % 16]. fp32: MFMA 16x16x4, lane l supplying
+// row l % 16 of P and column l % 16 of Q' at k = 4 ks + l / 16; fp64: FMA over k in
+// order. D may alias P, Q or C (every operand is read before D is written).
+template <bool QT, class T>
+__device__ __forceinline__ void mm16(T* D, const T* P, const T* Q, const T* C, T sgn, int lane) {
+  constexpr int PT = diag_pitch<T>();
   const int g = lane >> 4, l16 = lane & 15;
-  f32x4 acc;
+  if constexpr (sizeof(T) == 4) {
+    f32x4 acc;
 #pragma unroll
-  for (int e = 0; e < 4; ++e) acc[e] = C ? C[(4 * g + e) * PB + l16] : 0.f;
-  float a[4], b[4];
+    for (int e = 0; e < 4; ++e) acc[e] = C ? C[(4 * g + e) * PT + l16] : 0.f;
+    float a[4], b[4];
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks) {
-    const int k = 4 * ks + g;
-    a[ks] = sgn * P[l16 * PB + k];
-    b[ks] = QT ? Q[l16 * PB + k] : Q[k * PB + l16];
+    for (int ks = 0; ks < 4; ++ks) {
+      const int k = 4 * ks + g;
+      a[ks] = sgn * P[l16 * PT + k];
+      b[ks] = QT ? Q[l16 * PT + k] : Q[k * PT + l16];
+    }
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[ks], b[ks], acc, 0, 0, 0);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) D[(4 * g + e) * PT + l16] = acc[e];
+  } else {
+    T acc[4], q[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) q[k] = QT ? Q[l16 * PT + k] : Q[k * PT + l16];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const T* prow = P + (4 * g + e) * PT;
+      T a = 0;
+#pragma unroll
+      for (int k = 0; k < 16; ++k) a = fma(prow[k], q[k], a);
+      acc[e] = C ? fma(sgn, a, C[(4 * g + e) * PT + l16]) : sgn * a;
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) D[(4 * g + e) * PT + l16] = acc[e];
   }
-#pragma unroll
-  for (int ks = 0; ks < 4; ++ks) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[ks], b[ks], acc, 0, 0, 0);
-#pragma unroll
-  for (int e = 0; e < 4; ++e) D[(4 * g + e) * PB + l16] = acc[e];
 }
 
 __device__ __forceinline__ float bcast(float x, int src_lane) {
   return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), src_lane));
 }
+__device__ __forceinline__ double bcast(double x, int src_lane) {
+  const u32x2 w = __builtin_bit_cast(u32x2, x);
+  const u32x2 r = {(unsigned)__builtin_amdgcn_readlane((int)w[0], src_lane),
+                   (unsigned)__builtin_amdgcn_readlane((int)w[1], src_lane)};
+  return __builtin_bit_cast(double, r);
+}
+__device__ __forceinline__ float rsq_of(float x) { return __builtin_amdgcn_rsqf(x); }
+__device__ __forceinline__ double rsq_of(double x) { return rsq64(x); }
 
 // f(integral_constant<int, I>) for I = 0..N-1, unrolled at compile time
 template <class F, int... I>
@@ -766,26 +613,27 @@ __device__ __forceinline__ void static_for(F&& f) {
 // is not directly followed by its consumer. A pivot that is not positive (or NaN)
 // makes its L_jj, and every later one, NaN: the first NaN on the diagonal is the
 // failing column.
-template <int N>
-__device__ __forceinline__ void leaf(float* S, float* Xo, int lane, int col0, int bs, int32_t* info,
+template <int N, class T>
+__device__ __forceinline__ void leaf(T* S, T* Xo, int lane, int col0, int bs, int32_t* info,
                                      bool& failed) {
   static_assert(N == 16 || N == 32, "leaf width");
+  constexpr int PT = diag_pitch<T>();
   int r = lane & (N - 1);
   // opaque per call: keeps the per-step lane comparisons inside the call instead of
   // hoisting them into scalar registers for the whole kernel
   asm volatile("" : "+v"(r));
-  float v[N], x[N];
+  T v[N], x[N];
 #pragma unroll
   for (int c = 0; c < N; ++c) {
-    v[c] = S[r * PB + c];
-    x[c] = c == r ? 1.f : 0.f;
+    v[c] = S[r * PT + c];
+    x[c] = c == r ? T(1) : T(0);
   }
-  float rs_own = 0.f;
+  T rs_own = 0;
   // w[c0 .. c0+n) -= u * src(c), the n <= 8 values read first (the empty asm makes
   // them live at once, in distinct registers)
-  auto group = [&](float (&w)[N], auto c0_t, auto n_t, auto src, float u) {
+  auto group = [&](T (&w)[N], auto c0_t, auto n_t, auto src, T u) {
     constexpr int c0 = decltype(c0_t)::value, n = decltype(n_t)::value;
-    float t[8];
+    T t[8];
 #pragma unroll
     for (int q = 0; q < n; ++q) t[q] = src(c0 + q);
 #pragma unroll
@@ -793,13 +641,13 @@ __device__ __forceinline__ void leaf(float* S, float* Xo, int lane, int col0, in
     asm volatile("" ::"s"(t[0]), "s"(t[1]), "s"(t[2]), "s"(t[3]), "s"(t[4]), "s"(t[5]), "s"(t[6]),
                  "s"(t[7]));
 #pragma unroll
-    for (int q = 0; q < n; ++q) w[c0 + q] = fmaf(-u, t[q], w[c0 + q]);
+    for (int q = 0; q < n; ++q) w[c0 + q] = fma(-u, t[q], w[c0 + q]);
     __builtin_amdgcn_sched_barrier(0);
   };
   static_for<N>([&](auto j_t) {
     constexpr int j = decltype(j_t)::value;
-    const float rs = __builtin_amdgcn_rsqf(bcast(v[j], j));
-    const float u = r > j ? v[j] * (rs * rs) : 0.f;  // A[r][j] / p
+    const T rs = rsq_of(bcast(v[j], j));
+    const T u = r > j ? v[j] * (rs * rs) : T(0);  // A[r][j] / p
     if (r == j) rs_own = rs;
     // A_rc -= u_r A_cj, c = j+1..N-1 (A_cj is lane c's v[j])
     static_for<(N - 1 - j + 7) / 8>([&](auto g_t) {
@@ -818,11 +666,11 @@ __device__ __forceinline__ void leaf(float* S, float* Xo, int lane, int col0, in
     v[j] *= rs;
   });
   // first failing pivot of this block (padding pivots past bs are 1)
-  float diag = 0.f;
+  T diag = 0;
 #pragma unroll
   for (int c = 0; c < N; ++c)
     if (c == r) diag = v[c];
-  const uint64_t bad = __ballot(lane < N && col0 + r < bs && !(diag > 0.f));
+  const uint64_t bad = __ballot(lane < N && col0 + r < bs && !(diag > T(0)));
   if (bad != 0 && !failed) {
     failed = true;
     if (lane == 0 && *info == 0) *info = col0 + __builtin_ctzll(bad) + 1;
@@ -830,69 +678,81 @@ __device__ __forceinline__ void leaf(float* S, float* Xo, int lane, int col0, in
   if (lane < N) {
 #pragma unroll
     for (int c = 0; c < N; ++c) {
-      S[r * PB + c] = v[c];            // row r of L (upper part unused)
-      Xo[r * PB + c] = x[c] * rs_own;  // row r of X (zeros above the diagonal)
+      S[r * PT + c] = v[c];            // row r of L (upper part unused)
+      Xo[r * PT + c] = x[c] * rs_own;  // row r of X (zeros above the diagonal)
     }
   }
 }
 
 constexpr int kPotrfWaves = 8;  // 8 waves: the next leaf overlaps the trailing products
-constexpr int kLeaf = 16, kLeaves = 128 / kLeaf;  // leaf width, block steps
-__global__ __launch_bounds__(64 * kPotrfWaves) void potrf128_kernel(float* A, int64_t lda, int kb, int bs,
-                                                                   int32_t* info) {
-  constexpr int NT = 64 * kPotrfWaves, NL = 128 * 128 / 4 / NT;  // 16-byte chunks per thread
-  __shared__ float As[128 * PB];
-  __shared__ float Es[128 * PB];
+constexpr int kLeaf = 16;       // leaf width
+
+// The diagonal block at (kb, kb) of A (lda): L^{-1} (lower, zeros above) over it,
+// info = first failing column (1-based) if the block is not positive definite.
+template <class T>
+__global__ __launch_bounds__(64 * kPotrfWaves) void potrf_blk_kernel(T* A, int64_t lda, int kb, int bs,
+                                                                    int32_t* info) {
+  constexpr int NB = Blk<T>::NB, PT = diag_pitch<T>(), NT = 64 * kPotrfWaves;
+  constexpr int EV = 16 / sizeof(T), NL = NB * NB / EV / NT;  // 16-byte pieces per thread
+  constexpr int NLV = NB / kLeaf, NL1 = NLV - 1;
+  typedef T V16 __attribute__((ext_vector_type(EV)));
+  __shared__ __attribute__((aligned(16))) T As[NB * PT];
+  __shared__ __attribute__((aligned(16))) T Es[NB * PT];
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  // 16-byte accesses when every row start is 16-byte aligned (kb is a multiple of 128)
-  const bool vec = (lda & 3) == 0 && (((uintptr_t)A) & 15) == 0;
-  float* Ab = A + (int64_t)kb * lda + kb;
+  // 16-byte accesses when every row start is 16-byte aligned (kb is a multiple of NB)
+  const bool vec = (lda * (int64_t)sizeof(T)) % 16 == 0 && (((uintptr_t)A) & 15) == 0;
+  T* Ab = A + (int64_t)kb * lda + kb;
   {
     // every load in flight before the first LDS write; both triangles are copied
     // (the leaf reads whole rows of its diagonal block), identity past bs
-    f32x4 buf[NL];
+    V16 buf[NL];
 #pragma unroll
     for (int u = 0; u < NL; ++u) {
-      const int e = (u * NT + tid) * 4;  // 4 consecutive columns of one row
-      const int i = e >> 7, j0 = e & 127;
-      const float* src = Ab + (int64_t)i * lda + j0;
-      if (i < bs && vec && j0 + 3 < bs) {
-        buf[u] = *(const f32x4*)src;
+      const int e = (u * NT + tid) * EV;  // EV consecutive columns of one row
+      const int i = e / NB, j0 = e % NB;
+      const T* src = Ab + (int64_t)i * lda + j0;
+      if (i < bs && vec && j0 + EV - 1 < bs) {
+        buf[u] = *(const V16*)src;
       } else {
 #pragma unroll
-        for (int t = 0; t < 4; ++t)
-          buf[u][t] = (i < bs && j0 + t < bs) ? src[t] : (i == j0 + t ? 1.f : 0.f);
+        for (int t = 0; t < EV; ++t)
+          buf[u][t] = (i < bs && j0 + t < bs) ? src[t] : (i == j0 + t ? T(1) : T(0));
       }
     }
 #pragma unroll
     for (int u = 0; u < NL; ++u) {
-      const int e = (u * NT + tid) * 4;
-      const int i = e >> 7, j0 = e & 127;
-      *(f32x2*)&As[i * PB + j0] = f32x2{buf[u][0], buf[u][1]};
-      *(f32x2*)&As[i * PB + j0 + 2] = f32x2{buf[u][2], buf[u][3]};
+      const int e = (u * NT + tid) * EV;
+      const int i = e / NB, j0 = e % NB;
       // E = L^{-1} starts at zero in its strictly lower kLeaf-blocks (the diagonal
       // blocks are written whole by the leaf; the upper ones are never read)
-      if (i / kLeaf > j0 / kLeaf) {
-        *(f32x2*)&Es[i * PB + j0] = f32x2{0.f, 0.f};
-        *(f32x2*)&Es[i * PB + j0 + 2] = f32x2{0.f, 0.f};
+      const bool ez = i / kLeaf > j0 / kLeaf;
+      if constexpr (sizeof(T) == 4) {  // the row pitch keeps 8-byte alignment only
+        *(f32x2*)&As[i * PT + j0] = f32x2{buf[u][0], buf[u][1]};
+        *(f32x2*)&As[i * PT + j0 + 2] = f32x2{buf[u][2], buf[u][3]};
+        if (ez) {
+          *(f32x2*)&Es[i * PT + j0] = f32x2{0.f, 0.f};
+          *(f32x2*)&Es[i * PT + j0 + 2] = f32x2{0.f, 0.f};
+        }
+      } else {
+        *(V16*)&As[i * PT + j0] = buf[u];
+        if (ez) *(V16*)&Es[i * PT + j0] = V16{};
       }
     }
   }
   __syncthreads();
-  auto blk = [](float* base, int i, int j) { return base + (kLeaf * i) * PB + kLeaf * j; };
+  auto blk = [](T* base, int i, int j) { return base + (kLeaf * i) * PT + kLeaf * j; };
   bool failed = false;
   if (wid == 0) leaf<kLeaf>(blk(As, 0, 0), blk(Es, 0, 0), lane, kb, kb + bs, info, failed);
   __syncthreads();
-  constexpr int NL1 = kLeaves - 1;
-  for (int k = 0; k < kLeaves; ++k) {
+  for (int k = 0; k < NLV; ++k) {
     // phase B: (NL1 - k) panel products, k products of the identity's row block k
     for (int q = wid; q < NL1; q += kPotrfWaves) {
       if (q < NL1 - k) {
         const int i = k + 1 + q;
-        mm16<true>(blk(As, i, k), blk(As, i, k), blk(Es, k, k), nullptr, 1.f, lane);
+        mm16<true>(blk(As, i, k), blk(As, i, k), blk(Es, k, k), (const T*)nullptr, T(1), lane);
       } else {
         const int m = q - (NL1 - k);
-        mm16<false>(blk(Es, k, m), blk(Es, k, k), blk(Es, k, m), nullptr, 1.f, lane);
+        mm16<false>(blk(Es, k, m), blk(Es, k, k), blk(Es, k, m), (const T*)nullptr, T(1), lane);
       }
     }
     __syncthreads();
@@ -910,11 +770,11 @@ __global__ __launch_bounds__(64 * kPotrfWaves) void potrf128_kernel(float* A, in
           ++i;
         }
         const int j = k + 1 + t;
-        mm16<true>(blk(As, i, j), blk(As, i, k), blk(As, j, k), blk(As, i, j), -1.f, lane);
+        mm16<true>(blk(As, i, j), blk(As, i, k), blk(As, j, k), (const T*)blk(As, i, j), T(-1), lane);
       } else {
         const int t = q - ntr;
         const int i = k + 1 + t / (k + 1), m = t % (k + 1);
-        mm16<false>(blk(Es, i, m), blk(As, i, k), blk(Es, k, m), blk(Es, i, m), -1.f, lane);
+        mm16<false>(blk(Es, i, m), blk(As, i, k), blk(Es, k, m), (const T*)blk(Es, i, m), T(-1), lane);
       }
     };
     if (wid == 0) {
@@ -931,16 +791,16 @@ __global__ __launch_bounds__(64 * kPotrfWaves) void potrf128_kernel(float* A, in
   asm volatile("" : "+v"(tid2));
 #pragma unroll
   for (int u = 0; u < NL; ++u) {
-    const int e = (u * NT + tid2) * 4;
-    const int i = e >> 7, j0 = e & 127;
+    const int e = (u * NT + tid2) * EV;
+    const int i = e / NB, j0 = e % NB;
     if (i >= bs) continue;
-    f32x4 v;
+    V16 v;
 #pragma unroll
-    for (int t = 0; t < 4; ++t) v[t] = j0 + t <= i ? Es[i * PB + j0 + t] : 0.f;
-    float* dst = Ab + (int64_t)i * lda + j0;
-    if (vec && j0 + 3 < bs) *(f32x4*)dst = v;
+    for (int t = 0; t < EV; ++t) v[t] = j0 + t <= i ? Es[i * PT + j0 + t] : T(0);
+    T* dst = Ab + (int64_t)i * lda + j0;
+    if (vec && j0 + EV - 1 < bs) *(V16*)dst = v;
     else
-      for (int t = 0; t < 4; ++t)
+      for (int t = 0; t < EV; ++t)
         if (j0 + t < bs) dst[t] = v[t];
   }
 }
@@ -1232,12 +1092,8 @@ hipError_t solve_t(const T* G, const T* C, int64_t d64, int64_t dout64, double l
     for (int kb = K0; kb < K0 + W; kb += NB) {
       const int bs = std::min(NB, d - kb);
       const int rest = d - kb - bs;
-      if constexpr (sizeof(T) == 4)
-        hipLaunchKernelGGL(potrf128_kernel, dim3(1), dim3(64 * kPotrfWaves), 0, st, A, d64, kb, bs,
-                           info);
-      else
-        hipLaunchKernelGGL((potrf_inv_kernel<T>), dim3(1), dim3(diag_threads<T>()), 0, st, A, d64, kb,
-                           bs, info);
+      hipLaunchKernelGGL((potrf_blk_kernel<T>), dim3(1), dim3(64 * kPotrfWaves), 0, st, A, d64, kb, bs,
+                         info);
       PKV_TRY(hipGetLastError());
       const T* Linv = A + (int64_t)kb * d + kb;  // Linv(i,t) = Linv[i*d + t]
       {
@@ -1507,16 +1363,6 @@ __global__ __launch_bounds__(256) void rrr_init_kernel(float* Q, int64_t rows, i
   Q[e] = (float)(h >> 8) * (2.0f / 16777216.0f) - 1.0f;
 }
 
-// 1 / x and 1 / sqrt(x) in fp64: the native approximations and one Newton step each
-__device__ __forceinline__ double rcp64(double x) {
-  const double r = __builtin_amdgcn_rcp(x);
-  return fma(r, fma(-x, r, 1.0), r);
-}
-__device__ __forceinline__ double rsq64(double x) {
-  const double r = __builtin_amdgcn_rsq(x);
-  return fma(0.5 * r, fma(-x * r, r, 1.0), r);
-}
-
 // Eigenvectors of the symmetric b x b matrix (T + T^T) / 2 (b even, <= kRrrBlock) by
 // parallel cyclic Jacobi in fp64: each step rotates NB/2 disjoint index pairs of a
 // round-robin schedule, columns then rows. The matrix is padded with zeros to
@@ -1733,7 +1579,7 @@ hipError_t launch_low_rank(const float* G, const float* dW, int64_t din, int64_t
   // src (dout x b) -> dst = src L^-T with src^T src = L L^T (Gram and factor in fp64)
   auto orth = [&](const float* src, float* dst) -> hipError_t {
     PKV_TRY(gram(src, src, W64));
-    hipLaunchKernelGGL((potrf_inv_kernel<double>), dim3(1), dim3(diag_threads<double>()), 0, st, W64,
+    hipLaunchKernelGGL((potrf_blk_kernel<double>), dim3(1), dim3(64 * kPotrfWaves), 0, st, W64,
                        (int64_t)b, 0, b, info);
     PKV_TRY(hipGetLastError());
     hipLaunchKernelGGL(linv_t_kernel, dim3((b * b + 255) / 256), dim3(256), 0, st, W64, b, W);
