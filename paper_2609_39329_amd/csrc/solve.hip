@@ -238,6 +238,13 @@ constexpr int S_PR = S_BM + 16;   // pitch of a [k][row] LDS tile (bf16)
 constexpr int S_TILE = S_BM * S_PK > S_KC * S_PR ? S_BM * S_PK : S_KC * S_PR;  // bf16 per plane
 constexpr int S_LDS = 2 * 4 * S_TILE;  // 2 buffers x {A hi, A lo, B hi, B lo}
 
+// CHECK: bounds-checked staging loads (edge tiles); without it the tile must lie
+// inside M x N, K must be a multiple of the chunk and both operands vector-aligned,
+// and the loads are plain 16-byte loads from pointers advanced once per chunk.
+template <bool AK, bool BJ, bool CHECK>
+__device__ __forceinline__ void sgemm3_tile(const SGemm& g, int i0, int j0, __bf16* lds);
+
+// tile t of g (lower: the triangle's tiles in row order)
 template <bool AK, bool BJ>
 __device__ __forceinline__ void sgemm3_body(const SGemm& g, int t, __bf16* lds) {
   int ti, tj;
@@ -251,6 +258,13 @@ __device__ __forceinline__ void sgemm3_body(const SGemm& g, int t, __bf16* lds) 
     tj = t % g.tiles_n;
   }
   const int i0 = ti * S_BM, j0 = tj * S_BM;
+  const bool interior = i0 + S_BM <= g.M && j0 + S_BM <= g.N && g.K % S_KC == 0 && g.vecA && g.vecB;
+  if (interior) sgemm3_tile<AK, BJ, false>(g, i0, j0, lds);
+  else sgemm3_tile<AK, BJ, true>(g, i0, j0, lds);
+}
+
+template <bool AK, bool BJ, bool CHECK>
+__device__ __forceinline__ void sgemm3_tile(const SGemm& g, int i0, int j0, __bf16* lds) {
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int h32 = lane >> 5, l32 = lane & 31;
   const int wi = (wid >> 1) * 64, wj = (wid & 1) * 64;
@@ -287,7 +301,32 @@ __device__ __forceinline__ void sgemm3_body(const SGemm& g, int t, __bf16* lds) 
   // staging: 128 x 32 floats per operand and chunk = 4 float4 per thread, each a
   // run of 4 elements contiguous in memory
   f32x4 ra[4], rb[4];
+  // unchecked staging: this thread's runs of the first chunk, advanced by one chunk
+  // per fetch (fetches are issued in chunk order)
+  const float* pa[4];
+  const float* pb[4];
+  const int64_t stepA = AK ? S_KC : (int64_t)S_KC * g.sa, stepB = BJ ? (int64_t)S_KC * g.sb : S_KC;
+  if constexpr (!CHECK) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int c = u * 256 + tid;
+      if constexpr (AK) pa[u] = g.A + (int64_t)(i0 + c / (S_KC / 4)) * g.sa + (c % (S_KC / 4)) * 4;
+      else pa[u] = g.A + (int64_t)(c / (S_BM / 4)) * g.sa + i0 + (c % (S_BM / 4)) * 4;
+      if constexpr (BJ) pb[u] = g.B + (int64_t)(c / (S_BM / 4)) * g.sb + j0 + (c % (S_BM / 4)) * 4;
+      else pb[u] = g.B + (int64_t)(j0 + c / (S_KC / 4)) * g.sb + (c % (S_KC / 4)) * 4;
+    }
+  }
   auto fetch = [&](int k0) {
+    if constexpr (!CHECK) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        ra[u] = *(const f32x4*)pa[u];
+        rb[u] = *(const f32x4*)pb[u];
+        pa[u] += stepA;
+        pb[u] += stepB;
+      }
+      return;
+    }
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int c = u * 256 + tid;
@@ -321,15 +360,13 @@ __device__ __forceinline__ void sgemm3_body(const SGemm& g, int t, __bf16* lds) 
       }
     }
   };
+  // x_hi = bf16(x), x_lo = bf16(x - x_hi), two elements per conversion
   auto split_store = [](__bf16* hi, __bf16* lo, int off, f32x4 v) {
-    bf16x4 h, l;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      h[e] = to_bf16(v[e]);
-      l[e] = to_bf16(v[e] - (float)h[e]);
-    }
-    *(bf16x4*)(hi + off) = h;
-    *(bf16x4*)(lo + off) = l;
+    const unsigned h01 = cvt_pk_bf16(v[0], v[1]), h23 = cvt_pk_bf16(v[2], v[3]);
+    const float f0 = __builtin_bit_cast(float, h01 << 16), f1 = __builtin_bit_cast(float, h01 & 0xffff0000u);
+    const float f2 = __builtin_bit_cast(float, h23 << 16), f3 = __builtin_bit_cast(float, h23 & 0xffff0000u);
+    *(u32x2*)(hi + off) = u32x2{h01, h23};
+    *(u32x2*)(lo + off) = u32x2{cvt_pk_bf16(v[0] - f0, v[1] - f1), cvt_pk_bf16(v[2] - f2, v[3] - f3)};
   };
   auto plane = [&](int buf, int p) { return lds + (buf * 4 + p) * S_TILE; };
   auto stash = [&](int buf) {
