@@ -68,6 +68,9 @@ typedef enum {
 typedef enum {
   PATCHKV_RIDGE_ABSOLUTE = 0, /* lambda is the ridge coefficient itself (Eq. 6) */
   PATCHKV_RIDGE_ADAPTIVE = 1, /* lambda is lambda_0; ridge = lambda_0 ||G||_F^2 / tr(G) (Eq. 7) */
+  /* lambda is lambda_0; ridge = lambda_0 tr(G) / d_in, the mean eigenvalue: the
+   * trace-mean scaling that the paper's ridge-scaling ablation compares with Eq. 7 */
+  PATCHKV_RIDGE_TRACE_MEAN = 2,
   /* Flag OR-ed into either mode; used by the F32 solve only (F64 ignores it).
    * Without it the F32 solve forms its block products on bf16 MFMA with every fp32
    * operand split into two bf16 terms (hi + lo) and three cross products kept,
@@ -272,6 +275,8 @@ int patchkv_accumulate_normal_eq(int acc_dtype, const float* Xc, const float* Yf
 /* ridge_mode ABSOLUTE: lambda is the ridge coefficient (> 0).                  */
 /* ridge_mode ADAPTIVE: lambda is lambda_0 (> 0) and the coefficient is         */
 /*   lambda_0 ||G||_F^2 / tr(G) (Eq. 7), computed on the device in fp64.        */
+/* ridge_mode TRACE_MEAN: lambda is lambda_0 (> 0) and the coefficient is       */
+/*   lambda_0 tr(G) / d_in, computed on the device in fp64.                     */
 /* ridge_mode | PATCHKV_SOLVE_EXACT_F32: exact fp32 products in the F32 solve.   */
 /*   Any other bit set in ridge_mode: PATCHKV_E_VALUE.                          */
 /* dW [d_in][d_out] float, written.                                             */

@@ -219,11 +219,15 @@ def normal_equations_chunked(chunks):
 
 
 def ridge_lambda(G0: np.ndarray, lam: float, mode: str = "absolute") -> float:
-    """The ridge coefficient: absolute, or adaptive per Eq. 7 (lam is then lambda_0)."""
+    """The ridge coefficient: absolute; adaptive per Eq. 7, lambda_0 ||G||_F^2 / tr G; or the
+    trace mean lambda_0 tr G / d (the mean eigenvalue, the alternative scaling of the
+    paper's ridge-scaling ablation). For the last two, lam is lambda_0."""
     if mode == "absolute":
         return float(lam)
     if mode == "adaptive":
         return float(lam) * float(np.sum(G0 * G0)) / float(np.trace(G0))
+    if mode == "trace_mean":
+        return float(lam) * float(np.trace(G0)) / G0.shape[0]
     raise ValueError(mode)
 
 

@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(HERE, "lib", "libpatchkv.so")
 
 OK, E_NULL, E_SHAPE, E_DTYPE, E_VALUE, E_WORKSPACE, E_UNSUPPORTED, E_HIP = range(8)
 F32, BF16, F64 = 0, 1, 2
-RIDGE_ABSOLUTE, RIDGE_ADAPTIVE = 0, 1
+RIDGE_ABSOLUTE, RIDGE_ADAPTIVE, RIDGE_TRACE_MEAN = 0, 1, 2
 SOLVE_EXACT_F32 = 16  # flag OR-ed into a ridge mode: exact fp32 products in the F32 solve
 
 _c_i64 = ctypes.c_int64

@@ -14,8 +14,9 @@
 // of that of G + lambda I. The OB-wide inverses are assembled from the NB-wide ones
 // by batched GEMMs.
 // fp32 GEMM tiles run on MFMA 32x32x2 f32 (128 x 128 tiles, double-buffered LDS);
-// fp64 tiles on fp64 FMA. The adaptive ridge of Eq. 7, lambda_0 ||G||_F^2 / tr G,
-// is reduced on the device in fp64 in a fixed order (deterministic).
+// fp64 tiles on fp64 FMA. The adaptive ridge of Eq. 7, lambda_0 ||G||_F^2 / tr G, and
+// the trace-mean scaling lambda_0 tr G / d are reduced on the device in fp64 in a fixed
+// order (deterministic).
 #include <math.h>
 
 #include <algorithm>
@@ -873,7 +874,7 @@ __global__ __launch_bounds__(256) void init_kernel(const T* __restrict__ G, cons
   if (blockIdx.x == 0 && threadIdx.x == 0) *info = 0;
 }
 
-// Stage 1 of the adaptive ridge: per-block partial sums of G_ij^2 and G_ii, in fp64
+// Stage 1 of the scaled ridge: per-block partial sums of G_ij^2 and G_ii, in fp64
 // and in a fixed order (each thread strides over the matrix, then the diagonal).
 template <class T>
 __global__ __launch_bounds__(256) void ridge_partial_kernel(const T* __restrict__ G, int64_t d,
@@ -902,9 +903,10 @@ __global__ __launch_bounds__(256) void ridge_partial_kernel(const T* __restrict_
   }
 }
 
-// Stage 2: lambda = lambda_0 * sum(G^2) / tr(G)  (Eq. 7).
-__global__ __launch_bounds__(256) void ridge_final_kernel(const double* part, double lam0,
-                                                          double* lam_out) {
+// Stage 2: lambda = lambda_0 * sum(G^2) / tr(G) (Eq. 7, ridge 1) or lambda_0 * tr(G) / d
+// (trace mean, ridge 2).
+__global__ __launch_bounds__(256) void ridge_final_kernel(const double* part, double lam0, int ridge,
+                                                          double d, double* lam_out) {
   __shared__ double s2[256], st[256];
   double a = 0.0, b = 0.0;
   for (int i = threadIdx.x; i < kRedBlocks; i += 256) {
@@ -921,7 +923,7 @@ __global__ __launch_bounds__(256) void ridge_final_kernel(const double* part, do
     }
     __syncthreads();
   }
-  if (threadIdx.x == 0) lam_out[0] = lam0 * s2[0] / st[0];
+  if (threadIdx.x == 0) lam_out[0] = ridge == 1 ? lam0 * s2[0] / st[0] : lam0 * st[0] / d;
 }
 
 template <class T>
@@ -1085,7 +1087,7 @@ SolveLayout layout(int64_t d, int64_t dout) {
 
 template <class T>
 hipError_t solve_t(const T* G, const T* C, int64_t d64, int64_t dout64, double lambda,
-                   bool adaptive, bool exact, float* dW, int32_t* info, void* ws, hipStream_t st) {
+                   int ridge, bool exact, float* dW, int32_t* info, void* ws, hipStream_t st) {
   constexpr int NB = Blk<T>::NB;
   const SolveLayout L = layout<T>(d64, dout64);
   char* w = (char*)ws;
@@ -1098,17 +1100,19 @@ hipError_t solve_t(const T* G, const T* C, int64_t d64, int64_t dout64, double l
   double* lam = (double*)(w + L.lam);
   const int d = (int)d64, dout = (int)dout64;
 
-  if (adaptive) {
+  const bool scaled = ridge != 0;  // the coefficient is lambda times a statistic of G
+  if (scaled) {
     hipLaunchKernelGGL((ridge_partial_kernel<T>), dim3(kRedBlocks), dim3(256), 0, st, G, d64, part);
     PKV_TRY(hipGetLastError());
-    hipLaunchKernelGGL(ridge_final_kernel, dim3(1), dim3(256), 0, st, part, lambda, lam);
+    hipLaunchKernelGGL(ridge_final_kernel, dim3(1), dim3(256), 0, st, part, lambda, ridge, (double)d64,
+                       lam);
     PKV_TRY(hipGetLastError());
   }
   {
     const int64_t n = d64 * d64 + d64 * dout64;
     const int blocks = (int)std::min<int64_t>((n + 255) / 256, 4096);
     hipLaunchKernelGGL((init_kernel<T>), dim3(blocks), dim3(256), 0, st, G, C, A, R, d64, dout64,
-                       lambda, adaptive ? lam : (const double*)nullptr, info);
+                       lambda, scaled ? lam : (const double*)nullptr, info);
     PKV_TRY(hipGetLastError());
   }
   const T one = T(1), zero = T(0), mone = T(-1);
@@ -1650,12 +1654,12 @@ size_t solve_ws_bytes(bool f64, int64_t din, int64_t dout) {
 }
 
 hipError_t launch_solve(bool f64, const void* G, const void* C, int64_t din, int64_t dout,
-                        double lambda, bool adaptive, bool exact_f32, float* dW, int32_t* info,
+                        double lambda, int ridge, bool exact_f32, float* dW, int32_t* info,
                         void* ws, hipStream_t st) {
   if (f64)
-    return solve_t<double>((const double*)G, (const double*)C, din, dout, lambda, adaptive, true, dW,
+    return solve_t<double>((const double*)G, (const double*)C, din, dout, lambda, ridge, true, dW,
                            info, ws, st);
-  return solve_t<float>((const float*)G, (const float*)C, din, dout, lambda, adaptive, exact_f32, dW,
+  return solve_t<float>((const float*)G, (const float*)C, din, dout, lambda, ridge, exact_f32, dW,
                         info, ws, st);
 }
 

@@ -138,19 +138,21 @@ def test_solve(d, dout, rows, acc, lam, exact):
     assert err <= tol
 
 
+@pytest.mark.parametrize("ridge", ["adaptive", "trace_mean"])
 @pytest.mark.parametrize("exact", [False, True], ids=["split", "exact"])
 @pytest.mark.parametrize("acc", ["f32", "f64"])
-def test_solve_adaptive_ridge(acc, exact):
+def test_solve_adaptive_ridge(acc, exact, ridge):
     if acc == "f64" and exact:
         pytest.skip("the fp64 solve has a single arithmetic")
     G, C = _spd_system(200, 150, 300, 3)
     tdt = torch.float64 if acc == "f64" else torch.float32
-    mode = pkv.RIDGE_ADAPTIVE | (pkv.SOLVE_EXACT_F32 if exact else 0)
+    base = pkv.RIDGE_ADAPTIVE if ridge == "adaptive" else pkv.RIDGE_TRACE_MEAN
+    mode = base | (pkv.SOLVE_EXACT_F32 if exact else 0)
     dW, info = pkv.solve_patch(dev(G).to(tdt), dev(C).to(tdt), 0.01, mode=mode)
     assert int(info.item()) == 0
     Gin = G if acc == "f64" else G.astype(np.float32).astype(np.float64)
     Cin = C if acc == "f64" else C.astype(np.float32).astype(np.float64)
-    lam = oracle.ridge_lambda(Gin, 0.01, "adaptive")
+    lam = oracle.ridge_lambda(Gin, 0.01, ridge)
     err = rel(host(dW), oracle.solve_patch(Gin, Cin, lam))
     assert err <= _solve_tol(acc, exact, Gin, lam)
 

@@ -336,8 +336,28 @@ def test_solve_scaling_laws():
     lam_b = oracle.ridge_lambda(G2, 0.1, "adaptive")
     assert abs(lam_b / lam_a - a * a) < 1e-12
     assert rel(oracle.solve_patch(G2, C2, lam_b), oracle.solve_patch(G, C, lam_a) / a) < 1e-13
+    # the trace-mean scaling has the same invariance
+    lam_a = oracle.ridge_lambda(G, 0.1, "trace_mean")
+    lam_b = oracle.ridge_lambda(G2, 0.1, "trace_mean")
+    assert abs(lam_b / lam_a - a * a) < 1e-12
+    assert rel(oracle.solve_patch(G2, C2, lam_b), oracle.solve_patch(G, C, lam_a) / a) < 1e-13
     with pytest.raises(ValueError):
         oracle.solve_patch(G, C, 0.0)
+
+
+def test_ridge_scalings_closed_forms():
+    """Eq. 7 and the trace mean by hand on a 2 x 2 G; both equal lambda_0 c on G = c I
+    (every eigenvalue c: the mean and the eigenvalue-weighted mean coincide)."""
+    G = np.array([[2.0, 1.0], [1.0, 4.0]])
+    assert oracle.ridge_lambda(G, 0.5, "adaptive") == 0.5 * (4 + 1 + 1 + 16) / 6
+    assert oracle.ridge_lambda(G, 0.5, "trace_mean") == 0.5 * 6 / 2
+    assert oracle.ridge_lambda(G, 0.5, "absolute") == 0.5
+    c, lam0 = 7.0, 0.01
+    Gc = c * np.eye(5)
+    assert abs(oracle.ridge_lambda(Gc, lam0, "adaptive") - lam0 * c) < 1e-15
+    assert abs(oracle.ridge_lambda(Gc, lam0, "trace_mean") - lam0 * c) < 1e-15
+    with pytest.raises(ValueError):
+        oracle.ridge_lambda(G, 0.5, "spectral")
 
 
 def test_layer_patch_identity_cache_gives_zero_patch():
