@@ -854,21 +854,34 @@ __global__ __launch_bounds__(256) void zero_upper_kernel(T* A, int64_t d, int nb
   }
 }
 
-// A = G + lambda I (full copy), R = C, info = 0.
+// A = G + lambda I (full copy), R = C, info = 0. A workgroup copies whole rows (rows
+// of A first, then of R) in 16-byte runs when source and destination allow it; the
+// thread whose run holds A's diagonal element adds lambda to it.
 template <class T>
 __global__ __launch_bounds__(256) void init_kernel(const T* __restrict__ G, const T* __restrict__ C,
                                                    T* __restrict__ A, T* __restrict__ R, int64_t d,
                                                    int64_t dout, double lambda,
                                                    const double* lam_dev, int32_t* info) {
-  const int64_t nA = d * d, nR = d * dout;
-  const double lam = lam_dev ? *lam_dev : lambda;
-  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < nA + nR;
-       e += (int64_t)gridDim.x * blockDim.x) {
-    if (e < nA) {
-      const int64_t i = e / d, j = e % d;
-      A[e] = G[e] + (i == j ? (T)lam : T(0));
+  constexpr int EV = 16 / sizeof(T);
+  typedef T V16 __attribute__((ext_vector_type(EV)));
+  const T lam = (T)(lam_dev ? *lam_dev : lambda);
+  for (int64_t i = blockIdx.x; i < d + d; i += gridDim.x) {
+    const bool isA = i < d;
+    const int64_t r = isA ? i : i - d, n = isA ? d : dout;
+    const T* src = isA ? G + r * d : C + r * dout;
+    T* dst = isA ? A + r * d : R + r * dout;
+    const int64_t diag = isA ? r : -1;
+    if ((((uintptr_t)src | (uintptr_t)dst) & 15) == 0) {
+      const int64_t nv = n / EV;
+      for (int64_t v = threadIdx.x; v < nv; v += blockDim.x) {
+        V16 x = *(const V16*)(src + v * EV);
+        const int64_t t = diag - v * EV;
+        if (t >= 0 && t < EV) x[t] += lam;
+        *(V16*)(dst + v * EV) = x;
+      }
+      for (int64_t j = nv * EV + threadIdx.x; j < n; j += blockDim.x) dst[j] = src[j] + (j == diag ? lam : T(0));
     } else {
-      R[e - nA] = C[e - nA];
+      for (int64_t j = threadIdx.x; j < n; j += blockDim.x) dst[j] = src[j] + (j == diag ? lam : T(0));
     }
   }
   if (blockIdx.x == 0 && threadIdx.x == 0) *info = 0;
@@ -1095,7 +1108,9 @@ hipError_t solve_t(const T* G, const T* C, int64_t d64, int64_t dout64, double l
   T* Lm = (T*)(w + L.Lm);
   T* R = (T*)(w + L.R);
   T* Z = (T*)(w + L.Z);
-  T* X = (T*)(w + L.X);
+  // the backward substitution's result: in fp32 directly the caller's dW (G and C are
+  // read only before it is written), in fp64 a workspace matrix converted at the end
+  T* X = sizeof(T) == 4 ? (T*)dW : (T*)(w + L.X);
   double* part = (double*)(w + L.part);
   double* lam = (double*)(w + L.lam);
   const int d = (int)d64, dout = (int)dout64;
@@ -1109,8 +1124,7 @@ hipError_t solve_t(const T* G, const T* C, int64_t d64, int64_t dout64, double l
     PKV_TRY(hipGetLastError());
   }
   {
-    const int64_t n = d64 * d64 + d64 * dout64;
-    const int blocks = (int)std::min<int64_t>((n + 255) / 256, 4096);
+    const int blocks = (int)std::min<int64_t>(2 * d64, 4096);
     hipLaunchKernelGGL((init_kernel<T>), dim3(blocks), dim3(256), 0, st, G, C, A, R, d64, dout64,
                        lambda, scaled ? lam : (const double*)nullptr, info);
     PKV_TRY(hipGetLastError());
@@ -1228,7 +1242,7 @@ hipError_t solve_t(const T* G, const T* C, int64_t d64, int64_t dout64, double l
       PKV_TRY(run(&g, 1));
     }
   }
-  {
+  if constexpr (sizeof(T) == 8) {
     const int64_t n = d64 * dout64;
     const int blocks = (int)std::min<int64_t>((n + 255) / 256, 4096);
     hipLaunchKernelGGL((to_float_kernel<T>), dim3(blocks), dim3(256), 0, st, X, dW, n);
