@@ -117,6 +117,8 @@ SOLVE_CASES = [
     (1000, 700, 1500, "f32", 0.5),
     (64, 64, 30, "f32", 1.0),        # single block, rank-deficient X
     (700, 900, 1200, "f32", 0.2),    # d_out > d_in, ragged tiles in both directions
+    (301, 67, 500, "f32", 0.3),      # rows not 16-byte aligned: unvectorised loads everywhere
+    (257, 33, 400, "f64", 0.3),      # the same in fp64 (odd leading dimension)
 ]
 
 
