@@ -25,7 +25,8 @@ def dev(a):
     return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(DEV)
 
 
-@pytest.mark.parametrize("din,dout,r", [(256, 192, 8), (300, 512, 32), (128, 64, 64), (96, 40, 8)])
+@pytest.mark.parametrize("din,dout,r", [(256, 192, 8), (300, 512, 32), (128, 64, 64), (96, 40, 8),
+                                       (96, 42, 8)])
 def test_low_rank_planted_gap(din, dout, r):
     print(f"low rank planted gap din={din} dout={dout} r={r}", flush=True)
     rng = np.random.default_rng(din + r)
