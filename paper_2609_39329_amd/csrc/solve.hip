@@ -464,6 +464,166 @@ __global__ __launch_bounds__(256, 2) void sgemm3_kernel(SGemm d0, SGemm d1) {
   }
 }
 
+// ---- the same three-term products for K <= 128: 64 x 64 tiles, one staging round ------
+//
+// The small updates of the factorisation (K = one block column) are latency bound:
+// with 128 x 128 tiles a launch has few workgroups and every 32-wide chunk waits for
+// its loads. Here each workgroup (4 waves of 32 x 32) loads its whole K range in one
+// round (K padded to 16 with zeros, bounds-checked), splits it into the four bf16
+// planes in LDS and runs the MFMAs with no further waits.
+constexpr int T_BM = 64, T_KMAX = 128;
+constexpr int T_PK = T_KMAX + 8;  // pitch of a [row][k] LDS tile (bf16)
+constexpr int T_PR = T_BM + 16;   // pitch of a [k][row] LDS tile (bf16)
+constexpr int T_TILE = T_BM * T_PK > T_KMAX * T_PR ? T_BM * T_PK : T_KMAX * T_PR;  // bf16 per plane
+
+template <bool AK, bool BJ>
+__device__ __forceinline__ void sgemm3s_body(const SGemm& g, int t, __bf16* lds) {
+  int ti, tj;
+  if (g.lower) {
+    ti = (int)((sqrtf(8.f * (float)t + 1.f) - 1.f) * 0.5f);
+    while ((ti + 1) * (ti + 2) / 2 <= t) ++ti;
+    while (ti * (ti + 1) / 2 > t) --ti;
+    tj = t - ti * (ti + 1) / 2;
+  } else {
+    ti = t / g.tiles_n;
+    tj = t % g.tiles_n;
+  }
+  const int i0 = ti * T_BM, j0 = tj * T_BM;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int h32 = lane >> 5, l32 = lane & 31;
+  const int wi = (wid >> 1) * 32, wj = (wid & 1) * 32;
+  constexpr bool a_rk = AK, b_rk = !BJ;
+  constexpr int PA = a_rk ? T_PK : T_PR, PB = b_rk ? T_PK : T_PR;
+  const int Kp = (g.K + 15) & ~15;
+
+  // C prefetch: lane owns C[i0+wi+l32][j0+wj+8q+4h32 .. +3]
+  f32x4 cpre[4];
+  const bool use_c = g.beta != 0.f;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    f32x4 v = {};
+    const int i = i0 + wi + l32, j = j0 + wj + 8 * q + 4 * h32;
+    if (use_c && i < g.M && j < g.N) {
+      const float* c = g.C + (int64_t)i * g.ldc + j;
+      if (g.vecC && j + 3 < g.N) v = *(const f32x4*)c;
+      else
+        for (int e = 0; e < 4; ++e)
+          if (j + e < g.N) v[e] = c[e];
+    }
+    cpre[q] = v;
+  }
+
+  // the whole K range: 64 x Kp per operand = up to 8 runs of 4 floats per thread
+  constexpr int NU = T_BM * T_KMAX / 4 / 256;
+  f32x4 ra[NU], rb[NU];
+#pragma unroll
+  for (int u = 0; u < NU; ++u) {
+    const int c = u * 256 + tid;
+    {
+      int i, k;
+      if constexpr (AK) { i = c / (T_KMAX / 4); k = (c % (T_KMAX / 4)) * 4; }
+      else { k = c / (T_BM / 4); i = (c % (T_BM / 4)) * 4; }
+      const int gi = i0 + i;
+      const int nvalid = AK ? (gi < g.M ? g.K - k : 0) : (k < g.K ? g.M - gi : 0);
+      const float* src = g.A + (AK ? (int64_t)gi * g.sa + k : (int64_t)k * g.sa + gi);
+      f32x4 v = {};
+      if (k < Kp) {
+        if (nvalid >= 4 && g.vecA) v = *(const f32x4*)src;
+        else
+          for (int e = 0; e < 4; ++e)
+            if (e < nvalid) v[e] = src[e];
+      }
+      ra[u] = v;
+    }
+    {
+      int j, k;
+      if constexpr (BJ) { k = c / (T_BM / 4); j = (c % (T_BM / 4)) * 4; }
+      else { j = c / (T_KMAX / 4); k = (c % (T_KMAX / 4)) * 4; }
+      const int gj = j0 + j;
+      const int nvalid = BJ ? (k < g.K ? g.N - gj : 0) : (gj < g.N ? g.K - k : 0);
+      const float* src = g.B + (BJ ? (int64_t)k * g.sb + gj : (int64_t)gj * g.sb + k);
+      f32x4 v = {};
+      if (k < Kp) {
+        if (nvalid >= 4 && g.vecB) v = *(const f32x4*)src;
+        else
+          for (int e = 0; e < 4; ++e)
+            if (e < nvalid) v[e] = src[e];
+      }
+      rb[u] = v;
+    }
+  }
+  // x_hi = bf16(x), x_lo = bf16(x - x_hi), two elements per conversion
+  auto split_store = [](__bf16* hi, __bf16* lo, int off, f32x4 v) {
+    const unsigned h01 = cvt_pk_bf16(v[0], v[1]), h23 = cvt_pk_bf16(v[2], v[3]);
+    const float f0 = __builtin_bit_cast(float, h01 << 16), f1 = __builtin_bit_cast(float, h01 & 0xffff0000u);
+    const float f2 = __builtin_bit_cast(float, h23 << 16), f3 = __builtin_bit_cast(float, h23 & 0xffff0000u);
+    *(u32x2*)(hi + off) = u32x2{h01, h23};
+    *(u32x2*)(lo + off) = u32x2{cvt_pk_bf16(v[0] - f0, v[1] - f1), cvt_pk_bf16(v[2] - f2, v[3] - f3)};
+  };
+  __bf16 *ah = lds, *al = lds + T_TILE, *bh = lds + 2 * T_TILE, *bl = lds + 3 * T_TILE;
+#pragma unroll
+  for (int u = 0; u < NU; ++u) {
+    const int c = u * 256 + tid;
+    const int ka = AK ? (c % (T_KMAX / 4)) * 4 : c / (T_BM / 4);
+    const int kb = BJ ? c / (T_BM / 4) : (c % (T_KMAX / 4)) * 4;
+    if (ka < Kp)
+      split_store(ah, al, a_rk ? (c / (T_KMAX / 4)) * PA + (c % (T_KMAX / 4)) * 4
+                               : (c / (T_BM / 4)) * PA + (c % (T_BM / 4)) * 4, ra[u]);
+    if (kb < Kp)
+      split_store(bh, bl, b_rk ? (c / (T_KMAX / 4)) * PB + (c % (T_KMAX / 4)) * 4
+                               : (c / (T_BM / 4)) * PB + (c % (T_BM / 4)) * 4, rb[u]);
+  }
+  __syncthreads();
+  // 32 rows x 8 k fragment (row r0 + l32, k k0 + 8 h32 ..) of an LDS tile
+  const int tr_k = 8 * h32 + ((lane & 15) >> 2);
+  const int tr_r = ((lane >> 4) & 1) * 16 + 4 * (lane & 3);
+  auto frag = [&](const __bf16* base, int pitch, bool rk, int r0, int k0) -> bf16x8 {
+    if (rk) return *(const bf16x8*)(base + (r0 + l32) * pitch + k0 + h32 * 8);
+    const PKV_LDS __bf16* q = (const PKV_LDS __bf16*)(base + (k0 + tr_k) * pitch + r0 + tr_r);
+    return cat8(lds_read_tr16(q), lds_read_tr16(q + 4 * pitch));
+  };
+  f32x16 acc = {};
+  for (int ks = 0; ks < Kp; ks += 16) {
+    const bf16x8 fah = frag(ah, PA, a_rk, wi, ks), fal = frag(al, PA, a_rk, wi, ks);
+    const bf16x8 fbh = frag(bh, PB, b_rk, wj, ks), fbl = frag(bl, PB, b_rk, wj, ks);
+    // transposed tile: MFMA rows are output columns (B), MFMA columns output rows (A)
+    acc = mfma32(fbh, fah, acc);
+    acc = mfma32(fbh, fal, acc);
+    acc = mfma32(fbl, fah, acc);
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int i = i0 + wi + l32, j = j0 + wj + 8 * q + 4 * h32;
+    if (i >= g.M || j >= g.N) continue;
+    f32x4 v;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[e] = g.alpha * acc[4 * q + e];
+    if (use_c) v += g.beta * cpre[q];
+    float* d = g.C + (int64_t)i * g.ldc + j;
+    if (g.vecC && j + 3 < g.N) *(f32x4*)d = v;
+    else
+      for (int e = 0; e < 4; ++e)
+        if (j + e < g.N) d[e] = v[e];
+  }
+}
+
+template <bool AK0, bool BJ0, bool AK1, bool BJ1>
+__global__ __launch_bounds__(256, 2) void sgemm3s_kernel(SGemm d0, SGemm d1) {
+  __shared__ __attribute__((aligned(16))) __bf16 lds[4 * T_TILE];
+  const int total = d0.ntiles + d1.ntiles;
+  const int t = xcd_item((total + kXcds - 1) / kXcds);
+  if (t >= total) return;
+  if (t < d0.ntiles) {
+    int u = t;
+    const SGemm g = batch_item(d0, u);
+    sgemm3s_body<AK0, BJ0>(g, u, lds);
+  } else {
+    int u = t - d0.ntiles;
+    const SGemm g = batch_item(d1, u);
+    sgemm3s_body<AK1, BJ1>(g, u, lds);
+  }
+}
+
 // ---- fp64: 64 x 64 output tile, fp64 FMA, 4 x 4 outputs per thread ----------------
 constexpr int D_T = 64, D_KC = 32;
 
@@ -1013,7 +1173,7 @@ hipError_t run_group(const GemmDesc<T>* ds, int n, hipStream_t st) {
   return hipGetLastError();
 }
 
-SGemm to_sgemm(const GemmDesc<float>& g, bool& ak, bool& bj) {
+SGemm to_sgemm(const GemmDesc<float>& g, bool& ak, bool& bj, int tile) {
   SGemm s{};
   ak = g.sak == 1;
   bj = g.sbj == 1;
@@ -1023,7 +1183,7 @@ SGemm to_sgemm(const GemmDesc<float>& g, bool& ak, bool& bj) {
   s.M = g.M; s.N = g.N; s.K = g.K;
   s.alpha = g.alpha; s.beta = g.beta;
   s.lower = g.lower;
-  const int tm = (g.M + S_BM - 1) / S_BM, tn = (g.N + S_BM - 1) / S_BM;
+  const int tm = (g.M + tile - 1) / tile, tn = (g.N + tile - 1) / tile;
   s.tiles_n = tn;
   s.tiles_b = g.lower ? tm * (tm + 1) / 2 : tm * tn;  // a lower-triangle update is square
   s.batch = g.batch;
@@ -1040,10 +1200,20 @@ SGemm to_sgemm(const GemmDesc<float>& g, bool& ak, bool& bj) {
 hipError_t run_group_split(const GemmDesc<float>* ds, int n, hipStream_t st) {
   SGemm s[2] = {};
   bool ak[2] = {true, true}, bj[2] = {true, true};
+  // K <= 128 everywhere (the factorisation's block-column updates) and too few 128 x 128
+  // tiles to fill the CUs: the small-K kernel (latency rather than throughput)
+  int kmax = 0, tiles128 = 0;
+  for (int i = 0; i < n; ++i)
+    if (ds[i].M > 0 && ds[i].N > 0 && ds[i].K > 0) {
+      bool a, b;
+      kmax = std::max(kmax, ds[i].K);
+      tiles128 += to_sgemm(ds[i], a, b, S_BM).ntiles;
+    }
+  const bool small = kmax <= T_KMAX && tiles128 < 256;
   int m = 0;
   for (int i = 0; i < n; ++i)
     if (ds[i].M > 0 && ds[i].N > 0 && ds[i].K > 0) {
-      s[m] = to_sgemm(ds[i], ak[m], bj[m]);
+      s[m] = to_sgemm(ds[i], ak[m], bj[m], small ? T_BM : S_BM);
       ++m;
     }
   if (m == 0) return hipSuccess;
@@ -1054,13 +1224,21 @@ hipError_t run_group_split(const GemmDesc<float>* ds, int n, hipStream_t st) {
   const int total = s[0].ntiles + s[1].ntiles;
   const dim3 grid((total + kXcds - 1) / kXcds * kXcds), block(256);
   const int key = (ak[0] << 3) | (bj[0] << 2) | (ak[1] << 1) | (int)bj[1];
+#define PKV_SG(A0, B0, A1, B1)                                                                  \
+  do {                                                                                          \
+    if (small)                                                                                  \
+      hipLaunchKernelGGL((sgemm3s_kernel<A0, B0, A1, B1>), grid, block, 0, st, s[0], s[1]);     \
+    else                                                                                        \
+      hipLaunchKernelGGL((sgemm3_kernel<A0, B0, A1, B1>), grid, block, 0, st, s[0], s[1]);      \
+  } while (0)
   switch (key) {
-    case 0b1011: hipLaunchKernelGGL((sgemm3_kernel<true, false, true, true>), grid, block, 0, st, s[0], s[1]); break;
-    case 0b1010: hipLaunchKernelGGL((sgemm3_kernel<true, false, true, false>), grid, block, 0, st, s[0], s[1]); break;
-    case 0b1111: hipLaunchKernelGGL((sgemm3_kernel<true, true, true, true>), grid, block, 0, st, s[0], s[1]); break;
-    case 0b0101: hipLaunchKernelGGL((sgemm3_kernel<false, true, false, true>), grid, block, 0, st, s[0], s[1]); break;
+    case 0b1011: PKV_SG(true, false, true, true); break;
+    case 0b1010: PKV_SG(true, false, true, false); break;
+    case 0b1111: PKV_SG(true, true, true, true); break;
+    case 0b0101: PKV_SG(false, true, false, true); break;
     default: return hipErrorInvalidValue;
   }
+#undef PKV_SG
   return hipGetLastError();
 }
 
