@@ -119,6 +119,9 @@ SOLVE_CASES = [
     (700, 900, 1200, "f32", 0.2),    # d_out > d_in, ragged tiles in both directions
     (301, 67, 500, "f32", 0.3),      # rows not 16-byte aligned: unvectorised loads everywhere
     (257, 33, 400, "f64", 0.3),      # the same in fp64 (odd leading dimension)
+    (17, 3, 40, "f32", 0.1),         # one partial block: a full leaf and a 1-wide one
+    (1, 1, 5, "f32", 0.1),           # degenerate: a single unknown
+    (1, 1, 5, "f64", 0.1),
 ]
 
 
