@@ -26,7 +26,7 @@ def dev(a):
 
 
 @pytest.mark.parametrize("din,dout,r", [(256, 192, 8), (300, 512, 32), (128, 64, 64), (96, 40, 8),
-                                       (96, 42, 8)])
+                                       (96, 42, 8), (8, 2, 1), (10, 3, 2)])
 def test_low_rank_planted_gap(din, dout, r):
     print(f"low rank planted gap din={din} dout={dout} r={r}", flush=True)
     rng = np.random.default_rng(din + r)
