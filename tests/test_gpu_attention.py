@@ -32,6 +32,8 @@ SHAPES = [
     (128, 2048, 256, 4, 2, 64, "f32"),      # tiny fp32 layer shape
     (50, 333, 100, 8, 2, 128, "f32"),
     (8, 20000, 3000, 4, 2, 64, "f32"),      # fp32 split-key path
+    (1, 1, 1, 4, 2, 64, "bf16"),            # degenerate: one query, one key, one entry
+    (1, 1, 1, 4, 2, 128, "f32"),
 ]
 
 

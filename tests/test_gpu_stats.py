@@ -40,6 +40,8 @@ def dev(a):
     (77, 300, 300, "f32", 1),
     (130, 200, 96, "bf16", 0),       # rectangular, ragged tiles
     (1024, 1024, 1024, "bf16", 1),
+    (1, 64, 64, "bf16", 1),          # a single reference token
+    (1, 64, 40, "f32", 0),
 ])
 def test_targets(M, din, dout, wdt, rho):
     Of, Oc = randn((M, din), 1, 0.3), randn((M, din), 2, 0.3)
