@@ -13,8 +13,10 @@
 // GEMM instead of a substitution); its condition number is at most the square root
 // of that of G + lambda I. The OB-wide inverses are assembled from the NB-wide ones
 // by batched GEMMs.
-// fp32 GEMM tiles run on MFMA 32x32x2 f32 (128 x 128 tiles, double-buffered LDS);
-// fp64 tiles on fp64 FMA. The adaptive ridge of Eq. 7, lambda_0 ||G||_F^2 / tr G, and
+// fp32 block products split both operands into bf16 hi + lo and sum three bf16 MFMA
+// products (128 x 128 tiles; 64 x 64 with the whole K range staged at once for the
+// latency-bound K <= 128 updates), or run on MFMA 32x32x2 f32 when exact fp32 products
+// are asked for; fp64 tiles run on fp64 FMA. The adaptive ridge of Eq. 7, lambda_0 ||G||_F^2 / tr G, and
 // the trace-mean scaling lambda_0 tr G / d are reduced on the device in fp64 in a fixed
 // order (deterministic).
 #include <math.h>
