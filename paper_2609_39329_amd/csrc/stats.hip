@@ -7,6 +7,8 @@
 //
 // fp32-accumulate path: split pre-passes + bgemm_kernel (bf16 MFMA, fp32 accumulation).
 // fp64-accumulate path (f64_gemm_kernel): plain fp64 FMA tiles through LDS.
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -78,37 +80,63 @@ __global__ __launch_bounds__(256) void split_rows_kernel(const float* __restrict
 }
 
 // dst[c][r] (c < cols_p, r < rows_p) = split(S1 + s2 S2)[r][c] inside rows x cols,
-// zero outside: the transpose, through a 64 x 64 LDS tile (s2 = -1: a difference,
+// zero outside: the transpose, through a 128 x 64 LDS tile (s2 = -1: a difference,
 // +1: a bf16 weight plus an fp32 patch). SRC float (hi and lo planes,
-// lo may be null for a bf16 source) or bf16 (hi plane only).
+// lo may be null for a bf16 source) or bf16 (hi plane only). Each thread reads 4
+// consecutive source columns (one vector load when vec is set: S1, S2 and ld allow
+// it), and 16 threads write one 256-byte run of a destination row.
 template <class SRC>
 __global__ __launch_bounds__(256) void split_transpose_kernel(const SRC* __restrict__ S1,
                                                               const float* __restrict__ S2, float s2,
                                                               int rows, int cols, int64_t ld,
                                                               __bf16* __restrict__ hi,
                                                               __bf16* __restrict__ lo, int rows_p,
-                                                              int cols_p) {
-  __shared__ float tile[64][65];
-  const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+                                                              int cols_p, int vec) {
+  constexpr int TR = 128, TC = 64;
+  __shared__ float tile[TR][TC + 1];
+  const int r0 = blockIdx.y * TR, c0 = blockIdx.x * TC;
   const int tid = threadIdx.x;
 #pragma unroll
-  for (int u = 0; u < 16; ++u) {
+  for (int u = 0; u < TR * TC / 4 / 256; ++u) {
     const int e = u * 256 + tid;
-    const int rr = e / 64, cc = e % 64;
+    const int rr = e / 16, cc = (e % 16) * 4;
     const int r = r0 + rr, c = c0 + cc;
-    float v = 0.f;
-    if (r < rows && c < cols) {
-      v = (float)S1[(int64_t)r * ld + c];
-      if (S2) v = fmaf(s2, S2[(int64_t)r * ld + c], v);
+    float v[4] = {0.f, 0.f, 0.f, 0.f};
+    if (r < rows) {
+      const int64_t o = (int64_t)r * ld + c;
+      if (vec && c + 3 < cols) {
+        if constexpr (std::is_same<SRC, float>::value) {
+          const f32x4 x = *(const f32x4*)(S1 + o);
+#pragma unroll
+          for (int t = 0; t < 4; ++t) v[t] = x[t];
+        } else {
+          const bf16x4 x = *(const bf16x4*)(S1 + o);
+#pragma unroll
+          for (int t = 0; t < 4; ++t) v[t] = (float)x[t];
+        }
+        if (S2) {
+          const f32x4 y = *(const f32x4*)(S2 + o);
+#pragma unroll
+          for (int t = 0; t < 4; ++t) v[t] = fmaf(s2, y[t], v[t]);
+        }
+      } else {
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+          if (c + t < cols) {
+            v[t] = (float)S1[o + t];
+            if (S2) v[t] = fmaf(s2, S2[o + t], v[t]);
+          }
+      }
     }
-    tile[rr][cc] = v;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) tile[rr][cc + t] = v[t];
   }
   __syncthreads();
-  // write rows c of dst: 64 consecutive r as 8 chunks of 8 bf16
+  // row c of dst: 128 consecutive r as 16 chunks of 8 bf16
 #pragma unroll
-  for (int u = 0; u < 2; ++u) {
+  for (int u = 0; u < TR * TC / 8 / 256; ++u) {
     const int e = u * 256 + tid;
-    const int cc = e / 8, rr0 = (e % 8) * 8;
+    const int cc = e / 16, rr0 = (e % 16) * 8;
     const int c = c0 + cc;
     if (c >= cols_p || r0 + rr0 >= rows_p) continue;
     bf16x8 h, l;
@@ -308,9 +336,12 @@ template <class SRC>
 hipError_t run_split_transpose(const SRC* S1, const float* S2, int64_t rows, int64_t cols,
                                int64_t ld, __bf16* hi, __bf16* lo, int64_t rows_p, int64_t cols_p,
                                hipStream_t st, float s2 = -1.f) {
-  const dim3 grid((unsigned)((cols_p + 63) / 64), (unsigned)((rows_p + 63) / 64));
+  // rows_p is a multiple of 8 (every caller pads it to 64): whole 16-byte chunks
+  const dim3 grid((unsigned)((cols_p + 63) / 64), (unsigned)((rows_p + 127) / 128));
+  const int vec = ld % 4 == 0 && (uintptr_t)S1 % (4 * sizeof(SRC)) == 0 &&
+                  (S2 == nullptr || (uintptr_t)S2 % 16 == 0);
   hipLaunchKernelGGL((split_transpose_kernel<SRC>), grid, dim3(256), 0, st, S1, S2, s2, (int)rows,
-                     (int)cols, ld, hi, lo, (int)rows_p, (int)cols_p);
+                     (int)cols, ld, hi, lo, (int)rows_p, (int)cols_p, vec);
   return hipGetLastError();
 }
 
