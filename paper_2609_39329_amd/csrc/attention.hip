@@ -14,8 +14,11 @@
 // P fragments' k-slots, so the V operand is one 16-byte LDS read (the transposing
 // LDS read delivers about a third of the bandwidth). The online softmax runs in
 // fp32 in the exp2 domain with a fixed per-row offset (fast path) and falls back
-// to a lazily rescaled pass for work items whose scores outgrow it. K/V tiles
-// stream through four LDS slots with register prefetch; the workgroup -> work-item
+// to a lazily rescaled pass for work items whose scores outgrow it. On the main
+// path K/V^T tiles go from HBM straight into eight LDS slots (buffer_load ... lds, no
+// register staging), six tiles ahead, with XOR-swizzled 16-byte chunks in place of
+// row padding and one barrier per two tiles; the gathering, biased and two-term-P
+// variants stage through registers into four padded slots. The workgroup -> work-item
 // map keeps all row tiles of one KV head (and key range) on one XCD so its L2
 // serves the K/V re-reads.
 //
@@ -60,6 +63,14 @@ constexpr int kQT = 1;
 constexpr int kThreadsBf16 = kRowsWG / (32 * kQT) * 64;
 constexpr int kLoadSets = 2;
 constexpr int kKeyTileF32 = 32;
+// bf16 fast path without gather, bias or two-term P: K / V^T tiles are loaded straight
+// into LDS (buffer_load ... lds) through kDmaSlots slots, each tile's loads issued
+// kDmaAhead steps before the step that scores it, one barrier per kDmaSteps steps
+constexpr bool kAttnDma = true;
+constexpr int kDmaSlots = 8, kDmaAhead = 6, kDmaSteps = 2;
+static_assert(kDmaAhead <= kDmaSlots - kDmaSteps && kDmaAhead >= kDmaSteps + 1,
+              "a slot is refilled only after its last read");
+static_assert(kDmaSlots % (2 * kDmaSteps) == 0, "whole barrier groups per unrolled pass");
 
 struct AttnParams {
   const void* Q;
@@ -157,8 +168,15 @@ __global__ __launch_bounds__(kThreadsBf16, 1) void attn_bf16_kernel(AttnParams p
   constexpr int NT = kThreadsBf16;
   constexpr int NCH = KT * CH;             // 16-byte chunks per K tile (= per V^T tile)
   constexpr int LPT = (NCH + NT - 1) / NT;  // chunks per thread
-  __shared__ __attribute__((aligned(16))) __bf16 Ks[4][KT * KP];
-  __shared__ __attribute__((aligned(16))) __bf16 Vs[4][DH * VTP];
+  // DMA: the plain fast path streams K / V^T tiles straight into LDS (no register
+  // staging), through kDmaSlots unpadded slots whose 16-byte chunks are XOR-swizzled
+  // so that the MFMA operand reads stay conflict-free
+  constexpr bool DMA = kAttnDma && !SAFE && !GATHER && !BIAS && !PSPLIT;
+  constexpr int NSL = kDmaSlots;
+  __shared__ __attribute__((aligned(16))) __bf16 Ks[DMA ? 1 : 4][KT * KP];
+  __shared__ __attribute__((aligned(16))) __bf16 Vs[DMA ? 1 : 4][DH * VTP];
+  __shared__ __attribute__((aligned(16))) __bf16 Kd[DMA ? NSL : 1][DMA ? KT * DH : 8];
+  __shared__ __attribute__((aligned(16))) __bf16 Vd[DMA ? NSL : 1][DMA ? DH * KT : 8];
   __shared__ __attribute__((aligned(16))) float Bs[BIAS ? 4 : 1][BIAS ? KT : 4];
   __shared__ int overflow;
 
@@ -438,10 +456,119 @@ __global__ __launch_bounds__(kThreadsBf16, 1) void attn_bf16_kernel(AttnParams p
   };
 
   if (tid == 0) overflow = 0;
-  load_tile_to(0, 0);
-  store_tile_from(0, 0);
+  if constexpr (!DMA) {
+    load_tile_to(0, 0);
+    store_tile_from(0, 0);
+  }
 
-  if constexpr (!SAFE) {
+  if constexpr (DMA) {
+    // LDS position c (= tid) of a slot holds K row c / CH, chunk (c % CH) ^ swk(row), and
+    // V^T row c / 4, chunk (c % 4) ^ ((row / 4) % 4): for every 16 consecutive rows read
+    // at one chunk index the 16-byte reads land in 16 different bank groups.
+    constexpr int RPB = 16 / CH;  // K rows per 256 bytes of LDS
+    constexpr int D = kDmaAhead;
+    const int krow = tid / CH, kch = (tid % CH) ^ ((krow / RPB) % CH);
+    const uint32_t koff = (uint32_t)(krow * DH * 2 + kch * 16);
+    const int vrow = tid / 4, vch = (tid % 4) ^ ((vrow / 4) % 4);
+    const uint32_t voff = (uint32_t)(vrow * 64 + vch * 16);
+    // the tile offset goes into the per-lane offset, so the buffer range check covers it
+    // (OWN: the tiles after the cache range of the last key range are the chunk's own
+    // entries, from their own buffers)
+    auto issue = [&](int tile, auto slot_t) {
+      constexpr int SL = decltype(slot_t)::value;
+      if (tid < NCH) {
+        PKV_LDS void* kd = (PKV_LDS void*)&Kd[SL][wid * 512];
+        PKV_LDS void* vd = (PKV_LDS void*)&Vd[SL][wid * 512];
+        if (OWN && own_range && tile >= ct) {
+          const uint32_t j0 = (uint32_t)((tile - ct) * KT);
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(ksrs, kd, 16, koff + j0 * (DH * 2), 0, 0, 0);
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(vtsrs, vd, 16, voff + (j0 / 32) * (DH * 64), 0, 0, 0);
+        } else {
+          const uint32_t kb0 = (uint32_t)(k_begin + tile * KT);
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(krs, kd, 16, koff + kb0 * (DH * 2), 0, 0, 0);
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(vrs, vd, 16, voff + (kb0 / 32) * (DH * 64), 0, 0, 0);
+        }
+      }
+    };
+    // wait until at most N of this wave's loads are in flight, then a plain barrier (no
+    // fence: it would wait for every load in flight)
+    auto sync_slots = [&](auto n_t) {
+      constexpr int N = decltype(n_t)::value;
+      asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
+    };
+    const int swk = (l32 / RPB) % CH, swv = (l32 / 4) % 4;
+    auto scores_d = [&](f32x16 (&s)[NKT][QT], auto slot_t) {
+      constexpr int SL = decltype(slot_t)::value;
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt) s[0][qt] = f32x16{};
+#pragma unroll
+      for (int st = 0; st < NS; ++st) {
+        const bf16x8 a = *(const bf16x8*)(&Kd[SL][l32 * DH + (((2 * st + h32) ^ swk) * 8)]);
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) s[0][qt] = mfma32(a, qf[qt][st], s[0][qt]);
+      }
+    };
+    auto pv_d = [&](bf16x8 (&pb)[NKT][QT][2], auto slot_t) {
+      constexpr int SL = decltype(slot_t)::value;
+#pragma unroll
+      for (int p2 = 0; p2 < 2; ++p2)
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt) {
+          const bf16x8 a =
+              *(const bf16x8*)(&Vd[SL][(dt * 32 + l32) * 32 + (((2 * p2 + h32) ^ swv) * 8)]);
+#pragma unroll
+          for (int qt = 0; qt < QT; ++qt) o[qt][dt] = mfma32(a, pb[0][qt][p2], o[qt][dt]);
+        }
+    };
+    static_assert(NKT == 1 && !PSPLIT, "DMA path: one 32-key MFMA tile, one-term P");
+    static_for<D>([&](auto j_t) { issue(decltype(j_t)::value, j_t); });
+    // tiles 0 .. kDmaSteps resident
+    sync_slots(std::integral_constant<int, 2 * (D - kDmaSteps - 1)>{});
+    f32x16 sa[NKT][QT], sb[NKT][QT];
+    scores_d(sa, std::integral_constant<int, 0>{});
+    mask(sa, 0);  // a key range shorter than one tile
+    {
+      float mt[QT];
+      row_max(sa, mt);
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt) m_run[qt] = mt[qt];
+    }
+    bool over = false;
+    // step t (I = t % NSL): issue tile t + D; S_{t+1} = K_{t+1} Q^T; P_t; O += V_t P_t;
+    // then tile t + 2 must be resident (2 (D - 2) loads of later tiles may be in flight)
+    auto step = [&](auto i_t, auto masked_t, f32x16 (&sc)[NKT][QT], f32x16 (&sn)[NKT][QT], int t) {
+      constexpr int I = decltype(i_t)::value;
+      constexpr bool MASKED = decltype(masked_t)::value;
+      issue(t + D, std::integral_constant<int, (I + D) % NSL>{});
+      scores_d(sn, std::integral_constant<int, (I + 1) % NSL>{});
+      if constexpr (MASKED) mask(sn, t + 1);
+      bf16x8 pb[NKT][QT][2];
+      bf16x8 pl[NKT][QT][2];
+      softmax(sc, pb, pl);
+      pv_d(pb, std::integral_constant<int, I % NSL>{});
+      // a barrier after every kDmaSteps steps: the next group reads up to tile
+      // t + kDmaSteps + 1, and 2 (D - kDmaSteps - 1) loads of later tiles may be in flight
+      if constexpr (I % kDmaSteps == kDmaSteps - 1)
+        sync_slots(std::integral_constant<int, 2 * (D - kDmaSteps - 1)>{});
+    };
+    auto steps = [&](auto masked_t, int t) {
+      static_for<NSL / 2>([&](auto h_t) {
+        constexpr int H = decltype(h_t)::value;
+        step(std::integral_constant<int, 2 * H>{}, masked_t, sa, sb, t + 2 * H);
+        step(std::integral_constant<int, 2 * H + 1>{}, masked_t, sb, sa, t + 2 * H + 1);
+      });
+    };
+    const int t_full = (k_end - k_begin) / KT;
+    int t = 0;
+    for (; t + NSL < t_full; t += NSL) steps(std::false_type{}, t);
+    for (; t < ntiles; t += NSL) steps(std::true_type{}, t);
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) over |= !(l_part[qt] <= kBigSum);
+    if (__ballot(over) != 0) overflow = 1;
+    // every load has landed before the slots are given up
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+  } else if constexpr (!SAFE) {
     // Software pipeline over four LDS slots (tile t in slot t % 4) and NSET register
     // staging sets (tile j is loaded into set j % NSET). Step t:
     //   issue the loads of tile t + NSET + 1;

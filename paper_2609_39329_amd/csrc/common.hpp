@@ -4,6 +4,9 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+#include <utility>
+
 namespace pkv {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -20,6 +23,16 @@ constexpr int kWave = 64;
 constexpr int kXcds = 8;  // MI355X: 8 accelerator complex dies, each with its own L2
 
 #define PKV_LDS __attribute__((address_space(3)))
+
+// f(integral_constant<int, I>) for I = 0..N-1, unrolled at compile time
+template <class F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
 
 // D(32x32, f32) += A(32x16, bf16) * B(16x32, bf16).
 // Lane l holds A[row l%32][k (l/32)*8 + t] and B[k (l/32)*8 + t][col l%32], t = 0..7;

@@ -789,16 +789,6 @@ __device__ __forceinline__ double bcast(double x, int src_lane) {
 __device__ __forceinline__ float rsq_of(float x) { return __builtin_amdgcn_rsqf(x); }
 __device__ __forceinline__ double rsq_of(double x) { return rsq64(x); }
 
-// f(integral_constant<int, I>) for I = 0..N-1, unrolled at compile time
-template <class F, int... I>
-__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
-  (f(std::integral_constant<int, I>{}), ...);
-}
-template <int N, class F>
-__device__ __forceinline__ void static_for(F&& f) {
-  static_for_impl(f, std::make_integer_sequence<int, N>{});
-}
-
 // One wave: factor the SPD N x N block S (lower triangle read) and write
 // X = L^{-1} (lower, zeros above) to Xo, in one right-looking sweep.
 // Lane r (and its copies r + N, r + 2N, .., which repeat the same work so the wave
