@@ -33,6 +33,10 @@ SHAPES = [
     (50, 333, 100, 8, 2, 128, "f32"),
     (8, 20000, 3000, 4, 2, 64, "f32"),      # fp32 split-key path
     (1, 1, 1, 4, 2, 64, "bf16"),            # degenerate: one query, one key, one entry
+    # one row tile per KV head: the keys split into 32-key ranges, the last one 8 (9)
+    # keys long, so a work item's first tile is already past its range's end
+    (1, 1000, 7, 4, 2, 128, "bf16"),
+    (2, 1001, 9, 8, 2, 64, "bf16"),
     (1, 1, 1, 4, 2, 128, "f32"),
 ]
 
