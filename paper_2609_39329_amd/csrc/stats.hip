@@ -158,7 +158,8 @@ __global__ __launch_bounds__(256) void split_transpose_kernel(const SRC* __restr
 // Kp of 64), so the main loop has no bounds checks. Each K chunk loads every plane
 // once and applies all term products to it: term t multiplies plane a(t) = bit t of
 // TA with plane b(t) = bit t of TB. 256 x 256 tiles, 8 waves of 128 x 64, two LDS
-// stages with the next chunk prefetched into registers. The MFMA computes the
+// stages, the next chunk loaded straight into LDS while the current one is multiplied.
+// The MFMA computes the
 // transposed tile (rows = output columns), so a lane owns 4 consecutive output
 // columns and the epilogue uses 16-byte accesses. SYM: only tiles with
 // tile_i <= tile_j; the diagonal tiles keep their i <= j half and every tile is
@@ -179,7 +180,7 @@ struct BGemm {
   int vec_out;
 };
 
-constexpr int BG_T = 256, BG_WM = 128, BG_WN = 64, BG_KC = 32, BG_PK = BG_KC + 8;
+constexpr int BG_T = 256, BG_WM = 128, BG_WN = 64, BG_KC = 32;
 constexpr int BG_THREADS = (BG_T / BG_WM) * (BG_T / BG_WN) * 64;  // 512
 
 template <int NA, int NB, int NT, int TA, int TB, bool SYM>
@@ -187,7 +188,7 @@ __global__ __launch_bounds__(BG_THREADS, 1) void bgemm_kernel(BGemm p) {
   constexpr int ROWS = (NA + NB) * BG_T;            // stacked plane rows per stage
   constexpr int LPT = ROWS * (BG_KC / 8) / BG_THREADS;  // 16-byte loads per thread
   constexpr int MA = BG_WM / 32, MB = BG_WN / 32;
-  __shared__ __attribute__((aligned(16))) __bf16 lds[2][ROWS * BG_PK];
+  __shared__ __attribute__((aligned(16))) __bf16 lds[2][ROWS * BG_KC];
   int ti, tj;
   {
     const int t = xcd_item((p.ntiles + kXcds - 1) / kXcds);
@@ -217,49 +218,67 @@ __global__ __launch_bounds__(BG_THREADS, 1) void bgemm_kernel(BGemm p) {
 #pragma unroll
     for (int b = 0; b < MB; ++b) acc[a][b] = f32x16{};
 
-  // piece c: stacked row c / 4 (plane (row / 256), row % 256 within it), k (c % 4) * 8
-  u32x4 rg[LPT];
-  auto fetch = [&](int q) {
-    const int k0 = q * BG_KC;
-#pragma unroll
-    for (int u = 0; u < LPT; ++u) {
-      const int c = u * BG_THREADS + tid;
-      const int row = c >> 2, kk = (c & 3) * 8;
-      const int pl = row / BG_T, rr = row % BG_T;  // pl is uniform per u
-      const __bf16* src = pl < NA ? p.A[pl] + (int64_t)(i0 + rr) * p.ld
-                                  : p.B[pl - NA] + (int64_t)(j0 + rr) * p.ld;
-      rg[u] = *(const u32x4*)(src + k0 + kk);
-    }
+  // The K chunks go from HBM straight into LDS (buffer_load ... lds; no staging
+  // registers), two stages of unpadded [stacked row][32 k] tiles. LDS position c of a
+  // stage (16 bytes) holds stacked row c / 4, k chunk (c % 4) ^ ((row / 4) % 4): the 16
+  // consecutive rows an MFMA fragment read takes at one k chunk land in 16 different
+  // bank groups. Thread tid fills positions u * 512 + tid, u < LPT: rows u * 128 + tid / 4,
+  // which lie in plane u / 2 (256 rows per plane).
+  // buffer descriptors of the planes' 256 rows of this tile (unused ones repeat plane 0;
+  // plain variables: the host pass drops the kernel if a descriptor is a temporary)
+  auto plane_base = [&](int pl) {
+    return pl < NA ? p.A[pl] + (int64_t)i0 * p.ld : p.B[pl - NA] + (int64_t)j0 * p.ld;
   };
-  auto stash = [&](int buf) {
-#pragma unroll
-    for (int u = 0; u < LPT; ++u) {
-      const int c = u * BG_THREADS + tid;
-      const int row = c >> 2, kk = (c & 3) * 8;
-      *(u32x4*)(&lds[buf][row * BG_PK + kk]) = rg[u];
-    }
+  const uint32_t plane_bytes = (uint32_t)(BG_T * p.ld * 2);
+  const __amdgpu_buffer_rsrc_t rs0 =
+      __builtin_amdgcn_make_buffer_rsrc((void*)plane_base(0), 0, plane_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rs1 = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)plane_base(NA + NB > 1 ? 1 : 0), 0, plane_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rs2 = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)plane_base(NA + NB > 2 ? 2 : 0), 0, plane_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rs3 = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)plane_base(NA + NB > 3 ? 3 : 0), 0, plane_bytes, 0x00020000);
+  static_assert(NA + NB <= 4, "at most four planes");
+  static_assert(LPT == 2 * (NA + NB), "two 128-row pieces per plane");
+  const uint32_t voff0 = (uint32_t)(((tid / 4) * p.ld + (((tid % 4) ^ ((tid / 16) % 4)) * 8)) * 2);
+  const uint32_t voff1 = voff0 + (uint32_t)(128 * p.ld * 2);
+  auto issue = [&](int q, int buf) {
+    const uint32_t k0b = (uint32_t)(q * BG_KC * 2);
+    static_for<LPT>([&](auto u_t) {
+      constexpr int u = decltype(u_t)::value;
+      PKV_LDS void* dst = (PKV_LDS void*)&lds[buf][(u * BG_THREADS + wid * 64) * 8];
+      const uint32_t vo = (u & 1) ? voff1 : voff0;
+      if constexpr (u / 2 == 0) __builtin_amdgcn_raw_ptr_buffer_load_lds(rs0, dst, 16, vo, k0b, 0, 0);
+      else if constexpr (u / 2 == 1) __builtin_amdgcn_raw_ptr_buffer_load_lds(rs1, dst, 16, vo, k0b, 0, 0);
+      else if constexpr (u / 2 == 2) __builtin_amdgcn_raw_ptr_buffer_load_lds(rs2, dst, 16, vo, k0b, 0, 0);
+      else __builtin_amdgcn_raw_ptr_buffer_load_lds(rs3, dst, 16, vo, k0b, 0, 0);
+    });
   };
+  // every load of this wave has landed, then a plain barrier (the workgroup fence of
+  // __syncthreads adds nothing here)
+  auto landed = [&]() { asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory"); };
+  const int sw = (l32 / 4) % 4;
 
-  fetch(0);
-  stash(0);
-  __syncthreads();
+  issue(0, 0);
+  landed();
   for (int q = 0; q < nq; ++q) {
     const int buf = q & 1;
-    if (q + 1 < nq) fetch(q + 1);
+    if (q + 1 < nq) issue(q + 1, buf ^ 1);
     const __bf16* L0 = lds[buf];
 #pragma unroll
     for (int ks = 0; ks < BG_KC; ks += 16) {
+      const int ch = ((2 * (ks / 16) + h32) ^ sw) * 8;  // k chunk of this lane, swizzled
       bf16x8 fa[NA][MA], fb[NB][MB];
 #pragma unroll
       for (int pa = 0; pa < NA; ++pa)
 #pragma unroll
         for (int a = 0; a < MA; ++a)
-          fa[pa][a] = *(const bf16x8*)(L0 + (pa * BG_T + wi + 32 * a + l32) * BG_PK + ks + 8 * h32);
+          fa[pa][a] = *(const bf16x8*)(L0 + (pa * BG_T + wi + 32 * a + l32) * BG_KC + ch);
 #pragma unroll
       for (int pb = 0; pb < NB; ++pb)
 #pragma unroll
         for (int b = 0; b < MB; ++b)
-          fb[pb][b] = *(const bf16x8*)(L0 + ((NA + pb) * BG_T + wj + 32 * b + l32) * BG_PK + ks + 8 * h32);
+          fb[pb][b] = *(const bf16x8*)(L0 + ((NA + pb) * BG_T + wj + 32 * b + l32) * BG_KC + ch);
 #pragma unroll
       for (int t = 0; t < NT; ++t)
 #pragma unroll
@@ -268,8 +287,7 @@ __global__ __launch_bounds__(BG_THREADS, 1) void bgemm_kernel(BGemm p) {
           for (int b = 0; b < MB; ++b)
             acc[a][b] = mfma32(fb[(TB >> t) & 1][b], fa[(TA >> t) & 1][a], acc[a][b]);
     }
-    if (q + 1 < nq) stash(buf ^ 1);
-    __syncthreads();
+    landed();
   }
 
   // lane owns Out[i0+wi+32a+l32][j0+wj+32b+8g+4h32 .. +3]
