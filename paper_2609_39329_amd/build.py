@@ -59,6 +59,13 @@ def build(verbose: bool = False) -> str:
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"linking failed:\n{' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
+    # a library that links can still fail to load (a kernel whose host-side launch stub
+    # the compiler did not emit leaves an undefined symbol): load it in a child process,
+    # with every symbol resolved, before it replaces the previous build
+    chk = [sys.executable, "-c", "import ctypes, os, sys; ctypes.CDLL(sys.argv[1], mode=os.RTLD_NOW)", tmp]
+    r = subprocess.run(chk, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"the linked library does not load:\n{r.stderr}")
     os.replace(tmp, LIB)
     if verbose:
         print(f"built {LIB}", file=sys.stderr)
