@@ -134,7 +134,7 @@ int patchkv_attend_compressed(int dtype, const void* Q, const void* K, const voi
 
 /* ------------------------------------------------------------------------- */
 /* Attention of one reference chunk over a cache plus the chunk's own causal    */
-/* prefix (Sec. 2.4, chunked query encoding; Alg. 1, loop over reference       */
+/* prefix (Sec. 2.3, chunked query encoding; Alg. 1, loop over reference       */
 /* chunks). The chunk's M tokens are the queries; token m attends over every    */
 /* cache entry and over the chunk's own entries 0..m (itself included), never   */
 /* over other chunks:                                                          */
@@ -167,7 +167,7 @@ int patchkv_attend_chunk(int dtype, const void* Q, const void* K, const void* V,
 
 /* ------------------------------------------------------------------------- */
 /* Attention over a compressed cache in the storage formats of Sec. 3.1 and     */
-/* Sec. 4 (attention-matching logit bias; quantized KV caches):                */
+/* App. C (attention-matching logit bias; quantized KV caches):              */
 /*   O[m, h*dh + j] = sum_n softmax_n(scale <Q[m,h,:], K_n> + bias[g, n]) V_n[j] */
 /* over the n_cache entries of KV head g = floor(h / (Hq/Hkv)).                 */
 /*  - kv_format PATCHKV_KV_PLAIN: K, V [Hkv][n_src][dh] in dtype; Ke, Ve NULL.   */
@@ -209,7 +209,7 @@ int patchkv_compute_targets(int w_dtype, const float* Of, const float* Oc, const
                             void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------- */
-/* The MLP-shaped block (Sec. 2.3, "MLP activation matching"; Alg. 1). The      */
+/* The MLP-shaped block (Sec. 2.2, "MLP activation matching"; Alg. 1). The      */
 /* block output is y = h W + z: z [M][d] is the attention output, h [M][d_ff]   */
 /* the post-activation SwiGLU intermediate, W [d_ff][d] the down-projection     */
 /* that the patch corrects. The MLP reads z through an RMS norm with unit gain.  */
@@ -290,7 +290,7 @@ int patchkv_solve_patch(int acc_dtype, const void* G, const void* C, int64_t d_i
                         void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------- */
-/* Reduced-rank patch (App., low-rank weight patches; reduced-rank regression): */
+/* Reduced-rank patch (App. C, low-rank weight patches; reduced-rank regression):*/
 /* the ridge patch projected onto its top-r output subspace. In row form,       */
 /*   dW_r = dW U_r U_r^T,  U_r [d_out][r] = top-r eigenvectors of dW^T G dW,    */
 /* stored as the factors A = dW U_r [d_in][r] and U_r, (d_in + d_out) r floats. */

@@ -16,14 +16,14 @@ What it computes, per transformer block (paper, Sec. 2.2-2.3 and Alg. 1):
   (a5) ridge patch  Delta W = S_T (S_H + lambda I)^{-1}                 (Eq. 8),
        with lambda absolute or adaptive, lambda_0 ||S_H||_F^2 / tr S_H   (Eq. 7).
 
-and, for a reference set split into chunks (Sec. 2.4, chunked query encoding;
+and, for a reference set split into chunks (Sec. 2.3, chunked query encoding;
 Alg. 1, the loop over reference chunks):
 
   (f2) each chunk's tokens attend over the cache and over the chunk's own
        causal prefix (cross-chunk attention dropped); the statistics of all
        chunks are summed before the single solve.
 
-and, for the MLP-shaped patch of the paper's own block (Sec. 2.3; Alg. 1):
+and, for the MLP-shaped patch of the paper's own block (Sec. 2.2; Alg. 1):
 
   (f3) h = SwiGLU features of the normalised attention output, W the
        d_ff x d down-projection, z the attention output; targets
@@ -56,7 +56,8 @@ Readings where the paper is silent (each is also listed in the design notes):
   values serve both passes there; in general each pass takes its own.
 
 Parity pins for every function live in the CPU test suite (closed forms,
-invariants, brute force, library routines). Nothing here is "parity unpinned".
+invariants, brute force, library routines, hand-written bf16 bit patterns, and
+the whole block composed from independently written pieces).
 """
 from __future__ import annotations
 
@@ -127,7 +128,7 @@ def attention(Q: np.ndarray, K: np.ndarray, V: np.ndarray, scale: float | None =
 
 
 def dequantize_mx(q: np.ndarray, e: np.ndarray, block: int = 32) -> np.ndarray:
-    """A block-scaled integer cache entry (Sec. 4, quantized KV caches) as float64:
+    """A block-scaled integer cache entry (App. C, quantized KV caches) as float64:
     value = q * 2^e, q [..., dh] integers, e [..., dh / block] one power-of-two
     exponent per block of ``block`` consecutive channels."""
     q = np.asarray(q, dtype=np.float64)
@@ -144,7 +145,7 @@ def attention_rows(Q: np.ndarray, K: np.ndarray, V: np.ndarray, rows: np.ndarray
 def attention_chunk(Q: np.ndarray, K: np.ndarray, V: np.ndarray, Ks: np.ndarray,
                     Vs: np.ndarray, scale: float | None = None,
                     max_score_bytes: int = 1 << 28) -> np.ndarray:
-    """One reference chunk's attention (Sec. 2.4, chunked query encoding; Alg. 1).
+    """One reference chunk's attention (Sec. 2.3, chunked query encoding; Alg. 1).
 
     Q [Mc, Hq, dh] are the chunk's queries, K and V [Hkv, Nk, dh] the cache (full
     or compressed), Ks and Vs [Hkv, Mc, dh] the chunk's own keys and values. Query
@@ -274,7 +275,7 @@ def layer_patch(inp, rho: int = 1, mode: str = "absolute", lam: float | None = N
 
 def layer_patch_chunked(inp, chunks, rho: int = 1, mode: str = "absolute",
                         lam: float | None = None) -> dict:
-    """One block's patch from a reference set split into chunks (Sec. 2.4; Alg. 1).
+    """One block's patch from a reference set split into chunks (Sec. 2.3; Alg. 1).
 
     ``inp`` is a ``workloads`` LayerInputs (the cache, the compressed cache and W);
     ``chunks`` yields per-chunk (Q, Ks, Vs) in the same stored form. For every chunk
@@ -316,7 +317,7 @@ def silu(X: np.ndarray) -> np.ndarray:
 
 
 def mlp_features(Z: np.ndarray, Wg: np.ndarray, Wu: np.ndarray, eps: float = 1e-5) -> np.ndarray:
-    """The post-activation MLP intermediate h of Sec. 2.3 for a SwiGLU block whose
+    """The post-activation MLP intermediate h of Sec. 2.2 for a SwiGLU block whose
     MLP reads the attention output z: u = rms_norm(z), h = silu(u Wg) * (u Wu).
     Z [M, d], Wg and Wu [d, d_ff]; returns H [M, d_ff]."""
     U = rms_norm(Z, eps)
@@ -337,7 +338,7 @@ def propagate_student(Hc: np.ndarray, W: np.ndarray, dW: np.ndarray, Zc: np.ndar
 
 
 def mlp_layer_patch(inp, mlp, mode: str = "absolute", lam: float | None = None) -> dict:
-    """The MLP-shaped patch of one block (Sec. 2.3; Alg. 1), all in fp64.
+    """The MLP-shaped patch of one block (Sec. 2.2; Alg. 1), all in fp64.
 
     ``inp``: a ``workloads`` LayerInputs (queries, caches); ``mlp``: MlpWeights
     with Wg, Wu [d, d_ff] and Wd [d_ff, d] (stored form) and eps. Teacher and
@@ -366,7 +367,7 @@ def mlp_layer_patch(inp, mlp, mode: str = "absolute", lam: float | None = None) 
 
 
 def low_rank_patch(G0: np.ndarray, dW: np.ndarray, r: int) -> dict:
-    """The reduced-rank patch (App., low-rank weight patches; reduced-rank regression).
+    """The reduced-rank patch (App. C, low-rank weight patches; reduced-rank regression).
 
     In the paper's column form the ridge patch is projected onto its top-r output
     subspace, U_r U_r^T dW, with U_r the top-r eigenvectors of dW S_H dW^T. In row

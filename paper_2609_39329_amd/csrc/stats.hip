@@ -1,7 +1,7 @@
 // Targets and sufficient statistics (Eq. 5 and Eq. 9, row form):
 //   T = (O_f - O_c) W + rho (O_f - O_c)
 //   G (+)= X^T X,   C (+)= X^T (Yf - Yc)
-// and the MLP-shaped block (Sec. 2.3; Alg. 1): SwiGLU features of the RMS-normed
+// and the MLP-shaped block (Sec. 2.2; Alg. 1): SwiGLU features of the RMS-normed
 // attention output, targets through the down-projection plus the attention
 // residual, and the student state through the patched block.
 //

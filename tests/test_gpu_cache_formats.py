@@ -1,5 +1,5 @@
 """GPU parity of attention over compressed caches in the formats of Sec. 3.1 and
-Sec. 4: a per-entry logit bias (attention matching) and block-scaled int8 / int4
+App. C: a per-entry logit bias (attention matching) and block-scaled int8 / int4
 entries (quantized KV caches), against the fp64 oracle.
 
 Block-scaled entries are exact in bf16, so the tolerances are those of the plain

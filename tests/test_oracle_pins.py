@@ -843,3 +843,123 @@ def test_low_rank_pins_catch_planted_mistakes():
 
     for f in (bottom, no_gram, truncated_svd):
         assert check_low_rank(f) > 1e-4
+
+
+# ------------------------------------------- stored-input decoding and block composition
+
+def check_decode_bf16(dec) -> bool:
+    """Hand-written bf16 bit patterns decode to their values, and a random array decodes
+    as torch's own bfloat16 reinterpretation of the same bits does."""
+    cases = [(0x3F80, 1.0), (0xC000, -2.0), (0x3E80, 0.25), (0x4049, 3.140625),
+             (0x7F7F, (2.0 - 2.0 ** -7) * 2.0 ** 127),     # largest finite bf16
+             (0x0080, 2.0 ** -126),                      # smallest normal
+             (0x0001, 2.0 ** -133),                      # smallest subnormal
+             (0x8000, -0.0), (0x7F80, math.inf), (0xFF80, -math.inf)]
+    bits = np.array([c[0] for c in cases], dtype=np.uint16)
+    got = np.asarray(dec(bits, "bf16"), dtype=np.float64)
+    want = np.array([c[1] for c in cases])
+    ok = got.shape == want.shape and bool(np.array_equal(got, want))
+    ok = ok and bool(np.signbit(got[7])) and not bool(np.signbit(got[0]))
+    rnd = np.random.default_rng(77).integers(0, 1 << 16, size=4096, dtype=np.uint16)
+    rnd = rnd[(rnd & 0x7F80) != 0x7F80]                 # finite values (no inf / NaN)
+    ref = torch.from_numpy(rnd.view(np.int16).copy()).view(torch.bfloat16).double().numpy()
+    got = np.asarray(dec(rnd, "bf16"), dtype=np.float64)
+    return ok and got.shape == ref.shape and bool(np.array_equal(got, ref))
+
+
+def test_decode_bf16_bit_patterns_and_torch_view():
+    assert check_decode_bf16(oracle.decode)
+    x = np.random.default_rng(78).standard_normal(257).astype(np.float32)
+    assert np.array_equal(oracle.decode(x, "f32"), x.astype(np.float64))
+
+
+def _torch_decode(a, dtype):
+    """Stored input -> float64 through torch's own bf16 type (not the oracle's decode)."""
+    if dtype == "bf16":
+        t = torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16)
+        return t.double().numpy()
+    return np.asarray(a, dtype=np.float32).astype(np.float64)
+
+
+def _composed_patch(inp, rho):
+    """One block's patch composed from independently written pieces (Eq. 4-6):
+    scalar-loop attention for both caches, each token's block output y = h W + rho z
+    under either cache, the per-token target as the block-output discrepancy of
+    Eq. 4 (teacher minus student), and Eq. 6 as a stacked least-squares problem."""
+    dt = inp.dtype
+    Q, K, V, W = (_torch_decode(a, dt) for a in (inp.Q, inp.K, inp.V, inp.W))
+    if inp.idx is not None:
+        Kc = np.stack([[K[g, n] for n in inp.idx] for g in range(inp.Hkv)])
+        Vc = np.stack([[V[g, n] for n in inp.idx] for g in range(inp.Hkv)])
+    else:
+        Kc, Vc = _torch_decode(inp.Kc, dt), _torch_decode(inp.Vc, dt)
+    Hf = brute_attention(Q, K, V, inp.scale)            # teacher features h (and z)
+    Hc = brute_attention(Q, Kc, Vc, inp.scale)          # student features h' (and z')
+    Yf = np.array([h @ W + rho * h for h in Hf])        # teacher block outputs
+    Yc = np.array([h @ W + rho * h for h in Hc])        # unpatched student block outputs
+    T = Yf - Yc
+    d = W.shape[0]
+    A = np.vstack([Hc, np.sqrt(inp.lam) * np.eye(d)])
+    Bm = np.vstack([T, np.zeros((d, W.shape[1]))])
+    dW = np.linalg.lstsq(A, Bm, rcond=None)[0]
+    return dW, Hc, Yf, Yc, W
+
+
+def check_layer_patch(fn) -> float:
+    """Worst relative error of fn(inp, rho)["dW"] against the composed patch over both
+    cache kinds, both input dtypes and rho in {0, 1}; a patch that does not move the
+    student's block output toward the teacher's scores inf."""
+    worst = 0.0
+    for k, (cache, dt) in enumerate([("evict", "bf16"), ("synthesize", "f32"),
+                                     ("evict", "f32"), ("synthesize", "bf16")]):
+        inp = make_custom_inputs(M=6, N=11, B=4, Hq=4, Hkv=2, dh=4, dtype=dt, cache=cache,
+                                 n_mix=3, lam=0.05, seed=40 + k)
+        for rho in (0, 1):
+            ref, Hc, Yf, Yc, W = _composed_patch(inp, rho)
+            got = fn(inp, rho)["dW"]
+            worst = max(worst, rel(got, ref))
+            patched = Hc @ (W + got) + rho * Hc
+            if not np.linalg.norm(patched - Yf) < np.linalg.norm(Yc - Yf):
+                return math.inf
+    return worst
+
+
+def test_layer_patch_composed_from_independent_pieces():
+    assert check_layer_patch(lambda inp, rho: oracle.layer_patch(inp, rho=rho)) < 1e-10
+
+
+def test_decode_and_layer_patch_pins_catch_planted_mistakes():
+    def decode_shift15(x, dtype):
+        a = np.ascontiguousarray(x, dtype=np.uint16).astype(np.uint32) << np.uint32(15)
+        with np.errstate(invalid="ignore"):
+            return a.view(np.float32).astype(np.float64)    # wrong shift
+
+    def decode_half(x, dtype):
+        return np.ascontiguousarray(x, dtype=np.uint16).view(np.float16).astype(np.float64)
+
+    def layer_patch_swapped(inp, rho):
+        dt = inp.dtype
+        Q, K, V, W = (oracle.decode(a, dt) for a in (inp.Q, inp.K, inp.V, inp.W))
+        Kc, Vc = (oracle.gather_cache(K, V, inp.idx) if inp.idx is not None
+                  else (oracle.decode(inp.Kc, dt), oracle.decode(inp.Vc, dt)))
+        Of = oracle.attention(Q, K, V, inp.scale)
+        Oc = oracle.attention(Q, Kc, Vc, inp.scale)
+        T = oracle.targets(Oc, Of, W, rho)                   # student minus teacher
+        G, C = oracle.normal_equations(Oc, T)
+        return {"dW": oracle.solve_patch(G, C, inp.lam)}
+
+    def layer_patch_teacher_basis(inp, rho):
+        dt = inp.dtype
+        Q, K, V, W = (oracle.decode(a, dt) for a in (inp.Q, inp.K, inp.V, inp.W))
+        Kc, Vc = (oracle.gather_cache(K, V, inp.idx) if inp.idx is not None
+                  else (oracle.decode(inp.Kc, dt), oracle.decode(inp.Vc, dt)))
+        Of = oracle.attention(Q, K, V, inp.scale)
+        Oc = oracle.attention(Q, Kc, Vc, inp.scale)
+        T = oracle.targets(Of, Oc, W, rho)
+        G, C = oracle.normal_equations(Of, T)                # teacher features as basis
+        return {"dW": oracle.solve_patch(G, C, inp.lam)}
+
+    assert not check_decode_bf16(decode_shift15)
+    assert not check_decode_bf16(decode_half)
+    assert check_layer_patch(layer_patch_swapped) > 1e-2
+    assert check_layer_patch(layer_patch_teacher_basis) > 1e-2

@@ -1,6 +1,6 @@
 """The synthetic workload shapes.
 
-Each stands in for a setting the paper measures (Sec. 3 and App. B): contexts up to
+Each stands in for a setting the paper measures (Sec. 3.1 and App. C): contexts up to
 ~170K tokens, aggressive cache budgets (down to ~1 % of the context), and one
 reference chunk of a few thousand query tokens per block. The model shapes are
 those of Llama-3-8B (d=4096, 32 query / 8 KV heads, head_dim 128) and Qwen-2.5-7B
