@@ -103,6 +103,8 @@ class LayerDev:
         if mlp is not None:
             self.Wg, self.Wu, self.Wd, self.eps = t(mlp.Wg), t(mlp.Wu), t(mlp.Wd), mlp.eps
         self.idx = (torch.from_numpy(inp.idx).to(dev) if inp.idx is not None else None)
+        # per-KV-head index sets keep different numbers of entries per head
+        self.counts = (torch.from_numpy(inp.counts).to(dev) if inp.counts is not None else None)
         self.Kc = t(inp.Kc) if inp.Kc is not None else None
         self.Vc = t(inp.Vc) if inp.Vc is not None else None
 
@@ -149,9 +151,10 @@ def layer_steps(pkv, cfg, L, bufs, li: int, events=None):
                          scale=cfg.scale, p_terms=2, O=bufs.Oc)
     elif L.bias is not None:
         pkv.attend_cache(L.Q, *((L.K, L.V) if L.idx is not None else (L.Kc, L.Vc)), idx=L.idx,
-                         bias=L.bias, scale=cfg.scale, p_terms=2, O=bufs.Oc)
+                         counts=L.counts, bias=L.bias, scale=cfg.scale, p_terms=2, O=bufs.Oc)
     elif L.idx is not None:
-        pkv.attend_compressed(L.Q, L.K, L.V, idx=L.idx, scale=cfg.scale, O=bufs.Oc)
+        pkv.attend_compressed(L.Q, L.K, L.V, idx=L.idx, counts=L.counts, scale=cfg.scale,
+                              O=bufs.Oc)
     else:
         pkv.attend_compressed(L.Q, L.Kc, L.Vc, scale=cfg.scale, O=bufs.Oc)
     if cfg.d_ff:  # MLP-shaped patch
@@ -184,7 +187,8 @@ def chunked_layer_steps(pkv, cfg, L, bufs, li: int, events=None):
         if events is not None:
             events[j][1].record()
         if L.idx is not None:
-            pkv.attend_chunk(Q, L.K, L.V, Ks, Vs, idx=L.idx, scale=cfg.scale, p_terms=2, O=bufs.Oc)
+            pkv.attend_chunk(Q, L.K, L.V, Ks, Vs, idx=L.idx, counts=L.counts, scale=cfg.scale,
+                             p_terms=2, O=bufs.Oc)
         else:
             pkv.attend_chunk(Q, L.Kc, L.Vc, Ks, Vs, scale=cfg.scale, p_terms=2, O=bufs.Oc)
         pkv.compute_targets(bufs.Of, bufs.Oc, L.W, rho=1, T=bufs.T)
@@ -223,7 +227,7 @@ def cpu_baseline(cfg, rows: int) -> dict:
         unq = (lambda a: a) if qc.bits == 8 else unpack_int4
         Kc, Vc = oracle.dequantize_mx(unq(qc.Kq), qc.Ke), oracle.dequantize_mx(unq(qc.Vq), qc.Ve)
     elif inp.idx is not None:
-        Kc, Vc = oracle.gather_cache(K, V, inp.idx)
+        Kc, Vc = oracle.gather_cache(K, V, inp.idx, inp.counts)
     else:
         Kc, Vc = oracle.decode(inp.Kc, dt), oracle.decode(inp.Vc, dt)
     if ch is None:

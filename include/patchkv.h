@@ -79,6 +79,32 @@ typedef enum {
   PATCHKV_SOLVE_EXACT_F32 = 16
 } patchkv_ridge_mode;
 
+/* Index sets of an eviction-style compressed cache (the `idx_mode` argument).    */
+/* KVzip, the paper's eviction method, scores KV pairs with global head scoring  */
+/* (App. B.1; Sec. 3.1), so each KV head keeps its own tokens, and not           */
+/* necessarily as many as the others.                                          */
+typedef enum {
+  PATCHKV_IDX_SHARED = 0,  /* idx [B] int32: one set of cache rows for every KV head */
+  PATCHKV_IDX_PER_HEAD = 1 /* idx [Hkv][B] int32: KV head g keeps rows idx[g][0..B) */
+} patchkv_idx_mode;
+
+/* Shared by the compressed-cache calls (attend_compressed, attend_chunk,
+ * attend_cache, compute_layer_patch):
+ *  - counts (optional, device int32 [Hkv], 4-byte aligned): KV head g's compressed
+ *    cache is only its first counts[g] entries (idx[g][0..counts[g]) per head, the
+ *    first counts[g] entries of a shared set, or of the rows of a contiguous cache);
+ *    NULL means B for every head. Each count must lie in [1, B]; a count outside is
+ *    clamped into that range and reported through info.
+ *  - Every index entry a head uses must lie in [0, N). An entry outside reads as a
+ *    zero row (no memory outside the cache is touched) and is reported.
+ *  - info (device int32, 4-byte aligned; optional for the attend_* calls): written 0
+ *    when every used entry and every count is in range; otherwise -(1 + c) for the
+ *    smallest offending code c, where an entry at flat position q of idx (q = b for
+ *    a shared set, g * B + b per head) has code q and the count of head g has code
+ *    E + g, E being the number of entries in idx (B shared, Hkv * B per head, 0 with
+ *    no idx). compute_layer_patch reports such an input error in its info word in
+ *    place of the solve's result.                                              */
+
 /* Storage of a cache's keys and values (patchkv_attend_cache). */
 typedef enum {
   PATCHKV_KV_PLAIN = 0,  /* K, V in the call's dtype */
@@ -120,17 +146,19 @@ int patchkv_attend_full(int dtype, const void* Q, const void* K, const void* V,
 
 /* The same attention over a compressed cache of B entries (Alg. 1, student     */
 /* forward; Sec. 2.1 compressed cache C_b).                                     */
-/*  - idx != NULL: eviction subset. K, V are the FULL cache [Hkv][N][dh] and the */
-/*    compressed cache is K[:, idx[b], :], V[:, idx[b], :] for b < B, gathered   */
-/*    on the fly. idx [B] int32, every entry in [0, N) (precondition; no memory  */
-/*    outside the cache is read for entries outside it: the bf16 path reads     */
-/*    them as zero rows, the f32 path clamps them into range).                  */
-/*  - idx == NULL: synthesized cache. K, V are [Hkv][B][dh]; N is ignored.       */
+/*  - idx != NULL: eviction subset. K, V are the FULL cache [Hkv][N][dh]; the    */
+/*    compressed cache of KV head g is rows idx[b] (PATCHKV_IDX_SHARED, idx [B]) */
+/*    or idx[g][b] (PATCHKV_IDX_PER_HEAD, idx [Hkv][B]) of K[g], V[g], gathered  */
+/*    on the fly.                                                              */
+/*  - idx == NULL: synthesized cache. K, V are [Hkv][B][dh]; N is ignored;       */
+/*    idx_mode must be PATCHKV_IDX_SHARED.                                     */
+/* counts and info as described above patchkv_kv_format (info may be NULL).     */
 /* The workspace size is patchkv_attend_workspace_bytes(dtype, M, B, ...).       */
 int patchkv_attend_compressed(int dtype, const void* Q, const void* K, const void* V,
-                              const int32_t* idx, int64_t M, int64_t N, int64_t B,
-                              int Hq, int Hkv, int dh, float scale,
-                              float* O, void* workspace, size_t workspace_bytes, void* stream);
+                              const int32_t* idx, int idx_mode, const int32_t* counts,
+                              int64_t M, int64_t N, int64_t B, int Hq, int Hkv, int dh,
+                              float scale, float* O, int32_t* info, void* workspace,
+                              size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------- */
 /* Attention of one reference chunk over a cache plus the chunk's own causal    */
@@ -143,9 +171,12 @@ int patchkv_attend_compressed(int dtype, const void* Q, const void* K, const voi
 /*   the own entries Ks[g, 0..m, :] / Vs[g, 0..m, :].                           */
 /* The cache:                                                                  */
 /*  - idx != NULL: K, V [Hkv][n_src][dh] and the cache is rows idx[0..n_cache)  */
-/*    (eviction subset, gathered on the fly; every idx entry in [0, n_src)).   */
+/*    (idx_mode SHARED) or idx[g][0..n_cache) (PER_HEAD) of head g (eviction    */
+/*    subset, gathered on the fly; entries in [0, n_src)).                      */
 /*  - idx == NULL: rows 0..n_cache of K, V [Hkv][n_src][dh] (n_cache <= n_src); */
 /*    n_cache = n_src is the full cache, a synthesized cache is passed as is.   */
+/* counts and info as described above patchkv_kv_format, with B = n_cache and  */
+/* N = n_src (info may be NULL).                                               */
 /* Ks, Vs [Hkv][M][dh] (dtype): the chunk's own keys and values.                */
 /* p_terms: 1 = P enters the P V product rounded to bf16 (as attend_full),      */
 /*          2 = as a two-term bf16 split (as attend_compressed); f32 ignores it.*/
@@ -160,10 +191,10 @@ size_t patchkv_attend_chunk_workspace_bytes(int dtype, int64_t M, int64_t n_cach
                                             int dh);
 
 int patchkv_attend_chunk(int dtype, const void* Q, const void* K, const void* V,
-                         const int32_t* idx, int64_t n_src, int64_t n_cache, const void* Ks,
-                         const void* Vs, int64_t M, int Hq, int Hkv, int dh, float scale,
-                         int p_terms, float* O, void* workspace, size_t workspace_bytes,
-                         void* stream);
+                         const int32_t* idx, int idx_mode, const int32_t* counts, int64_t n_src,
+                         int64_t n_cache, const void* Ks, const void* Vs, int64_t M, int Hq,
+                         int Hkv, int dh, float scale, int p_terms, float* O, int32_t* info,
+                         void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------- */
 /* Attention over a compressed cache in the storage formats of Sec. 3.1 and     */
@@ -175,8 +206,10 @@ int patchkv_attend_chunk(int dtype, const void* Q, const void* K, const void* V,
 /*    [Hkv][n_src][dh/32]; entry value q * 2^e (exact in bf16).                 */
 /*  - PATCHKV_KV_MXINT4: K, V uint8 [Hkv][n_src][dh/2], two int4 per byte, the  */
 /*    even channel in the low nibble; Ke, Ve as for MXINT8.                     */
-/*  - idx != NULL: the cache is rows idx[0..n_cache) (eviction subset; entries  */
-/*    outside [0, n_src) read as zero rows); idx == NULL: rows 0..n_cache.       */
+/*  - idx != NULL: the cache is rows idx[0..n_cache) (idx_mode SHARED) or      */
+/*    idx[g][0..n_cache) of head g (PER_HEAD) (eviction subset); idx == NULL:  */
+/*    rows 0..n_cache. counts and info as described above patchkv_kv_format,    */
+/*    with B = n_cache and N = n_src (info may be NULL).                       */
 /*  - bias [Hkv][n_cache] float (natural-log units, indexed by cache entry) or  */
 /*    NULL for none.                                                           */
 /*  - p_terms as for patchkv_attend_chunk (1: P rounded to bf16; 2: two terms). */
@@ -189,10 +222,10 @@ size_t patchkv_attend_cache_workspace_bytes(int dtype, int kv_format, int64_t M,
                                             int Hq, int Hkv, int dh);
 
 int patchkv_attend_cache(int dtype, const void* Q, const void* K, const void* V, int kv_format,
-                         const int8_t* Ke, const int8_t* Ve, const int32_t* idx, int64_t n_src,
-                         int64_t n_cache, const float* bias, int64_t M, int Hq, int Hkv, int dh,
-                         float scale, int p_terms, float* O, void* workspace,
-                         size_t workspace_bytes, void* stream);
+                         const int8_t* Ke, const int8_t* Ve, const int32_t* idx, int idx_mode,
+                         const int32_t* counts, int64_t n_src, int64_t n_cache, const float* bias,
+                         int64_t M, int Hq, int Hkv, int dh, float scale, int p_terms, float* O,
+                         int32_t* info, void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------- */
 /* Per-token targets, Eq. 5 in row form with h = z = the attention output:      */
@@ -315,19 +348,23 @@ int patchkv_low_rank_patch(const float* G, const float* dW, int64_t d_in, int64_
 /*   dW = (G + lambda I)^{-1} C.                                                */
 /* dtype: input type of Q, K, V, Kc, Vc and W (PATCHKV_BF16 or PATCHKV_F32).     */
 /* acc_dtype: statistics and solve precision (PATCHKV_F32 or PATCHKV_F64).      */
-/* Compressed cache: idx != NULL -> eviction subset of (K, V) (Kc, Vc ignored); */
-/*   idx == NULL -> synthesized Kc, Vc [Hkv][B][dh].                            */
-/* W [d][d] with d = Hq*dh. dW [d][d] float. info as in solve_patch.            */
+/* Compressed cache: idx != NULL -> eviction subset of (K, V), idx [B] or      */
+/*   [Hkv][B] by idx_mode (Kc, Vc ignored); idx == NULL -> synthesized Kc, Vc   */
+/*   [Hkv][B][dh]. counts as described above patchkv_kv_format.                */
+/* W [d][d] with d = Hq*dh. dW [d][d] float. info (required): as in solve_patch, */
+/*   except that an out-of-range index entry or count is reported in its place  */
+/*   (negative code, as described above patchkv_kv_format).                    */
 /* ------------------------------------------------------------------------- */
 size_t patchkv_layer_workspace_bytes(int dtype, int acc_dtype, int64_t M, int64_t N, int64_t B,
                                      int Hq, int Hkv, int dh);
 
 int patchkv_compute_layer_patch(int dtype, int acc_dtype, const void* Q, const void* K,
-                                const void* V, const int32_t* idx, const void* Kc,
-                                const void* Vc, const void* W, int64_t M, int64_t N, int64_t B,
-                                int Hq, int Hkv, int dh, float scale, int rho, double lambda,
-                                int ridge_mode, float* dW, int32_t* info,
-                                void* workspace, size_t workspace_bytes, void* stream);
+                                const void* V, const int32_t* idx, int idx_mode,
+                                const int32_t* counts, const void* Kc, const void* Vc,
+                                const void* W, int64_t M, int64_t N, int64_t B, int Hq, int Hkv,
+                                int dh, float scale, int rho, double lambda, int ridge_mode,
+                                float* dW, int32_t* info, void* workspace,
+                                size_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus
 }

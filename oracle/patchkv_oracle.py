@@ -101,16 +101,22 @@ def attention(Q: np.ndarray, K: np.ndarray, V: np.ndarray, scale: float | None =
               max_score_bytes: int = 1 << 28, bias: np.ndarray | None = None) -> np.ndarray:
     """Reference-query attention over one cache (teacher Alg. 1 / student Alg. 1).
 
-    Q [M, Hq, dh], K and V [Hkv, Nk, dh], all float64. Returns O [M, Hq*dh]
-    with O[m, h*dh:(h+1)*dh] = softmax(scale * Q[m,h] K[g]^T + bias[g]) V[g],
+    Q [M, Hq, dh], K and V [Hkv, Nk, dh], all float64; K and V may also be
+    sequences of Hkv arrays [Nk_g, dh] (a compressed cache whose KV heads keep
+    different numbers of entries). Returns O [M, Hq*dh] with
+    O[m, h*dh:(h+1)*dh] = softmax(scale * Q[m,h] K[g]^T + bias[g]) V[g],
     g = floor(h / (Hq/Hkv)); ``bias`` [Hkv, Nk] (natural-log units, default none)
     is a per-entry logit bias, as an attention-matching compressed cache carries
     with its entries (Sec. 3.1). Rows are processed in chunks only to bound memory.
     """
     M, Hq, dh = Q.shape
-    Hkv, Nk, dh2 = K.shape
-    if dh2 != dh or V.shape != K.shape or Hq % Hkv:
+    Hkv = len(K)
+    if len(V) != Hkv or Hkv == 0 or Hq % Hkv:
         raise ValueError("shape mismatch")
+    for g in range(Hkv):
+        if K[g].ndim != 2 or K[g].shape[1] != dh or V[g].shape != K[g].shape:
+            raise ValueError("shape mismatch")
+    Nk = max(K[g].shape[0] for g in range(Hkv))
     if scale is None:
         scale = 1.0 / np.sqrt(dh)
     group = Hq // Hkv
@@ -153,18 +159,22 @@ def attention_chunk(Q: np.ndarray, K: np.ndarray, V: np.ndarray, Ks: np.ndarray,
     entries m+1.. get a score of -inf before the softmax. Returns O [Mc, Hq*dh].
     """
     M, Hq, dh = Q.shape
-    Hkv, Nk, dh2 = K.shape
-    if dh2 != dh or V.shape != K.shape or Ks.shape != (Hkv, M, dh) or Vs.shape != Ks.shape:
+    Hkv = len(K)
+    if len(V) != Hkv or Ks.shape != (Hkv, M, dh) or Vs.shape != Ks.shape:
         raise ValueError("shape mismatch")
+    for g in range(Hkv):
+        if K[g].ndim != 2 or K[g].shape[1] != dh or V[g].shape != K[g].shape:
+            raise ValueError("shape mismatch")
     if Hq % Hkv:
         raise ValueError("Hq must be a multiple of Hkv")
     if scale is None:
         scale = 1.0 / np.sqrt(dh)
     group = Hq // Hkv
     O = np.empty((M, Hq * dh), dtype=np.float64)
-    rows = max(1, min(M, max_score_bytes // (8 * (Nk + M))))
+    rows = max(1, min(M, max_score_bytes // (8 * (max(k.shape[0] for k in K) + M))))
     for h in range(Hq):
         g = h // group
+        Nk = K[g].shape[0]
         Kall = np.concatenate([K[g], Ks[g]], axis=0)     # [Nk + M, dh]
         Vall = np.concatenate([V[g], Vs[g]], axis=0)
         for r0 in range(0, M, rows):
@@ -177,10 +187,23 @@ def attention_chunk(Q: np.ndarray, K: np.ndarray, V: np.ndarray, Ks: np.ndarray,
     return O
 
 
-def gather_cache(K: np.ndarray, V: np.ndarray, idx: np.ndarray):
-    """Eviction-style compressed cache: the kept entries K[:, idx], V[:, idx]."""
+def gather_cache(K: np.ndarray, V: np.ndarray, idx: np.ndarray, counts=None):
+    """Eviction-style compressed cache: the kept entries of K, V [Hkv, N, dh].
+
+    ``idx`` [B], one set for every KV head: K[:, idx], V[:, idx]. ``idx`` [Hkv, B],
+    one set per KV head (KVzip's global head scoring, App. B.1, keeps different
+    tokens in different heads): head g keeps rows idx[g, :counts[g]] of K[g], V[g]
+    (all B when ``counts`` is None); the result is then a pair of lists of per-head
+    arrays, which ``attention`` accepts.
+    """
     idx = np.asarray(idx)
-    return K[:, idx, :], V[:, idx, :]
+    if idx.ndim == 1 and counts is None:
+        return K[:, idx, :], V[:, idx, :]
+    Hkv = K.shape[0]
+    sets = [idx] * Hkv if idx.ndim == 1 else [idx[g] for g in range(Hkv)]
+    if counts is not None:
+        sets = [sets[g][:int(counts[g])] for g in range(Hkv)]
+    return [K[g][sets[g]] for g in range(Hkv)], [V[g][sets[g]] for g in range(Hkv)]
 
 
 def targets(Of: np.ndarray, Oc: np.ndarray, W: np.ndarray, rho: int = 1) -> np.ndarray:
@@ -258,7 +281,7 @@ def layer_patch(inp, rho: int = 1, mode: str = "absolute", lam: float | None = N
     if cache is not None:
         Kc, Vc = cache
     elif inp.idx is not None:
-        Kc, Vc = gather_cache(K, V, inp.idx)
+        Kc, Vc = gather_cache(K, V, inp.idx, inp.counts)
     else:
         Kc, Vc = decode(inp.Kc, dt), decode(inp.Vc, dt)
     del K, V
@@ -289,7 +312,7 @@ def layer_patch_chunked(inp, chunks, rho: int = 1, mode: str = "absolute",
     V = decode(inp.V, dt)
     W = decode(inp.W, dt)
     if inp.idx is not None:
-        Kc, Vc = gather_cache(K, V, inp.idx)
+        Kc, Vc = gather_cache(K, V, inp.idx, inp.counts)
     else:
         Kc, Vc = decode(inp.Kc, dt), decode(inp.Vc, dt)
     G0 = np.zeros((W.shape[0], W.shape[0]))
@@ -351,7 +374,7 @@ def mlp_layer_patch(inp, mlp, mode: str = "absolute", lam: float | None = None) 
     Wg, Wu, Wd = decode(mlp.Wg, dt), decode(mlp.Wu, dt), decode(mlp.Wd, dt)
     Of = attention(Q, K, V, inp.scale)
     if inp.idx is not None:
-        Kc, Vc = gather_cache(K, V, inp.idx)
+        Kc, Vc = gather_cache(K, V, inp.idx, inp.counts)
     else:
         Kc, Vc = decode(inp.Kc, dt), decode(inp.Vc, dt)
     del K, V

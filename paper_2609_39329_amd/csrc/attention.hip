@@ -79,6 +79,8 @@ struct AttnParams {
   const __bf16* Vt;  // bf16 path: V transposed into 32-key tiles (see vt_kernel)
   int vt_tiles;      // tiles per KV head in Vt
   const int32_t* idx;
+  int idx_stride;         // 0: one index set for every KV head; else head g's set is idx + g * idx_stride
+  const int32_t* counts;  // per-head entry counts [Hkv] (clamped into [1, Nk]) or null: Nk for every head
   float* O;
   float* Opart;
   float* ML;
@@ -109,23 +111,27 @@ struct AttnParams {
 // k-slot order of the P fragments: key 16b + r (r < 16) sits at position
 // 16b + 8((r % 8) / 4) + 4(r / 8) + r % 4, so the 8 keys one lane feeds into an MFMA
 // (keys 16b + 4h + {0..3} and 16b + 8 + 4h + {0..3}) are 8 consecutive positions.
-// Keys at or past Nk (and gathered rows outside the cache) are zero. GATHER: key n
-// is row idx[n] of V.
+// Keys at or past the head's entry count (and gathered rows outside the cache) are
+// zero. GATHER: key n of head g is row idx[g * idx_stride + n] of V.
 template <int DH, bool GATHER>
 __global__ __launch_bounds__(256) void vt_kernel(const __bf16* __restrict__ V,
-                                                 const int32_t* __restrict__ idx, int64_t src_rows,
-                                                 int Nk, int ntiles, __bf16* __restrict__ Vt) {
+                                                 const int32_t* __restrict__ idx, int idx_stride,
+                                                 const int32_t* __restrict__ counts,
+                                                 int64_t src_rows, int Nk, int ntiles,
+                                                 __bf16* __restrict__ Vt) {
   constexpr int CH = DH / 8;     // 16-byte chunks per V row
   constexpr int SP = DH + 2;     // LDS pitch (elements) of the [key][d] staging tile
   __shared__ __bf16 sm[32 * SP];
   const int tile = blockIdx.x, g = blockIdx.y, tid = threadIdx.x;
   const __bf16* Vg = V + (int64_t)g * src_rows * DH;
+  const int nk = counts ? min(max(counts[g], 1), Nk) : Nk;
+  const int32_t* ig = GATHER ? idx + (int64_t)g * idx_stride : nullptr;
   for (int c = tid; c < 32 * CH; c += 256) {
     const int key = c / CH, col = (c % CH) * 8;
     const int n = tile * 32 + key;
     bf16x8 v = {};
-    if (n < Nk) {
-      const int64_t src = GATHER ? (int64_t)idx[n] : (int64_t)n;
+    if (n < nk) {
+      const int64_t src = GATHER ? (int64_t)ig[n] : (int64_t)n;
       if (src >= 0 && src < src_rows) v = load_bf16x8(Vg + src * DH + col);
     }
 #pragma unroll
@@ -191,13 +197,35 @@ __global__ __launch_bounds__(kThreadsBf16, 1) void attn_bf16_kernel(AttnParams p
   const int t2 = __builtin_amdgcn_readfirstlane(w / p.row_tiles);
   const int split = __builtin_amdgcn_readfirstlane(t2 % p.n_split);
   const int g = __builtin_amdgcn_readfirstlane(t2 / p.n_split);
+  // entries of this KV head's cache (a per-head index set may keep fewer than Nk)
+  const int nk = p.counts ? __builtin_amdgcn_readfirstlane(min(max(p.counts[g], 1), p.Nk)) : p.Nk;
   const int k_begin = split * p.keys_per_split;
-  const int k_end = min(p.Nk, k_begin + p.keys_per_split);
+  const int k_end = max(k_begin, min(nk, k_begin + p.keys_per_split));
   // cache tiles [0, ct) of this key range, then (OWN, last range) the own tiles up
   // to this workgroup's last query
   // (tiles past ntiles are masked like keys past k_end, also in the other ranges)
   const int ct = (k_end - k_begin + KT - 1) / KT;
   const bool own_range = OWN && split == p.n_split - 1;
+  if constexpr (PARTIAL) {
+    // a key range past the end of a shorter head's cache (and without own entries):
+    // an empty partial result, weight zero in the merge
+    if (ct == 0 && !own_range) {
+      if constexpr (!SAFE) {
+        if (threadIdx.x == 0) p.flags[w] = 0;
+      }
+      for (int i = threadIdx.x; i < kRowsWG; i += blockDim.x) {
+        const int r = rt * kRowsWG + i;
+        if (r >= p.rows) break;
+        const int64_t rid = ((int64_t)(g * p.n_split + split)) * p.rows + r;
+        f32x4* op = (f32x4*)(p.Opart + rid * DH);
+#pragma unroll
+        for (int c4 = 0; c4 < DH / 4; ++c4) op[c4] = f32x4{};
+        p.ML[2 * rid] = -INFINITY;
+        p.ML[2 * rid + 1] = 0.f;
+      }
+      return;
+    }
+  }
   int ntiles = ct;
   if (own_range) {
     const int last_q = min(p.rows - 1, rt * kRowsWG + kRowsWG - 1) / p.G;
@@ -231,8 +259,8 @@ __global__ __launch_bounds__(kThreadsBf16, 1) void attn_bf16_kernel(AttnParams p
   const __bf16* Vtg = p.Vt + (int64_t)g * p.vt_tiles * DH * 32;
   const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc(
       (void*)Vtg, 0, (uint32_t)p.vt_tiles * (DH * 32 * 2), 0x00020000);
-  const __amdgpu_buffer_rsrc_t irs =
-      __builtin_amdgcn_make_buffer_rsrc((void*)p.idx, 0, (uint32_t)(p.Nk * 4), 0x00020000);
+  const __amdgpu_buffer_rsrc_t irs = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(p.idx + (int64_t)g * p.idx_stride), 0, (uint32_t)(p.Nk * 4), 0x00020000);
   // own entries (OWN): rows past Ms and tiles past the last read as zeros
   const __amdgpu_buffer_rsrc_t ksrs = __builtin_amdgcn_make_buffer_rsrc(
       (void*)((const __bf16*)p.Ks + (int64_t)g * p.Ms * DH), 0, (uint32_t)(p.Ms * DH * 2), 0x00020000);
@@ -269,10 +297,13 @@ __global__ __launch_bounds__(kThreadsBf16, 1) void attn_bf16_kernel(AttnParams p
       const int c = i * NT + tid;  // 16-byte chunk: row c / CH, column c % CH
       if (NCH % NT != 0 && c >= NCH) break;
       if constexpr (GATHER) {
-        // entries past the index array read as 0; rows outside the cache read as 0
+        // entries past the index array read as 0; an entry outside the cache is checked
+        // before any offset is formed from it, and its row reads as zeros
         const int src = (int)__builtin_amdgcn_raw_buffer_load_b32(irs, (kb0 + c / CH) * 4, 0, 0);
-        const uint32_t off = (uint32_t)src * (DH * 2) + (c % CH) * 16;
-        kreg[set][i] = __builtin_amdgcn_raw_buffer_load_b128(krs, off, 0, 0);
+        const bool in = (uint32_t)src < (uint32_t)p.src_rows;
+        const uint32_t off = in ? (uint32_t)src * (DH * 2) + (c % CH) * 16 : 0u;
+        const u32x4 kv = __builtin_amdgcn_raw_buffer_load_b128(krs, off, 0, 0);
+        kreg[set][i] = in ? kv : u32x4{};
       } else {
         const uint32_t soff = (uint32_t)kb0 * (DH * 2);
         kreg[set][i] = __builtin_amdgcn_raw_buffer_load_b128(krs, c * 16, soff, 0);
@@ -719,8 +750,10 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnParams p) {
   const int t2 = w / p.row_tiles;
   const int split = t2 % p.n_split;
   const int g = t2 / p.n_split;
+  const int nk = p.counts ? min(max(p.counts[g], 1), p.Nk) : p.Nk;
   const int k_begin = split * p.keys_per_split;
-  const int k_end = min(p.Nk, k_begin + p.keys_per_split);
+  const int k_end = min(nk, k_begin + p.keys_per_split);  // empty range: (O, m, l) = (0, -inf, 0)
+  const int32_t* ig = GATHER ? p.idx + (int64_t)g * p.idx_stride : nullptr;
 
   const int tid = threadIdx.x;
   const int r = rt * kRowsWG + tid;
@@ -775,9 +808,17 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnParams p) {
     for (int c = tid; c < KT * C4; c += 256) {
       const int row = c / C4, col = c % C4;
       int src = min(tb + row, k_end - 1);
-      if constexpr (GATHER) src = min(max(p.idx[src], 0), p.src_valid - 1);
-      Ks[c] = *((const f32x4*)(Kb + (int64_t)src * DH) + col);
-      Vs[c] = *((const f32x4*)(Vb + (int64_t)src * DH) + col);
+      bool in = true;
+      if constexpr (GATHER) {
+        // an entry outside the cache reads as a zero row (no offset is formed from it)
+        src = ig[src];
+        in = (uint32_t)src < (uint32_t)p.src_valid;
+        src = in ? src : 0;
+      }
+      const f32x4 kv = *((const f32x4*)(Kb + (int64_t)src * DH) + col);
+      const f32x4 vv = *((const f32x4*)(Vb + (int64_t)src * DH) + col);
+      Ks[c] = in ? kv : f32x4{};
+      Vs[c] = in ? vv : f32x4{};
     }
     __syncthreads();
     for (int kk = 0; kk < nk; ++kk) attend_key(kk, BIAS ? p.bias[(int64_t)g * p.Nk + tb + kk] : 0.f);
@@ -849,12 +890,15 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restri
 }
 
 // Block-scaled integer cache -> rows [Hkv][n_cache][dh] of OUT (bf16 or f32). Entry n
-// is source row idx[n] (or n); rows outside [0, n_src) read as zeros. Exact: an int8
-// or int4 value times a power of two is a bf16 number. One thread per 8 channels.
+// of head g is source row idx[g * idx_stride + n] (or n); rows outside [0, n_src), and
+// entries at or past the head's count, read as zeros. Exact: an int8 or int4 value
+// times a power of two is a bf16 number. One thread per 8 channels.
 template <class OUT, int BITS>
 __global__ __launch_bounds__(256) void mx_dequant_kernel(const uint8_t* __restrict__ q,
                                                          const int8_t* __restrict__ e,
                                                          const int32_t* __restrict__ idx,
+                                                         int idx_stride,
+                                                         const int32_t* __restrict__ counts,
                                                          int64_t n_src, int n_cache, int dh,
                                                          OUT* __restrict__ out) {
   const int g = blockIdx.y;
@@ -862,7 +906,8 @@ __global__ __launch_bounds__(256) void mx_dequant_kernel(const uint8_t* __restri
   const int per_row = dh / 8;
   if (t >= (int64_t)n_cache * per_row) return;
   const int n = (int)(t / per_row), c0 = (int)(t % per_row) * 8;
-  const int64_t src = idx ? (int64_t)idx[n] : (int64_t)n;
+  const int nk = counts ? min(max(counts[g], 1), n_cache) : n_cache;
+  const int64_t src = n >= nk ? -1 : idx ? (int64_t)idx[(int64_t)g * idx_stride + n] : (int64_t)n;
   float v[8] = {};
   if (src >= 0 && src < n_src) {
     const int64_t row = (int64_t)g * n_src + src;
@@ -998,11 +1043,14 @@ AttnPlan plan_attention(const AttnShape& s) {
 }
 
 hipError_t launch_attention(const AttnShape& s, const void* Q, const void* K, const void* V,
-                            const int32_t* idx, int64_t src_rows, int64_t src_valid,
+                            const CacheIndex& ci, int64_t src_rows, int64_t src_valid,
                             float scale, bool psplit, float* O, void* ws, hipStream_t st,
                             const void* Ks, const void* Vs, const float* bias) {
   const AttnPlan pl = plan_attention(s);
+  const int32_t* idx = ci.idx;
   AttnParams p{};
+  p.idx_stride = (int)ci.stride;
+  p.counts = ci.counts;
   p.bias = bias;
   p.bias_mul = s.bf16 ? 1.0f / scale : 1.0f;
   p.Q = Q;
@@ -1030,8 +1078,9 @@ hipError_t launch_attention(const AttnShape& s, const void* Q, const void* K, co
     p.vt_tiles = (int)vt_tiles;
     const dim3 vg((unsigned)vt_tiles, (unsigned)s.Hkv), vb(256);
     const __bf16* Vb = (const __bf16*)V;
-#define PKV_VT(D_, G_) \
-  hipLaunchKernelGGL((vt_kernel<D_, G_>), vg, vb, 0, st, Vb, idx, src_rows, (int)s.Nk, (int)vt_tiles, vt)
+#define PKV_VT(D_, G_)                                                                         \
+  hipLaunchKernelGGL((vt_kernel<D_, G_>), vg, vb, 0, st, Vb, idx, p.idx_stride, ci.counts, src_rows, \
+                     (int)s.Nk, (int)vt_tiles, vt)
     if (s.dh == 128) { if (idx) PKV_VT(128, true); else PKV_VT(128, false); }
     else { if (idx) PKV_VT(64, true); else PKV_VT(64, false); }
     if (s.Ms > 0) {
@@ -1044,11 +1093,11 @@ hipError_t launch_attention(const AttnShape& s, const void* Q, const void* K, co
       const dim3 og((unsigned)own_tiles, (unsigned)s.Hkv);
       const __bf16* Vsb = (const __bf16*)Vs;
       if (s.dh == 128)
-        hipLaunchKernelGGL((vt_kernel<128, false>), og, vb, 0, st, Vsb, nullptr, s.Ms, (int)s.Ms,
-                           own_tiles, vts);
+        hipLaunchKernelGGL((vt_kernel<128, false>), og, vb, 0, st, Vsb, nullptr, 0, nullptr, s.Ms,
+                           (int)s.Ms, own_tiles, vts);
       else
-        hipLaunchKernelGGL((vt_kernel<64, false>), og, vb, 0, st, Vsb, nullptr, s.Ms, (int)s.Ms,
-                           own_tiles, vts);
+        hipLaunchKernelGGL((vt_kernel<64, false>), og, vb, 0, st, Vsb, nullptr, 0, nullptr, s.Ms,
+                           (int)s.Ms, own_tiles, vts);
     }
 #undef PKV_VT
     const hipError_t e = hipGetLastError();
@@ -1075,26 +1124,83 @@ hipError_t launch_attention(const AttnShape& s, const void* Q, const void* K, co
 namespace pkv {
 
 hipError_t launch_mx_dequant(bool bf16, int bits, const void* q, const int8_t* e,
-                             const int32_t* idx, int64_t n_src, int64_t n_cache, int Hkv, int dh,
+                             const CacheIndex& ci, int64_t n_src, int64_t n_cache, int Hkv, int dh,
                              void* out, hipStream_t st) {
   const int64_t n = n_cache * (dh / 8);
   const dim3 grid((unsigned)((n + 255) / 256), (unsigned)Hkv), block(256);
   const uint8_t* qb = (const uint8_t*)q;
+  const int is = (int)ci.stride;
   if (bf16) {
     if (bits == 8)
-      hipLaunchKernelGGL((mx_dequant_kernel<__bf16, 8>), grid, block, 0, st, qb, e, idx, n_src,
-                         (int)n_cache, dh, (__bf16*)out);
+      hipLaunchKernelGGL((mx_dequant_kernel<__bf16, 8>), grid, block, 0, st, qb, e, ci.idx, is,
+                         ci.counts, n_src, (int)n_cache, dh, (__bf16*)out);
     else
-      hipLaunchKernelGGL((mx_dequant_kernel<__bf16, 4>), grid, block, 0, st, qb, e, idx, n_src,
-                         (int)n_cache, dh, (__bf16*)out);
+      hipLaunchKernelGGL((mx_dequant_kernel<__bf16, 4>), grid, block, 0, st, qb, e, ci.idx, is,
+                         ci.counts, n_src, (int)n_cache, dh, (__bf16*)out);
   } else {
     if (bits == 8)
-      hipLaunchKernelGGL((mx_dequant_kernel<float, 8>), grid, block, 0, st, qb, e, idx, n_src,
-                         (int)n_cache, dh, (float*)out);
+      hipLaunchKernelGGL((mx_dequant_kernel<float, 8>), grid, block, 0, st, qb, e, ci.idx, is,
+                         ci.counts, n_src, (int)n_cache, dh, (float*)out);
     else
-      hipLaunchKernelGGL((mx_dequant_kernel<float, 4>), grid, block, 0, st, qb, e, idx, n_src,
-                         (int)n_cache, dh, (float*)out);
+      hipLaunchKernelGGL((mx_dequant_kernel<float, 4>), grid, block, 0, st, qb, e, ci.idx, is,
+                         ci.counts, n_src, (int)n_cache, dh, (float*)out);
   }
+  return hipGetLastError();
+}
+
+namespace {
+
+// Validity of a compressed cache's index set, one workgroup. Codes: an entry at flat
+// position q of idx (q = b for a shared set, g * B + b per head; only b below the
+// head's count is looked at) outside [0, n_src) has code q; a count outside [1, B] has
+// code E + g, E = the number of entries of idx (0 without idx). info = 0 if nothing
+// is out of range, else -(1 + the smallest code). Deterministic; needs no cleared
+// memory.
+__global__ __launch_bounds__(1024) void idx_check_kernel(const int32_t* __restrict__ idx,
+                                                         int64_t stride,
+                                                         const int32_t* __restrict__ counts,
+                                                         int heads, int64_t B, int64_t n_src,
+                                                         int32_t* __restrict__ info) {
+  __shared__ long long red[1024 / kWave];
+  const long long none = 1ll << 62;
+  const long long E = idx ? (stride ? (long long)heads * B : (long long)B) : 0;
+  long long best = none;
+  for (int g = 0; g < heads; ++g) {
+    const long long cnt = counts ? (long long)counts[g] : (long long)B;
+    if (cnt < 1 || cnt > B) best = min(best, E + g);
+    if (!idx || (stride == 0 && g > 0 && !counts)) continue;
+    const long long n = min(max(cnt, 1ll), (long long)B);
+    const int32_t* ig = idx + g * stride;
+    for (long long b = threadIdx.x; b < n; b += blockDim.x) {
+      const int32_t v = ig[b];
+      if (v < 0 || (long long)v >= n_src) best = min(best, (long long)g * stride + b);
+    }
+  }
+  for (int o = kWave / 2; o > 0; o >>= 1) best = min(best, (long long)__shfl_xor(best, o));
+  if ((threadIdx.x & (kWave - 1)) == 0) red[threadIdx.x / kWave] = best;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int i = 1; i < (int)(blockDim.x / kWave); ++i) best = min(best, red[i]);
+    *info = best == none ? 0 : (int32_t)-(min(best, (long long)INT32_MAX - 1) + 1);
+  }
+}
+
+// info <- status when status is non-zero (an input error outranks a later result)
+__global__ void info_merge_kernel(const int32_t* __restrict__ status, int32_t* __restrict__ info) {
+  if (threadIdx.x == 0 && *status != 0) *info = *status;
+}
+
+}  // namespace
+
+hipError_t launch_idx_check(const CacheIndex& ci, int heads, int64_t B, int64_t n_src,
+                            int32_t* info, hipStream_t st) {
+  hipLaunchKernelGGL(idx_check_kernel, dim3(1), dim3(1024), 0, st, ci.idx, ci.stride, ci.counts,
+                     heads, B, n_src, info);
+  return hipGetLastError();
+}
+
+hipError_t launch_info_merge(const int32_t* status, int32_t* info, hipStream_t st) {
+  hipLaunchKernelGGL(info_merge_kernel, dim3(1), dim3(64), 0, st, status, info);
   return hipGetLastError();
 }
 

@@ -18,6 +18,24 @@ constexpr int64_t kMaxDim = 1 << 16;           // d_in, d_out
 constexpr int64_t kMaxRows = (int64_t)1 << 31;  // M*Hq, N, B, rows
 
 bool al16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+bool al4(const void* p) { return ((uintptr_t)p & 3) == 0; }
+
+// The index set of an eviction-style compressed cache: mode and pointer alignment
+// (its values are checked on the device, see idx_check).
+int check_index(const int32_t* idx, int idx_mode, const int32_t* counts) {
+  if (idx_mode != PATCHKV_IDX_SHARED && idx_mode != PATCHKV_IDX_PER_HEAD) return PATCHKV_E_VALUE;
+  if (idx_mode == PATCHKV_IDX_PER_HEAD && !idx) return PATCHKV_E_NULL;
+  if (!al4(idx) || !al4(counts)) return PATCHKV_E_VALUE;
+  return PATCHKV_OK;
+}
+
+CacheIndex cache_index(const int32_t* idx, int idx_mode, const int32_t* counts, int64_t B) {
+  CacheIndex ci;
+  ci.idx = idx;
+  ci.stride = idx && idx_mode == PATCHKV_IDX_PER_HEAD ? B : 0;
+  ci.counts = counts;
+  return ci;
+}
 
 int status_of(hipError_t e) { return e == hipSuccess ? PATCHKV_OK : PATCHKV_E_HIP; }
 
@@ -70,7 +88,7 @@ int check_stats_dims(int64_t rows, int64_t din, int64_t dout) {
 
 // Layer-patch workspace layout.
 struct LayerWs {
-  size_t Of, Oc, T, G, C, attn, solve, total;
+  size_t Of, Oc, T, G, C, attn, solve, stat, total;
 };
 
 LayerWs layer_ws(int dtype, int acc, int64_t M, int64_t N, int64_t B, int Hq, int Hkv, int dh) {
@@ -92,6 +110,7 @@ LayerWs layer_ws(int dtype, int acc, int64_t M, int64_t N, int64_t B, int Hq, in
     scratch = std::max({scratch, targets_ws_bytes(M, d, d), normal_eq_ws_bytes(M, d, d)});
   o += align_up(scratch);
   L.solve = o; o += align_up(solve_ws_bytes(acc == PATCHKV_F64, d, d));
+  L.stat = o; o += align_up(sizeof(int32_t));  // index-set check, merged into info at the end
   L.total = o;
   return L;
 }
@@ -132,26 +151,48 @@ int patchkv_attend_full(int dtype, const void* Q, const void* K, const void* V, 
   const AttnShape sh = attn_shape(dtype, M, N, Hq, Hkv, dh);
   s = check_ws(workspace, workspace_bytes, plan_attention(sh).ws_bytes);
   if (s) return s;
-  return status_of(launch_attention(sh, Q, K, V, nullptr, N, N, scale, false, O, workspace,
+  return status_of(launch_attention(sh, Q, K, V, CacheIndex{}, N, N, scale, false, O, workspace,
                                     (hipStream_t)stream));
 }
 
-int patchkv_attend_compressed(int dtype, const void* Q, const void* K, const void* V,
-                              const int32_t* idx, int64_t M, int64_t N, int64_t B, int Hq, int Hkv,
-                              int dh, float scale, float* O, void* workspace,
-                              size_t workspace_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// attend_compressed with the scratch from the caller's workspace.
+int attend_compressed_impl(int dtype, const void* Q, const void* K, const void* V,
+                           const int32_t* idx, int idx_mode, const int32_t* counts, int64_t M,
+                           int64_t N, int64_t B, int Hq, int Hkv, int dh, float scale, float* O,
+                           int32_t* info, void* workspace, size_t workspace_bytes, void* stream) {
   if (!Q || !K || !V || !O) return PATCHKV_E_NULL;
   int s = check_attn_shape(dtype, M, B, Hq, Hkv, dh);
   if (s) return s;
   if (idx && !src_rows_ok(dtype, N, dh)) return PATCHKV_E_SHAPE;
+  s = check_index(idx, idx_mode, counts);
+  if (s) return s;
   if (!finite_pos(scale)) return PATCHKV_E_VALUE;
-  if (!al16(Q) || !al16(K) || !al16(V) || !al16(O)) return PATCHKV_E_VALUE;
+  if (!al16(Q) || !al16(K) || !al16(V) || !al16(O) || !al4(info)) return PATCHKV_E_VALUE;
   const AttnShape sh = attn_shape(dtype, M, B, Hq, Hkv, dh);
   s = check_ws(workspace, workspace_bytes, plan_attention(sh).ws_bytes);
   if (s) return s;
   const int64_t src = idx ? N : B;
-  return status_of(launch_attention(sh, Q, K, V, idx, src, src, scale, true, O, workspace,
-                                    (hipStream_t)stream));
+  const CacheIndex ci = cache_index(idx, idx_mode, counts, B);
+  const hipStream_t st = (hipStream_t)stream;
+  if (info && launch_idx_check(ci, Hkv, B, src, info, st) != hipSuccess) return PATCHKV_E_HIP;
+  return status_of(launch_attention(sh, Q, K, V, ci, src, src, scale, true, O, workspace, st));
+}
+
+}  // namespace
+
+extern "C" {
+
+int patchkv_attend_compressed(int dtype, const void* Q, const void* K, const void* V,
+                              const int32_t* idx, int idx_mode, const int32_t* counts, int64_t M,
+                              int64_t N, int64_t B, int Hq, int Hkv, int dh, float scale, float* O,
+                              int32_t* info, void* workspace, size_t workspace_bytes,
+                              void* stream) {
+  return attend_compressed_impl(dtype, Q, K, V, idx, idx_mode, counts, M, N, B, Hq, Hkv, dh,
+                                scale, O, info, workspace, workspace_bytes, stream);
 }
 
 size_t patchkv_attend_chunk_workspace_bytes(int dtype, int64_t M, int64_t n_cache, int Hq, int Hkv,
@@ -164,25 +205,31 @@ size_t patchkv_attend_chunk_workspace_bytes(int dtype, int64_t M, int64_t n_cach
 }
 
 int patchkv_attend_chunk(int dtype, const void* Q, const void* K, const void* V,
-                         const int32_t* idx, int64_t n_src, int64_t n_cache, const void* Ks,
-                         const void* Vs, int64_t M, int Hq, int Hkv, int dh, float scale,
-                         int p_terms, float* O, void* workspace, size_t workspace_bytes,
-                         void* stream) {
+                         const int32_t* idx, int idx_mode, const int32_t* counts, int64_t n_src,
+                         int64_t n_cache, const void* Ks, const void* Vs, int64_t M, int Hq,
+                         int Hkv, int dh, float scale, int p_terms, float* O, int32_t* info,
+                         void* workspace, size_t workspace_bytes, void* stream) {
   if (!Q || !K || !V || !Ks || !Vs || !O) return PATCHKV_E_NULL;
   int s = check_attn_shape(dtype, M, n_cache, Hq, Hkv, dh);
   if (s) return s;
   if (!src_rows_ok(dtype, n_src, dh) || !src_rows_ok(dtype, M, dh)) return PATCHKV_E_SHAPE;
   if (!idx && n_cache > n_src) return PATCHKV_E_SHAPE;
+  s = check_index(idx, idx_mode, counts);
+  if (s) return s;
   if (p_terms != 1 && p_terms != 2) return PATCHKV_E_VALUE;
   if (!finite_pos(scale)) return PATCHKV_E_VALUE;
-  if (!al16(Q) || !al16(K) || !al16(V) || !al16(Ks) || !al16(Vs) || !al16(O))
+  if (!al16(Q) || !al16(K) || !al16(V) || !al16(Ks) || !al16(Vs) || !al16(O) || !al4(info))
     return PATCHKV_E_VALUE;
   AttnShape sh = attn_shape(dtype, M, n_cache, Hq, Hkv, dh);
   sh.Ms = M;
   s = check_ws(workspace, workspace_bytes, plan_attention(sh).ws_bytes);
   if (s) return s;
-  return status_of(launch_attention(sh, Q, K, V, idx, n_src, n_src, scale, p_terms == 2, O,
-                                    workspace, (hipStream_t)stream, Ks, Vs));
+  const CacheIndex ci = cache_index(idx, idx_mode, counts, n_cache);
+  const hipStream_t st = (hipStream_t)stream;
+  if (info && launch_idx_check(ci, Hkv, n_cache, n_src, info, st) != hipSuccess)
+    return PATCHKV_E_HIP;
+  return status_of(launch_attention(sh, Q, K, V, ci, n_src, n_src, scale, p_terms == 2, O,
+                                    workspace, st, Ks, Vs));
 }
 
 namespace {
@@ -206,10 +253,10 @@ size_t patchkv_attend_cache_workspace_bytes(int dtype, int kv_format, int64_t M,
 }
 
 int patchkv_attend_cache(int dtype, const void* Q, const void* K, const void* V, int kv_format,
-                         const int8_t* Ke, const int8_t* Ve, const int32_t* idx, int64_t n_src,
-                         int64_t n_cache, const float* bias, int64_t M, int Hq, int Hkv, int dh,
-                         float scale, int p_terms, float* O, void* workspace,
-                         size_t workspace_bytes, void* stream) {
+                         const int8_t* Ke, const int8_t* Ve, const int32_t* idx, int idx_mode,
+                         const int32_t* counts, int64_t n_src, int64_t n_cache, const float* bias,
+                         int64_t M, int Hq, int Hkv, int dh, float scale, int p_terms, float* O,
+                         int32_t* info, void* workspace, size_t workspace_bytes, void* stream) {
   if (!Q || !K || !V || !O) return PATCHKV_E_NULL;
   if (!valid_kv_format(kv_format)) return PATCHKV_E_VALUE;
   const bool quant = kv_format != PATCHKV_KV_PLAIN;
@@ -218,29 +265,36 @@ int patchkv_attend_cache(int dtype, const void* Q, const void* K, const void* V,
   if (s) return s;
   if (!src_rows_ok(dtype, n_src, dh)) return PATCHKV_E_SHAPE;
   if (!idx && n_cache > n_src) return PATCHKV_E_SHAPE;
+  s = check_index(idx, idx_mode, counts);
+  if (s) return s;
   if (p_terms != 1 && p_terms != 2) return PATCHKV_E_VALUE;
   if (!finite_pos(scale)) return PATCHKV_E_VALUE;
-  if (!al16(Q) || !al16(K) || !al16(V) || !al16(O) || (bias && !al16(bias)))
+  if (!al16(Q) || !al16(K) || !al16(V) || !al16(O) || (bias && !al16(bias)) || !al4(info))
     return PATCHKV_E_VALUE;
   const AttnShape sh = attn_shape(dtype, M, n_cache, Hq, Hkv, dh);
   const size_t a = (plan_attention(sh).ws_bytes + 255) / 256 * 256;
   s = check_ws(workspace, workspace_bytes, a + dequant_bytes(dtype, kv_format, n_cache, Hkv, dh));
   if (s) return s;
+  const CacheIndex ci = cache_index(idx, idx_mode, counts, n_cache);
+  const hipStream_t st = (hipStream_t)stream;
+  if (info && launch_idx_check(ci, Hkv, n_cache, n_src, info, st) != hipSuccess)
+    return PATCHKV_E_HIP;
   if (!quant)
-    return status_of(launch_attention(sh, Q, K, V, idx, n_src, n_src, scale, p_terms == 2, O,
-                                      workspace, (hipStream_t)stream, nullptr, nullptr, bias));
+    return status_of(launch_attention(sh, Q, K, V, ci, n_src, n_src, scale, p_terms == 2, O,
+                                      workspace, st, nullptr, nullptr, bias));
   // expand the quantized entries (gathered through idx) into dtype rows, then attend
   const int bits = kv_format == PATCHKV_KV_MXINT8 ? 8 : 4;
   const size_t half = dequant_bytes(dtype, kv_format, n_cache, Hkv, dh) / 2;
   char* kx = (char*)workspace + a;
   char* vx = kx + half;
-  const hipStream_t st = (hipStream_t)stream;
-  hipError_t e = launch_mx_dequant(dtype == PATCHKV_BF16, bits, K, Ke, idx, n_src, n_cache, Hkv,
+  hipError_t e = launch_mx_dequant(dtype == PATCHKV_BF16, bits, K, Ke, ci, n_src, n_cache, Hkv,
                                    dh, kx, st);
   if (e == hipSuccess)
-    e = launch_mx_dequant(dtype == PATCHKV_BF16, bits, V, Ve, idx, n_src, n_cache, Hkv, dh, vx, st);
+    e = launch_mx_dequant(dtype == PATCHKV_BF16, bits, V, Ve, ci, n_src, n_cache, Hkv, dh, vx, st);
   if (e != hipSuccess) return PATCHKV_E_HIP;
-  return status_of(launch_attention(sh, Q, kx, vx, nullptr, n_cache, n_cache, scale, p_terms == 2,
+  CacheIndex dense;
+  dense.counts = counts;  // the expanded rows are dense; a head still keeps only its count
+  return status_of(launch_attention(sh, Q, kx, vx, dense, n_cache, n_cache, scale, p_terms == 2,
                                     O, workspace, st, nullptr, nullptr, bias));
 }
 
@@ -418,13 +472,19 @@ size_t patchkv_layer_workspace_bytes(int dtype, int acc_dtype, int64_t M, int64_
 }
 
 int patchkv_compute_layer_patch(int dtype, int acc_dtype, const void* Q, const void* K,
-                                const void* V, const int32_t* idx, const void* Kc, const void* Vc,
+                                const void* V, const int32_t* idx, int idx_mode,
+                                const int32_t* counts, const void* Kc, const void* Vc,
                                 const void* W, int64_t M, int64_t N, int64_t B, int Hq, int Hkv,
                                 int dh, float scale, int rho, double lambda, int ridge_mode,
                                 float* dW, int32_t* info, void* workspace, size_t workspace_bytes,
                                 void* stream) {
   if (!Q || !K || !V || !W || !dW || !info) return PATCHKV_E_NULL;
   if (!idx && (!Kc || !Vc)) return PATCHKV_E_NULL;
+  {
+    const int si = check_index(idx, idx_mode, counts);
+    if (si) return si;
+  }
+  if (!al4(info)) return PATCHKV_E_VALUE;
   if (acc_dtype != PATCHKV_F32 && acc_dtype != PATCHKV_F64) return PATCHKV_E_DTYPE;
   int s = check_attn_shape(dtype, M, N, Hq, Hkv, dh);
   if (s) return s;
@@ -450,16 +510,20 @@ int patchkv_compute_layer_patch(int dtype, int acc_dtype, const void* Q, const v
   void* C = w + L.C;
   void* wa = w + L.attn;
   void* wsv = w + L.solve;
+  int32_t* stat = (int32_t*)(w + L.stat);
 
-  hipError_t e = launch_attention(attn_shape(dtype, M, N, Hq, Hkv, dh), Q, K, V, nullptr, N, N,
-                                  scale, false, Of, wa, st);
+  const CacheIndex ci = cache_index(idx, idx_mode, counts, B);
+  hipError_t e = launch_idx_check(ci, Hkv, B, idx ? N : B, stat, st);
+  if (e != hipSuccess) return PATCHKV_E_HIP;
+  e = launch_attention(attn_shape(dtype, M, N, Hq, Hkv, dh), Q, K, V, CacheIndex{}, N, N, scale,
+                       false, Of, wa, st);
   if (e != hipSuccess) return PATCHKV_E_HIP;
   if (idx)
-    e = launch_attention(attn_shape(dtype, M, B, Hq, Hkv, dh), Q, K, V, idx, N, N, scale, true, Oc,
+    e = launch_attention(attn_shape(dtype, M, B, Hq, Hkv, dh), Q, K, V, ci, N, N, scale, true, Oc,
                          wa, st);
   else
-    e = launch_attention(attn_shape(dtype, M, B, Hq, Hkv, dh), Q, Kc, Vc, nullptr, B, B, scale,
-                         true, Oc, wa, st);
+    e = launch_attention(attn_shape(dtype, M, B, Hq, Hkv, dh), Q, Kc, Vc, ci, B, B, scale, true,
+                         Oc, wa, st);
   if (e != hipSuccess) return PATCHKV_E_HIP;
   const bool wbf = dtype == PATCHKV_BF16;
   if (acc_dtype == PATCHKV_F32) {
@@ -476,6 +540,7 @@ int patchkv_compute_layer_patch(int dtype, int acc_dtype, const void* Q, const v
   if (e != hipSuccess) return PATCHKV_E_HIP;
   e = launch_solve(acc_dtype == PATCHKV_F64, G, C, d, d, lambda, ridge_kind(ridge_mode),
                    exact(ridge_mode), dW, info, wsv, st);
+  if (e == hipSuccess) e = launch_info_merge(stat, info, st);
   return status_of(e);
 }
 

@@ -28,22 +28,39 @@ struct AttnPlan {
 
 AttnPlan plan_attention(const AttnShape& s);
 
-// Q [M][Hq][dh]; K, V rows of KV head g start at (g * src_rows) * dh; when idx is
-// non-null, cache entry n is row idx[n] (clamped into [0, src_valid)).
+// Which rows of K, V form the cache. idx null: rows 0..Nk of every KV head. Otherwise
+// entry n of KV head g is row idx[g * stride + n] (stride 0: one set for every head);
+// entries outside [0, src_rows) read as zero rows. counts non-null: head g keeps only
+// its first counts[g] entries (clamped into [1, Nk]).
+struct CacheIndex {
+  const int32_t* idx = nullptr;
+  int64_t stride = 0;
+  const int32_t* counts = nullptr;
+};
+
+// Q [M][Hq][dh]; K, V rows of KV head g start at (g * src_rows) * dh; the cache's
+// entries are selected by ci.
 // psplit: form P V from a two-term bf16 split of P (bf16 path only).
 // s.Ms > 0: Ks, Vs [Hkv][Ms][dh] are the chunk's own entries (causal, after the cache).
 hipError_t launch_attention(const AttnShape& s, const void* Q, const void* K, const void* V,
-                            const int32_t* idx, int64_t src_rows, int64_t src_valid,
+                            const CacheIndex& ci, int64_t src_rows, int64_t src_valid,
                             float scale, bool psplit, float* O, void* ws, hipStream_t st,
                             const void* Ks = nullptr, const void* Vs = nullptr,
                             const float* bias = nullptr);
 // bias [Hkv][Nk]: per-entry logit bias (natural-log units), added to entry n's logit.
 // Block-scaled integer cache rows -> [Hkv][n_cache][dh] bf16 (bf16) or f32: value
 // q * 2^e, q int8 (bits 8) or int4 packed two per byte (bits 4, even channel in the
-// low nibble), e int8 per 32 channels; entry n is row idx[n] (or n) of n_src rows.
+// low nibble), e int8 per 32 channels; entry n of head g is row idx[g * stride + n]
+// (or n) of n_src rows; entries past a head's count are zero rows.
 hipError_t launch_mx_dequant(bool bf16, int bits, const void* q, const int8_t* e,
-                             const int32_t* idx, int64_t n_src, int64_t n_cache, int Hkv, int dh,
+                             const CacheIndex& ci, int64_t n_src, int64_t n_cache, int Hkv, int dh,
                              void* out, hipStream_t st);
+// *info = 0 when every index entry lies in [0, n_src) and every count in [1, B], else
+// the negative code of the first offending entry or count (see patchkv.h).
+hipError_t launch_idx_check(const CacheIndex& ci, int heads, int64_t B, int64_t n_src,
+                            int32_t* info, hipStream_t st);
+// *info = *status where *status is non-zero.
+hipError_t launch_info_merge(const int32_t* status, int32_t* info, hipStream_t st);
 
 // ---------------------------------------------------------------- statistics (fp32 acc)
 size_t targets_ws_bytes(int64_t M, int64_t din, int64_t dout);

@@ -78,19 +78,33 @@ def test_attend_validation(L):
     # bf16 needs a workspace (V^T tiles, flags, split-key partials), given none
     assert attend(L, M=16, N=1 << 15, Hq=32, Hkv=8) == B.E_WORKSPACE
     assert attend(L) == B.E_WORKSPACE
-    r = L.patchkv_attend_compressed(B.BF16, FAKE, FAKE, FAKE, FAKE, 8, 0, 16, 4, 2, 128, 0.1, FAKE,
-                                    None, 0, None)
-    assert r == B.E_SHAPE                                 # idx given but N = 0
-    r = L.patchkv_attend_compressed(B.BF16, FAKE, FAKE, FAKE, None, 8, 64, 0, 4, 2, 128, 0.1, FAKE,
-                                    None, 0, None)
-    assert r == B.E_SHAPE                                 # B = 0
+
+
+def test_attend_compressed_validation(L):
+    def comp(dt=B.BF16, Q=FAKE, K=FAKE, V=FAKE, idx=FAKE, mode=B.IDX_SHARED, counts=None, M=8,
+             N=64, Bn=16, Hq=4, Hkv=2, dh=128, scale=0.1, O=FAKE, info=None, ws=None, wsb=0):
+        return L.patchkv_attend_compressed(dt, Q, K, V, idx, mode, counts, M, N, Bn, Hq, Hkv, dh,
+                                           scale, O, info, ws, wsb, None)
+    assert comp(N=0) == B.E_SHAPE                         # idx given but N = 0
+    assert comp(idx=None, Bn=0) == B.E_SHAPE              # B = 0
+    assert comp(mode=2) == B.E_VALUE                      # unknown index mode
+    assert comp(idx=None, mode=B.IDX_PER_HEAD) == B.E_NULL  # per-head sets need idx
+    assert comp(idx=FAKE + 2) == B.E_VALUE                # misaligned index set
+    assert comp(counts=FAKE + 1) == B.E_VALUE             # misaligned counts
+    assert comp(info=FAKE + 2) == B.E_VALUE               # misaligned info
+    # every index mode, with and without counts and info, stops at the missing workspace
+    for mode in (B.IDX_SHARED, B.IDX_PER_HEAD):
+        for counts in (None, FAKE):
+            for info in (None, FAKE):
+                assert comp(mode=mode, counts=counts, info=info) == B.E_WORKSPACE
 
 
 def test_attend_chunk_validation(L):
-    def chunk(dt=B.BF16, Q=FAKE, K=FAKE, V=FAKE, idx=None, n_src=64, n_cache=64, Ks=FAKE, Vs=FAKE,
-              M=8, Hq=4, Hkv=2, dh=128, scale=0.1, p_terms=1, O=FAKE, ws=None, wsb=0):
-        return L.patchkv_attend_chunk(dt, Q, K, V, idx, n_src, n_cache, Ks, Vs, M, Hq, Hkv, dh,
-                                      scale, p_terms, O, ws, wsb, None)
+    def chunk(dt=B.BF16, Q=FAKE, K=FAKE, V=FAKE, idx=None, mode=B.IDX_SHARED, counts=None,
+              n_src=64, n_cache=64, Ks=FAKE, Vs=FAKE, M=8, Hq=4, Hkv=2, dh=128, scale=0.1,
+              p_terms=1, O=FAKE, info=None, ws=None, wsb=0):
+        return L.patchkv_attend_chunk(dt, Q, K, V, idx, mode, counts, n_src, n_cache, Ks, Vs, M,
+                                      Hq, Hkv, dh, scale, p_terms, O, info, ws, wsb, None)
     assert chunk(Ks=None) == B.E_NULL
     assert chunk(Vs=None) == B.E_NULL
     assert chunk(dt=B.F64) == B.E_DTYPE
@@ -101,6 +115,9 @@ def test_attend_chunk_validation(L):
     assert chunk(p_terms=3) == B.E_VALUE
     assert chunk(scale=-1.0) == B.E_VALUE
     assert chunk(Ks=FAKE + 8) == B.E_VALUE                # misaligned
+    assert chunk(mode=5) == B.E_VALUE
+    assert chunk(mode=B.IDX_PER_HEAD) == B.E_NULL         # per-head sets need idx
+    assert chunk(idx=FAKE, mode=B.IDX_PER_HEAD, counts=FAKE, info=FAKE) == B.E_WORKSPACE
     assert chunk() == B.E_WORKSPACE
     # bf16 workspace: V^T tiles of the cache and of the own entries, one flag per item
     # (plus split-key partials, as for attend_full at the same shape)
@@ -151,17 +168,23 @@ def test_solve_validation(L):
 
 def test_layer_validation(L):
     f = L.patchkv_compute_layer_patch
-    args = dict(dt=B.BF16, acc=B.F32, Q=FAKE, K=FAKE, V=FAKE, idx=FAKE, Kc=None, Vc=None, W=FAKE,
-                M=8, N=64, Bn=16, Hq=4, Hkv=2, dh=128, scale=0.1, rho=1, lam=0.1, mode=0, dW=FAKE,
-                info=FAKE, ws=None, wsb=0)
+    args = dict(dt=B.BF16, acc=B.F32, Q=FAKE, K=FAKE, V=FAKE, idx=FAKE, imode=B.IDX_SHARED,
+                counts=None, Kc=None, Vc=None, W=FAKE, M=8, N=64, Bn=16, Hq=4, Hkv=2, dh=128,
+                scale=0.1, rho=1, lam=0.1, mode=0, dW=FAKE, info=FAKE, ws=None, wsb=0)
 
     def call(**kw):
         a = dict(args, **kw)
-        return f(a["dt"], a["acc"], a["Q"], a["K"], a["V"], a["idx"], a["Kc"], a["Vc"], a["W"],
-                 a["M"], a["N"], a["Bn"], a["Hq"], a["Hkv"], a["dh"], a["scale"], a["rho"],
-                 a["lam"], a["mode"], a["dW"], a["info"], a["ws"], a["wsb"], None)
+        return f(a["dt"], a["acc"], a["Q"], a["K"], a["V"], a["idx"], a["imode"], a["counts"],
+                 a["Kc"], a["Vc"], a["W"], a["M"], a["N"], a["Bn"], a["Hq"], a["Hkv"], a["dh"],
+                 a["scale"], a["rho"], a["lam"], a["mode"], a["dW"], a["info"], a["ws"], a["wsb"],
+                 None)
 
     assert call(idx=None) == B.E_NULL            # neither idx nor Kc/Vc
+    assert call(info=None) == B.E_NULL
+    assert call(imode=3) == B.E_VALUE
+    assert call(idx=None, Kc=FAKE, Vc=FAKE, imode=B.IDX_PER_HEAD) == B.E_NULL
+    assert call(counts=FAKE + 2) == B.E_VALUE
+    assert call(imode=B.IDX_PER_HEAD, counts=FAKE) == B.E_WORKSPACE
     assert call(acc=B.BF16) == B.E_DTYPE
     assert call(Hq=4, Hkv=3) == B.E_SHAPE
     assert call(lam=0.0) == B.E_VALUE
@@ -191,11 +214,11 @@ def test_mlp_validation(L):
 
 
 def test_attend_cache_validation(L):
-    def cache(dt=B.BF16, Q=FAKE, K=FAKE, V=FAKE, fmt=0, Ke=None, Ve=None, idx=None, n_src=64,
-              n_cache=64, bias=None, M=8, Hq=4, Hkv=2, dh=128, scale=0.1, p_terms=2, O=FAKE,
-              ws=None, wsb=0):
-        return L.patchkv_attend_cache(dt, Q, K, V, fmt, Ke, Ve, idx, n_src, n_cache, bias, M, Hq,
-                                      Hkv, dh, scale, p_terms, O, ws, wsb, None)
+    def cache(dt=B.BF16, Q=FAKE, K=FAKE, V=FAKE, fmt=0, Ke=None, Ve=None, idx=None,
+              mode=B.IDX_SHARED, counts=None, n_src=64, n_cache=64, bias=None, M=8, Hq=4, Hkv=2,
+              dh=128, scale=0.1, p_terms=2, O=FAKE, info=None, ws=None, wsb=0):
+        return L.patchkv_attend_cache(dt, Q, K, V, fmt, Ke, Ve, idx, mode, counts, n_src, n_cache,
+                                      bias, M, Hq, Hkv, dh, scale, p_terms, O, info, ws, wsb, None)
     assert cache(K=None) == B.E_NULL
     assert cache(fmt=3) == B.E_VALUE
     assert cache(fmt=B.KV_MXINT8) == B.E_NULL              # exponents missing
@@ -203,6 +226,9 @@ def test_attend_cache_validation(L):
     assert cache(n_cache=65) == B.E_SHAPE
     assert cache(bias=FAKE + 4) == B.E_VALUE              # misaligned
     assert cache(p_terms=0) == B.E_VALUE
+    assert cache(mode=9) == B.E_VALUE
+    assert cache(mode=B.IDX_PER_HEAD) == B.E_NULL
+    assert cache(idx=FAKE, mode=B.IDX_PER_HEAD, counts=FAKE, info=FAKE) == B.E_WORKSPACE
     assert cache() == B.E_WORKSPACE
     plain = L.patchkv_attend_cache_workspace_bytes(B.BF16, B.KV_PLAIN, 8, 64, 4, 2, 128)
     q8 = L.patchkv_attend_cache_workspace_bytes(B.BF16, B.KV_MXINT8, 8, 64, 4, 2, 128)

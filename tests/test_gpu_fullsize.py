@@ -36,7 +36,7 @@ from make_oracle_fixtures import fixture_path, sample_rows, sample_tokens, sketc
 pytestmark = pytest.mark.gpu
 
 CASES = [(1, 0), (2, 0), (4, 0), (3, 0), (3, 8), (3, 16), (3, 24), (3, 31), (5, 0), (6, 0), (7, 0),
-         (8, 0)]
+         (8, 0), (9, 0)]
 TOL = 2e-2
 
 
@@ -90,7 +90,7 @@ def test_full_size_layer_patch(cid, layer):
         q = (lambda a: a) if qc.bits == 8 else unpack_int4
         Kc, Vc = oracle.dequantize_mx(q(qc.Kq), qc.Ke), oracle.dequantize_mx(q(qc.Vq), qc.Ve)
     elif inp.idx is not None:
-        Kc, Vc = oracle.gather_cache(K, V, inp.idx)
+        Kc, Vc = oracle.gather_cache(K, V, inp.idx, inp.counts)
     else:
         Kc, Vc = oracle.decode(inp.Kc, dt), oracle.decode(inp.Vc, dt)
     cb = None if cbias is None else cbias.astype(np.float64)
@@ -118,7 +118,7 @@ def test_full_size_layer_patch(cid, layer):
         return
     # the single-call entry point runs the same kernels in the same order
     dW2, info2 = pkv.compute_layer_patch(L.Q, L.K, L.V, L.W, idx=L.idx, Kc=L.Kc, Vc=L.Vc,
-                                         lam=cfg.lam, scale=cfg.scale)
+                                         counts=L.counts, lam=cfg.lam, scale=cfg.scale)
     torch.cuda.synchronize()
     assert int(info2.item()) == 0
     assert torch.equal(dW2, bufs.dW[0])

@@ -963,3 +963,103 @@ def test_decode_and_layer_patch_pins_catch_planted_mistakes():
     assert not check_decode_bf16(decode_half)
     assert check_layer_patch(layer_patch_swapped) > 1e-2
     assert check_layer_patch(layer_patch_teacher_basis) > 1e-2
+
+
+# ------------------------------------------------- per-KV-head eviction index sets
+
+def brute_attention_heads(Q, K, V, sets, scale):
+    """Scalar loops: KV head g's cache is the rows of K[g], V[g] listed in sets[g]."""
+    M, Hq, dh = Q.shape
+    Hkv = K.shape[0]
+    grp = Hq // Hkv
+    O = np.zeros((M, Hq * dh))
+    for m in range(M):
+        for h in range(Hq):
+            g = h // grp
+            s = [scale * sum(Q[m, h, c] * K[g, n, c] for c in range(dh)) for n in sets[g]]
+            mx = max(s)
+            e = [math.exp(x - mx) for x in s]
+            for c in range(dh):
+                O[m, h * dh + c] = sum(e[i] * V[g, n, c] for i, n in enumerate(sets[g])) / sum(e)
+    return O
+
+
+def _head_sets_case(rng):
+    Q, K, V = rand_attn(rng, 4, 30, 6, 3, 4, kscale=1.5)
+    counts = np.array([7, 3, 5], dtype=np.int32)
+    idx = np.full((3, 7), -1, dtype=np.int32)
+    sets = []
+    for g in range(3):
+        sg = np.sort(rng.choice(30, size=counts[g], replace=False))
+        idx[g, :counts[g]] = sg
+        sets.append(list(sg))
+    return Q, K, V, idx, counts, sets
+
+
+def check_per_head_gather(gather) -> float:
+    rng = np.random.default_rng(91)
+    Q, K, V, idx, counts, sets = _head_sets_case(rng)
+    Kc, Vc = gather(K, V, idx, counts)
+    return rel(oracle.attention(Q, Kc, Vc, 0.5), brute_attention_heads(Q, K, V, sets, 0.5))
+
+
+def test_per_head_gather_bruteforce_and_reductions():
+    assert check_per_head_gather(oracle.gather_cache) < 1e-13
+    rng = np.random.default_rng(92)
+    Q, K, V = rand_attn(rng, 5, 40, 8, 4, 8)
+    shared = np.sort(rng.choice(40, size=9, replace=False)).astype(np.int32)
+    # one set replicated over the heads is the shared set
+    Ks, Vs = oracle.gather_cache(K, V, shared)
+    Kh, Vh = oracle.gather_cache(K, V, np.tile(shared, (4, 1)))
+    assert rel(oracle.attention(Q, Kh, Vh), oracle.attention(Q, Ks, Vs)) < 1e-15
+    # counts keep a prefix of each head's set; full counts change nothing
+    per = np.stack([np.sort(rng.choice(40, size=9, replace=False)) for _ in range(4)]).astype(np.int32)
+    Ka, Va = oracle.gather_cache(K, V, per)
+    Kb, Vb = oracle.gather_cache(K, V, per, np.full(4, 9))
+    assert rel(oracle.attention(Q, Kb, Vb), oracle.attention(Q, Ka, Va)) < 1e-15
+    cnt = np.array([9, 1, 4, 6])
+    Kt, Vt = oracle.gather_cache(K, V, per, cnt)
+    O = oracle.attention(Q, Kt, Vt)
+    for g in range(4):
+        Kg, Vg = oracle.gather_cache(K[g:g + 1], V[g:g + 1], per[g, :cnt[g]])
+        og = oracle.attention(Q[:, 2 * g:2 * g + 2], Kg, Vg)
+        assert rel(O[:, 2 * g * 8:(2 * g + 2) * 8], og) < 1e-15
+    # a head keeping one entry returns that entry's value
+    assert np.allclose(O[:, 2 * 8:3 * 8], V[1, per[1, 0]][None, :], atol=1e-15)
+    # permuting a head's own set leaves its output unchanged
+    pp = per.copy()
+    pp[2] = pp[2][::-1]
+    Kp, Vp = oracle.gather_cache(K, V, pp)
+    assert rel(oracle.attention(Q, Kp, Vp), oracle.attention(Q, Ka, Va)) < 1e-14
+
+
+def test_per_head_gather_pin_catches_planted_mistakes():
+    def gather_head0(K, V, idx, counts=None):
+        Hkv = K.shape[0]
+        s = idx[0][:int(counts[0])]                       # head 0's set for every head
+        return [K[g][s] for g in range(Hkv)], [V[g][s] for g in range(Hkv)]
+
+    def gather_no_counts(K, V, idx, counts=None):
+        idx = np.where(idx < 0, 0, idx)                   # padding read as row 0
+        return [K[g][idx[g]] for g in range(K.shape[0])], [V[g][idx[g]] for g in range(K.shape[0])]
+
+    assert check_per_head_gather(gather_head0) > 1e-2
+    assert check_per_head_gather(gather_no_counts) > 1e-2
+
+
+def test_per_head_eviction_sets_recipe():
+    inp = make_custom_inputs(M=4, N=500, B=40, Hq=8, Hkv=4, dh=8, cache="evict_heads",
+                             n_sink=4, n_recent=10, seed=5)
+    assert inp.idx.shape == (4, inp.B) and inp.counts.shape == (4,)
+    assert int(inp.counts.sum()) == 4 * 40 and inp.B == int(inp.counts.max())
+    assert len(set(inp.counts.tolist())) > 1                 # the heads' budgets differ
+    for g in range(4):
+        s = inp.idx[g, :inp.counts[g]]
+        assert np.all(np.diff(s) > 0) and np.all(inp.idx[g, inp.counts[g]:] == -1)
+        assert list(s[:4]) == [0, 1, 2, 3] and list(s[-10:]) == list(range(490, 500))
+    # the whole-block patch over per-head sets: ΔW = 0 for a compressed cache that
+    # keeps every token in every head
+    full = make_custom_inputs(M=6, N=12, B=12, Hq=4, Hkv=2, dh=4, cache="identity", seed=6)
+    full.idx = np.tile(np.arange(12, dtype=np.int32), (2, 1))
+    full.counts = np.full(2, 12, dtype=np.int32)
+    assert np.max(np.abs(oracle.layer_patch(full)["dW"])) == 0.0

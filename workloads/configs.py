@@ -10,6 +10,10 @@ Compressed-cache structure:
   * "evict":      B = n_sink sink tokens + the last n_recent tokens + n_random
                   seeded-random middle positions (sorted), i.e. an eviction subset
                   of the full cache, standing in for KVzip's output.
+  * "evict_heads": per-KV-head eviction subsets whose sizes differ between heads
+                  (B entries per head on average), standing in for KVzip's global
+                  head scoring: sinks and recent tokens in every head, the middle
+                  budget shared out over the heads.
   * "synthesize": B synthetic entries, each a seeded-random convex combination of
                   n_mix full-cache entries, standing in for an approximation method
                   (Attention Matching) whose entries are not a subset.
@@ -31,7 +35,7 @@ class Config:
     lam: float        # absolute ridge coefficient
     dtype: str        # "f32" or "bf16" (Q, K, V and W)
     layers: int = 1
-    cache: str = "evict"     # "evict" | "synthesize"
+    cache: str = "evict"     # "evict" | "evict_heads" | "synthesize"
     n_sink: int = 0
     n_recent: int = 0
     n_random: int = 0
@@ -90,6 +94,11 @@ CONFIGS = (
     Config(8, "qwen2.5-7b-layer-64k-synth-bias-mxint8", d=3584, Hq=28, Hkv=4, dh=128, N=65536,
            B=1024, M=2048, lam=5e-2, dtype="bf16", cache="synthesize", n_mix=64,
            kv_format="mxint8", cache_bias=True),
+    # config 3's 32-layer build with per-KV-head eviction sets (KVzip's global head
+    # scoring): 1,720 entries per head on average, the counts differing between heads
+    Config(9, "llama3-8b-32layer-172k-headwise", d=4096, Hq=32, Hkv=8, dh=128, N=172032,
+           B=1720, M=4096, lam=1e-1, dtype="bf16", layers=32, cache="evict_heads", n_sink=4,
+           n_recent=860, n_random=856),
 )
 
 

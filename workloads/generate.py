@@ -5,7 +5,8 @@ Recipe (the same bytes feed the oracle and the GPU path):
 * Every random tensor has a tensor id: 0 key scales, 1 K, 2 V, 3 Q, 4 W,
   5 eviction middle positions, 6 synthesis positions, 7 synthesis weights;
   8 MLP gate projection, 9 MLP up projection, 10 MLP down projection,
-  11 the compressed cache's per-entry logit bias;
+  11 the compressed cache's per-entry logit bias, 12 the per-head budget shares
+  of per-head eviction sets, 13 (block g) the middle positions of KV head g;
   reference chunk j of a chunked reference set: 16 + 4j its queries, 17 + 4j its
   own keys, 18 + 4j its own values.
 * Normal tensors are drawn in C order in blocks of ``BLOCK`` elements; block ``b``
@@ -30,6 +31,15 @@ Recipe (the same bytes feed the oracle and the GPU path):
 * Eviction subset: ``n_sink`` sinks, the last ``n_recent`` tokens, and
   ``n_random`` positions drawn uniformly without replacement from
   [n_sink, N - n_recent), sorted ascending, int32, shared by all KV heads.
+* Per-KV-head eviction subsets (standing in for KVzip's global head scoring,
+  where heads compete for one budget and keep different tokens): every head keeps
+  the sinks and the recent tokens; the Hkv * (B - n_sink - n_recent) middle slots
+  of the total budget are shared out over the heads in proportion to a
+  LogNormal(0, 0.5) weight per head (largest remainders round; no head takes more
+  than the N - n_sink - n_recent middle positions there are), and head g draws its
+  share uniformly without replacement from the middle positions. Each head's set
+  is sorted; the sets are stored as int32 [Hkv, B_max] padded with -1 past each
+  head's count, with the counts as int32 [Hkv].
 * Synthesized compressed cache: entry b mixes ``n_mix`` distinct full-cache
   positions (uniform without replacement over [0, N)) with weights u / sum(u),
   u ~ U(0, 1). The mix is formed in float64 from the (already rounded) K and V,
@@ -52,6 +62,7 @@ BLOCK = 1 << 22
 
 TID_SCALE, TID_K, TID_V, TID_Q, TID_W, TID_EVICT, TID_SYN_POS, TID_SYN_W = range(8)
 TID_GATE, TID_UP, TID_DOWN, TID_BIAS = 8, 9, 10, 11
+TID_HEAD_SHARE, TID_HEAD_EVICT = 12, 13
 TID_CHUNK = 16  # chunk j: 16 + 4j queries, 17 + 4j own keys, 18 + 4j own values
 
 
@@ -120,9 +131,10 @@ class LayerInputs:
     K: np.ndarray                # [Hkv, N, dh]
     V: np.ndarray                # [Hkv, N, dh]
     W: np.ndarray                # [d, d]
-    idx: Optional[np.ndarray] = None   # [B] int32 (eviction) or None
+    idx: Optional[np.ndarray] = None   # [B] or per KV head [Hkv, B] int32 (eviction), or None
     Kc: Optional[np.ndarray] = None    # [Hkv, B, dh] (synthesized) or None
     Vc: Optional[np.ndarray] = None
+    counts: Optional[np.ndarray] = None  # [Hkv] int32 entries kept per head (per-head sets)
     extra: dict = field(default_factory=dict)
 
     @property
@@ -140,6 +152,48 @@ def _eviction_idx(rng: Generator, N: int, n_sink: int, n_recent: int, n_random: 
     return idx.astype(np.int32)
 
 
+def _shares(total: int, weights: np.ndarray, cap: int) -> np.ndarray:
+    """Split ``total`` slots over the heads in proportion to ``weights`` (largest
+    remainders round), no head above ``cap``."""
+    n = np.zeros(len(weights), dtype=np.int64)
+    open_ = np.ones(len(weights), dtype=bool)
+    left = total
+    while left > 0 and open_.any():
+        w = np.where(open_, weights, 0.0)
+        exact = left * w / w.sum()
+        add = np.floor(exact).astype(np.int64)
+        rem = left - int(add.sum())
+        order = np.argsort(-(exact - add), kind="stable")
+        add[order[:rem]] += 1
+        add = np.minimum(add, cap - n)
+        n += add
+        left -= int(add.sum())
+        open_ &= n < cap
+    return n
+
+
+def _eviction_idx_heads(seed: int, cid: int, layer: int, Hkv: int, N: int, B: int,
+                        n_sink: int, n_recent: int):
+    if n_sink + n_recent > B or B > N:
+        raise ValueError("eviction budget inconsistent with the cache")
+    cap = N - n_sink - n_recent
+    w = _rng(seed, cid, layer, TID_HEAD_SHARE).lognormal(0.0, 0.5, size=Hkv)
+    mids = _shares(Hkv * (B - n_sink - n_recent), w, cap)
+    sets = []
+    for g in range(Hkv):
+        mid = _rng(seed, cid, layer, TID_HEAD_EVICT, g).choice(
+            np.arange(n_sink, N - n_recent, dtype=np.int64), size=int(mids[g]), replace=False)
+        ig = np.concatenate([np.arange(n_sink, dtype=np.int64), mid,
+                             np.arange(N - n_recent, N, dtype=np.int64)])
+        ig.sort()
+        sets.append(ig)
+    counts = np.array([len(x) for x in sets], dtype=np.int32)
+    idx = np.full((Hkv, int(counts.max())), -1, dtype=np.int32)
+    for g, ig in enumerate(sets):
+        idx[g, :len(ig)] = ig
+    return idx, counts
+
+
 def make_custom_inputs(*, M: int, N: int, B: int, Hq: int, Hkv: int, dh: int,
                        dtype: str = "bf16", cache: str = "evict", lam: float = 1e-1,
                        seed: int = 0, cid: int = 100, layer: int = 0,
@@ -150,6 +204,8 @@ def make_custom_inputs(*, M: int, N: int, B: int, Hq: int, Hkv: int, dh: int,
 
     For ``cache == "evict"`` the B kept positions are ``n_sink`` sinks + ``n_recent``
     recent + the rest random (defaults: 4 sinks, half of the remainder recent).
+    ``cache == "evict_heads"``: per-KV-head sets with B entries per head on average
+    (``idx`` [Hkv, B_max], ``counts`` [Hkv]; the returned ``B`` is B_max).
     ``cache == "identity"`` keeps every position (B = N): the compressed cache equals
     the full cache.
     """
@@ -181,6 +237,12 @@ def make_custom_inputs(*, M: int, N: int, B: int, Hq: int, Hkv: int, dh: int,
         ns = min(ns, B)
         nr = (B - ns) // 2 if n_recent is None else n_recent
         out.idx = _eviction_idx(_rng(seed, cid, layer, TID_EVICT), N, ns, nr, B - ns - nr)
+    elif cache == "evict_heads":
+        ns = min(4 if n_sink is None else n_sink, B)
+        nr = (B - ns) // 2 if n_recent is None else n_recent
+        out.idx, out.counts = _eviction_idx_heads(seed, cid, layer, Hkv, N, B, ns, nr)
+        out.B = int(out.idx.shape[1])
+        out.extra["B_mean"] = B
     elif cache == "identity":
         if B != N:
             raise ValueError("identity cache needs B == N")
@@ -339,9 +401,9 @@ def make_layer_inputs(cfg: Config, layer: int = 0, seed: int = 0) -> LayerInputs
     """Inputs of layer ``layer`` of one of the five workload configs."""
     if not 0 <= layer < cfg.layers:
         raise ValueError(f"config {cfg.cid} has {cfg.layers} layer(s)")
-    if cfg.cache == "evict":
+    if cfg.cache in ("evict", "evict_heads"):
         return make_custom_inputs(M=cfg.M, N=cfg.N, B=cfg.B, Hq=cfg.Hq, Hkv=cfg.Hkv,
-                                  dh=cfg.dh, dtype=cfg.dtype, cache="evict", lam=cfg.lam,
+                                  dh=cfg.dh, dtype=cfg.dtype, cache=cfg.cache, lam=cfg.lam,
                                   seed=seed, cid=cfg.cid, layer=layer, n_sink=cfg.n_sink,
                                   n_recent=cfg.n_recent)
     return make_custom_inputs(M=cfg.M, N=cfg.N, B=cfg.B, Hq=cfg.Hq, Hkv=cfg.Hkv, dh=cfg.dh,
