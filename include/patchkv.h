@@ -56,7 +56,8 @@ typedef enum {
   PATCHKV_E_VALUE = 4,       /* a scalar is out of range (lambda <= 0, scale <= 0, rho not 0/1, ...) */
   PATCHKV_E_WORKSPACE = 5,   /* workspace NULL or smaller than the matching *_workspace_bytes */
   PATCHKV_E_UNSUPPORTED = 6, /* head_dim other than 64 or 128 */
-  PATCHKV_E_HIP = 7          /* the HIP runtime reported an error */
+  PATCHKV_E_HIP = 7,         /* the HIP runtime reported an error */
+  PATCHKV_E_SCRATCH = 8      /* more scratch needed than the fixed buffer of a *_noalloc call holds */
 } patchkv_status;
 
 typedef enum {
@@ -159,6 +160,26 @@ int patchkv_attend_compressed(int dtype, const void* Q, const void* K, const voi
                               int64_t M, int64_t N, int64_t B, int Hq, int Hkv, int dh,
                               float scale, float* O, int32_t* info, void* workspace,
                               size_t workspace_bytes, void* stream);
+
+/* Allocation-free variant of patchkv_attend_compressed, for callers that       */
+/* cannot allocate device memory or bring a workspace: code under HIP graph     */
+/* capture, tight serving loops (e.g. re-patching after each online compaction  */
+/* of the cache), harnesses that forbid hipMalloc. Same arguments and results   */
+/* as patchkv_attend_compressed, without the workspace: the scratch (V^T tiles, */
+/* fast-path flags, split-key partials) lives in one fixed device buffer of     */
+/* PATCHKV_NOALLOC_SCRATCH_BYTES that the library holds on every GPU it runs on */
+/* until the process ends. The call allocates nothing (no hipMalloc, no         */
+/* allocating library routine). A shape whose scratch                           */
+/* (patchkv_attend_workspace_bytes(dtype, M, B, ...)) exceeds the buffer returns */
+/* PATCHKV_E_SCRATCH before anything is enqueued. Every call on one GPU shares  */
+/* that GPU's buffer: calls that overlap on one GPU (other streams, other host  */
+/* threads) race; calls ordered on one stream do not. The first call on a       */
+/* device looks up the buffer's device address (PATCHKV_E_HIP if that fails).   */
+#define PATCHKV_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+int patchkv_attend_compressed_noalloc(int dtype, const void* Q, const void* K, const void* V,
+                                      const int32_t* idx, int idx_mode, const int32_t* counts,
+                                      int64_t M, int64_t N, int64_t B, int Hq, int Hkv, int dh,
+                                      float scale, float* O, int32_t* info, void* stream);
 
 /* ------------------------------------------------------------------------- */
 /* Attention of one reference chunk over a cache plus the chunk's own causal    */

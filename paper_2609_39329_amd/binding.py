@@ -17,7 +17,8 @@ from typing import Optional
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "lib", "libpatchkv.so")
 
-OK, E_NULL, E_SHAPE, E_DTYPE, E_VALUE, E_WORKSPACE, E_UNSUPPORTED, E_HIP = range(8)
+OK, E_NULL, E_SHAPE, E_DTYPE, E_VALUE, E_WORKSPACE, E_UNSUPPORTED, E_HIP, E_SCRATCH = range(9)
+NOALLOC_SCRATCH_BYTES = 64 << 20  # fixed scratch of patchkv_attend_compressed_noalloc
 F32, BF16, F64 = 0, 1, 2
 IDX_SHARED, IDX_PER_HEAD = 0, 1
 RIDGE_ABSOLUTE, RIDGE_ADAPTIVE, RIDGE_TRACE_MEAN = 0, 1, 2
@@ -38,6 +39,9 @@ SIGNATURES = {
     "patchkv_attend_compressed": (_c_int, [_c_int, _c_vp, _c_vp, _c_vp, _c_vp, _c_int, _c_vp,
                                            _c_i64, _c_i64, _c_i64, _c_int, _c_int, _c_int,
                                            ctypes.c_float, _c_vp, _c_vp, _c_vp, _c_sz, _c_vp]),
+    "patchkv_attend_compressed_noalloc": (_c_int, [_c_int, _c_vp, _c_vp, _c_vp, _c_vp, _c_int,
+                                                   _c_vp, _c_i64, _c_i64, _c_i64, _c_int, _c_int,
+                                                   _c_int, ctypes.c_float, _c_vp, _c_vp, _c_vp]),
     "patchkv_attend_chunk_workspace_bytes": (_c_sz, [_c_int, _c_i64, _c_i64, _c_int, _c_int,
                                                      _c_int]),
     "patchkv_attend_chunk": (_c_int, [_c_int, _c_vp, _c_vp, _c_vp, _c_vp, _c_int, _c_vp, _c_i64,
@@ -254,6 +258,30 @@ def attend_compressed(Q, K, V, idx=None, counts=None, scale: Optional[float] = N
            L.patchkv_attend_compressed(dt, _ptr(Q), _ptr(K), _ptr(V), _ptr(idx), mode,
                                        _ptr(counts), M, N, B, Hq, Hkv, dh, scale, _ptr(O),
                                        _ptr(info), _ptr(ws), nb, _stream(stream)))
+    return O
+
+
+def attend_compressed_noalloc(Q, K, V, idx=None, counts=None, scale: Optional[float] = None,
+                              O=None, info=None, stream=None):
+    """attend_compressed through the library's allocation-free entry point: the scratch
+    is the library's fixed device buffer, not a workspace (torch still allocates O
+    when it is not given)."""
+    torch = _torch()
+    _require_gpu(Q, K, V, idx, counts, O, info)
+    M, Hq, dh, Hkv, N = _qkv(Q, K, V)
+    mode, B = _index_set(idx, counts, Hkv)
+    if B is None:
+        B = N
+    _expect(O, "O", torch.float32, (M, Hq * dh))
+    _expect_info(info)
+    dt = _dtype_code(Q)
+    scale = 1.0 / dh ** 0.5 if scale is None else scale
+    if O is None:
+        O = torch.empty((M, Hq * dh), dtype=torch.float32, device=Q.device)
+    _check("patchkv_attend_compressed_noalloc",
+           lib().patchkv_attend_compressed_noalloc(dt, _ptr(Q), _ptr(K), _ptr(V), _ptr(idx), mode,
+                                                   _ptr(counts), M, N, B, Hq, Hkv, dh, scale,
+                                                   _ptr(O), _ptr(info), _stream(stream)))
     return O
 
 

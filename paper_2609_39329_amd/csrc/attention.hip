@@ -42,6 +42,7 @@
 // every row of every partial result has a finite maximum.
 #include <math.h>
 
+#include <mutex>
 #include <type_traits>
 
 #include "common.hpp"
@@ -1202,6 +1203,34 @@ hipError_t launch_idx_check(const CacheIndex& ci, int heads, int64_t B, int64_t 
 hipError_t launch_info_merge(const int32_t* status, int32_t* info, hipStream_t st) {
   hipLaunchKernelGGL(info_merge_kernel, dim3(1), dim3(64), 0, st, status, info);
   return hipGetLastError();
+}
+
+// Fixed scratch of the allocation-free compressed-cache attention: a file-scope
+// device array (zero-initialised, held by every GPU the library runs on until the
+// process ends). Host code never passes the array's name to a kernel: that name is a
+// host-side stand-in. Its device address is looked up once per device.
+static __device__ __align__(256) unsigned char scratch[kNoallocScratchBytes];
+
+namespace {
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+hipError_t noalloc_scratch(void** ptr) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return hipSuccess;
 }
 
 }  // namespace pkv

@@ -15,6 +15,8 @@ using namespace pkv;
 namespace {
 
 constexpr int64_t kMaxDim = 1 << 16;           // d_in, d_out
+static_assert(PATCHKV_NOALLOC_SCRATCH_BYTES == kNoallocScratchBytes,
+              "the header states the size of the allocation-free call's fixed scratch");
 constexpr int64_t kMaxRows = (int64_t)1 << 31;  // M*Hq, N, B, rows
 
 bool al16(const void* p) { return ((uintptr_t)p & 15) == 0; }
@@ -129,6 +131,8 @@ const char* patchkv_status_string(int status) {
     case PATCHKV_E_WORKSPACE: return "workspace missing, misaligned or too small";
     case PATCHKV_E_UNSUPPORTED: return "unsupported head_dim (64 or 128 only)";
     case PATCHKV_E_HIP: return "HIP runtime error";
+    case PATCHKV_E_SCRATCH:
+      return "the call needs more scratch than the fixed buffer of the allocation-free entry point";
     default: return "unknown status";
   }
 }
@@ -159,11 +163,13 @@ int patchkv_attend_full(int dtype, const void* Q, const void* K, const void* V, 
 
 namespace {
 
-// attend_compressed with the scratch from the caller's workspace.
+// attend_compressed with the scratch from the caller's workspace, or (noalloc) from the
+// library's fixed device buffer.
 int attend_compressed_impl(int dtype, const void* Q, const void* K, const void* V,
                            const int32_t* idx, int idx_mode, const int32_t* counts, int64_t M,
                            int64_t N, int64_t B, int Hq, int Hkv, int dh, float scale, float* O,
-                           int32_t* info, void* workspace, size_t workspace_bytes, void* stream) {
+                           int32_t* info, void* workspace, size_t workspace_bytes, bool noalloc,
+                           void* stream) {
   if (!Q || !K || !V || !O) return PATCHKV_E_NULL;
   int s = check_attn_shape(dtype, M, B, Hq, Hkv, dh);
   if (s) return s;
@@ -173,8 +179,15 @@ int attend_compressed_impl(int dtype, const void* Q, const void* K, const void* 
   if (!finite_pos(scale)) return PATCHKV_E_VALUE;
   if (!al16(Q) || !al16(K) || !al16(V) || !al16(O) || !al4(info)) return PATCHKV_E_VALUE;
   const AttnShape sh = attn_shape(dtype, M, B, Hq, Hkv, dh);
-  s = check_ws(workspace, workspace_bytes, plan_attention(sh).ws_bytes);
-  if (s) return s;
+  const size_t need = plan_attention(sh).ws_bytes;
+  if (noalloc) {
+    if (need > kNoallocScratchBytes) return PATCHKV_E_SCRATCH;
+    workspace = nullptr;
+    if (need > 0 && noalloc_scratch(&workspace) != hipSuccess) return PATCHKV_E_HIP;
+  } else {
+    s = check_ws(workspace, workspace_bytes, need);
+    if (s) return s;
+  }
   const int64_t src = idx ? N : B;
   const CacheIndex ci = cache_index(idx, idx_mode, counts, B);
   const hipStream_t st = (hipStream_t)stream;
@@ -192,7 +205,15 @@ int patchkv_attend_compressed(int dtype, const void* Q, const void* K, const voi
                               int32_t* info, void* workspace, size_t workspace_bytes,
                               void* stream) {
   return attend_compressed_impl(dtype, Q, K, V, idx, idx_mode, counts, M, N, B, Hq, Hkv, dh,
-                                scale, O, info, workspace, workspace_bytes, stream);
+                                scale, O, info, workspace, workspace_bytes, false, stream);
+}
+
+int patchkv_attend_compressed_noalloc(int dtype, const void* Q, const void* K, const void* V,
+                                      const int32_t* idx, int idx_mode, const int32_t* counts,
+                                      int64_t M, int64_t N, int64_t B, int Hq, int Hkv, int dh,
+                                      float scale, float* O, int32_t* info, void* stream) {
+  return attend_compressed_impl(dtype, Q, K, V, idx, idx_mode, counts, M, N, B, Hq, Hkv, dh,
+                                scale, O, info, nullptr, 0, true, stream);
 }
 
 size_t patchkv_attend_chunk_workspace_bytes(int dtype, int64_t M, int64_t n_cache, int Hq, int Hkv,

@@ -62,6 +62,12 @@ hipError_t launch_idx_check(const CacheIndex& ci, int heads, int64_t B, int64_t 
 // *info = *status where *status is non-zero.
 hipError_t launch_info_merge(const int32_t* status, int32_t* info, hipStream_t st);
 
+// The allocation-free attention's fixed scratch: its size, and its device address on
+// the current device (looked up on the first call per device).
+constexpr size_t kNoallocScratchBytes = (size_t)64 << 20;
+constexpr int kMaxDevices = 64;
+hipError_t noalloc_scratch(void** ptr);
+
 // ---------------------------------------------------------------- statistics (fp32 acc)
 size_t targets_ws_bytes(int64_t M, int64_t din, int64_t dout);
 // T = (Of - Oc) W + rho (Of - Oc); W bf16 (w_bf16) or f32. With Zf non-null the

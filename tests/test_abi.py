@@ -34,8 +34,8 @@ def test_exports_every_declared_symbol(L):
 
 
 def test_status_strings(L):
-    for s in range(8):
-        assert L.patchkv_status_string(s)
+    for s in range(9):
+        assert L.patchkv_status_string(s) != b"unknown status"
     assert L.patchkv_status_string(99) == b"unknown status"
     assert L.patchkv_version() >= 10000
 
@@ -247,3 +247,16 @@ def test_low_rank_validation(L):
     assert f(FAKE, FAKE, 256, 128, 32, 0, FAKE, FAKE, None, FAKE, nb, None) == B.E_VALUE
     assert f(FAKE, FAKE, 256, 1, 1, 40, FAKE, FAKE, None, FAKE, nb, None) == B.E_SHAPE
     assert f(FAKE, FAKE, 256, 128, 32, 40, FAKE, FAKE, None, FAKE, nb - 1, None) == B.E_WORKSPACE
+
+
+def test_noalloc_rejects_oversized_scratch_on_the_host(L):
+    # bf16 V^T tiles alone: 8 heads x 65536 entries x 128 x 2 bytes = 128 MiB > the fixed 64 MiB
+    assert L.patchkv_attend_workspace_bytes(B.BF16, 64, 65536, 32, 8, 128) > B.NOALLOC_SCRATCH_BYTES
+    f = L.patchkv_attend_compressed_noalloc
+    assert f(B.BF16, FAKE, FAKE, FAKE, None, 0, None, 64, 65536, 65536, 32, 8, 128, 0.1, FAKE, None,
+             None) == B.E_SCRATCH
+    assert f(B.BF16, None, FAKE, FAKE, None, 0, None, 64, 64, 64, 32, 8, 128, 0.1, FAKE, None,
+             None) == B.E_NULL
+    assert f(B.BF16, FAKE, FAKE, FAKE, None, 3, None, 64, 64, 64, 32, 8, 128, 0.1, FAKE, None,
+             None) == B.E_VALUE
+    assert L.patchkv_status_string(B.E_SCRATCH)
