@@ -55,13 +55,15 @@ namespace {
 constexpr float kTau = 8.0f;   // lazy-rescale threshold of the fixup path (log2 units)
 constexpr float kBigSum = 0x1p64f;  // fast path: largest trusted partial row sum (2^kBig, kBig = 64)
 constexpr int kKeyTile = 32;  // keys per iteration, bf16 path
-constexpr int kRowsWG = 256;  // query rows per workgroup (both paths)
+constexpr int kRowsBf16 = 256;  // query rows per workgroup, bf16 path
+constexpr int kRowsF32 = 256;   // query rows per workgroup, f32 path (one thread per row)
+constexpr int kWgPerCu = 1;     // bf16 workgroups resident per CU (launch bound)
 // bf16 path: 32-row query tiles per wave (1: eight waves of 32 rows per workgroup,
 // two waves per SIMD, everything in VGPRs; 2: four waves of 64 rows, one per SIMD,
 // accumulators in AGPRs) and register staging sets of the K/V tile loads
 // (prefetch depth kLoadSets - 1 steps; 2 or 4).
 constexpr int kQT = 1;
-constexpr int kThreadsBf16 = kRowsWG / (32 * kQT) * 64;
+constexpr int kThreadsBf16 = kRowsBf16 / (32 * kQT) * 64;
 constexpr int kLoadSets = 2;
 constexpr int kKeyTileF32 = 32;
 // bf16 fast path without gather, bias or two-term P: K / V^T tiles are loaded straight
@@ -72,6 +74,10 @@ constexpr int kDmaSlots = 8, kDmaAhead = 6, kDmaSteps = 2;
 static_assert(kDmaAhead <= kDmaSlots - kDmaSteps && kDmaAhead >= kDmaSteps + 1,
               "a slot is refilled only after its last read");
 static_assert(kDmaSlots % (2 * kDmaSteps) == 0, "whole barrier groups per unrolled pass");
+// Waves 0 .. kDmaWaves-1 issue all of a tile's loads (the others only compute): with
+// the loads spread over all eight waves the kernel took 5 % more cycles
+constexpr int kDmaWaves = 4;
+constexpr int kDmaLpdMax = 4;  // 16-byte chunks of one K (or V^T) tile per issuing lane, at most
 
 struct AttnParams {
   const void* Q;
@@ -162,7 +168,7 @@ __global__ __launch_bounds__(256) void vt_kernel(const __bf16* __restrict__ V,
 // launched right after on the same stream): the lazy-rescale online softmax, run
 // only for marked work items, overwriting their outputs.
 template <int DH, bool GATHER, bool PSPLIT, bool PARTIAL, bool SAFE, bool OWN, bool BIAS>
-__global__ __launch_bounds__(kThreadsBf16, 1) void attn_bf16_kernel(AttnParams p) {
+__global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnParams p) {
   static_assert(!(OWN && BIAS), "own entries carry no bias");
   constexpr int KT = kKeyTile;
   constexpr int NKT = KT / 32;  // 32-key MFMA tiles per iteration
@@ -214,8 +220,8 @@ __global__ __launch_bounds__(kThreadsBf16, 1) void attn_bf16_kernel(AttnParams p
       if constexpr (!SAFE) {
         if (threadIdx.x == 0) p.flags[w] = 0;
       }
-      for (int i = threadIdx.x; i < kRowsWG; i += blockDim.x) {
-        const int r = rt * kRowsWG + i;
+      for (int i = threadIdx.x; i < kRowsBf16; i += blockDim.x) {
+        const int r = rt * kRowsBf16 + i;
         if (r >= p.rows) break;
         const int64_t rid = ((int64_t)(g * p.n_split + split)) * p.rows + r;
         f32x4* op = (f32x4*)(p.Opart + rid * DH);
@@ -229,7 +235,7 @@ __global__ __launch_bounds__(kThreadsBf16, 1) void attn_bf16_kernel(AttnParams p
   }
   int ntiles = ct;
   if (own_range) {
-    const int last_q = min(p.rows - 1, rt * kRowsWG + kRowsWG - 1) / p.G;
+    const int last_q = min(p.rows - 1, rt * kRowsBf16 + kRowsBf16 - 1) / p.G;
     ntiles = ct + last_q / KT + 1;
   }
 
@@ -238,7 +244,7 @@ __global__ __launch_bounds__(kThreadsBf16, 1) void attn_bf16_kernel(AttnParams p
   const int h32 = lane >> 5, l32 = lane & 31;
   const __bf16* Qb = (const __bf16*)p.Q;
   const __bf16* Kb = (const __bf16*)p.K + (int64_t)g * p.src_rows * DH;
-  const int row_base = rt * kRowsWG + wid * (32 * QT);
+  const int row_base = rt * kRowsBf16 + wid * (32 * QT);
 
   bf16x8 qf[QT][NS];
 #pragma unroll
@@ -494,36 +500,52 @@ __global__ __launch_bounds__(kThreadsBf16, 1) void attn_bf16_kernel(AttnParams p
   }
 
   if constexpr (DMA) {
-    // LDS position c (= tid) of a slot holds K row c / CH, chunk (c % CH) ^ swk(row), and
+    // LDS position c of a slot holds K row c / CH, chunk (c % CH) ^ swk(row), and
     // V^T row c / 4, chunk (c % 4) ^ ((row / 4) % 4): for every 16 consecutive rows read
     // at one chunk index the 16-byte reads land in 16 different bank groups.
     constexpr int RPB = 16 / CH;  // K rows per 256 bytes of LDS
     constexpr int D = kDmaAhead;
-    const int krow = tid / CH, kch = (tid % CH) ^ ((krow / RPB) % CH);
-    const uint32_t koff = (uint32_t)(krow * DH * 2 + kch * 16);
-    const int vrow = tid / 4, vch = (tid % 4) ^ ((vrow / 4) % 4);
-    const uint32_t voff = (uint32_t)(vrow * 64 + vch * 16);
+    // the issuing waves' lanes each move LPD 16-byte chunks of the K tile and LPD of the
+    // V^T tile; chunk c = i * DT + tid of round i
+    constexpr int DT = kDmaWaves * kWave;
+    constexpr int LPD = NCH / DT;
+    static_assert(NCH % DT == 0 && LPD >= 1 && LPD <= kDmaLpdMax && kDmaWaves <= NT / kWave,
+                  "whole DMA rounds of the issuing waves");
+    // (sized by a namespace-scope constant: an array sized by the local constexpr and
+    // captured by the lambdas below made the host pass drop these kernels' launch stubs)
+    uint32_t koff[kDmaLpdMax], voff[kDmaLpdMax];
+#pragma unroll
+    for (int i = 0; i < LPD; ++i) {
+      const int c = i * DT + tid % DT;
+      const int krow = c / CH, kch = (c % CH) ^ ((krow / RPB) % CH);
+      koff[i] = (uint32_t)(krow * DH * 2 + kch * 16);
+      const int vrow = c / 4, vch = (c % 4) ^ ((vrow / 4) % 4);
+      voff[i] = (uint32_t)(vrow * 64 + vch * 16);
+    }
     // the tile offset goes into the per-lane offset, so the buffer range check covers it
     // (OWN: the tiles after the cache range of the last key range are the chunk's own
     // entries, from their own buffers)
     auto issue = [&](int tile, auto slot_t) {
       constexpr int SL = decltype(slot_t)::value;
-      if (tid < NCH) {
-        PKV_LDS void* kd = (PKV_LDS void*)&Kd[SL][wid * 512];
-        PKV_LDS void* vd = (PKV_LDS void*)&Vd[SL][wid * 512];
+      if (wid >= kDmaWaves) return;
+#pragma unroll
+      for (int i = 0; i < LPD; ++i) {
+        // a wave's DMA instruction writes its 64 lanes' chunks to 1 KB of consecutive LDS
+        PKV_LDS void* kd = (PKV_LDS void*)&Kd[SL][(i * DT + wid * 64) * 8];
+        PKV_LDS void* vd = (PKV_LDS void*)&Vd[SL][(i * DT + wid * 64) * 8];
         if (OWN && own_range && tile >= ct) {
           const uint32_t j0 = (uint32_t)((tile - ct) * KT);
-          __builtin_amdgcn_raw_ptr_buffer_load_lds(ksrs, kd, 16, koff + j0 * (DH * 2), 0, 0, 0);
-          __builtin_amdgcn_raw_ptr_buffer_load_lds(vtsrs, vd, 16, voff + (j0 / 32) * (DH * 64), 0, 0, 0);
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(ksrs, kd, 16, koff[i] + j0 * (DH * 2), 0, 0, 0);
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(vtsrs, vd, 16, voff[i] + (j0 / 32) * (DH * 64), 0, 0, 0);
         } else {
           const uint32_t kb0 = (uint32_t)(k_begin + tile * KT);
-          __builtin_amdgcn_raw_ptr_buffer_load_lds(krs, kd, 16, koff + kb0 * (DH * 2), 0, 0, 0);
-          __builtin_amdgcn_raw_ptr_buffer_load_lds(vrs, vd, 16, voff + (kb0 / 32) * (DH * 64), 0, 0, 0);
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(krs, kd, 16, koff[i] + kb0 * (DH * 2), 0, 0, 0);
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(vrs, vd, 16, voff[i] + (kb0 / 32) * (DH * 64), 0, 0, 0);
         }
       }
     };
-    // wait until at most N of this wave's loads are in flight, then a plain barrier (no
-    // fence: it would wait for every load in flight)
+    // wait until at most N of this wave's loads are in flight (waves that issue none pass
+    // at once), then a plain barrier (no fence: it would wait for every load in flight)
     auto sync_slots = [&](auto n_t) {
       constexpr int N = decltype(n_t)::value;
       asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
@@ -555,7 +577,7 @@ __global__ __launch_bounds__(kThreadsBf16, 1) void attn_bf16_kernel(AttnParams p
     static_assert(NKT == 1 && !PSPLIT, "DMA path: one 32-key MFMA tile, one-term P");
     static_for<D>([&](auto j_t) { issue(decltype(j_t)::value, j_t); });
     // tiles 0 .. kDmaSteps resident
-    sync_slots(std::integral_constant<int, 2 * (D - kDmaSteps - 1)>{});
+    sync_slots(std::integral_constant<int, 2 * LPD * (D - kDmaSteps - 1)>{});
     f32x16 sa[NKT][QT], sb[NKT][QT];
     scores_d(sa, std::integral_constant<int, 0>{});
     mask(sa, 0);  // a key range shorter than one tile
@@ -581,7 +603,7 @@ __global__ __launch_bounds__(kThreadsBf16, 1) void attn_bf16_kernel(AttnParams p
       // a barrier after every kDmaSteps steps: the next group reads up to tile
       // t + kDmaSteps + 1, and 2 (D - kDmaSteps - 1) loads of later tiles may be in flight
       if constexpr (I % kDmaSteps == kDmaSteps - 1)
-        sync_slots(std::integral_constant<int, 2 * (D - kDmaSteps - 1)>{});
+        sync_slots(std::integral_constant<int, 2 * LPD * (D - kDmaSteps - 1)>{});
     };
     auto steps = [&](auto masked_t, int t) {
       static_for<NSL / 2>([&](auto h_t) {
@@ -757,7 +779,7 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnParams p) {
   const int32_t* ig = GATHER ? p.idx + (int64_t)g * p.idx_stride : nullptr;
 
   const int tid = threadIdx.x;
-  const int r = rt * kRowsWG + tid;
+  const int r = rt * kRowsF32 + tid;
   const int rr = min(r, p.rows - 1);
   const int m = rr / p.G, j = rr - m * p.G;
   const float* Kb = (const float*)p.K + (int64_t)g * p.src_rows * DH;
@@ -829,7 +851,7 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnParams p) {
     // own entries 0..m of this thread's query m, up to the workgroup's last query
     const float* Ksb = (const float*)p.Ks + (int64_t)g * p.Ms * DH;
     const float* Vsb = (const float*)p.Vs + (int64_t)g * p.Ms * DH;
-    const int last_q = min(p.rows - 1, rt * kRowsWG + kRowsWG - 1) / p.G;
+    const int last_q = min(p.rows - 1, rt * kRowsF32 + kRowsF32 - 1) / p.G;
     for (int tb = 0; tb <= last_q; tb += KT) {
       for (int c = tid; c < KT * C4; c += 256) {
         const int row = c / C4, col = c % C4;
@@ -1003,15 +1025,17 @@ hipError_t launch_dh(const AttnShape& s, const AttnPlan& pl, AttnParams& p, bool
 AttnPlan plan_attention(const AttnShape& s) {
   AttnPlan pl{};
   const int64_t rows = s.M * (s.Hq / s.Hkv);
-  pl.row_tiles = (int)((rows + kRowsWG - 1) / kRowsWG);
+  const int rows_wg = s.bf16 ? kRowsBf16 : kRowsF32;
+  pl.row_tiles = (int)((rows + rows_wg - 1) / rows_wg);
   const int kt = s.bf16 ? kKeyTile : kKeyTileF32;
   const int64_t ntiles = (s.Nk + kt - 1) / kt;
   const int64_t items = (int64_t)s.Hkv * pl.row_tiles;
   // Pick the number of key ranges that minimises (rounds of workgroups) x (tiles
-  // per workgroup) plus the merge traffic, on 256 CUs with one workgroup each.
-  const double slots = 256.0;
-  // one bf16 tile-iteration of a workgroup ~ 64 x 256 x dh x 4 flops at ~4 TFLOP/s per CU
-  const double tile_s = (double)kt * kRowsWG * s.dh * 4.0 / (s.bf16 ? 4e12 : 0.25e12);
+  // per workgroup) plus the merge traffic, on 256 CUs.
+  const double slots = 256.0 * (s.bf16 ? kWgPerCu : 1);
+  // one bf16 tile-iteration of a workgroup ~ 64 x rows x dh x 4 flops at ~4 TFLOP/s per CU
+  // (shared by the workgroups resident on the CU)
+  const double tile_s = (double)kt * rows_wg * s.dh * 4.0 / (s.bf16 ? 4e12 / kWgPerCu : 0.25e12);
   double best = 1e300;
   int best_s = 1;
   for (int sp = 1; sp <= 64 && sp <= ntiles; ++sp) {
