@@ -5,7 +5,7 @@ the same counters as a kernel of interest (FETCH_SIZE, WRITE_SIZE) gives the rat
 between counter readings and the bytes actually moved (1 GiB read and 1 GiB written
 per dispatch).
 
-    python paper_2609_39329_amd/copy_calib.py
+    python copy_calib.py
 """
 import torch
 

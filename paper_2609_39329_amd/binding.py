@@ -15,7 +15,9 @@ import os
 from typing import Optional
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "lib", "libpatchkv.so")
+# PATCHKV_LIBRARY names another build of the same library (the host AddressSanitizer
+# build of the C ABI layer, for the CPU validation tests)
+LIB_PATH = os.environ.get("PATCHKV_LIBRARY") or os.path.join(HERE, "lib", "libpatchkv.so")
 
 OK, E_NULL, E_SHAPE, E_DTYPE, E_VALUE, E_WORKSPACE, E_UNSUPPORTED, E_HIP, E_SCRATCH = range(9)
 NOALLOC_SCRATCH_BYTES = 64 << 20  # fixed scratch of patchkv_attend_compressed_noalloc

@@ -23,6 +23,8 @@ SOURCES = ["attention.hip", "stats.hip", "solve.hip", "capi.cpp"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function"]
 DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# The C ABI layer holds no device code: plain host C++ against the HIP runtime headers.
+HOST = ["-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include"]
 # Per-source extras. The attention kernels never see NaNs (masked scores are -inf),
 # so they run with the IEEE mode bit off, which lets max() skip NaN quieting.
 EXTRA = {"attention.hip": ["-mno-amdgpu-ieee", "-fno-honor-nans"]}
@@ -35,11 +37,19 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found (ROCm is required to build libpatchkv)")
 
 
+def host_cxx() -> str:
+    for c in (os.environ.get("CXX"), shutil.which("g++"), shutil.which("c++")):
+        if c and os.path.exists(c):
+            return c
+    raise RuntimeError("no host C++ compiler found")
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(OBJ, os.path.splitext(src)[0] + ".o")
-    cmd = [hipcc(), *COMMON]
     if src.endswith(".hip"):
-        cmd += DEVICE
+        cmd = [hipcc(), *COMMON, *DEVICE]
+    else:
+        cmd = [host_cxx(), *COMMON, *HOST]
     cmd += EXTRA.get(src, [])
     cmd += ["-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
