@@ -72,12 +72,14 @@ typedef enum {
   /* lambda is lambda_0; ridge = lambda_0 tr(G) / d_in, the mean eigenvalue: the
    * trace-mean scaling that the paper's ridge-scaling ablation compares with Eq. 7 */
   PATCHKV_RIDGE_TRACE_MEAN = 2,
-  /* Flag OR-ed into either mode; used by the F32 solve only (F64 ignores it).
-   * Without it the F32 solve forms its block products on bf16 MFMA with every fp32
-   * operand split into two bf16 terms (hi + lo) and three cross products kept,
-   * i.e. about 2^-16 relative error per product instead of fp32's 2^-24, at
-   * 2.5x-5x the speed. With it the products are exact fp32 multiplies (fp32 MFMA). */
-  PATCHKV_SOLVE_EXACT_F32 = 16
+  /* Flags OR-ed into any mode, used by the F32 solve only (F64 ignores them), at most
+   * one of them. By default the F32 solve keeps the paper's FP32 patch construction
+   * (App. B.1): every fp32 operand of a block product is split into three bf16 pieces
+   * and six bf16 MFMA products are summed in fp32, as exact as an fp32 multiply
+   * (about 2^-24 relative per product). */
+  PATCHKV_SOLVE_EXACT_F32 = 16, /* exact fp32 products on fp32 MFMA (slower) */
+  PATCHKV_SOLVE_FAST_BF16 = 32  /* two bf16 pieces, three products: about 2^-16 relative
+                                   per product, faster; below FP32 grade */
 } patchkv_ridge_mode;
 
 /* Index sets of an eviction-style compressed cache (the `idx_mode` argument).    */
@@ -331,8 +333,9 @@ int patchkv_accumulate_normal_eq(int acc_dtype, const float* Xc, const float* Yf
 /*   lambda_0 ||G||_F^2 / tr(G) (Eq. 7), computed on the device in fp64.        */
 /* ridge_mode TRACE_MEAN: lambda is lambda_0 (> 0) and the coefficient is       */
 /*   lambda_0 tr(G) / d_in, computed on the device in fp64.                     */
-/* ridge_mode | PATCHKV_SOLVE_EXACT_F32: exact fp32 products in the F32 solve.   */
-/*   Any other bit set in ridge_mode: PATCHKV_E_VALUE.                          */
+/* ridge_mode | PATCHKV_SOLVE_EXACT_F32 or | PATCHKV_SOLVE_FAST_BF16: the F32    */
+/*   solve's block products (see patchkv_ridge_mode; default FP32-grade). Both   */
+/*   flags, or any other bit set in ridge_mode: PATCHKV_E_VALUE.                */
 /* dW [d_in][d_out] float, written.                                             */
 /* info: device int32, written: 0 on success, else the 1-based column of the    */
 /*   first non-positive (or NaN) pivot, LAPACK style (dW is then meaningless).  */

@@ -24,7 +24,10 @@ NOALLOC_SCRATCH_BYTES = 64 << 20  # fixed scratch of patchkv_attend_compressed_n
 F32, BF16, F64 = 0, 1, 2
 IDX_SHARED, IDX_PER_HEAD = 0, 1
 RIDGE_ABSOLUTE, RIDGE_ADAPTIVE, RIDGE_TRACE_MEAN = 0, 1, 2
-SOLVE_EXACT_F32 = 16  # flag OR-ed into a ridge mode: exact fp32 products in the F32 solve
+# flags OR-ed into a ridge mode for the F32 solve's block products (default: three bf16
+# pieces, six products, FP32-grade)
+SOLVE_EXACT_F32 = 16  # exact fp32 products on fp32 MFMA
+SOLVE_FAST_BF16 = 32  # two bf16 pieces, three products (about 2^-16 per product)
 
 _c_i64 = ctypes.c_int64
 _c_int = ctypes.c_int

@@ -73,14 +73,21 @@ int check_ws(const void* ws, size_t have, size_t need) {
 }
 
 bool finite_pos(double x) { return isfinite(x) && x > 0.0; }
+constexpr int kProductFlags = PATCHKV_SOLVE_EXACT_F32 | PATCHKV_SOLVE_FAST_BF16;
 bool valid_ridge_mode(int m) {
-  const int base = m & ~PATCHKV_SOLVE_EXACT_F32;
+  const int base = m & ~kProductFlags;
+  if ((m & kProductFlags) == kProductFlags) return false;  // one product mode at most
   return base == PATCHKV_RIDGE_ABSOLUTE || base == PATCHKV_RIDGE_ADAPTIVE ||
          base == PATCHKV_RIDGE_TRACE_MEAN;
 }
 // 0: absolute, 1: Eq. 7, 2: trace mean (the solve's ridge selector)
-int ridge_kind(int m) { return m & ~PATCHKV_SOLVE_EXACT_F32; }
-bool exact(int m) { return (m & PATCHKV_SOLVE_EXACT_F32) != 0; }
+int ridge_kind(int m) { return m & ~kProductFlags; }
+// the F32 solve's block products
+int products(int m) {
+  if (m & PATCHKV_SOLVE_EXACT_F32) return kProductsExact;
+  if (m & PATCHKV_SOLVE_FAST_BF16) return kProductsSplit3;
+  return kProductsSplit6;
+}
 
 int check_stats_dims(int64_t rows, int64_t din, int64_t dout) {
   if (rows < 1 || din < 1 || dout < 1) return PATCHKV_E_SHAPE;
@@ -451,7 +458,7 @@ int patchkv_solve_patch(int acc_dtype, const void* G, const void* C, int64_t d_i
   int s = check_ws(workspace, workspace_bytes, solve_ws_bytes(acc_dtype == PATCHKV_F64, d_in, d_out));
   if (s) return s;
   return status_of(launch_solve(acc_dtype == PATCHKV_F64, G, C, d_in, d_out, lambda,
-                                ridge_kind(ridge_mode), exact(ridge_mode), dW, info, workspace,
+                                ridge_kind(ridge_mode), products(ridge_mode), dW, info, workspace,
                                 (hipStream_t)stream));
 }
 
@@ -560,7 +567,7 @@ int patchkv_compute_layer_patch(int dtype, int acc_dtype, const void* Q, const v
   }
   if (e != hipSuccess) return PATCHKV_E_HIP;
   e = launch_solve(acc_dtype == PATCHKV_F64, G, C, d, d, lambda, ridge_kind(ridge_mode),
-                   exact(ridge_mode), dW, info, wsv, st);
+                   products(ridge_mode), dW, info, wsv, st);
   if (e == hipSuccess) e = launch_info_merge(stat, info, st);
   return status_of(e);
 }

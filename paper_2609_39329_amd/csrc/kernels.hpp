@@ -109,10 +109,13 @@ hipError_t launch_low_rank(const float* G, const float* dW, int64_t din, int64_t
                            int iters, float* A, float* U, float* dWr, void* ws, hipStream_t st);
 size_t solve_ws_bytes(bool f64, int64_t din, int64_t dout);
 // ridge: 0 the coefficient is lambda; 1 lambda ||G||_F^2 / tr G (Eq. 7); 2 lambda tr G / d.
-// exact_f32: fp32 block products on fp32 MFMA (else three bf16 MFMA terms); the
-// fp64 solve always uses fp64 arithmetic.
+// products (fp32 solve): how block products are formed; the fp64 solve always uses
+// fp64 arithmetic.
+constexpr int kProductsSplit6 = 0;  // three bf16 pieces per operand, six MFMA terms (FP32-grade)
+constexpr int kProductsExact = 1;   // fp32 MFMA (exact fp32 products)
+constexpr int kProductsSplit3 = 2;  // two bf16 pieces, three MFMA terms (about 2^-16)
 hipError_t launch_solve(bool f64, const void* G, const void* C, int64_t din, int64_t dout,
-                        double lambda, int ridge, bool exact_f32, float* dW, int32_t* info,
+                        double lambda, int ridge, int products, float* dW, int32_t* info,
                         void* ws, hipStream_t st);
 
 // Small helpers.

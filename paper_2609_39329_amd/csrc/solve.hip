@@ -13,10 +13,11 @@
 // GEMM instead of a substitution); its condition number is at most the square root
 // of that of G + lambda I. The OB-wide inverses are assembled from the NB-wide ones
 // by batched GEMMs.
-// fp32 block products split both operands into bf16 hi + lo and sum three bf16 MFMA
-// products (128 x 128 tiles; 64 x 64 with the whole K range staged at once for the
-// latency-bound K <= 128 updates), or run on MFMA 32x32x2 f32 when exact fp32 products
-// are asked for; fp64 tiles run on fp64 FMA. The adaptive ridge of Eq. 7, lambda_0 ||G||_F^2 / tr G, and
+// fp32 block products split both operands into three bf16 pieces and sum six bf16
+// MFMA products, as exact as fp32 products (128 x 128 tiles; 64 x 64 with the whole K
+// range staged at once for the latency-bound K <= 128 updates); on request they split
+// into two pieces and three products (about 2^-16 relative, faster) or run on MFMA
+// 32x32x2 f32 (exact fp32 products). fp64 tiles run on fp64 FMA. The adaptive ridge of Eq. 7, lambda_0 ||G||_F^2 / tr G, and
 // the trace-mean scaling lambda_0 tr G / d are reduced on the device in fp64 in a fixed
 // order (deterministic).
 #include <math.h>
@@ -210,15 +211,19 @@ __device__ __forceinline__ void gemm_f32_body(const GemmDesc<float>& g, int t) {
       }
 }
 
-// ---- fp32 via three bf16 MFMA terms: 128 x 128 output tile, 4 waves ------------------
+// ---- fp32 via bf16 MFMA terms: 128 x 128 output tile, 4 waves -------------------------
 //
-// Each fp32 operand x is split as x_hi = bf16(x), x_lo = bf16(x - x_hi) while it is
-// staged into LDS, and a b ~ a_hi b_hi + a_hi b_lo + a_lo b_hi on MFMA 32x32x16 bf16
-// with fp32 accumulation (representation error of the split about 2^-18 relative,
-// the dropped a_lo b_lo term about the same). The MFMA computes the transposed tile
-// (rows = output columns), so every lane owns 4 consecutive output columns of one
-// output row and the read-modify-write of C uses 16-byte accesses. The C tile is
-// fetched before the K loop so its latency hides behind the products.
+// Each fp32 operand x is split into bf16 pieces while it is staged into LDS and the
+// product is formed from bf16 MFMA 32x32x16 products with fp32 accumulation:
+//  TERMS = 6 (FP32-grade): x = h + m + l, h = bf16(x), m = bf16(x - h),
+//    l = bf16(x - h - m), which represents x to about 2^-27; a b ~ hh + hm + mh + mm +
+//    hl + lh, the dropped ml, lm, ll about 2^-27 relative: the products are as exact as
+//    fp32 multiplication (2^-24) and the sums are fp32.
+//  TERMS = 3: x = h + l, a b ~ hh + hl + lh, about 2^-16 relative per product.
+// The MFMA computes the transposed tile (rows = output columns), so every lane owns 4
+// consecutive output columns of one output row and the read-modify-write of C uses
+// 16-byte accesses. The C tile is fetched before the K loop so its latency hides
+// behind the products.
 struct SGemm {
   const float* A;  // A(i,k) = AK ? A[i*sa + k] : A[k*sa + i]
   int64_t sa;
@@ -235,20 +240,71 @@ struct SGemm {
   int64_t bA, bB, bC;
 };
 
-constexpr int S_BM = 128, S_KC = 32;
-constexpr int S_PK = S_KC + 8;    // pitch of a [row][k] LDS tile (bf16)
-constexpr int S_PR = S_BM + 16;   // pitch of a [k][row] LDS tile (bf16)
-constexpr int S_TILE = S_BM * S_PK > S_KC * S_PR ? S_BM * S_PK : S_KC * S_PR;  // bf16 per plane
-constexpr int S_LDS = 2 * 4 * S_TILE;  // 2 buffers x {A hi, A lo, B hi, B lo}
+// bf16 pieces of each operand, and the K chunk staged per round (the six-term products
+// stage half the chunk, so two workgroups still fit in a CU's LDS)
+template <int TERMS>
+struct Split {
+  static_assert(TERMS == 3 || TERMS == 6, "three or six product terms");
+  static constexpr int P = TERMS == 6 ? 3 : 2;     // pieces per operand
+  static constexpr int KC = TERMS == 6 ? 16 : 32;  // K chunk
+};
+
+// x -> bf16 pieces (two elements per conversion), stored at off of each piece's plane
+template <int NP>
+__device__ __forceinline__ void split_store(__bf16* const (&pl)[NP], int off, f32x4 v) {
+  f32x4 r = v;
+#pragma unroll
+  for (int q = 0; q < NP; ++q) {
+    const unsigned h01 = cvt_pk_bf16(r[0], r[1]), h23 = cvt_pk_bf16(r[2], r[3]);
+    *(u32x2*)(pl[q] + off) = u32x2{h01, h23};
+    if (q + 1 < NP) {
+      r[0] -= __builtin_bit_cast(float, h01 << 16);
+      r[1] -= __builtin_bit_cast(float, h01 & 0xffff0000u);
+      r[2] -= __builtin_bit_cast(float, h23 << 16);
+      r[3] -= __builtin_bit_cast(float, h23 & 0xffff0000u);
+    }
+  }
+}
+
+// acc += b a over the kept piece pairs: fb[q] / fa[q] are the pieces of the B / A
+// fragments (transposed tile: MFMA rows are output columns)
+template <int TERMS>
+__device__ __forceinline__ f32x16 split_mfma(const bf16x8 (&fb)[Split<TERMS>::P],
+                                             const bf16x8 (&fa)[Split<TERMS>::P], f32x16 acc) {
+  if constexpr (TERMS == 6) {
+    // the smallest terms first
+    acc = mfma32(fb[2], fa[0], acc);
+    acc = mfma32(fb[0], fa[2], acc);
+    acc = mfma32(fb[1], fa[1], acc);
+    acc = mfma32(fb[1], fa[0], acc);
+    acc = mfma32(fb[0], fa[1], acc);
+    acc = mfma32(fb[0], fa[0], acc);
+  } else {
+    acc = mfma32(fb[0], fa[0], acc);
+    acc = mfma32(fb[0], fa[1], acc);
+    acc = mfma32(fb[1], fa[0], acc);
+  }
+  return acc;
+}
+
+constexpr int S_BM = 128;
+template <int TERMS>
+struct SLayout {
+  static constexpr int KC = Split<TERMS>::KC;
+  static constexpr int PK = KC + 8;    // pitch of a [row][k] LDS tile (bf16)
+  static constexpr int PR = S_BM + 16;   // pitch of a [k][row] LDS tile (bf16)
+  static constexpr int TILE = S_BM * PK > KC * PR ? S_BM * PK : KC * PR;  // bf16 per plane
+  static constexpr int LDS = 2 * 2 * Split<TERMS>::P * TILE;  // 2 buffers x {A, B} x pieces
+};
 
 // CHECK: bounds-checked staging loads (edge tiles); without it the tile must lie
 // inside M x N, K must be a multiple of the chunk and both operands vector-aligned,
 // and the loads are plain 16-byte loads from pointers advanced once per chunk.
-template <bool AK, bool BJ, bool CHECK>
+template <int TERMS, bool AK, bool BJ, bool CHECK>
 __device__ __forceinline__ void sgemm3_tile(const SGemm& g, int i0, int j0, __bf16* lds);
 
 // tile t of g (lower: the triangle's tiles in row order)
-template <bool AK, bool BJ>
+template <int TERMS, bool AK, bool BJ>
 __device__ __forceinline__ void sgemm3_body(const SGemm& g, int t, __bf16* lds) {
   int ti, tj;
   if (g.lower) {
@@ -261,19 +317,23 @@ __device__ __forceinline__ void sgemm3_body(const SGemm& g, int t, __bf16* lds) 
     tj = t % g.tiles_n;
   }
   const int i0 = ti * S_BM, j0 = tj * S_BM;
-  const bool interior = i0 + S_BM <= g.M && j0 + S_BM <= g.N && g.K % S_KC == 0 && g.vecA && g.vecB;
-  if (interior) sgemm3_tile<AK, BJ, false>(g, i0, j0, lds);
-  else sgemm3_tile<AK, BJ, true>(g, i0, j0, lds);
+  const bool interior = i0 + S_BM <= g.M && j0 + S_BM <= g.N && g.K % SLayout<TERMS>::KC == 0 &&
+                        g.vecA && g.vecB;
+  if (interior) sgemm3_tile<TERMS, AK, BJ, false>(g, i0, j0, lds);
+  else sgemm3_tile<TERMS, AK, BJ, true>(g, i0, j0, lds);
 }
 
-template <bool AK, bool BJ, bool CHECK>
+template <int TERMS, bool AK, bool BJ, bool CHECK>
 __device__ __forceinline__ void sgemm3_tile(const SGemm& g, int i0, int j0, __bf16* lds) {
+  using LY = SLayout<TERMS>;
+  constexpr int KC = LY::KC, NP = Split<TERMS>::P;
+  constexpr int NU = S_BM * KC / 4 / 256;  // float4 runs per thread, operand and chunk
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int h32 = lane >> 5, l32 = lane & 31;
   const int wi = (wid >> 1) * 64, wj = (wid & 1) * 64;
   // [row][k] when the contraction index is contiguous in memory, else [k][row]
   constexpr bool a_rk = AK, b_rk = !BJ;
-  constexpr int PA = a_rk ? S_PK : S_PR, PB = b_rk ? S_PK : S_PR;
+  constexpr int PA = a_rk ? LY::PK : LY::PR, PB = b_rk ? LY::PK : LY::PR;
 
   // C tile prefetch: lane owns C[i0+wi+32a+l32][j0+wj+32b+8q+4h32 .. +3]
   f32x4 cpre[2][2][4];
@@ -301,28 +361,28 @@ __device__ __forceinline__ void sgemm3_tile(const SGemm& g, int i0, int j0, __bf
 #pragma unroll
     for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
 
-  // staging: 128 x 32 floats per operand and chunk = 4 float4 per thread, each a
-  // run of 4 elements contiguous in memory
-  f32x4 ra[4], rb[4];
+  // staging: 128 x KC floats per operand and chunk = NU float4 per thread, each a run
+  // of 4 elements contiguous in memory
+  f32x4 ra[NU], rb[NU];
   // unchecked staging: this thread's runs of the first chunk, advanced by one chunk
   // per fetch (fetches are issued in chunk order)
-  const float* pa[4];
-  const float* pb[4];
-  const int64_t stepA = AK ? S_KC : (int64_t)S_KC * g.sa, stepB = BJ ? (int64_t)S_KC * g.sb : S_KC;
+  const float* pa[NU];
+  const float* pb[NU];
+  const int64_t stepA = AK ? KC : (int64_t)KC * g.sa, stepB = BJ ? (int64_t)KC * g.sb : KC;
   if constexpr (!CHECK) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < NU; ++u) {
       const int c = u * 256 + tid;
-      if constexpr (AK) pa[u] = g.A + (int64_t)(i0 + c / (S_KC / 4)) * g.sa + (c % (S_KC / 4)) * 4;
+      if constexpr (AK) pa[u] = g.A + (int64_t)(i0 + c / (KC / 4)) * g.sa + (c % (KC / 4)) * 4;
       else pa[u] = g.A + (int64_t)(c / (S_BM / 4)) * g.sa + i0 + (c % (S_BM / 4)) * 4;
       if constexpr (BJ) pb[u] = g.B + (int64_t)(c / (S_BM / 4)) * g.sb + j0 + (c % (S_BM / 4)) * 4;
-      else pb[u] = g.B + (int64_t)(j0 + c / (S_KC / 4)) * g.sb + (c % (S_KC / 4)) * 4;
+      else pb[u] = g.B + (int64_t)(j0 + c / (KC / 4)) * g.sb + (c % (KC / 4)) * 4;
     }
   }
   auto fetch = [&](int k0) {
     if constexpr (!CHECK) {
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
+      for (int u = 0; u < NU; ++u) {
         ra[u] = *(const f32x4*)pa[u];
         rb[u] = *(const f32x4*)pb[u];
         pa[u] += stepA;
@@ -331,11 +391,11 @@ __device__ __forceinline__ void sgemm3_tile(const SGemm& g, int i0, int j0, __bf
       return;
     }
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < NU; ++u) {
       const int c = u * 256 + tid;
       {
         int i, k;
-        if constexpr (AK) { i = c / (S_KC / 4); k = (c % (S_KC / 4)) * 4; }
+        if constexpr (AK) { i = c / (KC / 4); k = (c % (KC / 4)) * 4; }
         else { k = c / (S_BM / 4); i = (c % (S_BM / 4)) * 4; }
         const int gi = i0 + i, gk = k0 + k;
         const int nvalid = AK ? (gi < g.M ? g.K - gk : 0) : (gk < g.K ? g.M - gi : 0);
@@ -350,7 +410,7 @@ __device__ __forceinline__ void sgemm3_tile(const SGemm& g, int i0, int j0, __bf
       {
         int j, k;
         if constexpr (BJ) { k = c / (S_BM / 4); j = (c % (S_BM / 4)) * 4; }
-        else { j = c / (S_KC / 4); k = (c % (S_KC / 4)) * 4; }
+        else { j = c / (KC / 4); k = (c % (KC / 4)) * 4; }
         const int gj = j0 + j, gk = k0 + k;
         const int nvalid = BJ ? (gk < g.K ? g.N - gj : 0) : (gj < g.N ? g.K - gk : 0);
         const float* s = g.B + (BJ ? (int64_t)gk * g.sb + gj : (int64_t)gj * g.sb + gk);
@@ -363,24 +423,23 @@ __device__ __forceinline__ void sgemm3_tile(const SGemm& g, int i0, int j0, __bf
       }
     }
   };
-  // x_hi = bf16(x), x_lo = bf16(x - x_hi), two elements per conversion
-  auto split_store = [](__bf16* hi, __bf16* lo, int off, f32x4 v) {
-    const unsigned h01 = cvt_pk_bf16(v[0], v[1]), h23 = cvt_pk_bf16(v[2], v[3]);
-    const float f0 = __builtin_bit_cast(float, h01 << 16), f1 = __builtin_bit_cast(float, h01 & 0xffff0000u);
-    const float f2 = __builtin_bit_cast(float, h23 << 16), f3 = __builtin_bit_cast(float, h23 & 0xffff0000u);
-    *(u32x2*)(hi + off) = u32x2{h01, h23};
-    *(u32x2*)(lo + off) = u32x2{cvt_pk_bf16(v[0] - f0, v[1] - f1), cvt_pk_bf16(v[2] - f2, v[3] - f3)};
-  };
-  auto plane = [&](int buf, int p) { return lds + (buf * 4 + p) * S_TILE; };
+  // plane of operand X (0: A, 1: B), piece q, in buffer buf
+  auto plane = [&](int buf, int x, int q) { return lds + ((buf * 2 + x) * NP + q) * LY::TILE; };
   auto stash = [&](int buf) {
-    __bf16 *ah = plane(buf, 0), *al = plane(buf, 1), *bh = plane(buf, 2), *bl = plane(buf, 3);
+    __bf16* pa_[NP];
+    __bf16* pb_[NP];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int q = 0; q < NP; ++q) {
+      pa_[q] = plane(buf, 0, q);
+      pb_[q] = plane(buf, 1, q);
+    }
+#pragma unroll
+    for (int u = 0; u < NU; ++u) {
       const int c = u * 256 + tid;
-      split_store(ah, al, a_rk ? (c / (S_KC / 4)) * PA + (c % (S_KC / 4)) * 4
-                               : (c / (S_BM / 4)) * PA + (c % (S_BM / 4)) * 4, ra[u]);
-      split_store(bh, bl, b_rk ? (c / (S_KC / 4)) * PB + (c % (S_KC / 4)) * 4
-                               : (c / (S_BM / 4)) * PB + (c % (S_BM / 4)) * 4, rb[u]);
+      split_store<NP>(pa_, a_rk ? (c / (KC / 4)) * PA + (c % (KC / 4)) * 4
+                                : (c / (S_BM / 4)) * PA + (c % (S_BM / 4)) * 4, ra[u]);
+      split_store<NP>(pb_, b_rk ? (c / (KC / 4)) * PB + (c % (KC / 4)) * 4
+                                : (c / (S_BM / 4)) * PB + (c % (S_BM / 4)) * 4, rb[u]);
     }
   };
   // 32 rows x 8 k fragment (row r0 + l32, k k0 + 8 h32 ..) of an LDS tile
@@ -392,36 +451,27 @@ __device__ __forceinline__ void sgemm3_tile(const SGemm& g, int i0, int j0, __bf
     return cat8(lds_read_tr16(q), lds_read_tr16(q + 4 * pitch));
   };
 
-  const int nk = (g.K + S_KC - 1) / S_KC;
+  const int nk = (g.K + KC - 1) / KC;
   fetch(0);
   stash(0);
   __syncthreads();
   for (int kc = 0; kc < nk; ++kc) {
     const int buf = kc & 1;
-    if (kc + 1 < nk) fetch((kc + 1) * S_KC);
-    const __bf16 *ah = plane(buf, 0), *al = plane(buf, 1), *bh = plane(buf, 2), *bl = plane(buf, 3);
+    if (kc + 1 < nk) fetch((kc + 1) * KC);
 #pragma unroll
-    for (int ks = 0; ks < S_KC; ks += 16) {
-      bf16x8 fah[2], fal[2], fbh[2], fbl[2];
+    for (int ks = 0; ks < KC; ks += 16) {
+      bf16x8 fa[2][NP], fb[2][NP];
 #pragma unroll
-      for (int a = 0; a < 2; ++a) {
-        fah[a] = frag(ah, PA, a_rk, wi + 32 * a, ks);
-        fal[a] = frag(al, PA, a_rk, wi + 32 * a, ks);
+      for (int q = 0; q < NP; ++q) {
+#pragma unroll
+        for (int a = 0; a < 2; ++a) fa[a][q] = frag(plane(buf, 0, q), PA, a_rk, wi + 32 * a, ks);
+#pragma unroll
+        for (int b = 0; b < 2; ++b) fb[b][q] = frag(plane(buf, 1, q), PB, b_rk, wj + 32 * b, ks);
       }
-#pragma unroll
-      for (int b = 0; b < 2; ++b) {
-        fbh[b] = frag(bh, PB, b_rk, wj + 32 * b, ks);
-        fbl[b] = frag(bl, PB, b_rk, wj + 32 * b, ks);
-      }
-      // transposed tile: MFMA rows are output columns (B), MFMA columns output rows (A)
 #pragma unroll
       for (int a = 0; a < 2; ++a)
 #pragma unroll
-        for (int b = 0; b < 2; ++b) {
-          acc[a][b] = mfma32(fbh[b], fah[a], acc[a][b]);
-          acc[a][b] = mfma32(fbh[b], fal[a], acc[a][b]);
-          acc[a][b] = mfma32(fbl[b], fah[a], acc[a][b]);
-        }
+        for (int b = 0; b < 2; ++b) acc[a][b] = split_mfma<TERMS>(fb[b], fa[a], acc[a][b]);
     }
     if (kc + 1 < nk) stash(buf ^ 1);
     __syncthreads();
@@ -449,37 +499,38 @@ __device__ __forceinline__ void sgemm3_tile(const SGemm& g, int i0, int j0, __bf
 
 // Up to two problems per launch, each with its own operand layout; work items are
 // spread so that consecutive tiles of one problem share an XCD (and its L2).
-template <bool AK0, bool BJ0, bool AK1, bool BJ1>
+template <int TERMS, bool AK0, bool BJ0, bool AK1, bool BJ1>
 __global__ __launch_bounds__(256, 2) void sgemm3_kernel(SGemm d0, SGemm d1) {
-  __shared__ __attribute__((aligned(16))) __bf16 lds[S_LDS];
+  __shared__ __attribute__((aligned(16))) __bf16 lds[SLayout<TERMS>::LDS];
   const int total = d0.ntiles + d1.ntiles;
   const int t = xcd_item((total + kXcds - 1) / kXcds);
   if (t >= total) return;
   if (t < d0.ntiles) {
     int u = t;
     const SGemm g = batch_item(d0, u);
-    sgemm3_body<AK0, BJ0>(g, u, lds);
+    sgemm3_body<TERMS, AK0, BJ0>(g, u, lds);
   } else {
     int u = t - d0.ntiles;
     const SGemm g = batch_item(d1, u);
-    sgemm3_body<AK1, BJ1>(g, u, lds);
+    sgemm3_body<TERMS, AK1, BJ1>(g, u, lds);
   }
 }
 
-// ---- the same three-term products for K <= 128: 64 x 64 tiles, one staging round ------
+// ---- the same split products for K <= 128: 64 x 64 tiles, one staging round ----------
 //
 // The small updates of the factorisation (K = one block column) are latency bound:
-// with 128 x 128 tiles a launch has few workgroups and every 32-wide chunk waits for
-// its loads. Here each workgroup (4 waves of 32 x 32) loads its whole K range in one
-// round (K padded to 16 with zeros, bounds-checked), splits it into the four bf16
-// planes in LDS and runs the MFMAs with no further waits.
+// with 128 x 128 tiles a launch has few workgroups and every chunk waits for its loads.
+// Here each workgroup (4 waves of 32 x 32) loads its whole K range in one round (K
+// padded to 16 with zeros, bounds-checked), splits it into bf16 planes in LDS and runs
+// the MFMAs with no further waits.
 constexpr int T_BM = 64, T_KMAX = 128;
 constexpr int T_PK = T_KMAX + 8;  // pitch of a [row][k] LDS tile (bf16)
 constexpr int T_PR = T_BM + 16;   // pitch of a [k][row] LDS tile (bf16)
 constexpr int T_TILE = T_BM * T_PK > T_KMAX * T_PR ? T_BM * T_PK : T_KMAX * T_PR;  // bf16 per plane
 
-template <bool AK, bool BJ>
+template <int TERMS, bool AK, bool BJ>
 __device__ __forceinline__ void sgemm3s_body(const SGemm& g, int t, __bf16* lds) {
+  constexpr int NP = Split<TERMS>::P;
   int ti, tj;
   if (g.lower) {
     ti = (int)((sqrtf(8.f * (float)t + 1.f) - 1.f) * 0.5f);
@@ -554,26 +605,24 @@ __device__ __forceinline__ void sgemm3s_body(const SGemm& g, int t, __bf16* lds)
       rb[u] = v;
     }
   }
-  // x_hi = bf16(x), x_lo = bf16(x - x_hi), two elements per conversion
-  auto split_store = [](__bf16* hi, __bf16* lo, int off, f32x4 v) {
-    const unsigned h01 = cvt_pk_bf16(v[0], v[1]), h23 = cvt_pk_bf16(v[2], v[3]);
-    const float f0 = __builtin_bit_cast(float, h01 << 16), f1 = __builtin_bit_cast(float, h01 & 0xffff0000u);
-    const float f2 = __builtin_bit_cast(float, h23 << 16), f3 = __builtin_bit_cast(float, h23 & 0xffff0000u);
-    *(u32x2*)(hi + off) = u32x2{h01, h23};
-    *(u32x2*)(lo + off) = u32x2{cvt_pk_bf16(v[0] - f0, v[1] - f1), cvt_pk_bf16(v[2] - f2, v[3] - f3)};
-  };
-  __bf16 *ah = lds, *al = lds + T_TILE, *bh = lds + 2 * T_TILE, *bl = lds + 3 * T_TILE;
+  __bf16* pa_[NP];
+  __bf16* pb_[NP];
+#pragma unroll
+  for (int q = 0; q < NP; ++q) {
+    pa_[q] = lds + q * T_TILE;
+    pb_[q] = lds + (NP + q) * T_TILE;
+  }
 #pragma unroll
   for (int u = 0; u < NU; ++u) {
     const int c = u * 256 + tid;
     const int ka = AK ? (c % (T_KMAX / 4)) * 4 : c / (T_BM / 4);
     const int kb = BJ ? c / (T_BM / 4) : (c % (T_KMAX / 4)) * 4;
     if (ka < Kp)
-      split_store(ah, al, a_rk ? (c / (T_KMAX / 4)) * PA + (c % (T_KMAX / 4)) * 4
-                               : (c / (T_BM / 4)) * PA + (c % (T_BM / 4)) * 4, ra[u]);
+      split_store<NP>(pa_, a_rk ? (c / (T_KMAX / 4)) * PA + (c % (T_KMAX / 4)) * 4
+                                : (c / (T_BM / 4)) * PA + (c % (T_BM / 4)) * 4, ra[u]);
     if (kb < Kp)
-      split_store(bh, bl, b_rk ? (c / (T_KMAX / 4)) * PB + (c % (T_KMAX / 4)) * 4
-                               : (c / (T_BM / 4)) * PB + (c % (T_BM / 4)) * 4, rb[u]);
+      split_store<NP>(pb_, b_rk ? (c / (T_KMAX / 4)) * PB + (c % (T_KMAX / 4)) * 4
+                                : (c / (T_BM / 4)) * PB + (c % (T_BM / 4)) * 4, rb[u]);
   }
   __syncthreads();
   // 32 rows x 8 k fragment (row r0 + l32, k k0 + 8 h32 ..) of an LDS tile
@@ -586,12 +635,13 @@ __device__ __forceinline__ void sgemm3s_body(const SGemm& g, int t, __bf16* lds)
   };
   f32x16 acc = {};
   for (int ks = 0; ks < Kp; ks += 16) {
-    const bf16x8 fah = frag(ah, PA, a_rk, wi, ks), fal = frag(al, PA, a_rk, wi, ks);
-    const bf16x8 fbh = frag(bh, PB, b_rk, wj, ks), fbl = frag(bl, PB, b_rk, wj, ks);
-    // transposed tile: MFMA rows are output columns (B), MFMA columns output rows (A)
-    acc = mfma32(fbh, fah, acc);
-    acc = mfma32(fbh, fal, acc);
-    acc = mfma32(fbl, fah, acc);
+    bf16x8 fa[NP], fb[NP];
+#pragma unroll
+    for (int q = 0; q < NP; ++q) {
+      fa[q] = frag(pa_[q], PA, a_rk, wi, ks);
+      fb[q] = frag(pb_[q], PB, b_rk, wj, ks);
+    }
+    acc = split_mfma<TERMS>(fb, fa, acc);
   }
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
@@ -609,20 +659,22 @@ __device__ __forceinline__ void sgemm3s_body(const SGemm& g, int t, __bf16* lds)
   }
 }
 
-template <bool AK0, bool BJ0, bool AK1, bool BJ1>
-__global__ __launch_bounds__(256, 2) void sgemm3s_kernel(SGemm d0, SGemm d1) {
-  __shared__ __attribute__((aligned(16))) __bf16 lds[4 * T_TILE];
+// (six-term planes take 120 KB of LDS: one workgroup per CU; these launches are few
+// workgroups anyway)
+template <int TERMS, bool AK0, bool BJ0, bool AK1, bool BJ1>
+__global__ __launch_bounds__(256, TERMS == 6 ? 1 : 2) void sgemm3s_kernel(SGemm d0, SGemm d1) {
+  __shared__ __attribute__((aligned(16))) __bf16 lds[2 * Split<TERMS>::P * T_TILE];
   const int total = d0.ntiles + d1.ntiles;
   const int t = xcd_item((total + kXcds - 1) / kXcds);
   if (t >= total) return;
   if (t < d0.ntiles) {
     int u = t;
     const SGemm g = batch_item(d0, u);
-    sgemm3s_body<AK0, BJ0>(g, u, lds);
+    sgemm3s_body<TERMS, AK0, BJ0>(g, u, lds);
   } else {
     int u = t - d0.ntiles;
     const SGemm g = batch_item(d1, u);
-    sgemm3s_body<AK1, BJ1>(g, u, lds);
+    sgemm3s_body<TERMS, AK1, BJ1>(g, u, lds);
   }
 }
 
@@ -1189,6 +1241,7 @@ SGemm to_sgemm(const GemmDesc<float>& g, bool& ak, bool& bj, int tile) {
 // fp32 products on three bf16 MFMA terms, up to two problems per launch. The
 // operand layouts the solve uses: A contiguous along k with B along k or j, or A
 // contiguous along i with B along j.
+template <int TERMS>
 hipError_t run_group_split(const GemmDesc<float>* ds, int n, hipStream_t st) {
   SGemm s[2] = {};
   bool ak[2] = {true, true}, bj[2] = {true, true};
@@ -1219,9 +1272,9 @@ hipError_t run_group_split(const GemmDesc<float>* ds, int n, hipStream_t st) {
 #define PKV_SG(A0, B0, A1, B1)                                                                  \
   do {                                                                                          \
     if (small)                                                                                  \
-      hipLaunchKernelGGL((sgemm3s_kernel<A0, B0, A1, B1>), grid, block, 0, st, s[0], s[1]);     \
+      hipLaunchKernelGGL((sgemm3s_kernel<TERMS, A0, B0, A1, B1>), grid, block, 0, st, s[0], s[1]); \
     else                                                                                        \
-      hipLaunchKernelGGL((sgemm3_kernel<A0, B0, A1, B1>), grid, block, 0, st, s[0], s[1]);      \
+      hipLaunchKernelGGL((sgemm3_kernel<TERMS, A0, B0, A1, B1>), grid, block, 0, st, s[0], s[1]);  \
   } while (0)
   switch (key) {
     case 0b1011: PKV_SG(true, false, true, true); break;
@@ -1270,7 +1323,7 @@ SolveLayout layout(int64_t d, int64_t dout) {
 
 template <class T>
 hipError_t solve_t(const T* G, const T* C, int64_t d64, int64_t dout64, double lambda,
-                   int ridge, bool exact, float* dW, int32_t* info, void* ws, hipStream_t st) {
+                   int ridge, int products, float* dW, int32_t* info, void* ws, hipStream_t st) {
   constexpr int NB = Blk<T>::NB;
   const SolveLayout L = layout<T>(d64, dout64);
   char* w = (char*)ws;
@@ -1302,7 +1355,8 @@ hipError_t solve_t(const T* G, const T* C, int64_t d64, int64_t dout64, double l
   const T one = T(1), zero = T(0), mone = T(-1);
   auto run = [&](const GemmDesc<T>* g, int n) -> hipError_t {
     if constexpr (sizeof(T) == 4)
-      if (!exact) return run_group_split(g, n, st);
+      if (products == kProductsSplit6) return run_group_split<6>(g, n, st);
+      else if (products == kProductsSplit3) return run_group_split<3>(g, n, st);
     return run_group(g, n, st);
   };
   // Column blocks of NB are grouped into outer blocks of OB = NBO * NB. Within an
@@ -1767,9 +1821,9 @@ hipError_t launch_low_rank(const float* G, const float* dW, int64_t din, int64_t
   // S = dW^T (G dW): the two large products on the split-bf16 path
   {
     GemmDesc<float> g = desc<float>(G, din, 1, dW, dout, 1, X, dout, din_i, dout_i, din_i, 1.f, 0.f);
-    PKV_TRY(run_group_split(&g, 1, st));
+    PKV_TRY(run_group_split<6>(&g, 1, st));
     g = desc<float>(dW, 1, dout, X, dout, 1, S, dout, dout_i, dout_i, din_i, 1.f, 0.f);
-    PKV_TRY(run_group_split(&g, 1, st));
+    PKV_TRY(run_group_split<6>(&g, 1, st));
   }
   hipLaunchKernelGGL(diag_shift_kernel, dim3(1), dim3(256), 0, st, S, dout, dout,
                      (float)(1e-5 * (double)dout));
@@ -1838,12 +1892,12 @@ size_t solve_ws_bytes(bool f64, int64_t din, int64_t dout) {
 }
 
 hipError_t launch_solve(bool f64, const void* G, const void* C, int64_t din, int64_t dout,
-                        double lambda, int ridge, bool exact_f32, float* dW, int32_t* info,
+                        double lambda, int ridge, int products, float* dW, int32_t* info,
                         void* ws, hipStream_t st) {
   if (f64)
-    return solve_t<double>((const double*)G, (const double*)C, din, dout, lambda, ridge, true, dW,
-                           info, ws, st);
-  return solve_t<float>((const float*)G, (const float*)C, din, dout, lambda, ridge, exact_f32, dW,
+    return solve_t<double>((const double*)G, (const double*)C, din, dout, lambda, ridge,
+                           kProductsExact, dW, info, ws, st);
+  return solve_t<float>((const float*)G, (const float*)C, din, dout, lambda, ridge, products, dW,
                         info, ws, st);
 }
 

@@ -154,12 +154,14 @@ def test_solve_validation(L):
     assert f(B.F32, FAKE, FAKE, 16, 16, -1.0, 0, FAKE, FAKE, FAKE, nb, None) == B.E_VALUE
     assert f(B.F32, FAKE, FAKE, 16, 16, 0.1, 4, FAKE, FAKE, FAKE, nb, None) == B.E_VALUE
     assert f(B.F32, FAKE, FAKE, 16, 16, 0.1, 4 | B.SOLVE_EXACT_F32, FAKE, FAKE, FAKE, nb, None) == B.E_VALUE
-    assert f(B.F32, FAKE, FAKE, 16, 16, 0.1, 32, FAKE, FAKE, FAKE, nb, None) == B.E_VALUE
+    both = B.SOLVE_EXACT_F32 | B.SOLVE_FAST_BF16                # one product mode at most
+    assert f(B.F32, FAKE, FAKE, 16, 16, 0.1, both, FAKE, FAKE, FAKE, nb, None) == B.E_VALUE
+    assert f(B.F32, FAKE, FAKE, 16, 16, 0.1, 64, FAKE, FAKE, FAKE, nb, None) == B.E_VALUE  # unknown bit
     assert f(B.F32, FAKE, FAKE, 16, 16, 0.1, 3, FAKE, FAKE, FAKE, nb, None) == B.E_VALUE
     # the three ridge scalings, with and without exact products, pass the mode check
     # (and stop at the missing workspace, before any launch)
     for mode in (B.RIDGE_ABSOLUTE, B.RIDGE_ADAPTIVE, B.RIDGE_TRACE_MEAN):
-        for ex in (0, B.SOLVE_EXACT_F32):
+        for ex in (0, B.SOLVE_EXACT_F32, B.SOLVE_FAST_BF16):
             assert f(B.F32, FAKE, FAKE, 16, 16, 0.1, mode | ex, FAKE, FAKE, None, nb, None) == B.E_WORKSPACE
     assert f(B.F32, FAKE, FAKE, 16, 16, 0.1, 0, FAKE, FAKE, None, nb, None) == B.E_WORKSPACE
     assert f(B.F32, FAKE, FAKE, 16, 16, 0.1, 0, FAKE, FAKE, FAKE, nb - 1, None) == B.E_WORKSPACE

@@ -5,14 +5,16 @@ Tolerances (relative Frobenius error):
   error ~2^-17 relative) with fp32 accumulation: targets and statistics within
   5e-5.
 * fp64 accumulation path: fp64 products of fp32 inputs: 1e-12.
-* solve, fp32 with exact fp32 products (PATCHKV_SOLVE_EXACT_F32): Cholesky +
-  triangular solves in fp32 on systems with condition number kappa <= ~1e2:
-  error ~ kappa * 2^-24 * (growth), bound 1e-4.
-* solve, fp32 default (products on three bf16 MFMA terms): each product carries
-  about 3 * 2^-18 relative error (hi/lo representation of both operands and the
-  dropped lo*lo term), so the first-order forward error is kappa * 3 * 2^-18 times
-  a modest growth factor; bound kappa * 2^-14 (a factor ~5 of slack), computed
-  from the system's own kappa.
+* solve, fp32 with FP32-grade products (the default: three bf16 pieces per operand,
+  six MFMA products, about 2^-24 relative per product) or exact fp32 products
+  (PATCHKV_SOLVE_EXACT_F32): Cholesky + triangular solves in fp32 on systems with
+  condition number kappa <= ~1e2: error ~ kappa * 2^-24 * (growth), bound 1e-4; on
+  ill-conditioned systems (kappa 1e4 - 1e5) bound kappa * 2^-20.
+* solve, fp32 with PATCHKV_SOLVE_FAST_BF16 (two bf16 pieces, three products): each
+  product carries about 3 * 2^-18 relative error (hi/lo representation of both
+  operands and the dropped lo*lo term), so the first-order forward error is
+  kappa * 3 * 2^-18 times a modest growth factor; bound kappa * 2^-14 (a factor ~5 of
+  slack), computed from the system's own kappa.
 * solve, fp64: the solve is fp64 but dW is returned in fp32, whose rounding alone
   is ~3e-8 RMS; bound 1e-7.
 """
@@ -102,10 +104,14 @@ def _spd_system(d, dout, rows, seed, scale=0.3):
     return oracle.normal_equations(X, T)
 
 
-def _solve_tol(acc, exact, G, lam):
+def _mode(products):
+    return {"split6": 0, "exact": pkv.SOLVE_EXACT_F32, "split3": pkv.SOLVE_FAST_BF16}[products]
+
+
+def _solve_tol(acc, products, G, lam):
     if acc == "f64":
         return 1e-7
-    if exact:
+    if products in ("split6", "exact"):
         return 1e-4
     ev = np.linalg.eigvalsh(G + lam * np.eye(G.shape[0]))
     return float(ev[-1] / ev[0]) * 2.0 ** -14
@@ -127,41 +133,69 @@ SOLVE_CASES = [
 ]
 
 
-@pytest.mark.parametrize("exact", [False, True], ids=["split", "exact"])
+@pytest.mark.parametrize("products", ["split6", "exact", "split3"])
 @pytest.mark.parametrize("d,dout,rows,acc,lam", SOLVE_CASES)
-def test_solve(d, dout, rows, acc, lam, exact):
-    if acc == "f64" and exact:
+def test_solve(d, dout, rows, acc, lam, products):
+    if acc == "f64" and products != "split6":
         pytest.skip("the fp64 solve has a single arithmetic")
     G, C = _spd_system(d, dout, rows, d + dout)
     tdt = torch.float64 if acc == "f64" else torch.float32
-    mode = pkv.RIDGE_ABSOLUTE | (pkv.SOLVE_EXACT_F32 if exact else 0)
+    mode = pkv.RIDGE_ABSOLUTE | _mode(products)
     dW, info = pkv.solve_patch(dev(G).to(tdt), dev(C).to(tdt), lam, mode=mode)
     assert int(info.item()) == 0
     Gin = G if acc == "f64" else G.astype(np.float32).astype(np.float64)
     Cin = C if acc == "f64" else C.astype(np.float32).astype(np.float64)
     ref = oracle.solve_patch(Gin, Cin, lam)
-    err, tol = rel(host(dW), ref), _solve_tol(acc, exact, Gin, lam)
-    print(f"solve d={d} dout={dout} {acc} exact={exact}: err {err:.3e} tol {tol:.3e}", flush=True)
+    err, tol = rel(host(dW), ref), _solve_tol(acc, products, Gin, lam)
+    print(f"solve d={d} dout={dout} {acc} {products}: err {err:.3e} tol {tol:.3e}", flush=True)
     assert err <= tol
 
 
 @pytest.mark.parametrize("ridge", ["adaptive", "trace_mean"])
-@pytest.mark.parametrize("exact", [False, True], ids=["split", "exact"])
+@pytest.mark.parametrize("products", ["split6", "exact", "split3"])
 @pytest.mark.parametrize("acc", ["f32", "f64"])
-def test_solve_adaptive_ridge(acc, exact, ridge):
-    if acc == "f64" and exact:
+def test_solve_adaptive_ridge(acc, products, ridge):
+    if acc == "f64" and products != "split6":
         pytest.skip("the fp64 solve has a single arithmetic")
     G, C = _spd_system(200, 150, 300, 3)
     tdt = torch.float64 if acc == "f64" else torch.float32
     base = pkv.RIDGE_ADAPTIVE if ridge == "adaptive" else pkv.RIDGE_TRACE_MEAN
-    mode = base | (pkv.SOLVE_EXACT_F32 if exact else 0)
+    mode = base | _mode(products)
     dW, info = pkv.solve_patch(dev(G).to(tdt), dev(C).to(tdt), 0.01, mode=mode)
     assert int(info.item()) == 0
     Gin = G if acc == "f64" else G.astype(np.float32).astype(np.float64)
     Cin = C if acc == "f64" else C.astype(np.float32).astype(np.float64)
     lam = oracle.ridge_lambda(Gin, 0.01, ridge)
     err = rel(host(dW), oracle.solve_patch(Gin, Cin, lam))
-    assert err <= _solve_tol(acc, exact, Gin, lam)
+    assert err <= _solve_tol(acc, products, Gin, lam)
+
+
+@pytest.mark.parametrize("d,dout,kappa", [(512, 256, 1e4), (1000, 300, 1e5), (1536, 200, 3e4)])
+def test_solve_fp32_grade_on_ill_conditioned_systems(d, dout, kappa):
+    """G + lambda I with eigenvalues log-spaced from 1 down to 1/kappa: the default
+    (six-term) products and exact fp32 products both stay within kappa * 2^-20 of the
+    fp64 solution, and the six-term error is within a small factor of the exact one
+    (FP32 grade), where the three-term products lose about 2^8 more."""
+    rng = np.random.default_rng(d + int(kappa))
+    U, _ = np.linalg.qr(rng.standard_normal((d, d)))
+    ev = np.logspace(0.0, -np.log10(kappa), d)
+    lam = 0.5 * ev[-1]
+    G = ((U * (ev - lam)) @ U.T).astype(np.float32)
+    G = (0.5 * (G + G.T)).astype(np.float32)
+    C = rng.standard_normal((d, dout)).astype(np.float32)
+    Gin, Cin = G.astype(np.float64), C.astype(np.float64)
+    e = np.linalg.eigvalsh(Gin + lam * np.eye(d))
+    kap = float(e[-1] / e[0])
+    ref = oracle.solve_patch(Gin, Cin, lam)
+    errs = {}
+    for products in ("split6", "exact", "split3"):
+        dW, info = pkv.solve_patch(dev(G), dev(C), lam, mode=pkv.RIDGE_ABSOLUTE | _mode(products))
+        assert int(info.item()) == 0
+        errs[products] = rel(host(dW), ref)
+    print(f"ill-conditioned d={d} kappa={kap:.2e}: " +
+          "  ".join(f"{k} {v:.3e}" for k, v in errs.items()), flush=True)
+    assert errs["split6"] <= kap * 2.0 ** -20 and errs["exact"] <= kap * 2.0 ** -20
+    assert errs["split6"] <= 4.0 * errs["exact"] + 1e-6
 
 
 @pytest.mark.parametrize("acc", ["f32", "f64"])
