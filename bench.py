@@ -38,28 +38,34 @@ METRIC = "sec per layer patch + ref-query attention TFLOP/s (% of MFMA peak), 1 
 PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 MFMA
 PEAK_F32_TFLOPS = 157.3     # MI355X fp32 MFMA
 PEAK_HBM_GBS = 8000.0
-TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "attn_bf16_kernel_hbm_traffic__llama3-8b-32layer-172k.md")
+
+
+def traffic_profile(cfg) -> str:
+    return os.path.join(ROOT, "profiles", f"hbm_traffic__{cfg.name}.md")
 
 
 def measured_traffic(cfg):
-    """HBM bytes per full-cache attention launch from the committed counter summary
-    (FETCH_SIZE and WRITE_SIZE, calibrated on a plain copy), or None when the
-    workload differs or the kernel source changed since the counters were taken."""
+    """HBM bytes per full-cache attention launch (V^T pre-pass, fast path and fixup)
+    from the committed counter summary of this workload (FETCH_SIZE and WRITE_SIZE,
+    calibrated on a plain copy; written by traffic_summary.py), or None when there is
+    none or a kernel source changed since the counters were taken."""
     import hashlib
-    if cfg.cid != 3 or not os.path.exists(TRAFFIC_PROFILE):
+    path = traffic_profile(cfg)
+    if not os.path.exists(path):
         return None
-    want, nbytes = None, None
-    for line in open(TRAFFIC_PROFILE):
+    hashes, nbytes = [], None
+    for line in open(path):
         t = line.split()
         if len(t) == 3 and t[0] == "source_sha256":
-            want = (t[1], t[2])
-        elif len(t) == 2 and t[0] == "traffic_bytes_per_launch":
-            nbytes = float(t[1])
-    if want is None or nbytes is None:
+            hashes.append((t[1], t[2]))
+        elif len(t) == 3 and t[0] == "traffic_bytes_per_launch" and t[1] == "attend_full":
+            nbytes = float(t[2])
+    if not hashes or nbytes is None:
         return None
-    with open(os.path.join(ROOT, want[0]), "rb") as f:
-        if hashlib.sha256(f.read()).hexdigest() != want[1]:
-            return None
+    for src, h in hashes:
+        with open(os.path.join(ROOT, src), "rb") as f:
+            if hashlib.sha256(f.read()).hexdigest() != h:
+                return None
     return nbytes
 
 
@@ -378,6 +384,7 @@ def main():
             launches * (att_flops_full + att_flops_comp) / s_layer / 1e12,
         "context_tokens_per_s": cfg.N / s_layer,
         "kv_stream_gbs_full_attention": kv_bytes / t_attn / 1e9,
+        "kv_stream_frac_of_hbm_peak": kv_bytes / t_attn / 1e9 / PEAK_HBM_GBS,
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                      "frac": achieved / peak, "traffic": traffic,
                      "kernel": (("patchkv_attend_chunk" if chunked else "patchkv_attend_full")
@@ -385,7 +392,9 @@ def main():
                                    if cfg.dtype == "bf16" else ": attn_f32_kernel")),
                      "flops_per_launch": att_flops_full,
                      "traffic_unit": "HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
-                     "traffic_source": os.path.relpath(TRAFFIC_PROFILE, ROOT) if traffic else None},
+                     "traffic_source": os.path.relpath(traffic_profile(cfg), ROOT) if traffic else None,
+                     "hbm_gbs": traffic / t_attn / 1e9 if traffic else None,
+                     "hbm_frac": traffic / t_attn / 1e9 / PEAK_HBM_GBS if traffic else None},
         "solve_info_nonzero_layers": bad,
     }
     if not args.no_cpu_baseline:
