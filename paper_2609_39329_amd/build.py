@@ -19,7 +19,7 @@ LIB_DIR = os.path.join(HERE, "lib")
 LIB = os.path.join(LIB_DIR, "libpatchkv.so")
 ARCH = "gfx950"
 
-SOURCES = ["attention.hip", "stats.hip", "solve.hip", "capi.cpp"]
+SOURCES = ["attention.hip", "attention_mx.hip", "stats.hip", "solve.hip", "capi.cpp"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function"]
 DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
@@ -27,7 +27,7 @@ DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-p
 HOST = ["-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include"]
 # Per-source extras. The attention kernels never see NaNs (masked scores are -inf),
 # so they run with the IEEE mode bit off, which lets max() skip NaN quieting.
-EXTRA = {"attention.hip": ["-mno-amdgpu-ieee", "-fno-honor-nans"]}
+EXTRA = {s: ["-mno-amdgpu-ieee", "-fno-honor-nans"] for s in ("attention.hip", "attention_mx.hip")}
 
 
 def hipcc() -> str:

@@ -15,14 +15,14 @@ import sys
 
 sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
 from paper_2609_39329_amd.build import (ARCH, COMMON, CSRC, HOST, LIB_DIR, OBJ,  # noqa: E402
-                                        hipcc, host_cxx)
+                                        SOURCES, hipcc, host_cxx)
 
 ASAN_LIB = os.path.join(LIB_DIR, "libpatchkv_asan.so")
 SAN = ["-fsanitize=address", "-fno-omit-frame-pointer"]
 
 
 def build_asan(verbose: bool = False) -> str:
-    objs = [os.path.join(OBJ, f) for f in ("attention.o", "stats.o", "solve.o")]
+    objs = [os.path.join(OBJ, os.path.splitext(f)[0] + ".o") for f in SOURCES if f.endswith(".hip")]
     if not all(os.path.exists(o) for o in objs):
         raise RuntimeError("build the library first (paper_2609_39329_amd/build.py)")
     capi = os.path.join(OBJ, "capi_asan.o")

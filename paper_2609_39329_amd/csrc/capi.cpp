@@ -264,9 +264,10 @@ namespace {
 bool valid_kv_format(int f) {
   return f == PATCHKV_KV_PLAIN || f == PATCHKV_KV_MXINT8 || f == PATCHKV_KV_MXINT4;
 }
-// dequantized cache rows (quantized formats), carved after the attention workspace
+// dequantized cache rows (quantized formats, f32 path), carved after the attention
+// workspace; the bf16 kernels expand block-scaled entries themselves
 size_t dequant_bytes(int dtype, int kv_format, int64_t n_cache, int Hkv, int dh) {
-  if (kv_format == PATCHKV_KV_PLAIN) return 0;
+  if (kv_format == PATCHKV_KV_PLAIN || dtype == PATCHKV_BF16) return 0;
   const size_t e = dtype == PATCHKV_BF16 ? 2 : 4;
   return 2 * ((size_t)Hkv * n_cache * dh * e + 255) / 256 * 256;
 }
@@ -310,8 +311,16 @@ int patchkv_attend_cache(int dtype, const void* Q, const void* K, const void* V,
   if (!quant)
     return status_of(launch_attention(sh, Q, K, V, ci, n_src, n_src, scale, p_terms == 2, O,
                                       workspace, st, nullptr, nullptr, bias));
-  // expand the quantized entries (gathered through idx) into dtype rows, then attend
   const int bits = kv_format == PATCHKV_KV_MXINT8 ? 8 : 4;
+  if (dtype == PATCHKV_BF16) {  // the kernels read the block-scaled entries themselves
+    KvQuant kq;
+    kq.bits = bits;
+    kq.Ke = Ke;
+    kq.Ve = Ve;
+    return status_of(launch_attention(sh, Q, K, V, ci, n_src, n_src, scale, p_terms == 2, O,
+                                      workspace, st, nullptr, nullptr, bias, kq));
+  }
+  // f32: expand the quantized entries (gathered through idx) into f32 rows, then attend
   const size_t half = dequant_bytes(dtype, kv_format, n_cache, Hkv, dh) / 2;
   char* kx = (char*)workspace + a;
   char* vx = kx + half;

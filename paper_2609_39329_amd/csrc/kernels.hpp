@@ -38,16 +38,29 @@ struct CacheIndex {
   const int32_t* counts = nullptr;
 };
 
+// Block-scaled integer storage of a cache's K and V (bf16 path): bits 8 (int8 values)
+// or 4 (int4, two per byte, even channel in the low nibble), Ke / Ve one int8 exponent
+// per 32 channels ([Hkv][src_rows][dh / 32]); an entry's value is q * 2^e. bits 0: K
+// and V are plain bf16 / f32 rows.
+struct KvQuant {
+  int bits = 0;
+  const int8_t* Ke = nullptr;
+  const int8_t* Ve = nullptr;
+};
+
 // Q [M][Hq][dh]; K, V rows of KV head g start at (g * src_rows) * dh; the cache's
 // entries are selected by ci.
 // psplit: form P V from a two-term bf16 split of P (bf16 path only).
 // s.Ms > 0: Ks, Vs [Hkv][Ms][dh] are the chunk's own entries (causal, after the cache).
+// bias [Hkv][Nk]: per-entry logit bias (natural-log units), added to entry n's logit.
+// kq.bits != 0 (bf16, no own entries): K, V are block-scaled integers, expanded to
+// bf16 inside the kernels (keys at the LDS store of each tile, values by the V^T
+// pre-pass).
 hipError_t launch_attention(const AttnShape& s, const void* Q, const void* K, const void* V,
                             const CacheIndex& ci, int64_t src_rows, int64_t src_valid,
                             float scale, bool psplit, float* O, void* ws, hipStream_t st,
                             const void* Ks = nullptr, const void* Vs = nullptr,
-                            const float* bias = nullptr);
-// bias [Hkv][Nk]: per-entry logit bias (natural-log units), added to entry n's logit.
+                            const float* bias = nullptr, const KvQuant& kq = KvQuant{});
 // Block-scaled integer cache rows -> [Hkv][n_cache][dh] bf16 (bf16) or f32: value
 // q * 2^e, q int8 (bits 8) or int4 packed two per byte (bits 4, even channel in the
 // low nibble), e int8 per 32 channels; entry n of head g is row idx[g * stride + n]

@@ -234,7 +234,10 @@ def test_attend_cache_validation(L):
     assert cache() == B.E_WORKSPACE
     plain = L.patchkv_attend_cache_workspace_bytes(B.BF16, B.KV_PLAIN, 8, 64, 4, 2, 128)
     q8 = L.patchkv_attend_cache_workspace_bytes(B.BF16, B.KV_MXINT8, 8, 64, 4, 2, 128)
-    assert q8 - plain >= 2 * 2 * 64 * 128 * 2             # expanded K and V rows
+    assert q8 == plain        # bf16: the kernels read the block-scaled entries themselves
+    pf = L.patchkv_attend_cache_workspace_bytes(B.F32, B.KV_PLAIN, 8, 64, 4, 2, 128)
+    qf = L.patchkv_attend_cache_workspace_bytes(B.F32, B.KV_MXINT8, 8, 64, 4, 2, 128)
+    assert qf - pf >= 2 * 2 * 64 * 128 * 4                # f32: expanded K and V rows
     assert L.patchkv_attend_cache_workspace_bytes(B.BF16, 7, 8, 64, 4, 2, 128) == 0
 
 

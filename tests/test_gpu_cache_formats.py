@@ -4,7 +4,10 @@ entries (quantized KV caches), against the fp64 oracle.
 
 Block-scaled entries are exact in bf16, so the tolerances are those of the plain
 passes: bf16 with P rounded to bf16 (p_terms 1) 4e-3, with a two-term P (p_terms
-2) 5e-5; fp32 inputs 2e-5.
+2) 5e-5; fp32 inputs 2e-5. The bf16 kernels read block-scaled entries themselves
+(keys expanded when a tile is stored to LDS, values by the V^T pre-pass); since the
+expansion is exact, their output must equal, bit for bit, that of the same kernel
+variant over the expanded bf16 rows.
 """
 import numpy as np
 import pytest
@@ -98,3 +101,95 @@ def test_bias_of_log_k_equals_k_copies_on_gpu():
     idx3 = np.concatenate([np.arange(60), [7, 7]]).astype(np.int32)
     O3 = host(pkv.attend_cache(q, k, v, idx=idx_dev(idx3)))
     assert rel(O1, O3) <= 5e-5
+
+
+def _expanded(qc, bits):
+    """The block-scaled cache's exact values as bf16 device tensors."""
+    K = oracle.dequantize_mx(qc.Kq if bits == 8 else _unpack(qc.Kq), qc.Ke)
+    V = oracle.dequantize_mx(qc.Vq if bits == 8 else _unpack(qc.Vq), qc.Ve)
+    k = torch.from_numpy(K.astype(np.float32)).to(torch.bfloat16)
+    v = torch.from_numpy(V.astype(np.float32)).to(torch.bfloat16)
+    assert np.array_equal(k.double().numpy(), K) and np.array_equal(v.double().numpy(), V)
+    return K, V, k.to(DEV), v.to(DEV)
+
+
+@pytest.mark.parametrize("bits", [8, 4])
+@pytest.mark.parametrize("M,N,B,Hq,Hkv,dh", [
+    (96, 1200, 200, 8, 2, 128),
+    (40, 3000, 700, 8, 8, 64),      # head_dim 64, few rows: split key ranges + merge
+    (300, 2049, 260, 28, 4, 128),   # GQA group of 7, ragged tiles
+])
+def test_block_scaled_in_kernel_equals_expanded_rows(bits, M, N, B, Hq, Hkv, dh):
+    print(f"MXINT{bits} in-kernel vs expanded M={M} N={N} B={B} dh={dh}", flush=True)
+    inp = make_custom_inputs(M=M, N=N, B=B, Hq=Hq, Hkv=Hkv, dh=dh, dtype="bf16", seed=bits + dh)
+    qc = make_quant_cache(inp.K, inp.V, bits, "bf16")
+    K, V, kx, vx = _expanded(qc, bits)
+    fmt = pkv.KV_MXINT8 if bits == 8 else pkv.KV_MXINT4
+    q = to_dev(inp.Q, "bf16")
+    kq, vq, ke, ve = (torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+                      for a in (qc.Kq, qc.Vq, qc.Ke, qc.Ve))
+    idx = idx_dev(inp.idx)
+    b = torch.from_numpy(make_cache_bias(inp)).to(DEV)
+
+    def both(**kw):
+        Oq = pkv.attend_cache(q, kq, vq, kv_format=fmt, Ke=ke, Ve=ve, **kw)
+        Ox = pkv.attend_cache(q, kx, vx, **kw)
+        return Oq, Ox
+
+    # same kernel variant on both sides: bitwise
+    for kw in (dict(idx=idx, p_terms=1), dict(idx=idx, p_terms=2), dict(n_cache=B, p_terms=2),
+               dict(idx=idx, bias=b, p_terms=2)):
+        Oq, Ox = both(**kw)
+        torch.cuda.synchronize()
+        assert torch.equal(Oq, Ox), {k: v for k, v in kw.items() if k == "p_terms"}
+    # the whole cache, P rounded to bf16: the expanded rows take the direct-to-LDS kernel
+    Oq, Ox = both(p_terms=1)
+    assert rel(host(Oq), host(Ox)) <= 1e-6
+    assert rel(host(Oq), oracle.attention(oracle.decode(inp.Q, "bf16"), K, V, inp.scale)) <= 4e-3
+
+
+@pytest.mark.parametrize("bits", [8, 4])
+def test_block_scaled_full_context_parity(bits):
+    """Quantization as the compression: the student cache is the whole context in
+    block-scaled form (no eviction), attended with a two-term P against the oracle."""
+    M, N, Hq, Hkv, dh = 200, 9000, 16, 4, 128
+    print(f"MXINT{bits} full-context parity N={N}", flush=True)
+    inp = make_custom_inputs(M=M, N=N, B=N, Hq=Hq, Hkv=Hkv, dh=dh, dtype="bf16", seed=40 + bits,
+                             cache="identity")
+    qc = make_quant_cache(inp.K, inp.V, bits, "bf16")
+    K, V, _, _ = _expanded(qc, bits)
+    fmt = pkv.KV_MXINT8 if bits == 8 else pkv.KV_MXINT4
+    kq, vq, ke, ve = (torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+                      for a in (qc.Kq, qc.Vq, qc.Ke, qc.Ve))
+    O = host(pkv.attend_cache(to_dev(inp.Q, "bf16"), kq, vq, kv_format=fmt, Ke=ke, Ve=ve,
+                              p_terms=2))
+    e = rel(O, oracle.attention(oracle.decode(inp.Q, "bf16"), K, V, inp.scale))
+    print(f"  {e:.3e}", flush=True)
+    assert e <= 5e-5
+
+
+@pytest.mark.parametrize("bits", [8, 4])
+def test_block_scaled_per_head_sets_and_bad_entries(bits):
+    """Per-KV-head index sets with counts, one entry outside the cache: the in-kernel
+    expansion reads it as a zero row and reports it, like the plain path."""
+    M, N, B, Hq, Hkv, dh = 64, 1500, 300, 8, 4, 128
+    inp = make_custom_inputs(M=M, N=N, B=B, Hq=Hq, Hkv=Hkv, dh=dh, dtype="bf16", seed=7 * bits,
+                             cache="evict_heads")
+    qc = make_quant_cache(inp.K, inp.V, bits, "bf16")
+    _, _, kx, vx = _expanded(qc, bits)
+    fmt = pkv.KV_MXINT8 if bits == 8 else pkv.KV_MXINT4
+    kq, vq, ke, ve = (torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+                      for a in (qc.Kq, qc.Vq, qc.Ke, qc.Ve))
+    idx = np.array(inp.idx, dtype=np.int32)
+    assert inp.counts[1] > 5
+    idx[1, 5] = N + 3  # outside the cache: flat position 1 * B + 5
+    q, it, ct = to_dev(inp.Q, "bf16"), idx_dev(idx), idx_dev(inp.counts)
+    iq = torch.zeros(1, dtype=torch.int32, device=DEV)
+    ix = torch.zeros(1, dtype=torch.int32, device=DEV)
+    for pt in (1, 2):
+        Oq = pkv.attend_cache(q, kq, vq, kv_format=fmt, Ke=ke, Ve=ve, idx=it, counts=ct,
+                              p_terms=pt, info=iq)
+        Ox = pkv.attend_cache(q, kx, vx, idx=it, counts=ct, p_terms=pt, info=ix)
+        torch.cuda.synchronize()
+        assert torch.equal(Oq, Ox)
+        assert int(iq.item()) == int(ix.item()) == -(1 + 1 * idx.shape[1] + 5)
