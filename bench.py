@@ -149,7 +149,10 @@ def layer_steps(pkv, cfg, L, bufs, li: int, events=None):
     acc = pkv.F32 if bufs.acc == 1 else pkv.F64
     if events is not None:
         events[0].record()
-    pkv.attend_full(L.Q, L.K, L.V, scale=cfg.scale, O=bufs.Of)
+    if cfg.teacher_p_terms == 2:  # the full cache with a two-term P
+        pkv.attend_cache(L.Q, L.K, L.V, scale=cfg.scale, p_terms=2, O=bufs.Of)
+    else:
+        pkv.attend_full(L.Q, L.K, L.V, scale=cfg.scale, O=bufs.Of)
     if events is not None:
         events[1].record()
     if L.Kq is not None:  # block-scaled compressed cache (the compressed entries themselves)
@@ -387,7 +390,10 @@ def main():
         "kv_stream_frac_of_hbm_peak": kv_bytes / t_attn / 1e9 / PEAK_HBM_GBS,
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                      "frac": achieved / peak, "traffic": traffic,
-                     "kernel": (("patchkv_attend_chunk" if chunked else "patchkv_attend_full")
+                     "kernel": (("patchkv_attend_chunk" if chunked else
+                                 "patchkv_attend_cache (full cache, two-term P: 1.5x the MFMA "
+                                 "work of the algorithmic flops counted here)"
+                                 if cfg.teacher_p_terms == 2 else "patchkv_attend_full")
                                 + (": vt_kernel + attn_bf16_kernel fast path + fixup"
                                    if cfg.dtype == "bf16" else ": attn_f32_kernel")),
                      "flops_per_launch": att_flops_full,

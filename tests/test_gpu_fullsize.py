@@ -36,7 +36,7 @@ from make_oracle_fixtures import fixture_path, sample_rows, sample_tokens, sketc
 pytestmark = pytest.mark.gpu
 
 CASES = [(1, 0), (2, 0), (4, 0), (3, 0), (3, 8), (3, 16), (3, 24), (3, 31), (5, 0), (6, 0), (7, 0),
-         (8, 0), (9, 0)]
+         (8, 0), (9, 0), (10, 0), (11, 0)]
 TOL = 2e-2
 
 

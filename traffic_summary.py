@@ -30,7 +30,8 @@ import sys
 from collections import defaultdict
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
-SOURCES = ["paper_2609_39329_amd/csrc/attention.hip", "paper_2609_39329_amd/csrc/stats.hip",
+SOURCES = ["paper_2609_39329_amd/csrc/attention_kernels.hpp",
+           "paper_2609_39329_amd/csrc/attention.hip", "paper_2609_39329_amd/csrc/stats.hip",
            "paper_2609_39329_amd/csrc/solve.hip"]
 PEAK_GBS = 8000.0
 LIB_KERNEL = re.compile(r"pkv::|^_ZN3pkv")
@@ -129,6 +130,8 @@ def main() -> None:
     ap.add_argument("--trace")
     ap.add_argument("--workload", required=True)
     ap.add_argument("--command", required=True, help="the bench command that was profiled")
+    ap.add_argument("--teacher-psplit", action="store_true",
+                    help="the workload's full-cache pass forms P V from a two-term P")
     a = ap.parse_args()
 
     sf, rf = calibration(a.copy_fetch, "FETCH_SIZE")
@@ -186,14 +189,23 @@ def main() -> None:
                 line += " – | – | – |"
         print(line)
 
-    full = [k for k in totals
-            if re.fullmatch(r"vt_kernel<\d+, false>", k)
-            or re.fullmatch(r"attn_bf16_kernel<\d+, false, false, false, (false|true), false, false>", k)]
-    calls = {len(fetch[k]) for k in fetch if LIB_KERNEL.search(k) and short(k) in full}
-    if len(full) >= 2 and len(calls) == 1:  # the full pass's kernels are its own (no shared name)
+    # the full-cache pass: the V^T pre-pass over the whole cache (the largest dispatch of
+    # the non-gathering vt_kernel), the teacher's fast path and its fixup (one dispatch
+    # each per layer: no other call uses these instantiations)
+    ps = "true" if a.teacher_psplit else "false"
+    pats = [r"vt_kernel<\d+, false, 0>",
+            rf"attn_bf16_kernel<\d+, false, {ps}, false, (false|true), false, false, 0>"]
+    def largest(k):
+        f = max(fetch.get(k, [0.0])) * 1024.0 * sf
+        w = max(write.get(k, [0.0])) * 1024.0 * sw
+        return f + w
+    full = [k for k in set(fetch) | set(write)
+            if LIB_KERNEL.search(k) and any(re.fullmatch(pt, short(k)) for pt in pats)]
+    if len(full) >= 2:
         print("\n## One full-cache attention launch (V^T pre-pass, fast path, fixup)\n")
-        print(f"    traffic_bytes_per_launch attend_full {sum(totals[k] for k in full):.0f}")
-
+        for k in sorted(full, key=short):
+            print(f"- `{short(k)}`: {largest(k) / 1e6:,.1f} MB")
+        print(f"\n    traffic_bytes_per_launch attend_full {sum(largest(k) for k in full):.0f}")
 
 if __name__ == "__main__":
     main()

@@ -17,6 +17,8 @@ Compressed-cache structure:
   * "synthesize": B synthetic entries, each a seeded-random convex combination of
                   n_mix full-cache entries, standing in for an approximation method
                   (Attention Matching) whose entries are not a subset.
+  * "identity":   every position (B = N); with kv_format "mxint8" / "mxint4" the
+                  compression is the quantization of the whole context (App. C).
 """
 from dataclasses import dataclass
 
@@ -35,7 +37,7 @@ class Config:
     lam: float        # absolute ridge coefficient
     dtype: str        # "f32" or "bf16" (Q, K, V and W)
     layers: int = 1
-    cache: str = "evict"     # "evict" | "evict_heads" | "synthesize"
+    cache: str = "evict"     # "evict" | "evict_heads" | "synthesize" | "identity"
     n_sink: int = 0
     n_recent: int = 0
     n_random: int = 0
@@ -46,6 +48,11 @@ class Config:
     rank: int = 0            # > 0: also the reduced-rank patch of this rank
     kv_format: str = "plain" # compressed cache storage: "plain", "mxint8" or "mxint4"
     cache_bias: bool = False # compressed cache entries carry a logit bias
+    # 2: the full-cache (teacher) pass also forms P V from a two-term bf16 split of P.
+    # Needed where O_f - O_c is small next to O_f (int8 quantization of the whole
+    # context changes O by ~2 %): P rounded to bf16 (~1.6e-3 relative error in O_f)
+    # would then be ~8 % of the targets.
+    teacher_p_terms: int = 1
 
     @property
     def group(self) -> int:
@@ -99,6 +106,13 @@ CONFIGS = (
     Config(9, "llama3-8b-32layer-172k-headwise", d=4096, Hq=32, Hkv=8, dh=128, N=172032,
            B=1720, M=4096, lam=1e-1, dtype="bf16", layers=32, cache="evict_heads", n_sink=4,
            n_recent=860, n_random=856),
+    # quantization as the compression: the student cache is the whole 172,032-token
+    # context in block-scaled int8 (int4), read by the attention kernels as stored
+    Config(10, "llama3-8b-layer-172k-context-mxint8", d=4096, Hq=32, Hkv=8, dh=128, N=172032,
+           B=172032, M=4096, lam=1e-1, dtype="bf16", cache="identity", kv_format="mxint8",
+           teacher_p_terms=2),
+    Config(11, "llama3-8b-layer-172k-context-mxint4", d=4096, Hq=32, Hkv=8, dh=128, N=172032,
+           B=172032, M=4096, lam=1e-1, dtype="bf16", cache="identity", kv_format="mxint4"),
 )
 
 

@@ -366,7 +366,9 @@ def make_cache_extras(cfg, inp: LayerInputs):
     qc = None
     if cfg.kv_format != "plain":
         bits = {"mxint8": 8, "mxint4": 4}[cfg.kv_format]
-        if inp.idx is not None:
+        if cfg.cache == "identity":  # the whole context
+            Kc, Vc = inp.K, inp.V
+        elif inp.idx is not None:
             Kc, Vc = inp.K[:, inp.idx], inp.V[:, inp.idx]
         else:
             Kc, Vc = inp.Kc, inp.Vc
@@ -401,6 +403,10 @@ def make_layer_inputs(cfg: Config, layer: int = 0, seed: int = 0) -> LayerInputs
     """Inputs of layer ``layer`` of one of the five workload configs."""
     if not 0 <= layer < cfg.layers:
         raise ValueError(f"config {cfg.cid} has {cfg.layers} layer(s)")
+    if cfg.cache == "identity":
+        return make_custom_inputs(M=cfg.M, N=cfg.N, B=cfg.N, Hq=cfg.Hq, Hkv=cfg.Hkv, dh=cfg.dh,
+                                  dtype=cfg.dtype, cache="identity", lam=cfg.lam, seed=seed,
+                                  cid=cfg.cid, layer=layer)
     if cfg.cache in ("evict", "evict_heads"):
         return make_custom_inputs(M=cfg.M, N=cfg.N, B=cfg.B, Hq=cfg.Hq, Hkv=cfg.Hkv,
                                   dh=cfg.dh, dtype=cfg.dtype, cache=cfg.cache, lam=cfg.lam,
