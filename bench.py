@@ -18,7 +18,7 @@ kernel (the full-cache attention, timed with HIP events on its stream inside the
 timed region) and the fp64 CPU oracle timed on a bounded sample of the same
 workload.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 3] [--layers L]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 3] [--layers L] [--dump-dw DIR]
 """
 from __future__ import annotations
 
@@ -47,7 +47,7 @@ def traffic_profile(cfg) -> str:
 def measured_traffic(cfg):
     """HBM bytes per full-cache attention launch (V^T pre-pass, fast path and fixup)
     from the committed counter summary of this workload (FETCH_SIZE and WRITE_SIZE,
-    calibrated on a plain copy; written by traffic_summary.py), or None when there is
+    calibrated on a plain copy; written by profile_summary.py), or None when there is
     none or a kernel source changed since the counters were taken."""
     import hashlib
     path = traffic_profile(cfg)
@@ -83,6 +83,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=256,
                     help="query rows of the oracle sample for the CPU baseline")
+    ap.add_argument("--dump-dw", metavar="DIR", default=None,
+                    help="after the timed steps, write every layer's patch dW (fp32 .npy) to DIR")
     return ap.parse_args()
 
 
@@ -403,6 +405,14 @@ def main():
                      "hbm_frac": traffic / t_attn / 1e9 / PEAK_HBM_GBS if traffic else None},
         "solve_info_nonzero_layers": bad,
     }
+    if args.dump_dw:  # the patches are the artefact the method persists (outside the timed region)
+        os.makedirs(args.dump_dw, exist_ok=True)
+        for li in range(nl):
+            np.save(os.path.join(args.dump_dw, f"dW_layer{li:02d}.npy"), bufs.dW[li].cpu().numpy())
+            if cfg.rank:
+                np.save(os.path.join(args.dump_dw, f"A_layer{li:02d}.npy"), bufs.A[li].cpu().numpy())
+                np.save(os.path.join(args.dump_dw, f"U_layer{li:02d}.npy"), bufs.U[li].cpu().numpy())
+        log(f"[bench] wrote {nl} layer patch(es) to {args.dump_dw}")
     if not args.no_cpu_baseline:
         log("[bench] timing the fp64 CPU oracle on a bounded sample")
         out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_rows)

@@ -1354,9 +1354,10 @@ hipError_t solve_t(const T* G, const T* C, int64_t d64, int64_t dout64, double l
   }
   const T one = T(1), zero = T(0), mone = T(-1);
   auto run = [&](const GemmDesc<T>* g, int n) -> hipError_t {
-    if constexpr (sizeof(T) == 4)
+    if constexpr (sizeof(T) == 4) {
       if (products == kProductsSplit6) return run_group_split<6>(g, n, st);
-      else if (products == kProductsSplit3) return run_group_split<3>(g, n, st);
+      if (products == kProductsSplit3) return run_group_split<3>(g, n, st);
+    }
     return run_group(g, n, st);
   };
   // Column blocks of NB are grouped into outer blocks of OB = NBO * NB. Within an

@@ -1,22 +1,26 @@
-"""HBM traffic per kernel from rocprofv3 counter runs, calibrated on a plain copy.
+"""Markdown summaries of rocprofv3 runs of bench.py, for profiles/.
 
-Reads four ``rocprofv3 --pmc ... --output-format csv`` output folders: FETCH_SIZE and
-WRITE_SIZE of ``copy_calib.py`` (1 GiB read and 1 GiB written per dispatch), then
-FETCH_SIZE and WRITE_SIZE of a bench.py run. Optionally a ``--kernel-trace --stats``
-folder of the same bench command gives each kernel's average duration. Prints a
-markdown summary: per kernel of the library, the dispatches, the calibrated bytes
-read and written per dispatch, and (with durations) the achieved HBM GB/s and its
-fraction of the 8 TB/s peak. The lines
+Three modes (each prints one summary with the command it summarises):
 
-    traffic_bytes_per_launch <call> <bytes>
-    source_sha256 <file> <hash>
+  traffic  HBM traffic per kernel: four ``rocprofv3 --pmc ... --output-format csv``
+           folders, FETCH_SIZE and WRITE_SIZE of ``copy_calib.py`` (1 GiB read and 1 GiB
+           written per dispatch) and of the bench command; optionally a
+           ``--kernel-trace --stats`` folder of the same command for durations. Per kernel:
+           dispatches, calibrated bytes read and written, achieved HBM GB/s and fraction
+           of 8 TB/s. The lines
+               traffic_bytes_per_launch attend_full <bytes>
+               source_sha256 <file> <hash>
+           are what bench.py reads back (it trusts the figure only while the hashed
+           sources are unchanged): the V^T pre-pass, fast path and fixup of one
+           full-cache attention.
+  trace    kernel time per kernel from a ``--kernel-trace --stats`` folder.
+  mfma     ``--pmc MfmaUtil MfmaFlopsBF16 --kernel-trace`` folder: MFMA busy share and
+           executed bf16 MFMA work per kernel.
 
-are what bench.py reads back (it trusts a figure only while the hashed sources are
-unchanged). <call> is ``attend_full``: the V^T pre-pass, the fast path and the fixup
-of one full-cache attention.
-
-    python traffic_summary.py --copy-fetch D1 --copy-write D2 --fetch D3 --write D4 \\
+    python profile_summary.py traffic --copy-fetch D1 --copy-write D2 --fetch D3 --write D4 \\
         [--trace D5] --workload NAME --command "..." > profiles/hbm_traffic__NAME.md
+    python profile_summary.py trace --trace D --workload NAME --command "..."
+    python profile_summary.py mfma --counters D --workload NAME --command "..."
 """
 from __future__ import annotations
 
@@ -123,16 +127,84 @@ def mean(v):
     return sum(v) / len(v)
 
 
+def hashes() -> None:
+    for s in SOURCES:
+        with open(os.path.join(ROOT, s), "rb") as fh:
+            print(f"    source_sha256 {s} {hashlib.sha256(fh.read()).hexdigest()}")
+
+
+def trace_mode(a) -> None:
+    files = glob.glob(os.path.join(a.trace, "**", "*kernel_stats.csv"), recursive=True)
+    if not files:
+        sys.exit(f"no kernel_stats.csv under {a.trace}")
+    rows = [r for f in files for r in csv.DictReader(open(f, newline=""))]
+    total = sum(float(r["TotalDurationNs"]) for r in rows)
+    print(f"# Kernel trace: {a.workload}\n")
+    print("Command (run on the MI355X box from /tmp with TMPDIR=/tmp):\n")
+    print(f"    rocprofv3 --kernel-trace --stats --output-format csv -d <trace> -o p -- {a.command}")
+    print(f"    python profile_summary.py trace --trace <trace> --workload {a.workload} --command '...'\n")
+    print("Sources:\n")
+    hashes()
+    print("\n| kernel | calls | total us | avg us | % |\n|---|---|---|---|---|")
+    for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"])):
+        t = float(r["TotalDurationNs"])
+        if t < 1e-4 * total:
+            continue
+        print(f"| `{short(r['Name'])}` | {int(r['Calls'])} | {t / 1e3:,.0f} | "
+              f"{float(r['AverageNs']) / 1e3:,.2f} | {100 * t / total:.2f} |")
+
+
+def mfma_mode(a) -> None:
+    util = read_counter(a.counters, "MfmaUtil")
+    flops = read_counter(a.counters, "MfmaFlopsBF16")
+    files = glob.glob(os.path.join(a.counters, "**", "*counter_collection.csv"), recursive=True)
+    dur = defaultdict(list)
+    for f in files:
+        seen = set()
+        for row in csv.DictReader(open(f, newline="")):
+            key = (row["Kernel_Name"], row["Dispatch_Id"])
+            if key in seen:
+                continue
+            seen.add(key)
+            dur[row["Kernel_Name"]].append(int(row["End_Timestamp"]) - int(row["Start_Timestamp"]))
+    print(f"# MFMA utilisation per kernel: {a.workload}\n")
+    print("Command (run on the MI355X box from /tmp with TMPDIR=/tmp):\n")
+    print(f"    rocprofv3 --pmc MfmaUtil MfmaFlopsBF16 --kernel-trace --output-format csv -d <counters> -o p -- {a.command}")
+    print(f"    python profile_summary.py mfma --counters <counters> --workload {a.workload} --command '...'\n")
+    print("`MfmaUtil`: share of SIMD cycles with the MFMA pipe busy (duration-weighted mean over "
+          "dispatches). `MfmaFlopsBF16`: bf16 MFMA work the hardware executed (the split-bf16 fp32 "
+          "products execute several bf16 products per algorithmic one; fp32 MFMA is not counted). "
+          "Durations are those of the counter run (dispatches serialised by the profiler).\n")
+    print("Sources:\n")
+    hashes()
+    print("\n| kernel | dispatches | MfmaUtil % | bf16 MFMA FLOP / dispatch | duration us | "
+          "executed bf16 TFLOP/s |\n|---|---|---|---|---|---|")
+    ks = [k for k in util if LIB_KERNEL.search(k) and k in flops and mean(flops[k]) > 0]
+    for k in sorted(ks, key=lambda k: -mean(dur[k]) * len(dur[k])):
+        d = dur[k]
+        w = sum(u * t for u, t in zip(util[k], d)) / max(sum(d), 1)
+        fl = mean(flops[k])
+        print(f"| `{short(k)}` | {len(d)} | {w:.1f} | {fl:.4g} | {mean(d) / 1e3:,.1f} | "
+              f"{fl / (mean(d) * 1e-9) / 1e12:,.0f} |")
+
+
 def main() -> None:
     ap = argparse.ArgumentParser()
-    for a in ("copy-fetch", "copy-write", "fetch", "write"):
-        ap.add_argument(f"--{a}", required=True)
+    ap.add_argument("mode", choices=("traffic", "trace", "mfma"))
+    for x in ("copy-fetch", "copy-write", "fetch", "write", "counters"):
+        ap.add_argument(f"--{x}")
     ap.add_argument("--trace")
     ap.add_argument("--workload", required=True)
     ap.add_argument("--command", required=True, help="the bench command that was profiled")
     ap.add_argument("--teacher-psplit", action="store_true",
                     help="the workload's full-cache pass forms P V from a two-term P")
     a = ap.parse_args()
+    if a.mode == "trace":
+        return trace_mode(a)
+    if a.mode == "mfma":
+        return mfma_mode(a)
+    if not (a.copy_fetch and a.copy_write and a.fetch and a.write):
+        sys.exit("traffic needs --copy-fetch, --copy-write, --fetch and --write")
 
     sf, rf = calibration(a.copy_fetch, "FETCH_SIZE")
     sw, rw = calibration(a.copy_write, "WRITE_SIZE")
@@ -144,9 +216,7 @@ def main() -> None:
     print("Counters FETCH_SIZE and WRITE_SIZE (KiB per dispatch, summed over the XCDs), each from "
           "a run of its own, scaled by what the same counter reads for a plain 1 GiB copy.\n")
     print("## Sources these counters belong to\n")
-    for s in SOURCES:
-        with open(os.path.join(ROOT, s), "rb") as fh:
-            print(f"    source_sha256 {s} {hashlib.sha256(fh.read()).hexdigest()}")
+    hashes()
     print("\n## Commands\n")
     print("Run on the MI355X box from /tmp with TMPDIR=/tmp; one counter per pass:\n")
     print("    rocprofv3 --pmc FETCH_SIZE --output-format csv -d <copy-fetch> -o p -- "
@@ -157,7 +227,7 @@ def main() -> None:
     print(f"    rocprofv3 --pmc WRITE_SIZE --output-format csv -d <write> -o p -- {a.command}")
     if a.trace:
         print(f"    rocprofv3 --kernel-trace --stats --output-format csv -d <trace> -o p -- {a.command}")
-    print("    python traffic_summary.py --copy-fetch <copy-fetch> --copy-write <copy-write> "
+    print("    python profile_summary.py traffic --copy-fetch <copy-fetch> --copy-write <copy-write> "
           "--fetch <fetch> --write <write>" + (" --trace <trace>" if a.trace else "")
           + f" --workload {a.workload} --command '...'")
     print("\n## Calibration (plain copy, 1,073,741,824 bytes read and written)\n")
