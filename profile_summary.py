@@ -261,10 +261,11 @@ def main() -> None:
 
     # the full-cache pass: the V^T pre-pass over the whole cache (the largest dispatch of
     # the non-gathering vt_kernel), the teacher's fast path and its fixup (one dispatch
-    # each per layer: no other call uses these instantiations)
+    # each per layer: no other call uses these instantiations) and, with split key
+    # ranges, the merge (its largest dispatch)
     ps = "true" if a.teacher_psplit else "false"
-    pats = [r"vt_kernel<\d+, false, 0>",
-            rf"attn_bf16_kernel<\d+, false, {ps}, false, (false|true), false, false, 0>"]
+    pats = [r"vt_kernel<\d+, false, 0>", r"attn_combine_kernel<\d+, true>",
+            rf"attn_bf16_kernel<\d+, false, {ps}, (false|true), (false|true), false, false, 0>"]
     def largest(k):
         f = max(fetch.get(k, [0.0])) * 1024.0 * sf
         w = max(write.get(k, [0.0])) * 1024.0 * sw
@@ -272,7 +273,7 @@ def main() -> None:
     full = [k for k in set(fetch) | set(write)
             if LIB_KERNEL.search(k) and any(re.fullmatch(pt, short(k)) for pt in pats)]
     if len(full) >= 2:
-        print("\n## One full-cache attention launch (V^T pre-pass, fast path, fixup)\n")
+        print("\n## One full-cache attention launch (V^T pre-pass, fast path, fixup, merge)\n")
         for k in sorted(full, key=short):
             print(f"- `{short(k)}`: {largest(k) / 1e6:,.1f} MB")
         print(f"\n    traffic_bytes_per_launch attend_full {sum(largest(k) for k in full):.0f}")
