@@ -236,8 +236,9 @@ int patchkv_attend_chunk(int dtype, const void* Q, const void* K, const void* V,
 /*  - bias [Hkv][n_cache] float (natural-log units, indexed by cache entry) or  */
 /*    NULL for none.                                                           */
 /*  - p_terms as for patchkv_attend_chunk (1: P rounded to bf16; 2: two terms). */
-/* Quantized entries are first expanded to dtype rows in the workspace (the      */
-/* compressed cache is small), then attended like a plain cache.               */
+/* Quantized entries, exact in bf16: the bf16 kernels read them as stored and  */
+/* expand them on the way into LDS (no copy of the cache); with dtype F32 they */
+/* are first expanded into f32 rows in the workspace.                          */
 /* Limits as patchkv_attend_compressed with B = n_cache; dh a multiple of 32.  */
 /* Workspace: patchkv_attend_cache_workspace_bytes(...).                       */
 /* ------------------------------------------------------------------------- */
