@@ -60,8 +60,9 @@ def test_targets(M, din, dout, wdt, rho):
 
 
 @pytest.mark.parametrize("rows,din,dout", [(128, 256, 256), (300, 200, 130), (2048, 1024, 1024),
-                                           (5, 64, 33)])
+                                           (5, 64, 33), (1000, 3584, 512), (700, 4096, 256)])
 def test_normal_equations_f32(rows, din, dout):
+    """G exactly symmetric (mirrored tiles) and both products the same bits every call."""
     X, Yf, Yc = randn((rows, din), 4, 0.2), randn((rows, dout), 5), randn((rows, dout), 6)
     G, C = pkv.accumulate_normal_eq(dev(X), dev(Yf), dev(Yc), acc=pkv.F32)
     Gr, Cr = oracle.normal_equations(X.astype(np.float64), Yf.astype(np.float64) - Yc.astype(np.float64))
@@ -69,6 +70,8 @@ def test_normal_equations_f32(rows, din, dout):
     assert rel(host(C), Cr) <= 5e-5
     g = host(G)
     assert np.array_equal(g, g.T)
+    G2, C2 = pkv.accumulate_normal_eq(dev(X), dev(Yf), dev(Yc), acc=pkv.F32)
+    assert torch.equal(G2, G) and torch.equal(C2, C)
 
 
 @pytest.mark.parametrize("acc,din,dout", [("f32", 192, 160), ("f64", 192, 160), ("f32", 600, 300),
