@@ -19,9 +19,10 @@
 // fp32 in the exp2 domain with a fixed per-row offset (fast path) and falls back
 // to a lazily rescaled pass for work items whose scores outgrow it. On the main
 // path K/V^T tiles go from HBM straight into eight LDS slots (buffer_load ... lds, no
-// register staging), six tiles ahead, with XOR-swizzled 16-byte chunks in place of
-// row padding and one barrier per two tiles; the gathering, biased and two-term-P
-// variants stage through registers into four padded slots. The workgroup -> work-item
+// register staging; issued by waves 0-3 only), six tiles ahead, with XOR-swizzled
+// 16-byte chunks in place of row padding and one barrier per two tiles; the
+// gathering, biased, two-term-P and block-scaled variants stage through registers into
+// four padded slots. The workgroup -> work-item
 // map keeps all row tiles of one KV head (and key range) on one XCD so its L2
 // serves the K/V re-reads.
 //
@@ -43,6 +44,12 @@
 // of the cache, and the work item of the last key range then takes the own
 // entries' tiles, masked per query. Every range keeps at least one cache key, so
 // every row of every partial result has a finite maximum.
+//
+// Block-scaled integer caches (KQ = 8 or 4; App. C, quantized KV caches): K and V
+// hold int8 (or packed int4) values with one power-of-two exponent per 32 channels.
+// The register-staged loads fetch the stored bytes and expand each 8-channel chunk
+// to bf16 when the tile is stored to LDS; vt_kernel expands V on its way into the V^T
+// tiles. The expansion is exact, so the arithmetic after it is that of a bf16 cache.
 #pragma once
 
 #include <math.h>

@@ -16,7 +16,7 @@ import torch
 import oracle
 import paper_2609_39329_amd as pkv
 from gpu_util import DEV, host, idx_dev, rel, to_dev
-from workloads import make_cache_bias, make_custom_inputs, make_quant_cache
+from workloads import make_cache_bias, make_custom_inputs, make_quant_cache, pack_int4
 
 pytestmark = pytest.mark.gpu
 
@@ -193,3 +193,37 @@ def test_block_scaled_per_head_sets_and_bad_entries(bits):
         torch.cuda.synchronize()
         assert torch.equal(Oq, Ox)
         assert int(iq.item()) == int(ix.item()) == -(1 + 1 * idx.shape[1] + 5)
+
+
+@pytest.mark.parametrize("bits", [8, 4])
+def test_block_scaled_extreme_exponents(bits):
+    """Exponents far from the workloads' (values down in bf16's subnormal range and up
+    near 2^117 for V): the kernels' expansion (ldexp in fp32, then round to nearest even to
+    bf16) gives the same bits as the exact values rounded by torch, so the in-kernel
+    path equals attention over those rows bit for bit."""
+    M, N, Hq, Hkv, dh = 40, 700, 4, 2, 128
+    rng = np.random.default_rng(77 + bits)
+    qmax = 127 if bits == 8 else 7
+    Kq = rng.integers(-qmax, qmax + 1, (Hkv, N, dh)).astype(np.int8)
+    Vq = rng.integers(-qmax, qmax + 1, (Hkv, N, dh)).astype(np.int8)
+    Ke = rng.integers(-9, -5, (Hkv, N, dh // 32)).astype(np.int8)
+    # int8 exponents: the smallest ones put q 2^e (|q| <= 3) below 2^-126, in the
+    # subnormal range; the largest reach 127 2^110
+    Ve = np.where(rng.random((Hkv, N, dh // 32)) < 0.5, rng.integers(-128, -117, (Hkv, N, dh // 32)),
+                  rng.integers(100, 111, (Hkv, N, dh // 32))).astype(np.int8)
+    assert (Ve == -128).any() and np.abs(oracle.dequantize_mx(Vq, Ve)).max() < 3e38
+    pack = (lambda a: a) if bits == 8 else pack_int4
+    fmt = pkv.KV_MXINT8 if bits == 8 else pkv.KV_MXINT4
+    K = oracle.dequantize_mx(Kq, Ke)
+    V = oracle.dequantize_mx(Vq, Ve)
+    kx = torch.from_numpy(K.astype(np.float32)).to(torch.bfloat16).to(DEV)
+    vx = torch.from_numpy(V.astype(np.float32)).to(torch.bfloat16).to(DEV)
+    q = torch.from_numpy(rng.standard_normal((M, Hq, dh)).astype(np.float32)).to(torch.bfloat16).to(DEV)
+    kq, vq, ke, ve = (torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+                      for a in (pack(Kq), pack(Vq), Ke, Ve))
+    for pt in (1, 2):
+        Oq = pkv.attend_cache(q, kq, vq, kv_format=fmt, Ke=ke, Ve=ve, n_cache=N, p_terms=pt)
+        Ox = pkv.attend_cache(q, kx, vx, n_cache=N, p_terms=pt)
+        torch.cuda.synchronize()
+        assert torch.isfinite(Ox).all()
+        assert torch.equal(Oq, Ox)
