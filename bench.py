@@ -7,7 +7,8 @@ solve (the same five library calls, in the same order, that
 patchkv_compute_layer_patch makes). For a chunked reference set: the two
 attention passes, targets and statistics of every chunk, then one solve. For the
 MLP-shaped patch: both attention passes, the SwiGLU features of both, the block
-targets, the d_ff x d statistics and solve, and the student-state propagation.
+targets, the ridge solve (in the dual form, rows x rows, when d_ff exceeds the
+reference rows) and the student-state propagation.
 The default workload is the 32-layer Llama-3-8B-shaped patch build over a
 172,032-token context (1 % cache budget, 4,096 reference queries per layer). All
 layer inputs are resident in HBM before the timed region starts.
@@ -117,6 +118,12 @@ class LayerDev:
         self.Vc = t(inp.Vc) if inp.Vc is not None else None
 
 
+def dual_solve(cfg) -> bool:
+    """The ridge patch through X^T (X X^T + lambda I)^{-1} T: the MLP-shaped patch whose
+    d_ff exceeds the reference rows (and needs no G for a reduced-rank step)."""
+    return bool(cfg.d_ff) and not cfg.rank and cfg.M < cfg.d_ff
+
+
 class Buffers:
     """Per-step device buffers shared by all layers (the stream orders their reuse)."""
 
@@ -129,8 +136,12 @@ class Buffers:
         self.Of = torch.empty((M, d), dtype=torch.float32, device=dev)
         self.Oc = torch.empty((M, d), dtype=torch.float32, device=dev)
         self.T = torch.empty((M, d), dtype=torch.float32, device=dev)
-        self.G = torch.empty((din, din), dtype=adt, device=dev)
-        self.C = torch.empty((din, d), dtype=adt, device=dev)
+        # the MLP-shaped patch with fewer reference rows than d_ff: solved in the dual
+        # form (rows x rows) straight from H_c and T, no d_ff x d_ff statistics
+        self.dual = dual_solve(cfg)
+        if not self.dual:
+            self.G = torch.empty((din, din), dtype=adt, device=dev)
+            self.C = torch.empty((din, d), dtype=adt, device=dev)
         self.dW = [torch.empty((din, d), dtype=torch.float32, device=dev) for _ in range(nl)]
         self.info = torch.zeros((nl,), dtype=torch.int32, device=dev)
         if cfg.rank:  # reduced-rank factors of every layer's patch
@@ -172,12 +183,17 @@ def layer_steps(pkv, cfg, L, bufs, li: int, events=None):
         pkv.mlp_features(bufs.Of, L.Wg, L.Wu, eps=L.eps, H=bufs.Hf)
         pkv.mlp_features(bufs.Oc, L.Wg, L.Wu, eps=L.eps, H=bufs.Hc)
         pkv.compute_block_targets(bufs.Hf, bufs.Hc, L.Wd, bufs.Of, bufs.Oc, T=bufs.T)
-        pkv.accumulate_normal_eq(bufs.Hc, bufs.T, G=bufs.G, C=bufs.C, acc=acc)
+        if bufs.dual:
+            pkv.solve_patch_dual(bufs.Hc, bufs.T, cfg.lam, mode=bufs.mode, dW=bufs.dW[li],
+                                 info=bufs.info[li:li + 1])
+        else:
+            pkv.accumulate_normal_eq(bufs.Hc, bufs.T, G=bufs.G, C=bufs.C, acc=acc)
     else:
         pkv.compute_targets(bufs.Of, bufs.Oc, L.W, rho=1, T=bufs.T)
         pkv.accumulate_normal_eq(bufs.Oc, bufs.T, G=bufs.G, C=bufs.C, acc=acc)
-    pkv.solve_patch(bufs.G, bufs.C, cfg.lam, mode=bufs.mode, dW=bufs.dW[li],
-                    info=bufs.info[li:li + 1])
+    if not bufs.dual:
+        pkv.solve_patch(bufs.G, bufs.C, cfg.lam, mode=bufs.mode, dW=bufs.dW[li],
+                        info=bufs.info[li:li + 1])
     if cfg.d_ff:  # the student state through the patched block
         pkv.propagate_student(bufs.Hc, L.Wd, bufs.dW[li], bufs.Oc, Y=bufs.Y)
     if cfg.rank:  # the reduced-rank factors (A, U): dW_r = A U^T
@@ -381,7 +397,9 @@ def main():
                    "own_causal_prefix": chunked, "ridge": cfg.ridge, "rank": cfg.rank,
                    "kv_format": cfg.kv_format, "cache_bias": cfg.cache_bias,
                    "patch": (f"MLP down-projection {cfg.d_ff}x{d} (SwiGLU features, student "
-                             f"propagation)" if cfg.d_ff else f"{d}x{d} projection")},
+                             f"propagation)" if cfg.d_ff else f"{d}x{d} projection"),
+                   "solve": (f"dual ({M}x{M} system from H_c and T)" if dual_solve(cfg)
+                             else f"primal ({cfg.d_ff or d}x{cfg.d_ff or d} normal equations)")},
         "attention_full_ms": t_attn * 1e3,
         "attention_full_tflops": achieved,
         "attention_full_frac_of_peak": achieved / peak,

@@ -348,6 +348,28 @@ int patchkv_solve_patch(int acc_dtype, const void* G, const void* C, int64_t d_i
                         void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------- */
+/* The same ridge patch from the data, for few rows and a wide d_in (the       */
+/* MLP-shaped patch: one block of M reference tokens, d_in = d_ff > M). Eq. 8  */
+/* through the push-through identity:                                        */
+/*   dW = (X^T X + lambda I)^{-1} X^T T = X^T (X X^T + lambda I)^{-1} T,        */
+/* so the factored system is rows x rows: K = X X^T (split-bf16 MFMA, all four  */
+/* term pairs, fp32), the solve of patchkv_solve_patch on (K, T), then X^T Y.    */
+/* X [rows][d_in], T [rows][d_out] float (the statistics' inputs, not G and C); */
+/* dW [d_in][d_out] float, written. ridge_mode as for patchkv_solve_patch, and  */
+/* every mode gives the primal system's lambda: ||X^T X||_F = ||X X^T||_F and   */
+/* tr X^T X = tr X X^T, and the trace mean stays a mean over d_in. info as for  */
+/* the solve (first failing pivot of K + lambda I, 1-based).                   */
+/* Limits: 1 <= rows, d_in, d_out <= 65536;                                  */
+/* every pointer 16-byte aligned, info 4-byte aligned.                         */
+/* ------------------------------------------------------------------------- */
+size_t patchkv_solve_patch_dual_workspace_bytes(int64_t rows, int64_t d_in, int64_t d_out);
+
+int patchkv_solve_patch_dual(const float* X, const float* T, int64_t rows, int64_t d_in,
+                             int64_t d_out, double lambda, int ridge_mode, float* dW,
+                             int32_t* info, void* workspace, size_t workspace_bytes,
+                             void* stream);
+
+/* ------------------------------------------------------------------------- */
 /* Reduced-rank patch (App. C, low-rank weight patches; reduced-rank regression):*/
 /* the ridge patch projected onto its top-r output subspace. In row form,       */
 /*   dW_r = dW U_r U_r^T,  U_r [d_out][r] = top-r eigenvectors of dW^T G dW,    */

@@ -74,6 +74,9 @@ SIGNATURES = {
     "patchkv_accumulate_normal_eq": (_c_int, [_c_int, _c_vp, _c_vp, _c_vp, _c_i64, _c_i64, _c_i64,
                                               _c_int, _c_vp, _c_vp, _c_vp, _c_sz, _c_vp]),
     "patchkv_solve_workspace_bytes": (_c_sz, [_c_int, _c_i64, _c_i64]),
+    "patchkv_solve_patch_dual_workspace_bytes": (_c_sz, [_c_i64, _c_i64, _c_i64]),
+    "patchkv_solve_patch_dual": (_c_int, [_c_vp, _c_vp, _c_i64, _c_i64, _c_i64, ctypes.c_double,
+                                          _c_int, _c_vp, _c_vp, _c_vp, _c_sz, _c_vp]),
     "patchkv_solve_patch": (_c_int, [_c_int, _c_vp, _c_vp, _c_i64, _c_i64, ctypes.c_double, _c_int,
                                      _c_vp, _c_vp, _c_vp, _c_sz, _c_vp]),
     "patchkv_low_rank_workspace_bytes": (_c_sz, [_c_i64, _c_i64, _c_int]),
@@ -534,6 +537,35 @@ def solve_patch(G, C, lam: float, mode: int = RIDGE_ABSOLUTE, dW=None, info=None
     _check("patchkv_solve_patch",
            L.patchkv_solve_patch(acc, _ptr(G), _ptr(C), din, dout, lam, mode, _ptr(dW), _ptr(info),
                                  _ptr(ws), nb, _stream(stream)))
+    return dW, info
+
+
+def solve_patch_dual(X, T, lam: float, mode: int = RIDGE_ABSOLUTE, dW=None, info=None,
+                     stream=None):
+    """dW = X^T (X X^T + lam I)^{-1} T, equal to (X^T X + lam I)^{-1} X^T T (X [rows, d_in],
+    T [rows, d_out] float32; fp32 out); returns (dW, info tensor)."""
+    torch = _torch()
+    _require_gpu(X, T, dW, info)
+    _expect(X, "X", torch.float32)
+    if X.dim() != 2:
+        raise ValueError(f"X must have shape [rows, d_in], got {list(X.shape)}")
+    rows, din = X.shape
+    _expect(T, "T", torch.float32, (rows, None))
+    dout = T.shape[1]
+    _expect(dW, "dW", torch.float32, (din, dout))
+    _expect_info(info)
+    if dW is None:
+        dW = torch.empty((din, dout), dtype=torch.float32, device=X.device)
+    if info is None:
+        info = torch.empty((1,), dtype=torch.int32, device=X.device)
+    L = lib()
+    nb = L.patchkv_solve_patch_dual_workspace_bytes(rows, din, dout)
+    if nb == 0:
+        raise ValueError(f"unsupported dual solve shape rows={rows} d_in={din} d_out={dout}")
+    ws = _workspace(nb, X.device, stream)
+    _check("patchkv_solve_patch_dual",
+           L.patchkv_solve_patch_dual(_ptr(X), _ptr(T), rows, din, dout, lam, mode, _ptr(dW),
+                                      _ptr(info), _ptr(ws), nb, _stream(stream)))
     return dW, info
 
 

@@ -472,6 +472,64 @@ int patchkv_solve_patch(int acc_dtype, const void* G, const void* C, int64_t d_i
 }
 
 namespace {
+// Dual-form solve workspace: K = X X^T, Y = (K + lambda I)^{-1} T, the solve's own
+// workspace, the statistics' split planes.
+struct DualSolveWs {
+  size_t K, Y, solve, stats, total;
+};
+DualSolveWs dual_solve_layout(int64_t rows, int64_t din, int64_t dout) {
+  DualSolveWs L{};
+  size_t o = 0;
+  L.K = o; o += align_up(sizeof(float) * rows * rows);
+  L.Y = o; o += align_up(sizeof(float) * rows * dout);
+  L.solve = o; o += align_up(solve_ws_bytes(false, rows, dout));
+  L.stats = o; o += align_up(dual_stats_ws_bytes(rows, din, dout));
+  L.total = o;
+  return L;
+}
+int check_dual_dims(int64_t rows, int64_t din, int64_t dout) {
+  int s = check_stats_dims(rows, din, dout);
+  if (s) return s;
+  return rows > kMaxDim ? PATCHKV_E_SHAPE : PATCHKV_OK;
+}
+}  // namespace
+
+size_t patchkv_solve_patch_dual_workspace_bytes(int64_t rows, int64_t d_in, int64_t d_out) {
+  if (check_dual_dims(rows, d_in, d_out)) return 0;
+  return dual_solve_layout(rows, d_in, d_out).total;
+}
+
+int patchkv_solve_patch_dual(const float* X, const float* T, int64_t rows, int64_t d_in,
+                             int64_t d_out, double lambda, int ridge_mode, float* dW,
+                             int32_t* info, void* workspace, size_t workspace_bytes,
+                             void* stream) {
+  if (!X || !T || !dW || !info) return PATCHKV_E_NULL;
+  int s = check_dual_dims(rows, d_in, d_out);
+  if (s) return s;
+  if (!finite_pos(lambda)) return PATCHKV_E_VALUE;
+  if (!valid_ridge_mode(ridge_mode)) return PATCHKV_E_VALUE;
+  if (!al16(X) || !al16(T) || !al16(dW) || !al4(info)) return PATCHKV_E_VALUE;
+  const DualSolveWs L = dual_solve_layout(rows, d_in, d_out);
+  s = check_ws(workspace, workspace_bytes, L.total);
+  if (s) return s;
+  char* w = (char*)workspace;
+  float* K = (float*)(w + L.K);
+  float* Y = (float*)(w + L.Y);
+  const hipStream_t st = (hipStream_t)stream;
+  // The solve takes the trace mean over its own side (rows); the primal system's mean
+  // is over d_in, with the same trace.
+  const double lam = ridge_kind(ridge_mode) == PATCHKV_RIDGE_TRACE_MEAN
+                         ? lambda * (double)rows / (double)d_in
+                         : lambda;
+  hipError_t e = launch_gram_rows(X, rows, d_in, K, w + L.stats, st);
+  if (e == hipSuccess)
+    e = launch_solve(false, K, T, rows, d_out, lam, ridge_kind(ridge_mode), products(ridge_mode),
+                     Y, info, w + L.solve, st);
+  if (e == hipSuccess) e = launch_xt_y(X, Y, rows, d_in, d_out, dW, w + L.stats, st);
+  return status_of(e);
+}
+
+namespace {
 int check_low_rank(int64_t din, int64_t dout, int r, int iters) {
   if (din < 1 || dout < 2 || din > kMaxDim || dout > kMaxDim) return PATCHKV_E_SHAPE;
   const int b = (int)std::min<int64_t>(64, dout) & ~1;

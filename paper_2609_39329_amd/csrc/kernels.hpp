@@ -104,6 +104,15 @@ hipError_t launch_normal_eq_f32(const float* X, const float* Yf, const float* Yc
                                 int64_t din, int64_t dout, bool accumulate, float* G, float* C,
                                 void* ws, hipStream_t st);
 
+// Dual-form statistics (few rows, wide d_in): K [rows][rows] = X X^T (exactly
+// symmetric) and Out [din][dout] = X^T Y, X [rows][din], Y [rows][dout], split-bf16
+// MFMA with all four term pairs, fp32 accumulation.
+size_t dual_stats_ws_bytes(int64_t rows, int64_t din, int64_t dout);
+hipError_t launch_gram_rows(const float* X, int64_t rows, int64_t din, float* K, void* ws,
+                            hipStream_t st);
+hipError_t launch_xt_y(const float* X, const float* Y, int64_t rows, int64_t din, int64_t dout,
+                       float* Out, void* ws, hipStream_t st);
+
 // ---------------------------------------------------------------- statistics (fp64 acc)
 hipError_t launch_targets_f64(const float* Of, const float* Oc, const void* W, bool w_bf16,
                               int64_t M, int64_t din, int64_t dout, int rho, double* T,

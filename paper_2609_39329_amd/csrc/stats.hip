@@ -7,6 +7,7 @@
 //
 // fp32-accumulate path: split pre-passes + bgemm_kernel (bf16 MFMA, fp32 accumulation).
 // fp64-accumulate path (f64_gemm_kernel): plain fp64 FMA tiles through LDS.
+#include <algorithm>
 #include <type_traits>
 
 #include "common.hpp"
@@ -647,6 +648,80 @@ hipError_t launch_propagate(const float* Hc, const void* W, bool w_bf16, const f
 }
 size_t normal_eq_ws_bytes(int64_t rows, int64_t din, int64_t dout) {
   return normal_eq_layout(rows, din, dout).total;
+}
+
+// ---------------------------------------------------------------- dual-form statistics
+//
+// For the ridge patch through the push-through identity (few rows, wide d_in):
+// K = X X^T over the rows, and dW = X^T Y. Both sum all four hi/lo term pairs (the
+// split of both operands loses only the lo x lo cross term otherwise; X^T Y's result
+// can be much smaller than |X||Y| when the ridge is small, so it keeps every term).
+struct DualWs {
+  size_t Ah, Al, Bh, Bl, total;
+};
+DualWs dual_layout(int64_t rows, int64_t din, int64_t dout) {
+  // K: planes of X [rows_p][din_p] (contraction d_in); X^T Y: planes of X^T and Y^T
+  // [*][rows_p] (contraction rows)
+  const int64_t rK = pad_to(rows, G_BM), cK = pad_to(din, G_KC);
+  const int64_t kY = pad_to(rows, G_KC), iY = pad_to(din, G_BM), jY = pad_to(dout, G_BM);
+  const size_t a = std::max((size_t)rK * cK, (size_t)iY * kY) * 2;
+  const size_t b = (size_t)jY * kY * 2;
+  DualWs L{};
+  size_t o = 0;
+  L.Ah = o; o += align_up(a);
+  L.Al = o; o += align_up(a);
+  L.Bh = o; o += align_up(b);
+  L.Bl = o; o += align_up(b);
+  L.total = o;
+  return L;
+}
+
+hipError_t launch_gram_rows(const float* X, int64_t rows, int64_t din, float* K, void* ws,
+                            hipStream_t st) {
+  const DualWs L = dual_layout(rows, din, 1);
+  const int64_t rK = pad_to(rows, G_BM), cK = pad_to(din, G_KC);
+  char* w = (char*)ws;
+  __bf16 *Xh = (__bf16*)(w + L.Ah), *Xl = (__bf16*)(w + L.Al);
+  hipError_t e = run_split_rows(X, nullptr, rows, din, din, Xh, Xl, rK, cK, st);
+  if (e != hipSuccess) return e;
+  BGemm g{};
+  g.ld = cK;
+  g.Out = K;
+  g.ldo = rows;
+  g.I = (int)rows;
+  g.J = (int)rows;
+  g.Kp = (int)cK;
+  g.A[0] = Xh; g.A[1] = Xl;
+  g.B[0] = Xh; g.B[1] = Xl;
+  return run_bgemm<2, 2, 4, 0b1100, 0b1010, true>(g, st);
+}
+
+hipError_t launch_xt_y(const float* X, const float* Y, int64_t rows, int64_t din, int64_t dout,
+                       float* Out, void* ws, hipStream_t st) {
+  const DualWs L = dual_layout(rows, din, dout);
+  const int64_t kY = pad_to(rows, G_KC), iY = pad_to(din, G_BM), jY = pad_to(dout, G_BM);
+  char* w = (char*)ws;
+  __bf16 *Xh = (__bf16*)(w + L.Ah), *Xl = (__bf16*)(w + L.Al);
+  __bf16 *Yh = (__bf16*)(w + L.Bh), *Yl = (__bf16*)(w + L.Bl);
+  // X [rows][din] -> X^T [din][rows]; Y [rows][dout] -> Y^T [dout][rows]
+  hipError_t e = run_split_transpose(X, (const float*)nullptr, rows, din, din, Xh, Xl, kY, iY, st);
+  if (e != hipSuccess) return e;
+  e = run_split_transpose(Y, (const float*)nullptr, rows, dout, dout, Yh, Yl, kY, jY, st);
+  if (e != hipSuccess) return e;
+  BGemm p{};
+  p.ld = kY;
+  p.Out = Out;
+  p.ldo = dout;
+  p.I = (int)din;
+  p.J = (int)dout;
+  p.Kp = (int)kY;
+  p.A[0] = Xh; p.A[1] = Xl;
+  p.B[0] = Yh; p.B[1] = Yl;
+  return run_bgemm<2, 2, 4, 0b1100, 0b1010, false>(p, st);
+}
+
+size_t dual_stats_ws_bytes(int64_t rows, int64_t din, int64_t dout) {
+  return dual_layout(rows, din, dout).total;
 }
 
 hipError_t launch_targets(const float* Of, const float* Oc, const void* W, bool w_bf16, int64_t M,

@@ -168,6 +168,28 @@ def test_solve_validation(L):
     assert f(B.F32, FAKE, FAKE, 0, 16, 0.1, 0, FAKE, FAKE, FAKE, nb, None) == B.E_SHAPE
 
 
+def test_solve_dual_validation(L):
+    f = L.patchkv_solve_patch_dual
+    q = L.patchkv_solve_patch_dual_workspace_bytes
+    nb = q(64, 512, 32)
+    # K = X X^T, Y = (K + lam I)^{-1} T and the rows x rows solve's workspace at least
+    assert nb >= 4 * (64 * 64 + 64 * 32) + L.patchkv_solve_workspace_bytes(B.F32, 64, 32)
+    assert q(0, 512, 32) == 0 and q(64, 0, 32) == 0 and q(64, 512, 0) == 0
+    assert q(1 << 17, 512, 32) == 0 and q(64, 1 << 17, 32) == 0
+    assert f(FAKE, FAKE, 64, 512, 32, 0.1, 0, FAKE, None, FAKE, nb, None) == B.E_NULL
+    assert f(None, FAKE, 64, 512, 32, 0.1, 0, FAKE, FAKE, FAKE, nb, None) == B.E_NULL
+    assert f(FAKE, FAKE, 0, 512, 32, 0.1, 0, FAKE, FAKE, FAKE, nb, None) == B.E_SHAPE
+    assert f(FAKE, FAKE, 1 << 17, 512, 32, 0.1, 0, FAKE, FAKE, FAKE, nb, None) == B.E_SHAPE
+    assert f(FAKE, FAKE, 64, 512, 32, 0.0, 0, FAKE, FAKE, FAKE, nb, None) == B.E_VALUE
+    assert f(FAKE, FAKE, 64, 512, 32, float("nan"), 0, FAKE, FAKE, FAKE, nb, None) == B.E_VALUE
+    assert f(FAKE, FAKE, 64, 512, 32, 0.1, 3, FAKE, FAKE, FAKE, nb, None) == B.E_VALUE
+    assert f(FAKE + 4, FAKE, 64, 512, 32, 0.1, 0, FAKE, FAKE, FAKE, nb, None) == B.E_VALUE
+    for mode in (B.RIDGE_ABSOLUTE, B.RIDGE_ADAPTIVE, B.RIDGE_TRACE_MEAN):
+        for ex in (0, B.SOLVE_EXACT_F32, B.SOLVE_FAST_BF16):
+            assert f(FAKE, FAKE, 64, 512, 32, 0.1, mode | ex, FAKE, FAKE, None, nb, None) == B.E_WORKSPACE
+    assert f(FAKE, FAKE, 64, 512, 32, 0.1, 0, FAKE, FAKE, FAKE, nb - 1, None) == B.E_WORKSPACE
+
+
 def test_layer_validation(L):
     f = L.patchkv_compute_layer_patch
     args = dict(dt=B.BF16, acc=B.F32, Q=FAKE, K=FAKE, V=FAKE, idx=FAKE, imode=B.IDX_SHARED,
