@@ -70,7 +70,7 @@ AttnPlan plan_attention(const AttnShape& s) {
   const double slots = 256.0 * (s.bf16 ? kWgPerCu : 1);
   // one bf16 tile-iteration of a workgroup ~ 64 x rows x dh x 4 flops at ~4 TFLOP/s per CU
   // (shared by the workgroups resident on the CU)
-  const double tile_s = (double)kt * rows_wg * s.dh * 4.0 / (s.bf16 ? 4e12 / kWgPerCu : 0.25e12);
+  const double tile_s = (double)kt * rows_wg * s.dh * 4.0 / (s.bf16 ? 4e12 / kWgPerCu : 0.45e12);
   double best = 1e300;
   int best_s = 1;
   for (int sp = 1; sp <= 64 && sp <= ntiles; ++sp) {

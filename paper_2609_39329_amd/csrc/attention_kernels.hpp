@@ -26,8 +26,9 @@
 // map keeps all row tiles of one KV head (and key range) on one XCD so its L2
 // serves the K/V re-reads.
 //
-// f32 path (attn_f32_kernel): one thread per query row, fp32 FMA dot products
-// against K/V tiles broadcast from LDS, exact online softmax with expf.
+// f32 path (attn_f32_kernel): exact fp32 products on MFMA 32x32x2 f32 (32 rows per
+// wave, as in the bf16 kernel), K/V tiles in their natural layout in LDS, online
+// softmax with expf and rescaling whenever a row's maximum grows.
 //
 // Both paths can split the cache into key ranges (more workgroups for small M);
 // attn_combine_kernel then merges the partial (O, m, l) triples.
@@ -105,7 +106,7 @@ constexpr float kTau = 8.0f;   // lazy-rescale threshold of the fixup path (log2
 constexpr float kBigSum = 0x1p64f;  // fast path: largest trusted partial row sum (2^kBig, kBig = 64)
 constexpr int kKeyTile = 32;  // keys per iteration, bf16 path
 constexpr int kRowsBf16 = 256;  // query rows per workgroup, bf16 path
-constexpr int kRowsF32 = 256;   // query rows per workgroup, f32 path (one thread per row)
+constexpr int kRowsF32 = 256;   // query rows per workgroup, f32 path (32 per wave)
 constexpr int kWgPerCu = 1;     // bf16 workgroups resident per CU (launch bound)
 // bf16 path: 32-row query tiles per wave (1: eight waves of 32 rows per workgroup,
 // two waves per SIMD, everything in VGPRs; 2: four waves of 64 rows, one per SIMD,
@@ -115,6 +116,7 @@ constexpr int kQT = 1;
 constexpr int kThreadsBf16 = kRowsBf16 / (32 * kQT) * 64;
 constexpr int kLoadSets = 2;
 constexpr int kKeyTileF32 = 32;
+constexpr int kF32Waves = 8;  // f32 path: waves per workgroup (32 rows each)
 // bf16 fast path without gather, bias or two-term P: K / V^T tiles are loaded straight
 // into LDS (buffer_load ... lds) through kDmaSlots slots, each tile's loads issued
 // kDmaAhead steps before the step that scores it, one barrier per kDmaSteps steps
@@ -851,13 +853,35 @@ __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnP
   }
 }
 
+// fp32 inputs: exact fp32 products on MFMA 32x32x2 f32, fp32 online softmax with expf.
+// A workgroup of kF32Waves waves owns kRowsF32 rows of one KV head, 32 per wave, as in
+// the bf16 kernel. K and V tiles of 32 keys are staged through registers into two LDS
+// slots (natural [key][d] layout: an fp32 operand is one value per lane, so V needs no
+// transposed copy). The contraction orders are chosen so that every operand read is a
+// 16-byte (or 8-byte) LDS read:
+//   scores S^T = K Q^T: step s pairs channel h * DH/2 + s of lane half h, so a lane
+//     reads 4 consecutive channels of its key for 4 steps;
+//   O^T += V^T P^T: step s takes key 8 (s / 4) + 4 h + s % 4 on lane half h, which is
+//     where element s of the score accumulator already holds that key's weight, and
+//     output row rho of MFMA tile dt is channel ND * rho + dt, so one read fetches a
+//     key's ND channels for all ND tiles.
 template <int DH, bool GATHER, bool PARTIAL, bool OWN, bool BIAS>
-__global__ __launch_bounds__(256) void attn_f32_kernel(AttnParams p) {
+__global__ __launch_bounds__(kF32Waves * 64) void attn_f32_kernel(AttnParams p) {
   static_assert(!(OWN && BIAS), "own entries carry no bias");
-  constexpr int KT = kKeyTileF32;
-  constexpr int C4 = DH / 4;
-  __shared__ f32x4 Ks[KT * C4];
-  __shared__ f32x4 Vs[KT * C4];
+  static_assert(DH == 64 || DH == 128, "head_dim 64 or 128");
+  static_assert(kRowsF32 == 32 * kF32Waves, "32 rows per wave");
+  constexpr int KT = kKeyTileF32;  // 32 keys per tile
+  constexpr int HALF = DH / 2;     // score steps (two channels per MFMA)
+  constexpr int ND = DH / 32;      // 32-row output tiles of O^T
+  constexpr int KPF = DH + 4;      // K tile pitch (floats): conflict-free 16-byte reads
+  constexpr int C4 = DH / 4;       // 16-byte chunks per row
+  constexpr int NT = kF32Waves * 64;
+  constexpr int LPT = KT * C4 / NT;  // chunks per thread per tile, K and V each
+  static_assert(KT == 32 && KT * C4 % NT == 0 && LPT >= 1, "whole staging rounds");
+  typedef float VN __attribute__((ext_vector_type(ND)));
+  __shared__ __attribute__((aligned(16))) float Ks[2][KT * KPF];
+  __shared__ __attribute__((aligned(16))) float Vs[2][KT * DH];
+  __shared__ float Bs[2][BIAS ? KT : 1];
 
   const int w = xcd_item(p.per_xcd);
   if (w >= p.total_items) return;
@@ -869,108 +893,188 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnParams p) {
   const int k_begin = split * p.keys_per_split;
   const int k_end = min(nk, k_begin + p.keys_per_split);  // empty range: (O, m, l) = (0, -inf, 0)
   const int32_t* ig = GATHER ? p.idx + (int64_t)g * p.idx_stride : nullptr;
+  const int ct = k_end > k_begin ? (k_end - k_begin + KT - 1) / KT : 0;  // cache tiles
+  const bool own_range = OWN && split == p.n_split - 1;
+  int ntiles = ct;
+  if (own_range) {
+    const int last_q = min(p.rows - 1, rt * kRowsF32 + kRowsF32 - 1) / p.G;
+    ntiles = ct + last_q / KT + 1;
+  }
 
-  const int tid = threadIdx.x;
-  const int r = rt * kRowsF32 + tid;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int h = lane >> 5, l32 = lane & 31;
+  const int r = rt * kRowsF32 + wid * 32 + l32;
   const int rr = min(r, p.rows - 1);
-  const int m = rr / p.G, j = rr - m * p.G;
+  const int mq = rr / p.G, jq = rr - mq * p.G;
   const float* Kb = (const float*)p.K + (int64_t)g * p.src_rows * DH;
   const float* Vb = (const float*)p.V + (int64_t)g * p.src_rows * DH;
-  const f32x4* qp = (const f32x4*)((const float*)p.Q + ((int64_t)m * p.Hq + g * p.G + j) * DH);
+  const float* Ksb = OWN ? (const float*)p.Ks + (int64_t)g * p.Ms * DH : nullptr;
+  const float* Vsb = OWN ? (const float*)p.Vs + (int64_t)g * p.Ms * DH : nullptr;
 
-  f32x4 q[C4], o[C4];
+  // B operand of the score steps: channels h * HALF .. h * HALF + HALF - 1 of this row
+  float qv[HALF];
+  {
+    const f32x4* qp =
+        (const f32x4*)((const float*)p.Q + ((int64_t)mq * p.Hq + g * p.G + jq) * DH + h * HALF);
 #pragma unroll
-  for (int i = 0; i < C4; ++i) {
-    q[i] = qp[i];
-    o[i] = f32x4{};
+    for (int i = 0; i < HALF / 4; ++i) {
+      const f32x4 v = qp[i];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) qv[4 * i + u] = v[u];
+    }
   }
-  float mrun = -INFINITY, l = 0.f;
+  f32x16 o[ND];
+#pragma unroll
+  for (int dt = 0; dt < ND; ++dt) o[dt] = f32x16{};
+  float m_run = -INFINITY, l_part = 0.f;
 
-  // one key: online-softmax update of (mrun, l, o) with row kk of the LDS tiles and
-  // logit bias b
-  auto attend_key = [&](int kk, float b) {
-    f32x4 acc = {};
+  // staging: chunk c = u * NT + tid of a tile is key row c / C4, channels 4 (c % C4)..
+  f32x4 kst[LPT], vst[LPT];
+  float bst = 0.f;
+  auto load_tile = [&](int t) {
 #pragma unroll
-    for (int i = 0; i < C4; ++i) {
-      const f32x4 kv = Ks[kk * C4 + i];
-      acc[0] = fmaf(q[i][0], kv[0], acc[0]);
-      acc[1] = fmaf(q[i][1], kv[1], acc[1]);
-      acc[2] = fmaf(q[i][2], kv[2], acc[2]);
-      acc[3] = fmaf(q[i][3], kv[3], acc[3]);
+    for (int u = 0; u < LPT; ++u) {
+      const int c = u * NT + tid, row = c / C4, col = c % C4;
+      f32x4 kv = {}, vv = {};
+      if (!OWN || t < ct) {
+        const int key = k_begin + t * KT + row;
+        if (key < k_end) {
+          int src = key;
+          bool in = true;
+          if constexpr (GATHER) {
+            // an entry outside the cache reads as a zero row (no offset is formed from it)
+            src = ig[key];
+            in = (uint32_t)src < (uint32_t)p.src_valid;
+          }
+          if (in) {
+            kv = *((const f32x4*)(Kb + (int64_t)src * DH) + col);
+            vv = *((const f32x4*)(Vb + (int64_t)src * DH) + col);
+          }
+        }
+      } else {
+        const int j = (t - ct) * KT + row;  // own entry
+        if (j < p.Ms) {
+          kv = *((const f32x4*)(Ksb + (int64_t)j * DH) + col);
+          vv = *((const f32x4*)(Vsb + (int64_t)j * DH) + col);
+        }
+      }
+      kst[u] = kv;
+      vst[u] = vv;
     }
-    const float sc = fmaf((acc[0] + acc[1]) + (acc[2] + acc[3]), p.c, b);
-    if (sc > mrun) {
-      const float a = expf(mrun - sc);
-      l *= a;
-#pragma unroll
-      for (int i = 0; i < C4; ++i) o[i] *= a;
-      mrun = sc;
+    if constexpr (BIAS) {
+      if (tid < KT) {
+        const int key = k_begin + t * KT + tid;
+        bst = key < k_end ? p.bias[(int64_t)g * p.Nk + key] : 0.f;
+      }
     }
-    const float pe = expf(sc - mrun);
-    l += pe;
+  };
+  auto store_tile = [&](int buf) {
 #pragma unroll
-    for (int i = 0; i < C4; ++i) {
-      const f32x4 vv = Vs[kk * C4 + i];
-      o[i][0] = fmaf(pe, vv[0], o[i][0]);
-      o[i][1] = fmaf(pe, vv[1], o[i][1]);
-      o[i][2] = fmaf(pe, vv[2], o[i][2]);
-      o[i][3] = fmaf(pe, vv[3], o[i][3]);
+    for (int u = 0; u < LPT; ++u) {
+      const int c = u * NT + tid, row = c / C4, col = c % C4;
+      *(f32x4*)&Ks[buf][row * KPF + 4 * col] = kst[u];
+      *(f32x4*)&Vs[buf][row * DH + 4 * col] = vst[u];
+    }
+    if constexpr (BIAS) {
+      if (tid < KT) Bs[buf][tid] = bst;
     }
   };
 
-  for (int tb = k_begin; tb < k_end; tb += KT) {
-    const int nk = min(KT, k_end - tb);
-    for (int c = tid; c < KT * C4; c += 256) {
-      const int row = c / C4, col = c % C4;
-      int src = min(tb + row, k_end - 1);
-      bool in = true;
-      if constexpr (GATHER) {
-        // an entry outside the cache reads as a zero row (no offset is formed from it)
-        src = ig[src];
-        in = (uint32_t)src < (uint32_t)p.src_valid;
-        src = in ? src : 0;
-      }
-      const f32x4 kv = *((const f32x4*)(Kb + (int64_t)src * DH) + col);
-      const f32x4 vv = *((const f32x4*)(Vb + (int64_t)src * DH) + col);
-      Ks[c] = in ? kv : f32x4{};
-      Vs[c] = in ? vv : f32x4{};
+  auto compute_tile = [&](int t, int buf) {
+    // S^T: element e of this lane is key 8 (e / 4) + 4 h + e % 4 of the tile, row l32
+    f32x16 sc = {};
+    const float* kr = &Ks[buf][l32 * KPF + h * HALF];
+#pragma unroll
+    for (int s4 = 0; s4 < HALF / 4; ++s4) {
+      const f32x4 kv = *(const f32x4*)(kr + 4 * s4);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) sc = mfma32_f32(kv[u], qv[4 * s4 + u], sc);
     }
-    __syncthreads();
-    for (int kk = 0; kk < nk; ++kk) attend_key(kk, BIAS ? p.bias[(int64_t)g * p.Nk + tb + kk] : 0.f);
+    const bool own_tile = OWN && t >= ct;
+    float mx = -INFINITY;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int kk = 8 * (e >> 2) + 4 * h + (e & 3);
+      float v;
+      if (own_tile) {
+        const int j = (t - ct) * KT + kk;
+        v = (j <= mq && j < p.Ms) ? sc[e] * p.c : -INFINITY;
+      } else {
+        const int key = k_begin + t * KT + kk;
+        v = key < k_end ? fmaf(sc[e], p.c, BIAS ? Bs[buf][kk] : 0.f) : -INFINITY;
+      }
+      sc[e] = v;
+      mx = fmaxf(mx, v);
+    }
+    const float m_new = fmaxf(m_run, pair_max(mx));
+    if (m_new == -INFINITY) {  // every key so far masked (or a -inf bias): no weight
+#pragma unroll
+      for (int e = 0; e < 16; ++e) sc[e] = 0.f;
+    } else {
+      if (m_new > m_run) {
+        const float a = expf(m_run - m_new);
+        l_part *= a;
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt) o[dt] *= a;
+        m_run = m_new;
+      }
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        sc[e] = expf(sc[e] - m_run);
+        l_part += sc[e];
+      }
+    }
+    // O^T += V^T P^T
+#pragma unroll
+    for (int s = 0; s < 16; ++s) {
+      const int kk = 8 * (s >> 2) + 4 * h + (s & 3);
+      const VN vv = *(const VN*)&Vs[buf][kk * DH + ND * l32];
+#pragma unroll
+      for (int dt = 0; dt < ND; ++dt) o[dt] = mfma32_f32(vv[dt], sc[s], o[dt]);
+    }
+  };
+
+  // two slots: tile t + 1's loads are in flight while tile t is multiplied
+  if (ntiles > 0) {
+    load_tile(0);
+    store_tile(0);
     __syncthreads();
   }
-  if (OWN && split == p.n_split - 1) {
-    // own entries 0..m of this thread's query m, up to the workgroup's last query
-    const float* Ksb = (const float*)p.Ks + (int64_t)g * p.Ms * DH;
-    const float* Vsb = (const float*)p.Vs + (int64_t)g * p.Ms * DH;
-    const int last_q = min(p.rows - 1, rt * kRowsF32 + kRowsF32 - 1) / p.G;
-    for (int tb = 0; tb <= last_q; tb += KT) {
-      for (int c = tid; c < KT * C4; c += 256) {
-        const int row = c / C4, col = c % C4;
-        const int src = min(tb + row, p.Ms - 1);
-        Ks[c] = *((const f32x4*)(Ksb + (int64_t)src * DH) + col);
-        Vs[c] = *((const f32x4*)(Vsb + (int64_t)src * DH) + col);
-      }
-      __syncthreads();
-      const int nk = min(KT, m - tb + 1);  // own entries tb .. m of this query
-      for (int kk = 0; kk < nk; ++kk) attend_key(kk, 0.f);
-      __syncthreads();
-    }
+  for (int t = 0; t < ntiles; ++t) {
+    const int buf = t & 1;
+    if (t + 1 < ntiles) load_tile(t + 1);
+    compute_tile(t, buf);
+    if (t + 1 < ntiles) store_tile(buf ^ 1);
+    __syncthreads();
   }
 
   if (r >= p.rows) return;
+  const float l = pair_sum(l_part);
+  // element e of tile dt is channel ND (8 (e / 4) + 4 h + e % 4) + dt
   if constexpr (!PARTIAL) {
     const float inv = 1.0f / l;
-    f32x4* op = (f32x4*)(p.O + ((int64_t)m * p.Hq + g * p.G + j) * DH);
+    float* op = p.O + ((int64_t)mq * p.Hq + g * p.G + jq) * DH;
 #pragma unroll
-    for (int i = 0; i < C4; ++i) op[i] = o[i] * inv;
+    for (int e = 0; e < 16; ++e) {
+      VN v;
+#pragma unroll
+      for (int dt = 0; dt < ND; ++dt) v[dt] = o[dt][e] * inv;
+      *(VN*)(op + ND * (8 * (e >> 2) + 4 * h + (e & 3))) = v;
+    }
   } else {
     const int64_t rid = ((int64_t)(g * p.n_split + split)) * p.rows + r;
-    f32x4* op = (f32x4*)(p.Opart + rid * DH);
+    float* op = p.Opart + rid * DH;
 #pragma unroll
-    for (int i = 0; i < C4; ++i) op[i] = o[i];
-    p.ML[2 * rid] = mrun;
-    p.ML[2 * rid + 1] = l;
+    for (int e = 0; e < 16; ++e) {
+      VN v;
+#pragma unroll
+      for (int dt = 0; dt < ND; ++dt) v[dt] = o[dt][e];
+      *(VN*)(op + ND * (8 * (e >> 2) + 4 * h + (e & 3))) = v;
+    }
+    if (h == 0) {
+      p.ML[2 * rid] = m_run;
+      p.ML[2 * rid + 1] = l;
+    }
   }
 }
 
@@ -1068,10 +1172,11 @@ hipError_t run_attention(const AttnShape& s, const AttnPlan& pl, AttnParams& p, 
 #undef PKV_L
 #undef PKV_LB
   } else if constexpr (KQ == 0) {
+    const dim3 fblock(kF32Waves * 64);
 #define PKV_L(G_, S_, O_)                                                                         \
   do {                                                                                            \
-    if (bias) hipLaunchKernelGGL((attn_f32_kernel<DH, G_, S_, false, true>), grid, block, 0, st, p); \
-    else hipLaunchKernelGGL((attn_f32_kernel<DH, G_, S_, O_, false>), grid, block, 0, st, p);       \
+    if (bias) hipLaunchKernelGGL((attn_f32_kernel<DH, G_, S_, false, true>), grid, fblock, 0, st, p); \
+    else hipLaunchKernelGGL((attn_f32_kernel<DH, G_, S_, O_, false>), grid, fblock, 0, st, p);       \
   } while (0)
     if (own) {
       if (gather) { if (part) PKV_L(true, true, true); else PKV_L(true, false, true); }
