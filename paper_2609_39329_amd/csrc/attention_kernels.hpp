@@ -531,7 +531,10 @@ __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnP
     }
   };
   // P = exp2(S c - m_run) as bf16 MFMA operands (two-term split when PSPLIT). The row
-  // sums add up the bf16 values the MFMA actually uses (v_dot2 with (1, 1)).
+  // sums add up the bf16 values the MFMA actually uses (v_dot2 with (1, 1)), from the
+  // same packed pairs: one v_cvt_pk_bf16_f32 per pair serves both (converted element by
+  // element, the compiler repacked the pairs for the sums with extra conversions and
+  // permutes).
   auto softmax = [&](f32x16 (&s)[NKT][QT], bf16x8 (&pb)[NKT][QT][2], bf16x8 (&pl)[NKT][QT][2]) {
     const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 #pragma unroll
@@ -543,21 +546,27 @@ __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnP
         for (int e = 0; e < 16; ++e) s[kt][qt][e] = fast_exp2(fmaf(s[kt][qt][e], c, nm));
         float sum0 = 0.f, sum1 = 0.f;
 #pragma unroll
-        for (int p2 = 0; p2 < 2; ++p2)
+        for (int p2 = 0; p2 < 2; ++p2) {
+          u32x4 hw, lw = {};
 #pragma unroll
           for (int e = 0; e < 8; e += 2) {
             const float v0 = s[kt][qt][8 * p2 + e], v1 = s[kt][qt][8 * p2 + e + 1];
-            const bf16x2 h = {to_bf16(v0), to_bf16(v1)};
-            pb[kt][qt][p2][e] = h[0];
-            pb[kt][qt][p2][e + 1] = h[1];
-            sum0 = __builtin_amdgcn_fdot2_f32_bf16(h, ones, sum0, false);
+            const unsigned hp = pack_bf16(v0, v1);
+            hw[e / 2] = hp;
+            sum0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, hp), ones, sum0,
+                                                   false);
             if constexpr (PSPLIT) {
-              const bf16x2 lo = {to_bf16(v0 - (float)h[0]), to_bf16(v1 - (float)h[1])};
-              pl[kt][qt][p2][e] = lo[0];
-              pl[kt][qt][p2][e + 1] = lo[1];
-              sum1 = __builtin_amdgcn_fdot2_f32_bf16(lo, ones, sum1, false);
+              const float h0 = __builtin_bit_cast(float, hp << 16);
+              const float h1 = __builtin_bit_cast(float, hp & 0xffff0000u);
+              const unsigned lp = pack_bf16(v0 - h0, v1 - h1);
+              lw[e / 2] = lp;
+              sum1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, lp), ones, sum1,
+                                                     false);
             }
           }
+          pb[kt][qt][p2] = __builtin_bit_cast(bf16x8, hw);
+          if constexpr (PSPLIT) pl[kt][qt][p2] = __builtin_bit_cast(bf16x8, lw);
+        }
         l_part[qt] += sum0 + sum1;
       }
   };
@@ -621,7 +630,8 @@ __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnP
     // entries, from their own buffers)
     auto issue = [&](int tile, auto slot_t) {
       constexpr int SL = decltype(slot_t)::value;
-      if (wid >= kDmaWaves) return;
+      // a scalar branch (wid is wave-uniform)
+      if (__builtin_amdgcn_readfirstlane(wid) >= kDmaWaves) return;
 #pragma unroll
       for (int i = 0; i < LPD; ++i) {
         // a wave's DMA instruction writes its 64 lanes' chunks to 1 KB of consecutive LDS
@@ -694,6 +704,11 @@ __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnP
       bf16x8 pl[NKT][QT][2];
       softmax(sc, pb, pl);
       pv_d(pb, std::integral_constant<int, I % NSL>{});
+      // the row sums are complete at the end of each step: left free, the compiler sank
+      // every step's sums to the end of the unrolled loop, holding all eight tiles' P
+      // registers live (256 VGPRs against 202, 4 % slower)
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt) asm volatile("" : "+v"(l_part[qt]));
       // a barrier after every kDmaSteps steps: the next group reads up to tile
       // t + kDmaSteps + 1, and 2 (D - kDmaSteps - 1) loads of later tiles may be in flight
       if constexpr (I % kDmaSteps == kDmaSteps - 1)

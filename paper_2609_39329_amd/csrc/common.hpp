@@ -83,11 +83,11 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 __device__ __forceinline__ __bf16 to_bf16(float x) { return (__bf16)x; }
 
 // bf16(a) in the low half and bf16(b) in the high half of a dword, rounded to nearest
-// even, in one v_cvt_pk_bf16_f32 (the compiler emits one per element otherwise)
-__device__ __forceinline__ unsigned cvt_pk_bf16(float a, float b) {
-  unsigned r;
-  asm("v_cvt_pk_bf16_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
-  return r;
+// even: one v_cvt_pk_bf16_f32, selected by the compiler (which then also inserts the
+// wait states an MFMA reading the result needs; an inline-asm conversion hides the
+// write from its hazard checks)
+__device__ __forceinline__ unsigned pack_bf16(float a, float b) {
+  return __builtin_bit_cast(unsigned, __builtin_convertvector(f32x2{a, b}, bf16x2));
 }
 
 __device__ __forceinline__ bf16x8 load_bf16x8(const __bf16* p) {

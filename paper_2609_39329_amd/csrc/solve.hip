@@ -255,7 +255,7 @@ __device__ __forceinline__ void split_store(__bf16* const (&pl)[NP], int off, f3
   f32x4 r = v;
 #pragma unroll
   for (int q = 0; q < NP; ++q) {
-    const unsigned h01 = cvt_pk_bf16(r[0], r[1]), h23 = cvt_pk_bf16(r[2], r[3]);
+    const unsigned h01 = pack_bf16(r[0], r[1]), h23 = pack_bf16(r[2], r[3]);
     *(u32x2*)(pl[q] + off) = u32x2{h01, h23};
     if (q + 1 < NP) {
       r[0] -= __builtin_bit_cast(float, h01 << 16);
