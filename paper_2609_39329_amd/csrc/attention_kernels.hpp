@@ -567,7 +567,9 @@ __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnP
           pb[kt][qt][p2] = __builtin_bit_cast(bf16x8, hw);
           if constexpr (PSPLIT) pl[kt][qt][p2] = __builtin_bit_cast(bf16x8, lw);
         }
-        l_part[qt] += sum0 + sum1;
+        // (sum1 only with a two-term P: sum0 + 0 would cost an add the compiler keeps)
+        if constexpr (PSPLIT) l_part[qt] += sum0 + sum1;
+        else l_part[qt] += sum0;
       }
   };
   // O^T += V^T P^T with the V^T tile of LDS slot `buf`: the A operand (32 rows of d,
