@@ -20,9 +20,9 @@
 // to a lazily rescaled pass for work items whose scores outgrow it. On the main
 // path K/V^T tiles go from HBM straight into eight LDS slots (buffer_load ... lds, no
 // register staging; issued by waves 0-3 only), six tiles ahead, with XOR-swizzled
-// 16-byte chunks in place of row padding and one barrier per two tiles; the
-// gathering, biased, two-term-P and block-scaled variants stage through registers into
-// four padded slots. The workgroup -> work-item
+// 16-byte chunks in place of row padding and one barrier per two tiles (also with a
+// two-term P); the gathering, biased and block-scaled variants stage through registers
+// into four padded slots. The workgroup -> work-item
 // map keeps all row tiles of one KV head (and key range) on one XCD so its L2
 // serves the K/V re-reads.
 //
@@ -238,10 +238,11 @@ __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnP
   constexpr int NT = kThreadsBf16;
   constexpr int NCH = KT * CH;             // 16-byte chunks per K tile (= per V^T tile)
   constexpr int LPT = (NCH + NT - 1) / NT;  // chunks per thread
-  // DMA: the plain fast path streams K / V^T tiles straight into LDS (no register
-  // staging), through kDmaSlots unpadded slots whose 16-byte chunks are XOR-swizzled
-  // so that the MFMA operand reads stay conflict-free
-  constexpr bool DMA = kAttnDma && !SAFE && !GATHER && !BIAS && !PSPLIT && KQ == 0;
+  // DMA: the fast path over contiguous bf16 K (one- or two-term P) streams K / V^T
+  // tiles straight into LDS (no register staging), through kDmaSlots unpadded slots
+  // whose 16-byte chunks are XOR-swizzled so that the MFMA operand reads stay
+  // conflict-free
+  constexpr bool DMA = kAttnDma && !SAFE && !GATHER && !BIAS && KQ == 0;
   // stored K rows: bf16, or int8 / packed int4 values (KRB bytes per row, KCB bytes per
   // 8-channel chunk) with DH / 32 exponent bytes
   constexpr int KCB = KQ ? KQ : 16;
@@ -668,7 +669,7 @@ __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnP
         for (int qt = 0; qt < QT; ++qt) s[0][qt] = mfma32(a, qf[qt][st], s[0][qt]);
       }
     };
-    auto pv_d = [&](bf16x8 (&pb)[NKT][QT][2], auto slot_t) {
+    auto pv_d = [&](bf16x8 (&pb)[NKT][QT][2], bf16x8 (&pl)[NKT][QT][2], auto slot_t) {
       constexpr int SL = decltype(slot_t)::value;
 #pragma unroll
       for (int p2 = 0; p2 < 2; ++p2)
@@ -677,10 +678,13 @@ __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnP
           const bf16x8 a =
               *(const bf16x8*)(&Vd[SL][(dt * 32 + l32) * 32 + (((2 * p2 + h32) ^ swv) * 8)]);
 #pragma unroll
-          for (int qt = 0; qt < QT; ++qt) o[qt][dt] = mfma32(a, pb[0][qt][p2], o[qt][dt]);
+          for (int qt = 0; qt < QT; ++qt) {
+            o[qt][dt] = mfma32(a, pb[0][qt][p2], o[qt][dt]);
+            if constexpr (PSPLIT) o[qt][dt] = mfma32(a, pl[0][qt][p2], o[qt][dt]);
+          }
         }
     };
-    static_assert(NKT == 1 && !PSPLIT, "DMA path: one 32-key MFMA tile, one-term P");
+    static_assert(NKT == 1, "DMA path: one 32-key MFMA tile");
     static_for<D>([&](auto j_t) { issue(decltype(j_t)::value, j_t); });
     // tiles 0 .. kDmaSteps resident
     sync_slots(std::integral_constant<int, 2 * LPD * (D - kDmaSteps - 1)>{});
@@ -705,7 +709,7 @@ __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnP
       bf16x8 pb[NKT][QT][2];
       bf16x8 pl[NKT][QT][2];
       softmax(sc, pb, pl);
-      pv_d(pb, std::integral_constant<int, I % NSL>{});
+      pv_d(pb, pl, std::integral_constant<int, I % NSL>{});
       // the row sums are complete at the end of each step: left free, the compiler sank
       // every step's sums to the end of the unrolled loop, holding all eight tiles' P
       // registers live (256 VGPRs against 202, 4 % slower)
