@@ -47,7 +47,9 @@ def _tol(X, lam, products):
     X64 = X.astype(np.float64)
     s = np.linalg.svd(X64, compute_uv=False)
     s = s[s > s[0] * 1e-7] if s[0] > 0 else np.ones(1)
-    kappa = (s[0] ** 2 + lam) / (s[-1] ** 2 + lam)
+    # K = X X^T has rows - rank(X) zero eigenvalues: then lambda is the smallest of K + lambda I
+    smin2 = s[-1] ** 2 if len(s) == X.shape[0] else 0.0
+    kappa = (s[0] ** 2 + lam) / (smin2 + lam)
     stretch = s[0] / s[-1]
     per = 2.0 ** -16 if products != "split3" else 2.0 ** -14
     return max(1e-4, kappa * stretch * per)
