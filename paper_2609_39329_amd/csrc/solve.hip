@@ -841,6 +841,83 @@ __device__ __forceinline__ double bcast(double x, int src_lane) {
 __device__ __forceinline__ float rsq_of(float x) { return __builtin_amdgcn_rsqf(x); }
 __device__ __forceinline__ double rsq_of(double x) { return rsq64(x); }
 
+// Row G's value at each lane's position in its 16-lane row: permlane16_swap gives rows
+// (0, 0, 2, 2) and (1, 1, 3, 3), permlane32_swap of that gives its lower (or upper) half
+// twice.
+template <int G>
+__device__ __forceinline__ float from_row(float x) {
+  const unsigned u = __builtin_bit_cast(unsigned, x);
+  const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  const unsigned y = (G & 1) ? a[1] : a[0];
+  const auto b = __builtin_amdgcn_permlane32_swap(y, y, false, false);
+  return __builtin_bit_cast(float, (G & 2) ? b[1] : b[0]);
+}
+// lane J of each 16-lane row, to the whole row (DPP row_newbcast)
+template <int J>
+__device__ __forceinline__ float row_lane(float x) {
+  return __builtin_bit_cast(float,
+                            __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0x150 + J, 0xF, 0xF, false));
+}
+
+// The fp32 16-wide leaf on all 64 lanes: lane 16 q + r holds columns 4 k + q (k < 4) of
+// row r of the trailing matrix (v) and of Y (x), the block symmetrised from its lower
+// triangle on load. Step j, with pivot p = A_jj and u_r = A_rj / p (r > j, else 0):
+//   A_rc -= u_r A_jc for c > j (A_jc = A_cj: the trailing matrix stays symmetric), row j
+//     of the lane's column group through a DPP broadcast of lane j;
+//   Y_rm -= u_r Y_jm for m <= j, the same way;
+// A_rj itself comes from column group j % 4 through two lane-row swaps, the pivot through
+// one readlane. A lane updates its 4 - j/4 (and j/4 + 1) columns instead of all 16, so a
+// step takes about a third of the instructions of the row-per-lane sweep below.
+__device__ __forceinline__ void leaf16_groups(float* S, float* Xo, int lane, int col0, int bs,
+                                              int32_t* info, bool& failed) {
+  constexpr int PT = diag_pitch<float>();
+  int q = lane >> 4, r = lane & 15;
+  asm volatile("" : "+v"(q), "+v"(r));
+  float v[4], x[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int c = 4 * k + q;
+    v[k] = c > r ? S[c * PT + r] : S[r * PT + c];
+    x[k] = c == r ? 1.f : 0.f;
+  }
+  float rs_own = 0.f;
+  static_for<16>([&](auto j_t) {
+    constexpr int j = decltype(j_t)::value, jq = j % 4, jk = j / 4;
+    const float rs = rsq_of(bcast(v[jk], 16 * jq + j));
+    const float a = from_row<jq>(v[jk]);  // on every lane: the swaps are wave-wide
+    const float u = r > j ? a * (rs * rs) : 0.f;  // A[r][j] / p
+    if (r == j) rs_own = rs;
+    static_for<4 - jk>([&](auto kk_t) {  // columns 4 k + q > j
+      constexpr int k = jk + decltype(kk_t)::value;
+      const float uk = (k > jk || q > jq) ? u : 0.f;
+      v[k] = fmaf(-uk, row_lane<j>(v[k]), v[k]);
+    });
+    static_for<jk + 1>([&](auto k_t) {  // columns 4 k + q <= j
+      constexpr int k = decltype(k_t)::value;
+      const float uk = (k < jk || q <= jq) ? u : 0.f;
+      x[k] = fmaf(-uk, row_lane<j>(x[k]), x[k]);
+    });
+    if (q == jq) v[jk] *= rs;  // column j of L
+  });
+  // first failing pivot (padding pivots past bs are 1): row r's diagonal sits in group r % 4
+  float dg = v[0];
+#pragma unroll
+  for (int k = 1; k < 4; ++k)
+    if (k == (r >> 2)) dg = v[k];
+  const uint64_t bad = __ballot(q == (r & 3) && col0 + r < bs && !(dg > 0.f));
+  const unsigned rows = (unsigned)(bad | bad >> 16 | bad >> 32 | bad >> 48) & 0xFFFFu;
+  if (rows != 0 && !failed) {
+    failed = true;
+    if (lane == 0 && *info == 0) *info = col0 + __builtin_ctz(rows) + 1;
+  }
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int c = 4 * k + q;
+    S[r * PT + c] = v[k];             // row r of L (upper part unused)
+    Xo[r * PT + c] = x[k] * rs_own;   // row r of X (zeros above the diagonal)
+  }
+}
+
 // One wave: factor the SPD N x N block S (lower triangle read) and write
 // X = L^{-1} (lower, zeros above) to Xo, in one right-looking sweep.
 // Lane r (and its copies r + N, r + 2N, .., which repeat the same work so the wave
@@ -859,6 +936,10 @@ template <int N, class T>
 __device__ __forceinline__ void leaf(T* S, T* Xo, int lane, int col0, int bs, int32_t* info,
                                      bool& failed) {
   static_assert(N == 16 || N == 32, "leaf width");
+  if constexpr (N == 16 && sizeof(T) == 4) {
+    leaf16_groups(S, Xo, lane, col0, bs, info, failed);
+    return;
+  }
   constexpr int PT = diag_pitch<T>();
   int r = lane & (N - 1);
   // opaque per call: keeps the per-step lane comparisons inside the call instead of
