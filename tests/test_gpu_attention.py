@@ -32,6 +32,7 @@ SHAPES = [
     (128, 2048, 256, 4, 2, 64, "f32"),      # tiny fp32 layer shape
     (50, 333, 100, 8, 2, 128, "f32"),
     (8, 20000, 3000, 4, 2, 64, "f32"),      # fp32 split-key path
+    (300, 3000, 700, 16, 4, 128, "f32"),    # fp32 MFMA kernel: several row tiles per head, ragged tail
     (1, 1, 1, 4, 2, 64, "bf16"),            # degenerate: one query, one key, one entry
     # one row tile per KV head: the keys split into 32-key ranges, the last one 8 (9)
     # keys long, so a work item's first tile is already past its range's end
