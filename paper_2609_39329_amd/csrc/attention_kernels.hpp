@@ -21,8 +21,9 @@
 // path K/V^T tiles go from HBM straight into eight LDS slots (buffer_load ... lds, no
 // register staging; issued by waves 0-3 only), six tiles ahead, with XOR-swizzled
 // 16-byte chunks in place of row padding and one barrier per two tiles (also with a
-// two-term P); the gathering, biased and block-scaled variants stage through registers
-// into four padded slots. The workgroup -> work-item
+// two-term P; block-scaled keys come through registers into the same slots, V^T by
+// DMA); the gathering and biased variants stage through registers into four padded
+// slots. The workgroup -> work-item
 // map keeps all row tiles of one KV head (and key range) on one XCD so its L2
 // serves the K/V re-reads.
 //
@@ -48,9 +49,9 @@
 //
 // Block-scaled integer caches (KQ = 8 or 4; App. C, quantized KV caches): K and V
 // hold int8 (or packed int4) values with one power-of-two exponent per 32 channels.
-// The register-staged loads fetch the stored bytes and expand each 8-channel chunk
-// to bf16 when the tile is stored to LDS; vt_kernel expands V on its way into the V^T
-// tiles. The expansion is exact, so the arithmetic after it is that of a bf16 cache.
+// Register loads fetch the stored K bytes and expand each 8-channel chunk to bf16 when
+// the tile is stored to LDS; vt_kernel expands V on its way into the V^T tiles. The
+// expansion is exact, so the arithmetic after it is that of a bf16 cache.
 #pragma once
 
 #include <math.h>
@@ -242,7 +243,7 @@ __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnP
   // tiles straight into LDS (no register staging), through kDmaSlots unpadded slots
   // whose 16-byte chunks are XOR-swizzled so that the MFMA operand reads stay
   // conflict-free
-  constexpr bool DMA = kAttnDma && !SAFE && !GATHER && !BIAS && KQ == 0;
+  constexpr bool DMA = kAttnDma && !SAFE && !GATHER && !BIAS;
   // stored K rows: bf16, or int8 / packed int4 values (KRB bytes per row, KCB bytes per
   // 8-channel chunk) with DH / 32 exponent bytes
   constexpr int KCB = KQ ? KQ : 16;
@@ -646,7 +647,9 @@ __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnP
           __builtin_amdgcn_raw_ptr_buffer_load_lds(vtsrs, vd, 16, voff[i] + (j0 / 32) * (DH * 64), 0, 0, 0);
         } else {
           const uint32_t kb0 = (uint32_t)(k_begin + tile * KT);
-          __builtin_amdgcn_raw_ptr_buffer_load_lds(krs, kd, 16, koff[i] + kb0 * (DH * 2), 0, 0, 0);
+          // (block-scaled keys come through registers, kq_load / kq_store)
+          if constexpr (KQ == 0)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(krs, kd, 16, koff[i] + kb0 * (DH * 2), 0, 0, 0);
           __builtin_amdgcn_raw_ptr_buffer_load_lds(vrs, vd, 16, voff[i] + (kb0 / 32) * (DH * 64), 0, 0, 0);
         }
       }
@@ -685,9 +688,58 @@ __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnP
         }
     };
     static_assert(NKT == 1, "DMA path: one 32-key MFMA tile");
+    // Block-scaled keys (KQ): V^T tiles (expanded by vt_kernel) still arrive by DMA; the
+    // stored K bytes are loaded by every thread (chunk c = u * NT + tid) three steps before
+    // their LDS store, in four register sets, and expanded at the store into the slot's
+    // swizzled layout. Step t stores K tile t + 3 (read at step t + 2, after a barrier) and
+    // loads tile t + 6.
+    constexpr int LPK = (NCH + NT - 1) / NT;
+    constexpr int KSETS = 4, KLEAD = 3;
+    static_assert(KQ == 0 || (NSL % KSETS == 0 && KLEAD + 3 <= D + 1), "K register sets");
+    u32x4 kq[KQ ? KSETS : 1][LPK];
+    auto kq_load = [&](int tile, auto set_t) {
+      if constexpr (KQ != 0) {
+        constexpr int SET = decltype(set_t)::value;
+        const int kb0 = k_begin + tile * KT;
+#pragma unroll
+        for (int u = 0; u < LPK; ++u) {
+          const int cc = u * NT + tid;
+          if (NCH % NT != 0 && cc >= NCH) break;
+          kq[SET][u] = kload((uint32_t)kb0 * KRB + cc * KCB, (uint32_t)kb0 * (DH / 32) + cc / 4);
+        }
+      }
+    };
+    auto kq_store = [&](auto set_t, auto slot_t) {
+      if constexpr (KQ != 0) {
+        constexpr int SET = decltype(set_t)::value, SL = decltype(slot_t)::value;
+#pragma unroll
+        for (int u = 0; u < LPK; ++u) {
+          const int cc = u * NT + tid;
+          if (NCH % NT != 0 && cc >= NCH) break;
+          const int row = cc / CH, pos = row * CH + ((cc % CH) ^ ((row / RPB) % CH));
+          *(u32x4*)(&Kd[SL][pos * 8]) = kexpand(kq[SET][u]);
+        }
+      }
+    };
+    // loads a wave may leave in flight at a barrier (V^T tiles t + 4 .. t + 6 and, with
+    // block-scaled keys, the K loads issued after V^T tile t + 3)
+    constexpr int KLI = KQ ? 2 : 0;  // loads per kq_load (values, exponent)
+    constexpr int INFL = KQ ? KLI + 3 * (LPD + KLI) : 2 * LPD * (D - kDmaSteps - 1);
     static_for<D>([&](auto j_t) { issue(decltype(j_t)::value, j_t); });
+    if constexpr (KQ != 0) {
+      static_assert(D == 6 && kDmaSteps == 2, "the K schedule assumes six tiles ahead");
+      kq_load(0, std::integral_constant<int, 0>{});
+      kq_load(1, std::integral_constant<int, 1>{});
+      kq_load(2, std::integral_constant<int, 2>{});
+      kq_store(std::integral_constant<int, 0>{}, std::integral_constant<int, 0>{});
+      kq_store(std::integral_constant<int, 1>{}, std::integral_constant<int, 1>{});
+      kq_store(std::integral_constant<int, 2>{}, std::integral_constant<int, 2>{});
+      kq_load(3, std::integral_constant<int, 3>{});
+      kq_load(4, std::integral_constant<int, 0>{});
+      kq_load(5, std::integral_constant<int, 1>{});
+    }
     // tiles 0 .. kDmaSteps resident
-    sync_slots(std::integral_constant<int, 2 * LPD * (D - kDmaSteps - 1)>{});
+    sync_slots(std::integral_constant<int, INFL>{});
     f32x16 sa[NKT][QT], sb[NKT][QT];
     scores_d(sa, std::integral_constant<int, 0>{});
     mask(sa, 0);  // a key range shorter than one tile
@@ -704,6 +756,8 @@ __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnP
       constexpr int I = decltype(i_t)::value;
       constexpr bool MASKED = decltype(masked_t)::value;
       issue(t + D, std::integral_constant<int, (I + D) % NSL>{});
+      kq_store(std::integral_constant<int, (I + 3) % KSETS>{}, std::integral_constant<int, (I + 3) % NSL>{});
+      kq_load(t + 3 + KLEAD, std::integral_constant<int, (I + 3 + KLEAD) % KSETS>{});
       scores_d(sn, std::integral_constant<int, (I + 1) % NSL>{});
       if constexpr (MASKED) mask(sn, t + 1);
       bf16x8 pb[NKT][QT][2];
@@ -717,8 +771,7 @@ __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnP
       for (int qt = 0; qt < QT; ++qt) asm volatile("" : "+v"(l_part[qt]));
       // a barrier after every kDmaSteps steps: the next group reads up to tile
       // t + kDmaSteps + 1, and 2 (D - kDmaSteps - 1) loads of later tiles may be in flight
-      if constexpr (I % kDmaSteps == kDmaSteps - 1)
-        sync_slots(std::integral_constant<int, 2 * LPD * (D - kDmaSteps - 1)>{});
+      if constexpr (I % kDmaSteps == kDmaSteps - 1) sync_slots(std::integral_constant<int, INFL>{});
     };
     auto steps = [&](auto masked_t, int t) {
       static_for<NSL / 2>([&](auto h_t) {
