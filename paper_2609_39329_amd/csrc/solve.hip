@@ -866,8 +866,9 @@ __device__ __forceinline__ float row_lane(float x) {
 //     of the lane's column group through a DPP broadcast of lane j;
 //   Y_rm -= u_r Y_jm for m <= j, the same way;
 // A_rj itself comes from column group j % 4 through two lane-row swaps, the pivot through
-// one readlane. A lane updates its 4 - j/4 (and j/4 + 1) columns instead of all 16, so a
-// step takes about a third of the instructions of the row-per-lane sweep below.
+// one readlane. A lane updates its 4 - j/4 (and j/4 + 1) columns instead of all 16; with
+// the broadcasts (separate DPP moves, not fused into the FMAs) and their wait states a
+// step takes about 30 instructions against 36 for the row-per-lane sweep below.
 __device__ __forceinline__ void leaf16_groups(float* S, float* Xo, int lane, int col0, int bs,
                                               int32_t* info, bool& failed) {
   constexpr int PT = diag_pitch<float>();
@@ -933,13 +934,9 @@ __device__ __forceinline__ void leaf16_groups(float* S, float* Xo, int lane, int
 // makes its L_jj, and every later one, NaN: the first NaN on the diagonal is the
 // failing column.
 template <int N, class T>
-__device__ __forceinline__ void leaf(T* S, T* Xo, int lane, int col0, int bs, int32_t* info,
-                                     bool& failed) {
+__device__ __forceinline__ void leaf_rows(T* S, T* Xo, int lane, int col0, int bs, int32_t* info,
+                                          bool& failed) {
   static_assert(N == 16 || N == 32, "leaf width");
-  if constexpr (N == 16 && sizeof(T) == 4) {
-    leaf16_groups(S, Xo, lane, col0, bs, info, failed);
-    return;
-  }
   constexpr int PT = diag_pitch<T>();
   int r = lane & (N - 1);
   // opaque per call: keeps the per-step lane comparisons inside the call instead of
@@ -1005,6 +1002,14 @@ __device__ __forceinline__ void leaf(T* S, T* Xo, int lane, int col0, int bs, in
       Xo[r * PT + c] = x[c] * rs_own;  // row r of X (zeros above the diagonal)
     }
   }
+}
+
+// the fp32 16-wide leaf on four column groups, every other on the row-per-lane sweep
+template <int N, class T>
+__device__ __forceinline__ void leaf(T* S, T* Xo, int lane, int col0, int bs, int32_t* info,
+                                     bool& failed) {
+  if constexpr (N == 16 && sizeof(T) == 4) leaf16_groups(S, Xo, lane, col0, bs, info, failed);
+  else leaf_rows<N>(S, Xo, lane, col0, bs, info, failed);
 }
 
 constexpr int kPotrfWaves = 8;  // 8 waves: the next leaf overlaps the trailing products
