@@ -46,7 +46,8 @@ def traffic_profile(cfg) -> str:
 
 
 def measured_traffic(cfg):
-    """HBM bytes per full-cache attention launch (V^T pre-pass, fast path and fixup)
+    """HBM bytes per full-cache attention launch (fast path and fixup, and the V^T
+    pre-pass of a call that runs one)
     from the committed counter summary of this workload (FETCH_SIZE and WRITE_SIZE,
     calibrated on a plain copy; written by profile_summary.py), or None when there is
     none or a kernel source changed since the counters were taken."""
@@ -414,7 +415,9 @@ def main():
                                  "patchkv_attend_cache (full cache, two-term P: 1.5x the MFMA "
                                  "work of the algorithmic flops counted here)"
                                  if cfg.teacher_p_terms == 2 else "patchkv_attend_full")
-                                + (": vt_kernel + attn_bf16_kernel fast path + fixup"
+                                + ((": vt_kernel (V^T tiles of the cache and own entries) + "
+                                    "attn_bf16_kernel fast path + fixup" if chunked else
+                                    ": attn_bf16_kernel fast path (V tiles as stored) + fixup")
                                    if cfg.dtype == "bf16" else ": attn_f32_kernel")),
                      "flops_per_launch": att_flops_full,
                      "traffic_unit": "HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)",

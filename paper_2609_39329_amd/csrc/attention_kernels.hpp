@@ -12,13 +12,15 @@
 // Each wave keeps its rows of Q in registers and computes S^T = K Q^T on bf16 MFMA
 // 32x32x16 (keys along the MFMA rows, queries along its columns), so a lane owns
 // one query and softmax statistics need only one cross-lane exchange (lane l with
-// l^32). P stays in registers and feeds O^T += V^T P^T directly. V is first
-// rewritten by vt_kernel into 32-key tiles of V^T whose key order matches the
-// P fragments' k-slots, so the V operand is one 16-byte LDS read (the transposing
-// LDS read delivers about a third of the bandwidth). The online softmax runs in
+// l^32). P stays in registers and feeds O^T += V^T P^T directly. A contiguous cache's
+// V tiles go to LDS as stored, in 64-byte rows of 32 channels, and each V operand is
+// two transposing LDS reads (ds_read_b64_tr_b16) over four consecutive rows. Gathered,
+// block-scaled, biased and own-entry caches are first rewritten by vt_kernel into
+// 32-key tiles of V^T whose key order matches the P fragments' k-slots, so there the
+// V operand is one 16-byte LDS read. The online softmax runs in
 // fp32 in the exp2 domain with a fixed per-row offset (fast path) and falls back
 // to a lazily rescaled pass for work items whose scores outgrow it. On the main
-// path K/V^T tiles go from HBM straight into eight LDS slots (buffer_load ... lds, no
+// path K and V (or V^T) tiles go from HBM straight into eight LDS slots (buffer_load ... lds, no
 // register staging; issued by waves 0-3 only), six tiles ahead, with XOR-swizzled
 // 16-byte chunks in place of row padding and one barrier per two tiles (also with a
 // two-term P; block-scaled keys come through registers into the same slots, V^T by
@@ -105,6 +107,16 @@ namespace {
 
 constexpr float kTau = 8.0f;   // lazy-rescale threshold of the fixup path (log2 units)
 constexpr float kBigSum = 0x1p64f;  // fast path: largest trusted partial row sum (2^kBig, kBig = 64)
+
+// A partial row sum the fast path cannot trust: above kBigSum, infinite or NaN (an
+// overflowing weight gives inf, and inf - inf = NaN in a two-term P's low piece). The
+// test is on the bit pattern: these kernels are built without NaN semantics, and a
+// floating-point !(l <= kBigSum) compiled to kBigSum < l, which NaN passes. Sums are
+// non-negative, so a larger pattern is a larger value, inf or NaN (a sign bit, which no
+// sum has, counts as untrusted too).
+__device__ __forceinline__ bool untrusted_sum(float l) {
+  return __builtin_bit_cast(uint32_t, l) > __builtin_bit_cast(uint32_t, kBigSum);
+}
 constexpr int kKeyTile = 32;  // keys per iteration, bf16 path
 constexpr int kRowsBf16 = 256;  // query rows per workgroup, bf16 path
 constexpr int kRowsF32 = 256;   // query rows per workgroup, f32 path (32 per wave)
@@ -223,10 +235,15 @@ __global__ __launch_bounds__(256) void vt_kernel(const void* __restrict__ V,
 // KQ = 8 or 4: K holds block-scaled integers (exponents in p.Ke), loaded as such and
 // expanded to bf16 when the tile is stored to LDS (register-staged path); V was
 // expanded by vt_kernel into the V^T tiles.
-template <int DH, bool GATHER, bool PSPLIT, bool PARTIAL, bool SAFE, bool OWN, bool BIAS, int KQ>
+// VNAT (contiguous bf16 cache, every row of it used): no V^T tiles; V tiles arrive in
+// their stored [key][d] order and the P V product reads its V operand with transposing
+// LDS reads (see vfrag).
+template <int DH, bool GATHER, bool PSPLIT, bool PARTIAL, bool SAFE, bool OWN, bool BIAS, int KQ,
+          bool VNAT>
 __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnParams p) {
   static_assert(!(OWN && BIAS), "own entries carry no bias");
   static_assert(KQ == 0 || KQ == 8 || KQ == 4, "bf16, int8 or int4 keys");
+  static_assert(!VNAT || (!GATHER && !OWN && !BIAS && KQ == 0), "V tiles of a contiguous bf16 cache");
   static_assert(!(OWN && KQ), "own entries are bf16");
   constexpr int KT = kKeyTile;
   constexpr int NKT = KT / 32;  // 32-key MFMA tiles per iteration
@@ -327,9 +344,25 @@ __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnP
   const uint32_t head_bytes = (uint32_t)(p.src_rows * KRB);
   const __amdgpu_buffer_rsrc_t krs =
       __builtin_amdgcn_make_buffer_rsrc((void*)Kb, 0, head_bytes, 0x00020000);
-  const __bf16* Vtg = p.Vt + (int64_t)g * p.vt_tiles * DH * 32;
-  const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)Vtg, 0, (uint32_t)p.vt_tiles * (DH * 32 * 2), 0x00020000);
+  // V^T tiles of this KV head, or (VNAT) its V rows as stored
+  const __amdgpu_buffer_rsrc_t vrs =
+      VNAT ? __builtin_amdgcn_make_buffer_rsrc((void*)((const char*)p.V + (int64_t)g * p.src_rows * (DH * 2)),
+                                               0, head_bytes, 0x00020000)
+           : __builtin_amdgcn_make_buffer_rsrc((void*)(p.Vt + (int64_t)g * p.vt_tiles * DH * 32), 0,
+                                               (uint32_t)p.vt_tiles * (DH * 32 * 2), 0x00020000);
+  // A V tile in LDS (VNAT) is DH / 32 sub-tiles [dt][key][32 channels], 64-byte rows:
+  // 16-byte chunk c of the stored tile (key c / CH, channels 8 (c % CH) ..) sits at
+  // chunk position vnat_pos(c). The P V product's operand for channels dt * 32 + l32 and
+  // the 8 keys of a P fragment (16 p2 + 4 h32 + {0..3}, then + 8) is two transposing
+  // reads: in each 16-lane group, lane 4r + q points at key row r, channels 4q .. 4q + 3
+  // of a 4 x 16 block, and lane j receives channel j of the block's 4 keys. A half-wave
+  // reads 4 consecutive 64-byte rows (256 contiguous bytes): no bank conflicts.
+  auto vnat_pos = [](int c) { return ((c % CH) / 4) * (KT * 4) + (c / CH) * 4 + c % 4; };
+  const int vn_lane = (4 * h32 + ((lane & 15) >> 2)) * 32 + ((lane >> 4) & 1) * 16 + (lane & 3) * 4;
+  auto vfrag = [&](const __bf16* tile, int p2, int dt) -> bf16x8 {
+    const PKV_LDS __bf16* q = (const PKV_LDS __bf16*)(tile + dt * (KT * 32) + 16 * p2 * 32 + vn_lane);
+    return cat8(lds_read_tr16(q), lds_read_tr16(q + 8 * 32));
+  };
   const __amdgpu_buffer_rsrc_t irs = __builtin_amdgcn_make_buffer_rsrc(
       (void*)(p.idx + (int64_t)g * p.idx_stride), 0, (uint32_t)(p.Nk * 4), 0x00020000);
   // own entries (OWN): rows past Ms and tiles past the last read as zeros
@@ -410,9 +443,10 @@ __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnP
         // chunk c of the tile: byte c * KCB past its first row, exponent byte c / 4
         kreg[set][i] = kload((uint32_t)kb0 * KRB + c * KCB, (uint32_t)kb0 * (DH / 32) + c / 4);
       }
-      // V^T tile kb0 / 32 (already gathered); tiles past the end read as 0
+      // V^T tile kb0 / 32 (already gathered), or (VNAT) V rows kb0 ..; tiles past the end
+      // read as 0
       vreg[set][i] = __builtin_amdgcn_raw_buffer_load_b128(
-          vrs, (uint32_t)(kb0 / 32) * (DH * 64) + c * 16, 0, 0);
+          vrs, VNAT ? (uint32_t)kb0 * (DH * 2) + c * 16 : (uint32_t)(kb0 / 32) * (DH * 64) + c * 16, 0, 0);
     }
   };
   auto store_tile_from = [&](int buf, int set) {
@@ -422,7 +456,8 @@ __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnP
       if (NCH % NT != 0 && c >= NCH) break;
       const int row = c / CH, col = c % CH;
       *(u32x4*)(&Ks[buf][row * KP + col * 8]) = kexpand(kreg[set][i]);
-      *(u32x4*)(&Vs[buf][(c / 4) * VTP + (c % 4) * 8]) = vreg[set][i];
+      if constexpr (VNAT) *(u32x4*)(&Vs[buf][vnat_pos(c) * 8]) = vreg[set][i];
+      else *(u32x4*)(&Vs[buf][(c / 4) * VTP + (c % 4) * 8]) = vreg[set][i];
     }
     if constexpr (BIAS) {
       if (tid < KT) Bs[buf][tid] = breg[set] * p.bias_mul;
@@ -584,7 +619,8 @@ __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnP
       for (int p2 = 0; p2 < 2; ++p2) {
 #pragma unroll
         for (int dt = 0; dt < ND; ++dt) {
-          const bf16x8 a = *(const bf16x8*)(vs + (dt * 32 + l32) * VTP + kt * 32 + 16 * p2 + 8 * h32);
+          const bf16x8 a = VNAT ? vfrag(vs, p2, dt)
+                                : *(const bf16x8*)(vs + (dt * 32 + l32) * VTP + kt * 32 + 16 * p2 + 8 * h32);
 #pragma unroll
           for (int qt = 0; qt < QT; ++qt) {
             o[qt][dt] = mfma32(a, pb[kt][qt][p2], o[qt][dt]);
@@ -628,6 +664,11 @@ __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnP
       koff[i] = (uint32_t)(krow * DH * 2 + kch * 16);
       const int vrow = c / 4, vch = (c % 4) ^ ((vrow / 4) % 4);
       voff[i] = (uint32_t)(vrow * 64 + vch * 16);
+      if constexpr (VNAT) {
+        // LDS chunk position c holds channels 8 (4 dt + cq) .. of key (c / 4) % KT
+        const int dt = c / (KT * 4), key = (c / 4) % KT, cq = c % 4;
+        voff[i] = (uint32_t)(key * (DH * 2) + (4 * dt + cq) * 16);
+      }
     }
     // the tile offset goes into the per-lane offset, so the buffer range check covers it
     // (OWN: the tiles after the cache range of the last key range are the chunk's own
@@ -650,7 +691,8 @@ __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnP
           // (block-scaled keys come through registers, kq_load / kq_store)
           if constexpr (KQ == 0)
             __builtin_amdgcn_raw_ptr_buffer_load_lds(krs, kd, 16, koff[i] + kb0 * (DH * 2), 0, 0, 0);
-          __builtin_amdgcn_raw_ptr_buffer_load_lds(vrs, vd, 16, voff[i] + (kb0 / 32) * (DH * 64), 0, 0, 0);
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(
+              vrs, vd, 16, voff[i] + (VNAT ? kb0 * (DH * 2) : (kb0 / 32) * (DH * 64)), 0, 0, 0);
         }
       }
     };
@@ -679,7 +721,8 @@ __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnP
 #pragma unroll
         for (int dt = 0; dt < ND; ++dt) {
           const bf16x8 a =
-              *(const bf16x8*)(&Vd[SL][(dt * 32 + l32) * 32 + (((2 * p2 + h32) ^ swv) * 8)]);
+              VNAT ? vfrag(&Vd[SL][0], p2, dt)
+                   : *(const bf16x8*)(&Vd[SL][(dt * 32 + l32) * 32 + (((2 * p2 + h32) ^ swv) * 8)]);
 #pragma unroll
           for (int qt = 0; qt < QT; ++qt) {
             o[qt][dt] = mfma32(a, pb[0][qt][p2], o[qt][dt]);
@@ -785,7 +828,7 @@ __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnP
     for (; t + NSL < t_full; t += NSL) steps(std::false_type{}, t);
     for (; t < ntiles; t += NSL) steps(std::true_type{}, t);
 #pragma unroll
-    for (int qt = 0; qt < QT; ++qt) over |= !(l_part[qt] <= kBigSum);
+    for (int qt = 0; qt < QT; ++qt) over |= untrusted_sum(l_part[qt]);
     if (__ballot(over) != 0) overflow = 1;
     // every load has landed before the slots are given up
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -852,9 +895,9 @@ __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnP
     int t = 0;
     for (; t + UNR < t_full; t += UNR) steps(std::false_type{}, t);
     for (; t < ntiles; t += UNR) steps(std::true_type{}, t);
-    // a lane's partial sum bounds every weight it added (NaN fails the test too)
+    // a lane's partial sum bounds every weight it added
 #pragma unroll
-    for (int qt = 0; qt < QT; ++qt) over |= !(l_part[qt] <= kBigSum);
+    for (int qt = 0; qt < QT; ++qt) over |= untrusted_sum(l_part[qt]);
     if (__ballot(over) != 0) overflow = 1;
     __syncthreads();
   } else {
@@ -1185,6 +1228,8 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restri
 // The V^T pre-pass (bf16), the kernels (fast path then fixup, or the f32 kernel) and,
 // with split key ranges, the merge. p is complete (plan fields, buffers, Vt / Vts
 // workspace pointers). KQ = 8 or 4 (bf16 only, no own entries): block-scaled K / V.
+// A contiguous bf16 cache without bias, own entries or per-head counts, whose every row
+// is an entry, needs no V^T tiles: its kernels read V as stored (VNAT).
 template <int DH, int KQ>
 hipError_t run_attention(const AttnShape& s, const AttnPlan& pl, AttnParams& p, bool gather,
                          bool psplit, hipStream_t st) {
@@ -1192,13 +1237,14 @@ hipError_t run_attention(const AttnShape& s, const AttnPlan& pl, AttnParams& p, 
   const bool part = pl.n_split > 1;
   const bool own = s.Ms > 0;
   const bool bias = p.bias != nullptr;
+  const bool vnat = KQ == 0 && s.bf16 && !gather && !own && !bias && !p.counts && p.src_rows == p.Nk;
   dim3 grid(pl.grid), block(256);
   if (s.bf16) {
     const dim3 vg((unsigned)p.vt_tiles, (unsigned)s.Hkv);
     if (gather)
       hipLaunchKernelGGL((vt_kernel<DH, true, KQ>), vg, block, 0, st, p.V, p.Ve, p.idx,
                          p.idx_stride, p.counts, p.src_rows, p.Nk, p.vt_tiles, (__bf16*)p.Vt);
-    else
+    else if (!vnat)
       hipLaunchKernelGGL((vt_kernel<DH, false, KQ>), vg, block, 0, st, p.V, p.Ve, p.idx,
                          p.idx_stride, p.counts, p.src_rows, p.Nk, p.vt_tiles, (__bf16*)p.Vt);
     if constexpr (KQ == 0) {
@@ -1212,10 +1258,15 @@ hipError_t run_attention(const AttnShape& s, const AttnPlan& pl, AttnParams& p, 
     if (e != hipSuccess) return e;
     const dim3 bblock(kThreadsBf16);
     // fast path, then the lazy-rescale fixup for any work item it handed back
-#define PKV_LB(G_, P_, S_, O_, B_)                                                                    \
-  do {                                                                                                \
-    hipLaunchKernelGGL((attn_bf16_kernel<DH, G_, P_, S_, false, O_, B_, KQ>), grid, bblock, 0, st, p); \
-    hipLaunchKernelGGL((attn_bf16_kernel<DH, G_, P_, S_, true, O_, B_, KQ>), grid, bblock, 0, st, p);  \
+#define PKV_LB(G_, P_, S_, O_, B_)                                                                           \
+  do {                                                                                                       \
+    hipLaunchKernelGGL((attn_bf16_kernel<DH, G_, P_, S_, false, O_, B_, KQ, false>), grid, bblock, 0, st, p); \
+    hipLaunchKernelGGL((attn_bf16_kernel<DH, G_, P_, S_, true, O_, B_, KQ, false>), grid, bblock, 0, st, p);  \
+  } while (0)
+#define PKV_LV(P_, S_)                                                                                        \
+  do {                                                                                                        \
+    hipLaunchKernelGGL((attn_bf16_kernel<DH, false, P_, S_, false, false, false, 0, true>), grid, bblock, 0, st, p); \
+    hipLaunchKernelGGL((attn_bf16_kernel<DH, false, P_, S_, true, false, false, 0, true>), grid, bblock, 0, st, p);  \
   } while (0)
 #define PKV_L(G_, P_, S_, O_)                      \
   do {                                             \
@@ -1224,7 +1275,11 @@ hipError_t run_attention(const AttnShape& s, const AttnPlan& pl, AttnParams& p, 
   } while (0)
     bool done = false;
     if constexpr (KQ == 0) {
-      if (own) {
+      if (vnat) {
+        done = true;
+        if (psplit) { if (part) PKV_LV(true, true); else PKV_LV(true, false); }
+        else { if (part) PKV_LV(false, true); else PKV_LV(false, false); }
+      } else if (own) {
         done = true;
         if (gather) {
           if (psplit) { if (part) PKV_L(true, true, true, true); else PKV_L(true, true, false, true); }
@@ -1244,6 +1299,7 @@ hipError_t run_attention(const AttnShape& s, const AttnPlan& pl, AttnParams& p, 
       else { if (part) PKV_L(false, false, true, false); else PKV_L(false, false, false, false); }
     }
 #undef PKV_L
+#undef PKV_LV
 #undef PKV_LB
   } else if constexpr (KQ == 0) {
     const dim3 fblock(kF32Waves * 64);

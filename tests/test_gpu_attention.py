@@ -117,6 +117,47 @@ def test_attention_deterministic():
     assert torch.equal(a, b)
 
 
+NAT_CASES = [
+    # M, N, Hq, Hkv, dh, p_terms, late-key excess (0: none)
+    (300, 2049, 32, 8, 128, 1, 0.0),    # ragged tail, several row tiles
+    (100, 1000, 28, 4, 128, 2, 0.0),    # GQA group of 7, two-term P
+    (33, 129, 4, 4, 64, 1, 0.0),        # head_dim 64
+    (16, 40000, 8, 8, 128, 1, 0.0),     # split key ranges + merge
+    (8, 20000, 8, 2, 64, 2, 0.0),       # split key ranges, head_dim 64, two-term P
+    (64, 2000, 8, 2, 128, 1, 10.0),     # scores outgrow the first tile: the fixup runs
+    (64, 2000, 8, 2, 128, 2, 10.0),
+]
+
+
+@pytest.mark.parametrize("case", NAT_CASES, ids=lambda c: "x".join(map(str, c)))
+def test_stored_v_tiles_equal_transposed_tiles(case):
+    """A contiguous bf16 cache is read with its V rows as stored (transposing LDS reads
+    of the P V operand); the same cache with per-head counts (every count = n) goes
+    through the V^T pre-pass instead. The MFMA operands and their order are the same,
+    so the outputs must be equal bit for bit, on the fast path, with split key ranges
+    and in the fixup."""
+    M, N, Hq, Hkv, dh, pt, a = case
+    print(f"stored vs transposed V tiles: {case}", flush=True)
+    rng = np.random.default_rng(M + N + dh)
+    Qf = (rng.standard_normal((M, Hq, dh)) * 0.5 + (1.0 if a else 0.0)).astype(np.float32)
+    Kf = rng.standard_normal((Hkv, N, dh)).astype(np.float32)
+    Vf = rng.standard_normal((Hkv, N, dh)).astype(np.float32)
+    if a:
+        Kf[:, N * 3 // 4, :] = a
+    q, k, v = (torch.from_numpy(x).bfloat16().to(DEV) for x in (Qf, Kf, Vf))
+    counts = torch.full((Hkv,), N, dtype=torch.int32, device=DEV)
+    i1 = torch.full((1,), -5, dtype=torch.int32, device=DEV)
+    i2 = torch.full((1,), -5, dtype=torch.int32, device=DEV)
+    o_nat = pkv.attend_cache(q, k, v, p_terms=pt, info=i1)
+    o_vt = pkv.attend_cache(q, k, v, counts=counts, p_terms=pt, info=i2)
+    torch.cuda.synchronize()
+    assert int(i1.item()) == 0 and int(i2.item()) == 0
+    assert torch.isfinite(o_nat).all()
+    assert torch.equal(o_nat, o_vt)
+    if pt == 1:
+        assert torch.equal(o_nat, pkv.attend_full(q, k, v))
+
+
 @pytest.mark.parametrize("a", [1.0, 3.0, 4.0, 5.0, 8.0, 10.0])
 def test_scores_outgrowing_the_first_tile(a):
     """One late key (position 1500 of 2000) scores about 16a - 4 log2 units above the
@@ -140,6 +181,16 @@ def test_scores_outgrowing_the_first_tile(a):
     Oc = host(pkv.attend_compressed(q, k, v, idx=idx_dev(idx), scale=scale))
     Kc, Vc = oracle.gather_cache(K, V, idx)
     e_c = rel(Oc, oracle.attention(Q, Kc, Vc, scale))
-    print(f"  O_f {e_f:.3e}  O_c {e_c:.3e}", flush=True)
-    assert np.isfinite(Of).all() and np.isfinite(Oc).all()
+    # two-term P over every key, contiguous and gathered (an overflowing weight makes
+    # the low piece NaN, which must send the work item to the fixup too)
+    ref = oracle.attention(Q, K, V, scale)
+    O2 = host(pkv.attend_cache(q, k, v, scale=scale, p_terms=2))
+    e_2 = rel(O2, ref)
+    all_idx = np.arange(N, dtype=np.int32)
+    Og = host(pkv.attend_compressed(q, k, v, idx=idx_dev(all_idx), scale=scale))
+    e_g = rel(Og, ref)
+    print(f"  O_f {e_f:.3e}  O_c {e_c:.3e}  two-term P: contiguous {e_2:.3e} gathered {e_g:.3e}",
+          flush=True)
+    assert all(np.isfinite(x).all() for x in (Of, Oc, O2, Og))
     assert e_f <= TOL_FULL["bf16"] and e_c <= TOL_COMP["bf16"]
+    assert e_2 <= TOL_COMP["bf16"] and e_g <= TOL_COMP["bf16"]
