@@ -14,10 +14,10 @@
 // one query and softmax statistics need only one cross-lane exchange (lane l with
 // l^32). P stays in registers and feeds O^T += V^T P^T directly. A contiguous cache's
 // V tiles go to LDS as stored, in 64-byte rows of 32 channels, and each V operand is
-// two transposing LDS reads (ds_read_b64_tr_b16) over four consecutive rows. Gathered,
-// block-scaled, biased and own-entry caches are first rewritten by vt_kernel into
-// 32-key tiles of V^T whose key order matches the P fragments' k-slots, so there the
-// V operand is one 16-byte LDS read. The online softmax runs in
+// two transposing LDS reads (ds_read_b64_tr_b16) over four consecutive rows (a chunk's
+// own entries likewise). Gathered, block-scaled and biased caches are first rewritten by
+// vt_kernel into 32-key tiles of V^T whose key order matches the P fragments' k-slots,
+// so there the V operand is one 16-byte LDS read. The online softmax runs in
 // fp32 in the exp2 domain with a fixed per-row offset (fast path) and falls back
 // to a lazily rescaled pass for work items whose scores outgrow it. On the main
 // path K and V (or V^T) tiles go from HBM straight into eight LDS slots (buffer_load ... lds, no
@@ -235,15 +235,15 @@ __global__ __launch_bounds__(256) void vt_kernel(const void* __restrict__ V,
 // KQ = 8 or 4: K holds block-scaled integers (exponents in p.Ke), loaded as such and
 // expanded to bf16 when the tile is stored to LDS (register-staged path); V was
 // expanded by vt_kernel into the V^T tiles.
-// VNAT (contiguous bf16 cache, every row of it used): no V^T tiles; V tiles arrive in
-// their stored [key][d] order and the P V product reads its V operand with transposing
-// LDS reads (see vfrag).
+// VNAT (contiguous bf16 cache, every row of it used; own entries, if any, as stored):
+// no V^T tiles; V tiles arrive in their stored [key][d] order and the P V product reads
+// its V operand with transposing LDS reads (see vfrag).
 template <int DH, bool GATHER, bool PSPLIT, bool PARTIAL, bool SAFE, bool OWN, bool BIAS, int KQ,
           bool VNAT>
 __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnParams p) {
   static_assert(!(OWN && BIAS), "own entries carry no bias");
   static_assert(KQ == 0 || KQ == 8 || KQ == 4, "bf16, int8 or int4 keys");
-  static_assert(!VNAT || (!GATHER && !OWN && !BIAS && KQ == 0), "V tiles of a contiguous bf16 cache");
+  static_assert(!VNAT || (!GATHER && !BIAS && KQ == 0), "V tiles of a contiguous bf16 cache");
   static_assert(!(OWN && KQ), "own entries are bf16");
   constexpr int KT = kKeyTile;
   constexpr int NKT = KT / 32;  // 32-key MFMA tiles per iteration
@@ -365,12 +365,15 @@ __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnP
   };
   const __amdgpu_buffer_rsrc_t irs = __builtin_amdgcn_make_buffer_rsrc(
       (void*)(p.idx + (int64_t)g * p.idx_stride), 0, (uint32_t)(p.Nk * 4), 0x00020000);
-  // own entries (OWN): rows past Ms and tiles past the last read as zeros
+  // own entries (OWN): rows past Ms and tiles past the last read as zeros; their V^T
+  // tiles, or (VNAT) their V rows as stored
   const __amdgpu_buffer_rsrc_t ksrs = __builtin_amdgcn_make_buffer_rsrc(
       (void*)((const __bf16*)p.Ks + (int64_t)g * p.Ms * DH), 0, (uint32_t)(p.Ms * DH * 2), 0x00020000);
-  const __amdgpu_buffer_rsrc_t vtsrs = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)(p.Vts + (int64_t)g * p.own_tiles * DH * 32), 0, (uint32_t)p.own_tiles * (DH * 64),
-      0x00020000);
+  const __amdgpu_buffer_rsrc_t vtsrs =
+      VNAT ? __builtin_amdgcn_make_buffer_rsrc((void*)((const __bf16*)p.Vs + (int64_t)g * p.Ms * DH), 0,
+                                               (uint32_t)(p.Ms * DH * 2), 0x00020000)
+           : __builtin_amdgcn_make_buffer_rsrc((void*)(p.Vts + (int64_t)g * p.own_tiles * DH * 32), 0,
+                                               (uint32_t)p.own_tiles * (DH * 64), 0x00020000);
   // logit bias of this KV head's entries (BIAS): entries past Nk read as 0
   const __amdgpu_buffer_rsrc_t brs = __builtin_amdgcn_make_buffer_rsrc(
       (void*)(p.bias + (int64_t)g * p.Nk), 0, (uint32_t)(p.Nk * 4), 0x00020000);
@@ -421,7 +424,8 @@ __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnP
           if (NCH % NT != 0 && c >= NCH) break;
           kreg[set][i] = __builtin_amdgcn_raw_buffer_load_b128(ksrs, (uint32_t)j0 * (DH * 2) + c * 16, 0, 0);
           vreg[set][i] = __builtin_amdgcn_raw_buffer_load_b128(
-              vtsrs, (uint32_t)(j0 / 32) * (DH * 64) + c * 16, 0, 0);
+              vtsrs, VNAT ? (uint32_t)j0 * (DH * 2) + c * 16 : (uint32_t)(j0 / 32) * (DH * 64) + c * 16,
+              0, 0);
         }
         return;
       }
@@ -685,7 +689,8 @@ __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnP
         if (OWN && own_range && tile >= ct) {
           const uint32_t j0 = (uint32_t)((tile - ct) * KT);
           __builtin_amdgcn_raw_ptr_buffer_load_lds(ksrs, kd, 16, koff[i] + j0 * (DH * 2), 0, 0, 0);
-          __builtin_amdgcn_raw_ptr_buffer_load_lds(vtsrs, vd, 16, voff[i] + (j0 / 32) * (DH * 64), 0, 0, 0);
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(
+              vtsrs, vd, 16, voff[i] + (VNAT ? j0 * (DH * 2) : (j0 / 32) * (DH * 64)), 0, 0, 0);
         } else {
           const uint32_t kb0 = (uint32_t)(k_begin + tile * KT);
           // (block-scaled keys come through registers, kq_load / kq_store)
@@ -1228,8 +1233,9 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restri
 // The V^T pre-pass (bf16), the kernels (fast path then fixup, or the f32 kernel) and,
 // with split key ranges, the merge. p is complete (plan fields, buffers, Vt / Vts
 // workspace pointers). KQ = 8 or 4 (bf16 only, no own entries): block-scaled K / V.
-// A contiguous bf16 cache without bias, own entries or per-head counts, whose every row
-// is an entry, needs no V^T tiles: its kernels read V as stored (VNAT).
+// A contiguous bf16 cache without bias or per-head counts, whose every row is an entry,
+// needs no V^T tiles (nor do a chunk's own entries beside it): its kernels read V as
+// stored (VNAT).
 template <int DH, int KQ>
 hipError_t run_attention(const AttnShape& s, const AttnPlan& pl, AttnParams& p, bool gather,
                          bool psplit, hipStream_t st) {
@@ -1237,7 +1243,7 @@ hipError_t run_attention(const AttnShape& s, const AttnPlan& pl, AttnParams& p, 
   const bool part = pl.n_split > 1;
   const bool own = s.Ms > 0;
   const bool bias = p.bias != nullptr;
-  const bool vnat = KQ == 0 && s.bf16 && !gather && !own && !bias && !p.counts && p.src_rows == p.Nk;
+  const bool vnat = KQ == 0 && s.bf16 && !gather && !bias && !p.counts && p.src_rows == p.Nk;
   dim3 grid(pl.grid), block(256);
   if (s.bf16) {
     const dim3 vg((unsigned)p.vt_tiles, (unsigned)s.Hkv);
@@ -1248,7 +1254,7 @@ hipError_t run_attention(const AttnShape& s, const AttnPlan& pl, AttnParams& p, 
       hipLaunchKernelGGL((vt_kernel<DH, false, KQ>), vg, block, 0, st, p.V, p.Ve, p.idx,
                          p.idx_stride, p.counts, p.src_rows, p.Nk, p.vt_tiles, (__bf16*)p.Vt);
     if constexpr (KQ == 0) {
-      if (own) {  // V^T tiles of the chunk's own entries
+      if (own && !vnat) {  // V^T tiles of the chunk's own entries
         const dim3 og((unsigned)p.own_tiles, (unsigned)s.Hkv);
         hipLaunchKernelGGL((vt_kernel<DH, false, 0>), og, block, 0, st, p.Vs, nullptr, nullptr, 0,
                            nullptr, (int64_t)p.Ms, p.Ms, p.own_tiles, (__bf16*)p.Vts);
@@ -1263,10 +1269,10 @@ hipError_t run_attention(const AttnShape& s, const AttnPlan& pl, AttnParams& p, 
     hipLaunchKernelGGL((attn_bf16_kernel<DH, G_, P_, S_, false, O_, B_, KQ, false>), grid, bblock, 0, st, p); \
     hipLaunchKernelGGL((attn_bf16_kernel<DH, G_, P_, S_, true, O_, B_, KQ, false>), grid, bblock, 0, st, p);  \
   } while (0)
-#define PKV_LV(P_, S_)                                                                                        \
-  do {                                                                                                        \
-    hipLaunchKernelGGL((attn_bf16_kernel<DH, false, P_, S_, false, false, false, 0, true>), grid, bblock, 0, st, p); \
-    hipLaunchKernelGGL((attn_bf16_kernel<DH, false, P_, S_, true, false, false, 0, true>), grid, bblock, 0, st, p);  \
+#define PKV_LV(P_, S_, O_)                                                                                 \
+  do {                                                                                                     \
+    hipLaunchKernelGGL((attn_bf16_kernel<DH, false, P_, S_, false, O_, false, 0, true>), grid, bblock, 0, st, p); \
+    hipLaunchKernelGGL((attn_bf16_kernel<DH, false, P_, S_, true, O_, false, 0, true>), grid, bblock, 0, st, p);  \
   } while (0)
 #define PKV_L(G_, P_, S_, O_)                      \
   do {                                             \
@@ -1277,8 +1283,13 @@ hipError_t run_attention(const AttnShape& s, const AttnPlan& pl, AttnParams& p, 
     if constexpr (KQ == 0) {
       if (vnat) {
         done = true;
-        if (psplit) { if (part) PKV_LV(true, true); else PKV_LV(true, false); }
-        else { if (part) PKV_LV(false, true); else PKV_LV(false, false); }
+        if (own) {
+          if (psplit) { if (part) PKV_LV(true, true, true); else PKV_LV(true, false, true); }
+          else { if (part) PKV_LV(false, true, true); else PKV_LV(false, false, true); }
+        } else {
+          if (psplit) { if (part) PKV_LV(true, true, false); else PKV_LV(true, false, false); }
+          else { if (part) PKV_LV(false, true, false); else PKV_LV(false, false, false); }
+        }
       } else if (own) {
         done = true;
         if (gather) {

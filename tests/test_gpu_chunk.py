@@ -57,6 +57,24 @@ def test_attend_chunk_full_and_evicted(shape):
         assert e_f <= TOL[(dt, pt)] and e_c <= TOL[(dt, pt)]
 
 
+@pytest.mark.parametrize("shape", [s for s in SHAPES if s[6] == "bf16"],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_chunk_stored_v_tiles_equal_transposed_tiles(shape):
+    """A contiguous cache and the chunk's own entries are read with their V rows as
+    stored; with per-head counts (every count = N) the same call goes through the V^T
+    pre-pass. Same operands in the same order: equal bit for bit."""
+    M, N, B, Hq, Hkv, dh, dt = shape
+    inp, ch = _chunk(M, N, B, Hq, Hkv, dh, dt)
+    q, k, v, ks, vs = (to_dev(a, dt) for a in (ch.Q, inp.K, inp.V, ch.Ks, ch.Vs))
+    counts = torch.full((Hkv,), N, dtype=torch.int32, device=DEV)
+    for pt in (1, 2):
+        o_nat = pkv.attend_chunk(q, k, v, ks, vs, p_terms=pt)
+        o_vt = pkv.attend_chunk(q, k, v, ks, vs, counts=counts, p_terms=pt)
+        torch.cuda.synchronize()
+        print(f"chunk stored vs transposed V tiles {shape} p_terms {pt}", flush=True)
+        assert torch.isfinite(o_nat).all() and torch.equal(o_nat, o_vt)
+
+
 @pytest.mark.parametrize("dt", ["bf16", "f32"])
 def test_attend_chunk_synthesized_and_prefix_of_rows(dt):
     """A synthesized compressed cache (contiguous K_c, V_c), and a cache given as the
