@@ -155,16 +155,26 @@ __global__ __launch_bounds__(256) void split_transpose_kernel(const SRC* __restr
 
 // Out[i][j] (+)= sum_t sum_k A_{a(t)}[i][k] B_{b(t)}[j][k] (+ rho (E1 - E2)[i][j]).
 // The operands are up to two bf16 planes per side (hi, lo), each [rows_p][Kp] with
-// the contraction index contiguous and zero padding (rows_p multiple of the tile,
-// Kp of 64), so the main loop has no bounds checks. Each K chunk loads every plane
-// once and applies all term products to it: term t multiplies plane a(t) = bit t of
-// TA with plane b(t) = bit t of TB. 256 x 256 tiles, 8 waves of 128 x 64, two LDS
-// stages, the next chunk loaded straight into LDS while the current one is multiplied.
-// The MFMA computes the
-// transposed tile (rows = output columns), so a lane owns 4 consecutive output
-// columns and the epilogue uses 16-byte accesses. SYM: only tiles with
-// tile_i <= tile_j; the diagonal tiles keep their i <= j half and every tile is
-// mirrored, so the result is exactly symmetric.
+// the contraction index contiguous and zero padding (rows_p a multiple of G_BM, Kp of
+// 64), so the main loop has no bounds checks. Each K chunk loads every plane once and
+// applies all term products to it: term t multiplies plane a(t) = bit t of TA with
+// plane b(t) = bit t of TB. The MFMA computes the transposed tile (rows = output
+// columns), so a lane owns 4 consecutive output columns and the epilogue uses 16-byte
+// accesses. SYM: only tiles with tile_i <= tile_j; the diagonal tiles keep their i <= j
+// half and every tile is mirrored, so the result is exactly symmetric.
+//
+// Two tile shapes (BgTile<T>):
+//   T = 256: 8 waves of 128 x 64, two LDS stages; one 256-tile per CU fills the chip
+//     for a 4096 x 4096 output (16 x 16 tiles).
+//   T = 192: 8 waves, two per 96 x 96 quadrant (nine accumulators each): wave w takes
+//     the first 16 k of every 32-k chunk, wave w + 4 (on the same SIMD) the second 16,
+//     and the two partial tiles are summed once at the end through LDS. Three LDS
+//     stages; waves 0-3 load the A planes, waves 4-7 the B planes. The symmetric
+//     products use it: a 4096-wide triangle is 253 tiles of 192 (one round on 256 CUs)
+//     against 136 of 256.
+// A tile's K chunk goes from HBM straight into LDS (buffer_load ... lds; no staging
+// registers) while earlier chunks are multiplied. Rows past a plane's end (the last
+// 192-tile reaches past a 256-padded plane) read as zeros through the buffer range.
 struct BGemm {
   const __bf16* A[2];  // planes of A [Ip][Kp]
   const __bf16* B[2];  // planes of B [Jp][Kp]
@@ -181,15 +191,40 @@ struct BGemm {
   int vec_out;
 };
 
-constexpr int BG_T = 256, BG_WM = 128, BG_WN = 64, BG_KC = 32;
-constexpr int BG_THREADS = (BG_T / BG_WM) * (BG_T / BG_WN) * 64;  // 512
+constexpr int BG_KC = 32;  // contraction chunk per LDS stage
+template <int T>
+struct BgTile;
+template <>
+struct BgTile<256> {
+  static constexpr int WM = 128, WN = 64, STAGES = 2, KSPLIT = 1;
+};
+template <>
+struct BgTile<192> {
+  static constexpr int WM = 96, WN = 96, STAGES = 3, KSPLIT = 2;
+};
+template <int T>
+constexpr int bg_threads() {
+  return (T / BgTile<T>::WM) * (T / BgTile<T>::WN) * BgTile<T>::KSPLIT * 64;
+}
 
-template <int NA, int NB, int NT, int TA, int TB, bool SYM>
-__global__ __launch_bounds__(BG_THREADS, 1) void bgemm_kernel(BGemm p) {
-  constexpr int ROWS = (NA + NB) * BG_T;            // stacked plane rows per stage
-  constexpr int LPT = ROWS * (BG_KC / 8) / BG_THREADS;  // 16-byte loads per thread
-  constexpr int MA = BG_WM / 32, MB = BG_WN / 32;
-  __shared__ __attribute__((aligned(16))) __bf16 lds[2][ROWS * BG_KC];
+template <int T, int NA, int NB, int NT, int TA, int TB, bool SYM>
+__global__ __launch_bounds__(bg_threads<T>(), 1) void bgemm_kernel(BGemm p) {
+  constexpr int WM = BgTile<T>::WM, WN = BgTile<T>::WN, S = BgTile<T>::STAGES;
+  constexpr int KSP = BgTile<T>::KSPLIT;
+  constexpr int NTH = bg_threads<T>();
+  constexpr int ROWS = (NA + NB) * T;              // stacked plane rows per stage
+  // KSP = 1: all threads load every plane; KSP = 2: threads [0, NTH/2) the A planes,
+  // [NTH/2, NTH) the B planes
+  constexpr int LTH = KSP == 1 ? NTH : NTH / 2;    // threads loading one plane
+  constexpr int RPU = LTH / 4;                     // rows per load round (4 chunks per row)
+  constexpr int PPR = T / RPU;                     // load rounds per plane
+  constexpr int LPT = ROWS * (BG_KC / 8) / NTH;    // 16-byte loads per thread per stage
+  constexpr int MA = WM / 32, MB = WN / 32;
+  static_assert(KSP == 1 || (KSP == 2 && NA == NB), "split loads: as many A as B planes");
+  static_assert(T % RPU == 0 && LPT == PPR * (KSP == 1 ? NA + NB : NA), "whole load rounds per plane");
+  static_assert(BG_KC == 32 && (KSP == 1 || KSP == 2), "one or two 16-k halves per chunk");
+  static_assert(WM % 16 == 0 && WN % 16 == 0 && T % 16 == 0, "fragment rows aligned to the swizzle");
+  __shared__ __attribute__((aligned(16))) __bf16 lds[S][ROWS * BG_KC];
   int ti, tj;
   {
     const int t = xcd_item((p.ntiles + kXcds - 1) / kXcds);
@@ -207,10 +242,12 @@ __global__ __launch_bounds__(BG_THREADS, 1) void bgemm_kernel(BGemm p) {
       tj = t % p.tiles_j;
     }
   }
-  const int i0 = ti * BG_T, j0 = tj * BG_T;
+  const int i0 = ti * T, j0 = tj * T;
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int h32 = lane >> 5, l32 = lane & 31;
-  const int wi = (wid / (BG_T / BG_WN)) * BG_WM, wj = (wid % (BG_T / BG_WN)) * BG_WN;
+  constexpr int NQW = (T / WM) * (T / WN);  // waves per k half
+  const int wq = wid % NQW, kh = wid / NQW;  // output block, k half (KSP = 2)
+  const int wi = (wq / (T / WN)) * WM, wj = (wq % (T / WN)) * WN;
   const int nq = p.Kp / BG_KC;
 
   f32x16 acc[MA][MB];
@@ -219,67 +256,95 @@ __global__ __launch_bounds__(BG_THREADS, 1) void bgemm_kernel(BGemm p) {
 #pragma unroll
     for (int b = 0; b < MB; ++b) acc[a][b] = f32x16{};
 
-  // The K chunks go from HBM straight into LDS (buffer_load ... lds; no staging
-  // registers), two stages of unpadded [stacked row][32 k] tiles. LDS position c of a
-  // stage (16 bytes) holds stacked row c / 4, k chunk (c % 4) ^ ((row / 4) % 4): the 16
-  // consecutive rows an MFMA fragment read takes at one k chunk land in 16 different
-  // bank groups. Thread tid fills positions u * 512 + tid, u < LPT: rows u * 128 + tid / 4,
-  // which lie in plane u / 2 (256 rows per plane).
-  // buffer descriptors of the planes' 256 rows of this tile (unused ones repeat plane 0;
-  // plain variables: the host pass drops the kernel if a descriptor is a temporary)
+  // Stages of unpadded [stacked row][32 k] tiles. LDS position c of a stage (16 bytes)
+  // holds stacked row c / 4, k chunk (c % 4) ^ ((row / 4) % 4): the 16 consecutive rows
+  // an MFMA fragment read takes at one k chunk land in 16 different bank groups. Load u
+  // (u < LPT) of thread tid fills row (u % PPR) * RPU + lt / 4 of plane u / PPR (KSP =
+  // 1; lt = tid) or of plane (tid < NTH/2 ? 0 : NA) + u / PPR (KSP = 2; lt = tid % (NTH/2)).
+  // buffer descriptors of the planes' rows of this tile (unused ones repeat plane 0;
+  // plain variables: the host pass drops the kernel if a descriptor is a temporary);
+  // the planes hold pad(I) and pad(J) rows, pad = G_BM
+  const int ip = (p.I + G_BM - 1) / G_BM * G_BM, jp = (p.J + G_BM - 1) / G_BM * G_BM;
   auto plane_base = [&](int pl) {
     return pl < NA ? p.A[pl] + (int64_t)i0 * p.ld : p.B[pl - NA] + (int64_t)j0 * p.ld;
   };
-  const uint32_t plane_bytes = (uint32_t)(BG_T * p.ld * 2);
+  auto plane_bytes = [&](int pl) {
+    return (uint32_t)(min(T, pl < NA ? ip - i0 : jp - j0) * p.ld * 2);
+  };
   const __amdgpu_buffer_rsrc_t rs0 =
-      __builtin_amdgcn_make_buffer_rsrc((void*)plane_base(0), 0, plane_bytes, 0x00020000);
+      __builtin_amdgcn_make_buffer_rsrc((void*)plane_base(0), 0, plane_bytes(0), 0x00020000);
   const __amdgpu_buffer_rsrc_t rs1 = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)plane_base(NA + NB > 1 ? 1 : 0), 0, plane_bytes, 0x00020000);
+      (void*)plane_base(NA + NB > 1 ? 1 : 0), 0, plane_bytes(NA + NB > 1 ? 1 : 0), 0x00020000);
   const __amdgpu_buffer_rsrc_t rs2 = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)plane_base(NA + NB > 2 ? 2 : 0), 0, plane_bytes, 0x00020000);
+      (void*)plane_base(NA + NB > 2 ? 2 : 0), 0, plane_bytes(NA + NB > 2 ? 2 : 0), 0x00020000);
   const __amdgpu_buffer_rsrc_t rs3 = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)plane_base(NA + NB > 3 ? 3 : 0), 0, plane_bytes, 0x00020000);
+      (void*)plane_base(NA + NB > 3 ? 3 : 0), 0, plane_bytes(NA + NB > 3 ? 3 : 0), 0x00020000);
   static_assert(NA + NB <= 4, "at most four planes");
-  static_assert(LPT == 2 * (NA + NB), "two 128-row pieces per plane");
-  const uint32_t voff0 = (uint32_t)(((tid / 4) * p.ld + (((tid % 4) ^ ((tid / 16) % 4)) * 8)) * 2);
-  const uint32_t voff1 = voff0 + (uint32_t)(128 * p.ld * 2);
+  const int lt = tid % LTH, lw = lt / 64;  // thread and wave within the loading group
+  const uint32_t voff0 = (uint32_t)(((lt / 4) * p.ld + (((lt % 4) ^ ((lt / 16) % 4)) * 8)) * 2);
   auto issue = [&](int q, int buf) {
     const uint32_t k0b = (uint32_t)(q * BG_KC * 2);
     static_for<LPT>([&](auto u_t) {
       constexpr int u = decltype(u_t)::value;
-      PKV_LDS void* dst = (PKV_LDS void*)&lds[buf][(u * BG_THREADS + wid * 64) * 8];
-      const uint32_t vo = (u & 1) ? voff1 : voff0;
-      if constexpr (u / 2 == 0) __builtin_amdgcn_raw_ptr_buffer_load_lds(rs0, dst, 16, vo, k0b, 0, 0);
-      else if constexpr (u / 2 == 1) __builtin_amdgcn_raw_ptr_buffer_load_lds(rs1, dst, 16, vo, k0b, 0, 0);
-      else if constexpr (u / 2 == 2) __builtin_amdgcn_raw_ptr_buffer_load_lds(rs2, dst, 16, vo, k0b, 0, 0);
-      else __builtin_amdgcn_raw_ptr_buffer_load_lds(rs3, dst, 16, vo, k0b, 0, 0);
+      const uint32_t vo = voff0 + (uint32_t)((u % PPR) * RPU * p.ld * 2);
+      if constexpr (KSP == 1) {
+        constexpr int pl = u / PPR;
+        PKV_LDS void* dst = (PKV_LDS void*)&lds[buf][(u * NTH + wid * 64) * 8];
+        if constexpr (pl == 0) __builtin_amdgcn_raw_ptr_buffer_load_lds(rs0, dst, 16, vo, k0b, 0, 0);
+        else if constexpr (pl == 1) __builtin_amdgcn_raw_ptr_buffer_load_lds(rs1, dst, 16, vo, k0b, 0, 0);
+        else if constexpr (pl == 2) __builtin_amdgcn_raw_ptr_buffer_load_lds(rs2, dst, 16, vo, k0b, 0, 0);
+        else __builtin_amdgcn_raw_ptr_buffer_load_lds(rs3, dst, 16, vo, k0b, 0, 0);
+      } else {
+        // a wave's 64 lanes fill 16 rows (1 KB) of one plane; which plane is wave-uniform
+        constexpr int pu = u / PPR;  // plane within the side (hi or lo)
+        const int row = (u % PPR) * RPU + lw * 16;
+        if (__builtin_amdgcn_readfirstlane(wid) < NTH / 128) {
+          PKV_LDS void* dst = (PKV_LDS void*)&lds[buf][(pu * T + row) * BG_KC];
+          if constexpr (pu == 0) __builtin_amdgcn_raw_ptr_buffer_load_lds(rs0, dst, 16, vo, k0b, 0, 0);
+          else __builtin_amdgcn_raw_ptr_buffer_load_lds(rs1, dst, 16, vo, k0b, 0, 0);
+        } else {
+          PKV_LDS void* dst = (PKV_LDS void*)&lds[buf][((NA + pu) * T + row) * BG_KC];
+          if constexpr (pu == 0) __builtin_amdgcn_raw_ptr_buffer_load_lds(rs2, dst, 16, vo, k0b, 0, 0);
+          else __builtin_amdgcn_raw_ptr_buffer_load_lds(rs3, dst, 16, vo, k0b, 0, 0);
+        }
+      }
     });
   };
-  // every load of this wave has landed, then a plain barrier (the workgroup fence of
-  // __syncthreads adds nothing here)
-  auto landed = [&]() { asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory"); };
+  // at most N of this wave's loads still in flight (the chunks issued after the one
+  // needed next), then a plain barrier (the workgroup fence of __syncthreads adds
+  // nothing here)
+  auto landed = [&](auto n_t) {
+    constexpr int N = decltype(n_t)::value;
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
+  };
   const int sw = (l32 / 4) % 4;
 
-  issue(0, 0);
-  landed();
+  // chunk q in stage q % S; S - 1 chunks in flight ahead of the one multiplied
+#pragma unroll
+  for (int q = 0; q < S - 1; ++q)
+    if (q < nq) issue(q, q);
+  if (S == 3 && nq > 1) landed(std::integral_constant<int, LPT>{});
+  else landed(std::integral_constant<int, 0>{});
   for (int q = 0; q < nq; ++q) {
-    const int buf = q & 1;
-    if (q + 1 < nq) issue(q + 1, buf ^ 1);
+    const int buf = q % S;
+    // the stage of chunk q + S - 1 was last read in step q - 1 (a barrier ago)
+    if (q + S - 1 < nq) issue(q + S - 1, (q + S - 1) % S);
     const __bf16* L0 = lds[buf];
 #pragma unroll
-    for (int ks = 0; ks < BG_KC; ks += 16) {
+    for (int kk = 0; kk < BG_KC / KSP; kk += 16) {
+      const int ks = KSP == 1 ? kk : 16 * kh;
       const int ch = ((2 * (ks / 16) + h32) ^ sw) * 8;  // k chunk of this lane, swizzled
       bf16x8 fa[NA][MA], fb[NB][MB];
 #pragma unroll
       for (int pa = 0; pa < NA; ++pa)
 #pragma unroll
         for (int a = 0; a < MA; ++a)
-          fa[pa][a] = *(const bf16x8*)(L0 + (pa * BG_T + wi + 32 * a + l32) * BG_KC + ch);
+          fa[pa][a] = *(const bf16x8*)(L0 + (pa * T + wi + 32 * a + l32) * BG_KC + ch);
 #pragma unroll
       for (int pb = 0; pb < NB; ++pb)
 #pragma unroll
         for (int b = 0; b < MB; ++b)
-          fb[pb][b] = *(const bf16x8*)(L0 + ((NA + pb) * BG_T + wj + 32 * b + l32) * BG_KC + ch);
+          fb[pb][b] = *(const bf16x8*)(L0 + ((NA + pb) * T + wj + 32 * b + l32) * BG_KC + ch);
 #pragma unroll
       for (int t = 0; t < NT; ++t)
 #pragma unroll
@@ -288,7 +353,27 @@ __global__ __launch_bounds__(BG_THREADS, 1) void bgemm_kernel(BGemm p) {
           for (int b = 0; b < MB; ++b)
             acc[a][b] = mfma32(fb[(TB >> t) & 1][b], fa[(TA >> t) & 1][a], acc[a][b]);
     }
-    landed();
+    // chunk q + 1 has landed (with three stages, chunk q + 2 may still be in flight)
+    if (S == 3 && q + 2 < nq) landed(std::integral_constant<int, LPT>{});
+    else landed(std::integral_constant<int, 0>{});
+  }
+  // KSP = 2: the second k half's partial tile goes through the (now idle) stages,
+  // lane-major per register (a wave's 64 lanes write and read 256 consecutive bytes),
+  // and is added in the epilogue, four values at a time
+  static_assert(KSP == 1 || NQW * MA * MB * 16 * 64 * 4 <= (int)sizeof(lds), "partial tiles fit the stages");
+  const float* part = (const float*)&lds[0][0] + wq * (MA * MB * 16 * 64);
+  if constexpr (KSP == 2) {
+    if (kh == 1) {
+      float* pw = (float*)&lds[0][0] + wq * (MA * MB * 16 * 64);
+#pragma unroll
+      for (int a = 0; a < MA; ++a)
+#pragma unroll
+        for (int b = 0; b < MB; ++b)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) pw[((a * MB + b) * 16 + e) * 64 + lane] = acc[a][b][e];
+    }
+    __syncthreads();
+    if (kh == 1) return;
   }
 
   // lane owns Out[i0+wi+32a+l32][j0+wj+32b+8g+4h32 .. +3]
@@ -303,6 +388,10 @@ __global__ __launch_bounds__(BG_THREADS, 1) void bgemm_kernel(BGemm p) {
         f32x4 v;
 #pragma unroll
         for (int e = 0; e < 4; ++e) v[e] = acc[a][b][4 * g + e];
+        if constexpr (KSP == 2) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] += part[((a * MB + b) * 16 + 4 * g + e) * 64 + lane];
+        }
         if (p.E1) {
 #pragma unroll
           for (int e = 0; e < 4; ++e)
@@ -333,13 +422,15 @@ __global__ __launch_bounds__(BG_THREADS, 1) void bgemm_kernel(BGemm p) {
       }
 }
 
+// symmetric products on 192-tiles, the others on 256-tiles
 template <int NA, int NB, int NT, int TA, int TB, bool SYM>
 hipError_t run_bgemm(BGemm p, hipStream_t st) {
-  p.tiles_j = (int)((p.J + BG_T - 1) / BG_T);
-  p.ntiles = SYM ? p.tiles_j * (p.tiles_j + 1) / 2 : (int)((p.I + BG_T - 1) / BG_T) * p.tiles_j;
+  constexpr int T = SYM ? 192 : 256;
+  p.tiles_j = (int)((p.J + T - 1) / T);
+  p.ntiles = SYM ? p.tiles_j * (p.tiles_j + 1) / 2 : (int)((p.I + T - 1) / T) * p.tiles_j;
   p.vec_out = (p.ldo & 3) == 0 && ((uintptr_t)p.Out & 15) == 0;
-  const dim3 grid((p.ntiles + kXcds - 1) / kXcds * kXcds), block(BG_THREADS);
-  hipLaunchKernelGGL((bgemm_kernel<NA, NB, NT, TA, TB, SYM>), grid, block, 0, st, p);
+  const dim3 grid((p.ntiles + kXcds - 1) / kXcds * kXcds), block(bg_threads<T>());
+  hipLaunchKernelGGL((bgemm_kernel<T, NA, NB, NT, TA, TB, SYM>), grid, block, 0, st, p);
   return hipGetLastError();
 }
 
