@@ -191,7 +191,8 @@ struct BGemm {
   int vec_out;
 };
 
-constexpr int BG_KC = 32;  // contraction chunk per LDS stage
+constexpr int BG_KC = 32;    // contraction chunk per LDS stage
+constexpr int BG_GROUP = 4;  // tile rows per group of the non-symmetric tile order
 template <int T>
 struct BgTile;
 template <>
@@ -238,8 +239,16 @@ __global__ __launch_bounds__(bg_threads<T>(), 1) void bgemm_kernel(BGemm p) {
       ti = r;
       tj = r + rem;
     } else {
-      ti = t / p.tiles_j;
-      tj = t % p.tiles_j;
+      // groups of BG_GROUP tile rows, column by column inside a group: the run of items
+      // one XCD takes covers few tile rows and few tile columns, so its L2 serves more
+      // of the operand re-reads
+      const int tiles_i = p.ntiles / p.tiles_j;
+      const int per_group = BG_GROUP * p.tiles_j;
+      const int first = (t / per_group) * BG_GROUP;
+      const int rows = min(BG_GROUP, tiles_i - first);
+      const int r = t % per_group;
+      ti = first + r % rows;
+      tj = r / rows;
     }
   }
   const int i0 = ti * T, j0 = tj * T;
