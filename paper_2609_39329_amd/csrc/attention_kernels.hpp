@@ -23,9 +23,9 @@
 // path K and V (or V^T) tiles go from HBM straight into eight LDS slots (buffer_load ... lds, no
 // register staging; issued by waves 0-3 only), six tiles ahead, with XOR-swizzled
 // 16-byte chunks in place of row padding and one barrier per two tiles (also with a
-// two-term P; block-scaled keys come through registers into the same slots, V^T by
-// DMA); the gathering and biased variants stage through registers into four padded
-// slots. The workgroup -> work-item
+// two-term P; block-scaled and gathered keys come through registers into the same
+// slots, V^T by DMA); the biased variants and the fixup stage through registers into
+// four padded slots. The workgroup -> work-item
 // map keeps all row tiles of one KV head (and key range) on one XCD so its L2
 // serves the K/V re-reads.
 //
@@ -233,8 +233,8 @@ __global__ __launch_bounds__(256) void vt_kernel(const void* __restrict__ V,
 // launched right after on the same stream): the lazy-rescale online softmax, run
 // only for marked work items, overwriting their outputs.
 // KQ = 8 or 4: K holds block-scaled integers (exponents in p.Ke), loaded as such and
-// expanded to bf16 when the tile is stored to LDS (register-staged path); V was
-// expanded by vt_kernel into the V^T tiles.
+// expanded to bf16 when the tile is stored to LDS (through registers on either
+// pipeline); V was expanded by vt_kernel into the V^T tiles.
 // VNAT (contiguous bf16 cache, every row of it used; own entries, if any, as stored):
 // no V^T tiles; V tiles arrive in their stored [key][d] order and the P V product reads
 // its V operand with transposing LDS reads (see vfrag).
@@ -260,7 +260,9 @@ __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnP
   // tiles straight into LDS (no register staging), through kDmaSlots unpadded slots
   // whose 16-byte chunks are XOR-swizzled so that the MFMA operand reads stay
   // conflict-free
-  constexpr bool DMA = kAttnDma && !SAFE && !GATHER && !BIAS;
+  constexpr bool DMA = kAttnDma && !SAFE && !BIAS;
+  // K through registers on the DMA pipeline: block-scaled values, or gathered rows
+  constexpr bool KREG = KQ != 0 || GATHER;
   // stored K rows: bf16, or int8 / packed int4 values (KRB bytes per row, KCB bytes per
   // 8-channel chunk) with DH / 32 exponent bytes
   constexpr int KCB = KQ ? KQ : 16;
@@ -653,10 +655,13 @@ __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnP
     constexpr int RPB = 16 / CH;  // K rows per 256 bytes of LDS
     constexpr int D = kDmaAhead;
     // the issuing waves' lanes each move LPD 16-byte chunks of the K tile and LPD of the
-    // V^T tile; chunk c = i * DT + tid of round i
-    constexpr int DT = kDmaWaves * kWave;
+    // V^T tile; chunk c = i * DT + tid of round i (with K through registers, all eight
+    // waves issuing a share of the V tile measured slower: 14.0 against 13.5 ms for a
+    // config-3-sized MXINT8 pass)
+    constexpr int DW = kDmaWaves;
+    constexpr int DT = DW * kWave;
     constexpr int LPD = NCH / DT;
-    static_assert(NCH % DT == 0 && LPD >= 1 && LPD <= kDmaLpdMax && kDmaWaves <= NT / kWave,
+    static_assert(NCH % DT == 0 && LPD >= 1 && LPD <= kDmaLpdMax && DW <= NT / kWave,
                   "whole DMA rounds of the issuing waves");
     // (sized by a namespace-scope constant: an array sized by the local constexpr and
     // captured by the lambdas below made the host pass drop these kernels' launch stubs)
@@ -680,7 +685,7 @@ __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnP
     auto issue = [&](int tile, auto slot_t) {
       constexpr int SL = decltype(slot_t)::value;
       // a scalar branch (wid is wave-uniform)
-      if (__builtin_amdgcn_readfirstlane(wid) >= kDmaWaves) return;
+      if (__builtin_amdgcn_readfirstlane(wid) >= DW) return;
 #pragma unroll
       for (int i = 0; i < LPD; ++i) {
         // a wave's DMA instruction writes its 64 lanes' chunks to 1 KB of consecutive LDS
@@ -688,13 +693,14 @@ __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnP
         PKV_LDS void* vd = (PKV_LDS void*)&Vd[SL][(i * DT + wid * 64) * 8];
         if (OWN && own_range && tile >= ct) {
           const uint32_t j0 = (uint32_t)((tile - ct) * KT);
-          __builtin_amdgcn_raw_ptr_buffer_load_lds(ksrs, kd, 16, koff[i] + j0 * (DH * 2), 0, 0, 0);
+          if constexpr (!KREG)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(ksrs, kd, 16, koff[i] + j0 * (DH * 2), 0, 0, 0);
           __builtin_amdgcn_raw_ptr_buffer_load_lds(
               vtsrs, vd, 16, voff[i] + (VNAT ? j0 * (DH * 2) : (j0 / 32) * (DH * 64)), 0, 0, 0);
         } else {
           const uint32_t kb0 = (uint32_t)(k_begin + tile * KT);
-          // (block-scaled keys come through registers, kq_load / kq_store)
-          if constexpr (KQ == 0)
+          // (block-scaled and gathered keys come through registers, kq_load / kq_store)
+          if constexpr (!KREG)
             __builtin_amdgcn_raw_ptr_buffer_load_lds(krs, kd, 16, koff[i] + kb0 * (DH * 2), 0, 0, 0);
           __builtin_amdgcn_raw_ptr_buffer_load_lds(
               vrs, vd, 16, voff[i] + (VNAT ? kb0 * (DH * 2) : (kb0 / 32) * (DH * 64)), 0, 0, 0);
@@ -736,55 +742,98 @@ __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnP
         }
     };
     static_assert(NKT == 1, "DMA path: one 32-key MFMA tile");
-    // Block-scaled keys (KQ): V^T tiles (expanded by vt_kernel) still arrive by DMA; the
-    // stored K bytes are loaded by every thread (chunk c = u * NT + tid) three steps before
-    // their LDS store, in four register sets, and expanded at the store into the slot's
-    // swizzled layout. Step t stores K tile t + 3 (read at step t + 2, after a barrier) and
-    // loads tile t + 6.
+    // Block-scaled keys (KQ) and gathered keys (GATHER): V^T tiles (expanded or gathered
+    // by vt_kernel) still arrive by DMA; the stored K chunks are loaded by every thread
+    // (chunk c = u * NT + tid) three steps before their LDS store, in four register sets,
+    // and expanded (KQ) at the store into the slot's swizzled layout. Step t stores K tile
+    // t + 3 (read at step t + 2, after a barrier) and loads tile t + 6. A gathered row's
+    // index is loaded three steps before its K chunk (step t loads the indices of tile
+    // t + 9) into a ring of four, so no load waits on another one issued in the same step.
     constexpr int LPK = (NCH + NT - 1) / NT;
     constexpr int KSETS = 4, KLEAD = 3;
-    static_assert(KQ == 0 || (NSL % KSETS == 0 && KLEAD + 3 <= D + 1), "K register sets");
-    u32x4 kq[KQ ? KSETS : 1][LPK];
+    static_assert(!KREG || (NSL % KSETS == 0 && KLEAD + 3 <= D + 1), "K register sets");
+    static_assert(!GATHER || LPK == 1, "one gathered K chunk per thread and tile");
+    u32x4 kq[KREG ? KSETS : 1][LPK];
+    uint32_t kidx[GATHER ? KSETS : 1];
+    bool kin[GATHER ? KSETS : 1];  // the gathered row is inside the cache
+    // the index of the row of this thread's chunk in tile `tile` (entries past the index
+    // array read as 0; own tiles load a placeholder, so every step issues the same loads)
+    auto kidx_load = [&](int tile, auto set_t) {
+      if constexpr (GATHER) {
+        constexpr int SET = decltype(set_t)::value;
+        kidx[SET] = __builtin_amdgcn_raw_buffer_load_b32(irs, (k_begin + tile * KT + tid / CH) * 4, 0, 0);
+      }
+    };
     auto kq_load = [&](int tile, auto set_t) {
-      if constexpr (KQ != 0) {
+      if constexpr (KREG) {
         constexpr int SET = decltype(set_t)::value;
         const int kb0 = k_begin + tile * KT;
 #pragma unroll
         for (int u = 0; u < LPK; ++u) {
           const int cc = u * NT + tid;
           if (NCH % NT != 0 && cc >= NCH) break;
-          kq[SET][u] = kload((uint32_t)kb0 * KRB + cc * KCB, (uint32_t)kb0 * (DH / 32) + cc / 4);
+          if constexpr (GATHER) {
+            if (OWN && own_range && tile >= ct) {
+              kq[SET][u] = __builtin_amdgcn_raw_buffer_load_b128(
+                  ksrs, (uint32_t)((tile - ct) * KT) * (DH * 2) + cc * 16, 0, 0);
+              kin[SET] = true;
+            } else {
+              // an entry outside the cache is checked before any offset is formed from it,
+              // and its row is stored as zeros (the select waits until the store, so the
+              // load need not have landed here)
+              const int src = (int)kidx[SET];
+              const bool in = (uint32_t)src < (uint32_t)p.src_rows;
+              const uint32_t row = in ? (uint32_t)src : 0u;
+              kq[SET][u] = kload(row * KRB + (cc % CH) * KCB, row * (DH / 32) + (cc % CH) / 4);
+              kin[SET] = in;
+            }
+          } else {
+            kq[SET][u] = kload((uint32_t)kb0 * KRB + cc * KCB, (uint32_t)kb0 * (DH / 32) + cc / 4);
+          }
         }
       }
     };
     auto kq_store = [&](auto set_t, auto slot_t) {
-      if constexpr (KQ != 0) {
+      if constexpr (KREG) {
         constexpr int SET = decltype(set_t)::value, SL = decltype(slot_t)::value;
 #pragma unroll
         for (int u = 0; u < LPK; ++u) {
           const int cc = u * NT + tid;
           if (NCH % NT != 0 && cc >= NCH) break;
           const int row = cc / CH, pos = row * CH + ((cc % CH) ^ ((row / RPB) % CH));
-          *(u32x4*)(&Kd[SL][pos * 8]) = kexpand(kq[SET][u]);
+          u32x4 v = kexpand(kq[SET][u]);
+          if constexpr (GATHER) v = kin[SET] ? v : u32x4{};
+          *(u32x4*)(&Kd[SL][pos * 8]) = v;
         }
       }
     };
     // loads a wave may leave in flight at a barrier (V^T tiles t + 4 .. t + 6 and, with
-    // block-scaled keys, the K loads issued after V^T tile t + 3)
-    constexpr int KLI = KQ ? 2 : 0;  // loads per kq_load (values, exponent)
-    constexpr int INFL = KQ ? KLI + 3 * (LPD + KLI) : 2 * LPD * (D - kDmaSteps - 1);
+    // K through registers, the K loads issued after V^T tile t + 3)
+    // loads per step besides the V^T tile's: values and exponent (KQ), or index and row
+    // (GATHER)
+    constexpr int KLI = KREG ? 2 : 0;
+    constexpr int INFL = KREG ? KLI + 3 * (LPD + KLI) : 2 * LPD * (D - kDmaSteps - 1);
     static_for<D>([&](auto j_t) { issue(decltype(j_t)::value, j_t); });
-    if constexpr (KQ != 0) {
+    if constexpr (KREG) {
       static_assert(D == 6 && kDmaSteps == 2, "the K schedule assumes six tiles ahead");
+      kidx_load(0, std::integral_constant<int, 0>{});
+      kidx_load(1, std::integral_constant<int, 1>{});
+      kidx_load(2, std::integral_constant<int, 2>{});
       kq_load(0, std::integral_constant<int, 0>{});
       kq_load(1, std::integral_constant<int, 1>{});
       kq_load(2, std::integral_constant<int, 2>{});
       kq_store(std::integral_constant<int, 0>{}, std::integral_constant<int, 0>{});
       kq_store(std::integral_constant<int, 1>{}, std::integral_constant<int, 1>{});
       kq_store(std::integral_constant<int, 2>{}, std::integral_constant<int, 2>{});
+      kidx_load(3, std::integral_constant<int, 3>{});
+      kidx_load(4, std::integral_constant<int, 0>{});
+      kidx_load(5, std::integral_constant<int, 1>{});
       kq_load(3, std::integral_constant<int, 3>{});
       kq_load(4, std::integral_constant<int, 0>{});
       kq_load(5, std::integral_constant<int, 1>{});
+      kidx_load(6, std::integral_constant<int, 2>{});
+      kidx_load(7, std::integral_constant<int, 3>{});
+      kidx_load(8, std::integral_constant<int, 0>{});
     }
     // tiles 0 .. kDmaSteps resident
     sync_slots(std::integral_constant<int, INFL>{});
@@ -806,6 +855,7 @@ __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnP
       issue(t + D, std::integral_constant<int, (I + D) % NSL>{});
       kq_store(std::integral_constant<int, (I + 3) % KSETS>{}, std::integral_constant<int, (I + 3) % NSL>{});
       kq_load(t + 3 + KLEAD, std::integral_constant<int, (I + 3 + KLEAD) % KSETS>{});
+      kidx_load(t + 6 + KLEAD, std::integral_constant<int, (I + 6 + KLEAD) % KSETS>{});
       scores_d(sn, std::integral_constant<int, (I + 1) % NSL>{});
       if constexpr (MASKED) mask(sn, t + 1);
       bf16x8 pb[NKT][QT][2];
