@@ -671,12 +671,13 @@ __global__ __launch_bounds__(kThreadsBf16, kWgPerCu) void attn_bf16_kernel(AttnP
       const int c = i * DT + tid % DT;
       const int krow = c / CH, kch = (c % CH) ^ ((krow / RPB) % CH);
       koff[i] = (uint32_t)(krow * DH * 2 + kch * 16);
-      const int vrow = c / 4, vch = (c % 4) ^ ((vrow / 4) % 4);
-      voff[i] = (uint32_t)(vrow * 64 + vch * 16);
       if constexpr (VNAT) {
         // LDS chunk position c holds channels 8 (4 dt + cq) .. of key (c / 4) % KT
         const int dt = c / (KT * 4), key = (c / 4) % KT, cq = c % 4;
         voff[i] = (uint32_t)(key * (DH * 2) + (4 * dt + cq) * 16);
+      } else {
+        const int vrow = c / 4, vch = (c % 4) ^ ((vrow / 4) % 4);
+        voff[i] = (uint32_t)(vrow * 64 + vch * 16);
       }
     }
     // the tile offset goes into the per-lane offset, so the buffer range check covers it
