@@ -83,6 +83,41 @@ def test_identity_gather_matches_full(dt):
     assert rel(Oc, Of) <= TOL_FULL[dt]
 
 
+GATHER_ID_CASES = [
+    # M, N, Hq, Hkv, dh, late-key excess (0: none)
+    (300, 2049, 32, 8, 128, 0.0),    # ragged tail, several row tiles
+    (16, 40000, 8, 8, 128, 0.0),     # split key ranges + merge
+    (33, 129, 4, 4, 64, 0.0),        # head_dim 64
+    (64, 2000, 8, 2, 128, 10.0),     # the fixup runs
+]
+
+
+@pytest.mark.parametrize("case", GATHER_ID_CASES, ids=lambda c: "x".join(map(str, c)))
+def test_identity_gather_equals_contiguous_bitwise(case):
+    """Gathered keys (loaded through registers by row index) and gathered V^T tiles give
+    the same MFMA operands in the same order as the contiguous cache read directly, so
+    an identity index set (shared, and per KV head) reproduces the contiguous result bit
+    for bit, with one- and two-term P."""
+    M, N, Hq, Hkv, dh, a = case
+    print(f"identity gather vs contiguous: {case}", flush=True)
+    rng = np.random.default_rng(N + dh)
+    Qf = (rng.standard_normal((M, Hq, dh)) * 0.5 + (1.0 if a else 0.0)).astype(np.float32)
+    Kf = rng.standard_normal((Hkv, N, dh)).astype(np.float32)
+    Vf = rng.standard_normal((Hkv, N, dh)).astype(np.float32)
+    if a:
+        Kf[:, N * 3 // 4, :] = a
+    q, k, v = (torch.from_numpy(x).bfloat16().to(DEV) for x in (Qf, Kf, Vf))
+    ident = torch.arange(N, dtype=torch.int32, device=DEV)
+    per_head = ident.repeat(Hkv, 1).contiguous()
+    for pt in (1, 2):
+        ref = pkv.attend_cache(q, k, v, p_terms=pt)
+        shared = pkv.attend_cache(q, k, v, idx=ident, p_terms=pt)
+        heads = pkv.attend_cache(q, k, v, idx=per_head, p_terms=pt)
+        torch.cuda.synchronize()
+        assert torch.isfinite(ref).all()
+        assert torch.equal(shared, ref) and torch.equal(heads, ref), pt
+
+
 def test_gather_permutation_and_duplicates():
     """A permuted index set gives the same output; a duplicated entry counts twice."""
     inp = make_custom_inputs(M=30, N=300, B=64, Hq=8, Hkv=4, dh=128, dtype="bf16", seed=4)
