@@ -78,7 +78,9 @@ def test_normal_equations_f32(rows, din, dout):
                                           ("f64", 600, 300)])
 def test_normal_equations_accumulate_chunks(acc, din, dout):
     """Eq. 9: running sums over reference chunks equal the one-shot statistics. With
-    d_in = 600 G spans 3x3 tiles, so the mirrored lower triangle is accumulated too."""
+    d_in = 600 G spans several tiles per side (4 x 4 of the symmetric product's 192-tiles,
+    the last one ragged), so the mirrored lower triangle is accumulated too; d_in = 192 is
+    exactly one tile."""
     code = pkv.F32 if acc == "f32" else pkv.F64
     rows = 700
     X, Y = randn((rows, din), 7, 0.5), randn((rows, dout), 8)
