@@ -260,21 +260,23 @@ def main() -> None:
         print(line)
 
     # the full-cache pass: the teacher's fast path and its fixup (one dispatch each per
-    # layer: no other call uses these instantiations), the V^T pre-pass over the whole
-    # cache where the call runs one (the largest dispatch of the non-gathering vt_kernel)
-    # and, with split key ranges, the merge (its largest dispatch)
+    # layer or reference chunk: no other call uses these instantiations; a chunk's pass
+    # carries its own entries; the teacher reads its contiguous cache's V as stored, so no
+    # V^T pre-pass belongs to it), with split key ranges the merge (its largest dispatch),
+    # and for fp32 inputs the fp32 kernel over the cache
     ps = "true" if a.teacher_psplit else "false"
-    pats = [r"vt_kernel<\d+, false, 0>", r"attn_combine_kernel<\d+, true>",
-            rf"attn_bf16_kernel<\d+, false, {ps}, (false|true), (false|true), false, false, 0, "
-            r"(false|true)>"]
+    pats = [r"attn_combine_kernel<\d+, (true|false)>",
+            rf"attn_bf16_kernel<\d+, false, {ps}, (false|true), (false|true), (false|true), false, 0, "
+            r"(false|true)>",
+            r"attn_f32_kernel<\d+, false, (false|true), false, false>"]
     def largest(k):
         f = max(fetch.get(k, [0.0])) * 1024.0 * sf
         w = max(write.get(k, [0.0])) * 1024.0 * sw
         return f + w
     full = [k for k in set(fetch) | set(write)
             if LIB_KERNEL.search(k) and any(re.fullmatch(pt, short(k)) for pt in pats)]
-    if len(full) >= 2:
-        print("\n## One full-cache attention launch (fast path, fixup and, where present, V^T pre-pass and merge)\n")
+    if full:
+        print("\n## One full-cache attention launch (fast path, fixup and, where present, the merge)\n")
         for k in sorted(full, key=short):
             print(f"- `{short(k)}`: {largest(k) / 1e6:,.1f} MB")
         print(f"\n    traffic_bytes_per_launch attend_full {sum(largest(k) for k in full):.0f}")
