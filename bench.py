@@ -355,10 +355,14 @@ def main():
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for s in range(args.steps):
+        t0 = time.perf_counter()
         step(True)
         torch.cuda.synchronize()
-        attn_ms += [a.elapsed_time(b) for pairs in ev for a, b in pairs]
-        log(f"[bench] step {s + 1}/{args.steps} done")
+        dt = time.perf_counter() - t0
+        this = [a.elapsed_time(b) for pairs in ev for a, b in pairs]
+        attn_ms += this
+        log(f"[bench] step {s + 1}/{args.steps} done: {dt * 1e3:.1f} ms, full-cache attention "
+            f"{np.mean(this):.3f} ms per call")
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
     bad = int((bufs.info != 0).sum().item())
